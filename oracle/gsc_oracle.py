@@ -1,0 +1,236 @@
+"""CPU oracle for the generalized sparse convolution.  TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this module.  The HIP library never calls it, and it imports nothing from the
+HIP path: the two share no code.  It is deliberately plain and slow: a Python
+dict maps coordinates to rows, the kernel map is built by one dict lookup per
+(output, offset), and the convolution is a loop over offsets of float64
+matmuls.  Every function below cites the passage of the paper it writes out.
+
+Conventions (readings of the paper, listed with the others in the design notes):
+  * a coordinate row is (b, x1..xD): batch index first (Sec. 3, Eq. 1 puts it
+    last; only the column order differs);
+  * ``W[k]`` is C_in x C_out, the transpose of the paper's W_i of Sec. 3.1, so a
+    row-major feature row f contributes ``f @ W[k]``;
+  * offsets are applied as in Eq. 3: output u reads input u + i (no flip);
+  * the batch component of a coordinate is never offset or strided.
+
+Parity status: every function is pinned by the CPU tests (brute-force maps,
+closed-form counts, dense-convolution special cases, adjoint identities, finite
+differences); the row order of ``output_coordinates`` is an implementation
+choice and is compared canonically, not pinned.
+"""
+from __future__ import annotations
+
+import itertools
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+Pairs = Tuple[np.ndarray, np.ndarray]     # (I_k, O_k) int64 arrays
+
+
+class DuplicateCoordinate(ValueError):
+    pass
+
+
+# --------------------------------------------------------------------------- #
+# Kernel regions  (Sec. 3.1: hypercube V^D(K) and arbitrary offset sets N^D;
+# Sec. 5.1 / Fig. 3: cross, hypercross, hybrid)
+# --------------------------------------------------------------------------- #
+def axis_offsets(K: int) -> List[int]:
+    """V^1(K): K consecutive integers around the origin.
+
+    Sec. 3.1 gives V^1(3) = {-1, 0, 1}.  For even K a centred set does not
+    exist; the reading used here is {-floor((K-1)/2), ..., ceil((K-1)/2)}, i.e.
+    {0, 1} for K = 2 (the kernel of a stride-2 down-sampling convolution)."""
+    lo = -((K - 1) // 2)
+    return list(range(lo, lo + K))
+
+
+def hypercube(K: int, D: int) -> np.ndarray:
+    """V^D(K) = (V^1(K))^D, in lexicographic order (last axis fastest)."""
+    return np.array(list(itertools.product(axis_offsets(K), repeat=D)), dtype=np.int64).reshape(-1, D)
+
+
+def hypercross(K: int, D: int) -> np.ndarray:
+    """The origin plus the offsets along each single axis within V^1(K)
+    (the "cross"/"hypercross" of Fig. 3), sorted lexicographically."""
+    pts = {tuple([0] * D)}
+    for d in range(D):
+        for j in axis_offsets(K):
+            o = [0] * D
+            o[d] = j
+            pts.add(tuple(o))
+    return np.array(sorted(pts), dtype=np.int64).reshape(-1, D)
+
+
+def hybrid(K: int, D: int) -> np.ndarray:
+    """Hybrid kernel of Sec. 5.1: a cube over the D-1 spatial axes at zero time
+    offset, plus a cross along the last (time) axis through the origin."""
+    pts = {tuple(o) + (0,) for o in itertools.product(axis_offsets(K), repeat=D - 1)}
+    for j in axis_offsets(K):
+        pts.add(tuple([0] * (D - 1)) + (j,))
+    return np.array(sorted(pts), dtype=np.int64).reshape(-1, D)
+
+
+def region(name: str, K: int, D: int) -> np.ndarray:
+    return {"cube": hypercube, "cross": hypercross, "hybrid": hybrid}[name](K, D)
+
+
+# --------------------------------------------------------------------------- #
+# Coordinate map (Sec. 3: COO coordinates with batch index; Sec. 2 / Sec. 4:
+# a hash table answers neighbour queries -- a Python dict here)
+# --------------------------------------------------------------------------- #
+def coordinate_map(coords: np.ndarray) -> Dict[tuple, int]:
+    """Map each coordinate row to its row index.  Coordinates of a sparse tensor
+    are unique; a repeated row is an error (it would make Eq. 3 ambiguous)."""
+    m: Dict[tuple, int] = {}
+    for r, row in enumerate(np.asarray(coords).tolist()):
+        key = tuple(row)
+        if key in m:
+            raise DuplicateCoordinate(f"row {r} repeats row {m[key]}: {key}")
+        m[key] = r
+    return m
+
+
+# --------------------------------------------------------------------------- #
+# Output coordinates (Sec. 4.2): from the convolution stride, the input
+# coordinates and the input tensor stride.
+# --------------------------------------------------------------------------- #
+def output_coordinates(coords: np.ndarray, stride: Sequence[int] | int) -> np.ndarray:
+    """C^out of a strided convolution: every spatial component c is replaced by
+    floor(c / s) * s (floor, so -1 -> -2 for s = 2), the batch index is kept, and
+    repeated rows are merged.  Stride 1 leaves C^in unchanged (the submanifold
+    case of Sec. 3.1, same rows, same order).  Otherwise rows are returned in
+    lexicographic order."""
+    coords = np.asarray(coords)
+    D = coords.shape[1] - 1
+    s = [stride] * D if np.isscalar(stride) else list(stride)
+    if all(v == 1 for v in s):
+        return coords.astype(np.int64).copy()
+    out = set()
+    for row in coords.tolist():
+        out.add((row[0],) + tuple((c // sd) * sd for c, sd in zip(row[1:], s)))
+    return np.array(sorted(out), dtype=np.int64).reshape(-1, D + 1)
+
+
+# --------------------------------------------------------------------------- #
+# Kernel map (Sec. 4.2): M = {(I_i, O_i)}_i, for every offset i the input rows
+# and output rows it connects; Eq. 3 defines which: u in C^out reads u + i
+# when u + i is in C^in.
+# --------------------------------------------------------------------------- #
+def kernel_map(in_coords: np.ndarray, out_coords: np.ndarray, offsets: np.ndarray,
+               tensor_stride: Sequence[int] | int = 1) -> List[Pairs]:
+    """For each offset o_k (row of ``offsets``) the pairs (row of u + ts*o_k in
+    C^in, row of u in C^out), listed in increasing output row."""
+    in_map = coordinate_map(in_coords)
+    out_rows = np.asarray(out_coords).tolist()
+    D = np.asarray(offsets).shape[1]
+    ts = [tensor_stride] * D if np.isscalar(tensor_stride) else list(tensor_stride)
+    maps = []
+    for o in np.asarray(offsets).tolist():
+        step = [t * v for t, v in zip(ts, o)]
+        I, O = [], []
+        for j, u in enumerate(out_rows):
+            q = (u[0],) + tuple(a + b for a, b in zip(u[1:], step))
+            r = in_map.get(q)
+            if r is not None:
+                I.append(r)
+                O.append(j)
+        maps.append((np.array(I, dtype=np.int64), np.array(O, dtype=np.int64)))
+    return maps
+
+
+def transposed_map(maps: List[Pairs]) -> List[Pairs]:
+    """Sec. 4.2, last sentence: the transposed convolution exchanges the roles
+    of input and output coordinates, so each (I_k, O_k) becomes (O_k, I_k);
+    pairs are re-listed in increasing (new) output row."""
+    out = []
+    for I, O in maps:
+        order = np.argsort(I, kind="stable")
+        out.append((O[order].copy(), I[order].copy()))
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# Convolution (Alg. 2 for the forward pass; backward by the chain rule of Eq. 3)
+# --------------------------------------------------------------------------- #
+def conv_forward(X: np.ndarray, W: np.ndarray, maps: List[Pairs], n_out: int) -> np.ndarray:
+    """Alg. 2: F^o <- 0, then for every offset k gather the input rows I_k,
+    multiply by the offset's weight and add the result into rows O_k."""
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    Y = np.zeros((n_out, W.shape[2]), dtype=np.float64)
+    for k, (I, O) in enumerate(maps):
+        if len(I) == 0:
+            continue
+        assert len(np.unique(O)) == len(O), "an offset maps two inputs to one output"
+        Y[O] += X[I] @ W[k]
+    return Y
+
+
+def conv_backward(X: np.ndarray, W: np.ndarray, dY: np.ndarray, maps: List[Pairs]):
+    """Gradients of Alg. 2.  Y[O_k] += X[I_k] W_k for every k, so
+    dX[I_k] += dY[O_k] W_k^T and dW_k = X[I_k]^T dY[O_k] (zero for an empty k)."""
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    dY = np.asarray(dY, dtype=np.float64)
+    dX = np.zeros_like(X)
+    dW = np.zeros_like(W)
+    for k, (I, O) in enumerate(maps):
+        if len(I) == 0:
+            continue
+        assert len(np.unique(I)) == len(I), "an offset maps one input to two outputs"
+        dX[I] += dY[O] @ W[k].T
+        dW[k] = X[I].T @ dY[O]
+    return dX, dW
+
+
+# --------------------------------------------------------------------------- #
+# Eq. 3 evaluated one output (or one input) row at a time, for sampled checks
+# at sizes where the full map is too slow in Python.
+# --------------------------------------------------------------------------- #
+def conv_forward_rows(X: np.ndarray, W: np.ndarray, in_map: Dict[tuple, int], out_coords: np.ndarray,
+                      rows: Sequence[int], offsets: np.ndarray,
+                      tensor_stride: Sequence[int] | int = 1) -> np.ndarray:
+    """Eq. 3 for the listed outputs u: sum over offsets i with u + i in C^in of
+    x^in_{u+i} W_i."""
+    W = np.asarray(W, dtype=np.float64)
+    offs = np.asarray(offsets).tolist()
+    D = len(offs[0])
+    ts = [tensor_stride] * D if np.isscalar(tensor_stride) else list(tensor_stride)
+    Y = np.zeros((len(rows), W.shape[2]))
+    for n, j in enumerate(rows):
+        u = [int(v) for v in out_coords[j]]
+        for k, o in enumerate(offs):
+            q = (u[0],) + tuple(a + t * b for a, t, b in zip(u[1:], ts, o))
+            r = in_map.get(q)
+            if r is not None:
+                Y[n] += np.asarray(X[r], dtype=np.float64) @ W[k]
+    return Y
+
+
+def conv_dx_rows(dY: np.ndarray, W: np.ndarray, out_map: Dict[tuple, int], in_coords: np.ndarray,
+                 rows: Sequence[int], offsets: np.ndarray,
+                 tensor_stride: Sequence[int] | int = 1) -> np.ndarray:
+    """dX for the listed input rows r: input c_r feeds output u = c_r - i
+    through offset i whenever that u is in C^out, so
+    dX[r] = sum_i dY[u] W_i^T over those i."""
+    W = np.asarray(W, dtype=np.float64)
+    offs = np.asarray(offsets).tolist()
+    D = len(offs[0])
+    ts = [tensor_stride] * D if np.isscalar(tensor_stride) else list(tensor_stride)
+    dX = np.zeros((len(rows), W.shape[1]))
+    for n, r in enumerate(rows):
+        c = [int(v) for v in in_coords[r]]
+        for k, o in enumerate(offs):
+            q = (c[0],) + tuple(a - t * b for a, t, b in zip(c[1:], ts, o))
+            j = out_map.get(q)
+            if j is not None:
+                dX[n] += np.asarray(dY[j], dtype=np.float64) @ W[k].T
+    return dX
+
+
+def map_pair_count(maps: List[Pairs]) -> int:
+    return int(sum(len(I) for I, _ in maps))

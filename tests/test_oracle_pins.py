@@ -1,0 +1,468 @@
+"""Pins for the CPU oracle: results fixed by the paper and by mathematics,
+computed by means that share nothing with the oracle's own code.
+
+* kernel maps: brute force over all (input, output) coordinate pairs with
+  numpy broadcasting; closed-form counts on fully occupied boxes; the
+  symmetry and centre-offset invariants of submanifold maps; the partition
+  property of the stride-2, size-2 kernel;
+* output coordinates: floor semantics written out by hand (golden file);
+* forward: the dense special case of Eq. 3 (Sec. 3.1) through torch's
+  conv3d / conv_transpose3d in float64, and a dense 4D sum of shifted slices
+  for the hybrid kernel; the centre-only identity kernel;
+* backward: torch autograd of the dense convolution, adjoint identities and
+  central finite differences.
+
+The planted-mistake tests at the end check that each pin fails for a
+plausible error in the oracle (sign of the offset, a transposed weight, a
+dropped term, truncation instead of floor).
+"""
+import itertools
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle.gsc_oracle as O
+from paper_1904_08755_amd import workloads as WL
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# --------------------------------------------------------------------------- #
+# independent reference computations
+# --------------------------------------------------------------------------- #
+def brute_force_map(in_coords, out_coords, offsets, ts=1):
+    """All pairs (r, j) with c_r - u_j == ts * o_k, batch equal; by broadcasting."""
+    a = np.asarray(in_coords, np.int64)
+    b = np.asarray(out_coords, np.int64)
+    diff = a[None, :, :] - b[:, None, :]          # out x in x (1+D)
+    same_b = diff[:, :, 0] == 0
+    res = []
+    for o in np.asarray(offsets, np.int64):
+        hit = same_b & np.all(diff[:, :, 1:] == ts * o[None, None, :], axis=2)
+        j, r = np.nonzero(hit)                    # nonzero is row-major: sorted by j
+        res.append((r.astype(np.int64), j.astype(np.int64)))
+    return res
+
+
+def maps_equal(m1, m2):
+    if len(m1) != len(m2):
+        return False
+    for (I1, O1), (I2, O2) in zip(m1, m2):
+        if not (np.array_equal(I1, I2) and np.array_equal(O1, O2)):
+            return False
+    return True
+
+
+def dense_volume(coords, X, lo, shape):
+    """Scatter sparse rows into a zero (B, C, *shape) float64 tensor."""
+    B = int(coords[:, 0].max()) + 1
+    vol = torch.zeros((B, X.shape[1]) + tuple(shape), dtype=torch.float64)
+    idx = [torch.from_numpy(coords[:, 0].astype(np.int64))]
+    idx.append(slice(None))
+    c = coords[:, 1:].astype(np.int64) - np.asarray(lo)[None, :]
+    vol_perm = vol.permute(0, *range(2, 2 + len(shape)), 1)      # B, *shape, C
+    vol_perm[(idx[0],) + tuple(torch.from_numpy(c[:, d]) for d in range(len(shape)))] = \
+        torch.from_numpy(np.asarray(X, np.float64))
+    return vol
+
+
+def read_sites(vol, coords, lo):
+    c = coords[:, 1:].astype(np.int64) - np.asarray(lo)[None, :]
+    vp = vol.permute(0, *range(2, vol.dim()), 1)
+    return vp[(torch.from_numpy(coords[:, 0].astype(np.int64)),) +
+              tuple(torch.from_numpy(c[:, d]) for d in range(c.shape[1]))].numpy()
+
+
+def cube3_weight(W, offsets):
+    """conv3d weight (C_out, C_in, 3, 3, 3): cross-correlation tap at offset o
+    sits at index o + 1 and multiplies input u + o, as in Eq. 3."""
+    K, ci, co = W.shape
+    w = torch.zeros((co, ci, 3, 3, 3), dtype=torch.float64)
+    for k, o in enumerate(offsets):
+        w[:, :, o[0] + 1, o[1] + 1, o[2] + 1] = torch.from_numpy(np.asarray(W[k], np.float64).T)
+    return w
+
+
+def dense_subm_conv3d(coords, X, W, offsets):
+    lo = coords[:, 1:].min(0) - 1
+    shape = coords[:, 1:].max(0) - lo + 2
+    vol = dense_volume(coords, X, lo, shape)
+    out = F.conv3d(vol, cube3_weight(W, offsets), padding=1)
+    return read_sites(out, coords, lo)
+
+
+def rel_err(got, ref):
+    ref = np.asarray(ref, np.float64)
+    den = np.abs(ref).max()
+    return np.abs(np.asarray(got, np.float64) - ref).max() / (den if den > 0 else 1.0)
+
+
+def small_scene(cid=1, scale=0.12):
+    return WL.make_workload(cid, scale=scale)
+
+
+# --------------------------------------------------------------------------- #
+# regions
+# --------------------------------------------------------------------------- #
+def test_region_counts_golden():
+    for line in open(os.path.join(GOLDEN, "region_counts.txt")):
+        line = line.split("#")[0].split()
+        if not line:
+            continue
+        if line[0] == "axis":
+            assert O.axis_offsets(int(line[1])) == [int(v) for v in line[2:]]
+        else:
+            reg, K, D, cnt = line[0], int(line[1]), int(line[2]), int(line[3])
+            offs = O.region(reg, K, D)
+            assert offs.shape == (cnt, D)
+            assert len({tuple(o) for o in offs.tolist()}) == cnt
+
+
+def test_regions_structure():
+    cube = O.hypercube(3, 3)
+    assert cube.tolist() == sorted(cube.tolist())
+    assert {tuple(o) for o in cube.tolist()} == set(itertools.product((-1, 0, 1), repeat=3))
+    cross = O.hypercross(5, 3)
+    assert len(cross) == 2 * 3 * 2 + 1
+    assert all((np.count_nonzero(o) <= 1) for o in cross)
+    hyb = O.hybrid(3, 4)
+    assert sum(1 for o in hyb if o[3] != 0) == 2
+    assert all(o[:3].tolist() == [0, 0, 0] for o in hyb if o[3] != 0)
+    assert O.axis_offsets(2) == [0, 1]
+
+
+# --------------------------------------------------------------------------- #
+# output coordinates
+# --------------------------------------------------------------------------- #
+def test_stride_floor_golden():
+    rows_in, rows_out = [], set()
+    for line in open(os.path.join(GOLDEN, "stride_floor.txt")):
+        line = line.split("#")[0].strip()
+        if not line:
+            continue
+        a, b = line.split("->")
+        rows_in.append([int(v) for v in a.split()])
+        rows_out.add(tuple(int(v) for v in b.split()))
+    got = O.output_coordinates(np.array(rows_in), 2)
+    assert {tuple(r) for r in got.tolist()} == rows_out
+    assert len(got) == len(rows_out)
+
+
+def test_stride_full_box_closed_form():
+    n, D = 6, 3
+    box = np.array([(0,) + c for c in itertools.product(range(-4, -4 + n), repeat=D)])  # even-aligned
+    out = O.output_coordinates(box, 2)
+    assert len(out) == (n // 2) ** D
+    assert np.all(out[:, 1:] % 2 == 0)
+
+
+def test_stride_one_is_identity():
+    c = WL.random_coords(1, 200, 3, -5, 5, batch=2)
+    assert np.array_equal(O.output_coordinates(c, 1), c)
+
+
+# --------------------------------------------------------------------------- #
+# kernel maps
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("seed,D,reg,K", [(1, 3, "cube", 3), (2, 3, "cross", 5), (3, 4, "hybrid", 3),
+                                          (4, 2, "cube", 5), (5, 3, "cube", 2)])
+def test_map_vs_brute_force_submanifold(seed, D, reg, K):
+    c = WL.random_coords(seed, 300, D, -4, 5, batch=2)
+    offs = O.region(reg, K, D)
+    assert maps_equal(O.kernel_map(c, c, offs), brute_force_map(c, c, offs))
+
+
+def test_map_vs_brute_force_strided_and_tensor_stride():
+    c = WL.random_coords(7, 400, 3, -7, 7, batch=3)
+    out = O.output_coordinates(c, 2)
+    offs = O.hypercube(2, 3)
+    assert maps_equal(O.kernel_map(c, out, offs), brute_force_map(c, out, offs))
+    # second level: input with tensor stride 2, stride-2 output again, offsets scaled by 2
+    c2 = out
+    out2 = O.output_coordinates(c2, 4)
+    assert maps_equal(O.kernel_map(c2, out2, offs, 2), brute_force_map(c2, out2, offs, 2))
+    offs3 = O.hypercube(3, 3)
+    assert maps_equal(O.kernel_map(c2, c2, offs3, 2), brute_force_map(c2, c2, offs3, 2))
+
+
+def test_map_full_box_closed_form():
+    n, D = 5, 3
+    box = np.array([(0,) + c for c in itertools.product(range(n), repeat=D)])
+    offs = O.hypercube(3, D)
+    m = O.kernel_map(box, box, offs)
+    for o, (I, _) in zip(offs, m):
+        assert len(I) == np.prod([n - abs(v) for v in o])
+    # stride 2, size-2 kernel on an even box: (n/2)^D outputs, (n/2)^D pairs per offset
+    n = 6
+    box = np.array([(1,) + c for c in itertools.product(range(-2, -2 + n), repeat=D)])
+    out = O.output_coordinates(box, 2)
+    m = O.kernel_map(box, out, O.hypercube(2, D))
+    assert len(out) == (n // 2) ** D
+    assert all(len(I) == (n // 2) ** D for I, _ in m)
+
+
+def test_map_symmetry_and_centre():
+    c = small_scene().coords
+    offs = O.hypercube(3, 3)
+    m = O.kernel_map(c, c, offs)
+    index = {tuple(o): k for k, o in enumerate(offs.tolist())}
+    for k, o in enumerate(offs.tolist()):
+        I, Oo = m[k]
+        I2, O2 = m[index[tuple(-v for v in o)]]
+        assert set(zip(I.tolist(), Oo.tolist())) == set(zip(O2.tolist(), I2.tolist()))
+    centre = index[(0, 0, 0)]
+    assert np.array_equal(m[centre][0], np.arange(len(c)))
+    assert np.array_equal(m[centre][1], np.arange(len(c)))
+
+
+def test_map_stride2_partition_and_batches():
+    w = small_scene(2)
+    c = w.coords
+    out = O.output_coordinates(c, 2)
+    m = O.kernel_map(c, out, O.hypercube(2, 3))
+    allI = np.concatenate([I for I, _ in m])
+    assert np.array_equal(np.sort(allI), np.arange(len(c)))
+    for I, Oo in m:
+        assert np.array_equal(c[I, 0], out[Oo, 0])
+
+
+# --------------------------------------------------------------------------- #
+# forward
+# --------------------------------------------------------------------------- #
+def test_forward_dense_conv3d_random():
+    c = WL.random_coords(11, 700, 3, -6, 6, batch=2)
+    X, _ = WL.random_features(11, len(c), 5)
+    offs = O.hypercube(3, 3)
+    W, _ = WL.random_weights(11, 27, 5, 7)
+    Y = O.conv_forward(X, W, O.kernel_map(c, c, offs), len(c))
+    assert rel_err(Y, dense_subm_conv3d(c, X, W, offs)) < 1e-12
+
+
+def test_forward_dense_conv3d_scene_and_c1():
+    for w in (WL.make_workload(0), small_scene()):
+        offs = O.hypercube(3, 3)
+        L = w.layers[0]
+        Wt = L.W[:, :4, :5] if L.c_in > 4 else L.W
+        Xs = w.X[:, :Wt.shape[1]]
+        Y = O.conv_forward(Xs, Wt, O.kernel_map(w.coords, w.coords, offs), w.n)
+        assert rel_err(Y, dense_subm_conv3d(w.coords, Xs, Wt, offs)) < 1e-12
+
+
+def _down_up_dense(c, X, W1, W2):
+    """conv3d(kernel 2, stride 2) then conv_transpose3d(kernel 2, stride 2)
+    on a volume whose origin is even, read at the coarse / fine sites."""
+    lo = (c[:, 1:].min(0) // 2) * 2
+    shape = c[:, 1:].max(0) - lo + 1
+    shape = shape + (shape % 2)
+    vol = dense_volume(c, X, lo, shape)
+    offs = O.hypercube(2, 3)
+    w1 = torch.zeros((W1.shape[2], W1.shape[1], 2, 2, 2), dtype=torch.float64)
+    w2 = torch.zeros((W2.shape[1], W2.shape[2], 2, 2, 2), dtype=torch.float64)  # (C_in, C_out, k...)
+    for k, o in enumerate(offs.tolist()):
+        w1[:, :, o[0], o[1], o[2]] = torch.from_numpy(W1[k].astype(np.float64).T)
+        w2[:, :, o[0], o[1], o[2]] = torch.from_numpy(W2[k].astype(np.float64))
+    y1 = F.conv3d(vol, w1, stride=2)
+    out = O.output_coordinates(c, 2)
+    Y1 = read_sites(y1, np.concatenate([out[:, :1], (out[:, 1:] - lo) // 2], 1), np.zeros(3, np.int64))
+    # the transposed conv consumes the sparse Y1 (zero away from the coarse sites)
+    y1_sparse = dense_volume(np.concatenate([out[:, :1], (out[:, 1:] - lo) // 2], 1), Y1,
+                             np.zeros(3, np.int64), y1.shape[2:])
+    if y1_sparse.shape[0] < y1.shape[0]:
+        pad = torch.zeros((y1.shape[0] - y1_sparse.shape[0],) + tuple(y1_sparse.shape[1:]), dtype=torch.float64)
+        y1_sparse = torch.cat([y1_sparse, pad])
+    y2 = F.conv_transpose3d(y1_sparse, w2, stride=2)
+    Y2 = read_sites(y2, c, lo)
+    return out, Y1, Y2
+
+
+def test_forward_strided_and_transposed_dense():
+    c = WL.random_coords(13, 500, 3, -7, 6, batch=2)
+    X, _ = WL.random_features(13, len(c), 4)
+    W1, _ = WL.random_weights(131, 8, 4, 6)
+    W2, _ = WL.random_weights(132, 8, 6, 3)
+    out, Y1_ref, Y2_ref = _down_up_dense(c, X, W1, W2)
+    offs = O.hypercube(2, 3)
+    assert np.array_equal(O.output_coordinates(c, 2), out)
+    m = O.kernel_map(c, out, offs)
+    Y1 = O.conv_forward(X, W1, m, len(out))
+    assert rel_err(Y1, Y1_ref) < 1e-12
+    Y2 = O.conv_forward(Y1, W2, O.transposed_map(m), len(c))
+    assert rel_err(Y2, Y2_ref) < 1e-12
+
+
+def dense_hybrid4d(c, X, W, offs):
+    """Dense 4D sum over offsets of shifted slices of a padded volume."""
+    lo = c[:, 1:].min(0) - 1
+    shape = c[:, 1:].max(0) - lo + 2
+    B = int(c[:, 0].max()) + 1
+    vol = np.zeros((B,) + tuple(shape) + (X.shape[1],))
+    p = c[:, 1:] - lo
+    vol[(c[:, 0],) + tuple(p[:, d] for d in range(4))] = X
+    out = np.zeros(vol.shape[:-1] + (W.shape[2],))
+    inner = tuple(slice(1, s - 1) for s in shape)
+    for k, o in enumerate(offs.tolist()):
+        src = tuple(slice(1 + v, s - 1 + v) for v, s in zip(o, shape))
+        out[(slice(None),) + inner] += vol[(slice(None),) + src] @ W[k]
+    return out[(c[:, 0],) + tuple(p[:, d] for d in range(4))]
+
+
+def test_forward_hybrid4d_dense():
+    w = WL.make_workload(3, scale=0.12)
+    offs = O.hybrid(3, 4)
+    Xs, Ws = w.X[:, :6], w.layers[0].W[:, :6, :5]
+    Y = O.conv_forward(Xs, Ws, O.kernel_map(w.coords, w.coords, offs), w.n)
+    assert rel_err(Y, dense_hybrid4d(w.coords, Xs, Ws, offs)) < 1e-12
+
+
+def test_centre_identity_exact():
+    w = small_scene()
+    offs = np.zeros((1, 3), np.int64)
+    C = w.X.shape[1]
+    Y = O.conv_forward(w.X, np.eye(C)[None], O.kernel_map(w.coords, w.coords, offs), w.n)
+    assert np.array_equal(Y, w.X.astype(np.float64))
+    W0 = WL.random_weights(5, 1, C, 3)[0]
+    Y = O.conv_forward(w.X, W0, O.kernel_map(w.coords, w.coords, offs), w.n)
+    assert rel_err(Y, w.X.astype(np.float64) @ W0[0].astype(np.float64)) < 1e-14
+
+
+def test_forward_rows_match_eq3():
+    c = WL.random_coords(17, 400, 3, -5, 5, batch=2)
+    X, _ = WL.random_features(17, len(c), 4)
+    W, _ = WL.random_weights(17, 27, 4, 3)
+    offs = O.hypercube(3, 3)
+    ref = dense_subm_conv3d(c, X, W, offs)
+    rows = [0, 5, 77, len(c) - 1]
+    got = O.conv_forward_rows(X, W, O.coordinate_map(c), c, rows, offs)
+    assert rel_err(got, ref[rows]) < 1e-12
+
+
+# --------------------------------------------------------------------------- #
+# backward
+# --------------------------------------------------------------------------- #
+def test_backward_dense_autograd():
+    c = WL.random_coords(19, 500, 3, -5, 6, batch=2)
+    X, _ = WL.random_features(19, len(c), 4)
+    W, _ = WL.random_weights(19, 27, 4, 6)
+    G, _ = WL.random_features(191, len(c), 6)
+    offs = O.hypercube(3, 3)
+    dX, dW = O.conv_backward(X, W, G, O.kernel_map(c, c, offs))
+    lo = c[:, 1:].min(0) - 1
+    shape = c[:, 1:].max(0) - lo + 2
+    vol = dense_volume(c, X, lo, shape).requires_grad_(True)
+    wt = cube3_weight(W, offs).requires_grad_(True)
+    out = F.conv3d(vol, wt, padding=1)
+    gvol = dense_volume(c, G, lo, shape)          # dY zero at inactive outputs
+    (out * gvol).sum().backward()
+    assert rel_err(dX, read_sites(vol.grad, c, lo)) < 1e-12
+    dW_ref = np.stack([wt.grad[:, :, o[0] + 1, o[1] + 1, o[2] + 1].numpy().T for o in offs.tolist()])
+    assert rel_err(dW, dW_ref) < 1e-12
+
+
+def test_backward_adjoint_identities():
+    w = WL.make_workload(3, scale=0.1)
+    offs = O.hybrid(3, 4)
+    m = O.kernel_map(w.coords, w.coords, offs)
+    X = w.X[:, :5].astype(np.float64)
+    W, _ = WL.random_weights(23, len(offs), 5, 4)
+    V, _ = WL.random_weights(24, len(offs), 5, 4)
+    G, _ = WL.random_features(23, w.n, 4)
+    G = G.astype(np.float64)
+    Y = O.conv_forward(X, W, m, w.n)
+    dX, dW = O.conv_backward(X, W, G, m)
+    lhs, rhs = np.sum(Y * G), np.sum(X * dX)
+    assert abs(lhs - rhs) <= 1e-12 * max(abs(lhs), 1.0)
+    lhs2, rhs2 = np.sum(dW * V), np.sum(O.conv_forward(X, V, m, w.n) * G)
+    assert abs(lhs2 - rhs2) <= 1e-12 * max(abs(lhs2), 1.0)
+
+
+def test_backward_finite_differences():
+    c = WL.random_coords(29, 60, 3, -2, 2)
+    X, _ = WL.random_features(29, len(c), 3)
+    X = X.astype(np.float64)
+    W, _ = WL.random_weights(29, 27, 3, 2)
+    W = W.astype(np.float64)
+    G, _ = WL.random_features(291, len(c), 2)
+    offs = O.hypercube(3, 3)
+    m = O.kernel_map(c, c, offs)
+    dX, dW = O.conv_backward(X, W, G, m)
+    f = lambda X_, W_: float(np.sum(O.conv_forward(X_, W_, m, len(c)) * G))
+    h = 1e-6
+    for (r, ch) in [(0, 0), (7, 2), (len(c) - 1, 1)]:
+        E = np.zeros_like(X)
+        E[r, ch] = h
+        assert abs((f(X + E, W) - f(X - E, W)) / (2 * h) - dX[r, ch]) < 1e-7
+    for (k, i, o) in [(13, 0, 0), (0, 2, 1), (26, 1, 1)]:
+        E = np.zeros_like(W)
+        E[k, i, o] = h
+        assert abs((f(X, W + E) - f(X, W - E)) / (2 * h) - dW[k, i, o]) < 1e-7
+
+
+def test_dx_rows_and_transpose_identity():
+    c = WL.random_coords(31, 500, 3, -5, 5, batch=2)
+    G, _ = WL.random_features(31, len(c), 6)
+    W, _ = WL.random_weights(31, 27, 4, 6)
+    X, _ = WL.random_features(311, len(c), 4)
+    offs = O.hypercube(3, 3)
+    m = O.kernel_map(c, c, offs)
+    dX, _ = O.conv_backward(X, W, G, m)
+    rows = [1, 50, 123, len(c) - 1]
+    got = O.conv_dx_rows(G, W, O.coordinate_map(c), c, rows, offs)
+    assert rel_err(got, dX[rows]) < 1e-12
+    # transposed conv with W'_k = W_k^T equals the input gradient
+    Wt = np.ascontiguousarray(np.transpose(W, (0, 2, 1)))
+    assert rel_err(O.conv_forward(G, Wt, O.transposed_map(m), len(c)), dX) < 1e-12
+
+
+def test_duplicate_rejected():
+    c = np.array([[0, 1, 2, 3], [0, 1, 2, 3]])
+    with pytest.raises(O.DuplicateCoordinate):
+        O.coordinate_map(c)
+
+
+# --------------------------------------------------------------------------- #
+# planted mistakes: each pin above must fail for a plausible oracle error
+# --------------------------------------------------------------------------- #
+def _flipped_kernel_map(in_coords, out_coords, offsets, tensor_stride=1):
+    return O.kernel_map(in_coords, out_coords, -np.asarray(offsets), tensor_stride)
+
+
+def _transposed_weight_forward(X, W, maps, n_out):
+    return O.conv_forward(X, np.transpose(W, (0, 2, 1)), maps, n_out)
+
+
+def _dropped_offset_forward(X, W, maps, n_out):
+    return O.conv_forward(X, W[:-1], maps[:-1], n_out)
+
+
+def _truncating_stride(coords, stride):
+    out = {(r[0],) + tuple(int(v / stride) * stride for v in r[1:]) for r in np.asarray(coords).tolist()}
+    return np.array(sorted(out))
+
+
+def test_planted_mistakes_are_caught(monkeypatch):
+    c = WL.random_coords(41, 300, 3, -4, 5, batch=2)
+    offs = O.hypercube(3, 3)
+    assert not maps_equal(_flipped_kernel_map(c, c, offs), brute_force_map(c, c, offs))
+
+    X, _ = WL.random_features(41, len(c), 5)
+    W, _ = WL.random_weights(41, 27, 5, 5)
+    m = O.kernel_map(c, c, offs)
+    ref = dense_subm_conv3d(c, X, W, offs)
+    assert rel_err(_transposed_weight_forward(X, W, m, len(c)), ref) > 1e-3
+    assert rel_err(_dropped_offset_forward(X, W, m, len(c)), ref) > 1e-3
+    assert rel_err(O.conv_forward(X, W, _flipped_kernel_map(c, c, offs), len(c)), ref) > 1e-3
+
+    rows = [[0, -1, -3, 2], [0, 1, -1, -4]]
+    assert {tuple(r) for r in _truncating_stride(rows, 2).tolist()} != \
+        {tuple(r) for r in O.output_coordinates(np.array(rows), 2).tolist()}
+
+    # a backward that forgets the transpose in dX breaks the adjoint identity
+    G, _ = WL.random_features(42, len(c), 5)
+    Y = O.conv_forward(X, W, m, len(c))
+    bad_dX = np.zeros((len(c), 5))
+    for k, (I, Oo) in enumerate(m):
+        bad_dX[I] += G[Oo].astype(np.float64) @ W[k].astype(np.float64)
+    assert abs(np.sum(Y * G) - np.sum(X * bad_dX)) > 1e-6 * abs(np.sum(Y * G))
