@@ -1,0 +1,192 @@
+#!/usr/bin/env python3
+"""Benchmark of the generalized-sparse-convolution hot path on one MI355X.
+
+One step = one pass of the whole hot path over the workload, inputs already
+resident in HBM: coordinate hash table, output coordinates (strided layers),
+kernel maps, convolution forward, input gradient and weight gradient.
+
+    python bench.py [--steps K] [--warmup W] [--workload 1]
+
+Prints one JSON line.  ``value`` is voxels (input rows) per second of whole
+steps; the conv-only rate, the effective GFLOP/s and the kernel-map build time
+are reported beside it.  ``roofline`` covers the dominant kernel (the
+forward gather-MFMA-scatter), timed with HIP events on the stream it runs on.
+``cpu_baseline`` times the CPU oracle (test infrastructure, never tuned) on
+the same workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+MFMA_FP32_PEAK_TFLOPS = 157.3
+METRIC = "sparse-conv fwd+bwd voxels/s & effective GFLOP/s; kernel-map build ms"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def fwd_bytes(n_pairs, n_out, ci, co, K, s):
+    """Gather model: one input row and one index pair per kernel-map pair,
+    every output row written once, the weights read once."""
+    return n_pairs * (s * ci + 8) + n_out * s * co + K * ci * co * s
+
+
+def cpu_baseline(wl, budget_s: float = 30.0):
+    """Time the CPU oracle on this host over one full pass of the workload."""
+    import numpy as np
+    import oracle.gsc_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()]
+        threads = max([t for _, t in blas if t] or [1])
+    except Exception:
+        blas, threads = [], 1
+    kinds = [L.kind for L in wl.layers]
+    t0 = time.perf_counter()
+    X = wl.X.astype(np.float64)
+    dY = wl.dY.astype(np.float64)
+    if kinds == ["subm"]:
+        L = wl.layers[0]
+        m = O.kernel_map(wl.coords, wl.coords, O.region(L.region, L.ksize, wl.D))
+        O.conv_forward(X, L.W, m, wl.n)
+        O.conv_backward(X, L.W, dY, m)
+    else:
+        L0, L1 = wl.layers
+        out = O.output_coordinates(wl.coords, L0.stride)
+        kd = O.kernel_map(wl.coords, out, O.region(L0.region, L0.ksize, wl.D))
+        td = O.transposed_map(kd)
+        Y1 = O.conv_forward(X, L0.W, kd, len(out))
+        O.conv_forward(Y1, L1.W, td, wl.n)
+        dY1, _ = O.conv_backward(Y1, L1.W, dY, td)
+        O.conv_backward(X, L0.W, dY1, kd)
+    t = time.perf_counter() - t0
+    return {"value": wl.n / t, "unit": "voxels/s", "cores": threads, "kind": "oracle",
+            "sample": f"one full pass of {wl.name} ({wl.n} voxels): dict map (single-threaded Python) + "
+                      f"float64 numpy matmuls ({threads} BLAS threads); {t:.1f} s",
+            "seconds": t, "blas": blas}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print("bench.py runs on one GPU only: the sparse-convolution path here is a single-GPU build "
+              "(no collectives); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1904_08755_amd import gsc, pipeline
+    from paper_1904_08755_amd import workloads as WL
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    gsc.lib()
+    t = time.perf_counter()
+    wl = WL.make_workload(args.workload)
+    log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")
+    dw = pipeline.to_device(wl, "cuda")
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        pipeline.run_step(dw)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    steps_events = []
+    last = None
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ev = []
+
+        def mark(name, ev=ev):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            ev.append((name, e))
+
+        mark("start")
+        last = pipeline.run_step(dw, mark)
+        steps_events.append(ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sec = (t1 - t0) / args.steps
+    log(f"timed {args.steps} steps: {sec * 1e3:.3f} ms/step")
+
+    stage = {"map": [], "fwd": [], "bwd": []}
+    for ev in steps_events:
+        d = dict(ev)
+        stage["map"].append(d["start"].elapsed_time(d["map"]))
+        stage["fwd"].append(d["map"].elapsed_time(d["fwd"]))
+        stage["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
+    ms = {k: float(np.mean(v)) for k, v in stage.items()}
+
+    L0 = wl.layers[0]
+    s = 2 if wl.dtype == "bf16" else 4
+    pairs = [km.n_pairs for km in last.kmaps]
+    flops = sum(6.0 * km.n_pairs * L.c_in * L.c_out for km, L in zip(last.kmaps, wl.layers))
+    conv_s = (ms["fwd"] + ms["bwd"]) * 1e-3
+    km0 = last.kmaps[0]
+    n_out0 = km0.n_out
+    # dominant kernel: the forward gather -> MFMA -> LDS-accumulate of layer 0
+    dom_bytes = fwd_bytes(km0.n_pairs, n_out0, L0.c_in, L0.c_out, km0.K, s)
+    dom_ms = ms["fwd"] if len(wl.layers) == 1 else None
+    roof = None
+    if dom_ms:
+        ach = dom_bytes / (dom_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_conv_os (forward)", "bytes_per_launch": int(dom_bytes),
+                "avg_launch_us": round(dom_ms * 1e3, 2)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(wl)
+        log(f"cpu baseline: {cpu['seconds']:.1f} s")
+
+    out = {
+        "metric": METRIC,
+        "value": round(wl.n / sec, 1),
+        "unit": "voxels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "voxels": wl.n, "D": wl.D,
+                   "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
+                   "kernel_map_pairs": pairs, "parallelism": "single GPU"},
+        "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
+        "effective_gflops": round(flops / conv_s / 1e9, 1),
+        "kernel_map_build_ms": round(ms["map"], 4),
+        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

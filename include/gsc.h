@@ -1,0 +1,194 @@
+/*
+ * gsc.h -- C ABI of the generalized sparse convolution library (libgsc.so)
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the hot path of the generalized sparse convolution
+ * of "4D Spatio-Temporal ConvNets: Minkowski Convolutional Neural Networks"
+ * (Choy, Gwak, Savarese, CVPR 2019):
+ *
+ *   gsc_coords_build     hash table over the coordinates of a sparse tensor
+ *                        (Sec. 3, Eq. 1; neighbour queries through a hash
+ *                        table, Sec. 2 and Sec. 4.1)
+ *   gsc_coords_stride    output coordinates of a strided convolution
+ *                        (Sec. 4.2, first paragraph)
+ *   gsc_kernel_map       kernel map M = {(I_i, O_i)}_i for an arbitrary
+ *                        offset set N^D (Sec. 4.2; Eq. 3 of Sec. 3.1)
+ *   gsc_sparse_conv_fwd  Alg. 2 (and the transposed convolution of Sec. 4.2,
+ *                        run on the role-reversed kernel map)
+ *   gsc_sparse_conv_bwd  gradients of Alg. 2 with respect to the input
+ *                        features and the weights (chain rule of Eq. 3)
+ *
+ * Conventions
+ *   - A coordinate row is (b, x_1, ..., x_D) of int32, batch index first;
+ *     1 <= D <= 7.  Coordinates are row-major n x (1 + D); the row index is
+ *     the position in that array.  The batch index is never offset.
+ *   - Features are row-major n x C.  Weights are K x C_in x C_out row-major:
+ *     W[k] is the C_in x C_out matrix of offset k, the transpose of the
+ *     paper's W_i (Sec. 3.1), so a feature row f contributes f * W[k].
+ *   - Offsets follow Eq. 3 literally: output u reads input u + ts (.) o_k.
+ *   - Every device buffer is allocated and owned by the caller.  The library
+ *     never allocates or frees device memory; it exports size queries.
+ *     Host arrays (offsets, strides, counts) are read during the call only.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  All work is
+ *     enqueued on it.
+ *   - Every entry point returns GSC_OK (0) or a negative gsc_status.  On error
+ *     gsc_last_error() returns a message (thread-local, valid until the next
+ *     call on the same thread).  Arguments are validated on the host before
+ *     any HIP call; errors found on the device (duplicate coordinate, table
+ *     full, key range) are read back at the call's synchronisation point.
+ */
+#ifndef GSC_H
+#define GSC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GSC_OK = 0,
+    GSC_EINVAL = -1,  /* invalid argument (null pointer, negative size, bad D, ...) */
+    GSC_ESHORT = -2,  /* caller buffer too small; the required size is returned   */
+    GSC_ERANGE = -3,  /* coordinates span more than 62 bits of packed key          */
+    GSC_EDUP = -4,    /* a coordinate row occurs twice                             */
+    GSC_EFULL = -5,   /* hash table has no free slot                               */
+    GSC_EHIP = -6     /* a HIP runtime call failed                                 */
+} gsc_status;
+
+typedef enum { GSC_F32 = 0, GSC_BF16 = 1 } gsc_dtype;
+
+/* Rows of one kernel-map group: the pairs of every offset are indexed in
+ * groups of this many consecutive output rows (see gsc_kernel_map, gidx). */
+#define GSC_GROUP_ROWS 64
+
+const char* gsc_last_error(void);
+int gsc_abi_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* a1. Coordinate hash table (Sec. 3; hash-table neighbour search, Sec. 2).  */
+/* ------------------------------------------------------------------------ */
+/* Bytes of a table for n coordinates: a 256-byte header (key packing,
+ * bounding box, status) followed by a power-of-two number (>= 2n, >= 64) of
+ * 16-byte slots {uint64 key, int32 row, int32 pad}.  Open addressing with
+ * linear probing; the key is the row packed into <= 62 bits relative to the
+ * bounding box of the coordinates (batch column most significant). */
+size_t gsc_table_bytes(int64_t n);
+
+/* Build the table of `coords` (device, n x (1+D) int32) into `table` (device,
+ * table_bytes >= gsc_table_bytes(n)).  The table maps each row's coordinate to
+ * its row index.  Synchronises `stream` once to read the device status.
+ * Errors: EINVAL, ESHORT (table_bytes too small), ERANGE (bounding box needs
+ * more than 62 key bits), EDUP (a repeated row), EFULL, EHIP.  n == 0 builds an
+ * empty table. */
+int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D,
+                     void* table, size_t table_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* a2. Output coordinates of a strided convolution (Sec. 4.2).              */
+/* ------------------------------------------------------------------------ */
+/* Workspace bytes for gsc_coords_stride with n_in input rows. */
+size_t gsc_stride_ws_bytes(int64_t n_in);
+
+/* For every input row, the output coordinate is (b, floor(x_d / s_d) * s_d)
+ * (floor division, so -1 -> -2 for s = 2); repeated results are merged.  The
+ * output rows are written to `out_coords` (device, capacity n_in rows) in the
+ * order of the first input row that produces each of them, which is
+ * deterministic; `*n_out` (host) receives their number.  `out_table` (device,
+ * >= gsc_table_bytes(n_in) bytes) receives the hash table of the output
+ * coordinates, usable by gsc_kernel_map.  `stride` is a host array of D
+ * positive ints.  Synchronises `stream` once.  Errors: EINVAL, ESHORT (out_table
+ * or ws too small), ERANGE, EHIP. */
+int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                      int32_t* out_coords, int64_t* n_out, void* out_table, size_t out_table_bytes,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* a3. Kernel map (Sec. 4.2; Eq. 3, Sec. 3.1).                              */
+/* ------------------------------------------------------------------------ */
+/* Number of 64-row groups of n_out output rows: ceil(n_out / 64). */
+int64_t gsc_kmap_groups(int64_t n_out);
+/* Workspace bytes for gsc_kernel_map. */
+size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D);
+
+/* For each offset o_k (host array `offsets`, K x D int32, any region: cube,
+ * cross, hybrid, dilated, ...) and each output row j with coordinate u, emit
+ * the pair (r, j) when u + ts (.) o_k is the coordinate of input row r in
+ * `in_table` (built by gsc_coords_build or gsc_coords_stride).  `tensor_stride`
+ * is a host array of D positive ints (the input tensor stride), or NULL for 1.
+ *
+ * Output (device): in_idx[p], out_idx[p] for p < n_pairs, grouped by offset in
+ * the order of `offsets` and, within one offset, in increasing output row
+ * (so the kernel map is deterministic).  seg[K + 1]: pairs of offset k are
+ * [seg[k], seg[k+1]).  gidx[K * G + 1] with G = gsc_kmap_groups(n_out): the
+ * pairs of offset k whose output row lies in [64 g, 64 g + 64) are
+ * [gidx[k*G + g], gidx[k*G + g + 1]); gidx[K*G] = n_pairs.  gidx is what the
+ * convolution kernels use to find the pairs of a tile of output rows.
+ *
+ * *n_pairs (host) receives the total.  If it exceeds cap_pairs, nothing is
+ * written to in_idx/out_idx and ESHORT is returned with *n_pairs set, so the
+ * caller can allocate and call again.  Synchronises `stream` once.
+ *
+ * The transposed convolution's map (roles of input and output reversed,
+ * Sec. 4.2) is this function applied to the table of the original output
+ * coordinates, the original input coordinates as `out_coords` and the negated
+ * offsets: it lists the same pairs, ordered by the original input row. */
+int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D,
+                   const int32_t* offsets, int32_t K, const int32_t* tensor_stride,
+                   int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
+                   int64_t* seg, int64_t* gidx, int64_t* n_pairs,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* a4 / a5. Convolution forward (Alg. 2), transposed convolution.           */
+/* ------------------------------------------------------------------------ */
+/* Y = 0; for every offset k and pair p of it: Y[out_idx[p]] += X[in_idx[p]] W[k].
+ *
+ * dtype GSC_F32: X, W, Y float32.  GSC_BF16: X, W bfloat16, accumulation in
+ * float32, Y rounded to bfloat16 (nearest even).  X: n_in x c_in, Y: n_out x
+ * c_out (overwritten; rows without pairs become 0), W: K x c_in x c_out.
+ * The map (in_idx, out_idx, seg, gidx, n_pairs) must be as gsc_kernel_map
+ * produces it for n_out output rows: out_idx increasing within each offset
+ * and gidx its 64-row group index.  The transposed convolution is this call on
+ * the role-reversed map (see gsc_kernel_map).  Asynchronous; no workspace.
+ * Errors: EINVAL, EHIP. */
+int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in,
+                        const void* W, int32_t c_out, int32_t K,
+                        const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
+                        const int64_t* gidx, int64_t n_pairs,
+                        void* Y, int64_t n_out, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* a6 / a7. Backward: dX and dW.                                             */
+/* ------------------------------------------------------------------------ */
+/* Workspace bytes for gsc_sparse_conv_bwd. */
+size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K);
+
+/* Gradients of gsc_sparse_conv_fwd with the forward map (in_idx, out_idx, seg):
+ *   dW[k] = sum over pairs p of offset k of X[in_idx[p]]^T dY[out_idx[p]]
+ *           (float32, K x c_in x c_out; zero for an offset without pairs),
+ *   dX[r] = sum over pairs (r, j) of offset k of dY[j] W[k]^T (n_in x c_in).
+ * dX is computed on the dX map (t_in_idx, t_out_idx, t_seg, t_gidx, t_n_pairs):
+ * the same pairs with roles reversed (t_in_idx = output rows, t_out_idx = input
+ * rows, increasing within each segment, t_gidx its group index over n_in rows),
+ * and t_wsel (host, K ints) names the offset whose weight segment s of the dX
+ * map uses: dX[t_out_idx[p]] += dY[t_in_idx[p]] W[t_wsel[s]]^T.  For the
+ * role-reversed map from gsc_kernel_map t_wsel is the identity; for a stride-1
+ * map whose offset set is symmetric the forward map itself serves, with
+ * t_wsel[s] = the offset -o_s.
+ * dX (nullable: skip) has X's dtype; dW (nullable: skip) is float32.  Both are
+ * overwritten.  ws: gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K) bytes (only
+ * needed when dW is computed).  The dW reduction order is fixed, so dW is
+ * deterministic.  Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
+int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY,
+                        int64_t n_in, int32_t c_in, int32_t c_out, int32_t K,
+                        const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg, int64_t n_pairs,
+                        const int32_t* t_in_idx, const int32_t* t_out_idx, const int64_t* t_seg,
+                        const int64_t* t_gidx, int64_t t_n_pairs, const int32_t* t_wsel,
+                        void* dX, float* dW, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GSC_H */

@@ -1,0 +1,366 @@
+// Coordinate hash table (a1) and output coordinates of a strided
+// convolution (a2).
+//
+// The table is open addressing with linear probing over 16-byte slots in
+// HBM.  A coordinate row (b, x_1..x_D) is packed into a key relative to the
+// bounding box of the rows (computed on the device, so the build needs no
+// host round trip before the insert), batch column in the high bits, so the
+// numeric order of keys is the lexicographic order of rows.
+#include <climits>
+
+#include "gsc_internal.h"
+
+namespace gsc {
+
+constexpr int kThreads = 256;
+
+struct StrideArg {
+    int32_t s[kMaxCols];   // s[0] = 1 (batch), s[c] = stride of spatial column c
+    int32_t on;            // 0: identity transform
+};
+
+__device__ __forceinline__ void load_row(const int32_t* coords, int64_t r, int ncol, const StrideArg& st,
+                                         int64_t* v) {
+    for (int c = 0; c < ncol; ++c) {
+        int64_t x = coords[r * ncol + c];
+        if (st.on && c > 0) x = floor_mul(x, st.s[c]);
+        v[c] = x;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) k_table_init(TableHeader* h, Slot* slots, int64_t cap, int ncol,
+                                                         int64_t n, int32_t init_val) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cap; i += stride) {
+        Slot e;
+        e.key = kEmptyKey;
+        e.val = init_val;
+        e.pad = 0;
+        slots[i] = e;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        h->magic = kTableMagic;
+        h->ncol = ncol;
+        h->capacity = cap;
+        h->n = n;
+        h->status = 0;
+        h->total_bits = 0;
+        for (int c = 0; c < kMaxCols; ++c) {
+            h->lo[c] = INT_MAX;
+            h->hi[c] = INT_MIN;
+            h->shift[c] = 0;
+            h->bits[c] = 0;
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) k_bbox(const int32_t* coords, int64_t n, int ncol, StrideArg st,
+                                                   TableHeader* h) {
+    int64_t lo[kMaxCols], hi[kMaxCols];
+    for (int c = 0; c < kMaxCols; ++c) {
+        lo[c] = INT_MAX;
+        hi[c] = INT_MIN;
+    }
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += stride) {
+        int64_t v[kMaxCols];
+        load_row(coords, r, ncol, st, v);
+        for (int c = 0; c < ncol; ++c) {
+            if (v[c] < INT_MIN || v[c] > INT_MAX) atomicOr(&h->status, ST_RANGE);  // strided out of int32
+            lo[c] = v[c] < lo[c] ? v[c] : lo[c];
+            hi[c] = v[c] > hi[c] ? v[c] : hi[c];
+        }
+    }
+    for (int c = 0; c < ncol; ++c) {
+        int a = (int)lo[c], b = (int)hi[c];
+        for (int d = 32; d > 0; d >>= 1) {
+            int ta = __shfl_xor(a, d, 64), tb = __shfl_xor(b, d, 64);
+            a = ta < a ? ta : a;
+            b = tb > b ? tb : b;
+        }
+        if (__lane_id() == 0) {
+            atomicMin(&h->lo[c], a);
+            atomicMax(&h->hi[c], b);
+        }
+    }
+}
+
+// one thread: bit widths and shifts of the packed key
+__global__ void k_plan(TableHeader* h) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const int ncol = h->ncol;
+    int total = 0;
+    int bits[kMaxCols];
+    for (int c = 0; c < ncol; ++c) {
+        int64_t range = (int64_t)h->hi[c] - (int64_t)h->lo[c];
+        int b = 0;
+        if (range > 0) b = 64 - __clzll((unsigned long long)range);
+        if (h->lo[c] > h->hi[c]) b = 0;   // no rows
+        bits[c] = b;
+        total += b;
+    }
+    int sh = 0;
+    for (int c = ncol - 1; c >= 0; --c) {
+        h->shift[c] = sh;
+        h->bits[c] = bits[c];
+        sh += bits[c];
+    }
+    h->total_bits = total;
+    if (total > kMaxKeyBits) h->status |= ST_RANGE;
+}
+
+__global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int64_t n, TableHeader* h,
+                                                     Slot* slots) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    if (h->status & ST_RANGE) return;
+    const int ncol = h->ncol;
+    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    int64_t v[kMaxCols];
+    StrideArg none{};
+    load_row(coords, r, ncol, none, v);
+    unsigned long long key;
+    if (!pack_key(h, ncol, v, &key)) {  // cannot happen: the box holds every row
+        atomicOr(&h->status, ST_RANGE);
+        return;
+    }
+    unsigned long long s = mix64(key) & mask;
+    for (unsigned long long i = 0; i <= mask; ++i) {
+        unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
+        if (prev == kEmptyKey) {
+            slots[s].val = (int32_t)r;
+            return;
+        }
+        if (prev == key) {
+            atomicOr(&h->status, ST_DUP);
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+    atomicOr(&h->status, ST_FULL);
+}
+
+// strided: find-or-insert the strided key, keep the smallest input row that
+// produces it; remember the slot of every row.
+__global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, int64_t n, StrideArg st,
+                                                         TableHeader* h, Slot* slots, int64_t* slot_of) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    if (h->status & ST_RANGE) {
+        slot_of[r] = 0;
+        return;
+    }
+    const int ncol = h->ncol;
+    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    int64_t v[kMaxCols];
+    load_row(coords, r, ncol, st, v);
+    unsigned long long key;
+    if (!pack_key(h, ncol, v, &key)) {
+        atomicOr(&h->status, ST_RANGE);
+        slot_of[r] = 0;
+        return;
+    }
+    unsigned long long s = mix64(key) & mask;
+    for (unsigned long long i = 0; i <= mask; ++i) {
+        unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
+        if (prev == kEmptyKey || prev == key) {
+            atomicMin(&slots[s].val, (int32_t)r);
+            slot_of[r] = (int64_t)s;
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+    atomicOr(&h->status, ST_FULL);
+    slot_of[r] = 0;
+}
+
+// mark representatives (slot holds this row) and count them per 64-row group
+__global__ void __launch_bounds__(kThreads) k_rep_count(int64_t n, const TableHeader* h, const Slot* slots,
+                                                        int64_t* slot_of, int32_t* cnt) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool rep = false;
+    if (r < n && h->status == 0) {
+        const int64_t s = slot_of[r];
+        rep = slots[s].val == (int32_t)r;
+        if (rep) slot_of[r] = ~s;   // negative: representative
+    }
+    const unsigned long long m = __ballot(rep);
+    const int64_t g = r >> 6;
+    if (__lane_id() == 0 && g * 64 < n) cnt[g] = __popcll(m);
+}
+
+__global__ void __launch_bounds__(kThreads) k_rep_write(const int32_t* coords, int64_t n, StrideArg st,
+                                                        TableHeader* h, Slot* slots, const int64_t* slot_of,
+                                                        const int64_t* off, int32_t* out_coords) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool rep = false;
+    int64_t s = 0;
+    if (r < n && h->status == 0) {
+        s = slot_of[r];
+        rep = s < 0;
+        s = ~s;
+    }
+    const unsigned long long m = __ballot(rep);
+    if (!rep) return;
+    const int64_t row = off[r >> 6] + __popcll(m & lanemask_lt());
+    const int ncol = h->ncol;
+    int64_t v[kMaxCols];
+    load_row(coords, r, ncol, st, v);
+    for (int c = 0; c < ncol; ++c) out_coords[row * ncol + c] = (int32_t)v[c];
+    slots[s].val = (int32_t)row;
+}
+
+static unsigned grid_for(int64_t n, int per = kThreads) {
+    int64_t g = (n + per - 1) / per;
+    if (g < 1) g = 1;
+    return (unsigned)g;
+}
+
+static unsigned grid_capped(int64_t n) {
+    int64_t g = (n + kThreads - 1) / kThreads;
+    if (g < 1) g = 1;
+    if (g > 2048) g = 2048;
+    return (unsigned)g;
+}
+
+static int read_status(const void* table, hipStream_t s, TableHeader* out) {
+    GSC_HIP(hipMemcpyAsync(out, table, sizeof(TableHeader), hipMemcpyDeviceToHost, s));
+    GSC_HIP(hipStreamSynchronize(s));
+    return GSC_OK;
+}
+
+static int status_to_code(const TableHeader& h, const char* what) {
+    if (h.status & ST_RANGE)
+        return fail(GSC_ERANGE, "%s: coordinates need more than %d key bits (box needs %d)", what, kMaxKeyBits,
+                    h.total_bits);
+    if (h.status & ST_DUP) return fail(GSC_EDUP, "%s: a coordinate row occurs more than once", what);
+    if (h.status & ST_FULL) return fail(GSC_EFULL, "%s: hash table full", what);
+    return GSC_OK;
+}
+
+}  // namespace gsc
+
+using namespace gsc;
+
+extern "C" {
+
+size_t gsc_table_bytes(int64_t n) {
+    if (n < 0) return 0;
+    return kHeaderBytes + (size_t)table_capacity(n) * sizeof(Slot);
+}
+
+int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D, void* table, size_t table_bytes, void* stream) {
+    clear_error();
+    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "coords_build: D=%d outside [1,%d]", D, kMaxCols - 1);
+    if (n < 0 || n > INT32_MAX) return fail(GSC_EINVAL, "coords_build: n=%lld outside [0, 2^31)", (long long)n);
+    if (!table) return fail(GSC_EINVAL, "coords_build: table is null");
+    if (n > 0 && !coords) return fail(GSC_EINVAL, "coords_build: coords is null");
+    if (table_bytes < gsc_table_bytes(n))
+        return fail(GSC_ESHORT, "coords_build: table needs %zu bytes, got %zu", gsc_table_bytes(n), table_bytes);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int ncol = D + 1;
+    const int64_t cap = table_capacity(n);
+    TableHeader* h = reinterpret_cast<TableHeader*>(table);
+    Slot* slots = table_slots(table);
+    hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol, n, -1);
+    GSC_LAUNCH_CHECK();
+    StrideArg none{};
+    if (n > 0) {
+        hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n)), dim3(kThreads), 0, s, coords, n, ncol, none, h);
+        GSC_LAUNCH_CHECK();
+    }
+    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+    GSC_LAUNCH_CHECK();
+    if (n > 0) {
+        hipLaunchKernelGGL(k_insert, dim3(grid_for(n)), dim3(kThreads), 0, s, coords, n, h, slots);
+        GSC_LAUNCH_CHECK();
+    }
+    TableHeader hh;
+    int rc = read_status(table, s, &hh);
+    if (rc) return rc;
+    return status_to_code(hh, "coords_build");
+}
+
+size_t gsc_stride_ws_bytes(int64_t n_in) {
+    if (n_in < 0) return 0;
+    const int64_t groups = (n_in + 63) / 64;
+    size_t b = (size_t)n_in * sizeof(int64_t);            // slot of each row
+    b = (b + 255) & ~(size_t)255;
+    b += (size_t)groups * sizeof(int32_t);                // counts
+    b = (b + 255) & ~(size_t)255;
+    b += (size_t)(groups + 1) * sizeof(int64_t);          // offsets
+    b = (b + 255) & ~(size_t)255;
+    b += scan_ws_bytes(groups);
+    return b + 256;
+}
+
+int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                      int32_t* out_coords, int64_t* n_out, void* out_table, size_t out_table_bytes, void* ws,
+                      size_t ws_bytes, void* stream) {
+    clear_error();
+    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "coords_stride: D=%d outside [1,%d]", D, kMaxCols - 1);
+    if (n_in < 0 || n_in > INT32_MAX) return fail(GSC_EINVAL, "coords_stride: n_in=%lld invalid", (long long)n_in);
+    if (!stride || !n_out || !out_table) return fail(GSC_EINVAL, "coords_stride: null stride/n_out/out_table");
+    if (n_in > 0 && (!in_coords || !out_coords || !ws))
+        return fail(GSC_EINVAL, "coords_stride: null in_coords/out_coords/ws");
+    StrideArg st{};
+    st.on = 1;
+    st.s[0] = 1;
+    for (int d = 0; d < D; ++d) {
+        if (stride[d] < 1) return fail(GSC_EINVAL, "coords_stride: stride[%d]=%d must be >= 1", d, stride[d]);
+        st.s[d + 1] = stride[d];
+    }
+    if (out_table_bytes < gsc_table_bytes(n_in))
+        return fail(GSC_ESHORT, "coords_stride: out_table needs %zu bytes, got %zu", gsc_table_bytes(n_in),
+                    out_table_bytes);
+    if (n_in > 0 && ws_bytes < gsc_stride_ws_bytes(n_in))
+        return fail(GSC_ESHORT, "coords_stride: ws needs %zu bytes, got %zu", gsc_stride_ws_bytes(n_in), ws_bytes);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int ncol = D + 1;
+    const int64_t cap = table_capacity(n_in);
+    TableHeader* h = reinterpret_cast<TableHeader*>(out_table);
+    Slot* slots = table_slots(out_table);
+    hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol,
+                       (int64_t)0, (int32_t)INT_MAX);
+    GSC_LAUNCH_CHECK();
+    if (n_in == 0) {
+        hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+        GSC_LAUNCH_CHECK();
+        GSC_HIP(hipStreamSynchronize(s));
+        *n_out = 0;
+        return GSC_OK;
+    }
+    const int64_t groups = (n_in + 63) / 64;
+    char* w = reinterpret_cast<char*>(ws);
+    int64_t* slot_of = reinterpret_cast<int64_t*>(w);
+    w += ((size_t)n_in * sizeof(int64_t) + 255) & ~(size_t)255;
+    int32_t* cnt = reinterpret_cast<int32_t*>(w);
+    w += ((size_t)groups * sizeof(int32_t) + 255) & ~(size_t)255;
+    int64_t* off = reinterpret_cast<int64_t*>(w);
+    w += ((size_t)(groups + 1) * sizeof(int64_t) + 255) & ~(size_t)255;
+    void* scan_ws = w;
+
+    hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n_in)), dim3(kThreads), 0, s, in_coords, n_in, ncol, st, h);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_insert_min, dim3(grid_for(n_in)), dim3(kThreads), 0, s, in_coords, n_in, st, h, slots,
+                       slot_of);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_rep_count, dim3(grid_for(n_in)), dim3(kThreads), 0, s, n_in, h, slots, slot_of, cnt);
+    GSC_LAUNCH_CHECK();
+    int rc = scan_counts(cnt, groups, off, &h->n, scan_ws, s);   // header n = number of output rows
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_rep_write, dim3(grid_for(n_in)), dim3(kThreads), 0, s, in_coords, n_in, st, h, slots,
+                       slot_of, off, out_coords);
+    GSC_LAUNCH_CHECK();
+    TableHeader hh;
+    rc = read_status(out_table, s, &hh);
+    if (rc) return rc;
+    rc = status_to_code(hh, "coords_stride");
+    if (rc) return rc;
+    *n_out = hh.n;
+    return GSC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,141 @@
+// Internal definitions shared by the HIP sources of libgsc.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstddef>
+
+#include "../../include/gsc.h"
+
+namespace gsc {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+#define GSC_HIP(call)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return ::gsc::fail(GSC_EHIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+#define GSC_LAUNCH_CHECK()                                                             \
+    do {                                                                               \
+        hipError_t e_ = hipGetLastError();                                             \
+        if (e_ != hipSuccess)                                                          \
+            return ::gsc::fail(GSC_EHIP, "kernel launch failed: %s", hipGetErrorString(e_)); \
+    } while (0)
+
+// ---------------------------------------------------------------------------
+// coordinate hash table (lives in caller memory)
+// ---------------------------------------------------------------------------
+constexpr int kMaxCols = 8;                       // 1 batch column + up to 7 spatial
+constexpr unsigned long long kEmptyKey = ~0ull;    // packed keys use <= 62 bits
+constexpr uint32_t kTableMagic = 0x54435347u;      // "GSCT"
+constexpr size_t kHeaderBytes = 256;
+constexpr int kMaxKeyBits = 62;
+
+enum : int { ST_DUP = 1, ST_FULL = 2, ST_RANGE = 4 };
+
+struct TableHeader {
+    uint32_t magic;
+    int32_t ncol;          // 1 + D
+    int64_t capacity;      // slots, power of two
+    int64_t n;             // number of keys
+    int32_t status;        // ST_* bits set on the device
+    int32_t total_bits;
+    int32_t lo[kMaxCols];  // bounding box, inclusive
+    int32_t hi[kMaxCols];
+    int32_t shift[kMaxCols];
+    int32_t bits[kMaxCols];
+};
+static_assert(sizeof(TableHeader) <= kHeaderBytes, "header too large");
+
+struct alignas(16) Slot {
+    unsigned long long key;
+    int32_t val;
+    int32_t pad;
+};
+static_assert(sizeof(Slot) == 16, "slot must be 16 bytes");
+
+inline int64_t table_capacity(int64_t n) {
+    int64_t cap = 64;
+    while (cap < 2 * n) cap <<= 1;
+    return cap;
+}
+
+inline __host__ __device__ Slot* table_slots(void* t) {
+    return reinterpret_cast<Slot*>(reinterpret_cast<char*>(t) + kHeaderBytes);
+}
+inline __host__ __device__ const Slot* table_slots(const void* t) {
+    return reinterpret_cast<const Slot*>(reinterpret_cast<const char*>(t) + kHeaderBytes);
+}
+
+// 64-bit finaliser of MurmurHash3 (Appleby): a bijective avalanche mix.
+__device__ __forceinline__ unsigned long long mix64(unsigned long long k) {
+    k ^= k >> 33;
+    k *= 0xff51afd7ed558ccdull;
+    k ^= k >> 33;
+    k *= 0xc4ceb9fe1a85ec53ull;
+    k ^= k >> 33;
+    return k;
+}
+
+// Pack a coordinate (already offset, in 64-bit) into a key.  Returns false if
+// it lies outside the table's bounding box: such a coordinate cannot be in
+// the table, so a query for it is a miss (never an alias of another key).
+__device__ __forceinline__ bool pack_key(const TableHeader* h, int ncol, const int64_t* v,
+                                         unsigned long long* key) {
+    unsigned long long k = 0;
+    for (int c = 0; c < ncol; ++c) {
+        if (v[c] < h->lo[c] || v[c] > h->hi[c]) return false;
+        k |= (unsigned long long)(v[c] - h->lo[c]) << h->shift[c];
+    }
+    *key = k;
+    return true;
+}
+
+// Linear-probing lookup; at most `capacity` probes, so it ends even on a
+// table left full by a failed build.
+__device__ __forceinline__ int32_t table_find(const Slot* slots, unsigned long long mask,
+                                              unsigned long long key) {
+    unsigned long long s = mix64(key) & mask;
+    for (unsigned long long i = 0; i <= mask; ++i) {
+        const Slot e = slots[s];
+        if (e.key == key) return e.val;
+        if (e.key == kEmptyKey) return -1;
+        s = (s + 1) & mask;
+    }
+    return -1;
+}
+
+// floor(a / s) * s for s > 0
+__device__ __forceinline__ int64_t floor_mul(int64_t a, int64_t s) {
+    int64_t q = a / s;
+    if ((a % s) != 0 && a < 0) q -= 1;
+    return q * s;
+}
+
+// ---------------------------------------------------------------------------
+// device-wide exclusive scan of int32 counts into int64 offsets:
+// out[i] = sum(cnt[0..i)), out[m] = total; optionally also *total_out.
+// ---------------------------------------------------------------------------
+size_t scan_ws_bytes(int64_t m);
+int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
+                hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// wave helpers (wave64)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ unsigned long long lanemask_lt() {
+    const int l = __lane_id();
+    return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+}  // namespace gsc

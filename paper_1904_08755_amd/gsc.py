@@ -1,0 +1,284 @@
+"""Python binding of libgsc.so (include/gsc.h): argument marshalling only.
+
+Every function here checks tensor shapes, devices and dtypes, allocates the
+caller-owned output and workspace buffers with torch (device memory and
+streams are all torch provides), and calls the C entry point of the same
+name.  All computation runs in the HIP kernels of the library; if the
+library is missing, loading fails with an error (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgsc.so")
+
+GSC_OK, GSC_EINVAL, GSC_ESHORT, GSC_ERANGE, GSC_EDUP, GSC_EFULL, GSC_EHIP = 0, -1, -2, -3, -4, -5, -6
+GSC_F32, GSC_BF16 = 0, 1
+GROUP_ROWS = 64
+
+_STATUS = {GSC_EINVAL: "EINVAL", GSC_ESHORT: "ESHORT", GSC_ERANGE: "ERANGE", GSC_EDUP: "EDUP",
+           GSC_EFULL: "EFULL", GSC_EHIP: "EHIP"}
+
+
+class GscError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_c_i32p = ctypes.POINTER(ctypes.c_int32)
+_c_i64p = ctypes.POINTER(ctypes.c_int64)
+_vp = ctypes.c_void_p
+_i32, _i64, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+_SIGS = {
+    "gsc_last_error": (ctypes.c_char_p, []),
+    "gsc_abi_version": (ctypes.c_int, []),
+    "gsc_table_bytes": (_sz, [_i64]),
+    "gsc_coords_build": (ctypes.c_int, [_vp, _i64, _i32, _vp, _sz, _vp]),
+    "gsc_stride_ws_bytes": (_sz, [_i64]),
+    "gsc_coords_stride": (ctypes.c_int, [_vp, _i64, _i32, _c_i32p, _vp, _c_i64p, _vp, _sz, _vp, _sz, _vp]),
+    "gsc_kmap_groups": (_i64, [_i64]),
+    "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
+    "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
+                                      _c_i64p, _vp, _sz, _vp]),
+    "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp,
+                                           _i64, _vp]),
+    "gsc_conv_bwd_ws_bytes": (_sz, [_i64, _i32, _i32, _i32]),
+    "gsc_sparse_conv_bwd": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp,
+                                           _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _i64, _vp, _sz, _vp]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgsc.so (built in-tree by ``python -m paper_1904_08755_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise GscError(GSC_EHIP, f"{LIB_PATH} is not built; run python -m paper_1904_08755_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _check(rc: int):
+    if rc != GSC_OK:
+        raise GscError(rc, lib().gsc_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _host_i32(a) -> ctypes.Array:
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32)).ravel()
+    return (ctypes.c_int32 * max(len(a), 1))(*a.tolist())
+
+
+def _need(t: torch.Tensor, dtype, name, dims=None):
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dims is not None and t.dim() != dims:
+        raise ValueError(f"{name} must have {dims} dims")
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------------------- #
+# a1: coordinate hash table
+# --------------------------------------------------------------------------- #
+def gsc_table_bytes(n: int) -> int:
+    return int(lib().gsc_table_bytes(n))
+
+
+def gsc_coords_build(coords: torch.Tensor, table: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _need(coords, torch.int32, "coords", 2)
+    n, ncol = coords.shape
+    if table is None:
+        table = torch.empty(gsc_table_bytes(n), dtype=torch.uint8, device=coords.device)
+    _need(table, torch.uint8, "table", 1)
+    _check(lib().gsc_coords_build(_ptr(coords), n, ncol - 1, _ptr(table), table.numel(), _stream(stream)))
+    return table
+
+
+# --------------------------------------------------------------------------- #
+# a2: output coordinates of a strided convolution
+# --------------------------------------------------------------------------- #
+def gsc_coords_stride(coords: torch.Tensor, stride: Sequence[int], out_table: Optional[torch.Tensor] = None,
+                      stream=None):
+    """Returns (out_coords [n_out, 1+D] int32, out_table)."""
+    _need(coords, torch.int32, "coords", 2)
+    n, ncol = coords.shape
+    D = ncol - 1
+    st = [int(stride)] * D if np.isscalar(stride) else [int(v) for v in stride]
+    if len(st) != D:
+        raise ValueError("stride needs D entries")
+    dev = coords.device
+    out = torch.empty((max(n, 1), ncol), dtype=torch.int32, device=dev)
+    if out_table is None:
+        out_table = torch.empty(gsc_table_bytes(n), dtype=torch.uint8, device=dev)
+    ws = _ws(lib().gsc_stride_ws_bytes(n), dev)
+    n_out = ctypes.c_int64(0)
+    _check(lib().gsc_coords_stride(_ptr(coords), n, D, _host_i32(st), _ptr(out), ctypes.byref(n_out),
+                                   _ptr(out_table), out_table.numel(), _ptr(ws), ws.numel(), _stream(stream)))
+    return out[: n_out.value], out_table
+
+
+# --------------------------------------------------------------------------- #
+# a3: kernel map
+# --------------------------------------------------------------------------- #
+@dataclasses.dataclass
+class KernelMap:
+    in_idx: torch.Tensor       # int32 [n_pairs]
+    out_idx: torch.Tensor      # int32 [n_pairs]
+    seg: torch.Tensor          # int64 [K + 1]
+    gidx: torch.Tensor         # int64 [K * G + 1]
+    n_pairs: int
+    n_out: int
+    offsets: np.ndarray        # K x D
+
+    @property
+    def K(self) -> int:
+        return int(self.offsets.shape[0])
+
+
+def gsc_kmap_groups(n_out: int) -> int:
+    return int(lib().gsc_kmap_groups(n_out))
+
+
+def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, tensor_stride=None,
+                   cap_pairs: Optional[int] = None, stream=None) -> KernelMap:
+    _need(in_table, torch.uint8, "in_table", 1)
+    _need(out_coords, torch.int32, "out_coords", 2)
+    offs = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    K, D = offs.shape
+    n_out = out_coords.shape[0]
+    if out_coords.shape[1] != D + 1:
+        raise ValueError("offsets must be K x D with D = out_coords columns - 1")
+    dev = out_coords.device
+    G = gsc_kmap_groups(n_out)
+    seg = torch.empty(K + 1, dtype=torch.int64, device=dev)
+    gidx = torch.empty(K * G + 1, dtype=torch.int64, device=dev)
+    ws = _ws(lib().gsc_kmap_ws_bytes(n_out, K, D), dev)
+    ts = None if tensor_stride is None else _host_i32([tensor_stride] * D if np.isscalar(tensor_stride)
+                                                      else tensor_stride)
+    cap = K * n_out if cap_pairs is None else int(cap_pairs)
+    in_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    out_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    n_pairs = ctypes.c_int64(0)
+    rc = lib().gsc_kernel_map(_ptr(in_table), _ptr(out_coords), n_out, D, _host_i32(offs), K, ts, _ptr(in_idx),
+                              _ptr(out_idx), cap, _ptr(seg), _ptr(gidx), ctypes.byref(n_pairs), _ptr(ws), ws.numel(),
+                              _stream(stream))
+    _check(rc)
+    m = n_pairs.value
+    return KernelMap(in_idx[:m], out_idx[:m], seg, gidx, m, n_out, offs)
+
+
+def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offsets, tensor_stride=None,
+                          stream=None) -> KernelMap:
+    """The role-reversed map (Sec. 4.2): same pairs, listed by original input row."""
+    return gsc_kernel_map(out_table, in_coords, -np.asarray(offsets, dtype=np.int32), tensor_stride, stream=stream)
+
+
+def negation_permutation(offsets) -> np.ndarray:
+    """s -> index of -o_s (for symmetric offset sets)."""
+    offs = np.asarray(offsets)
+    index = {tuple(o): k for k, o in enumerate(offs.tolist())}
+    return np.array([index[tuple(-v for v in o)] for o in offs.tolist()], dtype=np.int32)
+
+
+# --------------------------------------------------------------------------- #
+# a4-a7: convolution
+# --------------------------------------------------------------------------- #
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GSC_F32
+    if t.dtype == torch.bfloat16:
+        return GSC_BF16
+    raise ValueError(f"unsupported feature dtype {t.dtype}")
+
+
+def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out: Optional[int] = None,
+                        Y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    dt = _dt(X)
+    _need(X, X.dtype, "X", 2)
+    _need(W, X.dtype, "W", 3)
+    K, ci, co = W.shape
+    if X.shape[1] != ci or K != kmap.K:
+        raise ValueError("shape mismatch between X, W and the kernel map")
+    n_out = kmap.n_out if n_out is None else n_out
+    if n_out != kmap.n_out:
+        raise ValueError("n_out differs from the kernel map's output rows")
+    if Y is None:
+        Y = torch.empty((n_out, co), dtype=X.dtype, device=X.device)
+    _need(Y, X.dtype, "Y", 2)
+    _check(lib().gsc_sparse_conv_fwd(dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx),
+                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_pairs, _ptr(Y),
+                                     n_out, _stream(stream)))
+    return Y
+
+
+def gsc_conv_bwd_ws_bytes(n_pairs: int, c_in: int, c_out: int, K: int) -> int:
+    return int(lib().gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K))
+
+
+def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap: KernelMap,
+                        tmap: KernelMap, wsel, need_dx: bool = True, need_dw: bool = True,
+                        dX: Optional[torch.Tensor] = None, dW: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None, stream=None):
+    """Returns (dX or None, dW or None).  ``tmap`` is the dX map (role-reversed
+    pairs, sorted by input row) and ``wsel`` its per-segment weight index."""
+    dt = _dt(X)
+    _need(X, X.dtype, "X", 2)
+    _need(W, X.dtype, "W", 3)
+    _need(dY, X.dtype, "dY", 2)
+    K, ci, co = W.shape
+    n_in, n_out = X.shape[0], dY.shape[0]
+    if X.shape[1] != ci or dY.shape[1] != co or kmap.K != K or tmap.K != K:
+        raise ValueError("shape mismatch")
+    if kmap.n_out != n_out or tmap.n_out != n_in:
+        raise ValueError("kernel maps do not match the row counts")
+    dev = X.device
+    if need_dx and dX is None:
+        dX = torch.empty((n_in, ci), dtype=X.dtype, device=dev)
+    if need_dw and dW is None:
+        dW = torch.empty((K, ci, co), dtype=torch.float32, device=dev)
+    if need_dw and ws is None:
+        ws = _ws(gsc_conv_bwd_ws_bytes(kmap.n_pairs, ci, co, K), dev)
+    sel = _host_i32(wsel)
+    _check(lib().gsc_sparse_conv_bwd(
+        dt, _ptr(X), _ptr(W), _ptr(dY), n_in, ci, co, K,
+        _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg), kmap.n_pairs,
+        _ptr(tmap.in_idx), _ptr(tmap.out_idx), _ptr(tmap.seg), _ptr(tmap.gidx), tmap.n_pairs, sel,
+        _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
+        _ptr(ws) if need_dw else None, ws.numel() if need_dw else 0, _stream(stream)))
+    return (dX if need_dx else None), (dW if need_dw else None)

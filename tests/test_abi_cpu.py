@@ -1,0 +1,142 @@
+"""CPU checks of the C-ABI library: it loads, exports every entry point that
+include/gsc.h declares, and its host-side validation rejects bad arguments
+before any HIP call (so these run without a GPU).  Also checks the product's
+region lists against the oracle's, since the two are written independently."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle.gsc_oracle as O
+from paper_1904_08755_amd import gsc, regions
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gsc.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gsc_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(gsc.LIB_PATH):
+        pytest.skip("libgsc.so not built")
+    return gsc.lib()
+
+
+def test_header_symbols_exported(L):
+    syms = declared_symbols()
+    assert len(syms) >= 12
+    for s in syms:
+        assert hasattr(L, s), s
+    assert sorted(gsc.exported_symbols()) == syms
+
+
+def test_abi_version(L):
+    assert L.gsc_abi_version() == 1
+
+
+def test_size_queries(L):
+    assert L.gsc_table_bytes(0) == 256 + 64 * 16
+    assert L.gsc_table_bytes(32) == 256 + 64 * 16
+    assert L.gsc_table_bytes(33) == 256 + 128 * 16
+    assert L.gsc_table_bytes(300_000) == 256 + (1 << 20) * 16
+    assert L.gsc_table_bytes(-1) == 0
+    assert L.gsc_kmap_groups(0) == 0
+    assert L.gsc_kmap_groups(1) == 1
+    assert L.gsc_kmap_groups(64) == 1
+    assert L.gsc_kmap_groups(65) == 2
+    assert L.gsc_kmap_ws_bytes(1000, 27, 3) > 27 * 16 * 4
+    assert L.gsc_kmap_ws_bytes(1000, 0, 3) == 0
+    assert L.gsc_stride_ws_bytes(1000) >= 8000
+    assert L.gsc_conv_bwd_ws_bytes(100000, 32, 32, 27) >= 27 * 32 * 32 * 4
+    assert L.gsc_conv_bwd_ws_bytes(10, 0, 32, 27) == 0
+
+
+def _err(L):
+    return L.gsc_last_error().decode()
+
+
+def test_coords_build_validation(L):
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+    assert L.gsc_coords_build(fake, 10, 0, fake, 1 << 20, None) == gsc.GSC_EINVAL
+    assert "D=0" in _err(L)
+    assert L.gsc_coords_build(fake, 10, 8, fake, 1 << 20, None) == gsc.GSC_EINVAL
+    assert L.gsc_coords_build(fake, -1, 3, fake, 1 << 20, None) == gsc.GSC_EINVAL
+    assert L.gsc_coords_build(None, 10, 3, fake, 1 << 20, None) == gsc.GSC_EINVAL
+    assert L.gsc_coords_build(fake, 10, 3, None, 1 << 20, None) == gsc.GSC_EINVAL
+    need = L.gsc_table_bytes(1000)
+    assert L.gsc_coords_build(fake, 1000, 3, fake, need - 1, None) == gsc.GSC_ESHORT
+    assert str(need) in _err(L)
+
+
+def test_coords_stride_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    n_out = ctypes.c_int64(0)
+    st = (ctypes.c_int32 * 3)(2, 2, 0)
+    assert L.gsc_coords_stride(fake, 100, 3, st, fake, ctypes.byref(n_out), fake, 1 << 20, fake, 1 << 20,
+                               None) == gsc.GSC_EINVAL
+    st = (ctypes.c_int32 * 3)(2, 2, 2)
+    assert L.gsc_coords_stride(fake, 100, 3, st, fake, ctypes.byref(n_out), fake, 10, fake, 1 << 20,
+                               None) == gsc.GSC_ESHORT
+    assert L.gsc_coords_stride(fake, 100, 3, st, fake, ctypes.byref(n_out), fake, 1 << 20, fake, 8,
+                               None) == gsc.GSC_ESHORT
+    assert L.gsc_coords_stride(fake, 100, 3, None, fake, ctypes.byref(n_out), fake, 1 << 20, fake, 1 << 20,
+                               None) == gsc.GSC_EINVAL
+
+
+def test_kernel_map_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    n = ctypes.c_int64(0)
+    offs = (ctypes.c_int32 * 3)(0, 0, 0)
+    ts_bad = (ctypes.c_int32 * 3)(1, 0, 1)
+    ws = L.gsc_kmap_ws_bytes(100, 1, 3)
+    args = lambda K, ts, wsb, cap=10: (fake, fake, 100, 3, offs, K, ts, fake, fake, cap, fake, fake,
+                                       ctypes.byref(n), fake, wsb, None)
+    assert L.gsc_kernel_map(*args(0, None, ws)) == gsc.GSC_EINVAL
+    assert L.gsc_kernel_map(*args(1, ts_bad, ws)) == gsc.GSC_EINVAL
+    assert L.gsc_kernel_map(*args(1, None, ws - 1)) == gsc.GSC_ESHORT
+    assert L.gsc_kernel_map(*args(1, None, ws, cap=-1)) == gsc.GSC_EINVAL
+    big = (ctypes.c_int32 * 3)(1 << 29, 0, 0)
+    ts4 = (ctypes.c_int32 * 3)(4, 1, 1)
+    a = list(args(1, ts4, ws))
+    a[4] = big
+    assert L.gsc_kernel_map(*a) == gsc.GSC_ERANGE
+
+
+def test_conv_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    fwd = lambda dt, ci, K, npairs=10: L.gsc_sparse_conv_fwd(dt, fake, 10, ci, fake, 4, K, fake, fake, fake, fake,
+                                                             npairs, fake, 10, None)
+    assert fwd(7, 4, 27) == gsc.GSC_EINVAL
+    assert fwd(0, 0, 27) == gsc.GSC_EINVAL
+    assert fwd(0, 4, 0) == gsc.GSC_EINVAL
+    assert fwd(0, 4, 5000) == gsc.GSC_EINVAL
+    assert fwd(0, 4, 27, -1) == gsc.GSC_EINVAL
+    sel = (ctypes.c_int32 * 2)(0, 2)   # 2 is out of range for K = 2
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, 10,
+                               sel, fake, None, 10, None, 0, None)
+    assert rc == gsc.GSC_EINVAL and "t_wsel" in _err(L)
+    sel = (ctypes.c_int32 * 2)(0, 1)
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, 10,
+                               sel, None, ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)), 10, fake, 8, None)
+    assert rc == gsc.GSC_ESHORT
+
+
+@pytest.mark.parametrize("name,K,D", [("cube", 3, 3), ("cube", 2, 3), ("cube", 5, 4), ("cross", 5, 3),
+                                      ("hybrid", 3, 4), ("cube", 3, 7)])
+def test_regions_match_oracle(name, K, D):
+    assert np.array_equal(regions.region(name, K, D), O.region(name, K, D))
+
+
+def test_negation_permutation():
+    offs = regions.hypercube(3, 3)
+    p = gsc.negation_permutation(offs)
+    assert np.array_equal(offs[p], -offs)
+    assert regions.is_symmetric(regions.hybrid(3, 4))
+    assert not regions.is_symmetric(regions.hypercube(2, 3))

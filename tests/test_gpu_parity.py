@@ -1,0 +1,266 @@
+"""Parity of the HIP path (through the C-ABI) with the CPU oracle.
+
+Kernel maps and output coordinates must match bit-exactly (after canonical
+alignment of strided output rows); features and gradients within the max
+relative error 1e-5 (fp32) or 2e-2 (bf16 inputs, fp32 accumulation).
+
+* all five workloads at full size, through the same pipeline the benchmark
+  times;
+* the same workloads shrunk (scale 0.3: several tiles and ragged tails, the
+  oracle finishes in seconds);
+* edge cases: empty input, one voxel, duplicates, key range, short buffers,
+  negative coordinates over several batches, non-symmetric and large regions,
+  tensor stride, odd channel counts, the centre-only identity kernel.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.gsc_oracle as O
+from paper_1904_08755_amd import gsc, pipeline, regions
+from paper_1904_08755_amd import workloads as WL
+from parity import TOL, check_gidx, compare_step, gpu_pairs, maps_equal_exact, oracle_step, rel_err, to_np
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gsc.lib()
+
+
+def _run(wl):
+    _say(f"[gpu] {wl.name} n={wl.n}")
+    dw = pipeline.to_device(wl, DEV)
+    step = pipeline.run_step(dw)
+    torch.cuda.synchronize()
+    return step
+
+
+@pytest.mark.parametrize("cid", [0, 1, 2, 3, 4])
+def test_workload_small(cid):
+    wl = WL.make_workload(cid, scale=0.3)
+    step = _run(wl)
+    errs = compare_step(wl, step, oracle_step(wl))
+    _say(f"  errors {errs}")
+
+
+@pytest.mark.parametrize("cid", [0, 1, 2, 3, 4])
+def test_workload_full(cid):
+    wl = WL.make_workload(cid)
+    step = _run(wl)
+    ref = oracle_step(wl)
+    errs = compare_step(wl, step, ref)
+    npairs = [km.n_pairs for km in step.kmaps]
+    _say(f"  pairs {npairs} errors {errs}")
+
+
+def test_map_symmetry_on_gpu():
+    wl = WL.make_workload(1, scale=0.3)
+    dw = pipeline.to_device(wl, DEV)
+    table = gsc.gsc_coords_build(dw.coords)
+    offs = regions.hypercube(3, 3)
+    pairs = gpu_pairs(gsc.gsc_kernel_map(table, dw.coords, offs))
+    neg = gsc.negation_permutation(offs)
+    for k in range(len(offs)):
+        a = set(zip(pairs[k][0].tolist(), pairs[k][1].tolist()))
+        b = set(zip(pairs[neg[k]][1].tolist(), pairs[neg[k]][0].tolist()))
+        assert a == b
+    centre = int(np.where((offs == 0).all(1))[0][0])
+    assert np.array_equal(pairs[centre][0], np.arange(wl.n))
+
+
+# --------------------------------------------------------------------------- #
+# edge cases
+# --------------------------------------------------------------------------- #
+def _t(a, dtype=torch.int32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV).to(dtype)
+
+
+def _conv_case(coords, ci, co, offs, seed, dtype="f32", ts=1):
+    """Submanifold conv fwd + bwd on explicit coordinates vs the oracle.  Uses
+    the explicitly built role-reversed map for dX (works for any region)."""
+    c = _t(coords)
+    X, Xb = WL.random_features(seed, len(coords), ci, dtype)
+    W, Wb = WL.random_weights(seed, len(offs), ci, co, dtype)
+    G, Gb = WL.random_features(seed + 1, len(coords), co, dtype)
+    if dtype == "bf16":
+        tX = torch.from_numpy(Xb.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tW = torch.from_numpy(Wb.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tG = torch.from_numpy(Gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    else:
+        tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
+    table = gsc.gsc_coords_build(c)
+    km = gsc.gsc_kernel_map(table, c, offs, tensor_stride=ts)
+    tm = gsc.transposed_kernel_map(table, c, offs, tensor_stride=ts)
+    Y = gsc.gsc_sparse_conv_fwd(tX, tW, km)
+    dX, dW = gsc.gsc_sparse_conv_bwd(tX, tW, tG, km, tm, np.arange(len(offs)))
+    torch.cuda.synchronize()
+    m = O.kernel_map(coords, coords, np.asarray(offs), ts)
+    maps_equal_exact(gpu_pairs(km), m)
+    check_gidx(km)
+    maps_equal_exact(gpu_pairs(tm), O.transposed_map(m))
+    Yr = O.conv_forward(X, W, m, len(coords))
+    dXr, dWr = O.conv_backward(X, W, G, m)
+    tol = TOL[dtype]
+    assert rel_err(to_np(Y), Yr) <= tol
+    assert rel_err(to_np(dX), dXr) <= tol
+    assert rel_err(to_np(dW), dWr) <= tol
+    return km
+
+
+def test_empty_input():
+    c = torch.empty((0, 4), dtype=torch.int32, device=DEV)
+    table = gsc.gsc_coords_build(c)
+    km = gsc.gsc_kernel_map(table, c, regions.hypercube(3, 3))
+    assert km.n_pairs == 0
+    out, _ = gsc.gsc_coords_stride(c, 2)
+    assert out.shape[0] == 0
+    X = torch.empty((0, 8), device=DEV)
+    W = torch.randn((27, 8, 4), device=DEV)
+    Y = gsc.gsc_sparse_conv_fwd(X, W, km)
+    assert Y.shape == (0, 4)
+    dX, dW = gsc.gsc_sparse_conv_bwd(X, W, torch.empty((0, 4), device=DEV), km, km, np.arange(27))
+    torch.cuda.synchronize()
+    assert dX.shape == (0, 8)
+    assert torch.count_nonzero(dW).item() == 0
+
+
+def test_empty_output_rows_are_zero():
+    # outputs that no input reaches: query a table of far-away inputs
+    cin = np.array([[0, 100, 100, 100], [0, 101, 100, 100]], np.int32)
+    cout = np.array([[0, 0, 0, 0], [0, 1, 1, 1], [0, 100, 100, 99]], np.int32)
+    table = gsc.gsc_coords_build(_t(cin))
+    km = gsc.gsc_kernel_map(table, _t(cout), regions.hypercube(3, 3))
+    X = torch.randn((2, 5), device=DEV)
+    W = torch.randn((27, 5, 3), device=DEV)
+    Y = gsc.gsc_sparse_conv_fwd(X, W, km)
+    torch.cuda.synchronize()
+    ref = O.conv_forward(X.cpu().numpy(), W.cpu().numpy(), O.kernel_map(cin, cout, O.hypercube(3, 3)), 3)
+    assert np.all(to_np(Y)[:2] == 0)
+    assert rel_err(to_np(Y), ref) <= 1e-5
+
+
+def test_single_voxel():
+    _conv_case(np.array([[0, -7, 3, 11]], np.int32), 4, 6, regions.hypercube(3, 3), 51)
+
+
+def test_duplicate_rejected():
+    c = _t(np.array([[0, 1, 2, 3], [0, 4, 5, 6], [0, 1, 2, 3]], np.int32))
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_coords_build(c)
+    assert e.value.code == gsc.GSC_EDUP
+
+
+def test_key_range_rejected():
+    # 8 columns each spanning 2^9 values need 72 key bits
+    rows = np.zeros((2, 8), np.int32)
+    rows[1, 1:] = 511
+    rows[1, 0] = 511
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_coords_build(_t(rows))
+    assert e.value.code == gsc.GSC_ERANGE
+
+
+def test_kernel_map_short_then_retry():
+    coords = WL.random_coords(61, 3000, 3, -20, 20, batch=2)
+    c = _t(coords)
+    table = gsc.gsc_coords_build(c)
+    offs = regions.hypercube(3, 3)
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_kernel_map(table, c, offs, cap_pairs=10)
+    assert e.value.code == gsc.GSC_ESHORT
+    ref = O.kernel_map(coords, coords, O.hypercube(3, 3))
+    km = gsc.gsc_kernel_map(table, c, offs, cap_pairs=O.map_pair_count(ref))
+    maps_equal_exact(gpu_pairs(km), ref)
+
+
+def test_negative_coords_many_batches_cube():
+    coords = WL.random_coords(71, 5000, 3, -30, 10, batch=5)
+    _conv_case(coords, 16, 32, regions.hypercube(3, 3), 71)
+
+
+def test_nonsymmetric_region_and_ragged_channels():
+    coords = WL.random_coords(72, 4000, 3, -12, 12, batch=2)
+    _conv_case(coords, 3, 70, regions.hypercube(2, 3), 72)   # 70 > 64: two column slices
+
+
+def test_large_region_cube5_and_cross():
+    coords = WL.random_coords(73, 2500, 3, -10, 10, batch=2)
+    _conv_case(coords, 8, 8, regions.hypercube(5, 3), 73)
+    _conv_case(coords, 5, 12, regions.hypercross(5, 3), 74)
+
+
+def test_tensor_stride_two():
+    coords = WL.random_coords(75, 3000, 3, -10, 10, batch=2)
+    coords[:, 1:] *= 2
+    _conv_case(coords, 8, 16, regions.hypercube(3, 3), 75, ts=2)
+
+
+def test_bf16_odd_channels():
+    coords = WL.random_coords(76, 3000, 3, -15, 15, batch=2)
+    _conv_case(coords, 24, 40, regions.hypercube(3, 3), 76, dtype="bf16")
+
+
+def test_4d_hybrid_and_tesseract():
+    coords = WL.random_coords(77, 3000, 4, -5, 5, batch=1)
+    _conv_case(coords, 8, 8, regions.hybrid(3, 4), 77)
+    _conv_case(coords, 8, 8, regions.hypercube(3, 4), 78)
+
+
+def test_centre_only_identity_exact():
+    coords = WL.random_coords(79, 1000, 3, -20, 20, batch=2)
+    c = _t(coords)
+    table = gsc.gsc_coords_build(c)
+    km = gsc.gsc_kernel_map(table, c, np.zeros((1, 3), np.int32))
+    X = torch.randn((len(coords), 32), device=DEV)
+    Y = gsc.gsc_sparse_conv_fwd(X, torch.eye(32, device=DEV)[None].contiguous(), km)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, X)
+
+
+def test_stride_coords_floor_and_order():
+    coords = WL.random_coords(81, 4000, 3, -9, 9, batch=3)
+    out, out_table = gsc.gsc_coords_stride(_t(coords), 2)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = O.output_coordinates(coords, 2)
+    assert {tuple(r) for r in got.tolist()} == {tuple(r) for r in ref.tolist()}
+    assert len(got) == len(ref)
+    # deterministic order: first input row producing each output
+    first = {}
+    for r, row in enumerate(coords.tolist()):
+        key = (row[0],) + tuple((v // 2) * 2 for v in row[1:])
+        first.setdefault(key, r)
+    assert [first[tuple(r)] for r in got.tolist()] == sorted(first.values())
+    # the output table answers queries for the output coordinates
+    km = gsc.gsc_kernel_map(out_table, out, np.zeros((1, 3), np.int32))
+    assert np.array_equal(gpu_pairs(km)[0][0], np.arange(len(got)))
+
+
+def test_stride_then_second_level():
+    coords = WL.random_coords(82, 6000, 3, -17, 17, batch=2)
+    c = _t(coords)
+    o1, t1 = gsc.gsc_coords_stride(c, 2)
+    o2, t2 = gsc.gsc_coords_stride(o1, 4)
+    torch.cuda.synchronize()
+    r1 = O.output_coordinates(coords, 2)
+    r2 = O.output_coordinates(r1, 4)
+    assert {tuple(r) for r in o2.cpu().numpy().tolist()} == {tuple(r) for r in r2.tolist()}
+    # stride-4 level map from the stride-2 level: tensor stride 2, size-2 kernel
+    km = gsc.gsc_kernel_map(t1, o2, regions.hypercube(2, 3), tensor_stride=2)
+    g1, g2 = o1.cpu().numpy(), o2.cpu().numpy()
+    from parity import row_perm
+    p1, p2 = row_perm(g1, r1), row_perm(g2, r2)
+    ref = O.kernel_map(r1, r2, O.hypercube(2, 3), 2)
+    maps_equal_exact(gpu_pairs(km), ref, out_perm=p2, in_perm=p1)
