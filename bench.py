@@ -105,13 +105,16 @@ def main():
     dw = pipeline.to_device(wl, "cuda")
     torch.cuda.synchronize()
 
+    plan0 = pipeline.StepPlan(dw)
     for _ in range(args.warmup):
-        pipeline.run_step(dw)
+        plan0.run()
+    gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
+    del plan0
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
     steps_events = []
-    last = None
+    plan = pipeline.StepPlan(dw)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -123,7 +126,7 @@ def main():
             ev.append((name, e))
 
         mark("start")
-        last = pipeline.run_step(dw, mark)
+        last = plan.run(mark)
         steps_events.append(ev)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -140,13 +143,13 @@ def main():
 
     L0 = wl.layers[0]
     s = 2 if wl.dtype == "bf16" else 4
-    pairs = [km.n_pairs for km in last.kmaps]
-    flops = sum(6.0 * km.n_pairs * L.c_in * L.c_out for km, L in zip(last.kmaps, wl.layers))
+    pairs = [km.count() for km in last.kmaps]
+    flops = sum(6.0 * m * L.c_in * L.c_out for m, L in zip(pairs, wl.layers))
     conv_s = (ms["fwd"] + ms["bwd"]) * 1e-3
     km0 = last.kmaps[0]
     n_out0 = km0.n_out
     # dominant kernel: the forward gather -> MFMA -> LDS-accumulate of layer 0
-    dom_bytes = fwd_bytes(km0.n_pairs, n_out0, L0.c_in, L0.c_out, km0.K, s)
+    dom_bytes = fwd_bytes(pairs[0], n_out0, L0.c_in, L0.c_out, km0.K, s)
     dom_ms = ms["fwd"] if len(wl.layers) == 1 else None
     roof = None
     if dom_ms:

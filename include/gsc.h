@@ -70,10 +70,12 @@ int gsc_abi_version(void);
 /* a1. Coordinate hash table (Sec. 3; hash-table neighbour search, Sec. 2).  */
 /* ------------------------------------------------------------------------ */
 /* Bytes of a table for n coordinates: a 256-byte header (key packing,
- * bounding box, status) followed by a power-of-two number (>= 2n, >= 64) of
+ * bounding box, status) followed by a power-of-two number (>= 4n, >= 64) of
  * 16-byte slots {uint64 key, int32 row, int32 pad}.  Open addressing with
  * linear probing; the key is the row packed into <= 62 bits relative to the
- * bounding box of the coordinates (batch column most significant). */
+ * bounding box of the coordinates (batch column most significant).  The home
+ * slot keeps each 2 x 2 x 2 block of neighbouring coordinates in one 128-byte
+ * line of slots, so a neighbourhood query touches few lines. */
 size_t gsc_table_bytes(int64_t n);
 
 /* Build the table of `coords` (device, n x (1+D) int32) into `table` (device,
@@ -84,6 +86,19 @@ size_t gsc_table_bytes(int64_t n);
  * empty table. */
 int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D,
                      void* table, size_t table_bytes, void* stream);
+
+/* gsc_coords_build without the synchronisation: the build is only enqueued
+ * and device-detected errors (EDUP, EFULL, ERANGE) are left in the table
+ * header, where gsc_table_status reads them.  A kernel map queried from a
+ * table whose build failed comes out empty.  Host-side errors (EINVAL,
+ * ESHORT) are returned at once. */
+int gsc_coords_build_async(const int32_t* coords, int64_t n, int32_t D,
+                           void* table, size_t table_bytes, void* stream);
+
+/* Synchronise `stream` and return the status the build left in `table`:
+ * GSC_OK, GSC_EDUP, GSC_EFULL or GSC_ERANGE (GSC_EINVAL if `table` was never
+ * built). */
+int gsc_table_status(const void* table, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* a2. Output coordinates of a strided convolution (Sec. 4.2).              */
@@ -129,6 +144,13 @@ size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D);
  * *n_pairs (host) receives the total.  If it exceeds cap_pairs, nothing is
  * written to in_idx/out_idx and ESHORT is returned with *n_pairs set, so the
  * caller can allocate and call again.  Synchronises `stream` once.
+ *
+ * Asynchronous mode: with n_pairs == NULL the call only enqueues work and
+ * never synchronises.  Then cap_pairs must be at least K * n_out (so no map
+ * can overflow), K * D must be at most 768, and the total is available on the
+ * device only (seg[K] = gidx[K*G]).  The convolution calls need no host pair
+ * count (they take an upper bound), so a whole layer can be enqueued without
+ * a round trip to the host.
  *
  * The transposed convolution's map (roles of input and output reversed,
  * Sec. 4.2) is this function applied to the table of the original output

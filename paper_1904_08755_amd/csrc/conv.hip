@@ -74,7 +74,8 @@ k_conv_os(const TIn* __restrict__ X, int64_t n_x, const TIn* __restrict__ W, con
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int r16 = lane & 15, q = lane >> 4;
-    const int64_t row0 = (int64_t)blockIdx.x * kTileRows;
+    const int64_t tile = xcd_unit(blockIdx.x, gridDim.x);
+    const int64_t row0 = tile * kTileRows;
     const int col0 = blockIdx.y * kColSlice;
     const int ncols = min(kColSlice, cb - col0);
     const int nnb = (ncols + 15) >> 4;
@@ -82,7 +83,7 @@ k_conv_os(const TIn* __restrict__ X, int64_t n_x, const TIn* __restrict__ W, con
     for (int i = tid; i < kTileRows * kAccStride; i += kThreads) acc[i] = 0.f;
     __syncthreads();
 
-    const int64_t g0 = (int64_t)blockIdx.x * kTileGroups;
+    const int64_t g0 = tile * kTileGroups;
     const int64_t g1 = min(g0 + kTileGroups, G);
     int item = 0;
     for (int k = 0; k < K; ++k) {
@@ -163,43 +164,275 @@ k_conv_os(const TIn* __restrict__ X, int64_t n_x, const TIn* __restrict__ W, con
 }
 
 // ---------------------------------------------------------------------------
+// fp32 specialisation for reduction width CA and output width CB (multiples of
+// 16, <= 64).  Differences from the generic kernel:
+//   * the (offset, 16-pair group) items of a tile are split into four
+//     contiguous ranges, one per wave, so a wave meets few distinct offsets and
+//     keeps the offset's B fragments (CA/4 x CB/16 floats per lane) in
+//     registers across its groups;
+//   * lane (r16, q) gathers channels [q*CA/4, (q+1)*CA/4) of pair r16's row with
+//     16-byte loads; MFMA step s then reduces over channels {q*CA/4 + s}, and B
+//     uses the same channel permutation;
+//   * the next group's row gather is issued before the current group's MFMAs.
+// ---------------------------------------------------------------------------
+template <int CA>
+struct RowFrag {
+    float v[CA / 4];
+};
+
+// Branch-free row fragment load: the address is always valid (row is
+// clamped by the caller) and invalid pairs are zeroed with a select, so the
+// loads of a batch are issued back to back with no wait between them.
+template <int CA>
+__device__ __forceinline__ void load_row_frag(const float* __restrict__ X, int64_t row, int q, bool ok,
+                                              RowFrag<CA>& a) {
+    constexpr int KS = CA / 4;
+    const float4* src = reinterpret_cast<const float4*>(X + row * CA + q * KS);
+#pragma unroll
+    for (int i = 0; i < KS / 4; ++i) {
+        const float4 t = src[i];
+        a.v[4 * i + 0] = ok ? t.x : 0.f;
+        a.v[4 * i + 1] = ok ? t.y : 0.f;
+        a.v[4 * i + 2] = ok ? t.z : 0.f;
+        a.v[4 * i + 3] = ok ? t.w : 0.f;
+    }
+}
+
+constexpr int kMaxKLds = 256;   // offsets whose tile table fits in LDS (specialised kernels)
+constexpr int kItemBatch = 4;   // items per wave in flight
+
+// Per-tile offset table in LDS: pairs of offset k in this tile start at
+// s_lo[k] (global pair index), there are s_np[k] of them, and its 16-pair
+// items are numbered from s_ib[k]; s_ib[K] = items of the tile.
+struct TileTable {
+    int64_t lo[kMaxKLds];
+    int32_t np[kMaxKLds];
+    int32_t ib[kMaxKLds + 1];
+};
+
+__device__ __forceinline__ void build_tile_table(TileTable& t, const int64_t* __restrict__ gidx, int K, int64_t G,
+                                                 int64_t g0, int64_t g1) {
+    for (int k = threadIdx.x; k < K; k += kThreads) {
+        const int64_t lo = gidx[(int64_t)k * G + g0];
+        t.lo[k] = lo;
+        t.np[k] = (int32_t)(gidx[(int64_t)k * G + g1] - lo);
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {   // wave 0: exclusive scan of item counts
+        int carry = 0;
+        for (int k0 = 0; k0 < K; k0 += 64) {
+            const int k = k0 + threadIdx.x;
+            const int v = k < K ? (t.np[k] + 15) >> 4 : 0;
+            int inc = v;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int u = __shfl_up(inc, d, 64);
+                if ((int)threadIdx.x >= d) inc += u;
+            }
+            if (k < K) t.ib[k] = carry + inc - v;
+            carry += __shfl(inc, 63, 64);
+        }
+        if (threadIdx.x == 0) t.ib[K] = carry;
+    }
+    __syncthreads();
+}
+
+// Wave-per-group fp32 kernel.  Each wave owns one 64-row group of output
+// rows (the kernel map's group granularity) and accumulates it in a private
+// LDS region with plain read-modify-write: no LDS atomics, no workgroup
+// barriers, deterministic order.  The wave's per-offset table (first pair,
+// pair count, first item) is held one offset per lane (K <= 64).
+constexpr int kWaveKMax = 64;
+
+template <int CA, int CB, bool WT, typename Sel>
+__global__ void __launch_bounds__(kThreads)
+k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, const int32_t* __restrict__ gat,
+           const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx, int K, int64_t G, int64_t n_y,
+           float* __restrict__ Y, Sel sel) {
+    constexpr int KS = CA / 4;
+    constexpr int NNB = CB / 16;
+    constexpr int AS = CB + 1;
+    constexpr int RG = GSC_GROUP_ROWS;
+    constexpr int B = CA * CB <= 1024 ? kItemBatch : kItemBatch / 2;   // bound the register footprint
+    __shared__ float acc_all[kThreads / 64][RG * AS];
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int r16 = lane & 15, q = lane >> 4;
+    const int64_t g = xcd_unit(blockIdx.x, gridDim.x) * (kThreads / 64) + wave;
+    if (g >= G) return;                        // no barrier below, so a wave may leave early
+    float* acc = acc_all[wave];
+    const int64_t row0 = g * RG;
+    for (int i = lane; i < RG * AS; i += 64) acc[i] = 0.f;
+
+    // per-offset table, one offset per lane
+    int64_t lo = 0;
+    int np = 0;
+    if (lane < K) {
+        lo = gidx[(int64_t)lane * G + g];
+        np = (int)(gidx[(int64_t)lane * G + g + 1] - lo);
+    }
+    const int nit = (np + 15) >> 4;
+    int incl = nit;                            // inclusive scan of items over lanes
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int u = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += u;
+    }
+    const int excl = incl - nit;
+    const int total = __shfl(incl, 63, 64);
+
+    for (int item0 = 0; item0 < total; item0 += B) {
+        // 1. pair indices of the batch; every address is valid (lanes past the
+        //    end of a group re-read its last pair, items past the end repeat
+        //    the last item) and the invalid ones are masked later
+        int kb[B];
+        int32_t gr[B], sr[B];
+        bool ok[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int item = min(item0 + b, total - 1);
+            const int k = __popcll(__ballot(incl <= item));     // offset of the item
+            kb[b] = k;
+            const int64_t klo = __shfl(lo, k, 64);
+            const int knp = __shfl(np, k, 64);
+            const int pb = (item - __shfl(excl, k, 64)) * 16 + r16;
+            const int64_t p = klo + min(pb, knp - 1);
+            gr[b] = gat[p];
+            sr[b] = sca[p];
+            ok[b] = item0 + b < total && pb < knp;
+        }
+        // 2. rows and weights of the whole batch
+        RowFrag<CA> a[B];
+        float bfr[B][KS][NNB];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            ok[b] = ok[b] && gr[b] >= 0 && gr[b] < n_x && sr[b] >= row0 && sr[b] < row0 + RG;
+            load_row_frag<CA>(X, ok[b] ? gr[b] : 0, q, ok[b], a[b]);
+            const int w = sel(kb[b]);
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int nb = 0; nb < NNB; ++nb) {
+                    const int brow = q * KS + s, col = nb * 16 + r16;
+                    bfr[b][s][nb] = WT ? W[((int64_t)w * CB + col) * CA + brow] : W[((int64_t)w * CA + brow) * CB + col];
+                }
+        }
+        // 3. group row of each MFMA output row (pair row 4q + j), -1 if none
+        int lrow[B][4];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int mine = ok[b] ? (int)(sr[b] - row0) : -1;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) lrow[b][j] = __shfl(mine, 4 * q + j, 64);
+        }
+        // 4. MFMA, then add the 16 result rows into the wave's rows (distinct
+        //    within an item; items of the wave are applied in order)
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            floatx4 d[NNB];
+#pragma unroll
+            for (int nb = 0; nb < NNB; ++nb) d[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int nb = 0; nb < NNB; ++nb)
+                    d[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[b].v[s], bfr[b][s][nb], d[nb], 0, 0, 0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (lrow[b][j] >= 0) {
+                    float* arow = acc + lrow[b][j] * AS;
+#pragma unroll
+                    for (int nb = 0; nb < NNB; ++nb) arow[nb * 16 + r16] += d[nb][j];
+                }
+            }
+        }
+    }
+    // 5. the group's rows, written once
+    for (int i = lane; i < RG * CB; i += 64) {
+        const int r = i / CB, cc = i - r * CB;
+        const int64_t row = row0 + r;
+        if (row < n_y) Y[row * CB + cc] = acc[r * AS + cc];
+    }
+}
+
+// ---------------------------------------------------------------------------
 // weight gradient
 // ---------------------------------------------------------------------------
-// item bases: ibase[k] = sum over k' < k of ceil(|M_k'| / CH); ibase[K] = total
-__global__ void k_dw_items(const int64_t* seg, int K, int64_t CH, int64_t* ibase) {
+// Work items of the weight gradient.  Offset k's pairs are split into
+// nch_k = min(cap, ceil(|M_k| / min_chunk)) chunks of chunk[k] pairs (a
+// multiple of 64); ibase[k] = first item of offset k, ibase[K] = total.
+// Capping the chunks per offset keeps the second-level reduction short.
+__global__ void k_dw_items(const int64_t* seg, int K, int cap, int64_t min_chunk, int64_t* ibase, int64_t* chunk) {
     if (blockIdx.x != 0 || threadIdx.x != 0) return;
     int64_t t = 0;
     for (int k = 0; k < K; ++k) {
-        ibase[k] = t;
         const int64_t n = seg[k + 1] - seg[k];
-        t += n > 0 ? (n + CH - 1) / CH : 0;
+        int64_t nch = n > 0 ? (n + min_chunk - 1) / min_chunk : 0;
+        if (nch > cap) nch = cap;
+        int64_t ch = nch > 0 ? (n + nch - 1) / nch : 0;
+        ch = (ch + 63) & ~(int64_t)63;
+        ibase[k] = t;
+        chunk[k] = ch;
+        t += nch;
     }
     ibase[K] = t;
 }
 
-template <typename TIn>
-__global__ void __launch_bounds__(kThreads)
-k_dw_partial(const TIn* __restrict__ X, int64_t n_in, const TIn* __restrict__ dY, int64_t n_out,
-             const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx, const int64_t* __restrict__ seg,
-             const int64_t* __restrict__ ibase, int K, int64_t CH, int ci, int co, float* __restrict__ part) {
-    __shared__ float acc[kDwTile * (kDwTile + 1)];
-    const int64_t item = blockIdx.x;
-    if (item >= ibase[K]) return;
+// offset and pair range of a work item
+__device__ __forceinline__ bool dw_item(const int64_t* ibase, const int64_t* chunk, const int64_t* seg, int K,
+                                        int64_t item, int* k_out, int64_t* p_begin, int64_t* p_end) {
+    if (item >= ibase[K]) return false;
     int lo = 0, hi = K - 1;   // last k with ibase[k] <= item
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if (ibase[mid] <= item) lo = mid; else hi = mid - 1;
     }
-    const int k = lo;
-    const int64_t p_begin = seg[k] + (item - ibase[k]) * CH;
-    const int64_t p_end = min(seg[k + 1], p_begin + CH);
+    *k_out = lo;
+    *p_begin = seg[lo] + (item - ibase[lo]) * chunk[lo];
+    *p_end = min(seg[lo + 1], *p_begin + chunk[lo]);
+    return true;
+}
+
+// Per-wave partial tiles are summed in wave order (deterministic), then stored.
+template <int R, int C>
+__device__ __forceinline__ void dw_store_partial(float* sh, const floatx4 (&d)[4][4], int na, int nbk, int wave,
+                                                 int q, int r16, int rows, int cols, float* __restrict__ out,
+                                                 int64_t ld) {
+    constexpr int S = C + 1;
+    float* mine = sh + wave * R * S;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            if (a < na && b < nbk)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) mine[(16 * a + 4 * q + j) * S + 16 * b + r16] = d[a][b][j];
+    __syncthreads();
+    for (int i = threadIdx.x; i < rows * cols; i += kThreads) {
+        const int r = i / cols, c = i - r * cols;
+        float v = sh[r * S + c];
+        for (int w = 1; w < kThreads / 64; ++w) v += sh[w * R * S + r * S + c];
+        out[r * ld + c] = v;
+    }
+}
+
+// Generic weight-gradient partial (any dtype, any width): a 64 x 64 tile of
+// X[in]^T dY[out] over one chunk of one offset's pairs.
+template <typename TIn>
+__global__ void __launch_bounds__(kThreads)
+k_dw_partial(const TIn* __restrict__ X, int64_t n_in, const TIn* __restrict__ dY, int64_t n_out,
+             const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx, const int64_t* __restrict__ seg,
+             const int64_t* __restrict__ ibase, const int64_t* __restrict__ chunk, int K, int ci, int co,
+             float* __restrict__ part) {
+    __shared__ float sh[4 * kDwTile * (kDwTile + 1)];
+    int k;
+    int64_t p_begin, p_end;
+    const int64_t item = xcd_unit(blockIdx.x, gridDim.x);
+    if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
     const int ntj = (co + kDwTile - 1) / kDwTile;
     const int ci0 = (blockIdx.y / ntj) * kDwTile, co0 = (blockIdx.y % ntj) * kDwTile;
     const int na = (min(kDwTile, ci - ci0) + 15) >> 4, nbk = (min(kDwTile, co - co0) + 15) >> 4;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, q = lane >> 4;
-
-    for (int i = tid; i < kDwTile * (kDwTile + 1); i += kThreads) acc[i] = 0.f;
-    __syncthreads();
 
     floatx4 d[4][4];
 #pragma unroll
@@ -267,44 +500,120 @@ k_dw_partial(const TIn* __restrict__ X, int64_t n_in, const TIn* __restrict__ dY
         }
     }
     // D[m][n]: m = 4q + j (input channel), n = r16 (output channel)
+    const int rows = min(kDwTile, ci - ci0), cols = min(kDwTile, co - co0);
+    dw_store_partial<kDwTile, kDwTile>(sh, d, na, nbk, wave, q, r16, rows, cols,
+                                       part + (item * ci + ci0) * (int64_t)co + co0, co);
+}
+
+// fp32 weight gradient for CI x CO <= 64 x 64 (multiples of 16).  Each wave
+// takes 64 consecutive pairs at a time: the 64 index pairs are read with one
+// coalesced load per lane and redistributed with shuffles, then all 16 MFMA
+// steps' row fragments are loaded before the MFMAs run.
+template <int CI, int CO>
+__global__ void __launch_bounds__(kThreads)
+k_dw_f32(const float* __restrict__ X, int64_t n_in, const float* __restrict__ dY, int64_t n_out,
+         const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx, const int64_t* __restrict__ seg,
+         const int64_t* __restrict__ ibase, const int64_t* __restrict__ chunk, int K, float* __restrict__ part) {
+    constexpr int NA = CI / 16, NB = CO / 16;
+    __shared__ float sh[4 * CI * (CO + 1)];
+    int k;
+    int64_t p_begin, p_end;
+    const int64_t item = xcd_unit(blockIdx.x, gridDim.x);
+    if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, q = lane >> 4;
+    floatx4 d[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-            if (a < na && b < nbk)
+        for (int b = 0; b < 4; ++b) d[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t p0 = p_begin + 64 * wave; p0 < p_end; p0 += 256) {
+        const int64_t p = p0 + lane;
+        int32_t g = p < p_end ? in_idx[p] : -1;
+        int32_t s = p < p_end ? out_idx[p] : -1;
+        if (g < 0 || g >= n_in || s < 0 || s >= n_out) g = s = -1;
+        float xa[16][NA], yb[16][NB];
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    atomicAdd(&acc[(16 * a + 4 * q + j) * (kDwTile + 1) + 16 * b + r16], d[a][b][j]);
-    __syncthreads();
-    const int rows = min(kDwTile, ci - ci0), cols = min(kDwTile, co - co0);
-    for (int i = tid; i < rows * cols; i += kThreads) {
-        const int r = i / cols, c = i - r * cols;
-        part[(item * ci + ci0 + r) * (int64_t)co + co0 + c] = acc[r * (kDwTile + 1) + c];
+        for (int t = 0; t < 16; ++t) {
+            const int32_t gg = __shfl(g, 4 * t + q, 64);
+            const int32_t ss = __shfl(s, 4 * t + q, 64);
+#pragma unroll
+            for (int a = 0; a < NA; ++a) xa[t][a] = gg >= 0 ? X[(int64_t)gg * CI + 16 * a + r16] : 0.f;
+#pragma unroll
+            for (int b = 0; b < NB; ++b) yb[t][b] = ss >= 0 ? dY[(int64_t)ss * CO + 16 * b + r16] : 0.f;
+        }
+#pragma unroll
+        for (int t = 0; t < 16; ++t)
+#pragma unroll
+            for (int a = 0; a < NA; ++a)
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[t][a], yb[t][b], d[a][b], 0, 0, 0);
     }
+    dw_store_partial<CI, CO>(sh, d, NA, NB, wave, q, r16, CI, CO, part + item * CI * (int64_t)CO, CO);
 }
 
+// dW[k] = sum of offset k's partials in item order.  A block covers 64
+// elements of one offset; its four waves add every fourth partial, then the
+// four sums are combined in wave order.
 __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict__ part, const int64_t* __restrict__ ibase,
                                                         int ci, int co, float* __restrict__ dW) {
+    __shared__ float sh[4][64];
     const int k = blockIdx.y;
-    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t cc = (int64_t)ci * co;
-    if (e >= cc) return;
-    float s = 0.f;
-    for (int64_t it = ibase[k]; it < ibase[k + 1]; ++it) s += part[it * cc + e];
-    dW[(int64_t)k * cc + e] = s;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t i0 = ibase[k], i1 = ibase[k + 1];
+    float v = 0.f;
+    if (e < cc)
+        for (int64_t it = i0 + wave; it < i1; it += 4) v += part[it * cc + e];
+    sh[wave][lane] = v;
+    __syncthreads();
+    if (wave == 0 && e < cc) dW[(int64_t)k * cc + e] = ((sh[0][lane] + sh[1][lane]) + sh[2][lane]) + sh[3][lane];
 }
 
-// chunk of pairs per dW work item: about 1024 work items in total
-static int64_t dw_chunk(int64_t n_pairs, int ci, int co) {
-    const int64_t tiles = (int64_t)((ci + kDwTile - 1) / kDwTile) * ((co + kDwTile - 1) / kDwTile);
-    int64_t ch = 256;
-    while (ch < (int64_t)1 << 16 && (n_pairs * tiles) / ch > 1024) ch <<= 1;
-    return ch;
+static int dw_tiles(int ci, int co) { return ((ci + kDwTile - 1) / kDwTile) * ((co + kDwTile - 1) / kDwTile); }
+
+// chunks per offset: enough items to fill the GPU, few enough partials to add
+static int dw_cap(int ci, int co, int K) {
+    int cap = 2048 / (K * dw_tiles(ci, co));
+    return cap < 2 ? 2 : (cap > 32 ? 32 : cap);
 }
 
-static int64_t dw_items_max(int64_t n_pairs, int32_t K, int64_t ch) { return (n_pairs + ch - 1) / ch + K; }
+constexpr int64_t kDwMinChunk = 256;
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+static bool dw_f32_specialised(int ci, int co) {
+    return (ci == 16 || ci == 32 || ci == 64) && (co == 16 || co == 32 || co == 64);
+}
+
+template <int CA, int CB, bool WT, typename Sel>
+static void launch_f32(const void* X, int64_t n_x, const void* W, const int32_t* gat, const int32_t* sca,
+                       const int64_t* gidx, int K, int64_t G, int64_t tiles, int64_t n_y, void* Y, Sel sel,
+                       hipStream_t s) {
+    (void)tiles;
+    const int64_t blocks = (G + kThreads / 64 - 1) / (kThreads / 64);
+    hipLaunchKernelGGL((k_conv_f32<CA, CB, WT, Sel>), dim3((unsigned)blocks), dim3(kThreads), 0, s,
+                       reinterpret_cast<const float*>(X), n_x, reinterpret_cast<const float*>(W), gat, sca, gidx, K,
+                       G, n_y, reinterpret_cast<float*>(Y), sel);
+}
+
+// fp32 shapes with a specialised kernel
+template <bool WT, typename Sel>
+static bool try_f32(int ca, int cb, const void* X, int64_t n_x, const void* W, const int32_t* gat,
+                    const int32_t* sca, const int64_t* gidx, int K, int64_t G, int64_t tiles, int64_t n_y, void* Y,
+                    Sel sel, hipStream_t s) {
+#define GSC_F32_CASE(A, B)                                                                     \
+    if (ca == A && cb == B) {                                                                  \
+        launch_f32<A, B, WT, Sel>(X, n_x, W, gat, sca, gidx, K, G, tiles, n_y, Y, sel, s);     \
+        return true;                                                                           \
+    }
+    GSC_F32_CASE(16, 16) GSC_F32_CASE(16, 32) GSC_F32_CASE(32, 16) GSC_F32_CASE(32, 32)
+    GSC_F32_CASE(32, 64) GSC_F32_CASE(64, 32) GSC_F32_CASE(64, 64) GSC_F32_CASE(16, 64) GSC_F32_CASE(64, 16)
+#undef GSC_F32_CASE
+    return false;
+}
 
 template <typename TIn, typename TOut, bool WT, typename Sel>
 static int launch_os(const void* X, int64_t n_x, const void* W, const int32_t* gat, const int32_t* sca,
@@ -312,6 +621,12 @@ static int launch_os(const void* X, int64_t n_x, const void* W, const int32_t* g
     if (n_y == 0) return GSC_OK;
     const int64_t tiles = (n_y + kTileRows - 1) / kTileRows;
     const int64_t G = (n_y + GSC_GROUP_ROWS - 1) / GSC_GROUP_ROWS;
+    if constexpr (sizeof(TIn) == 4) {
+        if (K <= kWaveKMax && try_f32<WT, Sel>(ca, cb, X, n_x, W, gat, sca, gidx, K, G, tiles, n_y, Y, sel, s)) {
+            GSC_LAUNCH_CHECK();
+            return GSC_OK;
+        }
+    }
     dim3 grid((unsigned)tiles, (unsigned)((cb + kColSlice - 1) / kColSlice));
     hipLaunchKernelGGL((k_conv_os<TIn, TOut, WT, Sel>), grid, dim3(kThreads), 0, s, reinterpret_cast<const TIn*>(X),
                        n_x, reinterpret_cast<const TIn*>(W), gat, sca, gidx, K, G, ca, cb, n_y,
@@ -349,9 +664,8 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
 
 size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K) {
     if (n_pairs < 0 || c_in < 1 || c_out < 1 || K < 1) return 0;
-    const int64_t ch = dw_chunk(n_pairs, c_in, c_out);
-    return al256((size_t)(K + 1) * sizeof(int64_t)) +
-           al256((size_t)dw_items_max(n_pairs, K, ch) * c_in * c_out * sizeof(float)) + 256;
+    const int64_t items = (int64_t)K * dw_cap(c_in, c_out, K);
+    return 2 * al256((size_t)(K + 1) * sizeof(int64_t)) + al256((size_t)items * c_in * c_out * sizeof(float)) + 256;
 }
 
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in, int32_t c_in,
@@ -392,26 +706,39 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         if (n_pairs > 0 && (!X || !dY || !in_idx || !out_idx)) return fail(GSC_EINVAL, "conv_bwd: null X/dY/idx");
         const size_t need = gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K);
         if (ws_bytes < need) return fail(GSC_ESHORT, "conv_bwd: ws needs %zu bytes, got %zu", need, ws_bytes);
-        const int64_t ch = dw_chunk(n_pairs, c_in, c_out);
-        const int64_t items = dw_items_max(n_pairs, K, ch);
+        const int cap = dw_cap(c_in, c_out, K);
+        const int64_t items = (int64_t)K * cap;
         char* w = reinterpret_cast<char*>(ws);
         int64_t* ibase = reinterpret_cast<int64_t*>(w);
-        float* part = reinterpret_cast<float*>(w + al256((size_t)(K + 1) * sizeof(int64_t)));
-        hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, ch, ibase);
+        int64_t* chunk = reinterpret_cast<int64_t*>(w + al256((size_t)(K + 1) * sizeof(int64_t)));
+        float* part = reinterpret_cast<float*>(w + 2 * al256((size_t)(K + 1) * sizeof(int64_t)));
+        hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, cap, kDwMinChunk, ibase, chunk);
         GSC_LAUNCH_CHECK();
-        const unsigned tiles = (unsigned)(((c_in + kDwTile - 1) / kDwTile) * ((c_out + kDwTile - 1) / kDwTile));
-        if (dtype == GSC_F32)
-            hipLaunchKernelGGL(k_dw_partial<float>, dim3((unsigned)items, tiles), dim3(kThreads), 0, s,
-                               reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(dY), n_out,
-                               in_idx, out_idx, seg, ibase, K, ch, c_in, c_out, part);
-        else
-            hipLaunchKernelGGL(k_dw_partial<uint16_t>, dim3((unsigned)items, tiles), dim3(kThreads), 0, s,
-                               reinterpret_cast<const uint16_t*>(X), n_in, reinterpret_cast<const uint16_t*>(dY),
-                               n_out, in_idx, out_idx, seg, ibase, K, ch, c_in, c_out, part);
+        if (dtype == GSC_F32 && dw_f32_specialised(c_in, c_out)) {
+            auto X32 = reinterpret_cast<const float*>(X);
+            auto dY32 = reinterpret_cast<const float*>(dY);
+#define GSC_DW_CASE(A, B)                                                                              \
+    if (c_in == A && c_out == B)                                                                       \
+        hipLaunchKernelGGL((k_dw_f32<A, B>), dim3((unsigned)items), dim3(kThreads), 0, s, X32, n_in, dY32, \
+                           n_out, in_idx, out_idx, seg, ibase, chunk, K, part);
+            GSC_DW_CASE(16, 16) GSC_DW_CASE(16, 32) GSC_DW_CASE(16, 64) GSC_DW_CASE(32, 16) GSC_DW_CASE(32, 32)
+            GSC_DW_CASE(32, 64) GSC_DW_CASE(64, 16) GSC_DW_CASE(64, 32) GSC_DW_CASE(64, 64)
+#undef GSC_DW_CASE
+        } else {
+            const unsigned tiles = (unsigned)dw_tiles(c_in, c_out);
+            if (dtype == GSC_F32)
+                hipLaunchKernelGGL(k_dw_partial<float>, dim3((unsigned)items, tiles), dim3(kThreads), 0, s,
+                                   reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(dY), n_out,
+                                   in_idx, out_idx, seg, ibase, chunk, K, c_in, c_out, part);
+            else
+                hipLaunchKernelGGL(k_dw_partial<uint16_t>, dim3((unsigned)items, tiles), dim3(kThreads), 0, s,
+                                   reinterpret_cast<const uint16_t*>(X), n_in, reinterpret_cast<const uint16_t*>(dY),
+                                   n_out, in_idx, out_idx, seg, ibase, chunk, K, c_in, c_out, part);
+        }
         GSC_LAUNCH_CHECK();
         const int64_t cc = (int64_t)c_in * c_out;
-        hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)((cc + kThreads - 1) / kThreads), (unsigned)K), dim3(kThreads),
-                           0, s, part, ibase, c_in, c_out, dW);
+        hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)((cc + 63) / 64), (unsigned)K), dim3(kThreads), 0, s, part,
+                           ibase, c_in, c_out, dW);
         GSC_LAUNCH_CHECK();
     }
     return GSC_OK;

@@ -51,37 +51,66 @@ __global__ void __launch_bounds__(kThreads) k_table_init(TableHeader* h, Slot* s
             h->shift[c] = 0;
             h->bits[c] = 0;
         }
+        h->nblk = 0;
+        for (int i = 0; i < 3; ++i) h->blk_shift[i] = 0;
+        for (int c = 0; c < kMaxCols; ++c) h->vary[c] = 0;
     }
 }
 
+// Bounding box of the (optionally strided) rows: per-thread min/max, wave
+// shuffles, then LDS across the block's waves, so the header sees one atomic
+// per column per block.
 __global__ void __launch_bounds__(kThreads) k_bbox(const int32_t* coords, int64_t n, int ncol, StrideArg st,
                                                    TableHeader* h) {
-    int64_t lo[kMaxCols], hi[kMaxCols];
+    __shared__ int sh_lo[kThreads / 64][kMaxCols], sh_hi[kThreads / 64][kMaxCols], sh_or[kThreads / 64][kMaxCols];
+    int64_t lo[kMaxCols], hi[kMaxCols], v0[kMaxCols];
+    int vary[kMaxCols];
     for (int c = 0; c < kMaxCols; ++c) {
         lo[c] = INT_MAX;
         hi[c] = INT_MIN;
+        vary[c] = 0;
     }
+    load_row(coords, 0, ncol, st, v0);   // n > 0 here
+    bool out_of_range = false;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += stride) {
         int64_t v[kMaxCols];
         load_row(coords, r, ncol, st, v);
         for (int c = 0; c < ncol; ++c) {
-            if (v[c] < INT_MIN || v[c] > INT_MAX) atomicOr(&h->status, ST_RANGE);  // strided out of int32
+            out_of_range |= v[c] < INT_MIN || v[c] > INT_MAX;   // strided value left int32
             lo[c] = v[c] < lo[c] ? v[c] : lo[c];
             hi[c] = v[c] > hi[c] ? v[c] : hi[c];
+            vary[c] |= (int)(v[c] ^ v0[c]);
         }
     }
+    if (out_of_range) atomicOr(&h->status, ST_RANGE);
+    const int w = threadIdx.x >> 6;
     for (int c = 0; c < ncol; ++c) {
-        int a = (int)lo[c], b = (int)hi[c];
+        int a = (int)max(lo[c], (int64_t)INT_MIN), b = (int)min(hi[c], (int64_t)INT_MAX), o = vary[c];
         for (int d = 32; d > 0; d >>= 1) {
-            int ta = __shfl_xor(a, d, 64), tb = __shfl_xor(b, d, 64);
+            int ta = __shfl_xor(a, d, 64), tb = __shfl_xor(b, d, 64), to = __shfl_xor(o, d, 64);
             a = ta < a ? ta : a;
             b = tb > b ? tb : b;
+            o |= to;
         }
         if (__lane_id() == 0) {
-            atomicMin(&h->lo[c], a);
-            atomicMax(&h->hi[c], b);
+            sh_lo[w][c] = a;
+            sh_hi[w][c] = b;
+            sh_or[w][c] = o;
         }
+    }
+    __syncthreads();
+    if (threadIdx.x < ncol) {
+        const int c = threadIdx.x;
+        int a = sh_lo[0][c], b = sh_hi[0][c], o = sh_or[0][c];
+        for (int i = 1; i < kThreads / 64; ++i) {
+            a = sh_lo[i][c] < a ? sh_lo[i][c] : a;
+            b = sh_hi[i][c] > b ? sh_hi[i][c] : b;
+            o |= sh_or[i][c];
+        }
+        atomicMin(&h->lo[c], a);
+        atomicMax(&h->hi[c], b);
+        if (o) atomicOr(&h->vary[c], o);
     }
 }
 
@@ -107,11 +136,17 @@ __global__ void k_plan(TableHeader* h) {
     }
     h->total_bits = total;
     if (total > kMaxKeyBits) h->status |= ST_RANGE;
+    int nb = 0;
+    for (int c = 1; c < ncol && nb < 3; ++c) {
+        const int t = h->vary[c] ? __ffs(h->vary[c]) - 1 : -1;   // lowest varying bit
+        if (t >= 0 && t < bits[c]) h->blk_shift[nb++] = h->shift[c] + t;
+    }
+    h->nblk = nb;
 }
 
 __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int64_t n, TableHeader* h,
                                                      Slot* slots) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (r >= n) return;
     if (h->status & ST_RANGE) return;
     const int ncol = h->ncol;
@@ -124,7 +159,7 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
         atomicOr(&h->status, ST_RANGE);
         return;
     }
-    unsigned long long s = mix64(key) & mask;
+    unsigned long long s = home_slot(h, key, mask);
     for (unsigned long long i = 0; i <= mask; ++i) {
         unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
         if (prev == kEmptyKey) {
@@ -144,7 +179,7 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
 // produces it; remember the slot of every row.
 __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, int64_t n, StrideArg st,
                                                          TableHeader* h, Slot* slots, int64_t* slot_of) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (r >= n) return;
     if (h->status & ST_RANGE) {
         slot_of[r] = 0;
@@ -160,7 +195,7 @@ __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, 
         slot_of[r] = 0;
         return;
     }
-    unsigned long long s = mix64(key) & mask;
+    unsigned long long s = home_slot(h, key, mask);
     for (unsigned long long i = 0; i <= mask; ++i) {
         unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
         if (prev == kEmptyKey || prev == key) {
@@ -177,7 +212,7 @@ __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, 
 // mark representatives (slot holds this row) and count them per 64-row group
 __global__ void __launch_bounds__(kThreads) k_rep_count(int64_t n, const TableHeader* h, const Slot* slots,
                                                         int64_t* slot_of, int32_t* cnt) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     bool rep = false;
     if (r < n && h->status == 0) {
         const int64_t s = slot_of[r];
@@ -192,7 +227,7 @@ __global__ void __launch_bounds__(kThreads) k_rep_count(int64_t n, const TableHe
 __global__ void __launch_bounds__(kThreads) k_rep_write(const int32_t* coords, int64_t n, StrideArg st,
                                                         TableHeader* h, Slot* slots, const int64_t* slot_of,
                                                         const int64_t* off, int32_t* out_coords) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     bool rep = false;
     int64_t s = 0;
     if (r < n && h->status == 0) {
@@ -216,10 +251,10 @@ static unsigned grid_for(int64_t n, int per = kThreads) {
     return (unsigned)g;
 }
 
-static unsigned grid_capped(int64_t n) {
+static unsigned grid_capped(int64_t n, int64_t cap = 2048) {
     int64_t g = (n + kThreads - 1) / kThreads;
     if (g < 1) g = 1;
-    if (g > 2048) g = 2048;
+    if (g > cap) g = cap;
     return (unsigned)g;
 }
 
@@ -249,15 +284,14 @@ size_t gsc_table_bytes(int64_t n) {
     return kHeaderBytes + (size_t)table_capacity(n) * sizeof(Slot);
 }
 
-int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D, void* table, size_t table_bytes, void* stream) {
-    clear_error();
-    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "coords_build: D=%d outside [1,%d]", D, kMaxCols - 1);
-    if (n < 0 || n > INT32_MAX) return fail(GSC_EINVAL, "coords_build: n=%lld outside [0, 2^31)", (long long)n);
-    if (!table) return fail(GSC_EINVAL, "coords_build: table is null");
-    if (n > 0 && !coords) return fail(GSC_EINVAL, "coords_build: coords is null");
+static int build_enqueue(const int32_t* coords, int64_t n, int32_t D, void* table, size_t table_bytes,
+                         hipStream_t s, const char* what) {
+    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "%s: D=%d outside [1,%d]", what, D, kMaxCols - 1);
+    if (n < 0 || n > INT32_MAX) return fail(GSC_EINVAL, "%s: n=%lld outside [0, 2^31)", what, (long long)n);
+    if (!table) return fail(GSC_EINVAL, "%s: table is null", what);
+    if (n > 0 && !coords) return fail(GSC_EINVAL, "%s: coords is null", what);
     if (table_bytes < gsc_table_bytes(n))
-        return fail(GSC_ESHORT, "coords_build: table needs %zu bytes, got %zu", gsc_table_bytes(n), table_bytes);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        return fail(GSC_ESHORT, "%s: table needs %zu bytes, got %zu", what, gsc_table_bytes(n), table_bytes);
     const int ncol = D + 1;
     const int64_t cap = table_capacity(n);
     TableHeader* h = reinterpret_cast<TableHeader*>(table);
@@ -266,7 +300,7 @@ int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D, void* table, s
     GSC_LAUNCH_CHECK();
     StrideArg none{};
     if (n > 0) {
-        hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n)), dim3(kThreads), 0, s, coords, n, ncol, none, h);
+        hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n, 256)), dim3(kThreads), 0, s, coords, n, ncol, none, h);
         GSC_LAUNCH_CHECK();
     }
     hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
@@ -275,10 +309,35 @@ int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D, void* table, s
         hipLaunchKernelGGL(k_insert, dim3(grid_for(n)), dim3(kThreads), 0, s, coords, n, h, slots);
         GSC_LAUNCH_CHECK();
     }
+    return GSC_OK;
+}
+
+int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D, void* table, size_t table_bytes, void* stream) {
+    clear_error();
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int rc = build_enqueue(coords, n, D, table, table_bytes, s, "coords_build");
+    if (rc) return rc;
     TableHeader hh;
-    int rc = read_status(table, s, &hh);
+    rc = read_status(table, s, &hh);
     if (rc) return rc;
     return status_to_code(hh, "coords_build");
+}
+
+int gsc_coords_build_async(const int32_t* coords, int64_t n, int32_t D, void* table, size_t table_bytes,
+                           void* stream) {
+    clear_error();
+    return build_enqueue(coords, n, D, table, table_bytes, reinterpret_cast<hipStream_t>(stream),
+                         "coords_build_async");
+}
+
+int gsc_table_status(const void* table, void* stream) {
+    clear_error();
+    if (!table) return fail(GSC_EINVAL, "table_status: table is null");
+    TableHeader hh;
+    int rc = read_status(table, reinterpret_cast<hipStream_t>(stream), &hh);
+    if (rc) return rc;
+    if (hh.magic != kTableMagic) return fail(GSC_EINVAL, "table_status: not a table built by gsc_coords_build");
+    return status_to_code(hh, "table");
 }
 
 size_t gsc_stride_ws_bytes(int64_t n_in) {
@@ -340,7 +399,7 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
     w += ((size_t)(groups + 1) * sizeof(int64_t) + 255) & ~(size_t)255;
     void* scan_ws = w;
 
-    hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n_in)), dim3(kThreads), 0, s, in_coords, n_in, ncol, st, h);
+    hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n_in, 256)), dim3(kThreads), 0, s, in_coords, n_in, ncol, st, h);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
     GSC_LAUNCH_CHECK();

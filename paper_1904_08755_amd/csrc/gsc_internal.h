@@ -52,6 +52,9 @@ struct TableHeader {
     int32_t hi[kMaxCols];
     int32_t shift[kMaxCols];
     int32_t bits[kMaxCols];
+    int32_t vary[kMaxCols];  // OR over rows of (row XOR first row): the bits that vary per column
+    int32_t nblk;            // spatial columns whose lowest varying key bit selects the slot in a line
+    int32_t blk_shift[3];    // that key bit, per blocked column
 };
 static_assert(sizeof(TableHeader) <= kHeaderBytes, "header too large");
 
@@ -62,9 +65,10 @@ struct alignas(16) Slot {
 };
 static_assert(sizeof(Slot) == 16, "slot must be 16 bytes");
 
+// capacity: a power of two >= 4n (load factor <= 1/4) and >= 64
 inline int64_t table_capacity(int64_t n) {
     int64_t cap = 64;
-    while (cap < 2 * n) cap <<= 1;
+    while (cap < 4 * n) cap <<= 1;
     return cap;
 }
 
@@ -99,11 +103,28 @@ __device__ __forceinline__ bool pack_key(const TableHeader* h, int ncol, const i
     return true;
 }
 
-// Linear-probing lookup; at most `capacity` probes, so it ends even on a
-// table left full by a failed build.
-__device__ __forceinline__ int32_t table_find(const Slot* slots, unsigned long long mask,
-                                              unsigned long long key) {
-    unsigned long long s = mix64(key) & mask;
+// Home slot of a key.  The lowest varying bit of each of the first (up to)
+// three spatial columns (bit 0 for unit tensor stride, bit 1 for coordinates
+// that are all even, ...) selects the slot inside an aligned group of 2^nblk slots
+// and the rest of the key is hashed to pick the group, so the 2 x 2 x 2 block
+// of coordinates around a point shares one 128-byte line of the table and a
+// 3 x 3 x 3 neighbourhood touches about 8 lines instead of 27.
+__device__ __forceinline__ unsigned long long home_slot(const TableHeader* h, unsigned long long key,
+                                                        unsigned long long mask) {
+    unsigned long long local = 0, bkey = key;
+    const int nb = h->nblk;
+    for (int i = 0; i < nb; ++i) {
+        const int sh = h->blk_shift[i];
+        local |= ((key >> sh) & 1ull) << i;
+        bkey &= ~(1ull << sh);
+    }
+    return ((mix64(bkey) << nb) | local) & mask;
+}
+
+// Linear-probing lookup from slot s; at most `capacity` probes, so it ends
+// even on a table left full by a failed build.
+__device__ __forceinline__ int32_t table_find_from(const Slot* slots, unsigned long long mask,
+                                                   unsigned long long key, unsigned long long s) {
     for (unsigned long long i = 0; i <= mask; ++i) {
         const Slot e = slots[s];
         if (e.key == key) return e.val;
@@ -111,6 +132,11 @@ __device__ __forceinline__ int32_t table_find(const Slot* slots, unsigned long l
         s = (s + 1) & mask;
     }
     return -1;
+}
+
+__device__ __forceinline__ int32_t table_find(const TableHeader* h, const Slot* slots, unsigned long long mask,
+                                              unsigned long long key) {
+    return table_find_from(slots, mask, key, home_slot(h, key, mask));
 }
 
 // floor(a / s) * s for s > 0
@@ -127,6 +153,21 @@ __device__ __forceinline__ int64_t floor_mul(int64_t a, int64_t s) {
 size_t scan_ws_bytes(int64_t m);
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
                 hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// XCD-aware block order.  The eight XCDs of the MI355X receive workgroups
+// round-robin (workgroup b runs on XCD b % 8) and each XCD has its own L2.
+// Work unit t = xcd_unit(b, n) gives XCD x a contiguous range of units, so
+// neighbouring units (which gather mostly the same rows) share an L2.  It is
+// a bijection of [0, n).
+// ---------------------------------------------------------------------------
+constexpr int kNumXcd = 8;
+
+__device__ __forceinline__ int64_t xcd_unit(int64_t b, int64_t n) {
+    const int64_t q = n / kNumXcd, r = n % kNumXcd;
+    const int64_t x = b % kNumXcd, i = b / kNumXcd;
+    return x * q + (x < r ? x : r) + i;
+}
 
 // ---------------------------------------------------------------------------
 // wave helpers (wave64)

@@ -4,8 +4,10 @@
 //          the pair count of every 64-row group;
 //   scan:  exclusive scan of the (offset-major, group-minor) counts gives the
 //          start of each group's pairs (the group index gidx) and the total;
-//   fill:  the same probes again; a hit is written at its group start plus
-//          its rank among the wave's hits (popcount of the lower-lane mask).
+//   fill:  from the hit masks kept by the count pass, each hit is placed at
+//          its group start plus its rank among the wave's hits (popcount of
+//          the lower-lane mask);
+//   resolve: one lane per pair probes the table again for the input row.
 // Pairs of one offset therefore come out sorted by output row, and the
 // result does not depend on scheduling.
 #include <climits>
@@ -16,65 +18,148 @@
 namespace gsc {
 
 constexpr int kThreads = 256;
+constexpr int kOffArgMax = 768;   // K * D offsets passed by value in the kernel arguments
+
+// Offsets of the region, either by value in the kernel arguments (no host
+// to device copy, so the map can be enqueued asynchronously) or in device
+// memory (large regions, synchronous mode only).
+struct OffsArg {
+    int32_t v[kOffArgMax];
+    __device__ __forceinline__ const int32_t* at(int64_t i) const { return v + i; }
+};
+struct OffsPtr {
+    const int32_t* p;
+    __device__ __forceinline__ const int32_t* at(int64_t i) const { return p + i; }
+};
 
 __device__ __forceinline__ bool header_ok(const TableHeader* h, int ncol) {
     return h->magic == kTableMagic && h->ncol == ncol && h->status == 0;
 }
 
-__device__ __forceinline__ int32_t probe(const TableHeader* h, const Slot* slots, unsigned long long mask, int ncol,
-                                         const int64_t* u, const int32_t* off) {
+// Key of u + off; false if it lies outside the table's bounding box (a miss).
+__device__ __forceinline__ bool query_key(const TableHeader* h, int ncol, const int64_t* u, const int32_t* off,
+                                          unsigned long long* key) {
     int64_t q[kMaxCols];
     q[0] = u[0];
     for (int c = 1; c < ncol; ++c) q[c] = u[c] + off[c - 1];
-    unsigned long long key;
-    if (!pack_key(h, ncol, q, &key)) return -1;
-    return table_find(slots, mask, key);
+    return pack_key(h, ncol, q, key);
 }
 
+constexpr int kBatch = 8;   // probes issued together per lane in the count pass
+
+// Count pass.  Each lane owns one output row.  Offsets are probed kBatch at a
+// time and collision chains are followed in rounds: every round issues the
+// next slot load of all unresolved probes of the batch together, so the
+// loads of a round are in flight at once.  Hits are recorded in a bit mask per
+// row (word w of row j at hits[w * n_out + j]) and counted per 64-row group
+// with a wave ballot.
+template <typename Offs>
 __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* out_coords, int64_t n_out,
-                                                         int ncol, const int32_t* offs, int K, int64_t G,
-                                                         int32_t* cnt, int64_t* err) {
+                                                         int ncol, Offs offs, int K, int64_t G, int32_t* cnt,
+                                                         uint32_t* hits, int64_t* err) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
     const Slot* slots = table_slots(table);
     const bool ok = header_ok(h, ncol);
-    if (!ok && blockIdx.x == 0 && threadIdx.x == 0) *err = 1;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
     const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
-    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     const bool valid = ok && j < n_out;
     int64_t u[kMaxCols];
     for (int c = 0; c < ncol; ++c) u[c] = valid ? out_coords[j * ncol + c] : 0;
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
     const int D = ncol - 1;
-    for (int k = 0; k < K; ++k) {
-        const bool hit = valid && probe(h, slots, mask, ncol, u, offs + (int64_t)k * D) >= 0;
-        const unsigned long long m = __ballot(hit);
-        if (writer) cnt[(int64_t)k * G + g] = __popcll(m);
+    uint32_t word = 0;
+    for (int k0 = 0; k0 < K; k0 += kBatch) {
+        unsigned long long key[kBatch], pos[kBatch];
+        bool pend[kBatch], hit[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            const int k = k0 + b;
+            pend[b] = valid && k < K && query_key(h, ncol, u, offs.at((int64_t)k * D), &key[b]);
+            pos[b] = pend[b] ? home_slot(h, key[b], mask) : 0;
+            hit[b] = false;
+        }
+        for (unsigned long long round = 0; round <= mask; ++round) {
+            bool any = false;
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b) any |= pend[b];
+            if (!__any(any)) break;
+            unsigned long long ek[kBatch];
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b) ek[b] = pend[b] ? slots[pos[b]].key : kEmptyKey;
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b) {
+                if (!pend[b]) continue;
+                if (ek[b] == key[b]) {
+                    hit[b] = true;
+                    pend[b] = false;
+                } else if (ek[b] == kEmptyKey) {
+                    pend[b] = false;
+                } else {
+                    pos[b] = (pos[b] + 1) & mask;
+                }
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            const int k = k0 + b;
+            if (k < K) {
+                const unsigned long long m = __ballot(hit[b]);
+                if (writer) cnt[(int64_t)k * G + g] = __popcll(m);
+                word |= (uint32_t)hit[b] << (k & 31);
+                if ((k & 31) == 31 || k == K - 1) {
+                    if (j < n_out) hits[(int64_t)(k >> 5) * n_out + j] = word;
+                    word = 0;
+                }
+            }
+        }
     }
 }
 
-__global__ void __launch_bounds__(kThreads) k_kmap_fill(const void* table, const int32_t* out_coords, int64_t n_out,
-                                                        int ncol, const int32_t* offs, int K, int64_t G,
+// Fill pass: the ballots come from the hit masks; each hit gets its position
+// (group start + rank among the wave's hits), out_idx = j, and temporarily
+// in_idx = k, which the resolve pass replaces by the input row.
+__global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, int64_t G, const uint32_t* hits,
                                                         const int64_t* gidx, int32_t* in_idx, int32_t* out_idx) {
-    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    const Slot* slots = table_slots(table);
-    if (!header_ok(h, ncol)) return;
-    const unsigned long long mask = (unsigned long long)h->capacity - 1;
-    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     const bool valid = j < n_out;
-    int64_t u[kMaxCols];
-    for (int c = 0; c < ncol; ++c) u[c] = valid ? out_coords[j * ncol + c] : 0;
     const int64_t g = j >> 6;
-    const int D = ncol - 1;
     const unsigned long long below = lanemask_lt();
+    uint32_t word = 0;
     for (int k = 0; k < K; ++k) {
-        const int32_t r = valid ? probe(h, slots, mask, ncol, u, offs + (int64_t)k * D) : -1;
-        const unsigned long long m = __ballot(r >= 0);
-        if (r >= 0) {
+        if ((k & 31) == 0) word = valid ? hits[(int64_t)(k >> 5) * n_out + j] : 0u;
+        const bool hit = (word >> (k & 31)) & 1u;
+        const unsigned long long m = __ballot(hit);
+        if (hit) {
             const int64_t pos = gidx[(int64_t)k * G + g] + __popcll(m & below);
-            in_idx[pos] = r;
+            in_idx[pos] = k;
             out_idx[pos] = (int32_t)j;
         }
+    }
+}
+
+// Resolve pass: one lane per pair probes u_j + o_k (a guaranteed hit).  The
+// pair count is read on the device (gidx[K*G]), so the grid only has to cover
+// an upper bound; lanes stride over it.
+template <typename Offs>
+__global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, const int32_t* out_coords, int ncol,
+                                                           Offs offs, const int64_t* total, int32_t* in_idx,
+                                                           const int32_t* out_idx) {
+    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
+    const Slot* slots = table_slots(table);
+    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    const int64_t n_pairs = *total;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t p = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x; p < n_pairs; p += stride) {
+        const int64_t j = out_idx[p];
+        const int k = in_idx[p];
+        int64_t u[kMaxCols];
+        for (int c = 0; c < ncol; ++c) u[c] = out_coords[j * ncol + c];
+        unsigned long long key;
+        int32_t r = -1;
+        if (query_key(h, ncol, u, offs.at((int64_t)k * (ncol - 1)), &key)) r = table_find(h, slots, mask, key);
+        in_idx[p] = r;
     }
 }
 
@@ -84,6 +169,46 @@ __global__ void k_seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* 
 }
 
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+template <typename Offs>
+static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t n_out, int ncol, Offs offs, int K,
+                        int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg, int64_t* gidx,
+                        int64_t* n_pairs, int64_t* res, int32_t* cnt, uint32_t* hits, void* scan_ws, hipStream_t s) {
+    const unsigned nblk = (unsigned)((n_out + kThreads - 1) / kThreads);
+    if (nblk > 0) {
+        hipLaunchKernelGGL((k_kmap_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol,
+                           offs, K, G, cnt, hits, res + 1);
+        GSC_LAUNCH_CHECK();
+    }
+    int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_seg_from_gidx, dim3((unsigned)((K + 1 + 255) / 256)), dim3(256), 0, s, gidx, K, G, seg);
+    GSC_LAUNCH_CHECK();
+    int64_t bound = cap_pairs;
+    if (n_pairs) {
+        int64_t hres[2];
+        GSC_HIP(hipMemcpyAsync(hres, res, sizeof(hres), hipMemcpyDeviceToHost, s));
+        GSC_HIP(hipStreamSynchronize(s));
+        // the count kernel (launched when n_out > 0) writes the header check
+        if (nblk > 0 && hres[1])
+            return fail(GSC_EINVAL, "kernel_map: in_table is not a valid table of %d-column rows", ncol);
+        *n_pairs = hres[0];
+        if (hres[0] > cap_pairs)
+            return fail(GSC_ESHORT, "kernel_map: %lld pairs exceed cap_pairs=%lld", (long long)hres[0],
+                        (long long)cap_pairs);
+        bound = hres[0];
+    }
+    if (nblk > 0 && bound > 0) {
+        hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, n_out, K, G, hits, gidx, in_idx, out_idx);
+        GSC_LAUNCH_CHECK();
+        int64_t rb = (bound + kThreads - 1) / kThreads;
+        if (rb > 4096) rb = 4096;
+        hipLaunchKernelGGL((k_kmap_resolve<Offs>), dim3((unsigned)rb), dim3(kThreads), 0, s, in_table, out_coords,
+                           ncol, offs, (const int64_t*)res, in_idx, out_idx);
+        GSC_LAUNCH_CHECK();
+    }
+    return GSC_OK;
+}
 
 }  // namespace gsc
 
@@ -99,6 +224,7 @@ size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D) {
     size_t b = align256((size_t)K * D * sizeof(int32_t));      // offsets (scaled)
     b += align256(2 * sizeof(int64_t));                         // total, error flag
     b += align256((size_t)K * G * sizeof(int32_t));             // counts
+    b += align256((size_t)((K + 31) / 32) * n_out * sizeof(uint32_t));   // hit masks
     b += scan_ws_bytes(K * G);
     return b + 256;
 }
@@ -110,13 +236,22 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "kernel_map: D=%d outside [1,%d]", D, kMaxCols - 1);
     if (K < 1) return fail(GSC_EINVAL, "kernel_map: K=%d must be >= 1", K);
     if (n_out < 0 || n_out > INT32_MAX) return fail(GSC_EINVAL, "kernel_map: n_out=%lld invalid", (long long)n_out);
-    if (!in_table || !offsets || !seg || !gidx || !n_pairs || !ws)
-        return fail(GSC_EINVAL, "kernel_map: null in_table/offsets/seg/gidx/n_pairs/ws");
+    if (!in_table || !offsets || !seg || !gidx || !ws)
+        return fail(GSC_EINVAL, "kernel_map: null in_table/offsets/seg/gidx/ws");
     if (n_out > 0 && !out_coords) return fail(GSC_EINVAL, "kernel_map: out_coords is null");
     if (cap_pairs < 0) return fail(GSC_EINVAL, "kernel_map: cap_pairs < 0");
     if (cap_pairs > 0 && (!in_idx || !out_idx)) return fail(GSC_EINVAL, "kernel_map: null in_idx/out_idx");
     if (ws_bytes < gsc_kmap_ws_bytes(n_out, K, D))
         return fail(GSC_ESHORT, "kernel_map: ws needs %zu bytes, got %zu", gsc_kmap_ws_bytes(n_out, K, D), ws_bytes);
+    const bool by_value = (int64_t)K * D <= kOffArgMax;
+    if (!n_pairs) {   // asynchronous mode
+        if (cap_pairs < (int64_t)K * n_out)
+            return fail(GSC_ESHORT, "kernel_map: asynchronous mode needs cap_pairs >= K*n_out = %lld",
+                        (long long)K * n_out);
+        if (!by_value)
+            return fail(GSC_EINVAL, "kernel_map: asynchronous mode needs K*D <= %d (got %d)", kOffArgMax, K * D);
+    }
+    OffsArg arg;
     std::vector<int32_t> offs((size_t)K * D);
     for (int k = 0; k < K; ++k)
         for (int d = 0; d < D; ++d) {
@@ -126,6 +261,7 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
             if (v < -(1ll << 30) || v > (1ll << 30))
                 return fail(GSC_ERANGE, "kernel_map: scaled offset %lld out of range", (long long)v);
             offs[(size_t)k * D + d] = (int32_t)v;
+            if (by_value) arg.v[(size_t)k * D + d] = (int32_t)v;
         }
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -138,34 +274,16 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     w += align256(2 * sizeof(int64_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += align256((size_t)K * G * sizeof(int32_t));
+    uint32_t* hits = reinterpret_cast<uint32_t*>(w);
+    w += align256((size_t)((K + 31) / 32) * n_out * sizeof(uint32_t));
     void* scan_ws = w;
-
+    if (by_value)
+        return kmap_enqueue(in_table, out_coords, n_out, ncol, arg, K, G, in_idx, out_idx, cap_pairs, seg, gidx,
+                            n_pairs, res, cnt, hits, scan_ws, s);
+    // synchronous mode: the copy below completes before this call returns
     GSC_HIP(hipMemcpyAsync(d_offs, offs.data(), offs.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
-    GSC_HIP(hipMemsetAsync(res, 0, 2 * sizeof(int64_t), s));
-    const unsigned nblk = (unsigned)((n_out + kThreads - 1) / kThreads);
-    if (nblk > 0) {
-        hipLaunchKernelGGL(k_kmap_count, dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol, d_offs,
-                           K, G, cnt, res + 1);
-        GSC_LAUNCH_CHECK();
-    }
-    int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_seg_from_gidx, dim3((unsigned)((K + 1 + 255) / 256)), dim3(256), 0, s, gidx, K, G, seg);
-    GSC_LAUNCH_CHECK();
-    int64_t hres[2];
-    GSC_HIP(hipMemcpyAsync(hres, res, sizeof(hres), hipMemcpyDeviceToHost, s));
-    GSC_HIP(hipStreamSynchronize(s));
-    if (hres[1]) return fail(GSC_EINVAL, "kernel_map: in_table is not a valid table of %d-column rows", ncol);
-    *n_pairs = hres[0];
-    if (hres[0] > cap_pairs)
-        return fail(GSC_ESHORT, "kernel_map: %lld pairs exceed cap_pairs=%lld", (long long)hres[0],
-                    (long long)cap_pairs);
-    if (nblk > 0 && hres[0] > 0) {
-        hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol, d_offs,
-                           K, G, gidx, in_idx, out_idx);
-        GSC_LAUNCH_CHECK();
-    }
-    return GSC_OK;
+    return kmap_enqueue(in_table, out_coords, n_out, ncol, OffsPtr{d_offs}, K, G, in_idx, out_idx, cap_pairs, seg,
+                        gidx, n_pairs, res, cnt, hits, scan_ws, s);
 }
 
 }  // extern "C"

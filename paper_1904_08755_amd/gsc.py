@@ -43,6 +43,8 @@ _SIGS = {
     "gsc_abi_version": (ctypes.c_int, []),
     "gsc_table_bytes": (_sz, [_i64]),
     "gsc_coords_build": (ctypes.c_int, [_vp, _i64, _i32, _vp, _sz, _vp]),
+    "gsc_coords_build_async": (ctypes.c_int, [_vp, _i64, _i32, _vp, _sz, _vp]),
+    "gsc_table_status": (ctypes.c_int, [_vp, _vp]),
     "gsc_stride_ws_bytes": (_sz, [_i64]),
     "gsc_coords_stride": (ctypes.c_int, [_vp, _i64, _i32, _c_i32p, _vp, _c_i64p, _vp, _sz, _vp, _sz, _vp]),
     "gsc_kmap_groups": (_i64, [_i64]),
@@ -120,14 +122,23 @@ def gsc_table_bytes(n: int) -> int:
     return int(lib().gsc_table_bytes(n))
 
 
-def gsc_coords_build(coords: torch.Tensor, table: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+def gsc_coords_build(coords: torch.Tensor, table: Optional[torch.Tensor] = None, stream=None,
+                     sync: bool = True) -> torch.Tensor:
+    """Hash table of ``coords``.  ``sync=False`` calls gsc_coords_build_async
+    (errors found on the device are then reported by gsc_table_status)."""
     _need(coords, torch.int32, "coords", 2)
     n, ncol = coords.shape
     if table is None:
         table = torch.empty(gsc_table_bytes(n), dtype=torch.uint8, device=coords.device)
     _need(table, torch.uint8, "table", 1)
-    _check(lib().gsc_coords_build(_ptr(coords), n, ncol - 1, _ptr(table), table.numel(), _stream(stream)))
+    f = lib().gsc_coords_build if sync else lib().gsc_coords_build_async
+    _check(f(_ptr(coords), n, ncol - 1, _ptr(table), table.numel(), _stream(stream)))
     return table
+
+
+def gsc_table_status(table: torch.Tensor, stream=None) -> None:
+    """Raise GscError if the build of ``table`` failed on the device."""
+    _check(lib().gsc_table_status(_ptr(table), _stream(stream)))
 
 
 # --------------------------------------------------------------------------- #
@@ -158,25 +169,48 @@ def gsc_coords_stride(coords: torch.Tensor, stride: Sequence[int], out_table: Op
 # --------------------------------------------------------------------------- #
 @dataclasses.dataclass
 class KernelMap:
-    in_idx: torch.Tensor       # int32 [n_pairs]
-    out_idx: torch.Tensor      # int32 [n_pairs]
+    in_idx: torch.Tensor       # int32 [>= n_pairs]
+    out_idx: torch.Tensor      # int32 [>= n_pairs]
     seg: torch.Tensor          # int64 [K + 1]
     gidx: torch.Tensor         # int64 [K * G + 1]
-    n_pairs: int
+    n_pairs: Optional[int]     # None when built asynchronously (the count stays on the device)
     n_out: int
     offsets: np.ndarray        # K x D
+    n_bound: int = 0           # n_pairs, or an upper bound of it
 
     @property
     def K(self) -> int:
         return int(self.offsets.shape[0])
+
+    def count(self) -> int:
+        """Number of pairs (reads seg[K] from the device when unknown)."""
+        return self.n_pairs if self.n_pairs is not None else int(self.seg[-1].item())
 
 
 def gsc_kmap_groups(n_out: int) -> int:
     return int(lib().gsc_kmap_groups(n_out))
 
 
+class MapBuffers:
+    """Caller-owned buffers of one kernel map (reusable across calls)."""
+
+    def __init__(self, n_out: int, K: int, D: int, device, cap_pairs: Optional[int] = None):
+        G = gsc_kmap_groups(n_out)
+        self.cap = K * n_out if cap_pairs is None else int(cap_pairs)
+        self.in_idx = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
+        self.out_idx = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
+        self.seg = torch.empty(K + 1, dtype=torch.int64, device=device)
+        self.gidx = torch.empty(K * G + 1, dtype=torch.int64, device=device)
+        self.ws = _ws(lib().gsc_kmap_ws_bytes(n_out, K, D), device)
+
+
 def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, tensor_stride=None,
-                   cap_pairs: Optional[int] = None, stream=None) -> KernelMap:
+                   cap_pairs: Optional[int] = None, stream=None, sync: bool = True,
+                   bufs: Optional[MapBuffers] = None, host_offsets=None, host_ts=None) -> KernelMap:
+    """Kernel map of ``offsets`` from the table ``in_table`` to ``out_coords``.
+    ``sync=False`` builds it without a host round trip (n_pairs stays on the
+    device).  ``bufs``/``host_offsets``/``host_ts`` let a caller reuse buffers
+    and converted host arrays across calls."""
     _need(in_table, torch.uint8, "in_table", 1)
     _need(out_coords, torch.int32, "out_coords", 2)
     offs = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
@@ -184,29 +218,29 @@ def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, te
     n_out = out_coords.shape[0]
     if out_coords.shape[1] != D + 1:
         raise ValueError("offsets must be K x D with D = out_coords columns - 1")
-    dev = out_coords.device
-    G = gsc_kmap_groups(n_out)
-    seg = torch.empty(K + 1, dtype=torch.int64, device=dev)
-    gidx = torch.empty(K * G + 1, dtype=torch.int64, device=dev)
-    ws = _ws(lib().gsc_kmap_ws_bytes(n_out, K, D), dev)
-    ts = None if tensor_stride is None else _host_i32([tensor_stride] * D if np.isscalar(tensor_stride)
-                                                      else tensor_stride)
-    cap = K * n_out if cap_pairs is None else int(cap_pairs)
-    in_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
-    out_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    if bufs is None:
+        bufs = MapBuffers(n_out, K, D, out_coords.device, cap_pairs)
+    if host_offsets is None:
+        host_offsets = _host_i32(offs)
+    if host_ts is None and tensor_stride is not None:
+        host_ts = _host_i32([tensor_stride] * D if np.isscalar(tensor_stride) else tensor_stride)
     n_pairs = ctypes.c_int64(0)
-    rc = lib().gsc_kernel_map(_ptr(in_table), _ptr(out_coords), n_out, D, _host_i32(offs), K, ts, _ptr(in_idx),
-                              _ptr(out_idx), cap, _ptr(seg), _ptr(gidx), ctypes.byref(n_pairs), _ptr(ws), ws.numel(),
+    rc = lib().gsc_kernel_map(_ptr(in_table), _ptr(out_coords), n_out, D, host_offsets, K, host_ts,
+                              _ptr(bufs.in_idx), _ptr(bufs.out_idx), bufs.cap, _ptr(bufs.seg), _ptr(bufs.gidx),
+                              ctypes.byref(n_pairs) if sync else None, _ptr(bufs.ws), bufs.ws.numel(),
                               _stream(stream))
     _check(rc)
-    m = n_pairs.value
-    return KernelMap(in_idx[:m], out_idx[:m], seg, gidx, m, n_out, offs)
+    if sync:
+        m = n_pairs.value
+        return KernelMap(bufs.in_idx[:m], bufs.out_idx[:m], bufs.seg, bufs.gidx, m, n_out, offs, m)
+    return KernelMap(bufs.in_idx, bufs.out_idx, bufs.seg, bufs.gidx, None, n_out, offs, bufs.cap)
 
 
 def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offsets, tensor_stride=None,
-                          stream=None) -> KernelMap:
+                          stream=None, sync: bool = True, bufs: Optional[MapBuffers] = None) -> KernelMap:
     """The role-reversed map (Sec. 4.2): same pairs, listed by original input row."""
-    return gsc_kernel_map(out_table, in_coords, -np.asarray(offsets, dtype=np.int32), tensor_stride, stream=stream)
+    return gsc_kernel_map(out_table, in_coords, -np.asarray(offsets, dtype=np.int32), tensor_stride, stream=stream,
+                          sync=sync, bufs=bufs)
 
 
 def negation_permutation(offsets) -> np.ndarray:
@@ -242,7 +276,7 @@ def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out
         Y = torch.empty((n_out, co), dtype=X.dtype, device=X.device)
     _need(Y, X.dtype, "Y", 2)
     _check(lib().gsc_sparse_conv_fwd(dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx),
-                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_pairs, _ptr(Y),
+                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_bound, _ptr(Y),
                                      n_out, _stream(stream)))
     return Y
 
@@ -254,7 +288,7 @@ def gsc_conv_bwd_ws_bytes(n_pairs: int, c_in: int, c_out: int, K: int) -> int:
 def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap: KernelMap,
                         tmap: KernelMap, wsel, need_dx: bool = True, need_dw: bool = True,
                         dX: Optional[torch.Tensor] = None, dW: Optional[torch.Tensor] = None,
-                        ws: Optional[torch.Tensor] = None, stream=None):
+                        ws: Optional[torch.Tensor] = None, stream=None, host_wsel=None):
     """Returns (dX or None, dW or None).  ``tmap`` is the dX map (role-reversed
     pairs, sorted by input row) and ``wsel`` its per-segment weight index."""
     dt = _dt(X)
@@ -273,12 +307,12 @@ def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap
     if need_dw and dW is None:
         dW = torch.empty((K, ci, co), dtype=torch.float32, device=dev)
     if need_dw and ws is None:
-        ws = _ws(gsc_conv_bwd_ws_bytes(kmap.n_pairs, ci, co, K), dev)
-    sel = _host_i32(wsel)
+        ws = _ws(gsc_conv_bwd_ws_bytes(kmap.n_bound, ci, co, K), dev)
+    sel = _host_i32(wsel) if host_wsel is None else host_wsel
     _check(lib().gsc_sparse_conv_bwd(
         dt, _ptr(X), _ptr(W), _ptr(dY), n_in, ci, co, K,
-        _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg), kmap.n_pairs,
-        _ptr(tmap.in_idx), _ptr(tmap.out_idx), _ptr(tmap.seg), _ptr(tmap.gidx), tmap.n_pairs, sel,
+        _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg), kmap.n_bound,
+        _ptr(tmap.in_idx), _ptr(tmap.out_idx), _ptr(tmap.seg), _ptr(tmap.gidx), tmap.n_bound, sel,
         _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
         _ptr(ws) if need_dw else None, ws.numel() if need_dw else 0, _stream(stream)))
     return (dX if need_dx else None), (dW if need_dw else None)

@@ -4,6 +4,12 @@ A pass is: hash table of the input coordinates, output coordinates (strided
 layers), kernel maps, convolution forward, then both backward passes.  It is
 host orchestration only: every stage is one call of libgsc.so.
 
+``StepPlan`` allocates every buffer and converts every host array once, so a
+pass only enqueues library calls.  The table build and the kernel maps run in
+their asynchronous modes (the pair count stays on the device), so a pass of a
+submanifold layer has no host round trip at all; a strided layer needs one,
+to learn how many output coordinates it has.
+
 Map reuse (Sec. 4.2 builds the kernel map once per coordinate pair):
   * submanifold layer with a symmetric region: the input-gradient map is the
     forward map itself with offset s using the weight of -o_s (no rebuild);
@@ -61,43 +67,102 @@ class StepResult:
     dYs_inner: List[torch.Tensor]            # gradients flowing between layers (down/up only)
 
 
-def _identity(K: int) -> np.ndarray:
-    return np.arange(K, dtype=np.int32)
+class StepPlan:
+    """Buffers for repeated passes over one device workload."""
+
+    def __init__(self, dw: DeviceWorkload):
+        self.dw = dw
+        wl = dw.wl
+        self.kinds = [L.kind for L in wl.layers]
+        n, D, dev = wl.n, wl.D, dw.X.device
+        feat = dw.X.dtype
+        self.table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device=dev)
+        if self.kinds == ["subm"]:
+            L = wl.layers[0]
+            offs = dw.offsets[0]
+            K = len(offs)
+            self.mb = gsc.MapBuffers(n, K, D, dev)
+            self.host_offs = gsc._host_i32(offs)
+            self.symmetric = regions.is_symmetric(offs)
+            if self.symmetric:
+                wsel = gsc.negation_permutation(offs)
+            else:
+                self.tb = gsc.MapBuffers(n, K, D, dev)
+                self.host_offs_neg = gsc._host_i32(-offs)
+                wsel = np.arange(K, dtype=np.int32)
+            self.host_wsel = gsc._host_i32(wsel)
+            self.Y = torch.empty((n, L.c_out), dtype=feat, device=dev)
+            self.dX = torch.empty((n, L.c_in), dtype=feat, device=dev)
+            self.dW = torch.empty((K, L.c_in, L.c_out), dtype=torch.float32, device=dev)
+            self.ws_bwd = gsc._ws(gsc.gsc_conv_bwd_ws_bytes(self.mb.cap, L.c_in, L.c_out, K), dev)
+        elif self.kinds == ["down", "up"]:
+            L0, L1 = wl.layers
+            offs = dw.offsets[0]
+            K = len(offs)
+            self.out_table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device=dev)
+            # n_out <= n: size every coarse-side buffer for n rows
+            self.kd = gsc.MapBuffers(n, K, D, dev)
+            self.td = gsc.MapBuffers(n, K, D, dev)
+            self.host_offs = gsc._host_i32(offs)
+            self.host_offs_neg = gsc._host_i32(-offs)
+            self.host_ident = gsc._host_i32(np.arange(K, dtype=np.int32))
+            self.Y1 = torch.empty((n, L0.c_out), dtype=feat, device=dev)
+            self.Y2 = torch.empty((n, L1.c_out), dtype=feat, device=dev)
+            self.dY1 = torch.empty((n, L0.c_out), dtype=feat, device=dev)
+            self.dX = torch.empty((n, L0.c_in), dtype=feat, device=dev)
+            self.dW1 = torch.empty((K, L0.c_in, L0.c_out), dtype=torch.float32, device=dev)
+            self.dW2 = torch.empty((K, L1.c_in, L1.c_out), dtype=torch.float32, device=dev)
+            self.ws_bwd1 = gsc._ws(gsc.gsc_conv_bwd_ws_bytes(self.kd.cap, L0.c_in, L0.c_out, K), dev)
+            self.ws_bwd2 = gsc._ws(gsc.gsc_conv_bwd_ws_bytes(self.kd.cap, L1.c_in, L1.c_out, K), dev)
+        else:
+            raise ValueError(f"unsupported layer sequence {self.kinds}")
+
+    def run(self, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
+        """Enqueue one pass.  ``mark(name)`` (optional) is called after each
+        stage is enqueued: "map" (coordinates + kernel maps), "fwd", "bwd"."""
+        mark = mark or (lambda name: None)
+        dw = self.dw
+        if self.kinds == ["subm"]:
+            offs = dw.offsets[0]
+            gsc.gsc_coords_build(dw.coords, self.table, stream=stream, sync=False)
+            kmap = gsc.gsc_kernel_map(self.table, dw.coords, offs, stream=stream, sync=False, bufs=self.mb,
+                                      host_offsets=self.host_offs)
+            if self.symmetric:
+                tmap = kmap
+            else:
+                tmap = gsc.gsc_kernel_map(self.table, dw.coords, -offs, stream=stream, sync=False, bufs=self.tb,
+                                          host_offsets=self.host_offs_neg)
+            mark("map")
+            Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kmap, Y=self.Y, stream=stream)
+            mark("fwd")
+            dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, kmap, tmap, None, dX=self.dX, dW=self.dW,
+                                             ws=self.ws_bwd, stream=stream, host_wsel=self.host_wsel)
+            mark("bwd")
+            return StepResult(None, [kmap], [Y], dX, [dW], [])
+        L0 = dw.wl.layers[0]
+        offs = dw.offsets[0]
+        gsc.gsc_coords_build(dw.coords, self.table, stream=stream, sync=False)
+        out_coords, _ = gsc.gsc_coords_stride(dw.coords, L0.stride, out_table=self.out_table, stream=stream)
+        n_out = out_coords.shape[0]
+        kd = gsc.gsc_kernel_map(self.table, out_coords, offs, stream=stream, sync=False, bufs=self.kd,
+                                host_offsets=self.host_offs)
+        td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
+                                host_offsets=self.host_offs_neg)
+        mark("map")
+        Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kd, Y=self.Y1[:n_out], stream=stream)
+        Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], td, Y=self.Y2, stream=stream)
+        mark("fwd")
+        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, td, kd, None, dX=self.dY1[:n_out], dW=self.dW2,
+                                           ws=self.ws_bwd2, stream=stream, host_wsel=self.host_ident)
+        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, kd, td, None, dX=self.dX, dW=self.dW1,
+                                          ws=self.ws_bwd1, stream=stream, host_wsel=self.host_ident)
+        mark("bwd")
+        return StepResult(out_coords, [kd, td], [Y1, Y2], dX, [dW1, dW2], [dY1])
 
 
 def run_step(dw: DeviceWorkload, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
-    """Run one pass.  ``mark(name)`` (optional) is called after each stage is
-    enqueued: "map" (coordinates + kernel maps), "fwd", "bwd"."""
-    mark = mark or (lambda name: None)
-    kinds = [L.kind for L in dw.wl.layers]
-    if kinds == ["subm"]:
-        offs = dw.offsets[0]
-        table = gsc.gsc_coords_build(dw.coords, stream=stream)
-        kmap = gsc.gsc_kernel_map(table, dw.coords, offs, stream=stream)
-        if regions.is_symmetric(offs):
-            tmap, wsel = kmap, gsc.negation_permutation(offs)
-        else:
-            tmap, wsel = gsc.transposed_kernel_map(table, dw.coords, offs, stream=stream), _identity(len(offs))
-        mark("map")
-        Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kmap, stream=stream)
-        mark("fwd")
-        dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, kmap, tmap, wsel, stream=stream)
-        mark("bwd")
-        return StepResult(None, [kmap], [Y], dX, [dW], [])
-    if kinds == ["down", "up"]:
-        L0 = dw.wl.layers[0]
-        offs = dw.offsets[0]
-        ident = _identity(len(offs))
-        table = gsc.gsc_coords_build(dw.coords, stream=stream)
-        out_coords, out_table = gsc.gsc_coords_stride(dw.coords, L0.stride, stream=stream)
-        kd = gsc.gsc_kernel_map(table, out_coords, offs, stream=stream)
-        td = gsc.transposed_kernel_map(out_table, dw.coords, offs, stream=stream)
-        mark("map")
-        Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kd, stream=stream)
-        Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], td, stream=stream)
-        mark("fwd")
-        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, td, kd, ident, stream=stream)
-        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, kd, td, ident, stream=stream)
-        mark("bwd")
-        return StepResult(out_coords, [kd, td], [Y1, Y2], dX, [dW1, dW2], [dY1])
-    raise ValueError(f"unsupported layer sequence {kinds}")
+    """One pass with freshly allocated buffers; the table build is then checked."""
+    plan = StepPlan(dw)
+    res = plan.run(mark, stream)
+    gsc.gsc_table_status(plan.table, stream)
+    return res

@@ -43,9 +43,9 @@ def test_abi_version(L):
 
 def test_size_queries(L):
     assert L.gsc_table_bytes(0) == 256 + 64 * 16
-    assert L.gsc_table_bytes(32) == 256 + 64 * 16
-    assert L.gsc_table_bytes(33) == 256 + 128 * 16
-    assert L.gsc_table_bytes(300_000) == 256 + (1 << 20) * 16
+    assert L.gsc_table_bytes(16) == 256 + 64 * 16
+    assert L.gsc_table_bytes(17) == 256 + 128 * 16
+    assert L.gsc_table_bytes(300_000) == 256 + (1 << 21) * 16
     assert L.gsc_table_bytes(-1) == 0
     assert L.gsc_kmap_groups(0) == 0
     assert L.gsc_kmap_groups(1) == 1
@@ -102,6 +102,17 @@ def test_kernel_map_validation(L):
     assert L.gsc_kernel_map(*args(1, ts_bad, ws)) == gsc.GSC_EINVAL
     assert L.gsc_kernel_map(*args(1, None, ws - 1)) == gsc.GSC_ESHORT
     assert L.gsc_kernel_map(*args(1, None, ws, cap=-1)) == gsc.GSC_EINVAL
+    # asynchronous mode (n_pairs NULL) needs cap_pairs >= K * n_out and K * D <= 768
+    a = list(args(1, None, ws, cap=99))
+    a[12] = None
+    assert L.gsc_kernel_map(*a) == gsc.GSC_ESHORT and "asynchronous" in _err(L)
+    K = 300
+    offs300 = (ctypes.c_int32 * (3 * K))()
+    ws300 = L.gsc_kmap_ws_bytes(100, K, 3)
+    a = [fake, fake, 100, 3, offs300, K, None, fake, fake, K * 100, fake, fake, None, fake, ws300, None]
+    assert L.gsc_kernel_map(*a) == gsc.GSC_EINVAL and "768" in _err(L)
+    assert L.gsc_table_status(None, None) == gsc.GSC_EINVAL
+    assert L.gsc_coords_build_async(fake, 10, 0, fake, 1 << 20, None) == gsc.GSC_EINVAL
     big = (ctypes.c_int32 * 3)(1 << 29, 0, 0)
     ts4 = (ctypes.c_int32 * 3)(4, 1, 1)
     a = list(args(1, ts4, ws))

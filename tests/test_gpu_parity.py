@@ -61,7 +61,7 @@ def test_workload_full(cid):
     step = _run(wl)
     ref = oracle_step(wl)
     errs = compare_step(wl, step, ref)
-    npairs = [km.n_pairs for km in step.kmaps]
+    npairs = [km.count() for km in step.kmaps]
     _say(f"  pairs {npairs} errors {errs}")
 
 
@@ -264,3 +264,27 @@ def test_stride_then_second_level():
     p1, p2 = row_perm(g1, r1), row_perm(g2, r2)
     ref = O.kernel_map(r1, r2, O.hypercube(2, 3), 2)
     maps_equal_exact(gpu_pairs(km), ref, out_perm=p2, in_perm=p1)
+
+
+def test_async_map_matches_sync():
+    coords = WL.random_coords(83, 6000, 3, -15, 15, batch=3)
+    c = _t(coords)
+    table = gsc.gsc_coords_build(c, sync=False)
+    gsc.gsc_table_status(table)
+    offs = regions.hypercube(3, 3)
+    ks = gsc.gsc_kernel_map(table, c, offs)
+    ka = gsc.gsc_kernel_map(table, c, offs, sync=False)
+    assert ka.n_pairs is None and ka.count() == ks.n_pairs
+    for (a, b), (x, y) in zip(gpu_pairs(ka), gpu_pairs(ks)):
+        assert np.array_equal(a, x) and np.array_equal(b, y)
+    check_gidx(ka)
+
+
+def test_async_build_reports_duplicate_later():
+    c = _t(np.array([[0, 1, 2, 3], [0, 4, 5, 6], [0, 1, 2, 3]], np.int32))
+    table = gsc.gsc_coords_build(c, sync=False)        # enqueued only: no error yet
+    km = gsc.gsc_kernel_map(table, c, regions.hypercube(3, 3), sync=False)
+    assert km.count() == 0                             # a failed table yields an empty map
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_table_status(table)
+    assert e.value.code == gsc.GSC_EDUP
