@@ -60,6 +60,15 @@ __device__ __forceinline__ TIn w_at(const TIn* W, int w, int brow, int col, int 
     return W[((int64_t)w * ca + brow) * cb + col];
 }
 
+// Order the LDS accesses of one wave: a lane may read what another lane of
+// the same wave wrote just before.  The LDS executes a wave's operations in
+// order; this keeps the compiler from moving accesses across the point.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---------------------------------------------------------------------------
 // output-stationary gather -> MFMA -> LDS accumulate
 //   Y[sca[p]] += X[gat[p]] * B_w  for every pair p of segment k, w = sel(k)
@@ -263,6 +272,7 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
     float* acc = acc_all[wave];
     const int64_t row0 = g * RG;
     for (int i = lane; i < RG * AS; i += 64) acc[i] = 0.f;
+    wave_lds_sync();
 
     // per-offset table, one offset per lane
     int64_t lo = 0;
@@ -281,13 +291,10 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
     const int excl = incl - nit;
     const int total = __shfl(incl, 63, 64);
 
-    for (int item0 = 0; item0 < total; item0 += B) {
-        // 1. pair indices of the batch; every address is valid (lanes past the
-        //    end of a group re-read its last pair, items past the end repeat
-        //    the last item) and the invalid ones are masked later
-        int kb[B];
-        int32_t gr[B], sr[B];
-        bool ok[B];
+    // pair indices of the batch starting at item0; every address is valid
+    // (lanes past the end of a group re-read its last pair, items past the
+    // end repeat the last item) and the invalid ones are masked
+    auto fetch_idx = [&](int item0, int (&kb)[B], int32_t (&gr)[B], int32_t (&sr)[B], bool (&ok)[B]) {
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const int item = min(item0 + b, total - 1);
@@ -301,7 +308,13 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
             sr[b] = sca[p];
             ok[b] = item0 + b < total && pb < knp;
         }
-        // 2. rows and weights of the whole batch
+    };
+    int kb[B], kbn[B];
+    int32_t gr[B], sr[B], grn[B], srn[B];
+    bool ok[B], okn[B];
+    if (total > 0) fetch_idx(0, kb, gr, sr, ok);
+    for (int item0 = 0; item0 < total; item0 += B) {
+        // 1. rows and weights of the batch
         RowFrag<CA> a[B];
         float bfr[B][KS][NNB];
 #pragma unroll
@@ -309,14 +322,31 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
             ok[b] = ok[b] && gr[b] >= 0 && gr[b] < n_x && sr[b] >= row0 && sr[b] < row0 + RG;
             load_row_frag<CA>(X, ok[b] ? gr[b] : 0, q, ok[b], a[b]);
             const int w = sel(kb[b]);
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
+            if constexpr (WT) {
+                // W[w]^T: lane (r16, q) needs W[w][col][q*KS .. q*KS + KS), contiguous
 #pragma unroll
                 for (int nb = 0; nb < NNB; ++nb) {
-                    const int brow = q * KS + s, col = nb * 16 + r16;
-                    bfr[b][s][nb] = WT ? W[((int64_t)w * CB + col) * CA + brow] : W[((int64_t)w * CA + brow) * CB + col];
+                    const float4* src =
+                        reinterpret_cast<const float4*>(W + ((int64_t)w * CB + nb * 16 + r16) * CA + q * KS);
+#pragma unroll
+                    for (int i = 0; i < KS / 4; ++i) {
+                        const float4 t = src[i];
+                        bfr[b][4 * i + 0][nb] = t.x;
+                        bfr[b][4 * i + 1][nb] = t.y;
+                        bfr[b][4 * i + 2][nb] = t.z;
+                        bfr[b][4 * i + 3][nb] = t.w;
+                    }
                 }
+            } else {
+#pragma unroll
+                for (int s = 0; s < KS; ++s)
+#pragma unroll
+                    for (int nb = 0; nb < NNB; ++nb)
+                        bfr[b][s][nb] = W[((int64_t)w * CA + q * KS + s) * CB + nb * 16 + r16];
+            }
         }
+        // 2. next batch's indices in flight during this batch's MFMAs
+        if (item0 + B < total) fetch_idx(item0 + B, kbn, grn, srn, okn);
         // 3. group row of each MFMA output row (pair row 4q + j), -1 if none
         int lrow[B][4];
 #pragma unroll
@@ -337,6 +367,7 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
 #pragma unroll
                 for (int nb = 0; nb < NNB; ++nb)
                     d[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[b].v[s], bfr[b][s][nb], d[nb], 0, 0, 0);
+            wave_lds_sync();   // rows updated by other lanes for earlier items
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (lrow[b][j] >= 0) {
@@ -346,7 +377,15 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
                 }
             }
         }
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            kb[b] = kbn[b];
+            gr[b] = grn[b];
+            sr[b] = srn[b];
+            ok[b] = okn[b];
+        }
     }
+    wave_lds_sync();
     // 5. the group's rows, written once
     for (int i = lane; i < RG * CB; i += 64) {
         const int r = i / CB, cc = i - r * CB;
@@ -358,22 +397,19 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
 // ---------------------------------------------------------------------------
 // weight gradient
 // ---------------------------------------------------------------------------
-// Work items of the weight gradient.  Offset k's pairs are split into
-// nch_k = min(cap, ceil(|M_k| / min_chunk)) chunks of chunk[k] pairs (a
-// multiple of 64); ibase[k] = first item of offset k, ibase[K] = total.
-// Capping the chunks per offset keeps the second-level reduction short.
-__global__ void k_dw_items(const int64_t* seg, int K, int cap, int64_t min_chunk, int64_t* ibase, int64_t* chunk) {
+// Work items of the weight gradient: offset k's pairs are split into chunks
+// of `ch` pairs (the last one shorter); ibase[k] = first item of offset k,
+// ibase[K] = total.  Equal chunks keep the work items balanced whatever the
+// offsets' sizes (the centre offset of a submanifold map has one pair per
+// row, the others far fewer).
+__global__ void k_dw_items(const int64_t* seg, int K, int64_t ch, int64_t* ibase, int64_t* chunk) {
     if (blockIdx.x != 0 || threadIdx.x != 0) return;
     int64_t t = 0;
     for (int k = 0; k < K; ++k) {
         const int64_t n = seg[k + 1] - seg[k];
-        int64_t nch = n > 0 ? (n + min_chunk - 1) / min_chunk : 0;
-        if (nch > cap) nch = cap;
-        int64_t ch = nch > 0 ? (n + nch - 1) / nch : 0;
-        ch = (ch + 63) & ~(int64_t)63;
         ibase[k] = t;
         chunk[k] = ch;
-        t += nch;
+        t += n > 0 ? (n + ch - 1) / ch : 0;
     }
     ibase[K] = t;
 }
@@ -427,7 +463,9 @@ k_dw_partial(const TIn* __restrict__ X, int64_t n_in, const TIn* __restrict__ dY
     __shared__ float sh[4 * kDwTile * (kDwTile + 1)];
     int k;
     int64_t p_begin, p_end;
-    const int64_t item = xcd_unit(blockIdx.x, gridDim.x);
+    // the grid covers an upper bound of the items; order the real ones XCD-wise
+    if ((int64_t)blockIdx.x >= ibase[K]) return;
+    const int64_t item = xcd_unit(blockIdx.x, ibase[K]);
     if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
     const int ntj = (co + kDwTile - 1) / kDwTile;
     const int ci0 = (blockIdx.y / ntj) * kDwTile, co0 = (blockIdx.y % ntj) * kDwTile;
@@ -506,56 +544,106 @@ k_dw_partial(const TIn* __restrict__ X, int64_t n_in, const TIn* __restrict__ dY
 }
 
 // fp32 weight gradient for CI x CO <= 64 x 64 (multiples of 16).  Each wave
-// takes 64 consecutive pairs at a time: the 64 index pairs are read with one
-// coalesced load per lane and redistributed with shuffles, then all 16 MFMA
-// steps' row fragments are loaded before the MFMAs run.
+// stages 32 pairs at a time in a private LDS buffer: lane l loads half a row
+// of X[in_idx] and of dY[out_idx] for pair l % 32 with 16-byte loads (all
+// addresses valid: pairs past the chunk are clamped and their dY half-rows
+// zeroed by a select), then eight 16x16x4 MFMA steps reduce the 32 pairs,
+// reading A = X rows and B = dY rows from LDS.
+constexpr int kDwStage = 32;
+
+// Row halves of the 32-pair sub-chunk at p0: lane (pr, half) loads half of
+// X[in_idx[p0 + pr]] and of dY[out_idx[p0 + pr]].  Every address is valid
+// (pairs past the chunk are clamped) and their dY half-rows are zeroed.
+template <int CI, int CO>
+struct DwRows {
+    float4 x[CI / 8];
+    float4 y[CO / 8];
+};
+
+template <int CI, int CO>
+__device__ __forceinline__ DwRows<CI, CO> dw_fetch(const float* __restrict__ X, const float* __restrict__ dY,
+                                                   const int32_t* __restrict__ in_idx,
+                                                   const int32_t* __restrict__ out_idx, int64_t n_in, int64_t n_out,
+                                                   int64_t p0, int64_t p_end, int pr, int half) {
+    DwRows<CI, CO> r;
+    const int64_t p = min(p0 + pr, p_end - 1);
+    int32_t g = in_idx[p], sidx = out_idx[p];
+    const bool v = p0 + pr < p_end && g >= 0 && g < n_in && sidx >= 0 && sidx < n_out;
+    g = v ? g : 0;
+    sidx = v ? sidx : 0;
+    const float4* xr = reinterpret_cast<const float4*>(X + (int64_t)g * CI + half * (CI / 2));
+    const float4* yr = reinterpret_cast<const float4*>(dY + (int64_t)sidx * CO + half * (CO / 2));
+#pragma unroll
+    for (int i = 0; i < CI / 8; ++i) r.x[i] = xr[i];
+#pragma unroll
+    for (int i = 0; i < CO / 8; ++i) {
+        const float4 t = yr[i];
+        r.y[i] = v ? t : float4{0.f, 0.f, 0.f, 0.f};
+    }
+    return r;
+}
+
 template <int CI, int CO>
 __global__ void __launch_bounds__(kThreads)
 k_dw_f32(const float* __restrict__ X, int64_t n_in, const float* __restrict__ dY, int64_t n_out,
          const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx, const int64_t* __restrict__ seg,
          const int64_t* __restrict__ ibase, const int64_t* __restrict__ chunk, int K, float* __restrict__ part) {
     constexpr int NA = CI / 16, NB = CO / 16;
-    __shared__ float sh[4 * CI * (CO + 1)];
+    constexpr int XS = CI + 4, YS = CO + 4;            // row strides (16-byte aligned rows)
+    constexpr int STAGE = kDwStage * (XS + YS);
+    constexpr int RED = CI * (CO + 1);
+    constexpr int SH = (STAGE > RED ? STAGE : RED) * (kThreads / 64);
+    __shared__ __attribute__((aligned(16))) float sh[SH];
     int k;
     int64_t p_begin, p_end;
-    const int64_t item = xcd_unit(blockIdx.x, gridDim.x);
+    // the grid covers an upper bound of the items; order the real ones XCD-wise
+    if ((int64_t)blockIdx.x >= ibase[K]) return;
+    const int64_t item = xcd_unit(blockIdx.x, ibase[K]);
     if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, q = lane >> 4;
+    float* xs = sh + wave * STAGE;
+    float* ys = xs + kDwStage * XS;
     floatx4 d[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b) d[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    for (int64_t p0 = p_begin + 64 * wave; p0 < p_end; p0 += 256) {
-        const int64_t p = p0 + lane;
-        int32_t g = p < p_end ? in_idx[p] : -1;
-        int32_t s = p < p_end ? out_idx[p] : -1;
-        if (g < 0 || g >= n_in || s < 0 || s >= n_out) g = s = -1;
-        float xa[16][NA], yb[16][NB];
+    const int pr = lane % kDwStage, half = lane / kDwStage;
+    constexpr int64_t kStep = kDwStage * (kThreads / 64);
+    int64_t p0 = p_begin + kDwStage * wave;
+    for (; p0 < p_end; p0 += kStep) {
+        const DwRows<CI, CO> rows = dw_fetch<CI, CO>(X, dY, in_idx, out_idx, n_in, n_out, p0, p_end, pr, half);
+        float4* xw = reinterpret_cast<float4*>(xs + pr * XS + half * (CI / 2));
+        float4* yw = reinterpret_cast<float4*>(ys + pr * YS + half * (CO / 2));
 #pragma unroll
-        for (int t = 0; t < 16; ++t) {
-            const int32_t gg = __shfl(g, 4 * t + q, 64);
-            const int32_t ss = __shfl(s, 4 * t + q, 64);
+        for (int i = 0; i < CI / 8; ++i) xw[i] = rows.x[i];
 #pragma unroll
-            for (int a = 0; a < NA; ++a) xa[t][a] = gg >= 0 ? X[(int64_t)gg * CI + 16 * a + r16] : 0.f;
+        for (int i = 0; i < CO / 8; ++i) yw[i] = rows.y[i];
+        wave_lds_sync();   // lanes read rows other lanes of the wave staged
 #pragma unroll
-            for (int b = 0; b < NB; ++b) yb[t][b] = ss >= 0 ? dY[(int64_t)ss * CO + 16 * b + r16] : 0.f;
-        }
+        for (int t = 0; t < kDwStage / 4; ++t) {
+            const int row = 4 * t + q;
+            float xa[NA], yb[NB];
 #pragma unroll
-        for (int t = 0; t < 16; ++t)
+            for (int a = 0; a < NA; ++a) xa[a] = xs[row * XS + 16 * a + r16];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) yb[b] = ys[row * YS + 16 * b + r16];
 #pragma unroll
             for (int a = 0; a < NA; ++a)
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
-                    d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[t][a], yb[t][b], d[a][b], 0, 0, 0);
+                    d[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[a], yb[b], d[a][b], 0, 0, 0);
+        }
+        wave_lds_sync();   // the next stage overwrites rows other lanes just read
     }
+    __syncthreads();   // staging buffers are reused for the partial sums
     dw_store_partial<CI, CO>(sh, d, NA, NB, wave, q, r16, CI, CO, part + item * CI * (int64_t)CO, CO);
 }
 
-// dW[k] = sum of offset k's partials in item order.  A block covers 64
-// elements of one offset; its four waves add every fourth partial, then the
-// four sums are combined in wave order.
+// dW[k] = sum of offset k's partials in a fixed order.  A block covers 64
+// elements of one offset; wave w adds partials w, w + 4, w + 8, ... with
+// eight loads in flight, and the four wave sums are combined in wave order.
 __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict__ part, const int64_t* __restrict__ ibase,
                                                         int ci, int co, float* __restrict__ dW) {
     __shared__ float sh[4][64];
@@ -564,9 +652,21 @@ __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict_
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t e = (int64_t)blockIdx.x * 64 + lane;
     const int64_t i0 = ibase[k], i1 = ibase[k + 1];
+    const int64_t ee = e < cc ? e : 0;
+    float acc8[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc8[u] = 0.f;
+    for (int64_t it = i0 + wave; it < i1; it += 32) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t i = it + 4 * u;
+            const float v = part[(i < i1 ? i : i0) * cc + ee];
+            acc8[u] += i < i1 ? v : 0.f;
+        }
+    }
     float v = 0.f;
-    if (e < cc)
-        for (int64_t it = i0 + wave; it < i1; it += 4) v += part[it * cc + e];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += acc8[u];
     sh[wave][lane] = v;
     __syncthreads();
     if (wave == 0 && e < cc) dW[(int64_t)k * cc + e] = ((sh[0][lane] + sh[1][lane]) + sh[2][lane]) + sh[3][lane];
@@ -574,13 +674,15 @@ __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict_
 
 static int dw_tiles(int ci, int co) { return ((ci + kDwTile - 1) / kDwTile) * ((co + kDwTile - 1) / kDwTile); }
 
-// chunks per offset: enough items to fill the GPU, few enough partials to add
-static int dw_cap(int ci, int co, int K) {
-    int cap = 2048 / (K * dw_tiles(ci, co));
-    return cap < 2 ? 2 : (cap > 32 ? 32 : cap);
+// pairs per dW work item: 1024 for one output tile, more for wide layers so
+// that the number of partial tiles stays moderate
+static int64_t dw_chunk(int ci, int co) {
+    const int t = dw_tiles(ci, co);
+    return t <= 1 ? 1024 : (t <= 4 ? 2048 : 8192);
 }
 
-constexpr int64_t kDwMinChunk = 256;
+// upper bound of the work items for at most n_pairs pairs
+static int64_t dw_items_bound(int64_t n_pairs, int K, int64_t ch) { return (n_pairs + ch - 1) / ch + K; }
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
@@ -664,7 +766,7 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
 
 size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K) {
     if (n_pairs < 0 || c_in < 1 || c_out < 1 || K < 1) return 0;
-    const int64_t items = (int64_t)K * dw_cap(c_in, c_out, K);
+    const int64_t items = dw_items_bound(n_pairs, K, dw_chunk(c_in, c_out));
     return 2 * al256((size_t)(K + 1) * sizeof(int64_t)) + al256((size_t)items * c_in * c_out * sizeof(float)) + 256;
 }
 
@@ -706,13 +808,13 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         if (n_pairs > 0 && (!X || !dY || !in_idx || !out_idx)) return fail(GSC_EINVAL, "conv_bwd: null X/dY/idx");
         const size_t need = gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K);
         if (ws_bytes < need) return fail(GSC_ESHORT, "conv_bwd: ws needs %zu bytes, got %zu", need, ws_bytes);
-        const int cap = dw_cap(c_in, c_out, K);
-        const int64_t items = (int64_t)K * cap;
+        const int64_t ch = dw_chunk(c_in, c_out);
+        const int64_t items = dw_items_bound(n_pairs, K, ch);
         char* w = reinterpret_cast<char*>(ws);
         int64_t* ibase = reinterpret_cast<int64_t*>(w);
         int64_t* chunk = reinterpret_cast<int64_t*>(w + al256((size_t)(K + 1) * sizeof(int64_t)));
         float* part = reinterpret_cast<float*>(w + 2 * al256((size_t)(K + 1) * sizeof(int64_t)));
-        hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, cap, kDwMinChunk, ibase, chunk);
+        hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, ch, ibase, chunk);
         GSC_LAUNCH_CHECK();
         if (dtype == GSC_F32 && dw_f32_specialised(c_in, c_out)) {
             auto X32 = reinterpret_cast<const float*>(X);

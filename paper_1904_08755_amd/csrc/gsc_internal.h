@@ -79,14 +79,19 @@ inline __host__ __device__ const Slot* table_slots(const void* t) {
     return reinterpret_cast<const Slot*>(reinterpret_cast<const char*>(t) + kHeaderBytes);
 }
 
-// 64-bit finaliser of MurmurHash3 (Appleby): a bijective avalanche mix.
-__device__ __forceinline__ unsigned long long mix64(unsigned long long k) {
-    k ^= k >> 33;
-    k *= 0xff51afd7ed558ccdull;
-    k ^= k >> 33;
-    k *= 0xc4ceb9fe1a85ec53ull;
-    k ^= k >> 33;
-    return k;
+// 32-bit finaliser of MurmurHash3 (Appleby): a bijective avalanche mix.
+__device__ __forceinline__ uint32_t fmix32(uint32_t h) {
+    h ^= h >> 16;
+    h *= 0x85ebca6bu;
+    h ^= h >> 13;
+    h *= 0xc2b2ae35u;
+    h ^= h >> 16;
+    return h;
+}
+
+// Hash of a (<= 62-bit) key: fold the high word in with a multiply, then mix.
+__device__ __forceinline__ uint32_t hash_key(unsigned long long k) {
+    return fmix32((uint32_t)k ^ ((uint32_t)(k >> 32) * 0x9e3779b1u));
 }
 
 // Pack a coordinate (already offset, in 64-bit) into a key.  Returns false if
@@ -118,7 +123,7 @@ __device__ __forceinline__ unsigned long long home_slot(const TableHeader* h, un
         local |= ((key >> sh) & 1ull) << i;
         bkey &= ~(1ull << sh);
     }
-    return ((mix64(bkey) << nb) | local) & mask;
+    return (((unsigned long long)hash_key(bkey) << nb) | local) & mask;
 }
 
 // Linear-probing lookup from slot s; at most `capacity` probes, so it ends

@@ -64,11 +64,22 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
     const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     const bool valid = ok && j < n_out;
-    int64_t u[kMaxCols];
-    for (int c = 0; c < ncol; ++c) u[c] = valid ? out_coords[j * ncol + c] : 0;
+    const int D = ncol - 1;
+    // The packed key is linear in the coordinate: key(u + o) = base(u) + delta(o)
+    // (mod 2^64) whenever every column of u + o lies in the table's box, so each
+    // probe costs a range check and one add.  base may be "negative" when u
+    // itself is outside the box; the sum is still exact for in-box queries.
+    int32_t ub[kMaxCols], lo_c[kMaxCols], hi_c[kMaxCols];
+    long long base = 0;
+    for (int c = 0; c < ncol; ++c) {
+        lo_c[c] = h->lo[c];
+        hi_c[c] = h->hi[c];
+        ub[c] = valid ? out_coords[j * ncol + c] : 0;
+        base += (long long)((unsigned long long)((int64_t)ub[c] - lo_c[c]) << h->shift[c]);
+    }
+    const bool batch_ok = valid && ub[0] >= lo_c[0] && ub[0] <= hi_c[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    const int D = ncol - 1;
     uint32_t word = 0;
     for (int k0 = 0; k0 < K; k0 += kBatch) {
         unsigned long long key[kBatch], pos[kBatch];
@@ -76,8 +87,19 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
             const int k = k0 + b;
-            pend[b] = valid && k < K && query_key(h, ncol, u, offs.at((int64_t)k * D), &key[b]);
-            pos[b] = pend[b] ? home_slot(h, key[b], mask) : 0;
+            bool in = batch_ok && k < K;
+            long long delta = 0;
+            if (k < K) {
+                const int32_t* o = offs.at((int64_t)k * D);
+                for (int c = 1; c < ncol; ++c) {
+                    const int32_t v = ub[c] + o[c - 1];
+                    in = in && v >= lo_c[c] && v <= hi_c[c];
+                    delta += (long long)((unsigned long long)(long long)o[c - 1] << h->shift[c]);
+                }
+            }
+            key[b] = (unsigned long long)(base + delta);
+            pend[b] = in;
+            pos[b] = in ? home_slot(h, key[b], mask) : 0;
             hit[b] = false;
         }
         for (unsigned long long round = 0; round <= mask; ++round) {
@@ -141,7 +163,8 @@ __global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, in
 
 // Resolve pass: one lane per pair probes u_j + o_k (a guaranteed hit).  The
 // pair count is read on the device (gidx[K*G]), so the grid only has to cover
-// an upper bound; lanes stride over it.
+// an upper bound; lanes stride over it (in plain block order, which spreads
+// the real pairs over all XCDs whatever the bound).
 template <typename Offs>
 __global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, const int32_t* out_coords, int ncol,
                                                            Offs offs, const int64_t* total, int32_t* in_idx,
@@ -151,7 +174,7 @@ __global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, co
     const unsigned long long mask = (unsigned long long)h->capacity - 1;
     const int64_t n_pairs = *total;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t p = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x; p < n_pairs; p += stride) {
+    for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < n_pairs; p += stride) {
         const int64_t j = out_idx[p];
         const int k = in_idx[p];
         int64_t u[kMaxCols];
