@@ -21,9 +21,10 @@ struct StrideArg {
 
 __device__ __forceinline__ void load_row(const int32_t* coords, int64_t r, int ncol, const StrideArg& st,
                                          int64_t* v) {
-    for (int c = 0; c < ncol; ++c) {
-        int64_t x = coords[r * ncol + c];
-        if (st.on && c > 0) x = floor_mul(x, st.s[c]);
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c) {
+        int64_t x = c < ncol ? coords[r * ncol + c] : 0;
+        if (st.on && c > 0 && c < ncol) x = floor_mul(x, st.s[c]);
         v[c] = x;
     }
 }
@@ -150,16 +151,17 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
     if (r >= n) return;
     if (h->status & ST_RANGE) return;
     const int ncol = h->ncol;
-    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    const TableView tv = table_view(h, ncol);
+    const unsigned long long mask = tv.sh.mask;
     int64_t v[kMaxCols];
     StrideArg none{};
     load_row(coords, r, ncol, none, v);
     unsigned long long key;
-    if (!pack_key(h, ncol, v, &key)) {  // cannot happen: the box holds every row
+    if (!pack_key(tv, v, &key)) {  // cannot happen: the box holds every row
         atomicOr(&h->status, ST_RANGE);
         return;
     }
-    unsigned long long s = home_slot(h, key, mask);
+    unsigned long long s = home_slot(tv.sh, key);
     for (unsigned long long i = 0; i <= mask; ++i) {
         unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
         if (prev == kEmptyKey) {

@@ -110,20 +110,77 @@ __device__ __forceinline__ bool pack_key(const TableHeader* h, int ncol, const i
 
 // Home slot of a key.  The lowest varying bit of each of the first (up to)
 // three spatial columns (bit 0 for unit tensor stride, bit 1 for coordinates
-// that are all even, ...) selects the slot inside an aligned group of 2^nblk slots
-// and the rest of the key is hashed to pick the group, so the 2 x 2 x 2 block
-// of coordinates around a point shares one 128-byte line of the table and a
-// 3 x 3 x 3 neighbourhood touches about 8 lines instead of 27.
+// that are all even, ...) selects the slot inside an aligned group of 2^nblk
+// slots and the rest of the key is hashed to pick the group, so the 2 x 2 x 2
+// block of coordinates around a point shares one 128-byte line of the table
+// and a 3 x 3 x 3 neighbourhood touches about 8 lines instead of 27.
+struct SlotHash {
+    unsigned long long mask;   // capacity - 1
+    int nblk;
+    int blk_shift[3];
+};
+
+__device__ __forceinline__ SlotHash slot_hash(const TableHeader* h) {
+    SlotHash sh;
+    sh.mask = (unsigned long long)h->capacity - 1;
+    sh.nblk = h->nblk;
+    for (int i = 0; i < 3; ++i) sh.blk_shift[i] = h->blk_shift[i];
+    return sh;
+}
+
+__device__ __forceinline__ unsigned long long home_slot(const SlotHash& sh, unsigned long long key) {
+    unsigned long long local = 0, bkey = key;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        if (i < sh.nblk) {
+            local |= ((key >> sh.blk_shift[i]) & 1ull) << i;
+            bkey &= ~(1ull << sh.blk_shift[i]);
+        }
+    }
+    return (((unsigned long long)hash_key(bkey) << sh.nblk) | local) & sh.mask;
+}
+
 __device__ __forceinline__ unsigned long long home_slot(const TableHeader* h, unsigned long long key,
                                                         unsigned long long mask) {
-    unsigned long long local = 0, bkey = key;
-    const int nb = h->nblk;
-    for (int i = 0; i < nb; ++i) {
-        const int sh = h->blk_shift[i];
-        local |= ((key >> sh) & 1ull) << i;
-        bkey &= ~(1ull << sh);
+    SlotHash sh = slot_hash(h);
+    sh.mask = mask;
+    return home_slot(sh, key);
+}
+
+// Register copy of the fields a query needs: loaded once per thread, so that
+// stores made between queries (which may alias the table for the compiler)
+// do not force the header to be read again.
+struct TableView {
+    SlotHash sh;
+    int ncol;
+    int32_t lo[kMaxCols], hi[kMaxCols], shift[kMaxCols];
+};
+
+__device__ __forceinline__ TableView table_view(const TableHeader* h, int ncol) {
+    TableView t;
+    t.sh = slot_hash(h);
+    t.ncol = ncol;
+    for (int c = 0; c < kMaxCols; ++c) {
+        t.lo[c] = c < ncol ? h->lo[c] : 0;
+        t.hi[c] = c < ncol ? h->hi[c] : 0;
+        t.shift[c] = c < ncol ? h->shift[c] : 0;
     }
-    return (((unsigned long long)hash_key(bkey) << nb) | local) & mask;
+    return t;
+}
+
+// (unrolled over kMaxCols with a guard, so the arrays stay in registers)
+__device__ __forceinline__ bool pack_key(const TableView& t, const int64_t* v, unsigned long long* key) {
+    unsigned long long k = 0;
+    bool in = true;
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c) {
+        if (c < t.ncol) {
+            in = in && v[c] >= t.lo[c] && v[c] <= t.hi[c];
+            k |= (unsigned long long)(v[c] - t.lo[c]) << t.shift[c];
+        }
+    }
+    *key = k;
+    return in;
 }
 
 // Linear-probing lookup from slot s; at most `capacity` probes, so it ends
@@ -142,6 +199,10 @@ __device__ __forceinline__ int32_t table_find_from(const Slot* slots, unsigned l
 __device__ __forceinline__ int32_t table_find(const TableHeader* h, const Slot* slots, unsigned long long mask,
                                               unsigned long long key) {
     return table_find_from(slots, mask, key, home_slot(h, key, mask));
+}
+
+__device__ __forceinline__ int32_t table_find(const TableView& t, const Slot* slots, unsigned long long key) {
+    return table_find_from(slots, t.sh.mask, key, home_slot(t.sh, key));
 }
 
 // floor(a / s) * s for s > 0

@@ -47,81 +47,121 @@ __device__ __forceinline__ bool query_key(const TableHeader* h, int ncol, const 
 
 constexpr int kBatch = 8;   // probes issued together per lane in the count pass
 
+// Key arithmetic in KeyT (uint32_t when the table's keys fit in 32 bits, the
+// usual case, else uint64_t).  The packed key is linear in the coordinate:
+// key(u + o) = base(u) + delta(o), exact (mod 2^bits) whenever every column of
+// u + o lies in the table's box, so a probe is a range check per column and
+// one add.
+template <typename KeyT>
+struct KeyOps;
+
+template <>
+struct KeyOps<uint32_t> {
+    static __device__ __forceinline__ uint32_t hash(uint32_t k) { return fmix32(k); }
+    static __device__ __forceinline__ bool eq(unsigned long long slot_key, uint32_t k) {
+        return slot_key == (unsigned long long)k;
+    }
+};
+template <>
+struct KeyOps<unsigned long long> {
+    static __device__ __forceinline__ uint32_t hash(unsigned long long k) { return hash_key(k); }
+    static __device__ __forceinline__ bool eq(unsigned long long slot_key, unsigned long long k) { return slot_key == k; }
+};
+
 // Count pass.  Each lane owns one output row.  Offsets are probed kBatch at a
-// time and collision chains are followed in rounds: every round issues the
-// next slot load of all unresolved probes of the batch together, so the
-// loads of a round are in flight at once.  Hits are recorded in a bit mask per
-// row (word w of row j at hits[w * n_out + j]) and counted per 64-row group
-// with a wave ballot.
-template <typename Offs>
-__global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* out_coords, int64_t n_out,
-                                                         int ncol, Offs offs, int K, int64_t G, int32_t* cnt,
-                                                         uint32_t* hits, int64_t* err) {
-    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    const Slot* slots = table_slots(table);
-    const bool ok = header_ok(h, ncol);
-    if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
-    const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
-    const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+// time; every load is issued unconditionally (a lane whose query is out of
+// the box reads slot 0 and ignores it) so the kBatch loads are in flight
+// together, and collision chains are followed in rounds.  Hits are recorded
+// in a bit mask per row (word w of row j at hits[w * n_out + j]) and counted
+// per 64-row group with a wave ballot.
+template <typename KeyT, typename Offs>
+__device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __restrict__ slots,
+                                           const int32_t* __restrict__ out_coords, int64_t n_out, int ncol,
+                                           const Offs& offs, int K, int64_t G, int32_t* __restrict__ cnt,
+                                           uint32_t* __restrict__ hits, bool ok, int64_t j) {
     const bool valid = ok && j < n_out;
     const int D = ncol - 1;
-    // The packed key is linear in the coordinate: key(u + o) = base(u) + delta(o)
-    // (mod 2^64) whenever every column of u + o lies in the table's box, so each
-    // probe costs a range check and one add.  base may be "negative" when u
-    // itself is outside the box; the sum is still exact for in-box queries.
-    int32_t ub[kMaxCols], lo_c[kMaxCols], hi_c[kMaxCols];
-    long long base = 0;
-    for (int c = 0; c < ncol; ++c) {
-        lo_c[c] = h->lo[c];
-        hi_c[c] = h->hi[c];
-        ub[c] = valid ? out_coords[j * ncol + c] : 0;
-        base += (long long)((unsigned long long)((int64_t)ub[c] - lo_c[c]) << h->shift[c]);
+    const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
+    const int nblk = h->nblk;
+    KeyT clear = ~(KeyT)0;
+    int bsh[3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        bsh[i] = h->blk_shift[i];
+        if (i < nblk) clear &= ~((KeyT)1 << bsh[i]);
     }
-    const bool batch_ok = valid && ub[0] >= lo_c[0] && ub[0] <= hi_c[0];
+    int32_t rel[kMaxCols], span[kMaxCols], shc[kMaxCols];
+    KeyT base = 0;
+    bool in_b = valid;
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c) {
+        if (c < ncol) {
+            const int32_t lo = h->lo[c];
+            shc[c] = h->shift[c];
+            span[c] = h->hi[c] - lo;
+            rel[c] = (valid ? out_coords[j * ncol + c] : lo) - lo;
+            base += (KeyT)(uint32_t)rel[c] << shc[c];    // (KeyT)(int) sign-extends for 64-bit keys below
+        }
+    }
+    if (sizeof(KeyT) == 8) {   // redo with sign extension: rel may be negative when u is outside the box
+        base = 0;
+#pragma unroll
+        for (int c = 0; c < kMaxCols; ++c)
+            if (c < ncol) base += (KeyT)(long long)rel[c] << shc[c];
+    }
+    in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
     uint32_t word = 0;
     for (int k0 = 0; k0 < K; k0 += kBatch) {
-        unsigned long long key[kBatch], pos[kBatch];
+        KeyT key[kBatch];
+        unsigned long long pos[kBatch];
         bool pend[kBatch], hit[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
-            const int k = k0 + b;
-            bool in = batch_ok && k < K;
-            long long delta = 0;
-            if (k < K) {
-                const int32_t* o = offs.at((int64_t)k * D);
-                for (int c = 1; c < ncol; ++c) {
-                    const int32_t v = ub[c] + o[c - 1];
-                    in = in && v >= lo_c[c] && v <= hi_c[c];
-                    delta += (long long)((unsigned long long)(long long)o[c - 1] << h->shift[c]);
+            const int k = min(k0 + b, K - 1);
+            const int32_t* o = offs.at((int64_t)k * D);
+            bool in = in_b && k0 + b < K;
+            KeyT delta = 0;
+#pragma unroll
+            for (int c = 1; c < kMaxCols; ++c) {
+                if (c < ncol) {
+                    in = in && (uint32_t)(rel[c] + o[c - 1]) <= (uint32_t)span[c];
+                    delta += (KeyT)(long long)o[c - 1] << shc[c];
                 }
             }
-            key[b] = (unsigned long long)(base + delta);
+            const KeyT kk = base + delta;
+            KeyT local = 0;
+#pragma unroll
+            for (int i = 0; i < 3; ++i)
+                if (i < nblk) local |= ((kk >> bsh[i]) & 1) << i;
+            const unsigned long long hs =
+                (((unsigned long long)KeyOps<KeyT>::hash(kk & clear) << nblk) | (unsigned long long)local) & mask;
+            key[b] = kk;
+            pos[b] = in ? hs : 0;
             pend[b] = in;
-            pos[b] = in ? home_slot(h, key[b], mask) : 0;
             hit[b] = false;
         }
         for (unsigned long long round = 0; round <= mask; ++round) {
+            unsigned long long ek[kBatch];
+            if (round == 0) {
+#pragma unroll
+                for (int b = 0; b < kBatch; ++b) ek[b] = slots[pos[b]].key;   // unconditional: all in flight
+            } else {   // collision chains: few probes still pending
+#pragma unroll
+                for (int b = 0; b < kBatch; ++b) ek[b] = pend[b] ? slots[pos[b]].key : kEmptyKey;
+            }
             bool any = false;
 #pragma unroll
-            for (int b = 0; b < kBatch; ++b) any |= pend[b];
-            if (!__any(any)) break;
-            unsigned long long ek[kBatch];
-#pragma unroll
-            for (int b = 0; b < kBatch; ++b) ek[b] = pend[b] ? slots[pos[b]].key : kEmptyKey;
-#pragma unroll
             for (int b = 0; b < kBatch; ++b) {
-                if (!pend[b]) continue;
-                if (ek[b] == key[b]) {
-                    hit[b] = true;
-                    pend[b] = false;
-                } else if (ek[b] == kEmptyKey) {
-                    pend[b] = false;
-                } else {
-                    pos[b] = (pos[b] + 1) & mask;
-                }
+                const bool h1 = pend[b] && KeyOps<KeyT>::eq(ek[b], key[b]);
+                const bool stop = h1 || ek[b] == kEmptyKey;
+                hit[b] = hit[b] || h1;
+                pend[b] = pend[b] && !stop;
+                pos[b] = pend[b] ? ((pos[b] + 1) & mask) : pos[b];
+                any = any || pend[b];
             }
+            if (!__any(any)) break;
         }
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
@@ -137,6 +177,22 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
             }
         }
     }
+}
+
+template <typename Offs>
+__global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* __restrict__ out_coords,
+                                                         int64_t n_out, int ncol, Offs offs, int K, int64_t G,
+                                                         int32_t* __restrict__ cnt, uint32_t* __restrict__ hits,
+                                                         int64_t* err) {
+    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
+    const Slot* __restrict__ slots = table_slots(table);
+    const bool ok = header_ok(h, ncol);
+    if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
+    const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+    if (h->total_bits <= 32)   // uniform: all lanes take the same path
+        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, hits, ok, j);
+    else
+        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, hits, ok, j);
 }
 
 // Fill pass: the ballots come from the hit masks; each hit gets its position
@@ -166,22 +222,26 @@ __global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, in
 // an upper bound; lanes stride over it (in plain block order, which spreads
 // the real pairs over all XCDs whatever the bound).
 template <typename Offs>
-__global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, const int32_t* out_coords, int ncol,
-                                                           Offs offs, const int64_t* total, int32_t* in_idx,
-                                                           const int32_t* out_idx) {
+__global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, const int32_t* __restrict__ out_coords,
+                                                           int ncol, Offs offs, const int64_t* total,
+                                                           int32_t* __restrict__ in_idx,
+                                                           const int32_t* __restrict__ out_idx) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    const Slot* slots = table_slots(table);
-    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    const Slot* __restrict__ slots = table_slots(table);
+    const TableView tv = table_view(h, ncol);
     const int64_t n_pairs = *total;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < n_pairs; p += stride) {
         const int64_t j = out_idx[p];
         const int k = in_idx[p];
-        int64_t u[kMaxCols];
-        for (int c = 0; c < ncol; ++c) u[c] = out_coords[j * ncol + c];
+        const int32_t* o = offs.at((int64_t)k * (ncol - 1));
+        int64_t q[kMaxCols];
+#pragma unroll
+        for (int c = 0; c < kMaxCols; ++c)
+            q[c] = c < ncol ? (int64_t)out_coords[j * ncol + c] + (c > 0 ? o[c - 1] : 0) : 0;
         unsigned long long key;
         int32_t r = -1;
-        if (query_key(h, ncol, u, offs.at((int64_t)k * (ncol - 1)), &key)) r = table_find(h, slots, mask, key);
+        if (pack_key(tv, q, &key)) r = table_find(tv, slots, key);
         in_idx[p] = r;
     }
 }
