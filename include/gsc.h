@@ -165,6 +165,12 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
 /* ------------------------------------------------------------------------ */
 /* a4 / a5. Convolution forward (Alg. 2), transposed convolution.           */
 /* ------------------------------------------------------------------------ */
+/* Workspace bytes for gsc_sparse_conv_fwd (0 when none is needed).  The
+ * bfloat16 engine for wide layers (c_in in {32, 64, 128, 256}, c_out in {64,
+ * 128, 256}, K <= 64) keeps a transposed copy of W there:
+ * K * c_in * c_out * 2 bytes. */
+size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t K);
+
 /* Y = 0; for every offset k and pair p of it: Y[out_idx[p]] += X[in_idx[p]] W[k].
  *
  * dtype GSC_F32: X, W, Y float32.  GSC_BF16: X, W bfloat16, accumulation in
@@ -173,13 +179,14 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
  * The map (in_idx, out_idx, seg, gidx, n_pairs) must be as gsc_kernel_map
  * produces it for n_out output rows: out_idx increasing within each offset
  * and gidx its 64-row group index.  The transposed convolution is this call on
- * the role-reversed map (see gsc_kernel_map).  Asynchronous; no workspace.
- * Errors: EINVAL, EHIP. */
+ * the role-reversed map (see gsc_kernel_map).  ws: gsc_conv_fwd_ws_bytes
+ * bytes of device memory (may be NULL when that is 0), contents not kept.
+ * Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in,
                         const void* W, int32_t c_out, int32_t K,
                         const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
                         const int64_t* gidx, int64_t n_pairs,
-                        void* Y, int64_t n_out, void* stream);
+                        void* Y, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* a6 / a7. Backward: dX and dW.                                             */

@@ -17,7 +17,8 @@
 // second kernel adds the partials of each offset in a fixed order.
 #include <climits>
 
-#include "gsc_internal.h"
+#include "conv_common.h"
+#include "conv_bf16.h"
 
 namespace gsc {
 
@@ -26,48 +27,7 @@ constexpr int kTileRows = 128;
 constexpr int kTileGroups = kTileRows / GSC_GROUP_ROWS;
 constexpr int kColSlice = 64;
 constexpr int kAccStride = kColSlice + 1;
-constexpr int kMaxKConv = 1024;
 constexpr int kDwTile = 64;
-
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef short shortx4 __attribute__((ext_vector_type(4)));
-
-struct WSel {
-    int16_t w[kMaxKConv];
-    __device__ __forceinline__ int operator()(int k) const { return w[k]; }
-};
-struct WIdentity {
-    __device__ __forceinline__ int operator()(int k) const { return k; }
-};
-
-__device__ __forceinline__ float to_f32(float v) { return v; }
-__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
-
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ void store_out(float* y, float v) { *y = v; }
-__device__ __forceinline__ void store_out(uint16_t* y, float v) { *y = f32_to_bf16_rne(v); }
-
-// B operand element: forward uses W[w] (ca x cb), the input gradient W[w]^T.
-template <typename TIn, bool WT>
-__device__ __forceinline__ TIn w_at(const TIn* W, int w, int brow, int col, int ca, int cb) {
-    if (WT) return W[((int64_t)w * cb + col) * ca + brow];
-    return W[((int64_t)w * ca + brow) * cb + col];
-}
-
-// Order the LDS accesses of one wave: a lane may read what another lane of
-// the same wave wrote just before.  The LDS executes a wave's operations in
-// order; this keeps the compiler from moving accesses across the point.
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 
 // ---------------------------------------------------------------------------
 // output-stationary gather -> MFMA -> LDS accumulate
@@ -414,21 +374,6 @@ __global__ void k_dw_items(const int64_t* seg, int K, int64_t ch, int64_t* ibase
     ibase[K] = t;
 }
 
-// offset and pair range of a work item
-__device__ __forceinline__ bool dw_item(const int64_t* ibase, const int64_t* chunk, const int64_t* seg, int K,
-                                        int64_t item, int* k_out, int64_t* p_begin, int64_t* p_end) {
-    if (item >= ibase[K]) return false;
-    int lo = 0, hi = K - 1;   // last k with ibase[k] <= item
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (ibase[mid] <= item) lo = mid; else hi = mid - 1;
-    }
-    *k_out = lo;
-    *p_begin = seg[lo] + (item - ibase[lo]) * chunk[lo];
-    *p_end = min(seg[lo + 1], *p_begin + chunk[lo]);
-    return true;
-}
-
 // Per-wave partial tiles are summed in wave order (deterministic), then stored.
 template <int R, int C>
 __device__ __forceinline__ void dw_store_partial(float* sh, const floatx4 (&d)[4][4], int na, int nbk, int wave,
@@ -678,7 +623,7 @@ static int dw_tiles(int ci, int co) { return ((ci + kDwTile - 1) / kDwTile) * ((
 // that the number of partial tiles stays moderate
 static int64_t dw_chunk(int ci, int co) {
     const int t = dw_tiles(ci, co);
-    return t <= 1 ? 1024 : (t <= 4 ? 2048 : 8192);
+    return t <= 1 ? 1024 : (t <= 4 ? 2048 : (t <= 16 ? 4096 : 8192));
 }
 
 // upper bound of the work items for at most n_pairs pairs
@@ -743,9 +688,19 @@ using namespace gsc;
 
 extern "C" {
 
+static bool fwd_uses_bf16_engine(int32_t dtype, int32_t c_in, int32_t c_out, int32_t K) {
+    return dtype == GSC_BF16 && conv_bf16_supported(c_in, c_out, K);
+}
+
+size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t K) {
+    if (c_in < 1 || c_out < 1 || K < 1) return 0;
+    return fwd_uses_bf16_engine(dtype, c_in, c_out, K) ? transpose_ws_bytes(K, c_in, c_out) : 0;
+}
+
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
                         int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
-                        const int64_t* gidx, int64_t n_pairs, void* Y, int64_t n_out, void* stream) {
+                        const int64_t* gidx, int64_t n_pairs, void* Y, int64_t n_out, void* ws, size_t ws_bytes,
+                        void* stream) {
     (void)seg;
     clear_error();
     if (dtype != GSC_F32 && dtype != GSC_BF16) return fail(GSC_EINVAL, "conv_fwd: unknown dtype %d", dtype);
@@ -756,10 +711,20 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
     if (n_pairs < 0) return fail(GSC_EINVAL, "conv_fwd: n_pairs < 0");
     if (n_out > 0 && (!Y || !gidx || !W)) return fail(GSC_EINVAL, "conv_fwd: null Y/gidx/W");
     if (n_pairs > 0 && (!X || !in_idx || !out_idx)) return fail(GSC_EINVAL, "conv_fwd: null X/in_idx/out_idx");
+    const size_t need = gsc_conv_fwd_ws_bytes(dtype, c_in, c_out, K);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(GSC_ESHORT, "conv_fwd: ws needs %zu bytes, got %zu", need, ws ? ws_bytes : (size_t)0);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (dtype == GSC_F32)
         return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, K, c_in, c_out, n_out, Y,
                                               WIdentity{}, s);
+    if (fwd_uses_bf16_engine(dtype, c_in, c_out, K)) {
+        if (n_out == 0) return GSC_OK;
+        int rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
+        if (rc) return rc;
+        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, nullptr, K, n_out, Y,
+                                    WIdentity{}, s);
+    }
     return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, K, c_in, c_out, n_out, Y,
                                                 WIdentity{}, s);
 }
@@ -795,11 +760,16 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                 return fail(GSC_EINVAL, "conv_bwd: t_wsel[%d]=%d outside [0,%d)", k, t_wsel[k], K);
             sel.w[k] = (int16_t)t_wsel[k];
         }
-        int rc = dtype == GSC_F32
-                     ? launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in, n_in,
-                                                     dX, sel, s)
-                     : launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in,
-                                                           n_in, dX, sel, s);
+        int rc;
+        if (dtype == GSC_F32)
+            rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in, n_in, dX,
+                                               sel, s);
+        else if (conv_bf16_supported(c_out, c_in, K))   // W[w] (c_in x c_out) is already the B layout of dY W^T
+            rc = conv_bf16<WSel>(c_out, c_in, dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, n_in, dX, sel,
+                                 s);
+        else
+            rc = launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in,
+                                                     n_in, dX, sel, s);
         if (rc) return rc;
     }
     if (dW) {
@@ -826,6 +796,9 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
             GSC_DW_CASE(16, 16) GSC_DW_CASE(16, 32) GSC_DW_CASE(16, 64) GSC_DW_CASE(32, 16) GSC_DW_CASE(32, 32)
             GSC_DW_CASE(32, 64) GSC_DW_CASE(64, 16) GSC_DW_CASE(64, 32) GSC_DW_CASE(64, 64)
 #undef GSC_DW_CASE
+        } else if (dtype == GSC_BF16 && dw_bf16_supported(c_in, c_out)) {
+            int rc = dw_bf16(c_in, c_out, X, n_in, dY, n_out, in_idx, out_idx, seg, ibase, chunk, K, items, part, s);
+            if (rc) return rc;
         } else {
             const unsigned tiles = (unsigned)dw_tiles(c_in, c_out);
             if (dtype == GSC_F32)

@@ -1,0 +1,392 @@
+// Large-channel bfloat16 convolution engine (inputs and weights in bfloat16,
+// accumulation in fp32): forward / transposed forward / input gradient
+// (Alg. 2 and its chain rule) and the weight gradient, on the 16 x 16 x 32
+// bf16 MFMA of CDNA4.
+//
+// Forward and input gradient (k_conv_bf16): output-stationary, like the fp32
+// engine, but sized for wide channels.  A workgroup of four waves owns a tile
+// of T output rows (T * C_out fp32 = 128 KiB of LDS) and every wave owns a
+// quarter of the columns.  The tile's work is a list of items (16 pairs of
+// one offset, pairs of one offset being sorted by output row); all four
+// waves walk the same list.  For an item a wave gathers the 16 input rows as
+// the MFMA A operand straight from global memory (each lane loads one
+// contiguous quarter of a row), multiplies them by its column slice of the
+// offset's weight (held in registers for as long as the offset lasts) and
+// adds the 16 result rows into the LDS tile.  The tile is rounded to bf16 and
+// written once.
+//
+// The B operand has to hold 8 consecutive reduction channels of one output
+// column per lane, so the kernel reads the weights as Bt[w][col][k]
+// (C_out x C_in per offset): the input gradient uses W[w] itself (W[w] is
+// C_in x C_out, i.e. already column-major for dX = dY W^T), the forward a
+// transposed copy made by k_transpose_w.
+//
+// Weight gradient (k_dw_bf16): split-K over the pairs of each offset.  The
+// reduction runs over pairs, so a workgroup stages 32 pairs' rows of X and
+// dY in LDS transposed (channel-major) and every lane then reads its 8
+// consecutive pairs of one channel with one 16-byte LDS load.
+#include "conv_common.h"
+#include "conv_bf16.h"
+
+namespace gsc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16_rne(lo) | ((uint32_t)f32_to_bf16_rne(hi) << 16);
+}
+
+constexpr int kBfThreads = 256;
+constexpr int kBfWaves = kBfThreads / 64;
+constexpr int kBfAccFloats = 32768;   // LDS accumulator: T rows x C_out columns of fp32
+
+template <int CA, int CB>
+struct BfShape {
+    static constexpr int T = kBfAccFloats / CB;      // output rows per tile (128 for C_out = 256)
+    static constexpr int TG = T / GSC_GROUP_ROWS;    // kernel-map groups per tile
+    static constexpr int AS = CB + 4;                // LDS row stride (floats)
+    static constexpr int CW = CB / kBfWaves;         // columns per wave
+    static constexpr int NB = CW / 16;               // 16-column MFMA blocks per wave
+    static constexpr int KS = CA / 32;               // MFMA steps over the reduction
+    static constexpr int QC = CA / 4;                // reduction channels per lane group
+    static_assert(CA % 32 == 0 && CB % 64 == 0 && NB >= 1, "unsupported shape");
+};
+
+// Bt[w][col][k] = W[w][k][col] for a K x rows x cols stack of bf16 matrices.
+__global__ void k_transpose_w(const uint16_t* __restrict__ W, int rows, int cols, int64_t total,
+                              uint16_t* __restrict__ Bt) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t rc = (int64_t)rows * cols;
+        const int64_t w = i / rc;
+        const int64_t e = i - w * rc;
+        const int64_t col = e / rows, k = e - col * rows;   // i walks Bt in order: coalesced writes
+        Bt[i] = W[w * rc + k * cols + col];
+    }
+}
+
+// Y[sca[p]] += X[gat[p]] * B_w for the pairs p of every offset, B_w[k][col] =
+// Bt[w][col][k], w = sel(offset).  gidx is the map's 64-row group index over
+// n_y output positions; when perm is given, position i is output row perm[i].
+template <int CA, int CB, typename Sel>
+__global__ void __launch_bounds__(kBfThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_conv_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __restrict__ Bt,
+            const int32_t* __restrict__ gat, const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx,
+            const int32_t* __restrict__ perm, int K, int64_t G, int64_t n_y, uint16_t* __restrict__ Y, Sel sel) {
+    using S = BfShape<CA, CB>;
+    __shared__ __attribute__((aligned(16))) float acc[S::T * S::AS];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, q = lane >> 4;
+    const int64_t tile = xcd_unit(blockIdx.x, gridDim.x);
+    const int64_t g0 = tile * S::TG;
+    const int64_t g1 = min(g0 + (int64_t)S::TG, G);
+    const int64_t row0 = g0 * GSC_GROUP_ROWS;
+    {
+        float4* a4 = reinterpret_cast<float4*>(acc);
+        for (int i = tid; i < S::T * S::AS / 4; i += kBfThreads) a4[i] = float4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    // lane k < K: first pair and pair count of offset k in this tile; items
+    // (16 pairs of one offset) are numbered offset by offset
+    int64_t lo = 0;
+    int np = 0;
+    if (lane < K) {
+        lo = gidx[(int64_t)lane * G + g0];
+        np = (int)(gidx[(int64_t)lane * G + g1] - lo);
+    }
+    const int nit = (np + 15) >> 4;
+    int incl = nit;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int u = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += u;
+    }
+    const int excl = incl - nit;
+    const int total = __shfl(incl, 63, 64);
+    __syncthreads();   // the tile is zero
+
+    const int colw = wave * S::CW;
+    // item -> its offset and the pair of this lane's row (clamped: every
+    // address stays valid; lanes past the offset's last pair are masked)
+    auto locate = [&](int item, int& k, int32_t& gr, int32_t& sr, bool& ok) {
+        k = __popcll(__ballot(incl <= item));
+        const int64_t klo = __shfl(lo, k, 64);
+        const int knp = __shfl(np, k, 64);
+        const int pb = (item - __shfl(excl, k, 64)) * 16 + r16;
+        const int64_t p = klo + min(pb, knp - 1);
+        gr = gat[p];
+        sr = sca[p];
+        ok = pb < knp;
+    };
+    auto load_a = [&](int32_t gr, bool ok, uint4 (&a)[S::KS]) {
+        const uint4* src = reinterpret_cast<const uint4*>(X + (int64_t)(ok ? gr : 0) * CA + q * S::QC);
+#pragma unroll
+        for (int s = 0; s < S::KS; ++s) a[s] = src[s];
+    };
+    auto load_b = [&](int w, uint4 (&b)[S::NB][S::KS]) {
+#pragma unroll
+        for (int nb = 0; nb < S::NB; ++nb) {
+            const uint4* src =
+                reinterpret_cast<const uint4*>(Bt + ((int64_t)w * CB + colw + nb * 16 + r16) * CA + q * S::QC);
+#pragma unroll
+            for (int s = 0; s < S::KS; ++s) b[nb][s] = src[s];
+        }
+    };
+
+    if (total > 0) {
+        int k_c, k_n = 0;
+        int32_t gr_c, sr_c, gr_n = 0, sr_n = 0;
+        bool ok_c, ok_n = false;
+        locate(0, k_c, gr_c, sr_c, ok_c);
+        if (total > 1) locate(1, k_n, gr_n, sr_n, ok_n);
+        uint4 bc[S::NB][S::KS], bn[S::NB][S::KS];
+        uint4 ac[S::KS], an[S::KS];
+        load_b(sel(k_c), bc);
+        ok_c = ok_c && gr_c >= 0 && gr_c < n_x;
+        load_a(gr_c, ok_c, ac);
+        for (int it = 0; it < total; ++it) {
+            const bool has_n = it + 1 < total;
+            const bool new_b = has_n && k_n != k_c;
+            // 1. the next item's rows (its indices arrived during this one's
+            //    predecessor) and, when its offset differs, its weights
+            if (has_n) {
+                ok_n = ok_n && gr_n >= 0 && gr_n < n_x;
+                load_a(gr_n, ok_n, an);
+            }
+            if (new_b) load_b(sel(k_n), bn);
+            // 2. indices of the item after next
+            int k_nn = 0;
+            int32_t gr_nn = 0, sr_nn = 0;
+            bool ok_nn = false;
+            if (it + 2 < total) locate(it + 2, k_nn, gr_nn, sr_nn, ok_nn);
+            // 3. 16 rows x CW columns of this item
+            floatx4 d[S::NB];
+#pragma unroll
+            for (int nb = 0; nb < S::NB; ++nb) d[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < S::KS; ++s)
+#pragma unroll
+                for (int nb = 0; nb < S::NB; ++nb)
+                    d[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ac[s]), as_bf16x8(bc[nb][s]), d[nb],
+                                                                    0, 0, 0);
+            // 4. add into the tile: D row 4q + j is the item's pair row 4q + j
+            const int64_t rel = (int64_t)sr_c - row0;
+            const int mine = (ok_c && rel >= 0 && rel < S::T) ? (int)rel : -1;
+            int lrow[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) lrow[j] = __shfl(mine, 4 * q + j, 64);
+            wave_lds_sync();   // rows this wave updated for earlier items
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (lrow[j] >= 0) {
+                    float* arow = acc + lrow[j] * S::AS + colw + r16;
+#pragma unroll
+                    for (int nb = 0; nb < S::NB; ++nb) arow[nb * 16] += d[nb][j];
+                }
+            }
+            // 5. rotate the pipeline
+#pragma unroll
+            for (int s = 0; s < S::KS; ++s) ac[s] = an[s];
+            if (new_b) {
+#pragma unroll
+                for (int nb = 0; nb < S::NB; ++nb)
+#pragma unroll
+                    for (int s = 0; s < S::KS; ++s) bc[nb][s] = bn[nb][s];
+            }
+            k_c = k_n;
+            gr_c = gr_n;
+            sr_c = sr_n;
+            ok_c = ok_n;
+            k_n = k_nn;
+            gr_n = gr_nn;
+            sr_n = sr_nn;
+            ok_n = ok_nn;
+        }
+    }
+    __syncthreads();
+    // the tile's rows, rounded to bf16 and written once (8 columns per lane)
+    constexpr int C8 = CB / 8;
+    for (int i = tid; i < S::T * C8; i += kBfThreads) {
+        const int r = i / C8, c8 = (i - r * C8) * 8;
+        const int64_t pos = row0 + r;
+        if (pos < n_y) {
+            const int64_t row = perm ? (int64_t)perm[pos] : pos;
+            const float4* a = reinterpret_cast<const float4*>(acc + r * S::AS + c8);
+            const float4 v0 = a[0], v1 = a[1];
+            uint4 o;
+            o.x = pack_bf16x2(v0.x, v0.y);
+            o.y = pack_bf16x2(v0.z, v0.w);
+            o.z = pack_bf16x2(v1.x, v1.y);
+            o.w = pack_bf16x2(v1.z, v1.w);
+            *reinterpret_cast<uint4*>(Y + row * CB + c8) = o;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// weight gradient: partial[item][CI][CO] = X[in]^T dY[out] over one chunk of
+// one offset's pairs, for one 128 x 128 tile of dW (grid.y = tile).
+// ---------------------------------------------------------------------------
+constexpr int kDwbTile = 128;
+constexpr int kDwbPairs = 32;                 // pairs per stage (one MFMA reduction step)
+constexpr int kDwbPS = kDwbPairs + 8;         // LDS stride of a channel row (bf16 elements)
+
+template <int CI, int CO>
+__global__ void __launch_bounds__(kBfThreads)
+k_dw_bf16(const uint16_t* __restrict__ X, int64_t n_in, const uint16_t* __restrict__ dY, int64_t n_out,
+          const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx, const int64_t* __restrict__ seg,
+          const int64_t* __restrict__ ibase, const int64_t* __restrict__ chunk, int K, float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t xt[kDwbTile * kDwbPS];
+    __shared__ __attribute__((aligned(16))) uint16_t yt[kDwbTile * kDwbPS];
+    if ((int64_t)blockIdx.x >= ibase[K]) return;
+    const int64_t item = xcd_unit(blockIdx.x, ibase[K]);
+    int k;
+    int64_t p_begin, p_end;
+    if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
+    constexpr int NTO = CO / kDwbTile;
+    const int ci0 = (blockIdx.y / NTO) * kDwbTile, co0 = (blockIdx.y % NTO) * kDwbTile;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, q = lane >> 4;
+    const int wi = wave >> 1, wo = wave & 1;   // 64 x 64 sub-tile of the wave
+
+    // staging map: thread -> pairs (2 pp2, 2 pp2 + 1), channels [8 cc, 8 cc + 8)
+    const int pp2 = tid & 15, cc = tid >> 4;
+    auto fetch = [&](int64_t p0, uint4 (&xr)[2], uint4 (&yr)[2]) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int64_t p = p0 + 2 * pp2 + h;
+            const int64_t pc = p < p_end ? p : p_end - 1;
+            int32_t g = in_idx[pc], s = out_idx[pc];
+            const bool v = p < p_end && g >= 0 && g < n_in && s >= 0 && s < n_out;
+            g = v ? g : 0;
+            s = v ? s : 0;
+            xr[h] = *reinterpret_cast<const uint4*>(X + (int64_t)g * CI + ci0 + 8 * cc);
+            const uint4 t = *reinterpret_cast<const uint4*>(dY + (int64_t)s * CO + co0 + 8 * cc);
+            yr[h] = v ? t : uint4{0u, 0u, 0u, 0u};   // a masked pair adds nothing
+        }
+    };
+    auto stage = [&](const uint4 (&xr)[2], const uint4 (&yr)[2]) {
+        const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&xr[0]);
+        const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&xr[1]);
+        const uint32_t* y0 = reinterpret_cast<const uint32_t*>(&yr[0]);
+        const uint32_t* y1 = reinterpret_cast<const uint32_t*>(&yr[1]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int sh = (e & 1) * 16;
+            const uint32_t xv = ((x0[e >> 1] >> sh) & 0xffffu) | (((x1[e >> 1] >> sh) & 0xffffu) << 16);
+            const uint32_t yv = ((y0[e >> 1] >> sh) & 0xffffu) | (((y1[e >> 1] >> sh) & 0xffffu) << 16);
+            *reinterpret_cast<uint32_t*>(xt + (8 * cc + e) * kDwbPS + 2 * pp2) = xv;
+            *reinterpret_cast<uint32_t*>(yt + (8 * cc + e) * kDwbPS + 2 * pp2) = yv;
+        }
+    };
+
+    floatx4 d[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) d[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    uint4 xr[2], yr[2];
+    fetch(p_begin, xr, yr);
+    for (int64_t p0 = p_begin; p0 < p_end; p0 += kDwbPairs) {
+        __syncthreads();   // the previous stage has been read
+        stage(xr, yr);
+        __syncthreads();
+        if (p0 + kDwbPairs < p_end) fetch(p0 + kDwbPairs, xr, yr);   // in flight during the MFMAs
+        uint4 av[4], bv[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+            av[a] = *reinterpret_cast<const uint4*>(xt + (wi * 64 + a * 16 + r16) * kDwbPS + 8 * q);
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            bv[b] = *reinterpret_cast<const uint4*>(yt + (wo * 64 + b * 16 + r16) * kDwbPS + 8 * q);
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                d[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[a]), as_bf16x8(bv[b]), d[a][b], 0, 0, 0);
+    }
+    // D[a][b] row 4q + j = input channel, column r16 = output channel
+    float* out = part + (item * CI + ci0 + wi * 64) * (int64_t)CO + co0 + wo * 64;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) out[(int64_t)(a * 16 + 4 * q + j) * CO + b * 16 + r16] = d[a][b][j];
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+bool conv_bf16_supported(int ca, int cb, int K) {
+    const bool a = ca == 32 || ca == 64 || ca == 128 || ca == 256;
+    const bool b = cb == 64 || cb == 128 || cb == 256;
+    return a && b && K <= 64;
+}
+
+size_t transpose_ws_bytes(int K, int rows, int cols) { return (size_t)K * rows * cols * sizeof(uint16_t); }
+
+int transpose_w_bf16(const void* W, int K, int rows, int cols, void* Bt, hipStream_t s) {
+    const int64_t total = (int64_t)K * rows * cols;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<const uint16_t*>(W),
+                       rows, cols, total, reinterpret_cast<uint16_t*>(Bt));
+    GSC_LAUNCH_CHECK();
+    return GSC_OK;
+}
+
+template <int CA, int CB, typename Sel>
+static void launch_bf16(const void* X, int64_t n_x, const void* Bt, const int32_t* gat, const int32_t* sca,
+                        const int64_t* gidx, const int32_t* perm, int K, int64_t G, int64_t n_y, void* Y, Sel sel,
+                        hipStream_t s) {
+    using S = BfShape<CA, CB>;
+    const int64_t tiles = (G + S::TG - 1) / S::TG;
+    hipLaunchKernelGGL((k_conv_bf16<CA, CB, Sel>), dim3((unsigned)tiles), dim3(kBfThreads), 0, s,
+                       reinterpret_cast<const uint16_t*>(X), n_x, reinterpret_cast<const uint16_t*>(Bt), gat, sca,
+                       gidx, perm, K, G, n_y, reinterpret_cast<uint16_t*>(Y), sel);
+}
+
+template <typename Sel>
+int conv_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const int32_t* gat, const int32_t* sca,
+              const int64_t* gidx, const int32_t* perm, int K, int64_t n_y, void* Y, Sel sel, hipStream_t s) {
+    if (n_y == 0) return GSC_OK;
+    const int64_t G = (n_y + GSC_GROUP_ROWS - 1) / GSC_GROUP_ROWS;
+#define GSC_BF_CASE(A, B)                                                                   \
+    if (ca == A && cb == B) {                                                               \
+        launch_bf16<A, B, Sel>(X, n_x, Bt, gat, sca, gidx, perm, K, G, n_y, Y, sel, s);     \
+        GSC_LAUNCH_CHECK();                                                                 \
+        return GSC_OK;                                                                      \
+    }
+    GSC_BF_CASE(32, 64) GSC_BF_CASE(64, 64) GSC_BF_CASE(128, 64) GSC_BF_CASE(256, 64)
+    GSC_BF_CASE(32, 128) GSC_BF_CASE(64, 128) GSC_BF_CASE(128, 128) GSC_BF_CASE(256, 128)
+    GSC_BF_CASE(32, 256) GSC_BF_CASE(64, 256) GSC_BF_CASE(128, 256) GSC_BF_CASE(256, 256)
+#undef GSC_BF_CASE
+    return fail(GSC_EINVAL, "conv_bf16: unsupported channels %d -> %d", ca, cb);
+}
+
+template int conv_bf16<WIdentity>(int, int, const void*, int64_t, const void*, const int32_t*, const int32_t*,
+                                  const int64_t*, const int32_t*, int, int64_t, void*, WIdentity, hipStream_t);
+template int conv_bf16<WSel>(int, int, const void*, int64_t, const void*, const int32_t*, const int32_t*,
+                             const int64_t*, const int32_t*, int, int64_t, void*, WSel, hipStream_t);
+
+bool dw_bf16_supported(int ci, int co) { return (ci == 128 || ci == 256) && (co == 128 || co == 256); }
+
+int dw_bf16(int ci, int co, const void* X, int64_t n_in, const void* dY, int64_t n_out, const int32_t* in_idx,
+            const int32_t* out_idx, const int64_t* seg, const int64_t* ibase, const int64_t* chunk, int K,
+            int64_t items, float* part, hipStream_t s) {
+    const unsigned tiles = (unsigned)((ci / kDwbTile) * (co / kDwbTile));
+#define GSC_DWB_CASE(A, B)                                                                                  \
+    if (ci == A && co == B) {                                                                               \
+        hipLaunchKernelGGL((k_dw_bf16<A, B>), dim3((unsigned)items, tiles), dim3(kBfThreads), 0, s,          \
+                           reinterpret_cast<const uint16_t*>(X), n_in, reinterpret_cast<const uint16_t*>(dY), n_out, \
+                           in_idx, out_idx, seg, ibase, chunk, K, part);                                    \
+        GSC_LAUNCH_CHECK();                                                                                 \
+        return GSC_OK;                                                                                      \
+    }
+    GSC_DWB_CASE(128, 128) GSC_DWB_CASE(128, 256) GSC_DWB_CASE(256, 128) GSC_DWB_CASE(256, 256)
+#undef GSC_DWB_CASE
+    return fail(GSC_EINVAL, "dw_bf16: unsupported channels %d x %d", ci, co);
+}
+
+}  // namespace gsc

@@ -1,0 +1,65 @@
+// Device helpers shared by the convolution kernels (conv.hip, conv_bf16.hip).
+#pragma once
+
+#include "gsc_internal.h"
+
+namespace gsc {
+
+constexpr int kMaxKConv = 1024;   // offsets per convolution call
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
+struct WSel {
+    int16_t w[kMaxKConv];
+    __device__ __forceinline__ int operator()(int k) const { return w[k]; }
+};
+struct WIdentity {
+    __device__ __forceinline__ int operator()(int k) const { return k; }
+};
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ void store_out(float* y, float v) { *y = v; }
+__device__ __forceinline__ void store_out(uint16_t* y, float v) { *y = f32_to_bf16_rne(v); }
+
+// B operand element: forward uses W[w] (ca x cb), the input gradient W[w]^T.
+template <typename TIn, bool WT>
+__device__ __forceinline__ TIn w_at(const TIn* W, int w, int brow, int col, int ca, int cb) {
+    if (WT) return W[((int64_t)w * cb + col) * ca + brow];
+    return W[((int64_t)w * ca + brow) * cb + col];
+}
+
+// Order the LDS accesses of one wave: a lane may read what another lane of
+// the same wave wrote just before.  The LDS executes a wave's operations in
+// order; this keeps the compiler from moving accesses across the point.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// offset and pair range of a work item
+__device__ __forceinline__ bool dw_item(const int64_t* ibase, const int64_t* chunk, const int64_t* seg, int K,
+                                        int64_t item, int* k_out, int64_t* p_begin, int64_t* p_end) {
+    if (item >= ibase[K]) return false;
+    int lo = 0, hi = K - 1;   // last k with ibase[k] <= item
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (ibase[mid] <= item) lo = mid; else hi = mid - 1;
+    }
+    *k_out = lo;
+    *p_begin = seg[lo] + (item - ibase[lo]) * chunk[lo];
+    *p_end = min(seg[lo + 1], *p_begin + chunk[lo]);
+    return true;
+}
+
+}  // namespace gsc

@@ -51,8 +51,9 @@ _SIGS = {
     "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
     "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
                                       _c_i64p, _vp, _sz, _vp]),
+    "gsc_conv_fwd_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp,
-                                           _i64, _vp]),
+                                           _i64, _vp, _sz, _vp]),
     "gsc_conv_bwd_ws_bytes": (_sz, [_i64, _i32, _i32, _i32]),
     "gsc_sparse_conv_bwd": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp,
                                            _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _i64, _vp, _sz, _vp]),
@@ -261,8 +262,12 @@ def _dt(t: torch.Tensor) -> int:
     raise ValueError(f"unsupported feature dtype {t.dtype}")
 
 
+def gsc_conv_fwd_ws_bytes(dtype: int, c_in: int, c_out: int, K: int) -> int:
+    return int(lib().gsc_conv_fwd_ws_bytes(dtype, c_in, c_out, K))
+
+
 def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out: Optional[int] = None,
-                        Y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                        Y: Optional[torch.Tensor] = None, stream=None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     dt = _dt(X)
     _need(X, X.dtype, "X", 2)
     _need(W, X.dtype, "W", 3)
@@ -275,9 +280,12 @@ def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out
     if Y is None:
         Y = torch.empty((n_out, co), dtype=X.dtype, device=X.device)
     _need(Y, X.dtype, "Y", 2)
+    need = gsc_conv_fwd_ws_bytes(dt, ci, co, K)
+    if ws is None and need > 0:
+        ws = _ws(need, X.device)
     _check(lib().gsc_sparse_conv_fwd(dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx),
                                      _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_bound, _ptr(Y),
-                                     n_out, _stream(stream)))
+                                     n_out, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
     return Y
 
 

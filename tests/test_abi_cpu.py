@@ -122,13 +122,19 @@ def test_kernel_map_validation(L):
 
 def test_conv_validation(L):
     fake = ctypes.c_void_p(0x1000)
-    fwd = lambda dt, ci, K, npairs=10: L.gsc_sparse_conv_fwd(dt, fake, 10, ci, fake, 4, K, fake, fake, fake, fake,
-                                                             npairs, fake, 10, None)
+    fwd = lambda dt, ci, K, npairs=10, co=4, ws=None, wsb=0: L.gsc_sparse_conv_fwd(
+        dt, fake, 10, ci, fake, co, K, fake, fake, fake, fake, npairs, fake, 10, ws, wsb, None)
     assert fwd(7, 4, 27) == gsc.GSC_EINVAL
     assert fwd(0, 0, 27) == gsc.GSC_EINVAL
     assert fwd(0, 4, 0) == gsc.GSC_EINVAL
     assert fwd(0, 4, 5000) == gsc.GSC_EINVAL
     assert fwd(0, 4, 27, -1) == gsc.GSC_EINVAL
+    # the bf16 engine for wide layers needs a workspace for the transposed weights
+    need = L.gsc_conv_fwd_ws_bytes(gsc.GSC_BF16, 256, 256, 27)
+    assert need == 27 * 256 * 256 * 2
+    assert L.gsc_conv_fwd_ws_bytes(gsc.GSC_F32, 256, 256, 27) == 0
+    assert fwd(gsc.GSC_BF16, 256, 27, co=256) == gsc.GSC_ESHORT
+    assert fwd(gsc.GSC_BF16, 256, 27, co=256, ws=fake, wsb=need - 1) == gsc.GSC_ESHORT
     sel = (ctypes.c_int32 * 2)(0, 2)   # 2 is out of range for K = 2
     rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, 10,
                                sel, fake, None, 10, None, 0, None)

@@ -212,6 +212,17 @@ def test_bf16_odd_channels():
     _conv_case(coords, 24, 40, regions.hypercube(3, 3), 76, dtype="bf16")
 
 
+@pytest.mark.parametrize("ci,co,region", [(256, 256, "cube2"), (128, 256, "cube3"), (256, 128, "cube2"),
+                                           (64, 128, "cube3"), (128, 64, "cube2"), (32, 256, "cube3")])
+def test_bf16_wide_channel_engine(ci, co, region):
+    # the MFMA engine for wide bf16 layers: forward, input gradient on the
+    # role-reversed map (non-symmetric regions included) and weight gradient
+    coords = WL.random_coords(90 + ci // 32 + co // 16, 2500, 3, -12, 12, batch=2)
+    offs = regions.hypercube(int(region[-1]), 3)
+    _say(f"[gpu] bf16 engine {ci}->{co} {region}")
+    _conv_case(coords, ci, co, offs, 91, dtype="bf16")
+
+
 def test_4d_hybrid_and_tesseract():
     coords = WL.random_coords(77, 3000, 4, -5, 5, batch=1)
     _conv_case(coords, 8, 8, regions.hybrid(3, 4), 77)
