@@ -84,6 +84,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row order (no tile plan)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB once (a copy of known size for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -108,7 +109,7 @@ def main():
     dw = pipeline.to_device(wl, "cuda")
     torch.cuda.synchronize()
 
-    plan0 = pipeline.StepPlan(dw)
+    plan0 = pipeline.StepPlan(dw, use_plan=not args.no_plan)
     for _ in range(args.warmup):
         plan0.run()
     gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
@@ -117,7 +118,7 @@ def main():
     log(f"warmup done ({args.warmup} steps)")
 
     steps_events = []
-    plan = pipeline.StepPlan(dw)
+    plan = pipeline.StepPlan(dw, use_plan=not args.no_plan)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -136,11 +137,12 @@ def main():
     sec = (t1 - t0) / args.steps
     log(f"timed {args.steps} steps: {sec * 1e3:.3f} ms/step")
 
-    stage = {"map": [], "fwd": [], "bwd": []}
+    stage = {"map": [], "plan": [], "fwd": [], "bwd": []}
     for ev in steps_events:
         d = dict(ev)
         stage["map"].append(d["start"].elapsed_time(d["map"]))
-        stage["fwd"].append(d["map"].elapsed_time(d["fwd"]))
+        stage["plan"].append(d["map"].elapsed_time(d["plan"]))
+        stage["fwd"].append(d["plan"].elapsed_time(d["fwd"]))
         stage["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
     ms = {k: float(np.mean(v)) for k, v in stage.items()}
 
@@ -155,11 +157,19 @@ def main():
     dom_bytes = fwd_bytes(pairs[0], n_out0, L0.c_in, L0.c_out, km0.K, s)
     dom_ms = ms["fwd"] if len(wl.layers) == 1 else None
     roof = None
-    if dom_ms:
+    if dom_ms and wl.dtype == "bf16":
+        # wide bf16 layer: the per-offset contractions on the MFMA units
+        dom_flops = 2.0 * pairs[0] * L0.c_in * L0.c_out
+        ach = dom_flops / (dom_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": "k_conv_bf16 (forward)", "flops_per_launch": int(dom_flops),
+                "bytes_per_launch": int(dom_bytes), "avg_launch_us": round(dom_ms * 1e3, 2)}
+    elif dom_ms:
         ach = dom_bytes / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "k_conv_os (forward)", "bytes_per_launch": int(dom_bytes),
+                "kernel": "k_conv_f32 (forward)", "bytes_per_launch": int(dom_bytes),
                 "avg_launch_us": round(dom_ms * 1e3, 2)}
 
     if args.copy_calibration:
@@ -191,10 +201,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "voxels": wl.n, "D": wl.D,
                    "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
-                   "kernel_map_pairs": pairs, "parallelism": "single GPU"},
+                   "kernel_map_pairs": pairs, "tile_plan": not args.no_plan, "parallelism": "single GPU"},
         "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
         "effective_gflops": round(flops / conv_s / 1e9, 1),
         "kernel_map_build_ms": round(ms["map"], 4),
+        "tile_plan_ms": round(ms["plan"], 4),
         "stage_ms": {k: round(v, 4) for k, v in ms.items()},
         "roofline": roof,
         "cpu_baseline": cpu,

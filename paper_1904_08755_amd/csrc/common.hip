@@ -65,28 +65,67 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const int32_t* cnt
     if (threadIdx.x == 0) part[blockIdx.x] = tot;
 }
 
-// single block: exclusive scan of the per-tile partials, in place
-__global__ void __launch_bounds__(kScanThreads) k_scan_partials(int64_t* part, int64_t nb, int64_t* out_total_a,
-                                                                int64_t* out_total_b) {
-    __shared__ int64_t sh[kScanThreads / 64];
-    int64_t carry = 0;
-    for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
-        const int64_t i = b0 + threadIdx.x;
-        int64_t v = i < nb ? part[i] : 0;
-        int64_t tot;
-        int64_t ex = block_exclusive(v, sh, &tot);
-        if (i < nb) part[i] = carry + ex;
-        carry += tot;
+// Single-block scan of up to kScanSingleMax counts (one tile: 1024 threads x
+// 8 contiguous counts each), for small scans where a launch matters more
+// than the bandwidth.
+constexpr int kScanSingleThreads = 1024;
+constexpr int kScanSingleE = 8;
+constexpr int64_t kScanSingleMax = (int64_t)kScanSingleThreads * kScanSingleE;
+
+__global__ void __launch_bounds__(kScanSingleThreads) k_scan_single(const int32_t* __restrict__ cnt, int64_t m,
+                                                                    int64_t* __restrict__ out,
+                                                                    int64_t* __restrict__ total_out) {
+    __shared__ int64_t sh[kScanSingleThreads / 64];
+    const int t = threadIdx.x, w = t >> 6, l = __lane_id();
+    const int64_t b = (int64_t)t * kScanSingleE;
+    int32_t v[kScanSingleE];
+#pragma unroll
+    for (int i = 0; i < kScanSingleE; ++i) v[i] = b + i < m ? cnt[b + i] : 0;
+    int64_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanSingleE; ++i) s += v[i];
+    const int64_t inc = wave_inclusive(s);
+    if (l == 63) sh[w] = inc;
+    __syncthreads();
+    int64_t base = 0, all = 0;
+    for (int i = 0; i < kScanSingleThreads / 64; ++i) {
+        if (i < w) base += sh[i];
+        all += sh[i];
     }
-    if (threadIdx.x == 0) {
-        if (out_total_a) *out_total_a = carry;
-        if (out_total_b) *out_total_b = carry;
+    int64_t run = base + inc - s;
+#pragma unroll
+    for (int i = 0; i < kScanSingleE; ++i) {
+        if (b + i < m) out[b + i] = run;
+        run += v[i];
+    }
+    if (t == 0) {
+        out[m] = all;
+        if (total_out) *total_out = all;
     }
 }
 
-__global__ void __launch_bounds__(kScanThreads) k_scan_down(const int32_t* cnt, int64_t m, const int64_t* part,
-                                                            int64_t* out) {
+// Second pass of the two-kernel scan: block b adds up the tile sums of the
+// blocks before it (a block-wide reduction over at most nb values, read from
+// L2), then scans its own tile.  The last block also writes the total.
+__global__ void __launch_bounds__(kScanThreads) k_scan_down2(const int32_t* __restrict__ cnt, int64_t m,
+                                                             const int64_t* __restrict__ part, int64_t nb,
+                                                             int64_t* __restrict__ out, int64_t* __restrict__ total_out) {
     __shared__ int64_t sh[kScanThreads / 64];
+    __shared__ int64_t carry_sh;
+    const int w = threadIdx.x >> 6, l = __lane_id();
+    int64_t c = 0;
+    for (int64_t i = threadIdx.x; i < (int64_t)blockIdx.x; i += kScanThreads) c += part[i];
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+    if (l == 0) sh[w] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t t = 0;
+        for (int i = 0; i < kScanThreads / 64; ++i) t += sh[i];
+        carry_sh = t;
+    }
+    __syncthreads();
+    const int64_t carry = carry_sh;
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPer;
     int64_t v[kScanPer];
     int64_t s = 0;
@@ -96,12 +135,31 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_down(const int32_t* cnt, 
         s += v[i];
     }
     int64_t tot;
-    int64_t run = part[blockIdx.x] + block_exclusive(s, sh, &tot);
+    int64_t run = carry + block_exclusive(s, sh, &tot);
 #pragma unroll
     for (int i = 0; i < kScanPer; ++i) {
         if (base + i < m) out[base + i] = run;
         run += v[i];
     }
+    if (blockIdx.x == nb - 1 && threadIdx.x == 0) {
+        out[m] = carry + tot;
+        if (total_out) *total_out = carry + tot;
+    }
+}
+
+__global__ void k_zero_i64(int64_t* p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0;
+}
+
+__global__ void k_seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* seg) {
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k <= K) seg[k] = gidx[(int64_t)k * G];
+}
+
+int seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* seg, hipStream_t s) {
+    hipLaunchKernelGGL(k_seg_from_gidx, dim3((unsigned)((K + 1 + 255) / 256)), dim3(256), 0, s, gidx, K, G, seg);
+    GSC_LAUNCH_CHECK();
+    return GSC_OK;
 }
 
 size_t scan_ws_bytes(int64_t m) {
@@ -110,18 +168,17 @@ size_t scan_ws_bytes(int64_t m) {
 }
 
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws, hipStream_t s) {
+    if (m <= kScanSingleMax) {
+        hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(kScanSingleThreads), 0, s, cnt, m, out, total_out);
+        GSC_LAUNCH_CHECK();
+        return GSC_OK;
+    }
     int64_t* part = reinterpret_cast<int64_t*>(ws);
     const int64_t nb = (m + kScanTile - 1) / kScanTile;
-    if (nb > 0) {
-        hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part);
-        GSC_LAUNCH_CHECK();
-    }
-    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nb, out + m, total_out);
+    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part);
     GSC_LAUNCH_CHECK();
-    if (nb > 0) {
-        hipLaunchKernelGGL(k_scan_down, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part, out);
-        GSC_LAUNCH_CHECK();
-    }
+    hipLaunchKernelGGL(k_scan_down2, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part, nb, out, total_out);
+    GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
 

@@ -37,13 +37,13 @@ constexpr int kDwTile = 64;
 template <typename TIn, typename TOut, bool WT, typename Sel>
 __global__ void __launch_bounds__(kThreads)
 k_conv_os(const TIn* __restrict__ X, int64_t n_x, const TIn* __restrict__ W, const int32_t* __restrict__ gat,
-          const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx, int K, int64_t G, int ca, int cb,
-          int64_t n_y, TOut* __restrict__ Y, Sel sel) {
+          const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx, const int32_t* __restrict__ perm, int K,
+          int64_t G, int ca, int cb, int64_t n_y, TOut* __restrict__ Y, Sel sel) {
     __shared__ float acc[kTileRows * kAccStride];
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int r16 = lane & 15, q = lane >> 4;
-    const int64_t tile = xcd_unit(blockIdx.x, gridDim.x);
+    const int64_t tile = tile_unit(blockIdx.x, gridDim.x, perm != nullptr);
     const int64_t row0 = tile * kTileRows;
     const int col0 = blockIdx.y * kColSlice;
     const int ncols = min(kColSlice, cb - col0);
@@ -127,8 +127,11 @@ k_conv_os(const TIn* __restrict__ X, int64_t n_x, const TIn* __restrict__ W, con
     __syncthreads();
     for (int i = tid; i < kTileRows * ncols; i += kThreads) {
         const int r = i / ncols, c = i - r * ncols;
-        const int64_t row = row0 + r;
-        if (row < n_y) store_out(Y + row * cb + col0 + c, acc[r * kAccStride + c]);
+        const int64_t pos = row0 + r;
+        if (pos < n_y) {
+            const int64_t row = perm ? (int64_t)perm[pos] : pos;
+            store_out(Y + row * cb + col0 + c, acc[r * kAccStride + c]);
+        }
     }
 }
 
@@ -216,8 +219,8 @@ constexpr int kWaveKMax = 64;
 template <int CA, int CB, bool WT, typename Sel>
 __global__ void __launch_bounds__(kThreads)
 k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, const int32_t* __restrict__ gat,
-           const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx, int K, int64_t G, int64_t n_y,
-           float* __restrict__ Y, Sel sel) {
+           const int32_t* __restrict__ sca, const int64_t* __restrict__ gidx, const int32_t* __restrict__ perm, int K,
+           int64_t G, int64_t n_y, float* __restrict__ Y, Sel sel) {
     constexpr int KS = CA / 4;
     constexpr int NNB = CB / 16;
     constexpr int AS = CB + 1;
@@ -227,7 +230,7 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int r16 = lane & 15, q = lane >> 4;
-    const int64_t g = xcd_unit(blockIdx.x, gridDim.x) * (kThreads / 64) + wave;
+    const int64_t g = tile_unit(blockIdx.x, gridDim.x, perm != nullptr) * (kThreads / 64) + wave;
     if (g >= G) return;                        // no barrier below, so a wave may leave early
     float* acc = acc_all[wave];
     const int64_t row0 = g * RG;
@@ -349,8 +352,11 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
     // 5. the group's rows, written once
     for (int i = lane; i < RG * CB; i += 64) {
         const int r = i / CB, cc = i - r * CB;
-        const int64_t row = row0 + r;
-        if (row < n_y) Y[row * CB + cc] = acc[r * AS + cc];
+        const int64_t pos = row0 + r;
+        if (pos < n_y) {
+            const int64_t row = perm ? (int64_t)perm[pos] : pos;
+            Y[row * CB + cc] = acc[r * AS + cc];
+        }
     }
 }
 
@@ -637,23 +643,22 @@ static bool dw_f32_specialised(int ci, int co) {
 
 template <int CA, int CB, bool WT, typename Sel>
 static void launch_f32(const void* X, int64_t n_x, const void* W, const int32_t* gat, const int32_t* sca,
-                       const int64_t* gidx, int K, int64_t G, int64_t tiles, int64_t n_y, void* Y, Sel sel,
+                       const int64_t* gidx, const int32_t* perm, int K, int64_t G, int64_t n_y, void* Y, Sel sel,
                        hipStream_t s) {
-    (void)tiles;
     const int64_t blocks = (G + kThreads / 64 - 1) / (kThreads / 64);
     hipLaunchKernelGGL((k_conv_f32<CA, CB, WT, Sel>), dim3((unsigned)blocks), dim3(kThreads), 0, s,
-                       reinterpret_cast<const float*>(X), n_x, reinterpret_cast<const float*>(W), gat, sca, gidx, K,
-                       G, n_y, reinterpret_cast<float*>(Y), sel);
+                       reinterpret_cast<const float*>(X), n_x, reinterpret_cast<const float*>(W), gat, sca, gidx,
+                       perm, K, G, n_y, reinterpret_cast<float*>(Y), sel);
 }
 
 // fp32 shapes with a specialised kernel
 template <bool WT, typename Sel>
 static bool try_f32(int ca, int cb, const void* X, int64_t n_x, const void* W, const int32_t* gat,
-                    const int32_t* sca, const int64_t* gidx, int K, int64_t G, int64_t tiles, int64_t n_y, void* Y,
-                    Sel sel, hipStream_t s) {
+                    const int32_t* sca, const int64_t* gidx, const int32_t* perm, int K, int64_t G, int64_t n_y,
+                    void* Y, Sel sel, hipStream_t s) {
 #define GSC_F32_CASE(A, B)                                                                     \
     if (ca == A && cb == B) {                                                                  \
-        launch_f32<A, B, WT, Sel>(X, n_x, W, gat, sca, gidx, K, G, tiles, n_y, Y, sel, s);     \
+        launch_f32<A, B, WT, Sel>(X, n_x, W, gat, sca, gidx, perm, K, G, n_y, Y, sel, s);      \
         return true;                                                                           \
     }
     GSC_F32_CASE(16, 16) GSC_F32_CASE(16, 32) GSC_F32_CASE(32, 16) GSC_F32_CASE(32, 32)
@@ -664,19 +669,20 @@ static bool try_f32(int ca, int cb, const void* X, int64_t n_x, const void* W, c
 
 template <typename TIn, typename TOut, bool WT, typename Sel>
 static int launch_os(const void* X, int64_t n_x, const void* W, const int32_t* gat, const int32_t* sca,
-                     const int64_t* gidx, int K, int ca, int cb, int64_t n_y, void* Y, Sel sel, hipStream_t s) {
+                     const int64_t* gidx, const int32_t* perm, int K, int ca, int cb, int64_t n_y, void* Y, Sel sel,
+                     hipStream_t s) {
     if (n_y == 0) return GSC_OK;
     const int64_t tiles = (n_y + kTileRows - 1) / kTileRows;
     const int64_t G = (n_y + GSC_GROUP_ROWS - 1) / GSC_GROUP_ROWS;
     if constexpr (sizeof(TIn) == 4) {
-        if (K <= kWaveKMax && try_f32<WT, Sel>(ca, cb, X, n_x, W, gat, sca, gidx, K, G, tiles, n_y, Y, sel, s)) {
+        if (K <= kWaveKMax && try_f32<WT, Sel>(ca, cb, X, n_x, W, gat, sca, gidx, perm, K, G, n_y, Y, sel, s)) {
             GSC_LAUNCH_CHECK();
             return GSC_OK;
         }
     }
     dim3 grid((unsigned)tiles, (unsigned)((cb + kColSlice - 1) / kColSlice));
     hipLaunchKernelGGL((k_conv_os<TIn, TOut, WT, Sel>), grid, dim3(kThreads), 0, s, reinterpret_cast<const TIn*>(X),
-                       n_x, reinterpret_cast<const TIn*>(W), gat, sca, gidx, K, G, ca, cb, n_y,
+                       n_x, reinterpret_cast<const TIn*>(W), gat, sca, gidx, perm, K, G, ca, cb, n_y,
                        reinterpret_cast<TOut*>(Y), sel);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
@@ -699,8 +705,8 @@ size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t
 
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
                         int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
-                        const int64_t* gidx, int64_t n_pairs, void* Y, int64_t n_out, void* ws, size_t ws_bytes,
-                        void* stream) {
+                        const int64_t* gidx, const int32_t* perm, int64_t n_pairs, void* Y, int64_t n_out, void* ws,
+                        size_t ws_bytes, void* stream) {
     (void)seg;
     clear_error();
     if (dtype != GSC_F32 && dtype != GSC_BF16) return fail(GSC_EINVAL, "conv_fwd: unknown dtype %d", dtype);
@@ -716,16 +722,16 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
         return fail(GSC_ESHORT, "conv_fwd: ws needs %zu bytes, got %zu", need, ws ? ws_bytes : (size_t)0);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (dtype == GSC_F32)
-        return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, K, c_in, c_out, n_out, Y,
+        return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, perm, K, c_in, c_out, n_out, Y,
                                               WIdentity{}, s);
     if (fwd_uses_bf16_engine(dtype, c_in, c_out, K)) {
         if (n_out == 0) return GSC_OK;
         int rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
         if (rc) return rc;
-        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, nullptr, K, n_out, Y,
+        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, perm, K, n_out, Y,
                                     WIdentity{}, s);
     }
-    return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, K, c_in, c_out, n_out, Y,
+    return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, perm, K, c_in, c_out, n_out, Y,
                                                 WIdentity{}, s);
 }
 
@@ -738,7 +744,8 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in, int32_t c_in,
                         int32_t c_out, int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
                         int64_t n_pairs, const int32_t* t_in_idx, const int32_t* t_out_idx, const int64_t* t_seg,
-                        const int64_t* t_gidx, int64_t t_n_pairs, const int32_t* t_wsel, void* dX, float* dW,
+                        const int64_t* t_gidx, const int32_t* t_perm, int64_t t_n_pairs, const int32_t* t_wsel,
+                        void* dX, float* dW,
                         int64_t n_out, void* ws, size_t ws_bytes, void* stream) {
     (void)t_seg;
     clear_error();
@@ -762,14 +769,14 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         }
         int rc;
         if (dtype == GSC_F32)
-            rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in, n_in, dX,
-                                               sel, s);
+            rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, c_out, c_in,
+                                               n_in, dX, sel, s);
         else if (conv_bf16_supported(c_out, c_in, K))   // W[w] (c_in x c_out) is already the B layout of dY W^T
-            rc = conv_bf16<WSel>(c_out, c_in, dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, n_in, dX, sel,
+            rc = conv_bf16<WSel>(c_out, c_in, dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, n_in, dX, sel,
                                  s);
         else
-            rc = launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, K, c_out, c_in,
-                                                     n_in, dX, sel, s);
+            rc = launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, c_out,
+                                                     c_in, n_in, dX, sel, s);
         if (rc) return rc;
     }
     if (dW) {

@@ -38,15 +38,6 @@ __device__ __forceinline__ TIn w_at(const TIn* W, int w, int brow, int col, int 
     return W[((int64_t)w * ca + brow) * cb + col];
 }
 
-// Order the LDS accesses of one wave: a lane may read what another lane of
-// the same wave wrote just before.  The LDS executes a wave's operations in
-// order; this keeps the compiler from moving accesses across the point.
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // offset and pair range of a work item
 __device__ __forceinline__ bool dw_item(const int64_t* ibase, const int64_t* chunk, const int64_t* seg, int K,
                                         int64_t item, int* k_out, int64_t* p_begin, int64_t* p_end) {

@@ -220,6 +220,15 @@ size_t scan_ws_bytes(int64_t m);
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
                 hipStream_t s);
 
+// Largest offset count of a convolution plan (neighbour masks are 64-bit).
+constexpr int kPlanMaxK = 64;
+
+// p[i] = 0 for i < n.
+__global__ void k_zero_i64(int64_t* p, int64_t n);
+
+// seg[k] = gidx[k * G] for k <= K (offset starts from a group index).
+int seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* seg, hipStream_t s);
+
 // ---------------------------------------------------------------------------
 // XCD-aware block order.  The eight XCDs of the MI355X receive workgroups
 // round-robin (workgroup b runs on XCD b % 8) and each XCD has its own L2.
@@ -235,10 +244,28 @@ __device__ __forceinline__ int64_t xcd_unit(int64_t b, int64_t n) {
     return x * q + (x < r ? x : r) + i;
 }
 
+// Work unit of a block for output tiles: tiles in the natural row order go
+// to XCDs in contiguous ranges (neighbouring tiles gather mostly the same
+// rows, which then share an L2); tiles of a plan (rows ordered by neighbour
+// mask, so their cost varies along the order) go round-robin, which spreads
+// cheap and expensive tiles evenly over the XCDs.
+__device__ __forceinline__ int64_t tile_unit(int64_t b, int64_t n, bool planned) {
+    return planned ? b : xcd_unit(b, n);
+}
+
 // ---------------------------------------------------------------------------
 // wave helpers (wave64)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Order the LDS accesses of one wave: a lane may read what another lane of
+// the same wave wrote just before.  The LDS executes a wave's operations in
+// order; this keeps the compiler from moving accesses across the point.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ __forceinline__ unsigned long long lanemask_lt() {
     const int l = __lane_id();

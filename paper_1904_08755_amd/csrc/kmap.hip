@@ -246,11 +246,6 @@ __global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, co
     }
 }
 
-__global__ void k_seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* seg) {
-    const int k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k <= K) seg[k] = gidx[(int64_t)k * G];
-}
-
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 template <typename Offs>
@@ -265,8 +260,8 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
     }
     int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_seg_from_gidx, dim3((unsigned)((K + 1 + 255) / 256)), dim3(256), 0, s, gidx, K, G, seg);
-    GSC_LAUNCH_CHECK();
+    rc = seg_from_gidx(gidx, K, G, seg, s);
+    if (rc) return rc;
     int64_t bound = cap_pairs;
     if (n_pairs) {
         int64_t hres[2];

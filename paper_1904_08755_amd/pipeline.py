@@ -10,6 +10,11 @@ their asynchronous modes (the pair count stays on the device), so a pass of a
 submanifold layer has no host round trip at all; a strided layer needs one,
 to learn how many output coordinates it has.
 
+Tile plans: with ``use_plan`` (the default) every map the convolution
+kernels read is first ordered by neighbour mask (gsc_conv_plan), so their
+output tiles touch few offsets; the weight gradients use the maps in row
+form.
+
 Map reuse (Sec. 4.2 builds the kernel map once per coordinate pair):
   * submanifold layer with a symmetric region: the input-gradient map is the
     forward map itself with offset s using the weight of -o_s (no rebuild);
@@ -70,8 +75,10 @@ class StepResult:
 class StepPlan:
     """Buffers for repeated passes over one device workload."""
 
-    def __init__(self, dw: DeviceWorkload):
+    def __init__(self, dw: DeviceWorkload, use_plan: bool = True):
         self.dw = dw
+        self.use_plan = use_plan
+        self.plans: List[gsc.KernelMap] = []
         wl = dw.wl
         self.kinds = [L.kind for L in wl.layers]
         n, D, dev = wl.n, wl.D, dw.X.device
@@ -91,6 +98,11 @@ class StepPlan:
                 self.host_offs_neg = gsc._host_i32(-offs)
                 wsel = np.arange(K, dtype=np.int32)
             self.host_wsel = gsc._host_i32(wsel)
+            if use_plan:
+                self.pb = gsc.PlanBuffers(n, K, self.mb.cap, dev)
+                if not self.symmetric:
+                    self.tpb = gsc.PlanBuffers(n, K, self.tb.cap, dev)
+            self.ws_fwd = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(gsc._dt(dw.X), L.c_in, L.c_out, K), dev)
             self.Y = torch.empty((n, L.c_out), dtype=feat, device=dev)
             self.dX = torch.empty((n, L.c_in), dtype=feat, device=dev)
             self.dW = torch.empty((K, L.c_in, L.c_out), dtype=torch.float32, device=dev)
@@ -106,6 +118,12 @@ class StepPlan:
             self.host_offs = gsc._host_i32(offs)
             self.host_offs_neg = gsc._host_i32(-offs)
             self.host_ident = gsc._host_i32(np.arange(K, dtype=np.int32))
+            if use_plan:
+                self.pkd = gsc.PlanBuffers(n, K, self.kd.cap, dev)
+                self.ptd = gsc.PlanBuffers(n, K, self.td.cap, dev)
+            dt = gsc._dt(dw.X)
+            self.ws_fwd1 = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(dt, L0.c_in, L0.c_out, K), dev)
+            self.ws_fwd2 = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(dt, L1.c_in, L1.c_out, K), dev)
             self.Y1 = torch.empty((n, L0.c_out), dtype=feat, device=dev)
             self.Y2 = torch.empty((n, L1.c_out), dtype=feat, device=dev)
             self.dY1 = torch.empty((n, L0.c_out), dtype=feat, device=dev)
@@ -119,7 +137,8 @@ class StepPlan:
 
     def run(self, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
         """Enqueue one pass.  ``mark(name)`` (optional) is called after each
-        stage is enqueued: "map" (coordinates + kernel maps), "fwd", "bwd"."""
+        stage is enqueued: "map" (coordinates + kernel maps), "plan" (tile
+        plans), "fwd", "bwd"."""
         mark = mark or (lambda name: None)
         dw = self.dw
         if self.kinds == ["subm"]:
@@ -133,9 +152,15 @@ class StepPlan:
                 tmap = gsc.gsc_kernel_map(self.table, dw.coords, -offs, stream=stream, sync=False, bufs=self.tb,
                                           host_offsets=self.host_offs_neg)
             mark("map")
-            Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kmap, Y=self.Y, stream=stream)
+            fmap, dxmap = kmap, tmap
+            if self.use_plan:
+                fmap = gsc.gsc_conv_plan(kmap, self.pb, stream=stream)
+                dxmap = fmap if self.symmetric else gsc.gsc_conv_plan(tmap, self.tpb, stream=stream)
+                self.plans = [fmap]
+            mark("plan")
+            Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], fmap, Y=self.Y, stream=stream, ws=self.ws_fwd)
             mark("fwd")
-            dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, kmap, tmap, None, dX=self.dX, dW=self.dW,
+            dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, kmap, dxmap, None, dX=self.dX, dW=self.dW,
                                              ws=self.ws_bwd, stream=stream, host_wsel=self.host_wsel)
             mark("bwd")
             return StepResult(None, [kmap], [Y], dX, [dW], [])
@@ -149,20 +174,27 @@ class StepPlan:
         td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
                                 host_offsets=self.host_offs_neg)
         mark("map")
-        Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], kd, Y=self.Y1[:n_out], stream=stream)
-        Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], td, Y=self.Y2, stream=stream)
+        pkd, ptd = kd, td
+        if self.use_plan:
+            pkd = gsc.gsc_conv_plan(kd, self.pkd, stream=stream)
+            ptd = gsc.gsc_conv_plan(td, self.ptd, stream=stream)
+            self.plans = [pkd, ptd]
+        mark("plan")
+        Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], pkd, Y=self.Y1[:n_out], stream=stream, ws=self.ws_fwd1)
+        Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], ptd, Y=self.Y2, stream=stream, ws=self.ws_fwd2)
         mark("fwd")
-        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, td, kd, None, dX=self.dY1[:n_out], dW=self.dW2,
+        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, td, pkd, None, dX=self.dY1[:n_out], dW=self.dW2,
                                            ws=self.ws_bwd2, stream=stream, host_wsel=self.host_ident)
-        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, kd, td, None, dX=self.dX, dW=self.dW1,
+        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, kd, ptd, None, dX=self.dX, dW=self.dW1,
                                           ws=self.ws_bwd1, stream=stream, host_wsel=self.host_ident)
         mark("bwd")
         return StepResult(out_coords, [kd, td], [Y1, Y2], dX, [dW1, dW2], [dY1])
 
 
-def run_step(dw: DeviceWorkload, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
+def run_step(dw: DeviceWorkload, mark: Optional[Callable[[str], None]] = None, stream=None,
+             use_plan: bool = True) -> StepResult:
     """One pass with freshly allocated buffers; the table build is then checked."""
-    plan = StepPlan(dw)
+    plan = StepPlan(dw, use_plan)
     res = plan.run(mark, stream)
     gsc.gsc_table_status(plan.table, stream)
     return res

@@ -123,7 +123,7 @@ def test_kernel_map_validation(L):
 def test_conv_validation(L):
     fake = ctypes.c_void_p(0x1000)
     fwd = lambda dt, ci, K, npairs=10, co=4, ws=None, wsb=0: L.gsc_sparse_conv_fwd(
-        dt, fake, 10, ci, fake, co, K, fake, fake, fake, fake, npairs, fake, 10, ws, wsb, None)
+        dt, fake, 10, ci, fake, co, K, fake, fake, fake, fake, None, npairs, fake, 10, ws, wsb, None)
     assert fwd(7, 4, 27) == gsc.GSC_EINVAL
     assert fwd(0, 0, 27) == gsc.GSC_EINVAL
     assert fwd(0, 4, 0) == gsc.GSC_EINVAL
@@ -136,13 +136,26 @@ def test_conv_validation(L):
     assert fwd(gsc.GSC_BF16, 256, 27, co=256) == gsc.GSC_ESHORT
     assert fwd(gsc.GSC_BF16, 256, 27, co=256, ws=fake, wsb=need - 1) == gsc.GSC_ESHORT
     sel = (ctypes.c_int32 * 2)(0, 2)   # 2 is out of range for K = 2
-    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, 10,
-                               sel, fake, None, 10, None, 0, None)
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, None,
+                               10, sel, fake, None, 10, None, 0, None)
     assert rc == gsc.GSC_EINVAL and "t_wsel" in _err(L)
     sel = (ctypes.c_int32 * 2)(0, 1)
-    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, 10,
-                               sel, None, ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)), 10, fake, 8, None)
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, None,
+                               10, sel, None, ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)), 10, fake, 8, None)
     assert rc == gsc.GSC_ESHORT
+
+
+def test_plan_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    ws = L.gsc_conv_plan_ws_bytes(100, 27)
+    assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 65) == 0
+    plan = lambda K, wsb=ws, cap=10, seg=fake: L.gsc_conv_plan(fake, fake, fake, 100, K, cap, fake, fake, fake, seg,
+                                                               fake, fake, wsb, None)
+    assert plan(65) == gsc.GSC_EINVAL and "K=65" in _err(L)
+    assert plan(0) == gsc.GSC_EINVAL
+    assert plan(27, wsb=ws - 1) == gsc.GSC_ESHORT
+    assert plan(27, cap=-1) == gsc.GSC_EINVAL
+    assert plan(27, seg=None) == gsc.GSC_EINVAL
 
 
 @pytest.mark.parametrize("name,K,D", [("cube", 3, 3), ("cube", 2, 3), ("cube", 5, 4), ("cross", 5, 3),

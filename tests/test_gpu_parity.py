@@ -223,6 +223,58 @@ def test_bf16_wide_channel_engine(ci, co, region):
     _conv_case(coords, ci, co, offs, 91, dtype="bf16")
 
 
+def _check_plan(km, plan):
+    """The plan lists the map's pairs over positions ordered by neighbour mask."""
+    n, K = km.n_out, km.K
+    perm = plan.perm.cpu().numpy().astype(np.int64)
+    assert np.array_equal(np.sort(perm), np.arange(n))
+    pairs = gpu_pairs(km)
+    mask = np.zeros(n, np.uint64)
+    for k, (_, o) in enumerate(pairs):
+        mask[o] |= np.uint64(1) << np.uint64(k)
+    ms = mask[perm]
+    assert np.all(ms[1:] >= ms[:-1])                                   # sorted by mask
+    same = ms[1:] == ms[:-1]
+    assert np.all(perm[1:][same] > perm[:-1][same])                    # stable: row order within a mask
+    ppairs = gpu_pairs(plan)
+    for k in range(K):
+        pi, pp = ppairs[k]
+        assert np.all(np.diff(pp) > 0)
+        order = np.argsort(perm[pp], kind="stable")
+        assert np.array_equal(perm[pp][order], pairs[k][1]) and np.array_equal(pi[order], pairs[k][0])
+    check_gidx(plan)
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_conv_plan_same_pairs_same_results(cid):
+    wl = WL.make_workload(cid, scale=0.3)
+    _say(f"[gpu] plan {wl.name} n={wl.n}")
+    dw = pipeline.to_device(wl, DEV)
+    base = pipeline.StepPlan(dw, use_plan=False).run()
+    planned = pipeline.StepPlan(dw, use_plan=True)
+    res = planned.run()
+    torch.cuda.synchronize()
+    for km, pl in zip(res.kmaps, planned.plans):
+        _check_plan(km, pl)
+    # per output row the plan changes neither the pairs nor their order of
+    # accumulation (offset order), so the results are identical
+    for a, b in zip(base.Ys + [base.dX], res.Ys + [res.dX]):
+        assert torch.equal(a, b)
+    for a, b in zip(base.dWs, res.dWs):
+        assert torch.equal(a, b)
+
+
+def test_conv_plan_bf16_wide():
+    wl = WL.make_workload(4, scale=0.3)
+    dw = pipeline.to_device(wl, DEV)
+    base = pipeline.StepPlan(dw, use_plan=False).run()
+    planned = pipeline.StepPlan(dw, use_plan=True)
+    res = planned.run()
+    torch.cuda.synchronize()
+    _check_plan(res.kmaps[0], planned.plans[0])
+    assert torch.equal(base.Ys[0], res.Ys[0]) and torch.equal(base.dX, res.dX)
+
+
 def test_4d_hybrid_and_tesseract():
     coords = WL.random_coords(77, 3000, 4, -5, 5, batch=1)
     _conv_case(coords, 8, 8, regions.hybrid(3, 4), 77)
