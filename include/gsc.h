@@ -13,8 +13,8 @@
  *                        (Sec. 4.2, first paragraph)
  *   gsc_kernel_map       kernel map M = {(I_i, O_i)}_i for an arbitrary
  *                        offset set N^D (Sec. 4.2; Eq. 3 of Sec. 3.1)
- *   gsc_conv_plan        an ordering of a kernel map's output rows by
- *                        neighbour mask, for the convolution kernels' tiles
+ *   gsc_conv_plan        the block plan of a kernel map: its output rows
+ *                        ordered by neighbour mask, in 16-row blocks
  *   gsc_sparse_conv_fwd  Alg. 2 (and the transposed convolution of Sec. 4.2,
  *                        run on the role-reversed kernel map)
  *   gsc_sparse_conv_bwd  gradients of Alg. 2 with respect to the input
@@ -165,33 +165,46 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
                    void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
-/* Tile plan of a kernel map (an ordering of the output rows for a4 - a6).  */
+/* Block plan of a kernel map (an ordering of the output rows for a4 - a6). */
 /* ------------------------------------------------------------------------ */
-/* The convolution kernels work on tiles of consecutive output positions, and
- * every offset that has pairs in a tile costs one pass over that offset's
- * weight matrix (Alg. 2 multiplies the gathered rows of offset i by W_i).  A
- * plan orders the output rows by their neighbour mask (bit k set when the
- * row has a pair at offset k), so rows with the same neighbourhood shape share
- * tiles and a tile touches few offsets; it matters most for wide layers.
+/* Eq. 3 sums, for every output row, one product per offset at which the row
+ * has a pair.  The block engines of gsc_sparse_conv_fwd/bwd compute 16 output
+ * rows together (one MFMA row block): for each offset that any of the 16 rows
+ * has they gather the 16 input rows of that offset (zero where a row has no
+ * pair) and multiply them by the offset's weight matrix, keeping the block's
+ * sums in registers; so a block costs one product per distinct offset of its
+ * rows.  The plan orders the output rows by neighbour mask (bit k set when
+ * the row has a pair at offset k), so rows with equal masks share blocks.
  *
- * Input: a kernel map in the form gsc_kernel_map produces (in_idx, out_idx,
- * gidx over n_out output rows, K <= 64 offsets; its pair count is read on the
- * device from gidx[K * G]).  Output (device, caller-allocated):
- *   perm[n_out]     perm[i] = the output row placed at position i;
- *   p_in, p_pos     (cap_pairs entries) every pair of the map as (input row,
- *                   position), grouped by offset in the map's offset order,
- *                   increasing position within an offset;
- *   p_seg[K + 1], p_gidx[K * G + 1]   offset starts and 64-position group
- *                   index, as gsc_kernel_map defines them.
- * (p_in, p_pos, p_seg, p_gidx) is a kernel map over output positions; pass it
- * with perm to gsc_sparse_conv_fwd / the dX map of gsc_sparse_conv_bwd.
- * Pairs beyond cap_pairs are dropped (size p_in, p_pos like the map).  ws:
+ * Input: a kernel map as gsc_kernel_map produces it (in_idx, out_idx, gidx
+ * over n_out output rows; K <= 32 offsets; the pair count is read on the
+ * device from gidx[K * G]; in_idx and out_idx may be NULL for a map without
+ * pairs).  Output (device, caller-allocated), with
+ * nb = gsc_plan_blocks(n_out) = ceil(n_out / 16):
+ *   perm[n_out]       perm[i] = the output row at position i (a stable sort
+ *                     of the rows by mask);
+ *   bmask[nb]         bmask[b] = OR of the masks of positions 16b..16b+15;
+ *   ibase[nb + 1]     exclusive scan of popcount(bmask); ibase[nb] = items;
+ *   items[16 * cap_items]  item t = ibase[b] + j belongs to block b and the
+ *                     j-th set bit k of bmask[b] (increasing k); entry
+ *                     items[16t + r] is the input row paired at offset k with
+ *                     the output row at position 16b + r, or -1 if none.
+ * cap_items must be >= K * nb (an upper bound of the item count).  ws:
  * gsc_conv_plan_ws_bytes(n_out, K) bytes.  Asynchronous, deterministic.
- * Errors: EINVAL (K > 64, null pointers), ESHORT (ws), EHIP. */
+ * Errors: EINVAL (K > 32, null pointers), ESHORT (cap_items, ws), EHIP. */
+int64_t gsc_plan_blocks(int64_t n_out);
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K);
 int gsc_conv_plan(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n_out, int32_t K,
-                  int64_t cap_pairs, int32_t* perm, int32_t* p_in, int32_t* p_pos, int64_t* p_seg, int64_t* p_gidx,
+                  int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, int64_t cap_items,
                   void* ws, size_t ws_bytes, void* stream);
+
+/* 1 if gsc_sparse_conv_fwd/bwd have a block engine for a convolution whose
+ * gathered rows have c_red channels and whose output rows have c_out channels
+ * (forward: c_red = c_in; input gradient: c_red = c_out of the layer and the
+ * output is c_in wide), else 0; a plan passed for another shape is ignored
+ * and the map's row form is used.  Present engine: float32 with c_red, c_out
+ * in {16, 32, 64} and K * c_red * c_out * 4 <= 147456. */
+int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K);
 
 /* ------------------------------------------------------------------------ */
 /* a4 / a5. Convolution forward (Alg. 2), transposed convolution.           */
@@ -209,16 +222,20 @@ size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t
  * c_out (overwritten; rows without pairs become 0), W: K x c_in x c_out.
  * The map (in_idx, out_idx, seg, gidx, n_pairs) must be as gsc_kernel_map
  * produces it for n_out output rows: out_idx increasing within each offset
- * and gidx its 64-row group index, or a plan of it (gsc_conv_plan) with perm
- * (perm NULL: out_idx holds output rows; else out_idx holds positions and
- * position i is output row perm[i]).  The transposed convolution is this call
- * on the role-reversed map (see gsc_kernel_map).  ws: gsc_conv_fwd_ws_bytes
+ * and gidx its 64-row group index.  (perm, bmask, ibase, items) is the map's
+ * block plan (gsc_conv_plan), or all four NULL; when given and
+ * gsc_conv_block_engine(dtype, c_in, c_out, K) is 1 (and X and W are 16-byte
+ * aligned) the block engine computes Y from the plan, otherwise the map is
+ * used.  Both give Eq. 3; each output row sums its offsets' products in
+ * increasing offset order.  The transposed convolution is this call on the
+ * role-reversed map (see gsc_kernel_map).  ws: gsc_conv_fwd_ws_bytes
  * bytes of device memory (may be NULL when that is 0), contents not kept.
  * Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in,
                         const void* W, int32_t c_out, int32_t K,
                         const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
-                        const int64_t* gidx, const int32_t* perm, int64_t n_pairs,
+                        const int64_t* gidx, int64_t n_pairs,
+                        const int32_t* perm, const uint32_t* bmask, const int64_t* ibase, const int32_t* items,
                         void* Y, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
@@ -238,9 +255,9 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
  * map uses: dX[t_out_idx[p]] += dY[t_in_idx[p]] W[t_wsel[s]]^T.  For the
  * role-reversed map from gsc_kernel_map t_wsel is the identity; for a stride-1
  * map whose offset set is symmetric the forward map itself serves, with
- * t_wsel[s] = the offset -o_s.  The dX map may be a plan (gsc_conv_plan) with
- * t_perm, as for gsc_sparse_conv_fwd; the forward map (used for dW) is always
- * in row form.
+ * t_wsel[s] = the offset -o_s.  (t_perm, t_bmask, t_ibase, t_items) is the
+ * dX map's block plan or all NULL, used as in gsc_sparse_conv_fwd when
+ * gsc_conv_block_engine(dtype, c_out, c_in, K) is 1.
  * dX (nullable: skip) has X's dtype; dW (nullable: skip) is float32.  Both are
  * overwritten.  ws: gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K) bytes (only
  * needed when dW is computed).  The dW reduction order is fixed, so dW is
@@ -249,7 +266,9 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                         int64_t n_in, int32_t c_in, int32_t c_out, int32_t K,
                         const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg, int64_t n_pairs,
                         const int32_t* t_in_idx, const int32_t* t_out_idx, const int64_t* t_seg,
-                        const int64_t* t_gidx, const int32_t* t_perm, int64_t t_n_pairs, const int32_t* t_wsel,
+                        const int64_t* t_gidx, int64_t t_n_pairs, const int32_t* t_wsel,
+                        const int32_t* t_perm, const uint32_t* t_bmask, const int64_t* t_ibase,
+                        const int32_t* t_items,
                         void* dX, float* dW, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus

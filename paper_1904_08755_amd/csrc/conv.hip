@@ -19,6 +19,7 @@
 
 #include "conv_common.h"
 #include "conv_bf16.h"
+#include "conv_blk.h"
 
 namespace gsc {
 
@@ -703,9 +704,28 @@ size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t
     return fwd_uses_bf16_engine(dtype, c_in, c_out, K) ? transpose_ws_bytes(K, c_in, c_out) : 0;
 }
 
+// The plan (perm, bmask, ibase, items) is all given or all null (checked
+// when there are output rows; with none the plan is not read).
+static int plan_args(const char* who, int64_t n, const int32_t* perm, const uint32_t* bmask, const int64_t* ibase,
+                     const int32_t* items, bool* given) {
+    *given = false;
+    if (n == 0) return GSC_OK;
+    const int nn = (perm != nullptr) + (bmask != nullptr) + (ibase != nullptr) + (items != nullptr);
+    if (nn != 0 && nn != 4) return fail(GSC_EINVAL, "%s: the block plan needs perm, bmask, ibase and items", who);
+    *given = nn == 4;
+    return GSC_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K) {
+    return dtype == GSC_F32 && blk_f32_supported(c_red, c_out, K) ? 1 : 0;
+}
+
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
                         int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
-                        const int64_t* gidx, const int32_t* perm, int64_t n_pairs, void* Y, int64_t n_out, void* ws,
+                        const int64_t* gidx, int64_t n_pairs, const int32_t* perm, const uint32_t* bmask,
+                        const int64_t* ibase, const int32_t* items, void* Y, int64_t n_out, void* ws,
                         size_t ws_bytes, void* stream) {
     (void)seg;
     clear_error();
@@ -720,18 +740,28 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
     const size_t need = gsc_conv_fwd_ws_bytes(dtype, c_in, c_out, K);
     if (need > 0 && (!ws || ws_bytes < need))
         return fail(GSC_ESHORT, "conv_fwd: ws needs %zu bytes, got %zu", need, ws ? ws_bytes : (size_t)0);
+    bool planned = false;
+    int rc = plan_args("conv_fwd", n_out, perm, bmask, ibase, items, &planned);
+    if (rc) return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (planned && gsc_conv_block_engine(dtype, c_in, c_out, K) && aligned16(X) && aligned16(W)) {
+        if (n_in > 0 && !X) return fail(GSC_EINVAL, "conv_fwd: X is null");
+        static const WSel kNoSel{};
+        return conv_blk_f32(c_in, c_out, reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(W),
+                            false, kNoSel, K, BlockPlan{perm, bmask, ibase, items}, n_out,
+                            reinterpret_cast<float*>(Y), s);
+    }
     if (dtype == GSC_F32)
-        return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, perm, K, c_in, c_out, n_out, Y,
+        return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
                                               WIdentity{}, s);
     if (fwd_uses_bf16_engine(dtype, c_in, c_out, K)) {
         if (n_out == 0) return GSC_OK;
-        int rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
+        rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
         if (rc) return rc;
-        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, perm, K, n_out, Y,
+        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, nullptr, K, n_out, Y,
                                     WIdentity{}, s);
     }
-    return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, perm, K, c_in, c_out, n_out, Y,
+    return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
                                                 WIdentity{}, s);
 }
 
@@ -744,8 +774,8 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in, int32_t c_in,
                         int32_t c_out, int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
                         int64_t n_pairs, const int32_t* t_in_idx, const int32_t* t_out_idx, const int64_t* t_seg,
-                        const int64_t* t_gidx, const int32_t* t_perm, int64_t t_n_pairs, const int32_t* t_wsel,
-                        void* dX, float* dW,
+                        const int64_t* t_gidx, int64_t t_n_pairs, const int32_t* t_wsel, const int32_t* t_perm,
+                        const uint32_t* t_bmask, const int64_t* t_ibase, const int32_t* t_items, void* dX, float* dW,
                         int64_t n_out, void* ws, size_t ws_bytes, void* stream) {
     (void)t_seg;
     clear_error();
@@ -767,15 +797,21 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                 return fail(GSC_EINVAL, "conv_bwd: t_wsel[%d]=%d outside [0,%d)", k, t_wsel[k], K);
             sel.w[k] = (int16_t)t_wsel[k];
         }
-        int rc;
-        if (dtype == GSC_F32)
-            rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, c_out, c_in,
+        bool planned = false;
+        int rc = plan_args("conv_bwd", n_in, t_perm, t_bmask, t_ibase, t_items, &planned);
+        if (rc) return rc;
+        if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W))
+            rc = conv_blk_f32(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,
+                              reinterpret_cast<const float*>(W), true, sel, K,
+                              BlockPlan{t_perm, t_bmask, t_ibase, t_items}, n_in, reinterpret_cast<float*>(dX), s);
+        else if (dtype == GSC_F32)
+            rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, c_out, c_in,
                                                n_in, dX, sel, s);
         else if (conv_bf16_supported(c_out, c_in, K))   // W[w] (c_in x c_out) is already the B layout of dY W^T
-            rc = conv_bf16<WSel>(c_out, c_in, dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, n_in, dX, sel,
+            rc = conv_bf16<WSel>(c_out, c_in, dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, n_in, dX, sel,
                                  s);
         else
-            rc = launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, t_perm, K, c_out,
+            rc = launch_os<uint16_t, uint16_t, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, c_out,
                                                      c_in, n_in, dX, sel, s);
         if (rc) return rc;
     }

@@ -1,0 +1,32 @@
+// Host-side interface of the block convolution engines (conv_blk.hip): the
+// forward and input-gradient convolutions over a block plan (plan.hip), with
+// each 16-row block's sums held in registers.
+#pragma once
+
+#include "conv_common.h"
+
+namespace gsc {
+
+// A block plan: perm[i] = output row at position i; block b covers positions
+// 16b..16b+15, its offsets are the set bits of bmask[b], and its items
+// (one per offset, in increasing offset order) start at ibase[b]; item t
+// holds the 16 input rows items[16t .. 16t+15] (-1 = none).
+struct BlockPlan {
+    const int32_t* perm;
+    const uint32_t* bmask;
+    const int64_t* ibase;
+    const int32_t* items;
+};
+
+// fp32 engine: reduction width ca and output width cb in {16, 32, 64}, with
+// the K weight matrices held in LDS (K * ca * cb * 4 bytes within the
+// engine's LDS budget).
+bool blk_f32_supported(int ca, int cb, int K);
+
+// Y (n_y x cb) = sum over the plan's items of X[item rows] * B_k with
+// B_k = W[k] (ca x cb) when !wt, or B_k = W[sel(k)]^T (W: K x cb x ca) when
+// wt.  Asynchronous.
+int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s);
+
+}  // namespace gsc

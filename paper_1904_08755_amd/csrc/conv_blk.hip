@@ -1,0 +1,327 @@
+// Block convolution engines: the sum of Eq. 3 (Alg. 2's per-offset products,
+// regrouped by output row block) over a block plan.
+//
+// A 16-row block of output positions is computed by one wave: for each
+// offset in the block's union mask (in increasing offset order) the wave
+// gathers the block's 16 input rows of that offset (zero rows where a row has
+// no pair there) and accumulates their product with the offset's weight
+// matrix into the block's sums, which stay in registers until the block is
+// written, once, to its rows.  There is no scatter, no atomic and no partial
+// buffer; a row's value is the sum of its offsets' products in increasing
+// offset order whatever the position order, so results do not depend on the
+// plan's row order.
+//
+// fp32 engine (reduction width CA, output width CB <= 64): all K weight
+// matrices live in LDS in MFMA fragment order for the whole launch (one
+// workgroup per CU, every wave of it walking its own blocks), so weights cost
+// no global traffic per item.  A wave's items stream through a software
+// pipeline of S slots: an item's 16 row indices are loaded S-1 items ahead,
+// its rows (and its positions' output rows) RD items ahead, and its MFMAs
+// (v_mfma_f32_16x16x4f32) run last.  (Deeper pipelines measured no faster:
+// with 16 waves per CU the loads are not what the engine waits for.)  The loop body is unrolled over the slots, so each slot keeps its
+// registers (no copies of loads in flight).
+#include <type_traits>
+#include <utility>
+
+#include "conv_blk.h"
+
+namespace gsc {
+
+constexpr int kBlkLdsBytes = 144 * 1024;   // weight storage of the fp32 engine
+
+// s_waitcnt operand for vmcnt(0) with expcnt and lgkmcnt left free (gfx9
+// encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int kWaitVm0 = (7 << 4) | (15 << 8);
+
+template <int CA, int CB>
+struct BlkF32 {
+    static constexpr int KS = CA / 4;        // MFMA steps (4 channels each)
+    static constexpr int NNB = CB / 16;      // 16-column output blocks
+    static constexpr int WF = KS * NNB;      // weight floats per lane per offset
+    static constexpr int WG4 = WF / 4;       // ... as float4 groups
+    static constexpr int RV = KS / 4;        // float4 row loads per lane
+    // 16 waves per CU (128 VGPRs each) for 16- and 32-wide rows, 8 (256 VGPRs) for 64-wide ones
+    static constexpr int THREADS = (CA == 64 || CB == 64) ? 512 : 1024;
+    static constexpr int WAVES = THREADS / 64;
+    static constexpr int S = 3;              // pipeline slots (items in flight)
+    static constexpr int ID = S - 1;         // row indices are loaded ID items ahead
+    static constexpr int RD = 1;             // rows are loaded RD items ahead
+};
+
+// One pipeline item: offset k (-1: a block with no offsets), block b (-1: a
+// dummy), and whether it is the block's last item.
+struct BlkItem {
+    int k;
+    int32_t b;
+    bool last;
+};
+
+// f(0) || f(1) || ... || f(N-1) with compile-time arguments (stops at the
+// first true).
+template <typename F, size_t... I>
+__device__ __forceinline__ bool run_steps(F& f, std::index_sequence<I...>) {
+    return (f(std::integral_constant<int, (int)I>{}) || ...);
+}
+
+__device__ __forceinline__ int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <int CA, int CB, bool WT>
+__global__ void __launch_bounds__((BlkF32<CA, CB>::THREADS))
+k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, int K, WSel sel,
+               const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
+               const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
+               float* __restrict__ Y) {
+    using C = BlkF32<CA, CB>;
+    __shared__ float wl[kBlkLdsBytes / 4];
+    // Weights in fragment order: lane (c, q) of offset k needs, for MFMA step
+    // s and column block j, B_k[q*KS + s][16j + c]; flat f = s*NNB + j is
+    // component f%4 of float4 group f/4 at ((k*WG4 + f/4)*64 + lane).  The
+    // source is read in its own order as float4s, kFillBatch per thread in
+    // flight before any is stored (the fill is latency-bound otherwise).
+    {
+        constexpr int kFillBatch = 8;
+        const int per4 = CA * CB / 4;
+        const int total4 = K * per4;
+        const float4* W4 = reinterpret_cast<const float4*>(W);
+        for (int e0 = threadIdx.x; e0 < total4; e0 += C::THREADS * kFillBatch) {
+            float4 v[kFillBatch];
+#pragma unroll
+            for (int u = 0; u < kFillBatch; ++u) {
+                const int e = e0 + u * C::THREADS;
+                const int k = e / per4;
+                const int src = WT ? sel(e < total4 ? k : 0) * per4 + (e - k * per4) : e;
+                v[u] = W4[e < total4 ? src : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < kFillBatch; ++u) {
+                const int e = e0 + u * C::THREADS;
+                if (e >= total4) break;
+                const int k = e / per4;
+                const int rem = 4 * (e - k * per4);
+                const float* vv = reinterpret_cast<const float*>(&v[u]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    int ch, col;
+                    if constexpr (WT) {   // W[sel(k)] is cb x ca: B_k[ch][col] = W[sel(k)][col][ch]
+                        col = (rem + i) / CA;
+                        ch = (rem + i) - col * CA;
+                    } else {
+                        ch = (rem + i) / CB;
+                        col = (rem + i) - ch * CB;
+                    }
+                    const int q = ch / C::KS, s = ch - q * C::KS;
+                    const int f = s * C::NNB + (col >> 4);
+                    wl[((k * C::WG4 + (f >> 2)) * 64 + (col & 15) + 16 * q) * 4 + (f & 3)] = vv[i];
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform: block walk in SGPRs
+    const int lane = threadIdx.x & 63;
+    const int r16 = lane & 15, q = lane >> 4;
+    const int64_t NW = (int64_t)gridDim.x * C::WAVES;
+    const int64_t gw = (int64_t)blockIdx.x * C::WAVES + wave;
+    const float4* wq = reinterpret_cast<const float4*>(wl) + lane;
+
+    for (int64_t c0 = gw; c0 < nb; c0 += 64 * NW) {
+        // this chunk: the wave's blocks c0 + l*NW, one per lane l
+        const int64_t bl = c0 + (int64_t)lane * NW;
+        const bool bv = bl < nb;
+        const uint32_t lm = bv ? bmask[bl] : 0u;
+        const int64_t lb = bv ? ibase[bl] : 0;
+        const int nit = bv ? max(__popc(lm), 1) : 0;   // a block with no offsets still writes zeros
+        int incl = nit;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int u = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += u;
+        }
+        const int T = readlane_i32(incl, 63);
+        // the chunk's block table has arrived: without this wait the loop
+        // would wait for every load in flight each time it reads the table
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+
+        // decoder of the next item (wave-uniform state); past the chunk's T
+        // items it yields dummies, so every pipeline step issues the same
+        // loads (a load skipped on some path would make the compiler wait
+        // for every load in flight before the MFMAs)
+        int dslot = -1, dcount = 0;
+        uint32_t drem = 0;
+        int64_t dgi = 0;
+        int32_t dblk = 0;
+        auto decode = [&](BlkItem& m) -> int64_t {   // returns the item's index (0 if none)
+            if (dcount >= T) {
+                m = BlkItem{-1, -1, false};
+                return 0;
+            }
+            ++dcount;
+            if (drem == 0) {
+                ++dslot;
+                const uint32_t mm = (uint32_t)readlane_i32((int)lm, dslot);
+                dgi = readlane_i64(lb, dslot);
+                dblk = (int32_t)(c0 + (int64_t)dslot * NW);
+                if (mm == 0) {
+                    m = BlkItem{-1, dblk, true};
+                    return 0;
+                }
+                drem = mm;
+            }
+            m.k = __ffs(drem) - 1;
+            drem &= drem - 1;
+            m.b = dblk;
+            m.last = drem == 0;
+            return dgi++;
+        };
+
+        constexpr int S = C::S;
+        BlkItem mt[S];
+        int32_t idxr[S], pmr[S];   // raw loads; validity is applied where they are used
+        bool okr[S];
+        float4 rv[S][C::RV];
+        floatx4 acc[C::NNB];
+#pragma unroll
+        for (int j = 0; j < C::NNB; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < S; ++i) {
+            mt[i] = BlkItem{-1, -1, false};
+            idxr[i] = -1;
+        }
+
+        auto issue_idx = [&](auto P) {
+            constexpr int p = decltype(P)::value;
+            const int64_t gi = decode(mt[p]);
+            idxr[p] = items[gi * 16 + r16];
+        };
+        auto issue_rows = [&](auto P) {
+            constexpr int p = decltype(P)::value;
+            const int32_t id = mt[p].k >= 0 ? idxr[p] : -1;
+            okr[p] = id >= 0 && id < n_x;
+            const float4* src = reinterpret_cast<const float4*>(X + (int64_t)(okr[p] ? id : 0) * CA + q * C::KS);
+#pragma unroll
+            for (int v = 0; v < C::RV; ++v) rv[p][v] = src[v];
+            int64_t pos = (int64_t)mt[p].b * 16 + r16;
+            pos = pos < 0 ? 0 : (pos < n_y ? pos : n_y - 1);
+            pmr[p] = perm[pos];
+        };
+        auto compute = [&](auto P) {
+            constexpr int p = decltype(P)::value;
+            const int k = mt[p].k;
+            if (k >= 0) {
+                float4 wf[C::WG4];
+#pragma unroll
+                for (int g = 0; g < C::WG4; ++g) wf[g] = wq[(k * C::WG4 + g) * 64];
+                const float* w = reinterpret_cast<const float*>(wf);
+                const float* ar = reinterpret_cast<const float*>(rv[p]);
+                float a[C::KS];
+#pragma unroll
+                for (int s = 0; s < C::KS; ++s) a[s] = okr[p] ? ar[s] : 0.f;
+#pragma unroll
+                for (int s = 0; s < C::KS; ++s)
+#pragma unroll
+                    for (int j = 0; j < C::NNB; ++j)
+                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], w[s * C::NNB + j], acc[j], 0, 0, 0);
+            }
+            if (mt[p].last) {
+                // lane (c, q) holds rows 4q+i, column 16j + c of the block
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int32_t row = __shfl(pmr[p], 4 * q + i, 64);
+                    const int64_t pos = (int64_t)mt[p].b * 16 + 4 * q + i;
+                    if (pos < n_y && row >= 0 && row < n_y) {
+#pragma unroll
+                        for (int j = 0; j < C::NNB; ++j) Y[(int64_t)row * CB + 16 * j + r16] = acc[j][i];
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < C::NNB; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+            }
+        };
+
+        // Item i uses slot i mod S.  At u + p (u a multiple of S) the wave
+        // loads item c + ID's row indices, item c + RD's rows and computes
+        // item c = u + p - ID.  The chunk has T >= 1 items (its lane 0 holds
+        // a block); before item 0 the slots hold dummies, so every step issues
+        // the same loads and none is issued outside the loop.
+        int u = 0;
+        auto step = [&](auto P) -> bool {
+            constexpr int p = decltype(P)::value;
+            const int c = u + p - C::ID;
+            issue_idx(std::integral_constant<int, p>{});
+            issue_rows(std::integral_constant<int, (p + S - C::ID + C::RD) % S>{});
+            if (c >= 0) compute(std::integral_constant<int, (p + S - C::ID) % S>{});
+            return c + 1 >= T;
+        };
+        for (;; u += S)
+            if (run_steps(step, std::make_index_sequence<S>{})) break;
+    }
+}
+
+// Y = 0 (an input with no rows contributes nothing).
+__global__ void k_zero_f32(float* __restrict__ y, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        y[i] = 0.f;
+}
+
+bool blk_f32_supported(int ca, int cb, int K) {
+    auto ok = [](int c) { return c == 16 || c == 32 || c == 64; };
+    return ok(ca) && ok(cb) && K >= 1 && K <= kPlanMaxK && (int64_t)K * ca * cb * 4 <= kBlkLdsBytes;
+}
+
+static int device_cus() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
+template <int CA, int CB, bool WT>
+static void launch_blk_f32(const float* X, int64_t n_x, const float* W, const WSel& sel, int K, const BlockPlan& p,
+                           int64_t nb, int64_t n_y, float* Y, hipStream_t s) {
+    using C = BlkF32<CA, CB>;
+    int64_t grid = (nb + C::WAVES - 1) / C::WAVES;
+    const int cus = device_cus();
+    if (grid > cus) grid = cus;
+    hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X, n_x, W, K, sel,
+                       p.perm, p.bmask, p.ibase, p.items, nb, n_y, Y);
+}
+
+int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s) {
+    if (!blk_f32_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no fp32 block engine for %dx%d, K=%d", ca, cb, K);
+    const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
+    if (nb == 0) return GSC_OK;
+    if (n_x == 0) {   // no input rows to read (the engine always issues its row loads)
+        const int64_t n = n_y * cb;
+        hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256),
+                           0, s, Y, n);
+        GSC_LAUNCH_CHECK();
+        return GSC_OK;
+    }
+#define GSC_BLK_CASE(A, B)                                                                  \
+    if (ca == A && cb == B) {                                                               \
+        if (wt)                                                                             \
+            launch_blk_f32<A, B, true>(X, n_x, W, sel, K, plan, nb, n_y, Y, s);              \
+        else                                                                                \
+            launch_blk_f32<A, B, false>(X, n_x, W, sel, K, plan, nb, n_y, Y, s);             \
+        GSC_LAUNCH_CHECK();                                                                 \
+        return GSC_OK;                                                                      \
+    }
+    GSC_BLK_CASE(16, 16) GSC_BLK_CASE(16, 32) GSC_BLK_CASE(16, 64) GSC_BLK_CASE(32, 16) GSC_BLK_CASE(32, 32)
+    GSC_BLK_CASE(32, 64) GSC_BLK_CASE(64, 16) GSC_BLK_CASE(64, 32) GSC_BLK_CASE(64, 64)
+#undef GSC_BLK_CASE
+    return fail(GSC_EINVAL, "conv: no fp32 block engine for %dx%d", ca, cb);
+}
+
+}  // namespace gsc

@@ -220,8 +220,11 @@ size_t scan_ws_bytes(int64_t m);
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
                 hipStream_t s);
 
-// Largest offset count of a convolution plan (neighbour masks are 64-bit).
-constexpr int kPlanMaxK = 64;
+// Largest offset count of a block plan (neighbour masks are 32-bit).
+constexpr int kPlanMaxK = 32;
+
+// Rows of a block of the block plan (one MFMA row block).
+constexpr int kPlanBlockRows = 16;
 
 // p[i] = 0 for i < n.
 __global__ void k_zero_i64(int64_t* p, int64_t n);

@@ -1,28 +1,33 @@
-// Tile plan of a kernel map for the convolution kernels.
+// Block plan of a kernel map for the convolution kernels.
 //
-// The output-stationary convolution kernels process a tile of consecutive
-// output positions at a time, and every offset present in a tile costs a
-// pass over that offset's weight matrix.  In the natural row order almost
-// every offset occurs in every tile (a tile is a short run of voxels, and
-// their neighbours point every way), so for wide layers the kernels would
-// read each weight matrix once per tile.  The plan orders the output rows by
-// their neighbour mask (bit k set when the row has a pair at offset k), so
-// rows with the same neighbourhood shape (say, voxels of one flat surface)
-// share tiles and a tile touches few offsets.
+// The block convolution engines compute 16 output rows at a time (one MFMA
+// row block) and keep the block's sums in registers: for every offset that
+// any of the 16 rows has, they gather the 16 input rows (a zero row where a
+// row has no pair at that offset) and multiply by that offset's weights.  The
+// cost of a block is therefore the number of distinct offsets among its rows.
+// In the natural row order a block's rows point every way and almost all
+// offsets occur; the plan orders the output rows by neighbour mask (bit k set
+// when the row has a pair at offset k), so rows with the same neighbourhood
+// shape share blocks, and the blocks' offset sets shrink to about those of
+// single rows.
 //
-// The result is the same kernel map over output positions: perm[i] is the
-// output row at position i, and (p_in, p_pos, p_seg, p_gidx) list every pair
-// of the original map as (input row, position), grouped by offset in the
-// original offset order, increasing position within an offset, with the
-// 64-position group index p_gidx.  Steps:
-//   masks:  one wave per 64-row group of the map: neighbour mask of every row
-//           (LDS OR of the offsets' bits) and a dense table nbr[k][row] of the
-//           input row of each pair;
+// Output, for n_out rows, nb = ceil(n_out / 16) blocks:
+//   perm[i]      output row at position i (i < n_out);
+//   bmask[b]     union of the masks of block b's rows (positions 16b..16b+15);
+//   ibase[b]     first item of block b (exclusive scan of popcount(bmask));
+//                ibase[nb] = number of items;
+//   items[16*t + r]  for item t = ibase[b] + j, the j-th offset k of bmask[b]
+//                in increasing order: the input row paired with position
+//                16b + r at offset k, or -1 if there is none.
+// Steps:
+//   masks:  one wave per 64-row group of the map: every row's mask (LDS OR
+//           of the offsets' bits) and its row of the dense neighbour table
+//           nbr[row][k] (-1 where no pair), staged in LDS and written with
+//           coalesced stores;
 //   sort:   stable LSD radix sort of (mask, row) by mask, 10-bit digits;
-//   count:  per 64-position group a wave ballot of every offset's bit;
-//   scan:   the counts give p_gidx (and p_seg);
-//   fill:   each (position, offset) pair is placed at its group start plus
-//           its rank among the wave's set bits.
+//   count:  block unions and item counts; a scan gives ibase;
+//   fill:   one lane per position writes its entry of each of its block's
+//           items.
 // Everything is deterministic and runs without a host round trip.
 #include <climits>
 
@@ -38,25 +43,21 @@ constexpr int kRsTile = kPlanThreads * kRsPer;    // keys per block
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-template <typename KeyT>
-__device__ __forceinline__ KeyT key_bit(int k) {
-    return (KeyT)1 << k;
-}
-
 // ---------------------------------------------------------------------------
 // masks + dense neighbour table
 // ---------------------------------------------------------------------------
-template <typename KeyT>
 __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ in_idx,
                                                              const int32_t* __restrict__ out_idx,
                                                              const int64_t* __restrict__ gidx, int K, int64_t G,
-                                                             int64_t n_out, KeyT* __restrict__ keys,
+                                                             int64_t n_out, uint32_t* __restrict__ keys,
                                                              int32_t* __restrict__ nbr) {
-    __shared__ KeyT sm[kPlanThreads / 64][64];
+    __shared__ uint32_t sm[kPlanThreads / 64][64];
+    __shared__ int32_t sn[kPlanThreads / 64][64 * kPlanMaxK];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int64_t g = (int64_t)blockIdx.x * (kPlanThreads / 64) + wave;
     if (g >= G) return;   // no block barrier below
     sm[wave][lane] = 0;
+    for (int i = lane; i < 64 * K; i += 64) sn[wave][i] = -1;
     int64_t lo = 0;
     int n = 0;
     if (lane < K) {
@@ -84,13 +85,17 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __re
         for (int b = 0; b < B; ++b) {
             if (v[b]) {
                 const int64_t rel = (int64_t)o[b] - row0;
-                if (rel >= 0 && rel < 64) atomicOr(&sm[wave][rel], key_bit<KeyT>(k0 + b));
-                if (o[b] >= 0 && o[b] < n_out) nbr[(int64_t)(k0 + b) * n_out + o[b]] = r[b];
+                if (rel >= 0 && rel < 64) {   // a consistent map has only this group's rows here
+                    atomicOr(&sm[wave][rel], 1u << (k0 + b));
+                    sn[wave][rel * K + k0 + b] = r[b];
+                }
             }
         }
     }
     wave_lds_sync();
     if (row0 + lane < n_out) keys[row0 + lane] = sm[wave][lane];
+    const int64_t rows = min((int64_t)64, n_out - row0);
+    for (int i = lane; i < rows * K; i += 64) nbr[row0 * K + i] = sn[wave][i];
 }
 
 // ---------------------------------------------------------------------------
@@ -183,125 +188,106 @@ __global__ void __launch_bounds__(kPlanThreads) k_rs_scatter(const KeyT* __restr
 }
 
 // ---------------------------------------------------------------------------
-// plan map: counts per (offset, 64-position group), then the fill
+// blocks: union masks and item counts, then the items
 // ---------------------------------------------------------------------------
-template <typename KeyT>
-__global__ void __launch_bounds__(kPlanThreads) k_plan_count(const KeyT* __restrict__ keys, int64_t n, int K,
-                                                             int64_t G, int32_t* __restrict__ cnt) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t g = (int64_t)blockIdx.x * (kPlanThreads / 64) + wave;
-    if (g >= G) return;
-    const int64_t i = g * 64 + lane;
-    const KeyT key = i < n ? keys[i] : (KeyT)0;
-    int mine = 0;
-    for (int k = 0; k < K; ++k) {
-        const int c = __popcll(__ballot((key >> k) & 1));
-        if (lane == k) mine = c;
-    }
-    if (lane < K) cnt[(int64_t)lane * G + g] = mine;
+// OR of a value over the 16 lanes of its block (lanes 16j..16j+15).
+__device__ __forceinline__ uint32_t block_or16(uint32_t v) {
+#pragma unroll
+    for (int d = 1; d < 16; d <<= 1) v |= (uint32_t)__shfl_xor((int)v, d, 64);
+    return v;
 }
 
-template <typename KeyT>
-__global__ void __launch_bounds__(kPlanThreads) k_plan_fill(const KeyT* __restrict__ keys,
-                                                            const int32_t* __restrict__ perm,
-                                                            const int32_t* __restrict__ nbr,
-                                                            const int64_t* __restrict__ pgidx, int64_t n, int K,
-                                                            int64_t G, int64_t cap, int32_t* __restrict__ p_in,
-                                                            int32_t* __restrict__ p_pos) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t g = (int64_t)blockIdx.x * (kPlanThreads / 64) + wave;
-    if (g >= G) return;
-    const int64_t i = g * 64 + lane;
+__global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __restrict__ keys, int64_t n, int64_t nb,
+                                                            uint32_t* __restrict__ bmask, int32_t* __restrict__ cnt) {
+    const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
+    const uint32_t u = block_or16(i < n ? keys[i] : 0u);
+    const int64_t b = i >> 4;
+    if ((threadIdx.x & 15) == 0 && b < nb) {
+        bmask[b] = u;
+        cnt[b] = __popc(u);
+    }
+}
+
+__global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __restrict__ keys,
+                                                           const int32_t* __restrict__ perm,
+                                                           const int32_t* __restrict__ nbr,
+                                                           const int64_t* __restrict__ ibase, int64_t n, int64_t nb,
+                                                           int K, int32_t* __restrict__ items) {
+    const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
+    const int64_t b = i >> 4;
+    const int r = threadIdx.x & 15;
     const bool valid = i < n;
-    const KeyT key = valid ? keys[i] : (KeyT)0;
+    const uint32_t key = valid ? keys[i] : 0u;
+    const uint32_t u = block_or16(key);
+    if (b >= nb) return;   // whole blocks of 16 lanes leave together
     const int64_t row = valid ? perm[i] : 0;
-    const int64_t st = lane < K ? pgidx[(int64_t)lane * G + g] : 0;
-    const unsigned long long below = lanemask_lt();
-    constexpr int B = 8;
-    for (int k0 = 0; k0 < K; k0 += B) {
-        int32_t r[B];
-        int64_t pos[B];
-        bool v[B];
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int k = min(k0 + b, K - 1);
-            v[b] = k0 + b < K && ((key >> k) & 1);
-            const unsigned long long m = __ballot(v[b]);
-            pos[b] = __shfl(st, k, 64) + __popcll(m & below);
-            if (v[b]) r[b] = nbr[(int64_t)k * n + row];
-        }
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            if (v[b] && pos[b] < cap) {
-                p_in[pos[b]] = r[b];
-                p_pos[pos[b]] = (int32_t)i;
-            }
-        }
+    const int64_t base = ibase[b];
+    const int32_t* nrow = nbr + row * K;
+    uint32_t m = u;
+    for (int j = 0; m != 0; ++j) {
+        const int k = __ffs(m) - 1;
+        m &= m - 1;
+        items[(base + j) * 16 + r] = ((key >> k) & 1u) ? nrow[k] : -1;
     }
 }
 
-template <typename KeyT>
 static int plan_enqueue(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n, int K,
-                        int64_t cap, int32_t* perm, int32_t* p_in, int32_t* p_pos, int64_t* p_seg, int64_t* p_gidx,
-                        void* ws, hipStream_t s) {
+                        int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, void* ws, hipStream_t s) {
     const int64_t G = (n + 63) / 64;
-    const int64_t nb = (n + kRsTile - 1) / kRsTile;
+    const int64_t nb = (n + 15) / 16;
+    const int64_t nrs = (n + kRsTile - 1) / kRsTile;
     char* w = reinterpret_cast<char*>(ws);
-    KeyT* ka = reinterpret_cast<KeyT*>(w);
-    w += al256((size_t)n * sizeof(KeyT));
-    KeyT* kb = reinterpret_cast<KeyT*>(w);
-    w += al256((size_t)n * sizeof(KeyT));
+    uint32_t* ka = reinterpret_cast<uint32_t*>(w);
+    w += al256((size_t)n * sizeof(uint32_t));
+    uint32_t* kb = reinterpret_cast<uint32_t*>(w);
+    w += al256((size_t)n * sizeof(uint32_t));
     int32_t* va = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)n * sizeof(int32_t));
     int32_t* vb = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)n * sizeof(int32_t));
     int32_t* hist = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)kRsBins * nb * sizeof(int32_t));
+    w += al256((size_t)kRsBins * nrs * sizeof(int32_t));
     int64_t* hoff = reinterpret_cast<int64_t*>(w);
-    w += al256((size_t)(kRsBins * nb + 1) * sizeof(int64_t));
+    w += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
     int32_t* nbr = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)K * n * sizeof(int32_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)K * G * sizeof(int32_t));
+    w += al256((size_t)nb * sizeof(int32_t));
     void* scan_ws = w;
 
-    const unsigned gblocks = (unsigned)((G + kPlanThreads / 64 - 1) / (kPlanThreads / 64));
-    if (n > 0) {
-        hipLaunchKernelGGL((k_plan_masks<KeyT>), dim3(gblocks), dim3(kPlanThreads), 0, s, in_idx, out_idx, gidx, K,
-                           G, n, ka, nbr);
+    if (n == 0) {
+        hipLaunchKernelGGL(k_zero_i64, dim3(1), dim3(256), 0, s, ibase, (int64_t)1);
         GSC_LAUNCH_CHECK();
-        const int passes = (K + kRsBits - 1) / kRsBits;
-        const KeyT* kin = ka;
-        const int32_t* vin = nullptr;
-        for (int p = 0; p < passes; ++p) {
-            KeyT* kout = (p & 1) ? ka : kb;
-            int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? va : vb);
-            hipLaunchKernelGGL((k_rs_hist<KeyT>), dim3((unsigned)nb), dim3(kPlanThreads), 0, s, kin, n, p * kRsBits,
-                               hist, nb);
-            GSC_LAUNCH_CHECK();
-            int rc = scan_counts(hist, kRsBins * nb, hoff, nullptr, scan_ws, s);
-            if (rc) return rc;
-            hipLaunchKernelGGL((k_rs_scatter<KeyT>), dim3((unsigned)nb), dim3(kPlanThreads), 0, s, kin, vin, n,
-                               p * kRsBits, hoff, nb, kout, vout);
-            GSC_LAUNCH_CHECK();
-            kin = kout;
-            vin = vout;
-        }
-        hipLaunchKernelGGL((k_plan_count<KeyT>), dim3(gblocks), dim3(kPlanThreads), 0, s, kin, n, K, G, cnt);
-        GSC_LAUNCH_CHECK();
-        int rc = scan_counts(cnt, K * G, p_gidx, nullptr, scan_ws, s);
-        if (rc) return rc;
-        rc = seg_from_gidx(p_gidx, K, G, p_seg, s);
-        if (rc) return rc;
-        hipLaunchKernelGGL((k_plan_fill<KeyT>), dim3(gblocks), dim3(kPlanThreads), 0, s, kin, perm, nbr, p_gidx, n, K,
-                           G, cap, p_in, p_pos);
-        GSC_LAUNCH_CHECK();
-    } else {
-        hipLaunchKernelGGL(k_zero_i64, dim3(1), dim3(256), 0, s, p_seg, (int64_t)K + 1);
-        GSC_LAUNCH_CHECK();
-        hipLaunchKernelGGL(k_zero_i64, dim3(1), dim3(256), 0, s, p_gidx, (int64_t)1);
-        GSC_LAUNCH_CHECK();
+        return GSC_OK;
     }
+    const unsigned gblocks = (unsigned)((G + kPlanThreads / 64 - 1) / (kPlanThreads / 64));
+    hipLaunchKernelGGL(k_plan_masks, dim3(gblocks), dim3(kPlanThreads), 0, s, in_idx, out_idx, gidx, K, G, n, ka,
+                       nbr);
+    GSC_LAUNCH_CHECK();
+    const int passes = (K + kRsBits - 1) / kRsBits;
+    const uint32_t* kin = ka;
+    const int32_t* vin = nullptr;
+    for (int p = 0; p < passes; ++p) {
+        uint32_t* kout = (p & 1) ? ka : kb;
+        int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? va : vb);
+        hipLaunchKernelGGL((k_rs_hist<uint32_t>), dim3((unsigned)nrs), dim3(kPlanThreads), 0, s, kin, n,
+                           p * kRsBits, hist, nrs);
+        GSC_LAUNCH_CHECK();
+        int rc = scan_counts(hist, kRsBins * nrs, hoff, nullptr, scan_ws, s);
+        if (rc) return rc;
+        hipLaunchKernelGGL((k_rs_scatter<uint32_t>), dim3((unsigned)nrs), dim3(kPlanThreads), 0, s, kin, vin, n,
+                           p * kRsBits, hoff, nrs, kout, vout);
+        GSC_LAUNCH_CHECK();
+        kin = kout;
+        vin = vout;
+    }
+    const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
+    hipLaunchKernelGGL(k_blk_count, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, n, nb, bmask, cnt);
+    GSC_LAUNCH_CHECK();
+    int rc = scan_counts(cnt, nb, ibase, nullptr, scan_ws, s);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, perm, nbr, ibase, n, nb, K, items);
+    GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
 
@@ -311,40 +297,40 @@ using namespace gsc;
 
 extern "C" {
 
+int64_t gsc_plan_blocks(int64_t n_out) { return n_out <= 0 ? 0 : (n_out + 15) / 16; }
+
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
     if (n_out < 0 || K < 1 || K > kPlanMaxK) return 0;
-    const int64_t G = (n_out + 63) / 64;
-    const int64_t nb = (n_out + kRsTile - 1) / kRsTile;
-    size_t b = 2 * al256((size_t)n_out * sizeof(uint64_t));
-    b += 2 * al256((size_t)n_out * sizeof(int32_t));
-    b += al256((size_t)kRsBins * nb * sizeof(int32_t));
-    b += al256((size_t)(kRsBins * nb + 1) * sizeof(int64_t));
+    const int64_t nb = (n_out + 15) / 16;
+    const int64_t nrs = (n_out + kRsTile - 1) / kRsTile;
+    size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
+    b += al256((size_t)kRsBins * nrs * sizeof(int32_t));
+    b += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
     b += al256((size_t)K * n_out * sizeof(int32_t));
-    b += al256((size_t)K * G * sizeof(int32_t));
-    const int64_t m = kRsBins * nb > K * G ? kRsBins * nb : K * G;
+    b += al256((size_t)nb * sizeof(int32_t));
+    const int64_t m = kRsBins * nrs > nb ? kRsBins * nrs : nb;
     b += scan_ws_bytes(m);
     return b + 256;
 }
 
 int gsc_conv_plan(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n_out, int32_t K,
-                  int64_t cap_pairs, int32_t* perm, int32_t* p_in, int32_t* p_pos, int64_t* p_seg, int64_t* p_gidx,
-                  void* ws, size_t ws_bytes, void* stream) {
+                  int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, int64_t cap_items, void* ws,
+                  size_t ws_bytes, void* stream) {
     clear_error();
     if (K < 1 || K > kPlanMaxK) return fail(GSC_EINVAL, "conv_plan: K=%d outside [1,%d]", K, kPlanMaxK);
     if (n_out < 0 || n_out > INT32_MAX) return fail(GSC_EINVAL, "conv_plan: n_out=%lld invalid", (long long)n_out);
-    if (cap_pairs < 0) return fail(GSC_EINVAL, "conv_plan: cap_pairs < 0");
-    if (!p_seg || !p_gidx || !ws) return fail(GSC_EINVAL, "conv_plan: null p_seg/p_gidx/ws");
-    if (n_out > 0 && (!gidx || !perm)) return fail(GSC_EINVAL, "conv_plan: null gidx/perm");
-    if (cap_pairs > 0 && (!in_idx || !out_idx || !p_in || !p_pos))
-        return fail(GSC_EINVAL, "conv_plan: null in_idx/out_idx/p_in/p_pos");
+    if (!ibase || !ws) return fail(GSC_EINVAL, "conv_plan: null ibase/ws");
+    // in_idx / out_idx are read only where gidx lists pairs (NULL for a map without any)
+    if (n_out > 0 && (!gidx || !perm || !bmask || !items))
+        return fail(GSC_EINVAL, "conv_plan: null gidx/perm/bmask/items");
+    const int64_t need_items = (int64_t)K * gsc_plan_blocks(n_out);
+    if (cap_items < need_items)
+        return fail(GSC_ESHORT, "conv_plan: cap_items=%lld, need K*ceil(n_out/16) = %lld", (long long)cap_items,
+                    (long long)need_items);
     const size_t need = gsc_conv_plan_ws_bytes(n_out, K);
     if (ws_bytes < need) return fail(GSC_ESHORT, "conv_plan: ws needs %zu bytes, got %zu", need, ws_bytes);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (K <= 32)
-        return plan_enqueue<uint32_t>(in_idx, out_idx, gidx, n_out, K, cap_pairs, perm, p_in, p_pos, p_seg, p_gidx,
-                                      ws, s);
-    return plan_enqueue<unsigned long long>(in_idx, out_idx, gidx, n_out, K, cap_pairs, perm, p_in, p_pos, p_seg,
-                                            p_gidx, ws, s);
+    return plan_enqueue(in_idx, out_idx, gidx, n_out, K, perm, bmask, ibase, items, ws,
+                        reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

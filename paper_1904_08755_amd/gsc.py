@@ -51,14 +51,17 @@ _SIGS = {
     "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
     "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
                                       _c_i64p, _vp, _sz, _vp]),
+    "gsc_plan_blocks": (_i64, [_i64]),
     "gsc_conv_plan_ws_bytes": (_sz, [_i64, _i32]),
-    "gsc_conv_plan": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gsc_conv_plan": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "gsc_conv_block_engine": (_i32, [_i32, _i32, _i32, _i32]),
     "gsc_conv_fwd_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
-    "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _i64,
-                                           _vp, _i64, _vp, _sz, _vp]),
+    "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64,
+                                           _vp, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "gsc_conv_bwd_ws_bytes": (_sz, [_i64, _i32, _i32, _i32]),
     "gsc_sparse_conv_bwd": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp,
-                                           _vp, _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _i64, _vp, _sz, _vp]),
+                                           _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp,
+                                           _sz, _vp]),
 }
 
 _lib = None
@@ -180,7 +183,7 @@ class KernelMap:
     n_out: int
     offsets: np.ndarray        # K x D
     n_bound: int = 0           # n_pairs, or an upper bound of it
-    perm: Optional[torch.Tensor] = None   # plan form: out_idx holds positions, position i is row perm[i]
+    plan: Optional["BlockPlan"] = None    # block plan of the map (gsc_conv_plan), if built
 
     @property
     def K(self) -> int:
@@ -247,37 +250,50 @@ def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offs
                           sync=sync, bufs=bufs)
 
 
-class PlanBuffers:
-    """Caller-owned buffers of one convolution plan (reusable across calls)."""
+@dataclasses.dataclass
+class BlockPlan:
+    """Block plan of a kernel map (see gsc_conv_plan in include/gsc.h)."""
+    perm: torch.Tensor         # int32 [n_out]: output row at each position
+    bmask: torch.Tensor        # uint32 bits as int32 [nb]: union mask of each 16-position block
+    ibase: torch.Tensor        # int64 [nb + 1]: first item of each block
+    items: torch.Tensor        # int32 [cap_items, 16]: input rows of each item (-1: none)
 
-    def __init__(self, n_out: int, K: int, cap_pairs: int, device):
-        G = gsc_kmap_groups(n_out)
-        self.cap = int(cap_pairs)
+    def ptrs(self):
+        return _ptr(self.perm), _ptr(self.bmask), _ptr(self.ibase), _ptr(self.items)
+
+
+def gsc_plan_blocks(n_out: int) -> int:
+    return int(lib().gsc_plan_blocks(n_out))
+
+
+def gsc_conv_block_engine(dtype: int, c_red: int, c_out: int, K: int) -> bool:
+    return bool(lib().gsc_conv_block_engine(dtype, c_red, c_out, K))
+
+
+class PlanBuffers:
+    """Caller-owned buffers of one block plan (reusable across calls)."""
+
+    def __init__(self, n_out: int, K: int, device):
+        nb = gsc_plan_blocks(n_out)
+        self.cap_items = K * nb
         self.perm = torch.empty(max(n_out, 1), dtype=torch.int32, device=device)
-        self.p_in = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
-        self.p_pos = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
-        self.p_seg = torch.empty(K + 1, dtype=torch.int64, device=device)
-        self.p_gidx = torch.empty(K * G + 1, dtype=torch.int64, device=device)
+        self.bmask = torch.empty(max(nb, 1), dtype=torch.int32, device=device)
+        self.ibase = torch.empty(nb + 1, dtype=torch.int64, device=device)
+        self.items = torch.empty((max(self.cap_items, 1), 16), dtype=torch.int32, device=device)
         self.ws = _ws(lib().gsc_conv_plan_ws_bytes(n_out, K), device)
 
 
 def gsc_conv_plan(kmap: KernelMap, bufs: Optional[PlanBuffers] = None, stream=None) -> KernelMap:
-    """The map's pairs over output positions ordered by neighbour mask, with
-    perm (position -> output row): the tile plan the convolution kernels use."""
-    if kmap.perm is not None:
-        raise ValueError("the map is already a plan")
+    """The map with its block plan attached (rows ordered by neighbour mask,
+    16-row blocks, per-block items of 16 input rows)."""
     n_out, K = kmap.n_out, kmap.K
-    cap = int(kmap.in_idx.numel())
     if bufs is None:
-        bufs = PlanBuffers(n_out, K, cap, kmap.seg.device)
-    _check(lib().gsc_conv_plan(_ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.gidx), n_out, K, min(cap, bufs.cap),
-                               _ptr(bufs.perm), _ptr(bufs.p_in), _ptr(bufs.p_pos), _ptr(bufs.p_seg),
-                               _ptr(bufs.p_gidx), _ptr(bufs.ws), bufs.ws.numel(), _stream(stream)))
-    m = kmap.n_pairs
-    p_in = bufs.p_in if m is None else bufs.p_in[:m]
-    p_pos = bufs.p_pos if m is None else bufs.p_pos[:m]
-    return KernelMap(p_in, p_pos, bufs.p_seg, bufs.p_gidx, m, n_out, kmap.offsets, kmap.n_bound,
-                     bufs.perm[:n_out])
+        bufs = PlanBuffers(n_out, K, kmap.seg.device)
+    _check(lib().gsc_conv_plan(_ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.gidx), n_out, K, _ptr(bufs.perm),
+                               _ptr(bufs.bmask), _ptr(bufs.ibase), _ptr(bufs.items), bufs.cap_items,
+                               _ptr(bufs.ws), bufs.ws.numel(), _stream(stream)))
+    plan = BlockPlan(bufs.perm[:n_out], bufs.bmask, bufs.ibase, bufs.items)
+    return dataclasses.replace(kmap, plan=plan)
 
 
 def negation_permutation(offsets) -> np.ndarray:
@@ -296,6 +312,10 @@ def _dt(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return GSC_BF16
     raise ValueError(f"unsupported feature dtype {t.dtype}")
+
+
+def _plan_ptrs(kmap: KernelMap):
+    return kmap.plan.ptrs() if kmap.plan is not None else (None, None, None, None)
 
 
 def gsc_conv_fwd_ws_bytes(dtype: int, c_in: int, c_out: int, K: int) -> int:
@@ -320,8 +340,8 @@ def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out
     if ws is None and need > 0:
         ws = _ws(need, X.device)
     _check(lib().gsc_sparse_conv_fwd(dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx),
-                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), _ptr(kmap.perm),
-                                     kmap.n_bound, _ptr(Y),
+                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_bound,
+                                     *_plan_ptrs(kmap), _ptr(Y),
                                      n_out, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
     return Y
 
@@ -346,8 +366,6 @@ def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap
         raise ValueError("shape mismatch")
     if kmap.n_out != n_out or tmap.n_out != n_in:
         raise ValueError("kernel maps do not match the row counts")
-    if need_dw and kmap.perm is not None:
-        raise ValueError("the forward map (used for dW) must be in row form, not a plan")
     dev = X.device
     if need_dx and dX is None:
         dX = torch.empty((n_in, ci), dtype=X.dtype, device=dev)
@@ -359,7 +377,7 @@ def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap
     _check(lib().gsc_sparse_conv_bwd(
         dt, _ptr(X), _ptr(W), _ptr(dY), n_in, ci, co, K,
         _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg), kmap.n_bound,
-        _ptr(tmap.in_idx), _ptr(tmap.out_idx), _ptr(tmap.seg), _ptr(tmap.gidx), _ptr(tmap.perm), tmap.n_bound, sel,
+        _ptr(tmap.in_idx), _ptr(tmap.out_idx), _ptr(tmap.seg), _ptr(tmap.gidx), tmap.n_bound, sel, *_plan_ptrs(tmap),
         _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
         _ptr(ws) if need_dw else None, ws.numel() if need_dw else 0, _stream(stream)))
     return (dX if need_dx else None), (dW if need_dw else None)

@@ -10,10 +10,11 @@ their asynchronous modes (the pair count stays on the device), so a pass of a
 submanifold layer has no host round trip at all; a strided layer needs one,
 to learn how many output coordinates it has.
 
-Tile plans: with ``use_plan`` (the default) every map the convolution
-kernels read is first ordered by neighbour mask (gsc_conv_plan), so their
-output tiles touch few offsets; the weight gradients use the maps in row
-form.
+Block plans: with ``use_plan`` (the default) every map that a block engine
+can use (gsc_conv_block_engine) gets its block plan (gsc_conv_plan): output
+rows ordered by neighbour mask, 16-row blocks with their per-offset items.
+The forward and input-gradient passes then run on the plan; the weight
+gradients always use the maps in row form.
 
 Map reuse (Sec. 4.2 builds the kernel map once per coordinate pair):
   * submanifold layer with a symmetric region: the input-gradient map is the
@@ -98,10 +99,13 @@ class StepPlan:
                 self.host_offs_neg = gsc._host_i32(-offs)
                 wsel = np.arange(K, dtype=np.int32)
             self.host_wsel = gsc._host_i32(wsel)
-            if use_plan:
-                self.pb = gsc.PlanBuffers(n, K, self.mb.cap, dev)
+            dt = gsc._dt(dw.X)
+            self.plan_maps = use_plan and (gsc.gsc_conv_block_engine(dt, L.c_in, L.c_out, K)
+                                           or gsc.gsc_conv_block_engine(dt, L.c_out, L.c_in, K))
+            if self.plan_maps:
+                self.pb = gsc.PlanBuffers(n, K, dev)
                 if not self.symmetric:
-                    self.tpb = gsc.PlanBuffers(n, K, self.tb.cap, dev)
+                    self.tpb = gsc.PlanBuffers(n, K, dev)
             self.ws_fwd = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(gsc._dt(dw.X), L.c_in, L.c_out, K), dev)
             self.Y = torch.empty((n, L.c_out), dtype=feat, device=dev)
             self.dX = torch.empty((n, L.c_in), dtype=feat, device=dev)
@@ -118,10 +122,15 @@ class StepPlan:
             self.host_offs = gsc._host_i32(offs)
             self.host_offs_neg = gsc._host_i32(-offs)
             self.host_ident = gsc._host_i32(np.arange(K, dtype=np.int32))
-            if use_plan:
-                self.pkd = gsc.PlanBuffers(n, K, self.kd.cap, dev)
-                self.ptd = gsc.PlanBuffers(n, K, self.td.cap, dev)
             dt = gsc._dt(dw.X)
+            eng = lambda a, b: gsc.gsc_conv_block_engine(dt, a, b, K)
+            # kd feeds layer 0's forward and layer 1's dX; td layer 1's forward and layer 0's dX
+            self.plan_kd = use_plan and (eng(L0.c_in, L0.c_out) or eng(L1.c_out, L1.c_in))
+            self.plan_td = use_plan and (eng(L1.c_in, L1.c_out) or eng(L0.c_out, L0.c_in))
+            if self.plan_kd:
+                self.pkd = gsc.PlanBuffers(n, K, dev)
+            if self.plan_td:
+                self.ptd = gsc.PlanBuffers(n, K, dev)
             self.ws_fwd1 = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(dt, L0.c_in, L0.c_out, K), dev)
             self.ws_fwd2 = gsc._ws(gsc.gsc_conv_fwd_ws_bytes(dt, L1.c_in, L1.c_out, K), dev)
             self.Y1 = torch.empty((n, L0.c_out), dtype=feat, device=dev)
@@ -153,14 +162,14 @@ class StepPlan:
                                           host_offsets=self.host_offs_neg)
             mark("map")
             fmap, dxmap = kmap, tmap
-            if self.use_plan:
+            if self.plan_maps:
                 fmap = gsc.gsc_conv_plan(kmap, self.pb, stream=stream)
                 dxmap = fmap if self.symmetric else gsc.gsc_conv_plan(tmap, self.tpb, stream=stream)
                 self.plans = [fmap]
             mark("plan")
             Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], fmap, Y=self.Y, stream=stream, ws=self.ws_fwd)
             mark("fwd")
-            dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, kmap, dxmap, None, dX=self.dX, dW=self.dW,
+            dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, fmap, dxmap, None, dX=self.dX, dW=self.dW,
                                              ws=self.ws_bwd, stream=stream, host_wsel=self.host_wsel)
             mark("bwd")
             return StepResult(None, [kmap], [Y], dX, [dW], [])
@@ -174,18 +183,16 @@ class StepPlan:
         td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
                                 host_offsets=self.host_offs_neg)
         mark("map")
-        pkd, ptd = kd, td
-        if self.use_plan:
-            pkd = gsc.gsc_conv_plan(kd, self.pkd, stream=stream)
-            ptd = gsc.gsc_conv_plan(td, self.ptd, stream=stream)
-            self.plans = [pkd, ptd]
+        pkd = gsc.gsc_conv_plan(kd, self.pkd, stream=stream) if self.plan_kd else kd
+        ptd = gsc.gsc_conv_plan(td, self.ptd, stream=stream) if self.plan_td else td
+        self.plans = [m for m in (pkd, ptd) if m.plan is not None]
         mark("plan")
         Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], pkd, Y=self.Y1[:n_out], stream=stream, ws=self.ws_fwd1)
         Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], ptd, Y=self.Y2, stream=stream, ws=self.ws_fwd2)
         mark("fwd")
-        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, td, pkd, None, dX=self.dY1[:n_out], dW=self.dW2,
+        dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, ptd, pkd, None, dX=self.dY1[:n_out], dW=self.dW2,
                                            ws=self.ws_bwd2, stream=stream, host_wsel=self.host_ident)
-        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, kd, ptd, None, dX=self.dX, dW=self.dW1,
+        dX, dW1 = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dY1, pkd, ptd, None, dX=self.dX, dW=self.dW1,
                                           ws=self.ws_bwd1, stream=stream, host_wsel=self.host_ident)
         mark("bwd")
         return StepResult(out_coords, [kd, td], [Y1, Y2], dX, [dW1, dW2], [dY1])

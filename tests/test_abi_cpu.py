@@ -123,7 +123,8 @@ def test_kernel_map_validation(L):
 def test_conv_validation(L):
     fake = ctypes.c_void_p(0x1000)
     fwd = lambda dt, ci, K, npairs=10, co=4, ws=None, wsb=0: L.gsc_sparse_conv_fwd(
-        dt, fake, 10, ci, fake, co, K, fake, fake, fake, fake, None, npairs, fake, 10, ws, wsb, None)
+        dt, fake, 10, ci, fake, co, K, fake, fake, fake, fake, npairs, None, None, None, None, fake, 10, ws, wsb,
+        None)
     assert fwd(7, 4, 27) == gsc.GSC_EINVAL
     assert fwd(0, 0, 27) == gsc.GSC_EINVAL
     assert fwd(0, 4, 0) == gsc.GSC_EINVAL
@@ -136,26 +137,39 @@ def test_conv_validation(L):
     assert fwd(gsc.GSC_BF16, 256, 27, co=256) == gsc.GSC_ESHORT
     assert fwd(gsc.GSC_BF16, 256, 27, co=256, ws=fake, wsb=need - 1) == gsc.GSC_ESHORT
     sel = (ctypes.c_int32 * 2)(0, 2)   # 2 is out of range for K = 2
-    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, None,
-                               10, sel, fake, None, 10, None, 0, None)
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake,
+                               10, sel, None, None, None, None, fake, None, 10, None, 0, None)
     assert rc == gsc.GSC_EINVAL and "t_wsel" in _err(L)
     sel = (ctypes.c_int32 * 2)(0, 1)
-    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake, None,
-                               10, sel, None, ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)), 10, fake, 8, None)
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake,
+                               10, sel, None, None, None, None, None,
+                               ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)), 10, fake, 8, None)
     assert rc == gsc.GSC_ESHORT
 
 
 def test_plan_validation(L):
     fake = ctypes.c_void_p(0x1000)
     ws = L.gsc_conv_plan_ws_bytes(100, 27)
-    assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 65) == 0
-    plan = lambda K, wsb=ws, cap=10, seg=fake: L.gsc_conv_plan(fake, fake, fake, 100, K, cap, fake, fake, fake, seg,
-                                                               fake, fake, wsb, None)
-    assert plan(65) == gsc.GSC_EINVAL and "K=65" in _err(L)
+    assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 33) == 0
+    assert L.gsc_plan_blocks(0) == 0 and L.gsc_plan_blocks(16) == 1 and L.gsc_plan_blocks(17) == 2
+    cap = 27 * 7
+    plan = lambda K, wsb=ws, cap=cap, ib=fake: L.gsc_conv_plan(fake, fake, fake, 100, K, fake, fake, ib, fake, cap,
+                                                               fake, wsb, None)
+    assert plan(33) == gsc.GSC_EINVAL and "K=33" in _err(L)
     assert plan(0) == gsc.GSC_EINVAL
     assert plan(27, wsb=ws - 1) == gsc.GSC_ESHORT
-    assert plan(27, cap=-1) == gsc.GSC_EINVAL
-    assert plan(27, seg=None) == gsc.GSC_EINVAL
+    assert plan(27, cap=cap - 1) == gsc.GSC_ESHORT and str(cap) in _err(L)
+    assert plan(27, ib=None) == gsc.GSC_EINVAL
+    # the block engines and the shapes they take
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 27) == 1
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 9) == 1
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 10) == 0
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33) == 0
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 3, 16, 27) == 0
+    # a plan is all four pointers or none
+    rc = L.gsc_sparse_conv_fwd(0, fake, 10, 16, fake, 16, 27, fake, fake, fake, fake, 10, fake, None, fake, fake,
+                               fake, 10, None, 0, None)
+    assert rc == gsc.GSC_EINVAL and "plan" in _err(L)
 
 
 @pytest.mark.parametrize("name,K,D", [("cube", 3, 3), ("cube", 2, 3), ("cube", 5, 4), ("cross", 5, 3),

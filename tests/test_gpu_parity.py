@@ -223,30 +223,48 @@ def test_bf16_wide_channel_engine(ci, co, region):
     _conv_case(coords, ci, co, offs, 91, dtype="bf16")
 
 
-def _check_plan(km, plan):
-    """The plan lists the map's pairs over positions ordered by neighbour mask."""
+def _check_plan(km):
+    """The block plan of a map: rows stably sorted by neighbour mask, 16-row
+    blocks with their union masks and item bases, and each item holding the
+    input rows of its block's positions at its offset (-1 where none)."""
+    pl = km.plan
     n, K = km.n_out, km.K
-    perm = plan.perm.cpu().numpy().astype(np.int64)
+    nb = (n + 15) // 16
+    perm = pl.perm.cpu().numpy().astype(np.int64)
     assert np.array_equal(np.sort(perm), np.arange(n))
     pairs = gpu_pairs(km)
-    mask = np.zeros(n, np.uint64)
-    for k, (_, o) in enumerate(pairs):
-        mask[o] |= np.uint64(1) << np.uint64(k)
+    mask = np.zeros(n, np.int64)
+    nbr = np.full((max(n, 1), K), -1, np.int64)
+    for k, (i, o) in enumerate(pairs):
+        mask[o] |= np.int64(1) << np.int64(k)
+        nbr[o, k] = i
     ms = mask[perm]
     assert np.all(ms[1:] >= ms[:-1])                                   # sorted by mask
     same = ms[1:] == ms[:-1]
     assert np.all(perm[1:][same] > perm[:-1][same])                    # stable: row order within a mask
-    ppairs = gpu_pairs(plan)
+    bm = pl.bmask.cpu().numpy()[:nb].astype(np.int64) & 0xFFFFFFFF
+    msp = np.zeros(nb * 16, np.int64)
+    msp[:n] = ms
+    assert np.array_equal(bm, np.bitwise_or.reduce(msp.reshape(nb, 16), axis=1) if nb else bm)
+    cnt = np.array([bin(int(x)).count("1") for x in bm], np.int64)
+    ib = pl.ibase.cpu().numpy()[: nb + 1]
+    assert ib[0] == 0 and np.array_equal(np.diff(ib), cnt)
+    items = pl.items.cpu().numpy()[: ib[-1]]
+    below = np.zeros(nb, np.int64)                                     # set bits of bmask below offset k
+    pos = np.arange(nb)[:, None] * 16 + np.arange(16)[None, :]
+    rows = perm[np.minimum(pos, max(n - 1, 0))] if n else pos
     for k in range(K):
-        pi, pp = ppairs[k]
-        assert np.all(np.diff(pp) > 0)
-        order = np.argsort(perm[pp], kind="stable")
-        assert np.array_equal(perm[pp][order], pairs[k][1]) and np.array_equal(pi[order], pairs[k][0])
-    check_gidx(plan)
+        blocks = np.nonzero((bm >> k) & 1)[0]
+        if len(blocks):
+            exp = np.where(pos[blocks] < n, nbr[rows[blocks], k], -1)
+            assert np.array_equal(items[ib[blocks] + below[blocks]], exp), k
+        below += (bm >> k) & 1
 
 
 @pytest.mark.parametrize("cid", [1, 2, 3])
-def test_conv_plan_same_pairs_same_results(cid):
+def test_conv_plan_block_engine(cid):
+    # the block engines on the plan against the oracle, the row-form kernels
+    # and themselves (deterministic)
     wl = WL.make_workload(cid, scale=0.3)
     _say(f"[gpu] plan {wl.name} n={wl.n}")
     dw = pipeline.to_device(wl, DEV)
@@ -254,25 +272,87 @@ def test_conv_plan_same_pairs_same_results(cid):
     planned = pipeline.StepPlan(dw, use_plan=True)
     res = planned.run()
     torch.cuda.synchronize()
-    for km, pl in zip(res.kmaps, planned.plans):
-        _check_plan(km, pl)
-    # per output row the plan changes neither the pairs nor their order of
-    # accumulation (offset order), so the results are identical
+    assert planned.plans
+    for km in planned.plans:
+        _check_plan(km)
+    compare_step(wl, res, oracle_step(wl))
     for a, b in zip(base.Ys + [base.dX], res.Ys + [res.dX]):
-        assert torch.equal(a, b)
-    for a, b in zip(base.dWs, res.dWs):
+        assert rel_err(to_np(b), to_np(a)) <= TOL["f32"]
+    for a, b in zip(base.dWs, res.dWs):   # same map; inner layers' inputs differ by rounding only
+        assert rel_err(to_np(b), to_np(a)) <= TOL["f32"]
+    again = planned.run()
+    torch.cuda.synchronize()
+    for a, b in zip(res.Ys + [res.dX], again.Ys + [again.dX]):
         assert torch.equal(a, b)
 
 
-def test_conv_plan_bf16_wide():
+def test_conv_plan_structure_bf16_wide():
+    # the plan depends only on the map: build it for the wide workload's map
     wl = WL.make_workload(4, scale=0.3)
     dw = pipeline.to_device(wl, DEV)
-    base = pipeline.StepPlan(dw, use_plan=False).run()
-    planned = pipeline.StepPlan(dw, use_plan=True)
-    res = planned.run()
+    table = gsc.gsc_coords_build(dw.coords)
+    km = gsc.gsc_kernel_map(table, dw.coords, dw.offsets[0])
+    _check_plan(gsc.gsc_conv_plan(km))
+
+
+def _plan_case(coords, ci, co, offs, seed, ts=1):
+    """_conv_case through the block engine: plans of the forward and the
+    role-reversed map, fp32."""
+    c = _t(coords)
+    X, _ = WL.random_features(seed, len(coords), ci)
+    W, _ = WL.random_weights(seed, len(offs), ci, co)
+    G, _ = WL.random_features(seed + 1, len(coords), co)
+    tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
+    table = gsc.gsc_coords_build(c)
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(table, c, offs, tensor_stride=ts))
+    tm = gsc.gsc_conv_plan(gsc.transposed_kernel_map(table, c, offs, tensor_stride=ts))
+    Y = gsc.gsc_sparse_conv_fwd(tX, tW, km)
+    dX, _ = gsc.gsc_sparse_conv_bwd(tX, tW, tG, km, tm, np.arange(len(offs)), need_dw=False)
     torch.cuda.synchronize()
-    _check_plan(res.kmaps[0], planned.plans[0])
-    assert torch.equal(base.Ys[0], res.Ys[0]) and torch.equal(base.dX, res.dX)
+    _check_plan(km)
+    _check_plan(tm)
+    m = O.kernel_map(coords, coords, np.asarray(offs), ts)
+    assert rel_err(to_np(Y), O.conv_forward(X, W, m, len(coords))) <= TOL["f32"]
+    assert rel_err(to_np(dX), O.conv_backward(X, W, G, m)[0]) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("ci,co,region", [(16, 16, "cube3"), (16, 64, "cube3"), (64, 16, "cube2"), (32, 64, "cube2"),
+                                           (64, 32, "cube2"), (64, 64, "cube2"), (32, 32, "cube2")])
+def test_block_engine_shapes(ci, co, region):
+    coords = WL.random_coords(120 + ci + co, 3000, 3, -12, 12, batch=2)
+    assert gsc.gsc_conv_block_engine(gsc.GSC_F32, ci, co, 27 if region == "cube3" else 8)
+    _say(f"[gpu] block engine {ci}->{co} {region}")
+    _plan_case(coords, ci, co, regions.hypercube(int(region[-1]), 3), 121)
+
+
+def test_block_engine_edges():
+    # one voxel, a ragged last block, no input rows, 4D hybrid region
+    _plan_case(np.array([[0, -7, 3, 11]], np.int32), 16, 32, regions.hypercube(3, 3), 131)
+    _plan_case(WL.random_coords(132, 37, 3, -3, 3, batch=2), 32, 32, regions.hypercube(3, 3), 132)
+    _plan_case(WL.random_coords(133, 2000, 4, -5, 5, batch=1), 32, 32, regions.hybrid(3, 4), 133)
+    c = torch.empty((0, 4), dtype=torch.int32, device=DEV)
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, regions.hypercube(3, 3)))
+    Y = gsc.gsc_sparse_conv_fwd(torch.empty((0, 16), device=DEV), torch.randn((27, 16, 16), device=DEV), km)
+    assert Y.shape == (0, 16)
+    # outputs no input reaches (a plan with empty blocks) and an input with no rows
+    cin = np.array([[0, 100, 100, 100], [0, 101, 100, 100]], np.int32)
+    cout = WL.random_coords(134, 40, 3, -3, 3, batch=1)
+    cout = np.concatenate([cout, np.array([[0, 100, 100, 99]], np.int32)])
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(cin)), _t(cout), regions.hypercube(3, 3)))
+    X = torch.randn((2, 16), device=DEV)
+    W = torch.randn((27, 16, 32), device=DEV)
+    Y = gsc.gsc_sparse_conv_fwd(X, W, km)
+    torch.cuda.synchronize()
+    ref = O.conv_forward(X.cpu().numpy(), W.cpu().numpy(), O.kernel_map(cin, cout, O.hypercube(3, 3)), len(cout))
+    assert rel_err(to_np(Y), ref) <= TOL["f32"] and np.all(to_np(Y)[:-1] == 0)
+    _check_plan(km)
+    empty_in = torch.empty((0, 16), device=DEV)
+    km0 = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(torch.empty((0, 4), dtype=torch.int32,
+                                                                                device=DEV)),
+                                               _t(cout), regions.hypercube(3, 3)))
+    Y0 = gsc.gsc_sparse_conv_fwd(empty_in, W, km0)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(Y0).item() == 0 and Y0.shape == (len(cout), 32)
 
 
 def test_4d_hybrid_and_tesseract():
