@@ -143,6 +143,10 @@ size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D);
  * [gidx[k*G + g], gidx[k*G + g + 1]); gidx[K*G] = n_pairs.  gidx is what the
  * convolution kernels use to find the pairs of a tile of output rows.
  *
+ * nbr (nullable, device, K * n_out int32): when given, the call also writes
+ * the map's dense form, nbr[k * n_out + j] = the input row paired with output
+ * row j at offset k, or -1 (the input of gsc_conv_plan).
+ *
  * *n_pairs (host) receives the total.  If it exceeds cap_pairs, nothing is
  * written to in_idx/out_idx and ESHORT is returned with *n_pairs set, so the
  * caller can allocate and call again.  Synchronises `stream` once.
@@ -161,7 +165,7 @@ size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D);
 int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D,
                    const int32_t* offsets, int32_t K, const int32_t* tensor_stride,
                    int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
-                   int64_t* seg, int64_t* gidx, int64_t* n_pairs,
+                   int64_t* seg, int64_t* gidx, int32_t* nbr, int64_t* n_pairs,
                    void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
@@ -176,10 +180,10 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
  * rows.  The plan orders the output rows by neighbour mask (bit k set when
  * the row has a pair at offset k), so rows with equal masks share blocks.
  *
- * Input: a kernel map as gsc_kernel_map produces it (in_idx, out_idx, gidx
- * over n_out output rows; K <= 32 offsets; the pair count is read on the
- * device from gidx[K * G]; in_idx and out_idx may be NULL for a map without
- * pairs).  Output (device, caller-allocated), with
+ * Input: the dense form of a kernel map over n_out output rows with K <= 32
+ * offsets, nbr[k * n_out + j] = input row paired with output row j at offset
+ * k or -1 (as gsc_kernel_map writes it).  Output (device, caller-allocated),
+ * with
  * nb = gsc_plan_blocks(n_out) = ceil(n_out / 16):
  *   perm[n_out]       perm[i] = the output row at position i (a stable sort
  *                     of the rows by mask);
@@ -194,7 +198,7 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
  * Errors: EINVAL (K > 32, null pointers), ESHORT (cap_items, ws), EHIP. */
 int64_t gsc_plan_blocks(int64_t n_out);
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K);
-int gsc_conv_plan(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n_out, int32_t K,
+int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K,
                   int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, int64_t cap_items,
                   void* ws, size_t ws_bytes, void* stream);
 

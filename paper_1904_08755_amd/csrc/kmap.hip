@@ -1,13 +1,14 @@
 // Kernel map (a3): for every offset o_k and output row j, the input row of
 // u_j + ts (.) o_k, if present.  Two passes over (output row, offset):
-//   count: one lane per output row; per offset a wave64 ballot of hits gives
-//          the pair count of every 64-row group;
+//   count: one lane per output row probes the table for every offset; the
+//          input row found (or -1) goes to a dense offset-major neighbour
+//          table nbr[k][j], and per offset a wave64 ballot of hits gives the
+//          pair count of every 64-row group;
 //   scan:  exclusive scan of the (offset-major, group-minor) counts gives the
 //          start of each group's pairs (the group index gidx) and the total;
-//   fill:  from the hit masks kept by the count pass, each hit is placed at
-//          its group start plus its rank among the wave's hits (popcount of
-//          the lower-lane mask);
-//   resolve: one lane per pair probes the table again for the input row.
+//   fill:  each hit is placed at its group start plus its rank among the
+//          wave's hits (popcount of the lower-lane mask), its input row read
+//          from the neighbour table.
 // Pairs of one offset therefore come out sorted by output row, and the
 // result does not depend on scheduling.
 #include <climits>
@@ -71,14 +72,15 @@ struct KeyOps<unsigned long long> {
 // Count pass.  Each lane owns one output row.  Offsets are probed kBatch at a
 // time; every load is issued unconditionally (a lane whose query is out of
 // the box reads slot 0 and ignores it) so the kBatch loads are in flight
-// together, and collision chains are followed in rounds.  Hits are recorded
-// in a bit mask per row (word w of row j at hits[w * n_out + j]) and counted
-// per 64-row group with a wave ballot.
+// together, and collision chains are followed in rounds.  A probe reads the
+// whole 16-byte slot, so a hit also yields the input row, which goes to
+// nbr[k * n_out + j] (-1 for a miss); hits are counted per 64-row group with
+// a wave ballot.
 template <typename KeyT, typename Offs>
 __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __restrict__ slots,
                                            const int32_t* __restrict__ out_coords, int64_t n_out, int ncol,
                                            const Offs& offs, int K, int64_t G, int32_t* __restrict__ cnt,
-                                           uint32_t* __restrict__ hits, bool ok, int64_t j) {
+                                           int32_t* __restrict__ nbr, bool ok, int64_t j) {
     const bool valid = ok && j < n_out;
     const int D = ncol - 1;
     const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
@@ -112,11 +114,11 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
     in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    uint32_t word = 0;
     for (int k0 = 0; k0 < K; k0 += kBatch) {
         KeyT key[kBatch];
         unsigned long long pos[kBatch];
         bool pend[kBatch], hit[kBatch];
+        int32_t row[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
             const int k = min(k0 + b, K - 1);
@@ -141,22 +143,28 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
             pos[b] = in ? hs : 0;
             pend[b] = in;
             hit[b] = false;
+            row[b] = -1;
         }
         for (unsigned long long round = 0; round <= mask; ++round) {
-            unsigned long long ek[kBatch];
+            Slot e[kBatch];
             if (round == 0) {
 #pragma unroll
-                for (int b = 0; b < kBatch; ++b) ek[b] = slots[pos[b]].key;   // unconditional: all in flight
+                for (int b = 0; b < kBatch; ++b) e[b] = slots[pos[b]];   // unconditional: all in flight
             } else {   // collision chains: few probes still pending
 #pragma unroll
-                for (int b = 0; b < kBatch; ++b) ek[b] = pend[b] ? slots[pos[b]].key : kEmptyKey;
+                for (int b = 0; b < kBatch; ++b) {
+                    e[b].key = kEmptyKey;
+                    e[b].val = -1;
+                    if (pend[b]) e[b] = slots[pos[b]];
+                }
             }
             bool any = false;
 #pragma unroll
             for (int b = 0; b < kBatch; ++b) {
-                const bool h1 = pend[b] && KeyOps<KeyT>::eq(ek[b], key[b]);
-                const bool stop = h1 || ek[b] == kEmptyKey;
+                const bool h1 = pend[b] && KeyOps<KeyT>::eq(e[b].key, key[b]);
+                const bool stop = h1 || e[b].key == kEmptyKey;
                 hit[b] = hit[b] || h1;
+                row[b] = h1 ? e[b].val : row[b];
                 pend[b] = pend[b] && !stop;
                 pos[b] = pend[b] ? ((pos[b] + 1) & mask) : pos[b];
                 any = any || pend[b];
@@ -169,11 +177,7 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
             if (k < K) {
                 const unsigned long long m = __ballot(hit[b]);
                 if (writer) cnt[(int64_t)k * G + g] = __popcll(m);
-                word |= (uint32_t)hit[b] << (k & 31);
-                if ((k & 31) == 31 || k == K - 1) {
-                    if (j < n_out) hits[(int64_t)(k >> 5) * n_out + j] = word;
-                    word = 0;
-                }
+                if (j < n_out) nbr[(int64_t)k * n_out + j] = hit[b] ? row[b] : -1;
             }
         }
     }
@@ -182,7 +186,7 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
 template <typename Offs>
 __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* __restrict__ out_coords,
                                                          int64_t n_out, int ncol, Offs offs, int K, int64_t G,
-                                                         int32_t* __restrict__ cnt, uint32_t* __restrict__ hits,
+                                                         int32_t* __restrict__ cnt, int32_t* __restrict__ nbr,
                                                          int64_t* err) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
     const Slot* __restrict__ slots = table_slots(table);
@@ -190,59 +194,38 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
     if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     if (h->total_bits <= 32)   // uniform: all lanes take the same path
-        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, hits, ok, j);
+        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, nbr, ok, j);
     else
-        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, hits, ok, j);
+        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, nbr, ok, j);
 }
 
-// Fill pass: the ballots come from the hit masks; each hit gets its position
-// (group start + rank among the wave's hits), out_idx = j, and temporarily
-// in_idx = k, which the resolve pass replaces by the input row.
-__global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, int64_t G, const uint32_t* hits,
-                                                        const int64_t* gidx, int32_t* in_idx, int32_t* out_idx) {
+// Fill pass: lane j reads its row of the neighbour table offset by offset;
+// each hit goes to its group start plus its rank among the wave's hits.
+__global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, int64_t G,
+                                                        const int32_t* __restrict__ nbr,
+                                                        const int64_t* __restrict__ gidx, int32_t* __restrict__ in_idx,
+                                                        int32_t* __restrict__ out_idx, int64_t cap) {
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     const bool valid = j < n_out;
     const int64_t g = j >> 6;
     const unsigned long long below = lanemask_lt();
-    uint32_t word = 0;
-    for (int k = 0; k < K; ++k) {
-        if ((k & 31) == 0) word = valid ? hits[(int64_t)(k >> 5) * n_out + j] : 0u;
-        const bool hit = (word >> (k & 31)) & 1u;
-        const unsigned long long m = __ballot(hit);
-        if (hit) {
-            const int64_t pos = gidx[(int64_t)k * G + g] + __popcll(m & below);
-            in_idx[pos] = k;
-            out_idx[pos] = (int32_t)j;
-        }
-    }
-}
-
-// Resolve pass: one lane per pair probes u_j + o_k (a guaranteed hit).  The
-// pair count is read on the device (gidx[K*G]), so the grid only has to cover
-// an upper bound; lanes stride over it (in plain block order, which spreads
-// the real pairs over all XCDs whatever the bound).
-template <typename Offs>
-__global__ void __launch_bounds__(kThreads) k_kmap_resolve(const void* table, const int32_t* __restrict__ out_coords,
-                                                           int ncol, Offs offs, const int64_t* total,
-                                                           int32_t* __restrict__ in_idx,
-                                                           const int32_t* __restrict__ out_idx) {
-    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    const Slot* __restrict__ slots = table_slots(table);
-    const TableView tv = table_view(h, ncol);
-    const int64_t n_pairs = *total;
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < n_pairs; p += stride) {
-        const int64_t j = out_idx[p];
-        const int k = in_idx[p];
-        const int32_t* o = offs.at((int64_t)k * (ncol - 1));
-        int64_t q[kMaxCols];
+    constexpr int B = 8;   // offsets whose table entries are loaded together
+    for (int k0 = 0; k0 < K; k0 += B) {
+        int32_t r[B];
 #pragma unroll
-        for (int c = 0; c < kMaxCols; ++c)
-            q[c] = c < ncol ? (int64_t)out_coords[j * ncol + c] + (c > 0 ? o[c - 1] : 0) : 0;
-        unsigned long long key;
-        int32_t r = -1;
-        if (pack_key(tv, q, &key)) r = table_find(tv, slots, key);
-        in_idx[p] = r;
+        for (int b = 0; b < B; ++b) r[b] = valid && k0 + b < K ? nbr[(int64_t)(k0 + b) * n_out + j] : -1;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const bool hit = r[b] >= 0;
+            const unsigned long long m = __ballot(hit);
+            if (hit) {
+                const int64_t pos = gidx[(int64_t)(k0 + b) * G + g] + __popcll(m & below);
+                if (pos < cap) {
+                    in_idx[pos] = r[b];
+                    out_idx[pos] = (int32_t)j;
+                }
+            }
+        }
     }
 }
 
@@ -251,11 +234,11 @@ static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 template <typename Offs>
 static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t n_out, int ncol, Offs offs, int K,
                         int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg, int64_t* gidx,
-                        int64_t* n_pairs, int64_t* res, int32_t* cnt, uint32_t* hits, void* scan_ws, hipStream_t s) {
+                        int64_t* n_pairs, int64_t* res, int32_t* cnt, int32_t* nbr, void* scan_ws, hipStream_t s) {
     const unsigned nblk = (unsigned)((n_out + kThreads - 1) / kThreads);
     if (nblk > 0) {
         hipLaunchKernelGGL((k_kmap_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol,
-                           offs, K, G, cnt, hits, res + 1);
+                           offs, K, G, cnt, nbr, res + 1);
         GSC_LAUNCH_CHECK();
     }
     int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
@@ -277,12 +260,8 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
         bound = hres[0];
     }
     if (nblk > 0 && bound > 0) {
-        hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, n_out, K, G, hits, gidx, in_idx, out_idx);
-        GSC_LAUNCH_CHECK();
-        int64_t rb = (bound + kThreads - 1) / kThreads;
-        if (rb > 4096) rb = 4096;
-        hipLaunchKernelGGL((k_kmap_resolve<Offs>), dim3((unsigned)rb), dim3(kThreads), 0, s, in_table, out_coords,
-                           ncol, offs, (const int64_t*)res, in_idx, out_idx);
+        hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, n_out, K, G, nbr, gidx, in_idx, out_idx,
+                           cap_pairs);
         GSC_LAUNCH_CHECK();
     }
     return GSC_OK;
@@ -302,14 +281,15 @@ size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D) {
     size_t b = align256((size_t)K * D * sizeof(int32_t));      // offsets (scaled)
     b += align256(2 * sizeof(int64_t));                         // total, error flag
     b += align256((size_t)K * G * sizeof(int32_t));             // counts
-    b += align256((size_t)((K + 31) / 32) * n_out * sizeof(uint32_t));   // hit masks
+    b += align256((size_t)K * n_out * sizeof(int32_t));         // neighbour table
     b += scan_ws_bytes(K * G);
     return b + 256;
 }
 
 int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D, const int32_t* offsets,
                    int32_t K, const int32_t* tensor_stride, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
-                   int64_t* seg, int64_t* gidx, int64_t* n_pairs, void* ws, size_t ws_bytes, void* stream) {
+                   int64_t* seg, int64_t* gidx, int32_t* nbr_out, int64_t* n_pairs, void* ws, size_t ws_bytes,
+                   void* stream) {
     clear_error();
     if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "kernel_map: D=%d outside [1,%d]", D, kMaxCols - 1);
     if (K < 1) return fail(GSC_EINVAL, "kernel_map: K=%d must be >= 1", K);
@@ -352,16 +332,16 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     w += align256(2 * sizeof(int64_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += align256((size_t)K * G * sizeof(int32_t));
-    uint32_t* hits = reinterpret_cast<uint32_t*>(w);
-    w += align256((size_t)((K + 31) / 32) * n_out * sizeof(uint32_t));
+    int32_t* nbr = nbr_out ? nbr_out : reinterpret_cast<int32_t*>(w);   // the caller's dense map, if asked for
+    w += align256((size_t)K * n_out * sizeof(int32_t));
     void* scan_ws = w;
     if (by_value)
         return kmap_enqueue(in_table, out_coords, n_out, ncol, arg, K, G, in_idx, out_idx, cap_pairs, seg, gidx,
-                            n_pairs, res, cnt, hits, scan_ws, s);
+                            n_pairs, res, cnt, nbr, scan_ws, s);
     // synchronous mode: the copy below completes before this call returns
     GSC_HIP(hipMemcpyAsync(d_offs, offs.data(), offs.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
     return kmap_enqueue(in_table, out_coords, n_out, ncol, OffsPtr{d_offs}, K, G, in_idx, out_idx, cap_pairs, seg,
-                        gidx, n_pairs, res, cnt, hits, scan_ws, s);
+                        gidx, n_pairs, res, cnt, nbr, scan_ws, s);
 }
 
 }  // extern "C"

@@ -19,11 +19,9 @@
 //   items[16*t + r]  for item t = ibase[b] + j, the j-th offset k of bmask[b]
 //                in increasing order: the input row paired with position
 //                16b + r at offset k, or -1 if there is none.
-// Steps:
-//   masks:  one wave per 64-row group of the map: every row's mask (LDS OR
-//           of the offsets' bits) and its row of the dense neighbour table
-//           nbr[row][k] (-1 where no pair), staged in LDS and written with
-//           coalesced stores;
+// Input: the map's dense form nbr[k][j] (input row or -1), which the kernel
+// map writes as it probes.  Steps:
+//   masks:  every row's mask from its column of nbr;
 //   sort:   stable LSD radix sort of (mask, row) by mask, 10-bit digits;
 //   count:  block unions and item counts; a scan gives ibase;
 //   fill:   one lane per position writes its entry of each of its block's
@@ -38,97 +36,66 @@ namespace gsc {
 constexpr int kPlanThreads = 256;
 constexpr int kRsBits = 10;                       // radix digit width
 constexpr int kRsBins = 1 << kRsBits;
-constexpr int kRsPer = 16;                        // keys per thread and block
-constexpr int kRsTile = kPlanThreads * kRsPer;    // keys per block
+constexpr int kRsThreads = 1024;                  // radix sort block
+constexpr int kRsPer = 4;                         // keys per thread and block
+constexpr int kRsTile = kRsThreads * kRsPer;      // keys per block
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // ---------------------------------------------------------------------------
-// masks + dense neighbour table
+// masks from the dense map
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ in_idx,
-                                                             const int32_t* __restrict__ out_idx,
-                                                             const int64_t* __restrict__ gidx, int K, int64_t G,
-                                                             int64_t n_out, uint32_t* __restrict__ keys,
-                                                             int32_t* __restrict__ nbr) {
-    __shared__ uint32_t sm[kPlanThreads / 64][64];
-    __shared__ int32_t sn[kPlanThreads / 64][64 * kPlanMaxK];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t g = (int64_t)blockIdx.x * (kPlanThreads / 64) + wave;
-    if (g >= G) return;   // no block barrier below
-    sm[wave][lane] = 0;
-    for (int i = lane; i < 64 * K; i += 64) sn[wave][i] = -1;
-    int64_t lo = 0;
-    int n = 0;
-    if (lane < K) {
-        lo = gidx[(int64_t)lane * G + g];
-        n = (int)(gidx[(int64_t)lane * G + g + 1] - lo);
-    }
-    wave_lds_sync();
-    const int64_t row0 = g * 64;
-    constexpr int B = 8;   // offsets whose pairs are loaded together
+__global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int K,
+                                                             uint32_t* __restrict__ keys) {
+    const int64_t j = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
+    if (j >= n) return;
+    uint32_t m = 0;
+    constexpr int B = 8;   // table entries loaded together
     for (int k0 = 0; k0 < K; k0 += B) {
-        int32_t o[B], r[B];
-        bool v[B];
+        int32_t r[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int k = min(k0 + b, K - 1);
-            const int64_t klo = __shfl(lo, k, 64);
-            const int kn = __shfl(n, k, 64);
-            v[b] = k0 + b < K && lane < kn;
-            if (v[b]) {
-                o[b] = out_idx[klo + lane];
-                r[b] = in_idx[klo + lane];
-            }
-        }
+        for (int b = 0; b < B; ++b) r[b] = k0 + b < K ? nbr[(int64_t)(k0 + b) * n + j] : -1;
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            if (v[b]) {
-                const int64_t rel = (int64_t)o[b] - row0;
-                if (rel >= 0 && rel < 64) {   // a consistent map has only this group's rows here
-                    atomicOr(&sm[wave][rel], 1u << (k0 + b));
-                    sn[wave][rel * K + k0 + b] = r[b];
-                }
-            }
-        }
+        for (int b = 0; b < B; ++b) m |= (uint32_t)(r[b] >= 0) << ((k0 + b) & 31);
     }
-    wave_lds_sync();
-    if (row0 + lane < n_out) keys[row0 + lane] = sm[wave][lane];
-    const int64_t rows = min((int64_t)64, n_out - row0);
-    for (int i = lane; i < rows * K; i += 64) nbr[row0 * K + i] = sn[wave][i];
+    keys[j] = m;
 }
 
 // ---------------------------------------------------------------------------
 // stable LSD radix sort of (key, value) by key
 // ---------------------------------------------------------------------------
 template <typename KeyT>
-__global__ void __launch_bounds__(kPlanThreads) k_rs_hist(const KeyT* __restrict__ keys, int64_t n, int shift,
-                                                          int32_t* __restrict__ hist, int64_t nb) {
+__global__ void __launch_bounds__(kRsThreads) k_rs_hist(const KeyT* __restrict__ keys, int64_t n, int shift,
+                                                        int32_t* __restrict__ hist, int64_t nb) {
     __shared__ int32_t h[kRsBins];
-    for (int i = threadIdx.x; i < kRsBins; i += kPlanThreads) h[i] = 0;
+    for (int i = threadIdx.x; i < kRsBins; i += kRsThreads) h[i] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kRsTile;
+    KeyT key[kRsPer];
 #pragma unroll
     for (int i = 0; i < kRsPer; ++i) {
-        const int64_t idx = base + (int64_t)i * kPlanThreads + threadIdx.x;
-        if (idx < n) atomicAdd(&h[(int)((keys[idx] >> shift) & (kRsBins - 1))], 1);
+        const int64_t idx = base + (int64_t)i * kRsThreads + threadIdx.x;
+        key[i] = idx < n ? keys[idx] : (KeyT)0;
     }
+#pragma unroll
+    for (int i = 0; i < kRsPer; ++i)
+        if (base + (int64_t)i * kRsThreads + threadIdx.x < n) atomicAdd(&h[(int)((key[i] >> shift) & (kRsBins - 1))], 1);
     __syncthreads();
-    for (int i = threadIdx.x; i < kRsBins; i += kPlanThreads) hist[(int64_t)i * nb + blockIdx.x] = h[i];
+    for (int i = threadIdx.x; i < kRsBins; i += kRsThreads) hist[(int64_t)i * nb + blockIdx.x] = h[i];
 }
 
-// Block b places its keys in rounds of 256 (in index order: stable).  All of
-// the block's keys are loaded first (16 per thread, in flight together).
-// Within a wave, lanes with equal digits are found with kRsBits ballots; the
-// wave's count of each digit goes to LDS, and a key's position is the block's
-// running start of its digit + the counts of lower waves in this round + its
-// rank in its wave.  vals_in == NULL means value = index.
+// Block b places its keys in rounds of kRsThreads (in index order: stable).
+// All of the block's keys are loaded first (kRsPer per thread, in flight
+// together).  Within a wave, lanes with equal digits are found with kRsBits
+// ballots; the wave's count of each digit goes to LDS, and a key's position
+// is the block's running start of its digit + the counts of lower waves in
+// this round + its rank in its wave.  vals_in == NULL means value = index.
 template <typename KeyT>
-__global__ void __launch_bounds__(kPlanThreads) k_rs_scatter(const KeyT* __restrict__ kin,
-                                                             const int32_t* __restrict__ vin, int64_t n, int shift,
-                                                             const int64_t* __restrict__ hoff, int64_t nb,
-                                                             KeyT* __restrict__ kout, int32_t* __restrict__ vout) {
-    constexpr int W = kPlanThreads / 64;
+__global__ void __launch_bounds__(kRsThreads) k_rs_scatter(const KeyT* __restrict__ kin,
+                                                           const int32_t* __restrict__ vin, int64_t n, int shift,
+                                                           const int64_t* __restrict__ hoff, int64_t nb,
+                                                           KeyT* __restrict__ kout, int32_t* __restrict__ vout) {
+    constexpr int W = kRsThreads / 64;
     __shared__ int64_t start[kRsBins];
     __shared__ int32_t wcnt[W][kRsBins];
     const int tid = threadIdx.x, wave = tid >> 6;
@@ -137,17 +104,17 @@ __global__ void __launch_bounds__(kPlanThreads) k_rs_scatter(const KeyT* __restr
     int32_t val[kRsPer];
 #pragma unroll
     for (int r = 0; r < kRsPer; ++r) {
-        const int64_t idx = base + (int64_t)r * kPlanThreads + tid;
+        const int64_t idx = base + (int64_t)r * kRsThreads + tid;
         const bool valid = idx < n;
         key[r] = valid ? kin[idx] : (KeyT)0;
         val[r] = valid ? (vin ? vin[idx] : (int32_t)idx) : 0;
     }
-    for (int i = tid; i < kRsBins; i += kPlanThreads) start[i] = hoff[(int64_t)i * nb + blockIdx.x];
-    for (int i = tid; i < W * kRsBins; i += kPlanThreads) (&wcnt[0][0])[i] = 0;
+    for (int i = tid; i < kRsBins; i += kRsThreads) start[i] = hoff[(int64_t)i * nb + blockIdx.x];
+    for (int i = tid; i < W * kRsBins; i += kRsThreads) (&wcnt[0][0])[i] = 0;
     const unsigned long long below = lanemask_lt();
 #pragma unroll
     for (int rnd = 0; rnd < kRsPer; ++rnd) {
-        const int64_t idx = base + (int64_t)rnd * kPlanThreads + tid;
+        const int64_t idx = base + (int64_t)rnd * kRsThreads + tid;
         const bool valid = idx < n;
         const int d = (int)((key[rnd] >> shift) & (kRsBins - 1));
         unsigned long long peers = __ballot(valid);
@@ -212,7 +179,7 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
                                                            const int32_t* __restrict__ perm,
                                                            const int32_t* __restrict__ nbr,
                                                            const int64_t* __restrict__ ibase, int64_t n, int64_t nb,
-                                                           int K, int32_t* __restrict__ items) {
+                                                           int32_t* __restrict__ items) {
     const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
     const int64_t b = i >> 4;
     const int r = threadIdx.x & 15;
@@ -222,18 +189,16 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
     if (b >= nb) return;   // whole blocks of 16 lanes leave together
     const int64_t row = valid ? perm[i] : 0;
     const int64_t base = ibase[b];
-    const int32_t* nrow = nbr + row * K;
     uint32_t m = u;
     for (int j = 0; m != 0; ++j) {
         const int k = __ffs(m) - 1;
         m &= m - 1;
-        items[(base + j) * 16 + r] = ((key >> k) & 1u) ? nrow[k] : -1;
+        items[(base + j) * 16 + r] = ((key >> k) & 1u) ? nbr[(int64_t)k * n + row] : -1;
     }
 }
 
-static int plan_enqueue(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n, int K,
-                        int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, void* ws, hipStream_t s) {
-    const int64_t G = (n + 63) / 64;
+static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
+                        int32_t* items, void* ws, hipStream_t s) {
     const int64_t nb = (n + 15) / 16;
     const int64_t nrs = (n + kRsTile - 1) / kRsTile;
     char* w = reinterpret_cast<char*>(ws);
@@ -249,8 +214,6 @@ static int plan_enqueue(const int32_t* in_idx, const int32_t* out_idx, const int
     w += al256((size_t)kRsBins * nrs * sizeof(int32_t));
     int64_t* hoff = reinterpret_cast<int64_t*>(w);
     w += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
-    int32_t* nbr = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)K * n * sizeof(int32_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)nb * sizeof(int32_t));
     void* scan_ws = w;
@@ -260,9 +223,8 @@ static int plan_enqueue(const int32_t* in_idx, const int32_t* out_idx, const int
         GSC_LAUNCH_CHECK();
         return GSC_OK;
     }
-    const unsigned gblocks = (unsigned)((G + kPlanThreads / 64 - 1) / (kPlanThreads / 64));
-    hipLaunchKernelGGL(k_plan_masks, dim3(gblocks), dim3(kPlanThreads), 0, s, in_idx, out_idx, gidx, K, G, n, ka,
-                       nbr);
+    const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
+    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka);
     GSC_LAUNCH_CHECK();
     const int passes = (K + kRsBits - 1) / kRsBits;
     const uint32_t* kin = ka;
@@ -270,23 +232,22 @@ static int plan_enqueue(const int32_t* in_idx, const int32_t* out_idx, const int
     for (int p = 0; p < passes; ++p) {
         uint32_t* kout = (p & 1) ? ka : kb;
         int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? va : vb);
-        hipLaunchKernelGGL((k_rs_hist<uint32_t>), dim3((unsigned)nrs), dim3(kPlanThreads), 0, s, kin, n,
+        hipLaunchKernelGGL((k_rs_hist<uint32_t>), dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, n,
                            p * kRsBits, hist, nrs);
         GSC_LAUNCH_CHECK();
         int rc = scan_counts(hist, kRsBins * nrs, hoff, nullptr, scan_ws, s);
         if (rc) return rc;
-        hipLaunchKernelGGL((k_rs_scatter<uint32_t>), dim3((unsigned)nrs), dim3(kPlanThreads), 0, s, kin, vin, n,
+        hipLaunchKernelGGL((k_rs_scatter<uint32_t>), dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n,
                            p * kRsBits, hoff, nrs, kout, vout);
         GSC_LAUNCH_CHECK();
         kin = kout;
         vin = vout;
     }
-    const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_blk_count, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, n, nb, bmask, cnt);
     GSC_LAUNCH_CHECK();
     int rc = scan_counts(cnt, nb, ibase, nullptr, scan_ws, s);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, perm, nbr, ibase, n, nb, K, items);
+    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, perm, nbr, ibase, n, nb, items);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
@@ -306,31 +267,27 @@ size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
     size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
     b += al256((size_t)kRsBins * nrs * sizeof(int32_t));
     b += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
-    b += al256((size_t)K * n_out * sizeof(int32_t));
     b += al256((size_t)nb * sizeof(int32_t));
     const int64_t m = kRsBins * nrs > nb ? kRsBins * nrs : nb;
     b += scan_ws_bytes(m);
     return b + 256;
 }
 
-int gsc_conv_plan(const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n_out, int32_t K,
-                  int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, int64_t cap_items, void* ws,
-                  size_t ws_bytes, void* stream) {
+int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
+                  int32_t* items, int64_t cap_items, void* ws, size_t ws_bytes, void* stream) {
     clear_error();
     if (K < 1 || K > kPlanMaxK) return fail(GSC_EINVAL, "conv_plan: K=%d outside [1,%d]", K, kPlanMaxK);
     if (n_out < 0 || n_out > INT32_MAX) return fail(GSC_EINVAL, "conv_plan: n_out=%lld invalid", (long long)n_out);
     if (!ibase || !ws) return fail(GSC_EINVAL, "conv_plan: null ibase/ws");
-    // in_idx / out_idx are read only where gidx lists pairs (NULL for a map without any)
-    if (n_out > 0 && (!gidx || !perm || !bmask || !items))
-        return fail(GSC_EINVAL, "conv_plan: null gidx/perm/bmask/items");
+    if (n_out > 0 && (!nbr || !perm || !bmask || !items))
+        return fail(GSC_EINVAL, "conv_plan: null nbr/perm/bmask/items");
     const int64_t need_items = (int64_t)K * gsc_plan_blocks(n_out);
     if (cap_items < need_items)
         return fail(GSC_ESHORT, "conv_plan: cap_items=%lld, need K*ceil(n_out/16) = %lld", (long long)cap_items,
                     (long long)need_items);
     const size_t need = gsc_conv_plan_ws_bytes(n_out, K);
     if (ws_bytes < need) return fail(GSC_ESHORT, "conv_plan: ws needs %zu bytes, got %zu", need, ws_bytes);
-    return plan_enqueue(in_idx, out_idx, gidx, n_out, K, perm, bmask, ibase, items, ws,
-                        reinterpret_cast<hipStream_t>(stream));
+    return plan_enqueue(nbr, n_out, K, perm, bmask, ibase, items, ws, reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -50,10 +50,10 @@ _SIGS = {
     "gsc_kmap_groups": (_i64, [_i64]),
     "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
     "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
-                                      _c_i64p, _vp, _sz, _vp]),
+                                      _vp, _c_i64p, _vp, _sz, _vp]),
     "gsc_plan_blocks": (_i64, [_i64]),
     "gsc_conv_plan_ws_bytes": (_sz, [_i64, _i32]),
-    "gsc_conv_plan": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "gsc_conv_plan": (ctypes.c_int, [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "gsc_conv_block_engine": (_i32, [_i32, _i32, _i32, _i32]),
     "gsc_conv_fwd_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64,
@@ -183,6 +183,7 @@ class KernelMap:
     n_out: int
     offsets: np.ndarray        # K x D
     n_bound: int = 0           # n_pairs, or an upper bound of it
+    nbr: Optional[torch.Tensor] = None    # dense form [K, n_out]: input row or -1 (if requested)
     plan: Optional["BlockPlan"] = None    # block plan of the map (gsc_conv_plan), if built
 
     @property
@@ -201,9 +202,11 @@ def gsc_kmap_groups(n_out: int) -> int:
 class MapBuffers:
     """Caller-owned buffers of one kernel map (reusable across calls)."""
 
-    def __init__(self, n_out: int, K: int, D: int, device, cap_pairs: Optional[int] = None):
+    def __init__(self, n_out: int, K: int, D: int, device, cap_pairs: Optional[int] = None, dense: bool = False):
         G = gsc_kmap_groups(n_out)
         self.cap = K * n_out if cap_pairs is None else int(cap_pairs)
+        # flat: a map over fewer rows than the buffers were sized for keeps row stride n_out
+        self.nbr = torch.empty(max(K * n_out, 1), dtype=torch.int32, device=device) if dense else None
         self.in_idx = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
         self.out_idx = torch.empty(max(self.cap, 1), dtype=torch.int32, device=device)
         self.seg = torch.empty(K + 1, dtype=torch.int64, device=device)
@@ -213,11 +216,13 @@ class MapBuffers:
 
 def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, tensor_stride=None,
                    cap_pairs: Optional[int] = None, stream=None, sync: bool = True,
-                   bufs: Optional[MapBuffers] = None, host_offsets=None, host_ts=None) -> KernelMap:
+                   bufs: Optional[MapBuffers] = None, host_offsets=None, host_ts=None,
+                   dense: bool = False) -> KernelMap:
     """Kernel map of ``offsets`` from the table ``in_table`` to ``out_coords``.
     ``sync=False`` builds it without a host round trip (n_pairs stays on the
-    device).  ``bufs``/``host_offsets``/``host_ts`` let a caller reuse buffers
-    and converted host arrays across calls."""
+    device).  ``dense`` also keeps the map's dense form (the input of
+    gsc_conv_plan).  ``bufs``/``host_offsets``/``host_ts`` let a caller reuse
+    buffers and converted host arrays across calls."""
     _need(in_table, torch.uint8, "in_table", 1)
     _need(out_coords, torch.int32, "out_coords", 2)
     offs = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
@@ -226,7 +231,10 @@ def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, te
     if out_coords.shape[1] != D + 1:
         raise ValueError("offsets must be K x D with D = out_coords columns - 1")
     if bufs is None:
-        bufs = MapBuffers(n_out, K, D, out_coords.device, cap_pairs)
+        bufs = MapBuffers(n_out, K, D, out_coords.device, cap_pairs, dense)
+    if dense and bufs.nbr is None:
+        raise ValueError("dense=True needs MapBuffers(..., dense=True)")
+    nbr = bufs.nbr if dense else None
     if host_offsets is None:
         host_offsets = _host_i32(offs)
     if host_ts is None and tensor_stride is not None:
@@ -234,20 +242,22 @@ def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, te
     n_pairs = ctypes.c_int64(0)
     rc = lib().gsc_kernel_map(_ptr(in_table), _ptr(out_coords), n_out, D, host_offsets, K, host_ts,
                               _ptr(bufs.in_idx), _ptr(bufs.out_idx), bufs.cap, _ptr(bufs.seg), _ptr(bufs.gidx),
-                              ctypes.byref(n_pairs) if sync else None, _ptr(bufs.ws), bufs.ws.numel(),
+                              _ptr(nbr), ctypes.byref(n_pairs) if sync else None, _ptr(bufs.ws), bufs.ws.numel(),
                               _stream(stream))
     _check(rc)
+    nbr = None if nbr is None else nbr[: K * n_out].view(K, n_out)
     if sync:
         m = n_pairs.value
-        return KernelMap(bufs.in_idx[:m], bufs.out_idx[:m], bufs.seg, bufs.gidx, m, n_out, offs, m)
-    return KernelMap(bufs.in_idx, bufs.out_idx, bufs.seg, bufs.gidx, None, n_out, offs, bufs.cap)
+        return KernelMap(bufs.in_idx[:m], bufs.out_idx[:m], bufs.seg, bufs.gidx, m, n_out, offs, m, nbr)
+    return KernelMap(bufs.in_idx, bufs.out_idx, bufs.seg, bufs.gidx, None, n_out, offs, bufs.cap, nbr)
 
 
 def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offsets, tensor_stride=None,
-                          stream=None, sync: bool = True, bufs: Optional[MapBuffers] = None) -> KernelMap:
+                          stream=None, sync: bool = True, bufs: Optional[MapBuffers] = None,
+                          dense: bool = False) -> KernelMap:
     """The role-reversed map (Sec. 4.2): same pairs, listed by original input row."""
     return gsc_kernel_map(out_table, in_coords, -np.asarray(offsets, dtype=np.int32), tensor_stride, stream=stream,
-                          sync=sync, bufs=bufs)
+                          sync=sync, bufs=bufs, dense=dense)
 
 
 @dataclasses.dataclass
@@ -287,11 +297,12 @@ def gsc_conv_plan(kmap: KernelMap, bufs: Optional[PlanBuffers] = None, stream=No
     """The map with its block plan attached (rows ordered by neighbour mask,
     16-row blocks, per-block items of 16 input rows)."""
     n_out, K = kmap.n_out, kmap.K
+    if kmap.nbr is None:
+        raise ValueError("gsc_conv_plan needs the map's dense form: build it with dense=True")
     if bufs is None:
         bufs = PlanBuffers(n_out, K, kmap.seg.device)
-    _check(lib().gsc_conv_plan(_ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.gidx), n_out, K, _ptr(bufs.perm),
-                               _ptr(bufs.bmask), _ptr(bufs.ibase), _ptr(bufs.items), bufs.cap_items,
-                               _ptr(bufs.ws), bufs.ws.numel(), _stream(stream)))
+    _check(lib().gsc_conv_plan(_ptr(kmap.nbr), n_out, K, _ptr(bufs.perm), _ptr(bufs.bmask), _ptr(bufs.ibase),
+                               _ptr(bufs.items), bufs.cap_items, _ptr(bufs.ws), bufs.ws.numel(), _stream(stream)))
     plan = BlockPlan(bufs.perm[:n_out], bufs.bmask, bufs.ibase, bufs.items)
     return dataclasses.replace(kmap, plan=plan)
 

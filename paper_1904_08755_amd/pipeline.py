@@ -89,19 +89,19 @@ class StepPlan:
             L = wl.layers[0]
             offs = dw.offsets[0]
             K = len(offs)
-            self.mb = gsc.MapBuffers(n, K, D, dev)
+            dt = gsc._dt(dw.X)
+            self.plan_maps = use_plan and (gsc.gsc_conv_block_engine(dt, L.c_in, L.c_out, K)
+                                           or gsc.gsc_conv_block_engine(dt, L.c_out, L.c_in, K))
+            self.mb = gsc.MapBuffers(n, K, D, dev, dense=self.plan_maps)
             self.host_offs = gsc._host_i32(offs)
             self.symmetric = regions.is_symmetric(offs)
             if self.symmetric:
                 wsel = gsc.negation_permutation(offs)
             else:
-                self.tb = gsc.MapBuffers(n, K, D, dev)
+                self.tb = gsc.MapBuffers(n, K, D, dev, dense=self.plan_maps)
                 self.host_offs_neg = gsc._host_i32(-offs)
                 wsel = np.arange(K, dtype=np.int32)
             self.host_wsel = gsc._host_i32(wsel)
-            dt = gsc._dt(dw.X)
-            self.plan_maps = use_plan and (gsc.gsc_conv_block_engine(dt, L.c_in, L.c_out, K)
-                                           or gsc.gsc_conv_block_engine(dt, L.c_out, L.c_in, K))
             if self.plan_maps:
                 self.pb = gsc.PlanBuffers(n, K, dev)
                 if not self.symmetric:
@@ -116,17 +116,17 @@ class StepPlan:
             offs = dw.offsets[0]
             K = len(offs)
             self.out_table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device=dev)
-            # n_out <= n: size every coarse-side buffer for n rows
-            self.kd = gsc.MapBuffers(n, K, D, dev)
-            self.td = gsc.MapBuffers(n, K, D, dev)
-            self.host_offs = gsc._host_i32(offs)
-            self.host_offs_neg = gsc._host_i32(-offs)
-            self.host_ident = gsc._host_i32(np.arange(K, dtype=np.int32))
             dt = gsc._dt(dw.X)
             eng = lambda a, b: gsc.gsc_conv_block_engine(dt, a, b, K)
             # kd feeds layer 0's forward and layer 1's dX; td layer 1's forward and layer 0's dX
             self.plan_kd = use_plan and (eng(L0.c_in, L0.c_out) or eng(L1.c_out, L1.c_in))
             self.plan_td = use_plan and (eng(L1.c_in, L1.c_out) or eng(L0.c_out, L0.c_in))
+            # n_out <= n: size every coarse-side buffer for n rows
+            self.kd = gsc.MapBuffers(n, K, D, dev, dense=self.plan_kd)
+            self.td = gsc.MapBuffers(n, K, D, dev, dense=self.plan_td)
+            self.host_offs = gsc._host_i32(offs)
+            self.host_offs_neg = gsc._host_i32(-offs)
+            self.host_ident = gsc._host_i32(np.arange(K, dtype=np.int32))
             if self.plan_kd:
                 self.pkd = gsc.PlanBuffers(n, K, dev)
             if self.plan_td:
@@ -154,12 +154,12 @@ class StepPlan:
             offs = dw.offsets[0]
             gsc.gsc_coords_build(dw.coords, self.table, stream=stream, sync=False)
             kmap = gsc.gsc_kernel_map(self.table, dw.coords, offs, stream=stream, sync=False, bufs=self.mb,
-                                      host_offsets=self.host_offs)
+                                      host_offsets=self.host_offs, dense=self.plan_maps)
             if self.symmetric:
                 tmap = kmap
             else:
                 tmap = gsc.gsc_kernel_map(self.table, dw.coords, -offs, stream=stream, sync=False, bufs=self.tb,
-                                          host_offsets=self.host_offs_neg)
+                                          host_offsets=self.host_offs_neg, dense=self.plan_maps)
             mark("map")
             fmap, dxmap = kmap, tmap
             if self.plan_maps:
@@ -179,9 +179,9 @@ class StepPlan:
         out_coords, _ = gsc.gsc_coords_stride(dw.coords, L0.stride, out_table=self.out_table, stream=stream)
         n_out = out_coords.shape[0]
         kd = gsc.gsc_kernel_map(self.table, out_coords, offs, stream=stream, sync=False, bufs=self.kd,
-                                host_offsets=self.host_offs)
+                                host_offsets=self.host_offs, dense=self.plan_kd)
         td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
-                                host_offsets=self.host_offs_neg)
+                                host_offsets=self.host_offs_neg, dense=self.plan_td)
         mark("map")
         pkd = gsc.gsc_conv_plan(kd, self.pkd, stream=stream) if self.plan_kd else kd
         ptd = gsc.gsc_conv_plan(td, self.ptd, stream=stream) if self.plan_td else td

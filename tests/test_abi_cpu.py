@@ -96,7 +96,7 @@ def test_kernel_map_validation(L):
     offs = (ctypes.c_int32 * 3)(0, 0, 0)
     ts_bad = (ctypes.c_int32 * 3)(1, 0, 1)
     ws = L.gsc_kmap_ws_bytes(100, 1, 3)
-    args = lambda K, ts, wsb, cap=10: (fake, fake, 100, 3, offs, K, ts, fake, fake, cap, fake, fake,
+    args = lambda K, ts, wsb, cap=10: (fake, fake, 100, 3, offs, K, ts, fake, fake, cap, fake, fake, None,
                                        ctypes.byref(n), fake, wsb, None)
     assert L.gsc_kernel_map(*args(0, None, ws)) == gsc.GSC_EINVAL
     assert L.gsc_kernel_map(*args(1, ts_bad, ws)) == gsc.GSC_EINVAL
@@ -104,12 +104,12 @@ def test_kernel_map_validation(L):
     assert L.gsc_kernel_map(*args(1, None, ws, cap=-1)) == gsc.GSC_EINVAL
     # asynchronous mode (n_pairs NULL) needs cap_pairs >= K * n_out and K * D <= 768
     a = list(args(1, None, ws, cap=99))
-    a[12] = None
+    a[13] = None
     assert L.gsc_kernel_map(*a) == gsc.GSC_ESHORT and "asynchronous" in _err(L)
     K = 300
     offs300 = (ctypes.c_int32 * (3 * K))()
     ws300 = L.gsc_kmap_ws_bytes(100, K, 3)
-    a = [fake, fake, 100, 3, offs300, K, None, fake, fake, K * 100, fake, fake, None, fake, ws300, None]
+    a = [fake, fake, 100, 3, offs300, K, None, fake, fake, K * 100, fake, fake, None, None, fake, ws300, None]
     assert L.gsc_kernel_map(*a) == gsc.GSC_EINVAL and "768" in _err(L)
     assert L.gsc_table_status(None, None) == gsc.GSC_EINVAL
     assert L.gsc_coords_build_async(fake, 10, 0, fake, 1 << 20, None) == gsc.GSC_EINVAL
@@ -153,8 +153,8 @@ def test_plan_validation(L):
     assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 33) == 0
     assert L.gsc_plan_blocks(0) == 0 and L.gsc_plan_blocks(16) == 1 and L.gsc_plan_blocks(17) == 2
     cap = 27 * 7
-    plan = lambda K, wsb=ws, cap=cap, ib=fake: L.gsc_conv_plan(fake, fake, fake, 100, K, fake, fake, ib, fake, cap,
-                                                               fake, wsb, None)
+    plan = lambda K, wsb=ws, cap=cap, ib=fake: L.gsc_conv_plan(fake, 100, K, fake, fake, ib, fake, cap, fake, wsb,
+                                                               None)
     assert plan(33) == gsc.GSC_EINVAL and "K=33" in _err(L)
     assert plan(0) == gsc.GSC_EINVAL
     assert plan(27, wsb=ws - 1) == gsc.GSC_ESHORT

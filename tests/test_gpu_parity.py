@@ -238,6 +238,7 @@ def _check_plan(km):
     for k, (i, o) in enumerate(pairs):
         mask[o] |= np.int64(1) << np.int64(k)
         nbr[o, k] = i
+    assert np.array_equal(km.nbr.cpu().numpy().T.astype(np.int64), nbr[:n])   # the dense form lists the same pairs
     ms = mask[perm]
     assert np.all(ms[1:] >= ms[:-1])                                   # sorted by mask
     same = ms[1:] == ms[:-1]
@@ -291,7 +292,7 @@ def test_conv_plan_structure_bf16_wide():
     wl = WL.make_workload(4, scale=0.3)
     dw = pipeline.to_device(wl, DEV)
     table = gsc.gsc_coords_build(dw.coords)
-    km = gsc.gsc_kernel_map(table, dw.coords, dw.offsets[0])
+    km = gsc.gsc_kernel_map(table, dw.coords, dw.offsets[0], dense=True)
     _check_plan(gsc.gsc_conv_plan(km))
 
 
@@ -304,8 +305,8 @@ def _plan_case(coords, ci, co, offs, seed, ts=1):
     G, _ = WL.random_features(seed + 1, len(coords), co)
     tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
     table = gsc.gsc_coords_build(c)
-    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(table, c, offs, tensor_stride=ts))
-    tm = gsc.gsc_conv_plan(gsc.transposed_kernel_map(table, c, offs, tensor_stride=ts))
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(table, c, offs, tensor_stride=ts, dense=True))
+    tm = gsc.gsc_conv_plan(gsc.transposed_kernel_map(table, c, offs, tensor_stride=ts, dense=True))
     Y = gsc.gsc_sparse_conv_fwd(tX, tW, km)
     dX, _ = gsc.gsc_sparse_conv_bwd(tX, tW, tG, km, tm, np.arange(len(offs)), need_dw=False)
     torch.cuda.synchronize()
@@ -331,14 +332,15 @@ def test_block_engine_edges():
     _plan_case(WL.random_coords(132, 37, 3, -3, 3, batch=2), 32, 32, regions.hypercube(3, 3), 132)
     _plan_case(WL.random_coords(133, 2000, 4, -5, 5, batch=1), 32, 32, regions.hybrid(3, 4), 133)
     c = torch.empty((0, 4), dtype=torch.int32, device=DEV)
-    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, regions.hypercube(3, 3)))
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, regions.hypercube(3, 3), dense=True))
     Y = gsc.gsc_sparse_conv_fwd(torch.empty((0, 16), device=DEV), torch.randn((27, 16, 16), device=DEV), km)
     assert Y.shape == (0, 16)
     # outputs no input reaches (a plan with empty blocks) and an input with no rows
     cin = np.array([[0, 100, 100, 100], [0, 101, 100, 100]], np.int32)
     cout = WL.random_coords(134, 40, 3, -3, 3, batch=1)
     cout = np.concatenate([cout, np.array([[0, 100, 100, 99]], np.int32)])
-    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(cin)), _t(cout), regions.hypercube(3, 3)))
+    km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(cin)), _t(cout), regions.hypercube(3, 3),
+                                              dense=True))
     X = torch.randn((2, 16), device=DEV)
     W = torch.randn((27, 16, 32), device=DEV)
     Y = gsc.gsc_sparse_conv_fwd(X, W, km)
@@ -349,7 +351,7 @@ def test_block_engine_edges():
     empty_in = torch.empty((0, 16), device=DEV)
     km0 = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(torch.empty((0, 4), dtype=torch.int32,
                                                                                 device=DEV)),
-                                               _t(cout), regions.hypercube(3, 3)))
+                                               _t(cout), regions.hypercube(3, 3), dense=True))
     Y0 = gsc.gsc_sparse_conv_fwd(empty_in, W, km0)
     torch.cuda.synchronize()
     assert torch.count_nonzero(Y0).item() == 0 and Y0.shape == (len(cout), 32)
@@ -416,11 +418,16 @@ def test_async_map_matches_sync():
     gsc.gsc_table_status(table)
     offs = regions.hypercube(3, 3)
     ks = gsc.gsc_kernel_map(table, c, offs)
-    ka = gsc.gsc_kernel_map(table, c, offs, sync=False)
+    ka = gsc.gsc_kernel_map(table, c, offs, sync=False, dense=True)
     assert ka.n_pairs is None and ka.count() == ks.n_pairs
     for (a, b), (x, y) in zip(gpu_pairs(ka), gpu_pairs(ks)):
         assert np.array_equal(a, x) and np.array_equal(b, y)
     check_gidx(ka)
+    dense = ka.nbr.cpu().numpy()
+    for k, (i, o) in enumerate(gpu_pairs(ks)):
+        col = np.full(len(coords), -1, np.int64)
+        col[o] = i
+        assert np.array_equal(dense[k], col)
 
 
 def test_async_build_reports_duplicate_later():
