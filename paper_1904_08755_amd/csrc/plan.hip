@@ -22,7 +22,8 @@
 // Input: the map's dense form nbr[k][j] (input row or -1), which the kernel
 // map writes as it probes.  Steps:
 //   masks:  every row's mask from its column of nbr;
-//   sort:   stable LSD radix sort of (mask, row) by mask, 10-bit digits;
+//   sort:   stable LSD radix sort of (mask, row) by mask, 10-bit digits, one
+//           kernel per digit;
 //   count:  block unions and item counts; a scan gives ibase;
 //   fill:   one lane per position writes its entry of each of its block's
 //           items.
@@ -62,55 +63,143 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __re
 }
 
 // ---------------------------------------------------------------------------
-// stable LSD radix sort of (key, value) by key
+// stable LSD radix sort of (key, value) by key, one kernel per pass
 // ---------------------------------------------------------------------------
-template <typename KeyT>
-__global__ void __launch_bounds__(kRsThreads) k_rs_hist(const KeyT* __restrict__ keys, int64_t n, int shift,
-                                                        int32_t* __restrict__ hist, int64_t nb) {
-    __shared__ int32_t h[kRsBins];
-    for (int i = threadIdx.x; i < kRsBins; i += kRsThreads) h[i] = 0;
+// The digit counts of every pass over all keys come first (one histogram
+// kernel), so a pass knows where each digit's range starts.  A pass kernel
+// takes tiles of kRsTile keys in ticket order (an atomic counter, so every
+// tile a block waits for is already running), publishes its tile's count of
+// each digit and looks back over the earlier tiles' published counts to find
+// how many keys with that digit precede the tile (decoupled look-back: a
+// tile's entry holds either its own count or, once known, its inclusive
+// prefix).  The keys are then placed stably: in rounds of kRsThreads keys in
+// index order, lanes with equal digits found with kRsBits ballots.
+constexpr int kRsMaxPasses = 4;                   // keys of up to 40 bits
+constexpr uint32_t kStAgg = 1u << 30;             // entry holds the tile's own count
+constexpr uint32_t kStIncl = 1u << 31;            // entry holds the inclusive prefix
+constexpr uint32_t kStCount = kStAgg - 1;
+constexpr int64_t kRsMaxKeys = kStCount;          // counts must fit below the flag bits
+constexpr int kSpinMax = 1 << 22;                 // bound on polls of one entry (never reached)
+
+__global__ void k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+__global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restrict__ keys, int64_t n, int passes,
+                                                         uint32_t* __restrict__ ghist) {
+    __shared__ int32_t h[kRsMaxPasses][kRsBins];
+    for (int i = threadIdx.x; i < kRsMaxPasses * kRsBins; i += kRsThreads) (&h[0][0])[i] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kRsTile;
-    KeyT key[kRsPer];
+    uint32_t key[kRsPer];
 #pragma unroll
     for (int i = 0; i < kRsPer; ++i) {
         const int64_t idx = base + (int64_t)i * kRsThreads + threadIdx.x;
-        key[i] = idx < n ? keys[idx] : (KeyT)0;
+        key[i] = idx < n ? keys[idx] : 0u;
     }
 #pragma unroll
-    for (int i = 0; i < kRsPer; ++i)
-        if (base + (int64_t)i * kRsThreads + threadIdx.x < n) atomicAdd(&h[(int)((key[i] >> shift) & (kRsBins - 1))], 1);
+    for (int i = 0; i < kRsPer; ++i) {
+        if (base + (int64_t)i * kRsThreads + threadIdx.x < n)
+            for (int p = 0; p < passes; ++p) atomicAdd(&h[p][(key[i] >> (p * kRsBits)) & (kRsBins - 1)], 1);
+    }
     __syncthreads();
-    for (int i = threadIdx.x; i < kRsBins; i += kRsThreads) hist[(int64_t)i * nb + blockIdx.x] = h[i];
+    for (int i = threadIdx.x; i < passes * kRsBins; i += kRsThreads) {
+        const int32_t c = (&h[0][0])[i];
+        if (c) atomicAdd(&ghist[i], (uint32_t)c);
+    }
 }
 
-// Block b places its keys in rounds of kRsThreads (in index order: stable).
-// All of the block's keys are loaded first (kRsPer per thread, in flight
-// together).  Within a wave, lanes with equal digits are found with kRsBits
-// ballots; the wave's count of each digit goes to LDS, and a key's position
-// is the block's running start of its digit + the counts of lower waves in
-// this round + its rank in its wave.  vals_in == NULL means value = index.
-template <typename KeyT>
-__global__ void __launch_bounds__(kRsThreads) k_rs_scatter(const KeyT* __restrict__ kin,
-                                                           const int32_t* __restrict__ vin, int64_t n, int shift,
-                                                           const int64_t* __restrict__ hoff, int64_t nb,
-                                                           KeyT* __restrict__ kout, int32_t* __restrict__ vout) {
+// gbase[p][d] = number of keys whose pass-p digit is below d.
+__global__ void __launch_bounds__(kRsThreads) k_rs_gscan(const uint32_t* __restrict__ ghist, int passes,
+                                                         int64_t* __restrict__ gbase) {
+    __shared__ int64_t wsum[kRsThreads / 64];
+    const int d = threadIdx.x, w = d >> 6, l = d & 63;
+    for (int p = 0; p < passes; ++p) {
+        const int64_t v = ghist[p * kRsBins + d];
+        int64_t inc = v;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t u = __shfl_up(inc, o, 64);
+            if (l >= o) inc += u;
+        }
+        if (l == 63) wsum[w] = inc;
+        __syncthreads();
+        int64_t before = 0;
+        for (int i = 0; i < w; ++i) before += wsum[i];
+        gbase[p * kRsBins + d] = before + inc - v;
+        __syncthreads();
+    }
+}
+
+__global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restrict__ kin,
+                                                        const int32_t* __restrict__ vin, int64_t n, int shift,
+                                                        const int64_t* __restrict__ gbase,
+                                                        uint32_t* __restrict__ status,
+                                                        uint32_t* __restrict__ status_next,
+                                                        uint32_t* __restrict__ ticket, uint32_t* __restrict__ kout,
+                                                        int32_t* __restrict__ vout) {
     constexpr int W = kRsThreads / 64;
+    static_assert(kRsThreads == kRsBins, "one thread per digit in the look-back");
     __shared__ int64_t start[kRsBins];
+    __shared__ int32_t hist[kRsBins];
     __shared__ int32_t wcnt[W][kRsBins];
+    __shared__ int64_t tile_sh;
     const int tid = threadIdx.x, wave = tid >> 6;
-    const int64_t base = (int64_t)blockIdx.x * kRsTile;
-    KeyT key[kRsPer];
+    if (tid == 0) tile_sh = atomicAdd(ticket, 1u);
+    hist[tid] = 0;
+    for (int i = tid; i < W * kRsBins; i += kRsThreads) (&wcnt[0][0])[i] = 0;
+    __syncthreads();
+    const int64_t t = tile_sh;
+    const int64_t base = t * kRsTile;
+    status_next[t * kRsBins + tid] = 0;   // the next pass's entry of this tile (that array is idle now)
+    uint32_t key[kRsPer];
     int32_t val[kRsPer];
 #pragma unroll
     for (int r = 0; r < kRsPer; ++r) {
         const int64_t idx = base + (int64_t)r * kRsThreads + tid;
         const bool valid = idx < n;
-        key[r] = valid ? kin[idx] : (KeyT)0;
+        key[r] = valid ? kin[idx] : 0u;
         val[r] = valid ? (vin ? vin[idx] : (int32_t)idx) : 0;
     }
-    for (int i = tid; i < kRsBins; i += kRsThreads) start[i] = hoff[(int64_t)i * nb + blockIdx.x];
-    for (int i = tid; i < W * kRsBins; i += kRsThreads) (&wcnt[0][0])[i] = 0;
+#pragma unroll
+    for (int r = 0; r < kRsPer; ++r)
+        if (base + (int64_t)r * kRsThreads + tid < n) atomicAdd(&hist[(key[r] >> shift) & (kRsBins - 1)], 1);
+    __syncthreads();
+    {   // publish this tile's count of digit tid, then look back for the keys before the tile
+        // (the entries are the only data exchanged, so relaxed atomics at
+        // agent scope suffice: they go to L2 and every poll sees the latest)
+        const uint32_t c = (uint32_t)hist[tid];
+        uint32_t* mine = status + t * kRsBins + tid;
+        uint32_t before = 0;
+        __hip_atomic_store(mine, (t == 0 ? kStIncl : kStAgg) | c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (t > 0) {
+            constexpr int LW = 16;   // predecessors' entries loaded together
+            bool done = false;
+            for (int64_t j0 = t - 1; !done && j0 >= 0; j0 -= LW) {
+                uint32_t v[LW];
+#pragma unroll
+                for (int i = 0; i < LW; ++i)
+                    v[i] = j0 - i >= 0 ? __hip_atomic_load(status + (j0 - i) * kRsBins + tid, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                       : kStIncl;
+#pragma unroll
+                for (int i = 0; i < LW; ++i) {
+                    if (done) break;
+                    uint32_t x = v[i];
+                    for (int spin = 0; x == 0 && spin < kSpinMax; ++spin) {   // not published yet: it will be
+                        __builtin_amdgcn_s_sleep(1);
+                        x = __hip_atomic_load(status + (j0 - i) * kRsBins + tid, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    before += x & kStCount;
+                    done = (x & kStIncl) != 0;
+                }
+            }
+            __hip_atomic_store(mine, kStIncl | (before + c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        start[tid] = gbase[tid] + before;
+    }
     const unsigned long long below = lanemask_lt();
 #pragma unroll
     for (int rnd = 0; rnd < kRsPer; ++rnd) {
@@ -135,18 +224,18 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_scatter(const KeyT* __restric
         }
         __syncthreads();   // every lane has read start and wcnt
         if (valid) {
-            if (pos < n) {   // always true for consistent histograms; keeps a bad input from writing outside
+            if (pos >= 0 && pos < n) {   // always true for consistent counts; keeps a bad input from writing outside
                 kout[pos] = key[rnd];
                 vout[pos] = val[rnd];
             }
             if (rank == 0) {   // the lowest wave holding digit d advances start[d] by the round's count
-                int32_t t = 0;
+                int32_t c = 0;
                 bool first = true;
                 for (int w = 0; w < W; ++w) {
-                    t += wcnt[w][d];
+                    c += wcnt[w][d];
                     if (w < wave) first = first && wcnt[w][d] == 0;
                 }
-                if (first) start[d] += t;
+                if (first) start[d] += c;
             }
         }
         __syncthreads();   // start updated by the first holders of each digit
@@ -201,6 +290,7 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
                         int32_t* items, void* ws, hipStream_t s) {
     const int64_t nb = (n + 15) / 16;
     const int64_t nrs = (n + kRsTile - 1) / kRsTile;
+    const int passes = (K + kRsBits - 1) / kRsBits;
     char* w = reinterpret_cast<char*>(ws);
     uint32_t* ka = reinterpret_cast<uint32_t*>(w);
     w += al256((size_t)n * sizeof(uint32_t));
@@ -210,10 +300,16 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
     w += al256((size_t)n * sizeof(int32_t));
     int32_t* vb = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)n * sizeof(int32_t));
-    int32_t* hist = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)kRsBins * nrs * sizeof(int32_t));
-    int64_t* hoff = reinterpret_cast<int64_t*>(w);
-    w += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
+    // zeroed together: digit counts, tickets, the first pass's look-back entries
+    uint32_t* ghist = reinterpret_cast<uint32_t*>(w);
+    uint32_t* ticket = ghist + kRsMaxPasses * kRsBins;
+    uint32_t* st0 = ticket + kRsMaxPasses;
+    const int64_t nzero = kRsMaxPasses * kRsBins + kRsMaxPasses + nrs * kRsBins;
+    w += al256((size_t)nzero * sizeof(uint32_t));
+    uint32_t* st1 = reinterpret_cast<uint32_t*>(w);
+    w += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
+    int64_t* gbase = reinterpret_cast<int64_t*>(w);
+    w += al256((size_t)kRsMaxPasses * kRsBins * sizeof(int64_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)nb * sizeof(int32_t));
     void* scan_ws = w;
@@ -224,21 +320,24 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
         return GSC_OK;
     }
     const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
+    const unsigned zblocks = (unsigned)((nzero + 255) / 256 < 1024 ? (nzero + 255) / 256 : 1024);
+    hipLaunchKernelGGL(k_zero_u32, dim3(zblocks), dim3(256), 0, s, ghist, nzero);
+    GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka);
     GSC_LAUNCH_CHECK();
-    const int passes = (K + kRsBits - 1) / kRsBits;
+    hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_rs_gscan, dim3(1), dim3(kRsThreads), 0, s, ghist, passes, gbase);
+    GSC_LAUNCH_CHECK();
     const uint32_t* kin = ka;
     const int32_t* vin = nullptr;
     for (int p = 0; p < passes; ++p) {
         uint32_t* kout = (p & 1) ? ka : kb;
         int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? va : vb);
-        hipLaunchKernelGGL((k_rs_hist<uint32_t>), dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, n,
-                           p * kRsBits, hist, nrs);
-        GSC_LAUNCH_CHECK();
-        int rc = scan_counts(hist, kRsBins * nrs, hoff, nullptr, scan_ws, s);
-        if (rc) return rc;
-        hipLaunchKernelGGL((k_rs_scatter<uint32_t>), dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n,
-                           p * kRsBits, hoff, nrs, kout, vout);
+        uint32_t* st = (p & 1) ? st1 : st0;
+        uint32_t* st_next = (p & 1) ? st0 : st1;
+        hipLaunchKernelGGL(k_rs_pass, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n, p * kRsBits,
+                           gbase + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout);
         GSC_LAUNCH_CHECK();
         kin = kout;
         vin = vout;
@@ -261,15 +360,15 @@ extern "C" {
 int64_t gsc_plan_blocks(int64_t n_out) { return n_out <= 0 ? 0 : (n_out + 15) / 16; }
 
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
-    if (n_out < 0 || K < 1 || K > kPlanMaxK) return 0;
+    if (n_out < 0 || n_out > kRsMaxKeys || K < 1 || K > kPlanMaxK) return 0;
     const int64_t nb = (n_out + 15) / 16;
     const int64_t nrs = (n_out + kRsTile - 1) / kRsTile;
     size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
-    b += al256((size_t)kRsBins * nrs * sizeof(int32_t));
-    b += al256((size_t)(kRsBins * nrs + 1) * sizeof(int64_t));
+    b += al256((size_t)(kRsMaxPasses * kRsBins + kRsMaxPasses + nrs * kRsBins) * sizeof(uint32_t));
+    b += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
+    b += al256((size_t)kRsMaxPasses * kRsBins * sizeof(int64_t));
     b += al256((size_t)nb * sizeof(int32_t));
-    const int64_t m = kRsBins * nrs > nb ? kRsBins * nrs : nb;
-    b += scan_ws_bytes(m);
+    b += scan_ws_bytes(nb);
     return b + 256;
 }
 
@@ -277,7 +376,8 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, u
                   int32_t* items, int64_t cap_items, void* ws, size_t ws_bytes, void* stream) {
     clear_error();
     if (K < 1 || K > kPlanMaxK) return fail(GSC_EINVAL, "conv_plan: K=%d outside [1,%d]", K, kPlanMaxK);
-    if (n_out < 0 || n_out > INT32_MAX) return fail(GSC_EINVAL, "conv_plan: n_out=%lld invalid", (long long)n_out);
+    if (n_out < 0 || n_out > kRsMaxKeys)
+        return fail(GSC_EINVAL, "conv_plan: n_out=%lld outside [0, %lld]", (long long)n_out, (long long)kRsMaxKeys);
     if (!ibase || !ws) return fail(GSC_EINVAL, "conv_plan: null ibase/ws");
     if (n_out > 0 && (!nbr || !perm || !bmask || !items))
         return fail(GSC_EINVAL, "conv_plan: null nbr/perm/bmask/items");
