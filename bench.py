@@ -19,6 +19,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -40,6 +41,37 @@ def fwd_bytes(n_pairs, n_out, ci, co, K, s):
     """Gather model: one input row and one index pair per kernel-map pair,
     every output row written once, the weights read once."""
     return n_pairs * (s * ci + 8) + n_out * s * co + K * ci * co * s
+
+
+def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool) -> str:
+    """Name of the kernel gsc_sparse_conv_fwd launches for this layer (the
+    library's dispatch: block engine on a plan, else the map's row form)."""
+    dt = gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32
+    if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
+        return f"k_conv_blk_{'bf16' if dtype == 'bf16' else 'f32'}<{ci}, {co}, false>"
+    if dtype == "bf16":
+        if ci in (128, 256) and co in (128, 256):
+            return f"k_conv_bf16_dma<{ci}, {co}, gsc::WIdentity>"
+        return "k_conv_bf16"
+    return f"k_conv_f32<{ci}, {co}, false, gsc::WIdentity>"
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of ``kernel`` on ``workload`` from the committed
+    counter summary (profiles/hbm_traffic_*), or None when there is none or
+    the kernel's source has changed since the counters were taken."""
+    import glob
+    import hashlib
+    for f in glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.md")):
+        text = open(f).read()
+        fields = dict(re.findall(r"^(kernel|source|source_sha256|traffic_bytes_per_launch): (.+)$", text, re.M))
+        if fields.get("kernel") != kernel or workload not in os.path.basename(f).replace("_cube3", ""):
+            continue
+        src = os.path.join(ROOT, fields["source"])
+        if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != fields["source_sha256"]:
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    return None
 
 
 def cpu_baseline(wl, budget_s: float = 30.0):
@@ -84,7 +116,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row order (no tile plan)")
+    ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB once (a copy of known size for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -153,7 +185,11 @@ def main():
     conv_s = (ms["fwd"] + ms["bwd"]) * 1e-3
     km0 = last.kmaps[0]
     n_out0 = km0.n_out
-    # dominant kernel: the forward gather -> MFMA -> LDS-accumulate of layer 0
+    # dominant kernel: the forward convolution of layer 0 (single-layer workloads, where the fwd stage is one launch)
+    planned = bool(plan.plans)
+    kernel = forward_kernel(gsc, wl.dtype, L0.c_in, L0.c_out, km0.K, planned)
+    wname = wl.name.replace("_cube3", "")
+    traffic = measured_traffic(kernel, wname)
     dom_bytes = fwd_bytes(pairs[0], n_out0, L0.c_in, L0.c_out, km0.K, s)
     dom_ms = ms["fwd"] if len(wl.layers) == 1 else None
     roof = None
@@ -162,14 +198,14 @@ def main():
         dom_flops = 2.0 * pairs[0] * L0.c_in * L0.c_out
         ach = dom_flops / (dom_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
-                "kernel": "k_conv_bf16 (forward)", "flops_per_launch": int(dom_flops),
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                "kernel": kernel, "flops_per_launch": int(dom_flops),
                 "bytes_per_launch": int(dom_bytes), "avg_launch_us": round(dom_ms * 1e3, 2)}
     elif dom_ms:
         ach = dom_bytes / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "k_conv_f32 (forward)", "bytes_per_launch": int(dom_bytes),
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": kernel, "bytes_per_launch": int(dom_bytes),
                 "avg_launch_us": round(dom_ms * 1e3, 2)}
 
     if args.copy_calibration:
@@ -201,11 +237,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "voxels": wl.n, "D": wl.D,
                    "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
-                   "kernel_map_pairs": pairs, "tile_plan": not args.no_plan, "parallelism": "single GPU"},
+                   "kernel_map_pairs": pairs, "block_plan": bool(plan.plans), "parallelism": "single GPU"},
         "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
         "effective_gflops": round(flops / conv_s / 1e9, 1),
         "kernel_map_build_ms": round(ms["map"], 4),
-        "tile_plan_ms": round(ms["plan"], 4),
+        "block_plan_ms": round(ms["plan"], 4),
         "stage_ms": {k: round(v, 4) for k, v in ms.items()},
         "roofline": roof,
         "cpu_baseline": cpu,
