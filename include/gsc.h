@@ -206,8 +206,9 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K,
  * gathered rows have c_red channels and whose output rows have c_out channels
  * (forward: c_red = c_in; input gradient: c_red = c_out of the layer and the
  * output is c_in wide), else 0; a plan passed for another shape is ignored
- * and the map's row form is used.  Present engine: float32 with c_red, c_out
- * in {16, 32, 64} and K * c_red * c_out * 4 <= 147456. */
+ * and the map's row form is used.  Present engines: float32 with c_red, c_out
+ * in {16, 32, 64} and K * c_red * c_out * 4 <= 147456; bfloat16 (fp32 sums)
+ * with c_red, c_out in {64, 128, 256}.  Both take K <= 32. */
 int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K);
 
 /* ------------------------------------------------------------------------ */

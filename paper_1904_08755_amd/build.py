@@ -31,6 +31,8 @@ COMMON_FLAGS = [
     "-Wno-unused-function",
     # never emit packed fp32 VALU ops (v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs (no AGPR copies around each MFMA)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -719,7 +719,9 @@ static int plan_args(const char* who, int64_t n, const int32_t* perm, const uint
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K) {
-    return dtype == GSC_F32 && blk_f32_supported(c_red, c_out, K) ? 1 : 0;
+    if (dtype == GSC_F32) return blk_f32_supported(c_red, c_out, K) ? 1 : 0;
+    if (dtype == GSC_BF16) return blk_bf16_supported(c_red, c_out, K) ? 1 : 0;
+    return 0;
 }
 
 int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
@@ -746,10 +748,15 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (planned && gsc_conv_block_engine(dtype, c_in, c_out, K) && aligned16(X) && aligned16(W)) {
         if (n_in > 0 && !X) return fail(GSC_EINVAL, "conv_fwd: X is null");
+        const BlockPlan plan{perm, bmask, ibase, items};
+        if (dtype == GSC_BF16) {   // B_k = W[k]: the engine reads its columns, so the transposed copy
+            rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
+            if (rc) return rc;
+            return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s);
+        }
         static const WSel kNoSel{};
         return conv_blk_f32(c_in, c_out, reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(W),
-                            false, kNoSel, K, BlockPlan{perm, bmask, ibase, items}, n_out,
-                            reinterpret_cast<float*>(Y), s);
+                            false, kNoSel, K, plan, n_out, reinterpret_cast<float*>(Y), s);
     }
     if (dtype == GSC_F32)
         return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
@@ -800,10 +807,15 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         bool planned = false;
         int rc = plan_args("conv_bwd", n_in, t_perm, t_bmask, t_ibase, t_items, &planned);
         if (rc) return rc;
-        if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W))
-            rc = conv_blk_f32(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,
-                              reinterpret_cast<const float*>(W), true, sel, K,
-                              BlockPlan{t_perm, t_bmask, t_ibase, t_items}, n_in, reinterpret_cast<float*>(dX), s);
+        if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W)) {
+            const BlockPlan plan{t_perm, t_bmask, t_ibase, t_items};
+            if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
+                rc = conv_blk_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan, n_in, dX, s);
+            else
+                rc = conv_blk_f32(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,
+                                  reinterpret_cast<const float*>(W), true, sel, K, plan, n_in,
+                                  reinterpret_cast<float*>(dX), s);
+        }
         else if (dtype == GSC_F32)
             rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, c_out, c_in,
                                                n_in, dX, sel, s);

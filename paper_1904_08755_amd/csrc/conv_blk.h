@@ -29,4 +29,14 @@ bool blk_f32_supported(int ca, int cb, int K);
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
                  const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s);
 
+// bf16 engine for wide layers: reduction width ca and output width cb in
+// {64, 128, 256}, K <= 32.  Y (n_y x cb, bf16) = sum over the plan's items
+// of X[item rows] * B_k, B_k[ch][col] = Bt[sel(k)][col][ch] (Bt: K x cb x ca
+// bf16: the transposed weights for the forward pass, W itself for the input
+// gradient).  Asynchronous.
+bool blk_bf16_supported(int ca, int cb, int K);
+template <typename Sel>
+int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
+                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s);
+
 }  // namespace gsc

@@ -32,6 +32,7 @@ constexpr int kBlkLdsBytes = 144 * 1024;   // weight storage of the fp32 engine
 // s_waitcnt operand for vmcnt(0) with expcnt and lgkmcnt left free (gfx9
 // encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
 constexpr int kWaitVm0 = (7 << 4) | (15 << 8);
+constexpr int kWaitLgkm0 = 0x3f | (7 << 4) | (3 << 14);   // lgkmcnt(0), vmcnt and expcnt left free
 
 template <int CA, int CB>
 struct BlkF32 {
@@ -268,6 +269,391 @@ __global__ void k_zero_f32(float* __restrict__ y, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         y[i] = 0.f;
 }
+
+// ---------------------------------------------------------------------------
+// bf16 engine for wide layers (reduction width CA in {64, 128, 256}, output
+// width CB in {64, 128, 256}): v_mfma_f32_16x16x32_bf16, fp32 sums, bf16
+// output (nearest even).
+//
+// A workgroup of four waves owns a tile of kBfT blocks (128 positions); wave
+// w owns output columns [w*CB/4, (w+1)*CB/4) of all of them and keeps their
+// sums in registers.  The tile is computed offset by offset over the union of
+// its blocks' masks, each offset's reduction in parts of 64 channels: a group
+// (offset, part) reads its weight fragments into registers once and applies
+// them to every block of the tile that has the offset (blocks in a static
+// loop, so the accumulators are addressed statically; the mask-sorted order
+// makes most blocks have most of the tile's offsets).
+//
+// After the tile's items and output rows are staged in LDS the waves are
+// independent: each wave gathers its items' rows into its own LDS ring with
+// LDS DMA (kBfAhead items ahead) and copies its next weight fragments into
+// the other of its two LDS buffers the same way.  Every item issues the same
+// number of copies (a group's real weight copies in its first items, copies
+// of one line into a scratch slot after that), so the waits are static
+// vector-memory counts and no register is ever loaded from global memory in
+// the loop.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+constexpr int kBfT = 8;                              // blocks per tile
+constexpr int kBfThreads = 256;
+constexpr int kBfIdxInts = kBfT * kPlanMaxK * 16;    // the tile's items, at most
+constexpr int kBfAhead = 5;                          // items whose rows are in flight
+constexpr int kBfRing = kBfAhead + 1;                // row slots per wave
+
+template <int CA, int CB>
+struct BlkBf16 {
+    static constexpr int NC = CB / 4;                // output columns per wave
+    static constexpr int NB = NC / 16;               // 16-column blocks per wave
+    static constexpr int CAH = 64;                   // channels per part
+    static constexpr int H = CA / CAH;               // parts of the reduction
+    static constexpr int KH = CAH / 32;              // MFMA steps per part
+    static constexpr int RW = KH * NB;               // 1 KiB weight regions per wave and group
+    static constexpr int WPS = RW / 4 > 0 ? RW / 4 : 1;   // weight copies per item
+    static constexpr int P = RW / WPS;               // items that carry a group's real copies
+    static constexpr int OPS = WPS + 2;              // copies per item (weights + two row halves)
+    static_assert(P * WPS == RW, "weight regions must split into parts");
+    static_assert(OPS * kBfAhead < 64, "vmcnt range");
+};
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// LDS reads as inline asm (the compiler would otherwise wait for every LDS
+// DMA copy in flight before them); after_wait() makes uses of a result
+// depend on the wait that follows the reads (volatile asm keeps its order).
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t a) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+}
+__device__ __forceinline__ int32_t lds_read_b32(uint32_t a) {
+    int32_t v;
+    asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+}
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+template <typename T>
+__device__ __forceinline__ void after_wait(T& x) {
+    asm volatile("" : "+v"(x));
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {   // at most N vector-memory operations in flight
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_vm_dyn(int n) {   // n clamped to [0, 63]
+    switch (n <= 0 ? 0 : (n >= 63 ? 63 : n)) {
+#define GSC_WVD(c) case c: wait_vm<c>(); break;
+        GSC_WVD(0) GSC_WVD(1) GSC_WVD(2) GSC_WVD(3) GSC_WVD(4) GSC_WVD(5) GSC_WVD(6) GSC_WVD(7)
+        GSC_WVD(8) GSC_WVD(9) GSC_WVD(10) GSC_WVD(11) GSC_WVD(12) GSC_WVD(13) GSC_WVD(14) GSC_WVD(15)
+        GSC_WVD(16) GSC_WVD(17) GSC_WVD(18) GSC_WVD(19) GSC_WVD(20) GSC_WVD(21) GSC_WVD(22) GSC_WVD(23)
+        GSC_WVD(24) GSC_WVD(25) GSC_WVD(26) GSC_WVD(27) GSC_WVD(28) GSC_WVD(29) GSC_WVD(30) GSC_WVD(31)
+        GSC_WVD(32) GSC_WVD(33) GSC_WVD(34) GSC_WVD(35) GSC_WVD(36) GSC_WVD(37) GSC_WVD(38) GSC_WVD(39)
+        GSC_WVD(40) GSC_WVD(41) GSC_WVD(42) GSC_WVD(43) GSC_WVD(44) GSC_WVD(45) GSC_WVD(46) GSC_WVD(47)
+        GSC_WVD(48) GSC_WVD(49) GSC_WVD(50) GSC_WVD(51) GSC_WVD(52) GSC_WVD(53) GSC_WVD(54) GSC_WVD(55)
+        GSC_WVD(56) GSC_WVD(57) GSC_WVD(58) GSC_WVD(59) GSC_WVD(60) GSC_WVD(61) GSC_WVD(62) GSC_WVD(63)
+#undef GSC_WVD
+        default: wait_vm<0>();
+    }
+}
+
+// Item walk of a tile (all wave-uniform): offsets k of the tile's union
+// ascending, parts h, blocks b having k ascending.
+struct BfIt {
+    int k, h, b;
+    uint32_t bk;   // blocks of the tile having offset k
+    bool valid;
+};
+
+template <int CA, int CB, typename Sel>
+__global__ void __launch_bounds__(kBfThreads, 1)
+k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __restrict__ Bt, int K, Sel sel,
+                const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
+                const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
+                uint16_t* __restrict__ Y) {
+    using C = BlkBf16<CA, CB>;
+    struct WaveLds {
+        uint8_t w[2][C::RW][1024];            // weight fragments of two groups
+        uint8_t scratch[C::WPS][1024];        // target of the copies that keep the count fixed
+        uint8_t rows[kBfRing][2][1024];       // 16 rows x 64 channels per item, two 8-row halves
+        uint32_t okmask[kBfRing];             // rows of each slot with an input row
+    };
+    __shared__ __attribute__((aligned(16))) WaveLds wl[4];
+    __shared__ int32_t idx_s[kBfIdxInts];
+    __shared__ int32_t perm_s[kBfT * 16];
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int r16 = lane & 15, q = lane >> 4;
+    const int64_t b0 = (int64_t)blockIdx.x * kBfT;
+    const int nbt = (int)min((int64_t)kBfT, nb - b0);
+    WaveLds& my = wl[wave];
+
+    // the tile's blocks (wave-uniform) and the offset -> weight map per lane
+    uint32_t bm[kBfT];
+    int32_t ibl[kBfT];
+    const int64_t ib0 = ibase[b0];
+    uint32_t U = 0;
+#pragma unroll
+    for (int b = 0; b < kBfT; ++b) {
+        bm[b] = b < nbt ? bmask[b0 + b] : 0u;
+        ibl[b] = b < nbt ? (int32_t)(ibase[b0 + b] - ib0) : 0;
+        U |= bm[b];
+    }
+    const int n_items = (int)(ibase[b0 + nbt] - ib0);
+    const int sel_lane = lane < K ? sel(lane) : 0;
+    for (int i = tid; i < n_items * 16; i += kBfThreads) idx_s[i] = items[ib0 * 16 + i];
+    for (int i = tid; i < kBfT * 16; i += kBfThreads) {
+        const int64_t pos = b0 * 16 + i;
+        perm_s[i] = pos < n_y ? perm[pos] : -1;
+    }
+    __syncthreads();   // items and output rows staged
+
+    auto blocks_with = [&](int k) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int b = 0; b < kBfT; ++b) m |= ((bm[b] >> k) & 1u) << b;
+        return m;
+    };
+    auto first = [&]() {
+        BfIt it{0, 0, 0, 0u, U != 0};
+        if (it.valid) {
+            it.k = __ffs(U) - 1;
+            it.bk = blocks_with(it.k);
+            it.b = __ffs(it.bk) - 1;
+        }
+        return it;
+    };
+    auto advance = [&](BfIt it) {
+        if (!it.valid) return it;
+        const uint32_t rem = it.bk & ~((2u << it.b) - 1u);
+        if (rem) {
+            it.b = __ffs(rem) - 1;
+        } else if (it.h + 1 < C::H) {
+            ++it.h;
+            it.b = __ffs(it.bk) - 1;
+        } else {
+            const uint32_t kr = it.k < 31 ? U & ~((2u << it.k) - 1u) : 0u;
+            if (kr) {
+                it.k = __ffs(kr) - 1;
+                it.h = 0;
+                it.bk = blocks_with(it.k);
+                it.b = __ffs(it.bk) - 1;
+            } else {
+                it.valid = false;
+            }
+        }
+        return it;
+    };
+
+    // copy part p (regions p*WPS ..) of this wave's weight fragments of group
+    // (k, h) into buffer buf: region (s, j) holds lane (c, q)'s 16 bytes of
+    // B_k rows 64 h + 32 s + 8 q .. +7, column w*NC + 16 j + c
+    auto copy_w = [&](int k, int h, int buf, int p) {
+        const uint16_t* src = Bt + (int64_t)readlane_i32(sel_lane, k) * CB * CA + h * C::CAH + 8 * q;
+#pragma unroll
+        for (int i = 0; i < C::WPS; ++i) {
+            const int reg = p * C::WPS + i;
+            const int st = reg / C::NB, j = reg % C::NB;
+            const uint16_t* g = src + (int64_t)(wave * C::NC + 16 * j + r16) * CA + 32 * st;
+            __builtin_amdgcn_global_load_lds((glb_void_t*)g, (lds_void_t*)&my.w[buf][reg][0], 16, 0, 0);
+        }
+    };
+    auto copy_dummy = [&]() {   // one cache line into the scratch slots
+#pragma unroll
+        for (int i = 0; i < C::WPS; ++i)
+            __builtin_amdgcn_global_load_lds((glb_void_t*)Bt, (lds_void_t*)&my.scratch[i][0], 16, 0, 0);
+    };
+    // rows of item it into ring slot: half i, lane l -> row 8 i + l / 8, its
+    // 16-byte chunk (l % 8) ^ (row % 8) (swizzled so that the fragment reads
+    // below hit distinct banks); slots of missing rows are recorded, not read
+    const uint32_t idx_base = lds_addr(idx_s);
+    auto copy_rows = [&](const BfIt& it, int slot) {
+        const int il = it.valid ? ibl[it.b] + __popc(bm[it.b] & ((1u << it.k) - 1u)) : 0;
+        const int rr0 = lane >> 3, t = lane & 7;
+        int32_t id0 = lds_read_b32(idx_base + (uint32_t)(il * 16 + rr0) * 4);
+        int32_t id1 = lds_read_b32(idx_base + (uint32_t)(il * 16 + 8 + rr0) * 4);
+        int32_t idr = lds_read_b32(idx_base + (uint32_t)(il * 16 + r16) * 4);
+        wait_lgkm0();
+        after_wait(id0);
+        after_wait(id1);
+        after_wait(idr);
+        const bool ok0 = it.valid && id0 >= 0 && id0 < n_x, ok1 = it.valid && id1 >= 0 && id1 < n_x;
+        const uint16_t* g0 = X + (int64_t)(ok0 ? id0 : 0) * CA + it.h * C::CAH + 8 * (t ^ (rr0 & 7));
+        const uint16_t* g1 = X + (int64_t)(ok1 ? id1 : 0) * CA + it.h * C::CAH + 8 * (t ^ ((8 + rr0) & 7));
+        __builtin_amdgcn_global_load_lds((glb_void_t*)g0, (lds_void_t*)&my.rows[slot][0][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((glb_void_t*)g1, (lds_void_t*)&my.rows[slot][1][0], 16, 0, 0);
+        const bool okr = it.valid && idr >= 0 && idr < n_x;
+        const uint32_t m = (uint32_t)__ballot(okr && lane < 16);
+        if (lane == 0) my.okmask[slot] = m;
+    };
+
+    floatx4 acc[kBfT][C::NB];
+#pragma unroll
+    for (int b = 0; b < kBfT; ++b)
+#pragma unroll
+        for (int j = 0; j < C::NB; ++j) acc[b][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    if (U != 0) {
+        // prologue: the first group's weights, the first kBfAhead items' rows
+        BfIt g = first();   // first item of the current group
+        BfIt ahead = g;     // next item whose rows are copied
+        for (int p = 0; p < C::P; ++p) copy_w(g.k, g.h, 0, p);
+        for (int i = 0; i < kBfAhead; ++i) {
+            copy_rows(ahead, i);
+            ahead = advance(ahead);
+        }
+        int e = 0;          // items done
+        int buf = 0;
+        for (;;) {
+            // group (g.k, g.h): its fragments, the next group's copy target
+            wait_vm<C::OPS * kBfAhead>();   // (only needed for the first group: later ones wait at their end)
+            u32x4 wf[C::KH][C::NB];
+#pragma unroll
+            for (int st = 0; st < C::KH; ++st)
+#pragma unroll
+                for (int j = 0; j < C::NB; ++j) wf[st][j] = lds_read_b128(lds_addr(&my.w[buf][st * C::NB + j][lane * 16]));
+            wait_lgkm0();
+#pragma unroll
+            for (int st = 0; st < C::KH; ++st)
+#pragma unroll
+                for (int j = 0; j < C::NB; ++j) after_wait(wf[st][j]);
+            int nk = g.k, nh = g.h + 1;   // the next group (none: copies of this one into the idle buffer)
+            if (nh == C::H) {
+                nh = 0;
+                const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
+                nk = kr ? __ffs(kr) - 1 : g.k;
+                if (!kr) nh = g.h;
+            }
+            const int n_g = __popc(g.bk);   // items of the group
+            int step = 0;                   // items of the group done
+#pragma unroll
+            for (int b = 0; b < kBfT; ++b) {
+                if ((g.bk >> b) & 1u) {
+                    if (step < C::P) copy_w(nk, nh, buf ^ 1, step);
+                    else copy_dummy();
+                    const int slot_new = (e + kBfAhead) % kBfRing;
+                    copy_rows(ahead, slot_new);
+                    ahead = advance(ahead);
+                    const int slot = e % kBfRing;
+                    wait_vm<C::OPS * kBfAhead>();   // item e's rows: the next kBfAhead items' copies may fly
+                    const uint32_t okm = (uint32_t)lds_read_b32(lds_addr(&my.okmask[slot]));
+                    u32x4 a[C::KH];
+#pragma unroll
+                    for (int st = 0; st < C::KH; ++st) {
+                        const int c = 4 * st + q;   // 16-byte chunk of row r16
+                        a[st] = lds_read_b128(lds_addr(&my.rows[slot][r16 >> 3][((r16 & 7) * 8 + (c ^ (r16 & 7))) * 16]));
+                    }
+                    wait_lgkm0();
+                    uint32_t okv = okm;
+                    after_wait(okv);
+                    const bool ok = (okv >> r16) & 1u;
+#pragma unroll
+                    for (int st = 0; st < C::KH; ++st) {
+                        after_wait(a[st]);
+                        a[st] = ok ? a[st] : u32x4{0u, 0u, 0u, 0u};
+                    }
+#pragma unroll
+                    for (int st = 0; st < C::KH; ++st)
+#pragma unroll
+                        for (int j = 0; j < C::NB; ++j)
+                            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[st]),
+                                                                                __builtin_bit_cast(bf16x8, wf[st][j]),
+                                                                                acc[b][j], 0, 0, 0);
+                    ++e;
+                    ++step;
+                }
+            }
+            // the next group's weights: issued in this group's first P items
+            // (all of them now if the group was shorter)
+            if (n_g < C::P) {
+                for (int p = n_g; p < C::P; ++p) copy_w(nk, nh, buf ^ 1, p);
+                wait_vm<0>();
+            } else {
+                wait_vm_dyn(2 + C::OPS * (n_g - C::P));   // all but what the later items issued
+            }
+            buf ^= 1;
+            // next group
+            if (g.h + 1 < C::H) {
+                ++g.h;
+            } else {
+                const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
+                if (!kr) break;
+                g.k = __ffs(kr) - 1;
+                g.h = 0;
+                g.bk = blocks_with(g.k);
+            }
+        }
+    }
+    wait_vm<0>();
+    // write the tile: lane (c, q) holds rows 4q+i, column 16 j + c of block b's wave columns
+#pragma unroll
+    for (int b = 0; b < kBfT; ++b) {
+        if (b >= nbt) break;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int32_t row = perm_s[16 * b + 4 * q + i];
+            if (row >= 0 && row < n_y) {
+#pragma unroll
+                for (int j = 0; j < C::NB; ++j)
+                    Y[(int64_t)row * CB + wave * C::NC + 16 * j + r16] = f32_to_bf16_rne(acc[b][j][i]);
+            }
+        }
+    }
+}
+
+bool blk_bf16_supported(int ca, int cb, int K) {
+    return (ca == 64 || ca == 128 || ca == 256) && (cb == 64 || cb == 128 || cb == 256) && K >= 1 && K <= kPlanMaxK;
+}
+
+template <int CA, int CB, typename Sel>
+static void launch_blk_bf16(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
+                            const BlockPlan& p, int64_t nb, int64_t n_y, uint16_t* Y, hipStream_t s) {
+    const int64_t tiles = (nb + kBfT - 1) / kBfT;
+    hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel>), dim3((unsigned)tiles), dim3(kBfThreads), 0, s, X, n_x, Bt, K,
+                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, Y);
+}
+
+__global__ void k_zero_u16(uint16_t* __restrict__ y, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        y[i] = 0;
+}
+
+template <typename Sel>
+int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
+                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s) {
+    if (!blk_bf16_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no bf16 block engine for %dx%d, K=%d", ca, cb, K);
+    const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
+    if (nb == 0) return GSC_OK;
+    auto Y16 = reinterpret_cast<uint16_t*>(Y);
+    if (n_x == 0) {   // no input rows to read (the engine always issues its row loads)
+        const int64_t n = n_y * cb;
+        hipLaunchKernelGGL(k_zero_u16, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256),
+                           0, s, Y16, n);
+        GSC_LAUNCH_CHECK();
+        return GSC_OK;
+    }
+    auto X16 = reinterpret_cast<const uint16_t*>(X);
+    auto B16 = reinterpret_cast<const uint16_t*>(Bt);
+#define GSC_BFB_CASE(A, B)                                                        \
+    if (ca == A && cb == B) {                                                     \
+        launch_blk_bf16<A, B, Sel>(X16, n_x, B16, K, sel, plan, nb, n_y, Y16, s); \
+        GSC_LAUNCH_CHECK();                                                       \
+        return GSC_OK;                                                            \
+    }
+    GSC_BFB_CASE(64, 64) GSC_BFB_CASE(64, 128) GSC_BFB_CASE(64, 256) GSC_BFB_CASE(128, 64) GSC_BFB_CASE(128, 128)
+    GSC_BFB_CASE(128, 256) GSC_BFB_CASE(256, 64) GSC_BFB_CASE(256, 128) GSC_BFB_CASE(256, 256)
+#undef GSC_BFB_CASE
+    return fail(GSC_EINVAL, "conv: no bf16 block engine for %dx%d", ca, cb);
+}
+
+template int conv_blk_bf16<WIdentity>(int, int, const void*, int64_t, const void*, const WIdentity&, int,
+                                      const BlockPlan&, int64_t, void*, hipStream_t);
+template int conv_blk_bf16<WSel>(int, int, const void*, int64_t, const void*, const WSel&, int, const BlockPlan&,
+                                 int64_t, void*, hipStream_t);
 
 bool blk_f32_supported(int ca, int cb, int K) {
     auto ok = [](int c) { return c == 16 || c == 32 || c == 64; };

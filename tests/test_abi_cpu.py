@@ -166,6 +166,8 @@ def test_plan_validation(L):
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 10) == 0
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33) == 0
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 3, 16, 27) == 0
+    assert L.gsc_conv_block_engine(gsc.GSC_BF16, 256, 256, 27) == 1
+    assert L.gsc_conv_block_engine(gsc.GSC_BF16, 32, 32, 27) == 0
     # a plan is all four pointers or none
     rc = L.gsc_sparse_conv_fwd(0, fake, 10, 16, fake, 16, 27, fake, fake, fake, fake, 10, fake, None, fake, fake,
                                fake, 10, None, 0, None)

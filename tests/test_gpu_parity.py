@@ -296,14 +296,18 @@ def test_conv_plan_structure_bf16_wide():
     _check_plan(gsc.gsc_conv_plan(km))
 
 
-def _plan_case(coords, ci, co, offs, seed, ts=1):
-    """_conv_case through the block engine: plans of the forward and the
-    role-reversed map, fp32."""
+def _plan_case(coords, ci, co, offs, seed, ts=1, dtype="f32"):
+    """_conv_case through the block engines: plans of the forward and the
+    role-reversed map."""
     c = _t(coords)
-    X, _ = WL.random_features(seed, len(coords), ci)
-    W, _ = WL.random_weights(seed, len(offs), ci, co)
-    G, _ = WL.random_features(seed + 1, len(coords), co)
-    tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
+    X, Xb = WL.random_features(seed, len(coords), ci, dtype)
+    W, Wb = WL.random_weights(seed, len(offs), ci, co, dtype)
+    G, Gb = WL.random_features(seed + 1, len(coords), co, dtype)
+    if dtype == "bf16":
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tX, tW, tG = dev(Xb), dev(Wb), dev(Gb)
+    else:
+        tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
     table = gsc.gsc_coords_build(c)
     km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(table, c, offs, tensor_stride=ts, dense=True))
     tm = gsc.gsc_conv_plan(gsc.transposed_kernel_map(table, c, offs, tensor_stride=ts, dense=True))
@@ -313,8 +317,8 @@ def _plan_case(coords, ci, co, offs, seed, ts=1):
     _check_plan(km)
     _check_plan(tm)
     m = O.kernel_map(coords, coords, np.asarray(offs), ts)
-    assert rel_err(to_np(Y), O.conv_forward(X, W, m, len(coords))) <= TOL["f32"]
-    assert rel_err(to_np(dX), O.conv_backward(X, W, G, m)[0]) <= TOL["f32"]
+    assert rel_err(to_np(Y), O.conv_forward(X, W, m, len(coords))) <= TOL[dtype]
+    assert rel_err(to_np(dX), O.conv_backward(X, W, G, m)[0]) <= TOL[dtype]
 
 
 @pytest.mark.parametrize("ci,co,region", [(16, 16, "cube3"), (16, 64, "cube3"), (64, 16, "cube2"), (32, 64, "cube2"),
@@ -326,11 +330,24 @@ def test_block_engine_shapes(ci, co, region):
     _plan_case(coords, ci, co, regions.hypercube(int(region[-1]), 3), 121)
 
 
+@pytest.mark.parametrize("ci,co,region", [(256, 256, "cube3"), (128, 256, "cube2"), (256, 128, "cube3"),
+                                           (64, 128, "cube3"), (128, 64, "cube2"), (64, 64, "cube3"),
+                                           (256, 64, "cube2"), (64, 256, "cube2"), (128, 128, "cube3")])
+def test_block_engine_bf16(ci, co, region):
+    coords = WL.random_coords(140 + ci // 32 + co // 16, 2500, 3, -12, 12, batch=2)
+    K = 27 if region == "cube3" else 8
+    assert gsc.gsc_conv_block_engine(gsc.GSC_BF16, ci, co, K) and gsc.gsc_conv_block_engine(gsc.GSC_BF16, co, ci, K)
+    _say(f"[gpu] bf16 block engine {ci}->{co} {region}")
+    _plan_case(coords, ci, co, regions.hypercube(int(region[-1]), 3), 141, dtype="bf16")
+
+
 def test_block_engine_edges():
     # one voxel, a ragged last block, no input rows, 4D hybrid region
     _plan_case(np.array([[0, -7, 3, 11]], np.int32), 16, 32, regions.hypercube(3, 3), 131)
     _plan_case(WL.random_coords(132, 37, 3, -3, 3, batch=2), 32, 32, regions.hypercube(3, 3), 132)
     _plan_case(WL.random_coords(133, 2000, 4, -5, 5, batch=1), 32, 32, regions.hybrid(3, 4), 133)
+    _plan_case(WL.random_coords(135, 37, 3, -3, 3, batch=2), 128, 256, regions.hypercube(3, 3), 135, dtype="bf16")
+    _plan_case(np.array([[0, -7, 3, 11]], np.int32), 64, 64, regions.hypercube(3, 3), 136, dtype="bf16")
     c = torch.empty((0, 4), dtype=torch.int32, device=DEV)
     km = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, regions.hypercube(3, 3), dense=True))
     Y = gsc.gsc_sparse_conv_fwd(torch.empty((0, 16), device=DEV), torch.randn((27, 16, 16), device=DEV), km)
