@@ -277,32 +277,29 @@ __global__ void k_zero_f32(float* __restrict__ y, int64_t n) {
 //
 // A workgroup of four waves owns a tile of kBfT blocks (128 positions); wave
 // w owns output columns [w*CB/4, (w+1)*CB/4) of all of them and keeps their
-// sums in registers.  The tile is computed offset by offset over the union of
-// its blocks' masks, each offset's reduction in parts of 64 channels: a group
-// (offset, part) reads its weight fragments into registers once and applies
-// them to every block of the tile that has the offset (blocks in a static
-// loop, so the accumulators are addressed statically; the mask-sorted order
-// makes most blocks have most of the tile's offsets).
-//
-// After the tile's items and output rows are staged in LDS the waves are
-// independent: each wave gathers its items' rows into its own LDS ring with
-// LDS DMA (kBfAhead items ahead) and copies its next weight fragments into
-// the other of its two LDS buffers the same way.  Every item issues the same
-// number of copies (a group's real weight copies in its first items, copies
-// of one line into a scratch slot after that), so the waits are static
-// vector-memory counts and no register is ever loaded from global memory in
-// the loop.
+// sums in registers.  The tile is computed group by group: a group is one
+// offset of the union of the tile's masks and one 64-channel part of the
+// reduction, and it applies that part of the offset's weights to every
+// block having the offset (the mask-sorted order makes that most of the
+// tile's blocks).  The schedule is a software pipeline over groups, written
+// out statically (blocks in a static loop, groups unrolled over the three
+// stages), so every iteration issues the same loads and the compiler's
+// waits cover exactly the data an MFMA needs:
+//   group g + 2: each wave loads its quarter of every block's 16 rows
+//                (4 rows x 128 bytes, a row missing in that block's item
+//                still loads row 0) and its own weight fragments into
+//                registers;
+//   group g + 1: the quarters go to the LDS slab of that group (two slabs),
+//                zeroed where the block's item has no row;
+//   group g:     the MFMAs, rows read from LDS, weights from registers.
+// One barrier per group hands a slab over.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
 constexpr int kBfT = 8;                              // blocks per tile
 constexpr int kBfThreads = 256;
 constexpr int kBfIdxInts = kBfT * kPlanMaxK * 16;    // the tile's items, at most
-constexpr int kBfAhead = 5;                          // items whose rows are in flight
-constexpr int kBfRing = kBfAhead + 1;                // row slots per wave
 
 template <int CA, int CB>
 struct BlkBf16 {
@@ -311,61 +308,18 @@ struct BlkBf16 {
     static constexpr int CAH = 64;                   // channels per part
     static constexpr int H = CA / CAH;               // parts of the reduction
     static constexpr int KH = CAH / 32;              // MFMA steps per part
-    static constexpr int RW = KH * NB;               // 1 KiB weight regions per wave and group
-    static constexpr int WPS = RW / 4 > 0 ? RW / 4 : 1;   // weight copies per item
-    static constexpr int P = RW / WPS;               // items that carry a group's real copies
-    static constexpr int OPS = WPS + 2;              // copies per item (weights + two row halves)
-    static_assert(P * WPS == RW, "weight regions must split into parts");
-    static_assert(OPS * kBfAhead < 64, "vmcnt range");
+    static constexpr int RW = KH * NB;               // weight fragments (16 bytes per lane) per group
+    static_assert(RW <= kBfT, "a group's weights load one fragment per block iteration");
 };
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
-// LDS reads as inline asm (the compiler would otherwise wait for every LDS
-// DMA copy in flight before them); after_wait() makes uses of a result
-// depend on the wait that follows the reads (volatile asm keeps its order).
-__device__ __forceinline__ u32x4 lds_read_b128(uint32_t a) {
-    u32x4 v;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
-    return v;
-}
-__device__ __forceinline__ int32_t lds_read_b32(uint32_t a) {
-    int32_t v;
-    asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a) : "memory");
-    return v;
-}
-__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-template <typename T>
-__device__ __forceinline__ void after_wait(T& x) {
-    asm volatile("" : "+v"(x));
-}
-template <int N>
-__device__ __forceinline__ void wait_vm() {   // at most N vector-memory operations in flight
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-__device__ __forceinline__ void wait_vm_dyn(int n) {   // n clamped to [0, 63]
-    switch (n <= 0 ? 0 : (n >= 63 ? 63 : n)) {
-#define GSC_WVD(c) case c: wait_vm<c>(); break;
-        GSC_WVD(0) GSC_WVD(1) GSC_WVD(2) GSC_WVD(3) GSC_WVD(4) GSC_WVD(5) GSC_WVD(6) GSC_WVD(7)
-        GSC_WVD(8) GSC_WVD(9) GSC_WVD(10) GSC_WVD(11) GSC_WVD(12) GSC_WVD(13) GSC_WVD(14) GSC_WVD(15)
-        GSC_WVD(16) GSC_WVD(17) GSC_WVD(18) GSC_WVD(19) GSC_WVD(20) GSC_WVD(21) GSC_WVD(22) GSC_WVD(23)
-        GSC_WVD(24) GSC_WVD(25) GSC_WVD(26) GSC_WVD(27) GSC_WVD(28) GSC_WVD(29) GSC_WVD(30) GSC_WVD(31)
-        GSC_WVD(32) GSC_WVD(33) GSC_WVD(34) GSC_WVD(35) GSC_WVD(36) GSC_WVD(37) GSC_WVD(38) GSC_WVD(39)
-        GSC_WVD(40) GSC_WVD(41) GSC_WVD(42) GSC_WVD(43) GSC_WVD(44) GSC_WVD(45) GSC_WVD(46) GSC_WVD(47)
-        GSC_WVD(48) GSC_WVD(49) GSC_WVD(50) GSC_WVD(51) GSC_WVD(52) GSC_WVD(53) GSC_WVD(54) GSC_WVD(55)
-        GSC_WVD(56) GSC_WVD(57) GSC_WVD(58) GSC_WVD(59) GSC_WVD(60) GSC_WVD(61) GSC_WVD(62) GSC_WVD(63)
-#undef GSC_WVD
-        default: wait_vm<0>();
-    }
-}
 
-// Item walk of a tile (all wave-uniform): offsets k of the tile's union
-// ascending, parts h, blocks b having k ascending.
-struct BfIt {
-    int k, h, b;
-    uint32_t bk;   // blocks of the tile having offset k
+// One group of the walk (wave-uniform): offset k, part h, blocks having k.
+struct BfGroup {
+    int k, h;
+    uint32_t bk;
     bool valid;
 };
 
@@ -376,13 +330,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
                 const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
                 uint16_t* __restrict__ Y) {
     using C = BlkBf16<CA, CB>;
-    struct WaveLds {
-        uint8_t w[2][C::RW][1024];            // weight fragments of two groups
-        uint8_t scratch[C::WPS][1024];        // target of the copies that keep the count fixed
-        uint8_t rows[kBfRing][2][1024];       // 16 rows x 64 channels per item, two 8-row halves
-        uint32_t okmask[kBfRing];             // rows of each slot with an input row
-    };
-    __shared__ __attribute__((aligned(16))) WaveLds wl[4];
+    __shared__ __attribute__((aligned(16))) uint8_t slab[2][kBfT][16 * 128];   // [group parity][block][row][128 B]
     __shared__ int32_t idx_s[kBfIdxInts];
     __shared__ int32_t perm_s[kBfT * 16];
     const int tid = threadIdx.x;
@@ -390,7 +338,6 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
     const int r16 = lane & 15, q = lane >> 4;
     const int64_t b0 = (int64_t)blockIdx.x * kBfT;
     const int nbt = (int)min((int64_t)kBfT, nb - b0);
-    WaveLds& my = wl[wave];
 
     // the tile's blocks (wave-uniform) and the offset -> weight map per lane
     uint32_t bm[kBfT];
@@ -418,77 +365,60 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         for (int b = 0; b < kBfT; ++b) m |= ((bm[b] >> k) & 1u) << b;
         return m;
     };
-    auto first = [&]() {
-        BfIt it{0, 0, 0, 0u, U != 0};
-        if (it.valid) {
-            it.k = __ffs(U) - 1;
-            it.bk = blocks_with(it.k);
-            it.b = __ffs(it.bk) - 1;
+    auto next_of = [&](BfGroup g) {
+        if (!g.valid) return g;
+        if (g.h + 1 < C::H) {
+            ++g.h;
+            return g;
         }
-        return it;
-    };
-    auto advance = [&](BfIt it) {
-        if (!it.valid) return it;
-        const uint32_t rem = it.bk & ~((2u << it.b) - 1u);
-        if (rem) {
-            it.b = __ffs(rem) - 1;
-        } else if (it.h + 1 < C::H) {
-            ++it.h;
-            it.b = __ffs(it.bk) - 1;
-        } else {
-            const uint32_t kr = it.k < 31 ? U & ~((2u << it.k) - 1u) : 0u;
-            if (kr) {
-                it.k = __ffs(kr) - 1;
-                it.h = 0;
-                it.bk = blocks_with(it.k);
-                it.b = __ffs(it.bk) - 1;
-            } else {
-                it.valid = false;
-            }
+        const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
+        if (!kr) {
+            g.valid = false;
+            return g;
         }
-        return it;
+        g.k = __ffs(kr) - 1;
+        g.h = 0;
+        g.bk = blocks_with(g.k);
+        return g;
     };
 
-    // copy part p (regions p*WPS ..) of this wave's weight fragments of group
-    // (k, h) into buffer buf: region (s, j) holds lane (c, q)'s 16 bytes of
-    // B_k rows 64 h + 32 s + 8 q .. +7, column w*NC + 16 j + c
-    auto copy_w = [&](int k, int h, int buf, int p) {
-        const uint16_t* src = Bt + (int64_t)readlane_i32(sel_lane, k) * CB * CA + h * C::CAH + 8 * q;
-#pragma unroll
-        for (int i = 0; i < C::WPS; ++i) {
-            const int reg = p * C::WPS + i;
-            const int st = reg / C::NB, j = reg % C::NB;
-            const uint16_t* g = src + (int64_t)(wave * C::NC + 16 * j + r16) * CA + 32 * st;
-            __builtin_amdgcn_global_load_lds((glb_void_t*)g, (lds_void_t*)&my.w[buf][reg][0], 16, 0, 0);
+    // registers of one pipeline stage: this wave's weight fragments of a group
+    // and its quarter (rows 4w .. 4w+3) of every block's rows
+    struct Stage {
+        u32x4 w[C::RW];
+        u32x4 r[kBfT];
+        bool ok[kBfT];
+    };
+    // lane l < 32 loads row 4w + l/8 of the block's item, the 16-byte chunk
+    // (l % 8) ^ (row % 8) of the group's 64 channels (swizzled so that the
+    // fragment reads hit distinct banks); lane l also loads weight fragment
+    // b of the group: region (s, j) = lane (c, q)'s 16 bytes of B_k rows
+    // 64 h + 32 s + 8 q .. +7, column w*NC + 16 j + c
+    const int lrow = 4 * wave + (lane >> 3) % 4, lchunk = lane & 7;
+    auto load_block = [&](const BfGroup& g, int b, Stage& st) {
+        const bool has = g.valid && ((g.bk >> b) & 1u);
+        const int il = has ? ibl[b] + __popc(bm[b] & ((1u << g.k) - 1u)) : 0;
+        const int32_t id = idx_s[il * 16 + lrow];
+        st.ok[b] = has && id >= 0 && id < n_x;
+        const uint16_t* src = X + (int64_t)(st.ok[b] ? id : 0) * CA + (g.valid ? g.h : 0) * C::CAH +
+                              8 * (lchunk ^ (lrow & 7));
+        st.r[b] = *reinterpret_cast<const u32x4*>(src);
+        if (b < C::RW) {
+            const int s2 = b / C::NB, j = b % C::NB;
+            const int kk = g.valid ? g.k : 0;
+            const uint16_t* wsrc = Bt + (int64_t)readlane_i32(sel_lane, kk) * CB * CA + (g.valid ? g.h : 0) * C::CAH +
+                                   8 * q + (int64_t)(wave * C::NC + 16 * j + r16) * CA + 32 * s2;
+            st.w[b] = *reinterpret_cast<const u32x4*>(wsrc);
         }
+        // keep the loads here: their uses sit in conditional blocks two groups
+        // on, and sinking them there would undo the pipeline
+        asm volatile("" ::: "memory");
     };
-    auto copy_dummy = [&]() {   // one cache line into the scratch slots
-#pragma unroll
-        for (int i = 0; i < C::WPS; ++i)
-            __builtin_amdgcn_global_load_lds((glb_void_t*)Bt, (lds_void_t*)&my.scratch[i][0], 16, 0, 0);
-    };
-    // rows of item it into ring slot: half i, lane l -> row 8 i + l / 8, its
-    // 16-byte chunk (l % 8) ^ (row % 8) (swizzled so that the fragment reads
-    // below hit distinct banks); slots of missing rows are recorded, not read
-    const uint32_t idx_base = lds_addr(idx_s);
-    auto copy_rows = [&](const BfIt& it, int slot) {
-        const int il = it.valid ? ibl[it.b] + __popc(bm[it.b] & ((1u << it.k) - 1u)) : 0;
-        const int rr0 = lane >> 3, t = lane & 7;
-        int32_t id0 = lds_read_b32(idx_base + (uint32_t)(il * 16 + rr0) * 4);
-        int32_t id1 = lds_read_b32(idx_base + (uint32_t)(il * 16 + 8 + rr0) * 4);
-        int32_t idr = lds_read_b32(idx_base + (uint32_t)(il * 16 + r16) * 4);
-        wait_lgkm0();
-        after_wait(id0);
-        after_wait(id1);
-        after_wait(idr);
-        const bool ok0 = it.valid && id0 >= 0 && id0 < n_x, ok1 = it.valid && id1 >= 0 && id1 < n_x;
-        const uint16_t* g0 = X + (int64_t)(ok0 ? id0 : 0) * CA + it.h * C::CAH + 8 * (t ^ (rr0 & 7));
-        const uint16_t* g1 = X + (int64_t)(ok1 ? id1 : 0) * CA + it.h * C::CAH + 8 * (t ^ ((8 + rr0) & 7));
-        __builtin_amdgcn_global_load_lds((glb_void_t*)g0, (lds_void_t*)&my.rows[slot][0][0], 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((glb_void_t*)g1, (lds_void_t*)&my.rows[slot][1][0], 16, 0, 0);
-        const bool okr = it.valid && idr >= 0 && idr < n_x;
-        const uint32_t m = (uint32_t)__ballot(okr && lane < 16);
-        if (lane == 0) my.okmask[slot] = m;
+    auto store_block = [&](const Stage& st, int b, int par) {
+        if (lane < 32) {
+            const u32x4 v = st.ok[b] ? st.r[b] : u32x4{0u, 0u, 0u, 0u};
+            *reinterpret_cast<u32x4*>(&slab[par][b][(4 * wave) * 128 + lane * 16]) = v;
+        }
     };
 
     floatx4 acc[kBfT][C::NB];
@@ -498,97 +428,55 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         for (int j = 0; j < C::NB; ++j) acc[b][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     if (U != 0) {
-        // prologue: the first group's weights, the first kBfAhead items' rows
-        BfIt g = first();   // first item of the current group
-        BfIt ahead = g;     // next item whose rows are copied
-        for (int p = 0; p < C::P; ++p) copy_w(g.k, g.h, 0, p);
-        for (int i = 0; i < kBfAhead; ++i) {
-            copy_rows(ahead, i);
-            ahead = advance(ahead);
-        }
-        int e = 0;          // items done
-        int buf = 0;
-        for (;;) {
-            // group (g.k, g.h): its fragments, the next group's copy target
-            wait_vm<C::OPS * kBfAhead>();   // (only needed for the first group: later ones wait at their end)
-            u32x4 wf[C::KH][C::NB];
-#pragma unroll
-            for (int st = 0; st < C::KH; ++st)
-#pragma unroll
-                for (int j = 0; j < C::NB; ++j) wf[st][j] = lds_read_b128(lds_addr(&my.w[buf][st * C::NB + j][lane * 16]));
-            wait_lgkm0();
-#pragma unroll
-            for (int st = 0; st < C::KH; ++st)
-#pragma unroll
-                for (int j = 0; j < C::NB; ++j) after_wait(wf[st][j]);
-            int nk = g.k, nh = g.h + 1;   // the next group (none: copies of this one into the idle buffer)
-            if (nh == C::H) {
-                nh = 0;
-                const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
-                nk = kr ? __ffs(kr) - 1 : g.k;
-                if (!kr) nh = g.h;
-            }
-            const int n_g = __popc(g.bk);   // items of the group
-            int step = 0;                   // items of the group done
+        // The walk starts two empty groups early, so that entering the loop
+        // leaves no loads in flight and the loop's own waits hold from its
+        // first group on; an empty group loads (and stores) but computes
+        // nothing.
+        Stage S[3] = {};
+        BfGroup g0{0, 0, 0u, false}, g1 = g0, g2{__ffs(U) - 1, 0, 0u, true};
+        g2.bk = blocks_with(g2.k);
+        int left = __popc(U) * C::H + 2;
+        int par = 0;   // slab of the current group
+        // one group: load g+2 into stage (p+2)%3, store g+1 (stage (p+1)%3) to
+        // the other slab, MFMAs of g (stage p) from this slab
+        auto group = [&](auto P) -> bool {
+            constexpr int p = decltype(P)::value;
+            Stage& cur = S[p];
+            Stage& nxt = S[(p + 1) % 3];
+            Stage& far = S[(p + 2) % 3];
 #pragma unroll
             for (int b = 0; b < kBfT; ++b) {
-                if ((g.bk >> b) & 1u) {
-                    if (step < C::P) copy_w(nk, nh, buf ^ 1, step);
-                    else copy_dummy();
-                    const int slot_new = (e + kBfAhead) % kBfRing;
-                    copy_rows(ahead, slot_new);
-                    ahead = advance(ahead);
-                    const int slot = e % kBfRing;
-                    wait_vm<C::OPS * kBfAhead>();   // item e's rows: the next kBfAhead items' copies may fly
-                    const uint32_t okm = (uint32_t)lds_read_b32(lds_addr(&my.okmask[slot]));
+                load_block(g2, b, far);
+                store_block(nxt, b, par ^ 1);
+                if ((g0.bk >> b) & 1u) {
                     u32x4 a[C::KH];
 #pragma unroll
-                    for (int st = 0; st < C::KH; ++st) {
-                        const int c = 4 * st + q;   // 16-byte chunk of row r16
-                        a[st] = lds_read_b128(lds_addr(&my.rows[slot][r16 >> 3][((r16 & 7) * 8 + (c ^ (r16 & 7))) * 16]));
-                    }
-                    wait_lgkm0();
-                    uint32_t okv = okm;
-                    after_wait(okv);
-                    const bool ok = (okv >> r16) & 1u;
-#pragma unroll
-                    for (int st = 0; st < C::KH; ++st) {
-                        after_wait(a[st]);
-                        a[st] = ok ? a[st] : u32x4{0u, 0u, 0u, 0u};
+                    for (int s2 = 0; s2 < C::KH; ++s2) {
+                        const int c = 4 * s2 + q;   // 16-byte chunk of row r16
+                        a[s2] = *reinterpret_cast<const u32x4*>(&slab[par][b][r16 * 128 + ((c ^ (r16 & 7)) * 16)]);
                     }
 #pragma unroll
-                    for (int st = 0; st < C::KH; ++st)
+                    for (int s2 = 0; s2 < C::KH; ++s2)
 #pragma unroll
                         for (int j = 0; j < C::NB; ++j)
-                            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[st]),
-                                                                                __builtin_bit_cast(bf16x8, wf[st][j]),
-                                                                                acc[b][j], 0, 0, 0);
-                    ++e;
-                    ++step;
+                            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8, a[s2]), __builtin_bit_cast(bf16x8, cur.w[s2 * C::NB + j]),
+                                acc[b][j], 0, 0, 0);
                 }
             }
-            // the next group's weights: issued in this group's first P items
-            // (all of them now if the group was shorter)
-            if (n_g < C::P) {
-                for (int p = n_g; p < C::P; ++p) copy_w(nk, nh, buf ^ 1, p);
-                wait_vm<0>();
-            } else {
-                wait_vm_dyn(2 + C::OPS * (n_g - C::P));   // all but what the later items issued
-            }
-            buf ^= 1;
-            // next group
-            if (g.h + 1 < C::H) {
-                ++g.h;
-            } else {
-                const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
-                if (!kr) break;
-                g.k = __ffs(kr) - 1;
-                g.h = 0;
-                g.bk = blocks_with(g.k);
-            }
+            __syncthreads();   // slab par ^ 1 written, slab par read by every wave
+            par ^= 1;
+            g0 = g1;
+            g1 = g2;
+            g2 = next_of(g2);
+            return --left == 0;
+        };
+        for (;;) {
+            if (group(std::integral_constant<int, 0>{})) break;
+            if (group(std::integral_constant<int, 1>{})) break;
+            if (group(std::integral_constant<int, 2>{})) break;
         }
     }
-    wait_vm<0>();
     // write the tile: lane (c, q) holds rows 4q+i, column 16 j + c of block b's wave columns
 #pragma unroll
     for (int b = 0; b < kBfT; ++b) {
