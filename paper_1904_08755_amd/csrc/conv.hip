@@ -746,7 +746,8 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
     int rc = plan_args("conv_fwd", n_out, perm, bmask, ibase, items, &planned);
     if (rc) return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (planned && gsc_conv_block_engine(dtype, c_in, c_out, K) && aligned16(X) && aligned16(W)) {
+    if (planned && gsc_conv_block_engine(dtype, c_in, c_out, K) && aligned16(X) && aligned16(W) &&
+        (dtype != GSC_BF16 || blk_bf16_fits(n_in, c_in))) {
         if (n_in > 0 && !X) return fail(GSC_EINVAL, "conv_fwd: X is null");
         const BlockPlan plan{perm, bmask, ibase, items};
         if (dtype == GSC_BF16) {   // B_k = W[k]: the engine reads its columns, so the transposed copy
@@ -807,7 +808,8 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         bool planned = false;
         int rc = plan_args("conv_bwd", n_in, t_perm, t_bmask, t_ibase, t_items, &planned);
         if (rc) return rc;
-        if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W)) {
+        if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W) &&
+            (dtype != GSC_BF16 || blk_bf16_fits(n_out, c_out))) {
             const BlockPlan plan{t_perm, t_bmask, t_ibase, t_items};
             if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
                 rc = conv_blk_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan, n_in, dX, s);

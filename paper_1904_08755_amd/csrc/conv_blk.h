@@ -35,6 +35,8 @@ int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bo
 // bf16: the transposed weights for the forward pass, W itself for the input
 // gradient).  Asynchronous.
 bool blk_bf16_supported(int ca, int cb, int K);
+// The engine addresses X with 32-bit byte offsets: n_x * ca below 2^30.
+bool blk_bf16_fits(int64_t n_x, int ca);
 template <typename Sel>
 int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
                   const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s);

@@ -285,12 +285,12 @@ __global__ void k_zero_f32(float* __restrict__ y, int64_t n) {
 // out statically (blocks in a static loop, groups unrolled over the three
 // stages), so every iteration issues the same loads and the compiler's
 // waits cover exactly the data an MFMA needs:
-//   group g + 2: each wave loads its quarter of every block's 16 rows
-//                (4 rows x 128 bytes, a row missing in that block's item
-//                still loads row 0) and its own weight fragments into
-//                registers;
-//   group g + 1: the quarters go to the LDS slab of that group (two slabs),
-//                zeroed where the block's item has no row;
+//   group g + 2: wave w loads the rows of blocks 2w and 2w + 1 (eight rows
+//                of 128 bytes per load) and its own weight fragments into
+//                registers, through buffer loads: a block without the
+//                offset, or an item without a row, reads out of range and
+//                so gets zeros;
+//   group g + 1: the rows go to the LDS slab of that group (two slabs);
 //   group g:     the MFMAs, rows read from LDS, weights from registers.
 // One barrier per group hands a slab over.
 // ---------------------------------------------------------------------------
@@ -300,6 +300,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBfT = 8;                              // blocks per tile
 constexpr int kBfThreads = 256;
 constexpr int kBfIdxInts = kBfT * kPlanMaxK * 16;    // the tile's items, at most
+constexpr int kBufFlags = 0x00020000;                // buffer descriptor word 3: 32-bit data format
+constexpr uint32_t kBufNone = 0x80000000u;           // an offset past any row buffer the engine takes
 
 template <int CA, int CB>
 struct BlkBf16 {
@@ -309,12 +311,10 @@ struct BlkBf16 {
     static constexpr int H = CA / CAH;               // parts of the reduction
     static constexpr int KH = CAH / 32;              // MFMA steps per part
     static constexpr int RW = KH * NB;               // weight fragments (16 bytes per lane) per group
-    static_assert(RW <= kBfT, "a group's weights load one fragment per block iteration");
+    static constexpr int WB = kBfT / 4;              // blocks whose rows one wave loads
+    static constexpr int RL = 2 * WB;                // row loads (eight rows each) per wave and group
+    static_assert(RW <= kBfT && RL <= kBfT, "a group's loads are spread over its block iterations");
 };
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
 
 // One group of the walk (wave-uniform): offset k, part h, blocks having k.
 struct BfGroup {
@@ -350,6 +350,20 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         ibl[b] = b < nbt ? (int32_t)(ibase[b0 + b] - ib0) : 0;
         U |= bm[b];
     }
+    // the blocks whose rows this wave loads
+    uint32_t bmw[C::WB];
+    int32_t iblw[C::WB];
+#pragma unroll
+    for (int j = 0; j < C::WB; ++j) {
+        bmw[j] = 0u;
+        iblw[j] = 0;
+#pragma unroll
+        for (int b = j; b < kBfT; b += C::WB)
+            if (b == C::WB * wave + j) {
+                bmw[j] = bm[b];
+                iblw[j] = ibl[b];
+            }
+    }
     const int n_items = (int)(ibase[b0 + nbt] - ib0);
     const int sel_lane = lane < K ? sel(lane) : 0;
     for (int i = tid; i < n_items * 16; i += kBfThreads) idx_s[i] = items[ib0 * 16 + i];
@@ -358,6 +372,12 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         perm_s[i] = pos < n_y ? perm[pos] : -1;
     }
     __syncthreads();   // items and output rows staged
+
+    // X as a buffer of n_x * CA * 2 bytes (below 2^31), so that kBufNone reads zeros
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)(n_x * CA * 2), kBufFlags);
+    const __amdgpu_buffer_rsrc_t wr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Bt, (short)0, (int)((int64_t)K * CB * CA * 2), kBufFlags);
 
     auto blocks_with = [&](int k) {
         uint32_t m = 0;
@@ -374,6 +394,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         const uint32_t kr = g.k < 31 ? U & ~((2u << g.k) - 1u) : 0u;
         if (!kr) {
             g.valid = false;
+            g.bk = 0u;
             return g;
         }
         g.k = __ffs(kr) - 1;
@@ -382,42 +403,56 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         return g;
     };
 
-    // registers of one pipeline stage: this wave's weight fragments of a group
-    // and its quarter (rows 4w .. 4w+3) of every block's rows
+    // registers of one pipeline stage: this wave's weight fragments of a
+    // group and the rows it loads
     struct Stage {
         u32x4 w[C::RW];
-        u32x4 r[kBfT];
-        bool ok[kBfT];
+        u32x4 r[C::RL];
     };
-    // lane l < 32 loads row 4w + l/8 of the block's item, the 16-byte chunk
-    // (l % 8) ^ (row % 8) of the group's 64 channels (swizzled so that the
-    // fragment reads hit distinct banks); lane l also loads weight fragment
-    // b of the group: region (s, j) = lane (c, q)'s 16 bytes of B_k rows
-    // 64 h + 32 s + 8 q .. +7, column w*NC + 16 j + c
-    const int lrow = 4 * wave + (lane >> 3) % 4, lchunk = lane & 7;
-    auto load_block = [&](const BfGroup& g, int b, Stage& st) {
-        const bool has = g.valid && ((g.bk >> b) & 1u);
-        const int il = has ? ibl[b] + __popc(bm[b] & ((1u << g.k) - 1u)) : 0;
-        const int32_t id = idx_s[il * 16 + lrow];
-        st.ok[b] = has && id >= 0 && id < n_x;
-        const uint16_t* src = X + (int64_t)(st.ok[b] ? id : 0) * CA + (g.valid ? g.h : 0) * C::CAH +
-                              8 * (lchunk ^ (lrow & 7));
-        st.r[b] = *reinterpret_cast<const u32x4*>(src);
+    // Row load j of a wave covers rows 8 (j % 2) .. +7 of block WB w + j / 2:
+    // lane l takes row 8 (j % 2) + l / 8 and stores its 16-byte chunk at
+    // position l % 8 of the slab row, which holds data chunk
+    // (l % 8) ^ (row % 8) (swizzled so that the fragment reads hit distinct
+    // banks).  Weight fragment f = (s, j) is lane (c, q)'s 16 bytes of B_k
+    // rows 64 h + 32 s + 8 q .. +7, column w NC + 16 j + c.
+    const int lrow = lane >> 3;
+    const uint32_t lchunk = 16u * (uint32_t)((lane & 7) ^ (lrow & 7));
+    uint32_t woff[C::RW];
+#pragma unroll
+    for (int f = 0; f < C::RW; ++f)
+        woff[f] = (uint32_t)(((wave * C::NC + 16 * (f % C::NB) + r16) * CA + 32 * (f / C::NB) + 8 * q) * 2);
+    // byte offsets of this lane's rows for group g (kBufNone: none)
+    auto row_offsets = [&](const BfGroup& g, uint32_t (&off)[C::RL]) {
+#pragma unroll
+        for (int j = 0; j < C::RL; ++j) {
+            const uint32_t m = bmw[j / 2];
+            const bool has = g.valid && ((m >> g.k) & 1u);
+            const int il = has ? iblw[j / 2] + __popc(m & ((1u << g.k) - 1u)) : 0;
+            const int32_t v = idx_s[il * 16 + 8 * (j % 2) + lrow];
+            off[j] = has && v >= 0 && v < n_x ? (uint32_t)v * (uint32_t)(CA * 2) + lchunk : kBufNone;
+        }
+    };
+    auto load = [&](const BfGroup& g, int b, const uint32_t (&off)[C::RL], Stage& st) {
+        const int h = g.valid ? g.h : 0;
+        if (b < C::RL) st.r[b] = __builtin_amdgcn_raw_buffer_load_b128(xr, off[b], h * C::CAH * 2, 0);
         if (b < C::RW) {
-            const int s2 = b / C::NB, j = b % C::NB;
-            const int kk = g.valid ? g.k : 0;
-            const uint16_t* wsrc = Bt + (int64_t)readlane_i32(sel_lane, kk) * CB * CA + (g.valid ? g.h : 0) * C::CAH +
-                                   8 * q + (int64_t)(wave * C::NC + 16 * j + r16) * CA + 32 * s2;
-            st.w[b] = *reinterpret_cast<const u32x4*>(wsrc);
+            const int wsel = readlane_i32(sel_lane, g.valid ? g.k : 0);
+            st.w[b] = __builtin_amdgcn_raw_buffer_load_b128(wr, woff[b], (wsel * CB * CA + h * C::CAH) * 2, 0);
         }
         // keep the loads here: their uses sit in conditional blocks two groups
         // on, and sinking them there would undo the pipeline
         asm volatile("" ::: "memory");
     };
-    auto store_block = [&](const Stage& st, int b, int par) {
-        if (lane < 32) {
-            const u32x4 v = st.ok[b] ? st.r[b] : u32x4{0u, 0u, 0u, 0u};
-            *reinterpret_cast<u32x4*>(&slab[par][b][(4 * wave) * 128 + lane * 16]) = v;
+    auto store = [&](const Stage& st, int b, int par) {
+        if (b < C::RL)
+            *reinterpret_cast<u32x4*>(&slab[par][C::WB * wave + b / 2][(b % 2) * 1024 + lane * 16]) = st.r[b];
+    };
+    // row r16's 16-byte chunks 4 s + q (s < KH) of block b in slab par
+    auto read_a = [&](int par, int b, u32x4 (&a)[C::KH]) {
+#pragma unroll
+        for (int s2 = 0; s2 < C::KH; ++s2) {
+            const int c = 4 * s2 + q;
+            a[s2] = *reinterpret_cast<const u32x4*>(&slab[par][b][r16 * 128 + ((c ^ (r16 & 7)) * 16)]);
         }
     };
 
@@ -431,7 +466,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         // The walk starts two empty groups early, so that entering the loop
         // leaves no loads in flight and the loop's own waits hold from its
         // first group on; an empty group loads (and stores) but computes
-        // nothing.
+        // nothing.  left counts the groups until the last one is computed.
         Stage S[3] = {};
         BfGroup g0{0, 0, 0u, false}, g1 = g0, g2{__ffs(U) - 1, 0, 0u, true};
         g2.bk = blocks_with(g2.k);
@@ -439,29 +474,28 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         int par = 0;   // slab of the current group
         // one group: load g+2 into stage (p+2)%3, store g+1 (stage (p+1)%3) to
         // the other slab, MFMAs of g (stage p) from this slab
-        auto group = [&](auto P) -> bool {
+        auto group = [&](auto P) {
             constexpr int p = decltype(P)::value;
             Stage& cur = S[p];
             Stage& nxt = S[(p + 1) % 3];
             Stage& far = S[(p + 2) % 3];
+            uint32_t off[C::RL];
+            row_offsets(g2, off);
+            u32x4 a[2][C::KH];
+            read_a(par, 0, a[0]);
 #pragma unroll
             for (int b = 0; b < kBfT; ++b) {
-                load_block(g2, b, far);
-                store_block(nxt, b, par ^ 1);
+                load(g2, b, off, far);
+                store(nxt, b, par ^ 1);
+                if (b + 1 < kBfT) read_a(par, b + 1, a[(b + 1) & 1]);
                 if ((g0.bk >> b) & 1u) {
-                    u32x4 a[C::KH];
-#pragma unroll
-                    for (int s2 = 0; s2 < C::KH; ++s2) {
-                        const int c = 4 * s2 + q;   // 16-byte chunk of row r16
-                        a[s2] = *reinterpret_cast<const u32x4*>(&slab[par][b][r16 * 128 + ((c ^ (r16 & 7)) * 16)]);
-                    }
 #pragma unroll
                     for (int s2 = 0; s2 < C::KH; ++s2)
 #pragma unroll
                         for (int j = 0; j < C::NB; ++j)
                             acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                __builtin_bit_cast(bf16x8, a[s2]), __builtin_bit_cast(bf16x8, cur.w[s2 * C::NB + j]),
-                                acc[b][j], 0, 0, 0);
+                                __builtin_bit_cast(bf16x8, a[b & 1][s2]),
+                                __builtin_bit_cast(bf16x8, cur.w[s2 * C::NB + j]), acc[b][j], 0, 0, 0);
                 }
             }
             __syncthreads();   // slab par ^ 1 written, slab par read by every wave
@@ -469,13 +503,17 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
             g0 = g1;
             g1 = g2;
             g2 = next_of(g2);
-            return --left == 0;
+            --left;
         };
-        for (;;) {
-            if (group(std::integral_constant<int, 0>{})) break;
-            if (group(std::integral_constant<int, 1>{})) break;
-            if (group(std::integral_constant<int, 2>{})) break;
-        }
+        // one exit, after whole rounds of three groups (the last round's
+        // extra groups are empty): an exit after each group would give the
+        // compiler a path around the later groups' loads, and with it
+        // waits as if every load were recent
+        do {
+            group(std::integral_constant<int, 0>{});
+            group(std::integral_constant<int, 1>{});
+            group(std::integral_constant<int, 2>{});
+        } while (left > 0);
     }
     // write the tile: lane (c, q) holds rows 4q+i, column 16 j + c of block b's wave columns
 #pragma unroll
@@ -497,6 +535,8 @@ bool blk_bf16_supported(int ca, int cb, int K) {
     return (ca == 64 || ca == 128 || ca == 256) && (cb == 64 || cb == 128 || cb == 256) && K >= 1 && K <= kPlanMaxK;
 }
 
+bool blk_bf16_fits(int64_t n_x, int ca) { return n_x >= 0 && n_x * ca < ((int64_t)1 << 30); }
+
 template <int CA, int CB, typename Sel>
 static void launch_blk_bf16(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
                             const BlockPlan& p, int64_t nb, int64_t n_y, uint16_t* Y, hipStream_t s) {
@@ -514,6 +554,7 @@ template <typename Sel>
 int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
                   const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s) {
     if (!blk_bf16_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no bf16 block engine for %dx%d, K=%d", ca, cb, K);
+    if (!blk_bf16_fits(n_x, ca)) return fail(GSC_EINVAL, "conv: bf16 block engine takes at most 2^30 input elements");
     const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
     if (nb == 0) return GSC_OK;
     auto Y16 = reinterpret_cast<uint16_t*>(Y);
