@@ -316,6 +316,19 @@ struct BlkBf16 {
     static_assert(RW <= kBfT && RL <= kBfT, "a group's loads are spread over its block iterations");
 };
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+
+// two fp32 values -> packed bf16 pair (lo, hi), nearest even
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
+}
+
+// value of lane l ^ 1 (DPP quad_perm 1, 0, 3, 2)
+__device__ __forceinline__ float xor1(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false));
+}
+
 // One group of the walk (wave-uniform): offset k, part h, blocks having k.
 struct BfGroup {
     int k, h;
@@ -515,17 +528,41 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
             group(std::integral_constant<int, 2>{});
         } while (left > 0);
     }
-    // write the tile: lane (c, q) holds rows 4q+i, column 16 j + c of block b's wave columns
+    // Write the tile through LDS, 64 positions per pass: the sums become bf16
+    // pairs (lane (c, q) holds rows 4q .. 4q+3 of column c; after an
+    // exchange with lane c ^ 1 an even lane holds rows 4q, 4q+1 of columns
+    // c, c+1 and an odd one rows 4q+2, 4q+3 of columns c-1, c), and whole
+    // output rows go out 16 bytes per lane.
+    constexpr int LPR = CB / 8;                  // lanes per output row
+    constexpr int RPI = kBfThreads / LPR;        // rows per pass of the workgroup
+    static_assert(64 * CB * 2 <= (int)sizeof(slab), "a pass of 64 positions fits the slabs");
+    uint32_t* out_s = reinterpret_cast<uint32_t*>(&slab[0][0][0]);
+    const bool odd = r16 & 1;
 #pragma unroll
-    for (int b = 0; b < kBfT; ++b) {
-        if (b >= nbt) break;
+    for (int half = 0; half < 2; ++half) {
+        if (half) __syncthreads();   // the first pass has been read
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int32_t row = perm_s[16 * b + 4 * q + i];
+        for (int b = 4 * half; b < 4 * half + 4; ++b)
+#pragma unroll
+            for (int j = 0; j < C::NB; ++j) {
+                const floatx4 v = acc[b][j];
+                const float e0 = xor1(odd ? v[0] : v[2]);
+                const float e1 = xor1(odd ? v[1] : v[3]);
+                const uint32_t p0 = odd ? pack_bf16(e0, v[2]) : pack_bf16(v[0], e0);
+                const uint32_t p1 = odd ? pack_bf16(e1, v[3]) : pack_bf16(v[1], e1);
+                const int row = 16 * (b - 4 * half) + 4 * q + (odd ? 2 : 0);
+                const int cp = (wave * C::NC + 16 * j + (r16 & ~1)) / 2;
+                out_s[row * (CB / 2) + cp] = p0;
+                out_s[(row + 1) * (CB / 2) + cp] = p1;
+            }
+        __syncthreads();   // the pass is staged
+#pragma unroll
+        for (int r0 = 0; r0 < 64; r0 += RPI) {
+            const int pos = r0 + tid / LPR;
+            const int32_t row = perm_s[64 * half + pos];
             if (row >= 0 && row < n_y) {
-#pragma unroll
-                for (int j = 0; j < C::NB; ++j)
-                    Y[(int64_t)row * CB + wave * C::NC + 16 * j + r16] = f32_to_bf16_rne(acc[b][j][i]);
+                const u32x4 val = *reinterpret_cast<const u32x4*>(&out_s[pos * (CB / 2) + (tid % LPR) * 4]);
+                *reinterpret_cast<u32x4*>(Y + (int64_t)row * CB + (tid % LPR) * 8) = val;
             }
         }
     }
