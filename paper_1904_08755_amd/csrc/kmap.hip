@@ -11,6 +11,16 @@
 //          from the neighbour table.
 // Pairs of one offset therefore come out sorted by output row, and the
 // result does not depend on scheduling.
+//
+// A map of a coordinate set onto itself (the stride-1 layers of Sec. 3.1:
+// the output coordinates are the array the table was built from) over a
+// region closed under negation, listed so that o_{K-1-k} = -o_k with the
+// origin in the middle, is symmetric: (i, j) is a pair at offset k exactly
+// when (j, i) is one at offset K-1-k, and the middle offset pairs every row
+// with itself.  Such a map probes only the offsets before the middle: each
+// hit also writes its mirrored entry of the neighbour table (set to -1
+// beforehand), the middle offset is written directly, and a second pass
+// counts the mirrored offsets' pairs per group from the table.
 #include <climits>
 #include <vector>
 
@@ -79,8 +89,9 @@ struct KeyOps<unsigned long long> {
 template <typename KeyT, typename Offs>
 __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __restrict__ slots,
                                            const int32_t* __restrict__ out_coords, int64_t n_out, int ncol,
-                                           const Offs& offs, int K, int64_t G, int32_t* __restrict__ cnt,
-                                           int32_t* __restrict__ nbr, bool ok, int64_t j) {
+                                           const Offs& offs, int K, int kprobe, bool self, int64_t G,
+                                           int32_t* __restrict__ cnt, int32_t* __restrict__ nbr, bool ok,
+                                           int64_t j) {
     const bool valid = ok && j < n_out;
     const int D = ncol - 1;
     const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
@@ -114,16 +125,16 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
     in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    for (int k0 = 0; k0 < K; k0 += kBatch) {
+    for (int k0 = 0; k0 < kprobe; k0 += kBatch) {
         KeyT key[kBatch];
         unsigned long long pos[kBatch];
         bool pend[kBatch], hit[kBatch];
         int32_t row[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
-            const int k = min(k0 + b, K - 1);
+            const int k = min(k0 + b, kprobe - 1);
             const int32_t* o = offs.at((int64_t)k * D);
-            bool in = in_b && k0 + b < K;
+            bool in = in_b && k0 + b < kprobe;
             KeyT delta = 0;
 #pragma unroll
             for (int c = 1; c < kMaxCols; ++c) {
@@ -174,29 +185,81 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
             const int k = k0 + b;
-            if (k < K) {
+            if (k < kprobe) {
                 const unsigned long long m = __ballot(hit[b]);
                 if (writer) cnt[(int64_t)k * G + g] = __popcll(m);
                 if (j < n_out) nbr[(int64_t)k * n_out + j] = hit[b] ? row[b] : -1;
+                // the mirrored pair (j, row) at offset K-1-k
+                if (self && hit[b] && row[b] >= 0 && row[b] < n_out) nbr[(int64_t)(K - 1 - k) * n_out + row[b]] = (int32_t)j;
             }
         }
     }
+    if (self) {   // the middle offset: every row with itself
+        const int c = kprobe;
+        const unsigned long long m = __ballot(j < n_out);
+        if (writer) cnt[(int64_t)c * G + g] = __popcll(m);
+        if (j < n_out) nbr[(int64_t)c * n_out + j] = (int32_t)j;
+    }
+}
+
+// Whether a map onto out_coords over a symmetric region (sym) is a map of the
+// table's own coordinate set onto itself.
+__device__ __forceinline__ bool self_map(const TableHeader* h, int ncol, const int32_t* out_coords, int64_t n_out,
+                                         int sym) {
+    return sym && header_ok(h, ncol) && h->src == out_coords && h->n == n_out;
 }
 
 template <typename Offs>
 __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* __restrict__ out_coords,
-                                                         int64_t n_out, int ncol, Offs offs, int K, int64_t G,
+                                                         int64_t n_out, int ncol, Offs offs, int K, int sym, int64_t G,
                                                          int32_t* __restrict__ cnt, int32_t* __restrict__ nbr,
                                                          int64_t* err) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
     const Slot* __restrict__ slots = table_slots(table);
     const bool ok = header_ok(h, ncol);
     if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
+    const bool self = self_map(h, ncol, out_coords, n_out, sym);
+    const int kprobe = self ? (K - 1) / 2 : K;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     if (h->total_bits <= 32)   // uniform: all lanes take the same path
-        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, nbr, ok, j);
+        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, kprobe, self, G, cnt, nbr, ok, j);
     else
-        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, G, cnt, nbr, ok, j);
+        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, kprobe, self, G, cnt, nbr, ok, j);
+}
+
+// Self map: the mirrored offsets' rows of the neighbour table start empty.
+__global__ void __launch_bounds__(kThreads) k_kmap_self_init(const void* table, const int32_t* out_coords,
+                                                             int64_t n_out, int ncol, int K, int sym,
+                                                             int32_t* __restrict__ nbr) {
+    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
+    if (!self_map(h, ncol, out_coords, n_out, sym)) return;
+    const int64_t first = (int64_t)((K + 1) / 2) * n_out, n = (int64_t)(K / 2) * n_out;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        nbr[first + i] = -1;
+}
+
+// Self map: pair counts of the mirrored offsets per 64-row group, from the
+// neighbour table.
+__global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* table, const int32_t* out_coords,
+                                                                int64_t n_out, int ncol, int K, int sym, int64_t G,
+                                                                const int32_t* __restrict__ nbr,
+                                                                int32_t* __restrict__ cnt) {
+    const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
+    if (!self_map(h, ncol, out_coords, n_out, sym)) return;
+    const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+    const int64_t g = j >> 6;
+    const bool writer = __lane_id() == 0 && g < G;
+    constexpr int B = 8;
+    for (int k0 = (K + 1) / 2; k0 < K; k0 += B) {
+        int32_t r[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) r[b] = j < n_out && k0 + b < K ? nbr[(int64_t)(k0 + b) * n_out + j] : -1;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const unsigned long long m = __ballot(r[b] >= 0);
+            if (writer && k0 + b < K) cnt[(int64_t)(k0 + b) * G + g] = __popcll(m);
+        }
+    }
 }
 
 // Fill pass: lane j reads its row of the neighbour table offset by offset;
@@ -233,13 +296,26 @@ static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 template <typename Offs>
 static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t n_out, int ncol, Offs offs, int K,
-                        int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg, int64_t* gidx,
-                        int64_t* n_pairs, int64_t* res, int32_t* cnt, int32_t* nbr, void* scan_ws, hipStream_t s) {
+                        int sym, int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg,
+                        int64_t* gidx, int64_t* n_pairs, int64_t* res, int32_t* cnt, int32_t* nbr, void* scan_ws,
+                        hipStream_t s) {
     const unsigned nblk = (unsigned)((n_out + kThreads - 1) / kThreads);
     if (nblk > 0) {
+        if (sym && K > 1) {   // whether the map is a self map is read from the table on the device
+            const int64_t n_init = (int64_t)(K / 2) * n_out;
+            const int64_t gi = (n_init + kThreads - 1) / kThreads;
+            hipLaunchKernelGGL(k_kmap_self_init, dim3((unsigned)(gi < 4096 ? gi : 4096)), dim3(kThreads), 0, s, in_table, out_coords,
+                               n_out, ncol, K, sym, nbr);
+            GSC_LAUNCH_CHECK();
+        }
         hipLaunchKernelGGL((k_kmap_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol,
-                           offs, K, G, cnt, nbr, res + 1);
+                           offs, K, sym, G, cnt, nbr, res + 1);
         GSC_LAUNCH_CHECK();
+        if (sym && K > 1) {
+            hipLaunchKernelGGL(k_kmap_mirror_count, dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out,
+                               ncol, K, sym, G, nbr, cnt);
+            GSC_LAUNCH_CHECK();
+        }
     }
     int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
     if (rc) return rc;
@@ -311,6 +387,13 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     }
     OffsArg arg;
     std::vector<int32_t> offs((size_t)K * D);
+    // symmetric listing: K odd, the middle offset the origin, o_{K-1-k} = -o_k
+    int sym = K % 2 == 1 ? 1 : 0;
+    for (int k = 0; k < K && sym; ++k)
+        for (int d = 0; d < D; ++d) {
+            const int32_t a = offsets[(size_t)k * D + d], b = offsets[(size_t)(K - 1 - k) * D + d];
+            if ((int64_t)a != -(int64_t)b) sym = 0;
+        }
     for (int k = 0; k < K; ++k)
         for (int d = 0; d < D; ++d) {
             const int64_t ts = tensor_stride ? tensor_stride[d] : 1;
@@ -336,12 +419,12 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     w += align256((size_t)K * n_out * sizeof(int32_t));
     void* scan_ws = w;
     if (by_value)
-        return kmap_enqueue(in_table, out_coords, n_out, ncol, arg, K, G, in_idx, out_idx, cap_pairs, seg, gidx,
+        return kmap_enqueue(in_table, out_coords, n_out, ncol, arg, K, sym, G, in_idx, out_idx, cap_pairs, seg, gidx,
                             n_pairs, res, cnt, nbr, scan_ws, s);
     // synchronous mode: the copy below completes before this call returns
     GSC_HIP(hipMemcpyAsync(d_offs, offs.data(), offs.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
-    return kmap_enqueue(in_table, out_coords, n_out, ncol, OffsPtr{d_offs}, K, G, in_idx, out_idx, cap_pairs, seg,
-                        gidx, n_pairs, res, cnt, nbr, scan_ws, s);
+    return kmap_enqueue(in_table, out_coords, n_out, ncol, OffsPtr{d_offs}, K, sym, G, in_idx, out_idx, cap_pairs,
+                        seg, gidx, n_pairs, res, cnt, nbr, scan_ws, s);
 }
 
 }  // extern "C"

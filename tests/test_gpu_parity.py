@@ -119,6 +119,46 @@ def _conv_case(coords, ci, co, offs, seed, dtype="f32", ts=1):
     return km
 
 
+def _map_arrays(km):
+    m = km.count()
+    return (to_np(km.in_idx[:m]), to_np(km.out_idx[:m]), to_np(km.seg), to_np(km.gidx), to_np(km.nbr))
+
+
+@pytest.mark.parametrize("case", ["cube3", "cube5", "cross3", "hybrid4d", "cube3_ts2", "sync_async"])
+def test_self_map_matches_copy(case):
+    """A map of the table's own coordinate array onto itself over a symmetric
+    region probes half the offsets and mirrors the rest; it must equal the map
+    onto a copy of the array (which probes every offset) bit for bit, and the
+    oracle's map."""
+    if case == "hybrid4d":
+        wl = WL.make_workload(3, scale=0.3)
+        offs = regions.hybrid(3, 4)
+    else:
+        wl = WL.make_workload(1, scale=0.15)
+        offs = {"cube3": regions.hypercube(3, 3), "cube5": regions.hypercube(5, 3),
+                "cross3": regions.hypercross(3, 3), "cube3_ts2": regions.hypercube(3, 3),
+                "sync_async": regions.hypercube(3, 3)}[case]
+    ts = 2 if case == "cube3_ts2" else None
+    coords = torch.from_numpy(wl.coords).to(DEV)
+    if ts:
+        coords = coords.clone()
+        coords[:, 1:] *= 2
+    table = gsc.gsc_coords_build(coords)
+    self_map = gsc.gsc_kernel_map(table, coords, offs, tensor_stride=ts, dense=True,
+                                  sync=case != "sync_async")
+    copy_map = gsc.gsc_kernel_map(table, coords.clone(), offs, tensor_stride=ts, dense=True)
+    torch.cuda.synchronize()
+    a, b = _map_arrays(self_map), _map_arrays(copy_map)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    c_np = to_np(coords)
+    ref = O.kernel_map(c_np, c_np, np.asarray(offs), ts or 1)
+    got = gpu_pairs(self_map)
+    for k in range(len(offs)):
+        assert np.array_equal(got[k][0], np.asarray(ref[k][0])) and np.array_equal(got[k][1], np.asarray(ref[k][1]))
+    _say(f"  {case}: K={len(offs)} pairs={self_map.count()}")
+
+
 def test_empty_input():
     c = torch.empty((0, 4), dtype=torch.int32, device=DEV)
     table = gsc.gsc_coords_build(c)
