@@ -38,7 +38,7 @@ constexpr int kPlanThreads = 256;
 constexpr int kRsBits = 10;                       // radix digit width
 constexpr int kRsBins = 1 << kRsBits;
 constexpr int kRsThreads = 1024;                  // radix sort block
-constexpr int kRsPer = 4;                         // keys per thread and block
+constexpr int kRsPer = 2;                         // keys per thread and block (2048-key tiles: more tiles in flight)
 constexpr int kRsTile = kRsThreads * kRsPer;      // keys per block
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
