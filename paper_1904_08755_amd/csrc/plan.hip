@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
         uint32_t before = 0;
         __hip_atomic_store(mine, (t == 0 ? kStIncl : kStAgg) | c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (t > 0) {
-            constexpr int LW = 16;   // predecessors' entries loaded together
+            constexpr int LW = 4;   // predecessors' entries loaded together (wider batches read more entries past the first inclusive one, and measured slower)
             bool done = false;
             for (int64_t j0 = t - 1; !done && j0 >= 0; j0 -= LW) {
                 uint32_t v[LW];
