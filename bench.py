@@ -48,7 +48,9 @@ def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool) -> 
     library's dispatch: block engine on a plan, else the map's row form)."""
     dt = gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32
     if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
-        return f"k_conv_blk_{'bf16' if dtype == 'bf16' else 'f32'}<{ci}, {co}, false>"
+        if dtype == "bf16":
+            return f"k_conv_blk_bf16<{ci}, {co}, gsc::WIdentity>"
+        return f"k_conv_blk_f32<{ci}, {co}, false>"
     if dtype == "bf16":
         if ci in (128, 256) and co in (128, 256):
             return f"k_conv_bf16_dma<{ci}, {co}, gsc::WIdentity>"
