@@ -17,7 +17,8 @@ Conventions (readings of the paper, listed with the others in the design notes):
 
 Parity status: every function is pinned by the CPU tests (brute-force maps,
 closed-form counts, dense-convolution special cases, adjoint identities, finite
-differences); the row order of ``output_coordinates`` is an implementation
+differences, dense max/average pooling and their gradients, per-batch
+reductions); the row order of ``output_coordinates`` is an implementation
 choice and is compared canonically, not pinned.
 """
 from __future__ import annotations
@@ -234,3 +235,87 @@ def conv_dx_rows(dY: np.ndarray, W: np.ndarray, out_map: Dict[tuple, int], in_co
 
 def map_pair_count(maps: List[Pairs]) -> int:
     return int(sum(len(I) for I, _ in maps))
+
+
+# --------------------------------------------------------------------------- #
+# Pooling over a kernel map (Sec. 4.3, Alg. 3; Sec. 4.4, Alg. 4)
+# --------------------------------------------------------------------------- #
+POOL_MODES = ("max", "avg", "sum")
+
+
+def pool_pairs(maps: List[Pairs]) -> Pairs:
+    """The concatenated lists I and O of Sec. 4.3 (all offsets' pairs, in
+    offset order), stably sorted by output row as in the first step of Alg. 3
+    (SortByKey(I, key=O)), so each output's inputs keep their offset order."""
+    I = np.concatenate([np.asarray(a, dtype=np.int64) for a, _ in maps]) if maps else np.zeros(0, np.int64)
+    O = np.concatenate([np.asarray(b, dtype=np.int64) for _, b in maps]) if maps else np.zeros(0, np.int64)
+    order = np.argsort(O, kind="stable")
+    return I[order], O[order]
+
+
+def pool_forward(X: np.ndarray, maps: List[Pairs], n_out: int, mode: str):
+    """Pooling of the input features over the kernel map M = (I, O).
+
+    max (Sec. 4.3, Alg. 3): for every output coordinate, the channel-wise
+    maximum over the inputs mapped to it; ``arg`` holds, per output and
+    channel, the input row attaining it (the first such input in the sorted
+    pair list), for the backward pass.
+    avg / sum (Sec. 4.4, Alg. 4): F' = S_M F with S_M the 0/1 matrix of the
+    map (row = O, column = I), N = S_M 1, and avg returns F' / N; sum pooling
+    (the variant without the division) returns F'.
+    An output with no input is 0 (arg -1, N 0).  Returns (Y, arg, N)."""
+    assert mode in POOL_MODES
+    X = np.asarray(X, dtype=np.float64)
+    C = X.shape[1]
+    I, O = pool_pairs(maps)
+    Y = np.zeros((n_out, C))
+    arg = np.full((n_out, C), -1, dtype=np.int64)
+    N = np.zeros(n_out, dtype=np.int64)
+    for i, j in zip(I.tolist(), O.tolist()):
+        N[j] += 1
+        if mode == "max":
+            for c in range(C):
+                if arg[j, c] < 0 or X[i, c] > Y[j, c]:
+                    Y[j, c] = X[i, c]
+                    arg[j, c] = i
+        else:
+            Y[j] += X[i]
+    if mode == "avg":
+        nz = N > 0
+        Y[nz] /= N[nz][:, None]
+    return Y, arg, N
+
+
+def pool_backward(dY: np.ndarray, maps: List[Pairs], n_in: int, mode: str, arg: np.ndarray, N: np.ndarray):
+    """Gradient of pool_forward with respect to the input features: sum
+    pooling sends dY[j] to every input of j, avg pooling dY[j] / N[j], and max
+    pooling dY[j, c] to the input that attained the maximum of channel c."""
+    assert mode in POOL_MODES
+    dY = np.asarray(dY, dtype=np.float64)
+    C = dY.shape[1]
+    dX = np.zeros((n_in, C))
+    if mode == "max":
+        for j in range(dY.shape[0]):
+            for c in range(C):
+                if arg[j, c] >= 0:
+                    dX[arg[j, c], c] += dY[j, c]
+        return dX
+    I, O = pool_pairs(maps)
+    for i, j in zip(I.tolist(), O.tolist()):
+        dX[i] += dY[j] / (N[j] if mode == "avg" else 1)
+    return dX
+
+
+def global_pool_forward(X: np.ndarray, batch: np.ndarray, n_batch: int, mode: str):
+    """Global pooling (Sec. 4.4): the kernel map sends every input of batch
+    index b to one output (the origin of b), then pool_forward; output b is the
+    max / mean / sum of the features of batch b's rows."""
+    batch = np.asarray(batch, dtype=np.int64)
+    maps = [(np.arange(len(batch), dtype=np.int64), batch)]
+    return pool_forward(X, maps, n_batch, mode)
+
+
+def global_pool_backward(dY: np.ndarray, batch: np.ndarray, mode: str, arg: np.ndarray, N: np.ndarray):
+    batch = np.asarray(batch, dtype=np.int64)
+    maps = [(np.arange(len(batch), dtype=np.int64), batch)]
+    return pool_backward(dY, maps, len(batch), mode, arg, N)

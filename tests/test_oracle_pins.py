@@ -10,7 +10,11 @@ computed by means that share nothing with the oracle's own code.
   conv3d / conv_transpose3d in float64, and a dense 4D sum of shifted slices
   for the hybrid kernel; the centre-only identity kernel;
 * backward: torch autograd of the dense convolution, adjoint identities and
-  central finite differences.
+  central finite differences;
+* pooling (Sec. 4.3, 4.4): torch max_pool3d over a -inf background and
+  (sum, count) window sums by avg_pool3d for the size-2 partition and the
+  overlapping size-3 window at stride 2, their autograd gradients, and
+  per-batch torch reductions for global pooling.
 
 The planted-mistake tests at the end check that each pin fails for a
 plausible error in the oracle (sign of the offset, a transposed weight, a
@@ -466,3 +470,119 @@ def test_planted_mistakes_are_caught(monkeypatch):
     for k, (I, Oo) in enumerate(m):
         bad_dX[I] += G[Oo].astype(np.float64) @ W[k].astype(np.float64)
     assert abs(np.sum(Y * G) - np.sum(X * bad_dX)) > 1e-6 * abs(np.sum(Y * G))
+
+
+# --------------------------------------------------------------------------- #
+# pooling (Sec. 4.3, Alg. 3; Sec. 4.4, Alg. 4)
+# --------------------------------------------------------------------------- #
+def _pool_setup(seed, K):
+    """Sparse stride-1 input in two batches, its stride-2 output coordinates
+    and the pooling map of a size-K window (K = 2: the {0,1}^3 partition;
+    K = 3: the overlapping {-1,0,1}^3 window)."""
+    c = WL.random_coords(seed, 400, 3, -6, 7, batch=2)
+    X, _ = WL.random_features(seed, len(c), 4)
+    out = O.output_coordinates(c, 2)
+    offs = O.hypercube(K, 3)
+    maps = O.kernel_map(c, out, offs)
+    lo = (np.floor_divide(c[:, 1:].min(0), 2) * 2 - 2).astype(np.int64)
+    shape = c[:, 1:].max(0) - lo + 4
+    shape = shape + (shape % 2)
+    return c, np.asarray(X, np.float64), out, maps, lo, shape
+
+
+def _dense_pool(c, X, out, lo, shape, K, mode, grad=None):
+    """The same pooling on a dense volume with torch: max_pool3d over a -inf
+    background, and (sum, count) by avg_pool3d over zero-filled features and
+    the occupancy; read at the output sites.  With ``grad`` also returns the
+    input gradient of sum(Y * grad) at the input sites (autograd)."""
+    pad = 0 if K == 2 else 1
+    Xt = torch.from_numpy(X).requires_grad_(grad is not None)
+    vol0 = dense_volume(c, np.zeros_like(X), lo, shape)
+    vp = vol0.permute(0, 2, 3, 4, 1).clone()
+    cc = torch.from_numpy((c[:, 1:] - lo).astype(np.int64))
+    b = torch.from_numpy(c[:, 0].astype(np.int64))
+    if mode == "max":
+        vp = torch.full_like(vp, float("-inf"))
+    vp = vp.index_put((b, cc[:, 0], cc[:, 1], cc[:, 2]), Xt)
+    vol = vp.permute(0, 4, 1, 2, 3)
+    if mode == "max":
+        P = F.max_pool3d(vol, K, stride=2, padding=pad)
+    else:
+        occ = dense_volume(c, np.ones((len(c), 1)), lo, shape)
+        n_win = K ** 3
+        S = F.avg_pool3d(vol, K, stride=2, padding=pad, count_include_pad=True) * n_win
+        P = S if mode == "sum" else S / (F.avg_pool3d(occ, K, stride=2, padding=pad, count_include_pad=True) * n_win)
+    oc = (out[:, 1:] - lo) // 2
+    Pp = P.permute(0, 2, 3, 4, 1)
+    Y = Pp[(torch.from_numpy(out[:, 0].astype(np.int64)),) + tuple(torch.from_numpy(oc[:, d]) for d in range(3))]
+    if grad is None:
+        return Y.detach().numpy(), None
+    (Y * torch.from_numpy(grad)).sum().backward()
+    return Y.detach().numpy(), Xt.grad.numpy()
+
+
+@pytest.mark.parametrize("K", [2, 3])
+@pytest.mark.parametrize("mode", ["max", "avg", "sum"])
+def test_pool_vs_dense(K, mode):
+    c, X, out, maps, lo, shape = _pool_setup(71 + K, K)
+    G, _ = WL.random_features(5, len(out), 4)
+    G = np.asarray(G, np.float64)
+    refY, refdX = _dense_pool(c, X, out, lo, shape, K, mode, grad=G)
+    Y, arg, N = O.pool_forward(X, maps, len(out), mode)
+    assert rel_err(Y, refY) < 1e-12
+    dX = O.pool_backward(G, maps, len(c), mode, arg, N)
+    assert rel_err(dX, refdX) < 1e-12
+    # every output of a strided pool has at least one input; the window sizes bound the count
+    assert N.min() >= 1 and N.max() <= K ** 3
+
+
+def test_global_pool_vs_per_batch_reductions():
+    c = WL.random_coords(73, 500, 3, -5, 6, batch=3)
+    X, _ = WL.random_features(73, len(c), 6)
+    X = np.asarray(X, np.float64)
+    G = np.asarray(WL.random_features(74, 3, 6)[0], np.float64)
+    b = c[:, 0].astype(np.int64)
+    for mode in ("max", "avg", "sum"):
+        Y, arg, N = O.global_pool_forward(X, b, 3, mode)
+        Xt = torch.from_numpy(X).requires_grad_(True)
+        parts = []
+        for i in range(3):
+            rows = Xt[torch.from_numpy(b == i)]
+            parts.append(rows.max(0).values if mode == "max" else (rows.mean(0) if mode == "avg" else rows.sum(0)))
+        ref = torch.stack(parts)
+        (ref * torch.from_numpy(G)).sum().backward()
+        assert rel_err(Y, ref.detach().numpy()) < 1e-12
+        assert np.array_equal(N, np.bincount(b, minlength=3))
+        dX = O.global_pool_backward(G, b, mode, arg, N)
+        assert rel_err(dX, Xt.grad.numpy()) < 1e-12
+
+
+def test_pool_planted_mistakes_are_caught():
+    c, X, out, maps, lo, shape = _pool_setup(75, 3)
+    refY, _ = _dense_pool(c, X, out, lo, shape, 3, "avg")
+    Ysum, _, _ = O.pool_forward(X, maps, len(out), "sum")
+    assert rel_err(Ysum, refY) > 1e-3                        # avg without the division by N
+    refM, _ = _dense_pool(c, X, out, lo, shape, 3, "max")
+    Ydrop, _, _ = O.pool_forward(X, maps[:-1], len(out), "max")
+    assert rel_err(Ydrop, refM) > 1e-6                        # a dropped offset
+    # a flipped offset sign: invisible for the symmetric window {-1,0,1}^3,
+    # caught by the size-2 window {0,1}^3
+    c2, X2, out2, maps2, lo2, shape2 = _pool_setup(76, 2)
+    ref2, _ = _dense_pool(c2, X2, out2, lo2, shape2, 2, "max")
+    flip2 = O.kernel_map(c2, out2, -O.hypercube(2, 3))
+    Yf2, _, _ = O.pool_forward(X2, flip2, len(out2), "max")
+    assert rel_err(Yf2, ref2) > 1e-6
+    # max-pool gradient sent to the last input attaining the maximum instead of
+    # the first: with random features there are no ties, so it must agree; sent
+    # to the first input of the output instead, it must not
+    G = np.asarray(WL.random_features(77, len(out), 4)[0], np.float64)
+    Y, arg, N = O.pool_forward(X, maps, len(out), "max")
+    _, refdX = _dense_pool(c, X, out, lo, shape, 3, "max", grad=G)
+    I, Oo = O.pool_pairs(maps)
+    first = np.full(len(out), -1)
+    for i, j in zip(I.tolist()[::-1], Oo.tolist()[::-1]):
+        first[j] = i
+    bad = np.zeros_like(refdX)
+    for j in range(len(out)):
+        bad[first[j]] += G[j]
+    assert rel_err(bad, refdX) > 1e-3
