@@ -111,6 +111,105 @@ def cpu_baseline(wl, budget_s: float = 30.0):
             "seconds": t, "blas": blas}
 
 
+def pool_bytes(n_pairs, n_out, C, K, mode):
+    """Forward pooling pass: each output's K neighbour entries, one input row
+    per pair, the output row, its argmax row (max) and its count."""
+    return n_out * K * 4 + n_pairs * C * 4 + n_out * C * 4 * (2 if mode == "max" else 1) + n_out * 4
+
+
+def pool_cpu_baseline(mode: str):
+    """The oracle's pooling pass (map, forward, backward) over the same scene
+    (about 12 s of single-threaded Python)."""
+    import numpy as np
+    import oracle.gsc_oracle as O
+    from paper_1904_08755_amd import workloads as WL
+    wl = WL.make_workload(1)
+    t0 = time.perf_counter()
+    out = O.output_coordinates(wl.coords, 2)
+    maps = O.kernel_map(wl.coords, out, O.region("cube", 2, wl.D))
+    X = wl.X.astype(np.float64)
+    Y, arg, N = O.pool_forward(X, maps, len(out), mode)
+    O.pool_backward(np.ones_like(Y), maps, wl.n, mode, arg, N)
+    t = time.perf_counter() - t0
+    return {"value": wl.n / t, "unit": "voxels/s", "cores": 1, "kind": "oracle",
+            "sample": f"one full pooling pass (map, forward, backward) of the scene ({wl.n} voxels), "
+                      f"single-threaded Python; {t:.1f} s", "seconds": t}
+
+
+def run_pool(args):
+    """Pooling pass over workload 1's scene: table, stride-2 output coordinates,
+    the 2^3 window's map and its role-reversed map (dense forms), pooling
+    forward and backward.  One JSON line, like the convolution pass."""
+    import numpy as np
+    import torch
+
+    from paper_1904_08755_amd import gsc, regions
+    from paper_1904_08755_amd import workloads as WL
+
+    wl = WL.make_workload(1)
+    coords = torch.from_numpy(wl.coords).cuda()
+    X = torch.from_numpy(wl.X).cuda()
+    offs = regions.hypercube(2, wl.D)
+    C, K = X.shape[1], len(offs)
+
+    def one(mark):
+        table = gsc.gsc_coords_build(coords, sync=False)
+        out, out_table = gsc.gsc_coords_stride(coords, 2)
+        fmap = gsc.gsc_kernel_map(table, out, offs, dense=True)
+        tmap = gsc.transposed_kernel_map(out_table, coords, offs, dense=True)
+        mark("map")
+        p = gsc.gsc_sparse_pool_fwd(X, fmap, args.pool)
+        mark("fwd")
+        dX = gsc.gsc_sparse_pool_bwd(p.Y, tmap, args.pool, p)
+        mark("bwd")
+        return fmap, p, dX
+
+    for _ in range(args.warmup):
+        one(lambda name: None)
+    torch.cuda.synchronize()
+    evs = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ev = []
+
+        def mark(name, ev=ev):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            ev.append((name, e))
+
+        mark("start")
+        fmap, p, dX = one(mark)
+        evs.append(ev)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    ms = {k: [] for k in ("map", "fwd", "bwd")}
+    for ev in evs:
+        d = dict(ev)
+        ms["map"].append(d["start"].elapsed_time(d["map"]))
+        ms["fwd"].append(d["map"].elapsed_time(d["fwd"]))
+        ms["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
+    ms = {k: float(np.mean(v)) for k, v in ms.items()}
+    n_pairs, n_out = fmap.count(), fmap.n_out
+    nbytes = pool_bytes(n_pairs, n_out, C, K, args.pool)
+    ach = nbytes / (ms["fwd"] * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_pool_fwd",
+            "bytes_per_launch": int(nbytes), "avg_launch_us": round(ms["fwd"] * 1e3, 2)}
+    cpu = None if args.no_cpu_baseline else pool_cpu_baseline(args.pool)
+    out = {
+        "metric": f"sparse {args.pool}-pool fwd+bwd voxels/s", "value": round(wl.n / sec, 1), "unit": "voxels/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{wl.name}_{args.pool}pool2_s2", "voxels": wl.n, "pooled_rows": n_out,
+                   "map_pairs": n_pairs, "channels": C, "parallelism": "single GPU"},
+        "pool_fwd_bwd_voxels_per_s": round(wl.n / ((ms["fwd"] + ms["bwd"]) * 1e-3), 1),
+        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,6 +218,8 @@ def main():
     ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
+    ap.add_argument("--pool", choices=["max", "avg", "sum"], default=None,
+                    help="time pooling instead (Sec. 4.3, 4.4): the 2^3 stride-2 window over the scene of workload 1")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB once (a copy of known size for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -137,6 +238,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     gsc.lib()
+    if args.pool:
+        return run_pool(args)
     t = time.perf_counter()
     wl = WL.make_workload(args.workload)
     log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")

@@ -19,6 +19,9 @@
  *                        run on the role-reversed kernel map)
  *   gsc_sparse_conv_bwd  gradients of Alg. 2 with respect to the input
  *                        features and the weights (chain rule of Eq. 3)
+ *   gsc_sparse_pool_*    max / average / sum pooling over a kernel map and
+ *   gsc_global_pool_*    global pooling, with their gradients (Sec. 4.3,
+ *                        Alg. 3; Sec. 4.4, Alg. 4)
  *
  * Conventions
  *   - A coordinate row is (b, x_1, ..., x_D) of int32, batch index first;
@@ -275,6 +278,54 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                         const int32_t* t_perm, const uint32_t* t_bmask, const int64_t* t_ibase,
                         const int32_t* t_items,
                         void* dX, float* dW, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Pooling over a kernel map (Sec. 4.3 max pooling, Alg. 3; Sec. 4.4         */
+/* average and sum pooling, Alg. 4) and global pooling.  float32.            */
+/* ------------------------------------------------------------------------ */
+typedef enum { GSC_POOL_MAX = 0, GSC_POOL_AVG = 1, GSC_POOL_SUM = 2 } gsc_pool_mode;
+
+/* Y[j] (n_out x C, overwritten) = the channel-wise maximum (MAX), mean (AVG)
+ * or sum (SUM) of the input rows X[i] (n_in x C) paired with output row j in
+ * the kernel map whose dense form is nbr (K x n_out int32, nbr[k*n_out + j]
+ * = input row or -1, as gsc_kernel_map writes it; a pooling layer's map is
+ * the kernel map of its window from the input table to its output
+ * coordinates, e.g. gsc_coords_stride's).  An output without inputs is 0.
+ * arg (n_out x C int32; required for MAX, else nullable): the input row
+ * attaining the maximum, the first in offset order on ties (-1: none).  cnt
+ * (n_out int32, nullable): the number of inputs of each output (Alg. 4's N).
+ * Asynchronous.  Errors: EINVAL, EHIP. */
+int gsc_sparse_pool_fwd(int32_t mode, const float* X, int64_t n_in, int32_t C,
+                        const int32_t* nbr, int32_t K, int64_t n_out,
+                        float* Y, int32_t* arg, int32_t* cnt, void* stream);
+
+/* dX (n_in x C, overwritten) = gradient of gsc_sparse_pool_fwd: each input row
+ * i receives, for every output j it is paired with, dY[j] (SUM), dY[j] /
+ * cnt[j] (AVG), or dY[j][c] in the channels c where arg[j][c] == i (MAX).
+ * nbrT (K x n_in int32) is the dense form of the role-reversed map
+ * (gsc_kernel_map on the output table with the input coordinates and the
+ * negated offsets): nbrT[k*n_in + i] = the output fed by input i at offset
+ * k, or -1.  arg is required for MAX, cnt for AVG.  The sum over outputs
+ * runs in offset order (deterministic, no atomics).  Asynchronous.
+ * Errors: EINVAL, EHIP. */
+int gsc_sparse_pool_bwd(int32_t mode, const float* dY, int64_t n_out, int32_t C,
+                        const int32_t* nbrT, int32_t K, int64_t n_in,
+                        const int32_t* arg, const int32_t* cnt, float* dX, void* stream);
+
+/* Global pooling (Sec. 4.4): every row of batch index b (column 0 of coords,
+ * n x (1+D) int32) maps to output row b < n_batch <= 32; rows with a batch
+ * index outside [0, n_batch) are ignored.  Y (n_batch x C), arg (n_batch x
+ * C, required for MAX: the first row attaining the maximum) and cnt
+ * (n_batch, nullable) as in gsc_sparse_pool_fwd.  ws:
+ * gsc_global_pool_ws_bytes(n, C, n_batch) bytes of device memory (partial
+ * reductions; contents not kept).  Asynchronous.  Errors: EINVAL, ESHORT, EHIP. */
+size_t gsc_global_pool_ws_bytes(int64_t n, int32_t C, int32_t n_batch);
+int gsc_global_pool_fwd(int32_t mode, const float* X, int64_t n, int32_t C, const int32_t* coords, int32_t D,
+                        int32_t n_batch, float* Y, int32_t* arg, int32_t* cnt, void* ws, size_t ws_bytes,
+                        void* stream);
+/* dX (n x C, overwritten) = gradient of gsc_global_pool_fwd. */
+int gsc_global_pool_bwd(int32_t mode, const float* dY, int32_t n_batch, int32_t C, const int32_t* coords, int32_t D,
+                        int64_t n, const int32_t* arg, const int32_t* cnt, float* dX, void* stream);
 
 #ifdef __cplusplus
 }

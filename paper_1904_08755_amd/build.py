@@ -19,7 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgsc.so")
-SOURCES = ["common.hip", "coords.hip", "kmap.hip", "plan.hip", "conv.hip", "conv_bf16.hip", "conv_blk.hip"]
+SOURCES = ["common.hip", "coords.hip", "kmap.hip", "plan.hip", "conv.hip", "conv_bf16.hip", "conv_blk.hip",
+           "pool.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

@@ -62,7 +62,15 @@ _SIGS = {
     "gsc_sparse_conv_bwd": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp,
                                            _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp,
                                            _sz, _vp]),
+    "gsc_sparse_pool_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i64, _vp, _vp, _vp, _vp]),
+    "gsc_sparse_pool_bwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i64, _vp, _vp, _vp, _vp]),
+    "gsc_global_pool_ws_bytes": (_sz, [_i64, _i32, _i32]),
+    "gsc_global_pool_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gsc_global_pool_bwd": (ctypes.c_int, [_i32, _vp, _i32, _i32, _vp, _i32, _i64, _vp, _vp, _vp, _vp]),
 }
+
+GSC_POOL_MAX, GSC_POOL_AVG, GSC_POOL_SUM = 0, 1, 2
+POOL_MODES = {"max": GSC_POOL_MAX, "avg": GSC_POOL_AVG, "sum": GSC_POOL_SUM}
 
 _lib = None
 
@@ -392,3 +400,68 @@ def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap
         _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
         _ptr(ws) if need_dw else None, ws.numel() if need_dw else 0, _stream(stream)))
     return (dX if need_dx else None), (dW if need_dw else None)
+
+
+# --------------------------------------------------------------------------- #
+# pooling (Sec. 4.3, 4.4)
+# --------------------------------------------------------------------------- #
+@dataclasses.dataclass
+class Pooled:
+    Y: torch.Tensor                  # float32 [n_out, C]
+    arg: Optional[torch.Tensor]      # int32 [n_out, C]: input row of the maximum (max pooling)
+    cnt: torch.Tensor                # int32 [n_out]: inputs per output
+
+
+def gsc_sparse_pool_fwd(X: torch.Tensor, kmap: KernelMap, mode: str, stream=None) -> Pooled:
+    """Pooling of ``X`` over a kernel map built with ``dense=True``."""
+    _need(X, torch.float32, "X", 2)
+    if kmap.nbr is None:
+        raise ValueError("pooling needs the map's dense form (gsc_kernel_map(..., dense=True))")
+    m = POOL_MODES[mode]
+    n_out, C = kmap.n_out, X.shape[1]
+    Y = torch.empty((n_out, C), dtype=torch.float32, device=X.device)
+    arg = torch.empty((n_out, C), dtype=torch.int32, device=X.device) if m == GSC_POOL_MAX else None
+    cnt = torch.empty((n_out,), dtype=torch.int32, device=X.device)
+    _check(lib().gsc_sparse_pool_fwd(m, _ptr(X), X.shape[0], C, _ptr(kmap.nbr), kmap.K, n_out, _ptr(Y), _ptr(arg),
+                                     _ptr(cnt), _stream(stream)))
+    return Pooled(Y, arg, cnt)
+
+
+def gsc_sparse_pool_bwd(dY: torch.Tensor, tmap: KernelMap, mode: str, pooled: Pooled, stream=None) -> torch.Tensor:
+    """Input gradient of gsc_sparse_pool_fwd; ``tmap`` is the role-reversed map
+    (dense form over the input rows)."""
+    _need(dY, torch.float32, "dY", 2)
+    if tmap.nbr is None:
+        raise ValueError("the pooling gradient needs the role-reversed map's dense form")
+    m = POOL_MODES[mode]
+    n_in, C = tmap.n_out, dY.shape[1]
+    dX = torch.empty((n_in, C), dtype=torch.float32, device=dY.device)
+    _check(lib().gsc_sparse_pool_bwd(m, _ptr(dY), dY.shape[0], C, _ptr(tmap.nbr), tmap.K, n_in, _ptr(pooled.arg),
+                                     _ptr(pooled.cnt), _ptr(dX), _stream(stream)))
+    return dX
+
+
+def gsc_global_pool_fwd(X: torch.Tensor, coords: torch.Tensor, n_batch: int, mode: str, stream=None) -> Pooled:
+    """Global pooling: one output row per batch index (column 0 of ``coords``)."""
+    _need(X, torch.float32, "X", 2)
+    _need(coords, torch.int32, "coords", 2)
+    m = POOL_MODES[mode]
+    n, C = X.shape
+    D = coords.shape[1] - 1
+    Y = torch.empty((n_batch, C), dtype=torch.float32, device=X.device)
+    arg = torch.empty((n_batch, C), dtype=torch.int32, device=X.device) if m == GSC_POOL_MAX else None
+    cnt = torch.empty((n_batch,), dtype=torch.int32, device=X.device)
+    ws = _ws(lib().gsc_global_pool_ws_bytes(n, C, n_batch), X.device)
+    _check(lib().gsc_global_pool_fwd(m, _ptr(X), n, C, _ptr(coords), D, n_batch, _ptr(Y), _ptr(arg), _ptr(cnt),
+                                     _ptr(ws), ws.numel(), _stream(stream)))
+    return Pooled(Y, arg, cnt)
+
+
+def gsc_global_pool_bwd(dY: torch.Tensor, coords: torch.Tensor, mode: str, pooled: Pooled, stream=None) -> torch.Tensor:
+    _need(dY, torch.float32, "dY", 2)
+    m = POOL_MODES[mode]
+    n, C = coords.shape[0], dY.shape[1]
+    dX = torch.empty((n, C), dtype=torch.float32, device=dY.device)
+    _check(lib().gsc_global_pool_bwd(m, _ptr(dY), dY.shape[0], C, _ptr(coords), coords.shape[1] - 1, n,
+                                     _ptr(pooled.arg), _ptr(pooled.cnt), _ptr(dX), _stream(stream)))
+    return dX

@@ -495,3 +495,66 @@ def test_async_build_reports_duplicate_later():
     with pytest.raises(gsc.GscError) as e:
         gsc.gsc_table_status(table)
     assert e.value.code == gsc.GSC_EDUP
+
+
+# --------------------------------------------------------------------------- #
+# pooling (Sec. 4.3, Alg. 3; Sec. 4.4, Alg. 4)
+# --------------------------------------------------------------------------- #
+def _pool_case(seed, scale, window, extra_outputs=0):
+    """A scene, its stride-2 output coordinates (plus ``extra_outputs`` far
+    away rows that no input reaches), the pooling maps on the GPU (forward
+    and role-reversed, dense forms) and the oracle's map."""
+    wl = WL.make_workload(1, scale=scale)
+    coords = torch.from_numpy(wl.coords).to(DEV)
+    table = gsc.gsc_coords_build(coords)
+    out, out_table = gsc.gsc_coords_stride(coords, 2)
+    if extra_outputs:
+        far = out[:extra_outputs].clone()
+        far[:, 1] += 10_000
+        out = torch.cat([out, far]).contiguous()
+        out_table = gsc.gsc_coords_build(out)
+    offs = regions.hypercube(window, 3)
+    fmap = gsc.gsc_kernel_map(table, out, offs, dense=True)
+    tmap = gsc.transposed_kernel_map(out_table, coords, offs, dense=True)
+    X, _ = WL.random_features(seed, wl.n, 32)
+    G, _ = WL.random_features(seed + 1, out.shape[0], 32)
+    ref_maps = O.kernel_map(wl.coords, to_np(out), np.asarray(offs))
+    return wl, coords, out, fmap, tmap, X, G, ref_maps
+
+
+@pytest.mark.parametrize("window", [2, 3])
+@pytest.mark.parametrize("mode", ["max", "avg", "sum"])
+def test_pool_parity(mode, window):
+    wl, coords, out, fmap, tmap, X, G, ref_maps = _pool_case(81 + window, 0.3, window, extra_outputs=5)
+    n_out = out.shape[0]
+    _say(f"[gpu] pool {mode} window {window}: n_in={wl.n} n_out={n_out}")
+    Xd = torch.from_numpy(X).to(DEV)
+    p = gsc.gsc_sparse_pool_fwd(Xd, fmap, mode)
+    dX = gsc.gsc_sparse_pool_bwd(torch.from_numpy(G).to(DEV), tmap, mode, p)
+    torch.cuda.synchronize()
+    Y, arg, N = O.pool_forward(X, ref_maps, n_out, mode)
+    assert np.array_equal(to_np(p.cnt), N)
+    assert N[-5:].max() == 0 and np.all(to_np(p.Y)[-5:] == 0)      # outputs no input reaches
+    assert rel_err(to_np(p.Y), Y) <= TOL["f32"]
+    if mode == "max":
+        assert np.array_equal(to_np(p.arg), arg)                   # the same input wins, bit for bit
+        assert np.all(to_np(p.Y) == X[np.maximum(arg, 0), np.arange(32)[None, :]] * (arg >= 0))
+    ref_dX = O.pool_backward(G, ref_maps, wl.n, mode, arg, N)
+    assert rel_err(to_np(dX), ref_dX) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("mode", ["max", "avg", "sum"])
+def test_global_pool_parity(mode):
+    c = WL.random_coords(91, 3000, 3, -20, 21, batch=3)
+    X, _ = WL.random_features(91, len(c), 40)
+    G, _ = WL.random_features(92, 3, 40)
+    cd = torch.from_numpy(c).to(DEV)
+    p = gsc.gsc_global_pool_fwd(torch.from_numpy(X).to(DEV), cd, 3, mode)
+    dX = gsc.gsc_global_pool_bwd(torch.from_numpy(G).to(DEV), cd, mode, p)
+    torch.cuda.synchronize()
+    Y, arg, N = O.global_pool_forward(X, c[:, 0], 3, mode)
+    assert np.array_equal(to_np(p.cnt), N)
+    assert rel_err(to_np(p.Y), Y) <= TOL["f32"]
+    if mode == "max":
+        assert np.array_equal(to_np(p.arg), arg)
+    assert rel_err(to_np(dX), O.global_pool_backward(G, c[:, 0], mode, arg, N)) <= TOL["f32"]
