@@ -7,7 +7,8 @@
 // -1, as the kernel map writes it) already lists every output's inputs in
 // offset order, so the forward pass is output-stationary with no sort: one
 // lane per (output row, channel), consecutive lanes on consecutive channels
-// of a row (coalesced feature rows, the row's neighbour entries shared).  The
+// of a row (coalesced feature rows, the row's neighbour entries shared; four
+// channels per lane when C is a multiple of 4).  The
 // backward pass is input-stationary over the role-reversed map's dense form,
 // so every input gradient is a sum in a fixed order (no atomics).
 //
@@ -75,6 +76,57 @@ __global__ void __launch_bounds__(kPoolThreads) k_pool_fwd(int mode, const float
     Y[t] = acc;
     if (arg) arg[t] = best;
     if (cnt && c == 0) cnt[j] = n;
+}
+
+// The same with four channels per lane (C a multiple of 4, 16-byte aligned
+// rows): one float4 gather per (output, offset), so a 32-channel row takes 8
+// lanes and a wave covers 8 outputs.
+__global__ void __launch_bounds__(kPoolThreads) k_pool_fwd4(int mode, const float* __restrict__ X, int64_t n_in, int C,
+                                                            const int32_t* __restrict__ nbr, int K, int64_t n_out,
+                                                            float* __restrict__ Y, int32_t* __restrict__ arg,
+                                                            int32_t* __restrict__ cnt) {
+    const int nq = C >> 2;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n_out * nq) return;
+    const int64_t j = t / nq;
+    const int q = (int)(t - j * nq);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int4 best = make_int4(-1, -1, -1, -1);
+    int32_t n = 0;
+    for (int k0 = 0; k0 < K; k0 += kPoolBatch) {
+        int32_t r[kPoolBatch];
+        float4 v[kPoolBatch];
+#pragma unroll
+        for (int b = 0; b < kPoolBatch; ++b) r[b] = k0 + b < K ? nbr[(int64_t)(k0 + b) * n_out + j] : -1;
+#pragma unroll
+        for (int b = 0; b < kPoolBatch; ++b) {
+            const bool ok = r[b] >= 0 && r[b] < n_in;
+            v[b] = ok ? reinterpret_cast<const float4*>(X + (int64_t)r[b] * C)[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int b = 0; b < kPoolBatch; ++b) {
+            if (!(r[b] >= 0 && r[b] < n_in)) continue;
+            ++n;
+            if (mode == GSC_POOL_MAX) {
+                if (best.x < 0 || v[b].x > acc.x) { acc.x = v[b].x; best.x = r[b]; }
+                if (best.y < 0 || v[b].y > acc.y) { acc.y = v[b].y; best.y = r[b]; }
+                if (best.z < 0 || v[b].z > acc.z) { acc.z = v[b].z; best.z = r[b]; }
+                if (best.w < 0 || v[b].w > acc.w) { acc.w = v[b].w; best.w = r[b]; }
+            } else {
+                acc.x += v[b].x;
+                acc.y += v[b].y;
+                acc.z += v[b].z;
+                acc.w += v[b].w;
+            }
+        }
+    }
+    if (mode == GSC_POOL_AVG && n > 0) {
+        const float fn = (float)n;
+        acc = make_float4(acc.x / fn, acc.y / fn, acc.z / fn, acc.w / fn);
+    }
+    reinterpret_cast<float4*>(Y)[t] = acc;
+    if (arg) reinterpret_cast<int4*>(arg)[t] = best;
+    if (cnt && q == 0) cnt[j] = n;
 }
 
 // Backward: lane (i, c); nbrT[k][i] = the output that input i feeds at offset k.
@@ -217,6 +269,55 @@ __global__ void __launch_bounds__(kPoolThreads) k_gpool_bwd(int mode, const floa
     dX[t] = g;
 }
 
+// Backward with four channels per lane.
+__global__ void __launch_bounds__(kPoolThreads) k_pool_bwd4(int mode, const float* __restrict__ dY, int64_t n_out,
+                                                            int C, const int32_t* __restrict__ nbrT, int K,
+                                                            int64_t n_in, const int32_t* __restrict__ arg,
+                                                            const int32_t* __restrict__ cnt, float* __restrict__ dX) {
+    const int nq = C >> 2;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n_in * nq) return;
+    const int64_t i = t / nq;
+    const int q = (int)(t - i * nq);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k0 = 0; k0 < K; k0 += kPoolBatch) {
+        int32_t o[kPoolBatch];
+#pragma unroll
+        for (int b = 0; b < kPoolBatch; ++b) o[b] = k0 + b < K ? nbrT[(int64_t)(k0 + b) * n_in + i] : -1;
+#pragma unroll
+        for (int b = 0; b < kPoolBatch; ++b) {
+            if (!(o[b] >= 0 && o[b] < n_out)) continue;
+            const int64_t e = (int64_t)o[b] * nq + q;
+            const float4 g = reinterpret_cast<const float4*>(dY)[e];
+            if (mode == GSC_POOL_MAX) {
+                const int4 a = reinterpret_cast<const int4*>(arg)[e];
+                const int32_t ii = (int32_t)i;
+                acc.x += a.x == ii ? g.x : 0.f;
+                acc.y += a.y == ii ? g.y : 0.f;
+                acc.z += a.z == ii ? g.z : 0.f;
+                acc.w += a.w == ii ? g.w : 0.f;
+            } else if (mode == GSC_POOL_AVG) {
+                const int32_t n = cnt[o[b]];
+                if (n > 0) {
+                    const float fn = (float)n;
+                    acc.x += g.x / fn;
+                    acc.y += g.y / fn;
+                    acc.z += g.z / fn;
+                    acc.w += g.w / fn;
+                }
+            } else {
+                acc.x += g.x;
+                acc.y += g.y;
+                acc.z += g.z;
+                acc.w += g.w;
+            }
+        }
+    }
+    reinterpret_cast<float4*>(dX)[t] = acc;
+}
+
+static bool aligned16(const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; }
+
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 static bool mode_ok(int mode) { return mode == GSC_POOL_MAX || mode == GSC_POOL_AVG || mode == GSC_POOL_SUM; }
@@ -237,8 +338,12 @@ int gsc_sparse_pool_fwd(int32_t mode, const float* X, int64_t n_in, int32_t C, c
     if (!nbr || !Y || (n_in > 0 && !X)) return fail(GSC_EINVAL, "pool_fwd: null X/nbr/Y");
     if (mode == GSC_POOL_MAX && !arg) return fail(GSC_EINVAL, "pool_fwd: max pooling needs arg");
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    hipLaunchKernelGGL(k_pool_fwd, dim3(blocks_for(n_out * C)), dim3(kPoolThreads), 0, s, (int)mode, X, n_in, (int)C,
-                       nbr, (int)K, n_out, Y, arg, cnt);
+    if (C % 4 == 0 && aligned16(X) && aligned16(Y) && aligned16(arg))
+        hipLaunchKernelGGL(k_pool_fwd4, dim3(blocks_for(n_out * (C / 4))), dim3(kPoolThreads), 0, s, (int)mode, X,
+                           n_in, (int)C, nbr, (int)K, n_out, Y, arg, cnt);
+    else
+        hipLaunchKernelGGL(k_pool_fwd, dim3(blocks_for(n_out * C)), dim3(kPoolThreads), 0, s, (int)mode, X, n_in,
+                           (int)C, nbr, (int)K, n_out, Y, arg, cnt);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
@@ -253,8 +358,12 @@ int gsc_sparse_pool_bwd(int32_t mode, const float* dY, int64_t n_out, int32_t C,
     if (mode == GSC_POOL_MAX && !arg) return fail(GSC_EINVAL, "pool_bwd: max pooling needs arg");
     if (mode == GSC_POOL_AVG && !cnt) return fail(GSC_EINVAL, "pool_bwd: average pooling needs cnt");
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    hipLaunchKernelGGL(k_pool_bwd, dim3(blocks_for(n_in * C)), dim3(kPoolThreads), 0, s, (int)mode, dY, n_out, (int)C,
-                       nbrT, (int)K, n_in, arg, cnt, dX);
+    if (C % 4 == 0 && aligned16(dY) && aligned16(dX) && aligned16(arg))
+        hipLaunchKernelGGL(k_pool_bwd4, dim3(blocks_for(n_in * (C / 4))), dim3(kPoolThreads), 0, s, (int)mode, dY,
+                           n_out, (int)C, nbrT, (int)K, n_in, arg, cnt, dX);
+    else
+        hipLaunchKernelGGL(k_pool_bwd, dim3(blocks_for(n_in * C)), dim3(kPoolThreads), 0, s, (int)mode, dY, n_out,
+                           (int)C, nbrT, (int)K, n_in, arg, cnt, dX);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }

@@ -500,7 +500,7 @@ def test_async_build_reports_duplicate_later():
 # --------------------------------------------------------------------------- #
 # pooling (Sec. 4.3, Alg. 3; Sec. 4.4, Alg. 4)
 # --------------------------------------------------------------------------- #
-def _pool_case(seed, scale, window, extra_outputs=0):
+def _pool_case(seed, scale, window, extra_outputs=0, C=32):
     """A scene, its stride-2 output coordinates (plus ``extra_outputs`` far
     away rows that no input reaches), the pooling maps on the GPU (forward
     and role-reversed, dense forms) and the oracle's map."""
@@ -516,18 +516,19 @@ def _pool_case(seed, scale, window, extra_outputs=0):
     offs = regions.hypercube(window, 3)
     fmap = gsc.gsc_kernel_map(table, out, offs, dense=True)
     tmap = gsc.transposed_kernel_map(out_table, coords, offs, dense=True)
-    X, _ = WL.random_features(seed, wl.n, 32)
-    G, _ = WL.random_features(seed + 1, out.shape[0], 32)
+    X, _ = WL.random_features(seed, wl.n, C)
+    G, _ = WL.random_features(seed + 1, out.shape[0], C)
     ref_maps = O.kernel_map(wl.coords, to_np(out), np.asarray(offs))
     return wl, coords, out, fmap, tmap, X, G, ref_maps
 
 
-@pytest.mark.parametrize("window", [2, 3])
+@pytest.mark.parametrize("window,C", [(2, 32), (3, 32), (3, 6)])
 @pytest.mark.parametrize("mode", ["max", "avg", "sum"])
-def test_pool_parity(mode, window):
-    wl, coords, out, fmap, tmap, X, G, ref_maps = _pool_case(81 + window, 0.3, window, extra_outputs=5)
+def test_pool_parity(mode, window, C):
+    """Four channels per lane (C = 32) and one (C = 6)."""
+    wl, coords, out, fmap, tmap, X, G, ref_maps = _pool_case(81 + window, 0.3, window, extra_outputs=5, C=C)
     n_out = out.shape[0]
-    _say(f"[gpu] pool {mode} window {window}: n_in={wl.n} n_out={n_out}")
+    _say(f"[gpu] pool {mode} window {window} C {C}: n_in={wl.n} n_out={n_out}")
     Xd = torch.from_numpy(X).to(DEV)
     p = gsc.gsc_sparse_pool_fwd(Xd, fmap, mode)
     dX = gsc.gsc_sparse_pool_bwd(torch.from_numpy(G).to(DEV), tmap, mode, p)
@@ -538,7 +539,7 @@ def test_pool_parity(mode, window):
     assert rel_err(to_np(p.Y), Y) <= TOL["f32"]
     if mode == "max":
         assert np.array_equal(to_np(p.arg), arg)                   # the same input wins, bit for bit
-        assert np.all(to_np(p.Y) == X[np.maximum(arg, 0), np.arange(32)[None, :]] * (arg >= 0))
+        assert np.all(to_np(p.Y) == X[np.maximum(arg, 0), np.arange(C)[None, :]] * (arg >= 0))
     ref_dX = O.pool_backward(G, ref_maps, wl.n, mode, arg, N)
     assert rel_err(to_np(dX), ref_dX) <= TOL["f32"]
 
