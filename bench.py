@@ -151,18 +151,29 @@ def run_pool(args):
     X = torch.from_numpy(wl.X).cuda()
     offs = regions.hypercube(2, wl.D)
     C, K = X.shape[1], len(offs)
+    n = wl.n
+    # every buffer allocated once (output rows <= input rows)
+    table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device="cuda")
+    out_table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device="cuda")
+    fb = gsc.MapBuffers(n, K, wl.D, "cuda", dense=True)
+    tb = gsc.MapBuffers(n, K, wl.D, "cuda", dense=True)
+    host_offs, host_neg = gsc._host_i32(offs), gsc._host_i32(-offs)
+    pooled = gsc.Pooled(torch.empty((n, C), dtype=torch.float32, device="cuda"),
+                        torch.empty((n, C), dtype=torch.int32, device="cuda"),
+                        torch.empty((n,), dtype=torch.int32, device="cuda"))
+    dX = torch.empty((n, C), dtype=torch.float32, device="cuda")
 
     def one(mark):
-        table = gsc.gsc_coords_build(coords, sync=False)
-        out, out_table = gsc.gsc_coords_stride(coords, 2)
-        fmap = gsc.gsc_kernel_map(table, out, offs, dense=True)
-        tmap = gsc.transposed_kernel_map(out_table, coords, offs, dense=True)
+        gsc.gsc_coords_build(coords, table, sync=False)
+        out, _ = gsc.gsc_coords_stride(coords, 2, out_table=out_table)
+        fmap = gsc.gsc_kernel_map(table, out, offs, sync=False, bufs=fb, host_offsets=host_offs, dense=True)
+        tmap = gsc.gsc_kernel_map(out_table, coords, -offs, sync=False, bufs=tb, host_offsets=host_neg, dense=True)
         mark("map")
-        p = gsc.gsc_sparse_pool_fwd(X, fmap, args.pool)
+        p = gsc.gsc_sparse_pool_fwd(X, fmap, args.pool, out=pooled)
         mark("fwd")
-        dX = gsc.gsc_sparse_pool_bwd(p.Y, tmap, args.pool, p)
+        g = gsc.gsc_sparse_pool_bwd(p.Y, tmap, args.pool, p, dX=dX)
         mark("bwd")
-        return fmap, p, dX
+        return fmap, p, g
 
     for _ in range(args.warmup):
         one(lambda name: None)

@@ -412,22 +412,29 @@ class Pooled:
     cnt: torch.Tensor                # int32 [n_out]: inputs per output
 
 
-def gsc_sparse_pool_fwd(X: torch.Tensor, kmap: KernelMap, mode: str, stream=None) -> Pooled:
-    """Pooling of ``X`` over a kernel map built with ``dense=True``."""
+def gsc_sparse_pool_fwd(X: torch.Tensor, kmap: KernelMap, mode: str, stream=None,
+                        out: Optional[Pooled] = None) -> Pooled:
+    """Pooling of ``X`` over a kernel map built with ``dense=True``; ``out``
+    (optional) holds preallocated output buffers."""
     _need(X, torch.float32, "X", 2)
     if kmap.nbr is None:
         raise ValueError("pooling needs the map's dense form (gsc_kernel_map(..., dense=True))")
     m = POOL_MODES[mode]
     n_out, C = kmap.n_out, X.shape[1]
-    Y = torch.empty((n_out, C), dtype=torch.float32, device=X.device)
-    arg = torch.empty((n_out, C), dtype=torch.int32, device=X.device) if m == GSC_POOL_MAX else None
-    cnt = torch.empty((n_out,), dtype=torch.int32, device=X.device)
+    if out is None:
+        out = Pooled(torch.empty((n_out, C), dtype=torch.float32, device=X.device),
+                     torch.empty((n_out, C), dtype=torch.int32, device=X.device) if m == GSC_POOL_MAX else None,
+                     torch.empty((n_out,), dtype=torch.int32, device=X.device))
+    Y, arg, cnt = out.Y[:n_out], (out.arg[:n_out] if out.arg is not None else None), out.cnt[:n_out]
+    if m == GSC_POOL_MAX and arg is None:
+        raise ValueError("max pooling needs an arg buffer")
     _check(lib().gsc_sparse_pool_fwd(m, _ptr(X), X.shape[0], C, _ptr(kmap.nbr), kmap.K, n_out, _ptr(Y), _ptr(arg),
                                      _ptr(cnt), _stream(stream)))
     return Pooled(Y, arg, cnt)
 
 
-def gsc_sparse_pool_bwd(dY: torch.Tensor, tmap: KernelMap, mode: str, pooled: Pooled, stream=None) -> torch.Tensor:
+def gsc_sparse_pool_bwd(dY: torch.Tensor, tmap: KernelMap, mode: str, pooled: Pooled, stream=None,
+                        dX: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Input gradient of gsc_sparse_pool_fwd; ``tmap`` is the role-reversed map
     (dense form over the input rows)."""
     _need(dY, torch.float32, "dY", 2)
@@ -435,7 +442,8 @@ def gsc_sparse_pool_bwd(dY: torch.Tensor, tmap: KernelMap, mode: str, pooled: Po
         raise ValueError("the pooling gradient needs the role-reversed map's dense form")
     m = POOL_MODES[mode]
     n_in, C = tmap.n_out, dY.shape[1]
-    dX = torch.empty((n_in, C), dtype=torch.float32, device=dY.device)
+    if dX is None:
+        dX = torch.empty((n_in, C), dtype=torch.float32, device=dY.device)
     _check(lib().gsc_sparse_pool_bwd(m, _ptr(dY), dY.shape[0], C, _ptr(tmap.nbr), tmap.K, n_in, _ptr(pooled.arg),
                                      _ptr(pooled.cnt), _ptr(dX), _stream(stream)))
     return dX
