@@ -18,8 +18,9 @@ Conventions (readings of the paper, listed with the others in the design notes):
 Parity status: every function is pinned by the CPU tests (brute-force maps,
 closed-form counts, dense-convolution special cases, adjoint identities, finite
 differences, dense max/average pooling and their gradients, per-batch
-reductions); the row order of ``output_coordinates`` is an implementation
-choice and is compared canonically, not pinned.
+reductions, a hand-written quantization example and np.unique); the row order
+of ``output_coordinates`` is an implementation choice and is compared
+canonically, not pinned.
 """
 from __future__ import annotations
 
@@ -235,6 +236,45 @@ def conv_dx_rows(dY: np.ndarray, W: np.ndarray, out_map: Dict[tuple, int], in_co
 
 def map_pair_count(maps: List[Pairs]) -> int:
     return int(sum(len(I) for I, _ in maps))
+
+
+# --------------------------------------------------------------------------- #
+# Sparse tensor quantization (Sec. 4.1, Alg. 1)
+# --------------------------------------------------------------------------- #
+def quantize(points: np.ndarray, batch: np.ndarray, voxel, labels=None, ignore_label: int = -100):
+    """Alg. 1 in the paper's order.  C' = floor(C / v) per spatial axis, in
+    float32 (the precision the GPU path divides in, so both take the same
+    floor); the keys are the coordinate rows (batch index first); the pairs
+    (i, l) are sorted by key, stably, so within a key the points keep their
+    order; UniqueByKey keeps the first point of every run of equal (key,
+    label); ReduceByKey merges the runs of one key with f, which turns any
+    second run into IGNORE_LABEL and keeps the first point.  Returns the
+    voxel coordinates (n_out x (1+D) int64, in key order), the representative
+    point of each voxel, its label (None without labels) and, for every
+    point, the row of its voxel."""
+    P = np.asarray(points, dtype=np.float32)
+    N, D = P.shape
+    v = np.broadcast_to(np.asarray(voxel, dtype=np.float32), (D,))
+    Cq = np.floor(P / v[None, :]).astype(np.int64)                  # C'_p (float32 quotient, then floor)
+    keys = [(int(b),) + tuple(int(x) for x in row) for b, row in zip(np.asarray(batch).tolist(), Cq)]
+    lab = [0] * N if labels is None else [int(x) for x in np.asarray(labels).tolist()]
+    order = sorted(range(N), key=lambda i: keys[i])                   # SortByKey (stable)
+    runs = []                                                         # UniqueByKey on (key, label)
+    for i in order:
+        if not runs or runs[-1][0] != keys[i] or runs[-1][1] != lab[i]:
+            runs.append((keys[i], lab[i], i))
+    vox, rep, out_lab = [], [], []                                    # ReduceByKey with f
+    for key, l, i in runs:
+        if vox and vox[-1] == key:
+            out_lab[-1] = ignore_label
+        else:
+            vox.append(key)
+            rep.append(i)
+            out_lab.append(l)
+    row_of = {k: r for r, k in enumerate(vox)}
+    inverse = np.array([row_of[k] for k in keys], dtype=np.int64)
+    return (np.array(vox, dtype=np.int64).reshape(-1, D + 1), np.array(rep, dtype=np.int64),
+            None if labels is None else np.array(out_lab, dtype=np.int64), inverse)
 
 
 # --------------------------------------------------------------------------- #

@@ -420,6 +420,45 @@ def test_4d_hybrid_and_tesseract():
     _conv_case(coords, 8, 8, regions.hypercube(3, 4), 78)
 
 
+def test_dilated_kernel():
+    """Dilation (Sec. 3.1: the offset set is arbitrary): the 3^3 cube with
+    offsets scaled by 2 and by 3."""
+    coords = WL.random_coords(85, 3000, 3, -12, 12, batch=2)
+    _conv_case(coords, 8, 16, regions.hypercube(3, 3) * 2, 85)
+    _conv_case(coords, 16, 8, regions.hypercube(3, 3) * 3, 86)
+
+
+def test_arbitrary_output_coordinates():
+    """Generalized convolution onto a caller-given output set (Sec. 4.2: the
+    output coordinates may be arbitrary): half of them input sites, half new
+    sites (some with no input in reach); backward through the role-reversed
+    map built from the output table."""
+    cin = WL.random_coords(87, 2500, 3, -10, 10, batch=2)
+    cnew = WL.random_coords(88, 2000, 3, -14, 14, batch=2)
+    seen = {tuple(r) for r in cin[:1200].tolist()}
+    cout = np.concatenate([cin[:1200], np.array([r for r in cnew.tolist() if tuple(r) not in seen], np.int32)])
+    offs = regions.hypercube(3, 3)
+    X, _ = WL.random_features(87, len(cin), 8)
+    W, _ = WL.random_weights(87, len(offs), 8, 12)
+    G, _ = WL.random_features(88, len(cout), 12)
+    tin, tout = _t(cin), _t(cout)
+    table_in = gsc.gsc_coords_build(tin)
+    table_out = gsc.gsc_coords_build(tout)
+    km = gsc.gsc_kernel_map(table_in, tout, offs)
+    tm = gsc.gsc_kernel_map(table_out, tin, -offs)
+    Y = gsc.gsc_sparse_conv_fwd(_t(X, torch.float32), _t(W, torch.float32), km)
+    dX, dW = gsc.gsc_sparse_conv_bwd(_t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32), km, tm,
+                                     np.arange(len(offs)))
+    torch.cuda.synchronize()
+    m = O.kernel_map(cin, cout, offs)
+    maps_equal_exact(gpu_pairs(km), m)
+    maps_equal_exact(gpu_pairs(tm), O.transposed_map(m))
+    assert rel_err(to_np(Y), O.conv_forward(X, W, m, len(cout))) <= TOL["f32"]
+    dXr, dWr = O.conv_backward(X, W, G, m)
+    assert rel_err(to_np(dX), dXr) <= TOL["f32"]
+    assert rel_err(to_np(dW), dWr) <= TOL["f32"]
+
+
 def test_centre_only_identity_exact():
     coords = WL.random_coords(79, 1000, 3, -20, 20, batch=2)
     c = _t(coords)

@@ -14,7 +14,9 @@ computed by means that share nothing with the oracle's own code.
 * pooling (Sec. 4.3, 4.4): torch max_pool3d over a -inf background and
   (sum, count) window sums by avg_pool3d for the size-2 partition and the
   overlapping size-3 window at stride 2, their autograd gradients, and
-  per-batch torch reductions for global pooling.
+  per-batch torch reductions for global pooling;
+* quantization (Sec. 4.1, Alg. 1): a hand-written example (golden file) and
+  np.unique over the floored rows.
 
 The planted-mistake tests at the end check that each pin fails for a
 plausible error in the oracle (sign of the offset, a transposed weight, a
@@ -586,3 +588,47 @@ def test_pool_planted_mistakes_are_caught():
     for j in range(len(out)):
         bad[first[j]] += G[j]
     assert rel_err(bad, refdX) > 1e-3
+
+
+# --------------------------------------------------------------------------- #
+# sparse tensor quantization (Sec. 4.1, Alg. 1)
+# --------------------------------------------------------------------------- #
+def test_quantize_golden():
+    pts, vox = [], set()
+    for line in open(os.path.join(GOLDEN, "quantize_small.txt")):
+        f = line.split("#")[0].split()
+        if not f:
+            continue
+        if f[0] == "P":
+            pts.append((int(f[2]), [float(x) for x in f[3:6]], int(f[6])))
+        else:
+            vox.add((tuple(int(x) for x in f[1:5]), int(f[5]), -100 if f[6] == "IGNORE" else int(f[6])))
+    b = np.array([p[0] for p in pts])
+    P = np.array([p[1] for p in pts])
+    L = np.array([p[2] for p in pts])
+    C, rep, lab, inv = O.quantize(P, b, 0.5, L)
+    got = {(tuple(int(x) for x in C[r]), int(rep[r]), int(lab[r])) for r in range(len(C))}
+    assert got == vox and len(C) == len(vox)
+    assert np.array_equal(C[inv][:, 1:], np.floor(P / 0.5).astype(np.int64))
+
+
+def test_quantize_vs_numpy_unique():
+    """Against np.unique over the floored rows (a library sort, not the
+    oracle's dict walk): the same voxel set, the first point of each as its
+    representative, and labels uniform or IGNORE."""
+    rng = np.random.default_rng(7)
+    P = rng.uniform(-3, 3, size=(4000, 3)).astype(np.float32)
+    b = rng.integers(0, 3, size=4000)
+    L = rng.integers(0, 3, size=4000)
+    C, rep, lab, inv = O.quantize(P, b, 0.25, L)
+    rows = np.concatenate([b[:, None], np.floor(P / np.float32(0.25)).astype(np.int64)], 1)
+    u, first, uinv = np.unique(rows, axis=0, return_index=True, return_inverse=True)
+    assert np.array_equal(C, u) and np.array_equal(rep, first)
+    assert np.array_equal(inv, uinv.ravel())
+    for r in range(len(u)):
+        ls = set(L[uinv.ravel() == r].tolist())
+        assert lab[r] == (ls.pop() if len(ls) == 1 else -100)
+    # a planted mistake: truncation toward zero instead of floor merges the
+    # voxels on either side of 0
+    trunc = np.concatenate([b[:, None], np.trunc(P / np.float32(0.25)).astype(np.int64)], 1)
+    assert len(np.unique(trunc, axis=0)) != len(u)
