@@ -125,6 +125,32 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
                       void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Sparse tensor quantization (Sec. 4.1, Alg. 1): the step before a1.       */
+/* ------------------------------------------------------------------------ */
+/* Workspace bytes for gsc_quantize with n points in D dimensions. */
+size_t gsc_quantize_ws_bytes(int64_t n, int32_t D);
+
+/* Points (device, n x D float32) with batch indices (device, n int32, or NULL
+ * for batch 0) become voxels: coordinate (b, floor(p_1 / v_1), ...,
+ * floor(p_D / v_D)), the quotient being the correctly rounded float32
+ * division; voxel (host, D positive floats).  One output row per distinct
+ * coordinate, written to out_coords (device, capacity n rows of 1 + D int32)
+ * in the order of each voxel's first point; *n_out (host) receives their
+ * number.  rep (device, capacity n int32): the first point of each voxel (the
+ * row whose features it takes).  labels (device, n int32, nullable) and
+ * out_labels (device, capacity n, nullable): a voxel's label is its points'
+ * common label, or ignore_label when they carry more than one.  inverse
+ * (device, n int32, nullable): the voxel row of every point.  out_table
+ * (>= gsc_table_bytes(n) bytes) receives the hash table of the voxel
+ * coordinates, usable by gsc_kernel_map.  Synchronises `stream` once.
+ * Errors: EINVAL, ESHORT, ERANGE (a coordinate outside +-2^30, or a box needing
+ * more than 62 key bits), EHIP. */
+int gsc_quantize(const float* points, const int32_t* batch, int64_t n, int32_t D, const float* voxel,
+                 const int32_t* labels, int32_t ignore_label, int32_t* out_coords, int64_t* n_out, int32_t* rep,
+                 int32_t* out_labels, int32_t* inverse, void* out_table, size_t out_table_bytes,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* a3. Kernel map (Sec. 4.2; Eq. 3, Sec. 3.1).                              */
 /* ------------------------------------------------------------------------ */
 /* Number of 64-row groups of n_out output rows: ceil(n_out / 64). */

@@ -229,7 +229,7 @@ __global__ void __launch_bounds__(kThreads) k_rep_count(int64_t n, const TableHe
 
 __global__ void __launch_bounds__(kThreads) k_rep_write(const int32_t* coords, int64_t n, StrideArg st,
                                                         TableHeader* h, Slot* slots, const int64_t* slot_of,
-                                                        const int64_t* off, int32_t* out_coords) {
+                                                        const int64_t* off, int32_t* out_coords, int32_t* rep_row) {
     const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     bool rep = false;
     int64_t s = 0;
@@ -246,6 +246,70 @@ __global__ void __launch_bounds__(kThreads) k_rep_write(const int32_t* coords, i
     load_row(coords, r, ncol, st, v);
     for (int c = 0; c < ncol; ++c) out_coords[row * ncol + c] = (int32_t)v[c];
     slots[s].val = (int32_t)row;
+    if (rep_row) rep_row[row] = (int32_t)r;
+}
+
+// ---------------------------------------------------------------------------
+// Sparse tensor quantization (Sec. 4.1, Alg. 1): integer rows (b, floor(p/v))
+// deduplicated through the table exactly as strided output coordinates are
+// (first point of a voxel is its representative, rows in the order of their
+// representatives), then labels merged per voxel.
+// ---------------------------------------------------------------------------
+struct VoxelArg {
+    float v[kMaxCols - 1];   // voxel size per spatial axis
+};
+
+// qc[r] = (batch[r] or 0, floor(p_d / v_d)); the quotient is the correctly
+// rounded float32 division, then floor.  A coordinate outside +-2^30 sets the
+// range status.
+__global__ void __launch_bounds__(kThreads) k_quantize(const float* __restrict__ points,
+                                                       const int32_t* __restrict__ batch, int64_t n, int D, VoxelArg va,
+                                                       int32_t* __restrict__ qc, TableHeader* h) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    const int ncol = D + 1;
+    qc[r * ncol] = batch ? batch[r] : 0;
+    bool bad = false;
+    for (int d = 0; d < D; ++d) {
+        const float q = floorf(points[r * D + d] / va.v[d]);
+        bad |= !(q >= -1073741824.f && q <= 1073741824.f);   // also NaN
+        qc[r * ncol + 1 + d] = bad ? 0 : (int32_t)q;
+    }
+    if (bad) atomicOr(&h->status, ST_RANGE);
+}
+
+// per voxel: the row of every point (inverse) and the min / max label of its points
+__global__ void __launch_bounds__(kThreads) k_quant_labels(int64_t n, const TableHeader* h, const Slot* slots,
+                                                           const int64_t* __restrict__ slot_of,
+                                                           const int32_t* __restrict__ labels,
+                                                           int32_t* __restrict__ inverse, int32_t* __restrict__ lmin,
+                                                           int32_t* __restrict__ lmax) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n || h->status != 0) return;
+    int64_t sl = slot_of[r];
+    if (sl < 0) sl = ~sl;   // a representative
+    const int32_t o = slots[sl].val;
+    if (o < 0 || o >= n) return;
+    if (inverse) inverse[r] = o;
+    if (labels) {
+        atomicMin(&lmin[o], labels[r]);
+        atomicMax(&lmax[o], labels[r]);
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) k_fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// voxel label: the points' common label, else ignore_label (f of Alg. 1)
+__global__ void __launch_bounds__(kThreads) k_quant_final(int64_t cap, const TableHeader* h,
+                                                          const int32_t* __restrict__ lmin,
+                                                          const int32_t* __restrict__ lmax, int32_t ignore_label,
+                                                          int32_t* __restrict__ out_labels) {
+    const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (o >= cap || o >= h->n || h->status != 0) return;
+    out_labels[o] = lmin[o] == lmax[o] ? lmin[o] : ignore_label;
 }
 
 static unsigned grid_for(int64_t n, int per = kThreads) {
@@ -415,12 +479,119 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
     int rc = scan_counts(cnt, groups, off, &h->n, scan_ws, s);   // header n = number of output rows
     if (rc) return rc;
     hipLaunchKernelGGL(k_rep_write, dim3(grid_for(n_in)), dim3(kThreads), 0, s, in_coords, n_in, st, h, slots,
-                       slot_of, off, out_coords);
+                       slot_of, off, out_coords, (int32_t*)nullptr);
     GSC_LAUNCH_CHECK();
     TableHeader hh;
     rc = read_status(out_table, s, &hh);
     if (rc) return rc;
     rc = status_to_code(hh, "coords_stride");
+    if (rc) return rc;
+    *n_out = hh.n;
+    return GSC_OK;
+}
+
+size_t gsc_quantize_ws_bytes(int64_t n, int32_t D) {
+    if (n < 0 || D < 1 || D + 1 > kMaxCols) return 0;
+    const int64_t groups = (n + 63) / 64;
+    auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    size_t b = al((size_t)n * (D + 1) * sizeof(int32_t));   // integer rows
+    b += al((size_t)n * sizeof(int64_t));                    // slot of each row
+    b += al((size_t)groups * sizeof(int32_t));               // counts
+    b += al((size_t)(groups + 1) * sizeof(int64_t));         // offsets
+    b += 2 * al((size_t)n * sizeof(int32_t));                // label min / max per voxel
+    b += scan_ws_bytes(groups);
+    return b + 256;
+}
+
+int gsc_quantize(const float* points, const int32_t* batch, int64_t n, int32_t D, const float* voxel,
+                 const int32_t* labels, int32_t ignore_label, int32_t* out_coords, int64_t* n_out, int32_t* rep,
+                 int32_t* out_labels, int32_t* inverse, void* out_table, size_t out_table_bytes, void* ws,
+                 size_t ws_bytes, void* stream) {
+    clear_error();
+    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "quantize: D=%d outside [1,%d]", D, kMaxCols - 1);
+    if (n < 0 || n > INT32_MAX) return fail(GSC_EINVAL, "quantize: n=%lld invalid", (long long)n);
+    if (!voxel || !n_out || !out_table) return fail(GSC_EINVAL, "quantize: null voxel/n_out/out_table");
+    if (n > 0 && (!points || !out_coords || !rep || !ws))
+        return fail(GSC_EINVAL, "quantize: null points/out_coords/rep/ws");
+    if (n > 0 && out_labels && !labels) return fail(GSC_EINVAL, "quantize: out_labels without labels");
+    VoxelArg va{};
+    for (int d = 0; d < D; ++d) {
+        if (!(voxel[d] > 0.f) || voxel[d] == INFINITY)
+            return fail(GSC_EINVAL, "quantize: voxel[%d]=%g must be positive and finite", d, (double)voxel[d]);
+        va.v[d] = voxel[d];
+    }
+    if (out_table_bytes < gsc_table_bytes(n))
+        return fail(GSC_ESHORT, "quantize: out_table needs %zu bytes, got %zu", gsc_table_bytes(n), out_table_bytes);
+    if (n > 0 && ws_bytes < gsc_quantize_ws_bytes(n, D))
+        return fail(GSC_ESHORT, "quantize: ws needs %zu bytes, got %zu", gsc_quantize_ws_bytes(n, D), ws_bytes);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int ncol = D + 1;
+    const int64_t cap = table_capacity(n);
+    TableHeader* h = reinterpret_cast<TableHeader*>(out_table);
+    Slot* slots = table_slots(out_table);
+    hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol, (int64_t)0,
+                       (int32_t)INT_MAX, (const int32_t*)out_coords);
+    GSC_LAUNCH_CHECK();
+    if (n == 0) {
+        hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+        GSC_LAUNCH_CHECK();
+        GSC_HIP(hipStreamSynchronize(s));
+        *n_out = 0;
+        return GSC_OK;
+    }
+    const int64_t groups = (n + 63) / 64;
+    auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    char* w = reinterpret_cast<char*>(ws);
+    int32_t* qc = reinterpret_cast<int32_t*>(w);
+    w += al((size_t)n * ncol * sizeof(int32_t));
+    int64_t* slot_of = reinterpret_cast<int64_t*>(w);
+    w += al((size_t)n * sizeof(int64_t));
+    int32_t* cnt = reinterpret_cast<int32_t*>(w);
+    w += al((size_t)groups * sizeof(int32_t));
+    int64_t* off = reinterpret_cast<int64_t*>(w);
+    w += al((size_t)(groups + 1) * sizeof(int64_t));
+    int32_t* lmin = reinterpret_cast<int32_t*>(w);
+    w += al((size_t)n * sizeof(int32_t));
+    int32_t* lmax = reinterpret_cast<int32_t*>(w);
+    w += al((size_t)n * sizeof(int32_t));
+    void* scan_ws = w;
+
+    StrideArg none{};
+    hipLaunchKernelGGL(k_quantize, dim3(grid_for(n)), dim3(kThreads), 0, s, points, batch, n, (int)D, va, qc, h);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n, 256)), dim3(kThreads), 0, s, qc, n, ncol, none, h);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_insert_min, dim3(grid_for(n)), dim3(kThreads), 0, s, qc, n, none, h, slots, slot_of);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_rep_count, dim3(grid_for(n)), dim3(kThreads), 0, s, n, h, slots, slot_of, cnt);
+    GSC_LAUNCH_CHECK();
+    int rc = scan_counts(cnt, groups, off, &h->n, scan_ws, s);   // header n = number of voxels
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_rep_write, dim3(grid_for(n)), dim3(kThreads), 0, s, qc, n, none, h, slots, slot_of, off,
+                       out_coords, rep);
+    GSC_LAUNCH_CHECK();
+    if (labels) {
+        hipLaunchKernelGGL(k_fill_i32, dim3(grid_capped(n)), dim3(kThreads), 0, s, lmin, n, (int32_t)INT_MAX);
+        GSC_LAUNCH_CHECK();
+        hipLaunchKernelGGL(k_fill_i32, dim3(grid_capped(n)), dim3(kThreads), 0, s, lmax, n, (int32_t)INT_MIN);
+        GSC_LAUNCH_CHECK();
+    }
+    if (labels || inverse) {
+        hipLaunchKernelGGL(k_quant_labels, dim3(grid_for(n)), dim3(kThreads), 0, s, n, h, slots, slot_of, labels,
+                           inverse, lmin, lmax);
+        GSC_LAUNCH_CHECK();
+    }
+    if (labels && out_labels) {
+        hipLaunchKernelGGL(k_quant_final, dim3(grid_for(n)), dim3(kThreads), 0, s, n, h, lmin, lmax, ignore_label,
+                           out_labels);
+        GSC_LAUNCH_CHECK();
+    }
+    TableHeader hh;
+    rc = read_status(out_table, s, &hh);
+    if (rc) return rc;
+    rc = status_to_code(hh, "quantize");
     if (rc) return rc;
     *n_out = hh.n;
     return GSC_OK;

@@ -47,6 +47,9 @@ _SIGS = {
     "gsc_table_status": (ctypes.c_int, [_vp, _vp]),
     "gsc_stride_ws_bytes": (_sz, [_i64]),
     "gsc_coords_stride": (ctypes.c_int, [_vp, _i64, _i32, _c_i32p, _vp, _c_i64p, _vp, _sz, _vp, _sz, _vp]),
+    "gsc_quantize_ws_bytes": (_sz, [_i64, _i32]),
+    "gsc_quantize": (ctypes.c_int, [_vp, _vp, _i64, _i32, ctypes.POINTER(ctypes.c_float), _vp, _i32, _vp, _c_i64p,
+                                    _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
     "gsc_kmap_groups": (_i64, [_i64]),
     "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
     "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
@@ -473,3 +476,40 @@ def gsc_global_pool_bwd(dY: torch.Tensor, coords: torch.Tensor, mode: str, poole
     _check(lib().gsc_global_pool_bwd(m, _ptr(dY), dY.shape[0], C, _ptr(coords), coords.shape[1] - 1, n,
                                      _ptr(pooled.arg), _ptr(pooled.cnt), _ptr(dX), _stream(stream)))
     return dX
+
+
+# --------------------------------------------------------------------------- #
+# sparse tensor quantization (Sec. 4.1, Alg. 1)
+# --------------------------------------------------------------------------- #
+@dataclasses.dataclass
+class Quantized:
+    coords: torch.Tensor             # int32 [n_out, 1 + D]
+    rep: torch.Tensor                # int32 [n_out]: first point of each voxel
+    labels: Optional[torch.Tensor]   # int32 [n_out] (when labels were given)
+    inverse: torch.Tensor            # int32 [n]: voxel row of every point
+    table: torch.Tensor              # hash table of the voxel coordinates
+
+
+def gsc_quantize(points: torch.Tensor, voxel, batch: Optional[torch.Tensor] = None,
+                 labels: Optional[torch.Tensor] = None, ignore_label: int = -100, stream=None) -> Quantized:
+    _need(points, torch.float32, "points", 2)
+    n, D = points.shape
+    dev = points.device
+    if batch is not None:
+        _need(batch, torch.int32, "batch", 1)
+    if labels is not None:
+        _need(labels, torch.int32, "labels", 1)
+    v = [float(voxel)] * D if np.isscalar(voxel) else [float(x) for x in voxel]
+    hv = (ctypes.c_float * D)(*v)
+    out = torch.empty((max(n, 1), D + 1), dtype=torch.int32, device=dev)
+    rep = torch.empty((max(n, 1),), dtype=torch.int32, device=dev)
+    out_labels = torch.empty((max(n, 1),), dtype=torch.int32, device=dev) if labels is not None else None
+    inverse = torch.empty((max(n, 1),), dtype=torch.int32, device=dev)
+    table = torch.empty(gsc_table_bytes(n), dtype=torch.uint8, device=dev)
+    ws = _ws(lib().gsc_quantize_ws_bytes(n, D), dev)
+    n_out = ctypes.c_int64(0)
+    _check(lib().gsc_quantize(_ptr(points), _ptr(batch), n, D, hv, _ptr(labels), ignore_label, _ptr(out),
+                              ctypes.byref(n_out), _ptr(rep), _ptr(out_labels), _ptr(inverse), _ptr(table),
+                              table.numel(), _ptr(ws), ws.numel(), _stream(stream)))
+    m = n_out.value
+    return Quantized(out[:m], rep[:m], None if out_labels is None else out_labels[:m], inverse[:n], table)

@@ -12,6 +12,7 @@ relative error 1e-5 (fp32) or 2e-2 (bf16 inputs, fp32 accumulation).
   negative coordinates over several batches, non-symmetric and large regions,
   tensor stride, odd channel counts, the centre-only identity kernel.
 """
+import os
 import sys
 
 import numpy as np
@@ -598,3 +599,54 @@ def test_global_pool_parity(mode):
     if mode == "max":
         assert np.array_equal(to_np(p.arg), arg)
     assert rel_err(to_np(dX), O.global_pool_backward(G, c[:, 0], mode, arg, N)) <= TOL["f32"]
+
+
+# --------------------------------------------------------------------------- #
+# sparse tensor quantization (Sec. 4.1, Alg. 1)
+# --------------------------------------------------------------------------- #
+def _quant_compare(P, b, voxel, L):
+    q = gsc.gsc_quantize(_t(P, torch.float32), voxel, batch=_t(b), labels=None if L is None else _t(L))
+    torch.cuda.synchronize()
+    C, rep, lab, inv = O.quantize(P, b, voxel, L)
+    gc = q.coords.cpu().numpy().astype(np.int64)
+    grep, ginv = q.rep.cpu().numpy().astype(np.int64), q.inverse.cpu().numpy().astype(np.int64)
+    assert len(gc) == len(C)
+    # rows come in the order of their first points; the oracle's in key order
+    order = np.argsort(grep)
+    oc = np.argsort(rep)
+    assert np.array_equal(gc[order], C[oc]) and np.array_equal(grep[order], rep[oc])
+    assert np.array_equal(grep, np.sort(grep))                      # first-point order
+    if L is not None:
+        assert np.array_equal(q.labels.cpu().numpy()[order], lab[oc])
+    # every point lands in the voxel of its own coordinate
+    assert np.array_equal(gc[ginv], C[inv])
+    return q
+
+
+def test_quantize_golden_on_gpu():
+    pts, b, L = [], [], []
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", "quantize_small.txt")):
+        f = line.split("#")[0].split()
+        if f and f[0] == "P":
+            b.append(int(f[2]))
+            pts.append([float(x) for x in f[3:6]])
+            L.append(int(f[6]))
+    _quant_compare(np.array(pts, np.float32), np.array(b, np.int32), 0.5, np.array(L, np.int32))
+
+
+def test_quantize_random_and_scene():
+    rng = np.random.default_rng(95)
+    P = rng.uniform(-4, 4, size=(60000, 3)).astype(np.float32)
+    b = rng.integers(0, 3, size=60000).astype(np.int32)
+    L = rng.integers(0, 4, size=60000).astype(np.int32)
+    _quant_compare(P, b, 0.1, L)
+    _quant_compare(P, b, (0.05, 0.1, 0.2), None)                    # anisotropic voxels, no labels
+    # the synthetic indoor scene's points (two scenes) at 2 cm
+    pts, bs = [], []
+    for bi in range(2):
+        geom = WL.draw_scene(WL.rng_for(1, WL.S_GEOM, bi), scale=0.5)
+        p = WL.sample_points(geom, WL.rng_for(1, WL.S_GEOM, bi, 1), 40000)
+        pts.append(np.asarray(p, np.float32))
+        bs.append(np.full(len(p), bi, np.int32))
+    q = _quant_compare(np.concatenate(pts), np.concatenate(bs), 0.02, None)
+    _say(f"  scene points {sum(len(p) for p in pts)} -> voxels {q.coords.shape[0]}")
