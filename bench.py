@@ -221,6 +221,62 @@ def run_pool(args):
     print(json.dumps(out), flush=True)
 
 
+def scene_points(scale: float = 1.0):
+    """The float points of workload 1's two scenes (before voxelisation),
+    their batch indices and per-point labels (the surface each point lies on
+    is not tracked, so the labels are a seeded random class per point)."""
+    import numpy as np
+    from paper_1904_08755_amd import workloads as WL
+    pts, bs = [], []
+    n = int(round(WL.SCENE_POINTS_2CM * scale * scale))
+    for b in range(2):
+        geom = WL.draw_scene(WL.rng_for(1, WL.S_GEOM, b), scale=scale)
+        p = WL.sample_points(geom, WL.rng_for(1, WL.S_GEOM, b, 1), n)
+        pts.append(np.asarray(p, np.float32))
+        bs.append(np.full(len(p), b, np.int32))
+    P, B = np.concatenate(pts), np.concatenate(bs)
+    L = np.random.default_rng(np.random.SeedSequence(WL.ROOT_SEED, spawn_key=(2000,))).integers(0, 20, len(P))
+    return P, B, L.astype(np.int32)
+
+
+def run_quantize(args):
+    """Quantization of the scenes' points at 2 cm (the step before the
+    hash table): voxel rows, representatives, labels, inverse map.  The call
+    synchronises once (it returns the voxel count)."""
+    import numpy as np
+    import torch
+
+    from paper_1904_08755_amd import gsc
+    P, B, L = scene_points()
+    tp, tb, tl = torch.from_numpy(P).cuda(), torch.from_numpy(B).cuda(), torch.from_numpy(L).cuda()
+    for _ in range(args.warmup):
+        q = gsc.gsc_quantize(tp, 0.02, batch=tb, labels=tl)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        q = gsc.gsc_quantize(tp, 0.02, batch=tb, labels=tl)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    n, n_out = len(P), int(q.coords.shape[0])
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.gsc_oracle as O
+        t1 = time.perf_counter()
+        O.quantize(P, B, 0.02, L)
+        tc = time.perf_counter() - t1
+        cpu = {"value": n / tc, "unit": "points/s", "cores": 1, "kind": "oracle",
+               "sample": f"all {n} points, single-threaded Python; {tc:.1f} s", "seconds": tc}
+    out = {
+        "metric": "sparse tensor quantization points/s", "value": round(n / sec, 1), "unit": "points/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "scene2cm_b2_points_quantize", "points": n, "voxels": n_out, "voxel_m": 0.02,
+                   "parallelism": "single GPU"},
+        "roofline": None, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,6 +287,8 @@ def main():
     ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
     ap.add_argument("--pool", choices=["max", "avg", "sum"], default=None,
                     help="time pooling instead (Sec. 4.3, 4.4): the 2^3 stride-2 window over the scene of workload 1")
+    ap.add_argument("--quantize", action="store_true",
+                    help="time sparse tensor quantization (Alg. 1) of the two indoor scenes' points at 2 cm instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB once (a copy of known size for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -251,6 +309,8 @@ def main():
     gsc.lib()
     if args.pool:
         return run_pool(args)
+    if args.quantize:
+        return run_quantize(args)
     t = time.perf_counter()
     wl = WL.make_workload(args.workload)
     log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")
