@@ -337,19 +337,28 @@ struct BfGroup {
 };
 
 template <int CA, int CB, typename Sel>
-__global__ void __launch_bounds__(kBfThreads, 1)
+__global__ void __launch_bounds__(kBfThreads, 2)
 k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __restrict__ Bt, int K, Sel sel,
                 const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
                 const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
-                uint16_t* __restrict__ Y) {
+                int cb_full, int64_t ntiles, uint16_t* __restrict__ Y) {
     using C = BlkBf16<CA, CB>;
     __shared__ __attribute__((aligned(16))) uint8_t slab[2][kBfT][16 * 128];   // [group parity][block][row][128 B]
     __shared__ int32_t idx_s[kBfIdxInts];
     __shared__ int32_t perm_s[kBfT * 16];
+    // Workgroup -> (tile, column slice): the slices of one tile are 8
+    // workgroups apart, so they run on the same XCD (workgroup i runs on XCD
+    // i mod 8) at about the same time and share the tile's rows in its L2.
+    const int nslice = cb_full / CB;
+    const int64_t rest = blockIdx.x >> 3;
+    const int slice = (int)(rest % nslice);
+    const int64_t tile = (rest / nslice) * 8 + (blockIdx.x & 7);
+    if (tile >= ntiles) return;
+    const int col0 = slice * CB;
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int r16 = lane & 15, q = lane >> 4;
-    const int64_t b0 = (int64_t)blockIdx.x * kBfT;
+    const int64_t b0 = tile * kBfT;
     const int nbt = (int)min((int64_t)kBfT, nb - b0);
 
     // the tile's blocks (wave-uniform) and the offset -> weight map per lane
@@ -390,7 +399,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
     const __amdgpu_buffer_rsrc_t xr =
         __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)(n_x * CA * 2), kBufFlags);
     const __amdgpu_buffer_rsrc_t wr =
-        __builtin_amdgcn_make_buffer_rsrc((void*)Bt, (short)0, (int)((int64_t)K * CB * CA * 2), kBufFlags);
+        __builtin_amdgcn_make_buffer_rsrc((void*)Bt, (short)0, (int)((int64_t)K * cb_full * CA * 2), kBufFlags);
 
     auto blocks_with = [&](int k) {
         uint32_t m = 0;
@@ -433,7 +442,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
     uint32_t woff[C::RW];
 #pragma unroll
     for (int f = 0; f < C::RW; ++f)
-        woff[f] = (uint32_t)(((wave * C::NC + 16 * (f % C::NB) + r16) * CA + 32 * (f / C::NB) + 8 * q) * 2);
+        woff[f] = (uint32_t)(((col0 + wave * C::NC + 16 * (f % C::NB) + r16) * CA + 32 * (f / C::NB) + 8 * q) * 2);
     // byte offsets of this lane's rows for group g (kBufNone: none)
     auto row_offsets = [&](const BfGroup& g, uint32_t (&off)[C::RL]) {
 #pragma unroll
@@ -450,7 +459,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         if (b < C::RL) st.r[b] = __builtin_amdgcn_raw_buffer_load_b128(xr, off[b], h * C::CAH * 2, 0);
         if (b < C::RW) {
             const int wsel = readlane_i32(sel_lane, g.valid ? g.k : 0);
-            st.w[b] = __builtin_amdgcn_raw_buffer_load_b128(wr, woff[b], (wsel * CB * CA + h * C::CAH) * 2, 0);
+            st.w[b] = __builtin_amdgcn_raw_buffer_load_b128(wr, woff[b], (wsel * cb_full * CA + h * C::CAH) * 2, 0);
         }
         // keep the loads here: their uses sit in conditional blocks two groups
         // on, and sinking them there would undo the pipeline
@@ -562,7 +571,7 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
             const int32_t row = perm_s[64 * half + pos];
             if (row >= 0 && row < n_y) {
                 const u32x4 val = *reinterpret_cast<const u32x4*>(&out_s[pos * (CB / 2) + (tid % LPR) * 4]);
-                *reinterpret_cast<u32x4*>(Y + (int64_t)row * CB + (tid % LPR) * 8) = val;
+                *reinterpret_cast<u32x4*>(Y + (int64_t)row * cb_full + col0 + (tid % LPR) * 8) = val;
             }
         }
     }
@@ -576,10 +585,11 @@ bool blk_bf16_fits(int64_t n_x, int ca) { return n_x >= 0 && n_x * ca < ((int64_
 
 template <int CA, int CB, typename Sel>
 static void launch_blk_bf16(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
-                            const BlockPlan& p, int64_t nb, int64_t n_y, uint16_t* Y, hipStream_t s) {
+                            const BlockPlan& p, int64_t nb, int64_t n_y, int cb_full, uint16_t* Y, hipStream_t s) {
     const int64_t tiles = (nb + kBfT - 1) / kBfT;
-    hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel>), dim3((unsigned)tiles), dim3(kBfThreads), 0, s, X, n_x, Bt, K,
-                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, Y);
+    const int64_t grid = 8 * (int64_t)(cb_full / CB) * ((tiles + 7) / 8);
+    hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel>), dim3((unsigned)grid), dim3(kBfThreads), 0, s, X, n_x, Bt, K,
+                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, cb_full, tiles, Y);
 }
 
 __global__ void k_zero_u16(uint16_t* __restrict__ y, int64_t n) {
@@ -604,14 +614,18 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
     }
     auto X16 = reinterpret_cast<const uint16_t*>(X);
     auto B16 = reinterpret_cast<const uint16_t*>(Bt);
-#define GSC_BFB_CASE(A, B)                                                        \
-    if (ca == A && cb == B) {                                                     \
-        launch_blk_bf16<A, B, Sel>(X16, n_x, B16, K, sel, plan, nb, n_y, Y16, s); \
-        GSC_LAUNCH_CHECK();                                                       \
-        return GSC_OK;                                                            \
+    // 256 output columns go in two 128-column slices (two workgroups per
+    // tile): a slice's sums fit in 167 VGPRs, so two workgroups share a CU
+    // (two waves per SIMD), where one 256-column workgroup holds a CU alone
+#define GSC_BFB_CASE(A, B, S)                                                         \
+    if (ca == A && cb == B) {                                                         \
+        launch_blk_bf16<A, S, Sel>(X16, n_x, B16, K, sel, plan, nb, n_y, B, Y16, s); \
+        GSC_LAUNCH_CHECK();                                                           \
+        return GSC_OK;                                                                \
     }
-    GSC_BFB_CASE(64, 64) GSC_BFB_CASE(64, 128) GSC_BFB_CASE(64, 256) GSC_BFB_CASE(128, 64) GSC_BFB_CASE(128, 128)
-    GSC_BFB_CASE(128, 256) GSC_BFB_CASE(256, 64) GSC_BFB_CASE(256, 128) GSC_BFB_CASE(256, 256)
+    GSC_BFB_CASE(64, 64, 64) GSC_BFB_CASE(64, 128, 128) GSC_BFB_CASE(64, 256, 128) GSC_BFB_CASE(128, 64, 64)
+    GSC_BFB_CASE(128, 128, 128) GSC_BFB_CASE(128, 256, 128) GSC_BFB_CASE(256, 64, 64) GSC_BFB_CASE(256, 128, 128)
+    GSC_BFB_CASE(256, 256, 128)
 #undef GSC_BFB_CASE
     return fail(GSC_EINVAL, "conv: no bf16 block engine for %dx%d", ca, cb);
 }
