@@ -48,8 +48,8 @@ def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool) -> 
     library's dispatch: block engine on a plan, else the map's row form)."""
     dt = gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32
     if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
-        if dtype == "bf16":
-            return f"k_conv_blk_bf16<{ci}, {co}, gsc::WIdentity>"
+        if dtype == "bf16":   # 256 output columns run as two 128-column workgroups per tile
+            return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity>"
         return f"k_conv_blk_f32<{ci}, {co}, false>"
     if dtype == "bf16":
         if ci in (128, 256) and co in (128, 256):
