@@ -43,14 +43,15 @@ def fwd_bytes(n_pairs, n_out, ci, co, K, s):
     return n_pairs * (s * ci + 8) + n_out * s * co + K * ci * co * s
 
 
-def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool) -> str:
+def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool, epilogue: bool = False) -> str:
     """Name of the kernel gsc_sparse_conv_fwd launches for this layer (the
     library's dispatch: block engine on a plan, else the map's row form)."""
     dt = gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32
+    ep = "true" if epilogue else "false"
     if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
         if dtype == "bf16":   # 256 output columns run as two 128-column workgroups per tile
-            return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity>"
-        return f"k_conv_blk_f32<{ci}, {co}, false>"
+            return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity, {ep}>"
+        return f"k_conv_blk_f32<{ci}, {co}, false, {ep}>"
     if dtype == "bf16":
         if ci in (128, 256) and co in (128, 256):
             return f"k_conv_bf16_dma<{ci}, {co}, gsc::WIdentity>"
@@ -283,6 +284,12 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
+    ap.add_argument("--region", choices=["hybrid", "cube", "spatial", "cross"], default=None,
+                    help="region of workload 3 (3D video): hybrid (default, 29 offsets), cube (tesseract, 81), "
+                         "spatial (3^3 at zero time offset, 27: each frame on its own), cross (9)")
+    ap.add_argument("--affine", action="store_true",
+                    help="forward with batch normalisation (per-channel affine form) and ReLU fused into the "
+                         "convolution's output write (Sec. 4.5); single-layer workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
     ap.add_argument("--pool", choices=["max", "avg", "sum"], default=None,
@@ -312,12 +319,24 @@ def main():
     if args.quantize:
         return run_quantize(args)
     t = time.perf_counter()
-    wl = WL.make_workload(args.workload)
+    if args.region is not None and args.workload != 3:
+        print("--region applies to workload 3 (the 3D video) only", file=sys.stderr)
+        sys.exit(2)
+    wl = WL.make_workload(args.workload, region=args.region)
     log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")
     dw = pipeline.to_device(wl, "cuda")
+    epi = None
+    if args.affine:
+        if len(wl.layers) != 1:
+            print("--affine applies to the single-layer workloads (0, 1, 3, 4)", file=sys.stderr)
+            sys.exit(2)
+        rng = np.random.default_rng(np.random.SeedSequence(WL.ROOT_SEED, spawn_key=(wl.config_id, 9)))
+        co = wl.layers[0].c_out
+        epi = (torch.from_numpy(rng.uniform(0.5, 2.0, co).astype(np.float32)).cuda(),
+               torch.from_numpy(rng.uniform(-0.5, 0.5, co).astype(np.float32)).cuda())
     torch.cuda.synchronize()
 
-    plan0 = pipeline.StepPlan(dw, use_plan=not args.no_plan)
+    plan0 = pipeline.StepPlan(dw, use_plan=not args.no_plan, epilogue=epi)
     for _ in range(args.warmup):
         plan0.run()
     gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
@@ -326,7 +345,7 @@ def main():
     log(f"warmup done ({args.warmup} steps)")
 
     steps_events = []
-    plan = pipeline.StepPlan(dw, use_plan=not args.no_plan)
+    plan = pipeline.StepPlan(dw, use_plan=not args.no_plan, epilogue=epi)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -363,7 +382,7 @@ def main():
     n_out0 = km0.n_out
     # dominant kernel: the forward convolution of layer 0 (single-layer workloads, where the fwd stage is one launch)
     planned = bool(plan.plans)
-    kernel = forward_kernel(gsc, wl.dtype, L0.c_in, L0.c_out, km0.K, planned)
+    kernel = forward_kernel(gsc, wl.dtype, L0.c_in, L0.c_out, km0.K, planned, epilogue=epi is not None)
     wname = wl.name.replace("_cube3", "")
     traffic = measured_traffic(kernel, wname)
     dom_bytes = fwd_bytes(pairs[0], n_out0, L0.c_in, L0.c_out, km0.K, s)
@@ -413,7 +432,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "voxels": wl.n, "D": wl.D,
                    "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
-                   "kernel_map_pairs": pairs, "block_plan": bool(plan.plans), "parallelism": "single GPU"},
+                   "kernel_map_pairs": pairs, "block_plan": bool(plan.plans), "parallelism": "single GPU",
+                   **({"epilogue": "batchnorm_affine+relu"} if epi is not None else {})},
         "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
         "effective_gflops": round(flops / conv_s / 1e9, 1),
         "kernel_map_build_ms": round(ms["map"], 4),

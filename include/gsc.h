@@ -17,6 +17,8 @@
  *                        ordered by neighbour mask, in 16-row blocks
  *   gsc_sparse_conv_fwd  Alg. 2 (and the transposed convolution of Sec. 4.2,
  *                        run on the role-reversed kernel map)
+ *   gsc_sparse_conv_fwd_affine  the same with a per-channel affine map and
+ *                        ReLU applied to the sums as they are stored (Sec. 4.5)
  *   gsc_sparse_conv_bwd  gradients of Alg. 2 with respect to the input
  *                        features and the weights (chain rule of Eq. 3)
  *   gsc_sparse_pool_*    max / average / sum pooling over a kernel map and
@@ -260,8 +262,11 @@ size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t
  * block plan (gsc_conv_plan), or all four NULL; when given and
  * gsc_conv_block_engine(dtype, c_in, c_out, K) is 1 (and X and W are 16-byte
  * aligned) the block engine computes Y from the plan, otherwise the map is
- * used.  Both give Eq. 3; each output row sums its offsets' products in
- * increasing offset order.  The transposed convolution is this call on the
+ * used.  Both give Eq. 3.  The block engines and the row form's specialised
+ * float32 kernels add each output row's products in increasing offset order
+ * (bit-reproducible); the general row-form kernel (other shapes, K > 64)
+ * adds them into its LDS tile atomically, in no fixed order, so its last
+ * bits can differ between calls.  The transposed convolution is this call on the
  * role-reversed map (see gsc_kernel_map).  ws: gsc_conv_fwd_ws_bytes
  * bytes of device memory (may be NULL when that is 0), contents not kept.
  * Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
@@ -271,6 +276,29 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
                         const int64_t* gidx, int64_t n_pairs,
                         const int32_t* perm, const uint32_t* bmask, const int64_t* ibase, const int32_t* items,
                         void* Y, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Forward convolution with a per-output-channel affine map and activation
+ * fused into the kernel that writes Y (Sec. 4.5: batch normalisation, whose
+ * inference form is an affine map per channel, and ReLU act on the feature
+ * matrix alone, so they can be applied to each output row as it is produced):
+ *   Y[j][c] = act(S[j][c] * scale[c] + shift[c]),
+ * S = the sums of gsc_sparse_conv_fwd (same arguments, same meaning).  scale
+ * and shift: device float32 arrays of c_out values, each nullable (null scale
+ * = 1, null shift = 0); act: GSC_ACT_NONE or GSC_ACT_RELU (max(v, 0); NaN
+ * passes through).  The map is applied to the float32 sums before bf16
+ * rounding on the block engines; the row form applies it in a second pass
+ * over Y (so a bf16 Y is rounded twice there).  A batch-normalised layer in
+ * training takes scale = gamma / sqrt(var + eps), shift = beta - mean * scale
+ * once its batch statistics are known.  Asynchronous.  Errors: as
+ * gsc_sparse_conv_fwd, and EINVAL for an unknown act. */
+typedef enum { GSC_ACT_NONE = 0, GSC_ACT_RELU = 1 } gsc_act;
+int gsc_sparse_conv_fwd_affine(int32_t dtype, const void* X, int64_t n_in, int32_t c_in,
+                               const void* W, int32_t c_out, int32_t K,
+                               const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
+                               const int64_t* gidx, int64_t n_pairs,
+                               const int32_t* perm, const uint32_t* bmask, const int64_t* ibase,
+                               const int32_t* items, const float* scale, const float* shift, int32_t act,
+                               void* Y, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* a6 / a7. Backward: dX and dW.                                             */

@@ -18,7 +18,8 @@ Conventions (readings of the paper, listed with the others in the design notes):
 Parity status: every function is pinned by the CPU tests (brute-force maps,
 closed-form counts, dense-convolution special cases, adjoint identities, finite
 differences, dense max/average pooling and their gradients, per-batch
-reductions, a hand-written quantization example and np.unique); the row order
+reductions, a hand-written quantization example and np.unique, batch
+statistics after normalisation); the row order
 of ``output_coordinates`` is an implementation choice and is compared
 canonically, not pinned.
 """
@@ -76,8 +77,15 @@ def hybrid(K: int, D: int) -> np.ndarray:
     return np.array(sorted(pts), dtype=np.int64).reshape(-1, D)
 
 
+def spatial(K: int, D: int) -> np.ndarray:
+    """The cube over the D-1 spatial axes at zero time offset: a 3D convolution
+    of every frame of a 3D video on its own (the 3D counterpart of Sec. 7)."""
+    pts = [tuple(o) + (0,) for o in itertools.product(axis_offsets(K), repeat=D - 1)]
+    return np.array(sorted(pts), dtype=np.int64).reshape(-1, D)
+
+
 def region(name: str, K: int, D: int) -> np.ndarray:
-    return {"cube": hypercube, "cross": hypercross, "hybrid": hybrid}[name](K, D)
+    return {"cube": hypercube, "cross": hypercross, "hybrid": hybrid, "spatial": spatial}[name](K, D)
 
 
 # --------------------------------------------------------------------------- #
@@ -187,6 +195,34 @@ def conv_backward(X: np.ndarray, W: np.ndarray, dY: np.ndarray, maps: List[Pairs
         dX[I] += dY[O] @ W[k].T
         dW[k] = X[I].T @ dY[O]
     return dX, dW
+
+
+# --------------------------------------------------------------------------- #
+# Non-spatial functions (Sec. 4.5) on the output features of a convolution:
+# batch normalisation (in the per-channel affine form it takes once its
+# statistics are known) and ReLU act on each row on its own
+# --------------------------------------------------------------------------- #
+def batchnorm_coefficients(Y: np.ndarray, gamma=None, beta=None, eps: float = 1e-5):
+    """scale, shift with scale * y + shift = gamma (y - mean) / sqrt(var + eps) + beta,
+    mean and (biased) variance taken per channel over the rows of Y."""
+    Y = np.asarray(Y, dtype=np.float64)
+    C = Y.shape[1]
+    gamma = np.ones(C) if gamma is None else np.asarray(gamma, dtype=np.float64)
+    beta = np.zeros(C) if beta is None else np.asarray(beta, dtype=np.float64)
+    mean = Y.mean(axis=0)
+    var = Y.var(axis=0)
+    scale = gamma / np.sqrt(var + eps)
+    return scale, beta - mean * scale
+
+
+def affine_act(Y: np.ndarray, scale=None, shift=None, relu: bool = False) -> np.ndarray:
+    """Y * scale + shift per channel (column), then max(., 0) if relu."""
+    Z = np.array(Y, dtype=np.float64)
+    if scale is not None:
+        Z = Z * np.asarray(scale, dtype=np.float64)[None, :]
+    if shift is not None:
+        Z = Z + np.asarray(shift, dtype=np.float64)[None, :]
+    return np.maximum(Z, 0.0) if relu else Z
 
 
 # --------------------------------------------------------------------------- #

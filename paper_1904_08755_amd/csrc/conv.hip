@@ -689,6 +689,31 @@ static int launch_os(const void* X, int64_t n_x, const void* W, const int32_t* g
     return GSC_OK;
 }
 
+// The epilogue as a pass of its own over complete rows (row-form forward).
+template <typename T>
+__global__ void k_affine_act(T* __restrict__ y, int64_t n, int c, Epilogue ep) {
+    const int64_t total = n * c;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int col = (int)(i % c);
+        const float sc = ep.scale ? ep.scale[col] : 1.f;
+        const float sh = ep.shift ? ep.shift[col] : 0.f;
+        store_out(&y[i], epi_apply(to_f32(y[i]), sc, sh, ep.relu));
+    }
+}
+
+int affine_act(int dtype, void* Y, int64_t n, int c, const Epilogue& ep, hipStream_t s) {
+    const int64_t total = n * c;
+    if (total == 0) return GSC_OK;
+    const unsigned grid = (unsigned)((total + 255) / 256 < 8192 ? (total + 255) / 256 : 8192);
+    if (dtype == GSC_BF16)
+        hipLaunchKernelGGL(k_affine_act<uint16_t>, dim3(grid), dim3(256), 0, s, reinterpret_cast<uint16_t*>(Y), n, c,
+                           ep);
+    else
+        hipLaunchKernelGGL(k_affine_act<float>, dim3(grid), dim3(256), 0, s, reinterpret_cast<float*>(Y), n, c, ep);
+    GSC_LAUNCH_CHECK();
+    return GSC_OK;
+}
+
 }  // namespace gsc
 
 using namespace gsc;
@@ -724,13 +749,10 @@ int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32
     return 0;
 }
 
-int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
-                        int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
-                        const int64_t* gidx, int64_t n_pairs, const int32_t* perm, const uint32_t* bmask,
-                        const int64_t* ibase, const int32_t* items, void* Y, int64_t n_out, void* ws,
-                        size_t ws_bytes, void* stream) {
-    (void)seg;
-    clear_error();
+static int conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
+                    int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* gidx, int64_t n_pairs,
+                    const int32_t* perm, const uint32_t* bmask, const int64_t* ibase, const int32_t* items,
+                    const Epilogue& ep, void* Y, int64_t n_out, void* ws, size_t ws_bytes, hipStream_t s) {
     if (dtype != GSC_F32 && dtype != GSC_BF16) return fail(GSC_EINVAL, "conv_fwd: unknown dtype %d", dtype);
     if (n_in < 0 || n_out < 0 || n_in > INT32_MAX || n_out > INT32_MAX)
         return fail(GSC_EINVAL, "conv_fwd: bad row counts n_in=%lld n_out=%lld", (long long)n_in, (long long)n_out);
@@ -745,7 +767,6 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
     bool planned = false;
     int rc = plan_args("conv_fwd", n_out, perm, bmask, ibase, items, &planned);
     if (rc) return rc;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (planned && gsc_conv_block_engine(dtype, c_in, c_out, K) && aligned16(X) && aligned16(W) &&
         (dtype != GSC_BF16 || blk_bf16_fits(n_in, c_in))) {
         if (n_in > 0 && !X) return fail(GSC_EINVAL, "conv_fwd: X is null");
@@ -753,24 +774,57 @@ int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in
         if (dtype == GSC_BF16) {   // B_k = W[k]: the engine reads its columns, so the transposed copy
             rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
             if (rc) return rc;
-            return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s);
+            return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s, ep);
         }
         static const WSel kNoSel{};
         return conv_blk_f32(c_in, c_out, reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(W),
-                            false, kNoSel, K, plan, n_out, reinterpret_cast<float*>(Y), s);
+                            false, kNoSel, K, plan, n_out, reinterpret_cast<float*>(Y), s, ep);
     }
-    if (dtype == GSC_F32)
-        return launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
-                                              WIdentity{}, s);
-    if (fwd_uses_bf16_engine(dtype, c_in, c_out, K)) {
+    // row form: the sums are complete only once the call's kernels are done,
+    // so the epilogue is a pass of its own over Y
+    if (dtype == GSC_F32) {
+        rc = launch_os<float, float, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
+                                            WIdentity{}, s);
+    } else if (fwd_uses_bf16_engine(dtype, c_in, c_out, K)) {
         if (n_out == 0) return GSC_OK;
         rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
         if (rc) return rc;
-        return conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, nullptr, K, n_out, Y,
-                                    WIdentity{}, s);
+        rc = conv_bf16<WIdentity>(c_in, c_out, X, n_in, ws, in_idx, out_idx, gidx, nullptr, K, n_out, Y, WIdentity{},
+                                  s);
+    } else {
+        rc = launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out,
+                                                  Y, WIdentity{}, s);
     }
-    return launch_os<uint16_t, uint16_t, false>(X, n_in, W, in_idx, out_idx, gidx, nullptr, K, c_in, c_out, n_out, Y,
-                                                WIdentity{}, s);
+    if (rc || !ep.on()) return rc;
+    return affine_act(dtype, Y, n_out, c_out, ep, s);
+}
+
+int gsc_sparse_conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W, int32_t c_out,
+                        int32_t K, const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg,
+                        const int64_t* gidx, int64_t n_pairs, const int32_t* perm, const uint32_t* bmask,
+                        const int64_t* ibase, const int32_t* items, void* Y, int64_t n_out, void* ws,
+                        size_t ws_bytes, void* stream) {
+    (void)seg;
+    clear_error();
+    return conv_fwd(dtype, X, n_in, c_in, W, c_out, K, in_idx, out_idx, gidx, n_pairs, perm, bmask, ibase, items,
+                    Epilogue{}, Y, n_out, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream));
+}
+
+int gsc_sparse_conv_fwd_affine(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, const void* W,
+                               int32_t c_out, int32_t K, const int32_t* in_idx, const int32_t* out_idx,
+                               const int64_t* seg, const int64_t* gidx, int64_t n_pairs, const int32_t* perm,
+                               const uint32_t* bmask, const int64_t* ibase, const int32_t* items, const float* scale,
+                               const float* shift, int32_t act, void* Y, int64_t n_out, void* ws, size_t ws_bytes,
+                               void* stream) {
+    (void)seg;
+    clear_error();
+    if (act != GSC_ACT_NONE && act != GSC_ACT_RELU) return fail(GSC_EINVAL, "conv_fwd_affine: unknown act %d", act);
+    Epilogue ep;
+    ep.scale = scale;
+    ep.shift = shift;
+    ep.relu = act == GSC_ACT_RELU;
+    return conv_fwd(dtype, X, n_in, c_in, W, c_out, K, in_idx, out_idx, gidx, n_pairs, perm, bmask, ibase, items, ep,
+                    Y, n_out, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K) {

@@ -26,19 +26,26 @@ bool blk_f32_supported(int ca, int cb, int K);
 // Y (n_y x cb) = sum over the plan's items of X[item rows] * B_k with
 // B_k = W[k] (ca x cb) when !wt, or B_k = W[sel(k)]^T (W: K x cb x ca) when
 // wt.  Asynchronous.
+// A forward call (!wt) may carry an epilogue, applied to the sums before
+// they are stored.
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
-                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s);
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep = Epilogue{});
 
 // bf16 engine for wide layers: reduction width ca and output width cb in
 // {64, 128, 256}, K <= 32.  Y (n_y x cb, bf16) = sum over the plan's items
 // of X[item rows] * B_k, B_k[ch][col] = Bt[sel(k)][col][ch] (Bt: K x cb x ca
 // bf16: the transposed weights for the forward pass, W itself for the input
-// gradient).  Asynchronous.
+// gradient).  The forward call (Sel = WIdentity) may carry an epilogue,
+// applied to the fp32 sums before they are rounded.  Asynchronous.
 bool blk_bf16_supported(int ca, int cb, int K);
 // The engine addresses X with 32-bit byte offsets: n_x * ca below 2^30.
 bool blk_bf16_fits(int64_t n_x, int ca);
 template <typename Sel>
 int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
-                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s);
+                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s, const Epilogue& ep = Epilogue{});
+
+// Y (n x c, float32 or bf16 by dtype) = the epilogue applied in place (the
+// row-form paths, whose sums are complete only in Y).  Asynchronous.
+int affine_act(int dtype, void* Y, int64_t n, int c, const Epilogue& ep, hipStream_t s);
 
 }  // namespace gsc

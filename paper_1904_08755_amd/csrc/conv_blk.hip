@@ -71,12 +71,12 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-template <int CA, int CB, bool WT>
+template <int CA, int CB, bool WT, bool EP>
 __global__ void __launch_bounds__((BlkF32<CA, CB>::THREADS))
 k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, int K, WSel sel,
                const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
                const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
-               float* __restrict__ Y) {
+               Epilogue ep, float* __restrict__ Y) {
     using C = BlkF32<CA, CB>;
     __shared__ float wl[kBlkLdsBytes / 4];
     // Weights in fragment order: lane (c, q) of offset k needs, for MFMA step
@@ -130,6 +130,13 @@ k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict
     const int64_t NW = (int64_t)gridDim.x * C::WAVES;
     const int64_t gw = (int64_t)blockIdx.x * C::WAVES + wave;
     const float4* wq = reinterpret_cast<const float4*>(wl) + lane;
+    // epilogue coefficients of the lane's output columns 16j + r16
+    float esc[C::NNB], esh[C::NNB];
+#pragma unroll
+    for (int j = 0; j < C::NNB; ++j) {
+        esc[j] = EP && ep.scale ? ep.scale[16 * j + r16] : 1.f;
+        esh[j] = EP && ep.shift ? ep.shift[16 * j + r16] : 0.f;
+    }
 
     for (int64_t c0 = gw; c0 < nb; c0 += 64 * NW) {
         // this chunk: the wave's blocks c0 + l*NW, one per lane l
@@ -237,7 +244,9 @@ k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict
                     const int64_t pos = (int64_t)mt[p].b * 16 + 4 * q + i;
                     if (pos < n_y && row >= 0 && row < n_y) {
 #pragma unroll
-                        for (int j = 0; j < C::NNB; ++j) Y[(int64_t)row * CB + 16 * j + r16] = acc[j][i];
+                        for (int j = 0; j < C::NNB; ++j)
+                            Y[(int64_t)row * CB + 16 * j + r16] =
+                                EP ? epi_apply(acc[j][i], esc[j], esh[j], ep.relu) : acc[j][i];
                     }
                 }
 #pragma unroll
@@ -336,12 +345,12 @@ struct BfGroup {
     bool valid;
 };
 
-template <int CA, int CB, typename Sel>
+template <int CA, int CB, typename Sel, bool EP>
 __global__ void __launch_bounds__(kBfThreads, 2)
 k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __restrict__ Bt, int K, Sel sel,
                 const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
                 const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
-                int cb_full, int64_t ntiles, uint16_t* __restrict__ Y) {
+                int cb_full, int64_t ntiles, Epilogue ep, uint16_t* __restrict__ Y) {
     using C = BlkBf16<CA, CB>;
     __shared__ __attribute__((aligned(16))) uint8_t slab[2][kBfT][16 * 128];   // [group parity][block][row][128 B]
     __shared__ int32_t idx_s[kBfIdxInts];
@@ -547,6 +556,14 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
     static_assert(64 * CB * 2 <= (int)sizeof(slab), "a pass of 64 positions fits the slabs");
     uint32_t* out_s = reinterpret_cast<uint32_t*>(&slab[0][0][0]);
     const bool odd = r16 & 1;
+    // epilogue coefficients of the lane's output columns (before rounding to bf16)
+    float esc[C::NB], esh[C::NB];
+#pragma unroll
+    for (int j = 0; j < C::NB; ++j) {
+        const int col = col0 + wave * C::NC + 16 * j + r16;
+        esc[j] = EP && ep.scale ? ep.scale[col] : 1.f;
+        esh[j] = EP && ep.shift ? ep.shift[col] : 0.f;
+    }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
         if (half) __syncthreads();   // the first pass has been read
@@ -554,7 +571,11 @@ k_conv_blk_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __r
         for (int b = 4 * half; b < 4 * half + 4; ++b)
 #pragma unroll
             for (int j = 0; j < C::NB; ++j) {
-                const floatx4 v = acc[b][j];
+                floatx4 v = acc[b][j];
+                if constexpr (EP) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = epi_apply(v[i], esc[j], esh[j], ep.relu);
+                }
                 const float e0 = xor1(odd ? v[0] : v[2]);
                 const float e1 = xor1(odd ? v[1] : v[3]);
                 const uint32_t p0 = odd ? pack_bf16(e0, v[2]) : pack_bf16(v[0], e0);
@@ -585,11 +606,19 @@ bool blk_bf16_fits(int64_t n_x, int ca) { return n_x >= 0 && n_x * ca < ((int64_
 
 template <int CA, int CB, typename Sel>
 static void launch_blk_bf16(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
-                            const BlockPlan& p, int64_t nb, int64_t n_y, int cb_full, uint16_t* Y, hipStream_t s) {
+                            const BlockPlan& p, int64_t nb, int64_t n_y, int cb_full, const Epilogue& ep, uint16_t* Y,
+                            hipStream_t s) {
     const int64_t tiles = (nb + kBfT - 1) / kBfT;
     const int64_t grid = 8 * (int64_t)(cb_full / CB) * ((tiles + 7) / 8);
-    hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel>), dim3((unsigned)grid), dim3(kBfThreads), 0, s, X, n_x, Bt, K,
-                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, cb_full, tiles, Y);
+    if constexpr (std::is_same<Sel, WIdentity>::value) {   // the epilogue is a forward-pass option
+        if (ep.on()) {
+            hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel, true>), dim3((unsigned)grid), dim3(kBfThreads), 0, s, X,
+                               n_x, Bt, K, sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, cb_full, tiles, ep, Y);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((k_conv_blk_bf16<CA, CB, Sel, false>), dim3((unsigned)grid), dim3(kBfThreads), 0, s, X, n_x,
+                       Bt, K, sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, cb_full, tiles, ep, Y);
 }
 
 __global__ void k_zero_u16(uint16_t* __restrict__ y, int64_t n) {
@@ -599,8 +628,10 @@ __global__ void k_zero_u16(uint16_t* __restrict__ y, int64_t n) {
 
 template <typename Sel>
 int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
-                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s) {
+                  const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s, const Epilogue& ep) {
     if (!blk_bf16_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no bf16 block engine for %dx%d, K=%d", ca, cb, K);
+    if (ep.on() && !std::is_same<Sel, WIdentity>::value)
+        return fail(GSC_EINVAL, "conv: the epilogue applies to the forward pass only");
     if (!blk_bf16_fits(n_x, ca)) return fail(GSC_EINVAL, "conv: bf16 block engine takes at most 2^30 input elements");
     const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
     if (nb == 0) return GSC_OK;
@@ -610,7 +641,7 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
         hipLaunchKernelGGL(k_zero_u16, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256),
                            0, s, Y16, n);
         GSC_LAUNCH_CHECK();
-        return GSC_OK;
+        return ep.on() ? affine_act(GSC_BF16, Y16, n_y, cb, ep, s) : GSC_OK;
     }
     auto X16 = reinterpret_cast<const uint16_t*>(X);
     auto B16 = reinterpret_cast<const uint16_t*>(Bt);
@@ -619,7 +650,7 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
     // (two waves per SIMD), where one 256-column workgroup holds a CU alone
 #define GSC_BFB_CASE(A, B, S)                                                         \
     if (ca == A && cb == B) {                                                         \
-        launch_blk_bf16<A, S, Sel>(X16, n_x, B16, K, sel, plan, nb, n_y, B, Y16, s); \
+        launch_blk_bf16<A, S, Sel>(X16, n_x, B16, K, sel, plan, nb, n_y, B, ep, Y16, s); \
         GSC_LAUNCH_CHECK();                                                           \
         return GSC_OK;                                                                \
     }
@@ -631,9 +662,9 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
 }
 
 template int conv_blk_bf16<WIdentity>(int, int, const void*, int64_t, const void*, const WIdentity&, int,
-                                      const BlockPlan&, int64_t, void*, hipStream_t);
+                                      const BlockPlan&, int64_t, void*, hipStream_t, const Epilogue&);
 template int conv_blk_bf16<WSel>(int, int, const void*, int64_t, const void*, const WSel&, int, const BlockPlan&,
-                                 int64_t, void*, hipStream_t);
+                                 int64_t, void*, hipStream_t, const Epilogue&);
 
 bool blk_f32_supported(int ca, int cb, int K) {
     auto ok = [](int c) { return c == 16 || c == 32 || c == 64; };
@@ -652,20 +683,21 @@ static int device_cus() {
     return cus[dev];
 }
 
-template <int CA, int CB, bool WT>
+template <int CA, int CB, bool WT, bool EP>
 static void launch_blk_f32(const float* X, int64_t n_x, const float* W, const WSel& sel, int K, const BlockPlan& p,
-                           int64_t nb, int64_t n_y, float* Y, hipStream_t s) {
+                           int64_t nb, int64_t n_y, const Epilogue& ep, float* Y, hipStream_t s) {
     using C = BlkF32<CA, CB>;
     int64_t grid = (nb + C::WAVES - 1) / C::WAVES;
     const int cus = device_cus();
     if (grid > cus) grid = cus;
-    hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X, n_x, W, K, sel,
-                       p.perm, p.bmask, p.ibase, p.items, nb, n_y, Y);
+    hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT, EP>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X, n_x, W, K,
+                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, Y);
 }
 
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
-                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s) {
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep) {
     if (!blk_f32_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no fp32 block engine for %dx%d, K=%d", ca, cb, K);
+    if (ep.on() && wt) return fail(GSC_EINVAL, "conv: the epilogue applies to the forward pass only");
     const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
     if (nb == 0) return GSC_OK;
     if (n_x == 0) {   // no input rows to read (the engine always issues its row loads)
@@ -673,14 +705,16 @@ int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bo
         hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256),
                            0, s, Y, n);
         GSC_LAUNCH_CHECK();
-        return GSC_OK;
+        return ep.on() ? affine_act(GSC_F32, Y, n_y, cb, ep, s) : GSC_OK;
     }
 #define GSC_BLK_CASE(A, B)                                                                  \
     if (ca == A && cb == B) {                                                               \
         if (wt)                                                                             \
-            launch_blk_f32<A, B, true>(X, n_x, W, sel, K, plan, nb, n_y, Y, s);              \
+            launch_blk_f32<A, B, true, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);   \
+        else if (ep.on())                                                                   \
+            launch_blk_f32<A, B, false, true>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);   \
         else                                                                                \
-            launch_blk_f32<A, B, false>(X, n_x, W, sel, K, plan, nb, n_y, Y, s);             \
+            launch_blk_f32<A, B, false, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);  \
         GSC_LAUNCH_CHECK();                                                                 \
         return GSC_OK;                                                                      \
     }

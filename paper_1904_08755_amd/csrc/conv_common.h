@@ -18,6 +18,23 @@ struct WIdentity {
     __device__ __forceinline__ int operator()(int k) const { return k; }
 };
 
+// Per-output-channel affine map and activation applied to a convolution's
+// fp32 sums before they are stored: y[c] = act(sum[c] * scale[c] + shift[c])
+// (batch normalisation in its inference form followed by a ReLU: non-spatial
+// functions of Sec. 4.5 fused into the kernel that produces the rows).
+struct Epilogue {
+    const float* scale = nullptr;   // null: 1
+    const float* shift = nullptr;   // null: 0
+    int relu = 0;
+    bool on() const { return scale || shift || relu; }
+};
+
+// NaN propagates through the ReLU (a NaN sum is not clipped to 0)
+__device__ __forceinline__ float epi_apply(float v, float sc, float sh, int relu) {
+    v = fmaf(v, sc, sh);
+    return relu && v < 0.f ? 0.f : v;
+}
+
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
 

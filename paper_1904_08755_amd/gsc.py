@@ -61,6 +61,8 @@ _SIGS = {
     "gsc_conv_fwd_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "gsc_sparse_conv_fwd": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64,
                                            _vp, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "gsc_sparse_conv_fwd_affine": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64,
+                                                  _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _vp, _sz, _vp]),
     "gsc_conv_bwd_ws_bytes": (_sz, [_i64, _i32, _i32, _i32]),
     "gsc_sparse_conv_bwd": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _vp,
                                            _vp, _vp, _vp, _i64, _c_i32p, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp,
@@ -344,8 +346,7 @@ def gsc_conv_fwd_ws_bytes(dtype: int, c_in: int, c_out: int, K: int) -> int:
     return int(lib().gsc_conv_fwd_ws_bytes(dtype, c_in, c_out, K))
 
 
-def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out: Optional[int] = None,
-                        Y: Optional[torch.Tensor] = None, stream=None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+def _fwd_args(X, W, kmap, n_out, Y, ws):
     dt = _dt(X)
     _need(X, X.dtype, "X", 2)
     _need(W, X.dtype, "W", 3)
@@ -361,10 +362,38 @@ def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out
     need = gsc_conv_fwd_ws_bytes(dt, ci, co, K)
     if ws is None and need > 0:
         ws = _ws(need, X.device)
-    _check(lib().gsc_sparse_conv_fwd(dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx),
-                                     _ptr(kmap.out_idx), _ptr(kmap.seg), _ptr(kmap.gidx), kmap.n_bound,
-                                     *_plan_ptrs(kmap), _ptr(Y),
-                                     n_out, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+    head = (dt, _ptr(X), X.shape[0], ci, _ptr(W), co, K, _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg),
+            _ptr(kmap.gidx), kmap.n_bound, *_plan_ptrs(kmap))
+    return head, Y, n_out, ws
+
+
+def gsc_sparse_conv_fwd(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap, n_out: Optional[int] = None,
+                        Y: Optional[torch.Tensor] = None, stream=None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    head, Y, n_out, ws = _fwd_args(X, W, kmap, n_out, Y, ws)
+    _check(lib().gsc_sparse_conv_fwd(*head, _ptr(Y), n_out, _ptr(ws), 0 if ws is None else ws.numel(),
+                                     _stream(stream)))
+    return Y
+
+
+GSC_ACT_NONE, GSC_ACT_RELU = 0, 1
+
+
+def gsc_sparse_conv_fwd_affine(X: torch.Tensor, W: torch.Tensor, kmap: KernelMap,
+                               scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None,
+                               relu: bool = False, n_out: Optional[int] = None, Y: Optional[torch.Tensor] = None,
+                               stream=None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Y = act(conv(X) * scale + shift), per output channel (float32 scale and
+    shift of c_out values on X's device, each optional)."""
+    co = W.shape[2]
+    for name, v in (("scale", scale), ("shift", shift)):
+        if v is not None:
+            _need(v, torch.float32, name, 1)
+            if v.shape[0] != co:
+                raise ValueError(f"{name} needs {co} values")
+    head, Y, n_out, ws = _fwd_args(X, W, kmap, n_out, Y, ws)
+    _check(lib().gsc_sparse_conv_fwd_affine(*head, _ptr(scale), _ptr(shift), GSC_ACT_RELU if relu else GSC_ACT_NONE,
+                                            _ptr(Y), n_out, _ptr(ws), 0 if ws is None else ws.numel(),
+                                            _stream(stream)))
     return Y
 
 

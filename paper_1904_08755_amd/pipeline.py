@@ -76,9 +76,13 @@ class StepResult:
 class StepPlan:
     """Buffers for repeated passes over one device workload."""
 
-    def __init__(self, dw: DeviceWorkload, use_plan: bool = True):
+    def __init__(self, dw: DeviceWorkload, use_plan: bool = True, epilogue=None):
+        """``epilogue``: optional (scale, shift) float32 device tensors of c_out
+        values; the forward pass of a single-layer workload then applies
+        relu(Y * scale + shift) as it writes Y (gsc_sparse_conv_fwd_affine)."""
         self.dw = dw
         self.use_plan = use_plan
+        self.epilogue = epilogue
         self.plans: List[gsc.KernelMap] = []
         wl = dw.wl
         self.kinds = [L.kind for L in wl.layers]
@@ -167,12 +171,18 @@ class StepPlan:
                 dxmap = fmap if self.symmetric else gsc.gsc_conv_plan(tmap, self.tpb, stream=stream)
                 self.plans = [fmap]
             mark("plan")
-            Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], fmap, Y=self.Y, stream=stream, ws=self.ws_fwd)
+            if self.epilogue is None:
+                Y = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], fmap, Y=self.Y, stream=stream, ws=self.ws_fwd)
+            else:
+                Y = gsc.gsc_sparse_conv_fwd_affine(dw.X, dw.Ws[0], fmap, *self.epilogue, relu=True, Y=self.Y,
+                                                   stream=stream, ws=self.ws_fwd)
             mark("fwd")
             dX, dW = gsc.gsc_sparse_conv_bwd(dw.X, dw.Ws[0], dw.dY, fmap, dxmap, None, dX=self.dX, dW=self.dW,
                                              ws=self.ws_bwd, stream=stream, host_wsel=self.host_wsel)
             mark("bwd")
             return StepResult(None, [kmap], [Y], dX, [dW], [])
+        if self.epilogue is not None:
+            raise ValueError("the epilogue option covers single-layer workloads")
         L0 = dw.wl.layers[0]
         offs = dw.offsets[0]
         gsc.gsc_coords_build(dw.coords, self.table, stream=stream, sync=False)

@@ -3,7 +3,9 @@
 Sec. 3.1 defines the generalized sparse convolution over an arbitrary offset
 set N^D; the hypercube V^D(K) is the usual one (V^1(3) = {-1, 0, 1}).  Sec. 5.1
 and Fig. 3 name the cross / hypercross and the hybrid kernel (a spatial cube
-at zero time offset plus a temporal cross).  The library takes the offsets
+at zero time offset plus a temporal cross).  The spatial region (the cube of
+the first D - 1 axes at zero offset on the last) is the 3D convolution applied
+to every frame of a 3D video on its own, the 3D counterpart of Sec. 7.  The library takes the offsets
 as a K x D array, so every region is just a different list; the order of the
 list fixes which weight matrix W[k] belongs to which offset.  Lists here are
 in lexicographic order of the offset tuples (last axis fastest).  For even
@@ -41,8 +43,13 @@ def hybrid(K: int, D: int) -> np.ndarray:
     return np.array(sorted(s), dtype=np.int32).reshape(-1, D)
 
 
+def spatial(K: int, D: int) -> np.ndarray:
+    return np.array([tuple(o) + (0,) for o in itertools.product(_axis(K), repeat=D - 1)],
+                    dtype=np.int32).reshape(-1, D)
+
+
 def region(name: str, K: int, D: int) -> np.ndarray:
-    return {"cube": hypercube, "cross": hypercross, "hybrid": hybrid}[name](K, D)
+    return {"cube": hypercube, "cross": hypercross, "hybrid": hybrid, "spatial": spatial}[name](K, D)
 
 
 def is_symmetric(offsets: np.ndarray) -> bool:

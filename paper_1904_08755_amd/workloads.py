@@ -152,7 +152,7 @@ class Layer:
     kind: "subm" (output coordinates = input coordinates), "down" (strided,
     output coordinates derived from the input by the stride) or "up" (the
     transposed convolution back to the coordinates of the matching "down").
-    region: "cube" (hypercube of side ``ksize``), "cross" or "hybrid".
+    region: "cube" (hypercube of side ``ksize``), "cross", "hybrid" or "spatial".
     """
     kind: str
     region: str
@@ -190,6 +190,8 @@ def _region_size(region: str, ksize: int, D: int) -> int:
         return 2 * D * ((ksize - 1) // 2) + 1
     if region == "hybrid":
         return ksize ** (D - 1) + 2
+    if region == "spatial":
+        return ksize ** (D - 1)
     raise ValueError(region)
 
 
@@ -234,10 +236,13 @@ def scene_coords(cid: int, batch: int, scale: float, voxel: float, n_points: int
     return unique_rows(np.concatenate(rows, axis=0)), npts
 
 
-def make_workload(cid: int, scale: float = 1.0) -> Workload:
+def make_workload(cid: int, scale: float = 1.0, region: Optional[str] = None) -> Workload:
     """Workload ``cid`` (0..4).  ``scale`` < 1 shrinks the scene (room, boxes and
     point count) for quick checks while keeping its structure; it is ignored for
-    workload 0, which is already small."""
+    workload 0, which is already small.  ``region`` replaces the region of the 3D
+    video (workload 3): "cube" gives the full 3^4 tesseract (81 offsets) that the
+    hybrid kernel of Sec. 5.1 is a cheaper stand-in for, "spatial" the 3^3 cube
+    at zero time offset (27 offsets: every frame convolved on its own)."""
     dtype = "bf16" if cid == 4 else "f32"
     npts: List[int] = []
     if cid == 0:
@@ -259,7 +264,7 @@ def make_workload(cid: int, scale: float = 1.0) -> Workload:
     elif cid == 3:
         coords, npts = scene_coords(cid, 1, scale, 0.05, SCENE_POINTS_5CM, frames=3)
         D = 4
-        specs = [("subm", "hybrid", 3, 1, 32, 32)]
+        specs = [("subm", region or "hybrid", 3, 1, 32, 32)]
     else:
         raise ValueError(cid)
 
@@ -274,7 +279,10 @@ def make_workload(cid: int, scale: float = 1.0) -> Workload:
     # single strided layer; no workload ends on a "down" layer.
     assert layers[-1].kind != "down"
     dY, dYb = _as_dtype(rng_for(cid, S_GRAD).standard_normal((N, layers[-1].c_out)).astype(np.float32), dtype)
-    return Workload(cid, CONFIG_NAMES[cid], D, dtype, coords, X, Xb, layers, dY, dYb, npts)
+    name = CONFIG_NAMES[cid]
+    if region is not None and cid == 3 and region != "hybrid":
+        name = f"video4d_5cm_t3_c32_{'tesseract' if region == 'cube' else region}{layers[0].W.shape[0]}"
+    return Workload(cid, name, D, dtype, coords, X, Xb, layers, dY, dYb, npts)
 
 
 def random_coords(seed: int, n: int, D: int, lo: int, hi: int, batch: int = 1) -> np.ndarray:

@@ -172,10 +172,16 @@ def test_plan_validation(L):
     rc = L.gsc_sparse_conv_fwd(0, fake, 10, 16, fake, 16, 27, fake, fake, fake, fake, 10, fake, None, fake, fake,
                                fake, 10, None, 0, None)
     assert rc == gsc.GSC_EINVAL and "plan" in _err(L)
+    # the affine forward validates its activation and then as the plain forward
+    aff = lambda act, K=27: L.gsc_sparse_conv_fwd_affine(0, fake, 10, 16, fake, 16, K, fake, fake, fake, fake, 10,
+                                                         None, None, None, None, fake, fake, act, fake, 10, None, 0,
+                                                         None)
+    assert aff(2) == gsc.GSC_EINVAL and "act" in _err(L)
+    assert aff(1, K=0) == gsc.GSC_EINVAL and "K=0" in _err(L)
 
 
 @pytest.mark.parametrize("name,K,D", [("cube", 3, 3), ("cube", 2, 3), ("cube", 5, 4), ("cross", 5, 3),
-                                      ("hybrid", 3, 4), ("cube", 3, 7)])
+                                      ("hybrid", 3, 4), ("spatial", 3, 4), ("cube", 3, 7)])
 def test_regions_match_oracle(name, K, D):
     assert np.array_equal(regions.region(name, K, D), O.region(name, K, D))
 

@@ -419,6 +419,7 @@ def test_4d_hybrid_and_tesseract():
     coords = WL.random_coords(77, 3000, 4, -5, 5, batch=1)
     _conv_case(coords, 8, 8, regions.hybrid(3, 4), 77)
     _conv_case(coords, 8, 8, regions.hypercube(3, 4), 78)
+    _conv_case(coords, 8, 8, regions.spatial(3, 4), 79)
 
 
 def test_dilated_kernel():
@@ -650,3 +651,83 @@ def test_quantize_random_and_scene():
         bs.append(np.full(len(p), bi, np.int32))
     q = _quant_compare(np.concatenate(pts), np.concatenate(bs), 0.02, None)
     _say(f"  scene points {sum(len(p) for p in pts)} -> voxels {q.coords.shape[0]}")
+
+
+# --------------------------------------------------------------------------- #
+# forward with the per-channel affine map and ReLU fused (Sec. 4.5)
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("dtype,ci,co,region,planned", [
+    ("f32", 32, 32, "cube3", True), ("f32", 16, 64, "cube2", True), ("f32", 32, 32, "cube3", False),
+    ("f32", 3, 16, "cube3", False), ("bf16", 256, 256, "cube3", True), ("bf16", 64, 128, "cube2", True),
+    ("bf16", 256, 256, "cube3", False), ("bf16", 48, 80, "cube3", False)])
+@pytest.mark.parametrize("mode", ["bn_relu", "scale_only", "shift_relu", "none"])
+def test_conv_affine_epilogue(dtype, ci, co, region, planned, mode):
+    """gsc_sparse_conv_fwd_affine against the oracle's convolution followed by
+    batch normalisation (coefficients from the oracle's batch statistics) and
+    ReLU; with no coefficients and no activation it is the plain forward."""
+    _say(f"[gpu] affine epilogue {dtype} {ci}->{co} {region} planned={planned} {mode}")
+    coords = WL.random_coords(160 + ci + co, 2600, 3, -12, 12, batch=2)
+    offs = regions.hypercube(int(region[-1]), 3)
+    X, Xb = WL.random_features(161, len(coords), ci, dtype)
+    W, Wb = WL.random_weights(162, len(offs), ci, co, dtype)
+    if dtype == "bf16":
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tX, tW = dev(Xb), dev(Wb)
+    else:
+        tX, tW = _t(X, torch.float32), _t(W, torch.float32)
+    table = gsc.gsc_coords_build(_t(coords))
+    km = gsc.gsc_kernel_map(table, _t(coords), offs, dense=planned)
+    if planned:
+        km = gsc.gsc_conv_plan(km)
+        assert gsc.gsc_conv_block_engine(gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32, ci, co, len(offs))
+    m = O.kernel_map(coords, coords, np.asarray(offs))
+    S = O.conv_forward(X, W, m, len(coords))
+    rng = np.random.default_rng(163)
+    scale, shift = O.batchnorm_coefficients(S, rng.uniform(0.5, 2.0, co), rng.uniform(-0.5, 0.5, co))
+    scale, shift = scale.astype(np.float32), shift.astype(np.float32)
+    relu = mode in ("bn_relu", "shift_relu")
+    sc = scale if mode in ("bn_relu", "scale_only") else None
+    sh = shift if mode in ("bn_relu", "shift_relu") else None
+    Y = gsc.gsc_sparse_conv_fwd_affine(tX, tW, km, None if sc is None else _t(sc, torch.float32),
+                                       None if sh is None else _t(sh, torch.float32), relu=relu)
+    torch.cuda.synchronize()
+    ref = O.affine_act(S, sc, sh, relu)
+    got = to_np(Y)
+    assert rel_err(got, ref) <= TOL[dtype]
+    if relu:
+        assert np.all(got >= 0)
+    if mode == "none":
+        # the block engines add in a fixed order; the general row-form kernel
+        # does not, so there only the tolerance holds between two calls
+        plain = gsc.gsc_sparse_conv_fwd(tX, tW, km)
+        torch.cuda.synchronize()
+        if planned:
+            assert torch.equal(plain, Y)
+        else:
+            assert rel_err(got, to_np(plain)) <= TOL[dtype]
+
+
+def test_conv_affine_no_input_rows():
+    """Outputs that no input reaches hold act(shift); an input with no rows
+    gives the same through the engines' zero fill."""
+    cin = np.array([[0, 100, 100, 100], [0, 101, 100, 100]], np.int32)
+    cout = np.array([[0, 0, 0, 0], [0, 1, 1, 1], [0, 100, 100, 99]], np.int32)
+    shift = np.linspace(-1, 1, 32).astype(np.float32)
+    for planned in (False, True):
+        km = gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(cin)), _t(cout), regions.hypercube(3, 3), dense=planned)
+        km = gsc.gsc_conv_plan(km) if planned else km
+        X = _t(WL.random_features(171, 2, 16)[0], torch.float32)
+        W = _t(WL.random_weights(172, 27, 16, 32)[0], torch.float32)
+        Y = gsc.gsc_sparse_conv_fwd_affine(X, W, km, None, _t(shift, torch.float32), relu=True)
+        torch.cuda.synchronize()
+        ref = O.affine_act(O.conv_forward(to_np(X), to_np(W), O.kernel_map(cin, cout, O.hypercube(3, 3)), 3),
+                           None, shift, True)
+        assert rel_err(to_np(Y), ref) <= TOL["f32"]
+        assert np.array_equal(to_np(Y)[:2], np.broadcast_to(np.maximum(shift, 0), (2, 32)))
+    km0 = gsc.gsc_conv_plan(gsc.gsc_kernel_map(gsc.gsc_coords_build(torch.empty((0, 4), dtype=torch.int32,
+                                                                                device=DEV)),
+                                               _t(cout), regions.hypercube(3, 3), dense=True))
+    Y0 = gsc.gsc_sparse_conv_fwd_affine(torch.empty((0, 16), device=DEV), W, km0, None, _t(shift, torch.float32),
+                                        relu=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(Y0), np.broadcast_to(np.maximum(shift, 0), (3, 32)))

@@ -16,7 +16,9 @@ computed by means that share nothing with the oracle's own code.
   overlapping size-3 window at stride 2, their autograd gradients, and
   per-batch torch reductions for global pooling;
 * quantization (Sec. 4.1, Alg. 1): a hand-written example (golden file) and
-  np.unique over the floored rows.
+  np.unique over the floored rows;
+* batch normalisation and ReLU after a convolution (Sec. 4.5): torch's
+  batch_norm with batch statistics and the moments of the normalised columns.
 
 The planted-mistake tests at the end check that each pin fails for a
 plausible error in the oracle (sign of the offset, a transposed weight, a
@@ -137,6 +139,9 @@ def test_regions_structure():
     hyb = O.hybrid(3, 4)
     assert sum(1 for o in hyb if o[3] != 0) == 2
     assert all(o[:3].tolist() == [0, 0, 0] for o in hyb if o[3] != 0)
+    sp = O.spatial(3, 4)
+    assert {tuple(o) for o in sp.tolist()} == {o + (0,) for o in itertools.product((-1, 0, 1), repeat=3)}
+    assert {tuple(o) for o in hyb.tolist()} == {tuple(o) for o in sp.tolist()} | {(0, 0, 0, -1), (0, 0, 0, 1)}
     assert O.axis_offsets(2) == [0, 1]
 
 
@@ -632,3 +637,32 @@ def test_quantize_vs_numpy_unique():
     # voxels on either side of 0
     trunc = np.concatenate([b[:, None], np.trunc(P / np.float32(0.25)).astype(np.int64)], 1)
     assert len(np.unique(trunc, axis=0)) != len(u)
+
+
+# --------------------------------------------------------------------------- #
+# non-spatial functions fused after the convolution (Sec. 4.5)
+# --------------------------------------------------------------------------- #
+def test_batchnorm_relu_vs_torch():
+    """Batch normalisation with batch statistics through torch's batch_norm
+    (training mode, float64) and its ReLU, against the oracle's per-channel
+    affine form of it; the normalised columns have mean 0 and variance
+    var / (var + eps)."""
+    rng = np.random.default_rng(11)
+    Y = rng.standard_normal((500, 24)) * rng.uniform(0.5, 3.0, 24) + rng.uniform(-2, 2, 24)
+    gamma, beta, eps = rng.uniform(0.5, 2.0, 24), rng.uniform(-1, 1, 24), 1e-3
+    scale, shift = O.batchnorm_coefficients(Y, gamma, beta, eps)
+    ref = F.batch_norm(torch.from_numpy(Y), None, None, torch.from_numpy(gamma), torch.from_numpy(beta),
+                       training=True, eps=eps).numpy()
+    assert np.allclose(O.affine_act(Y, scale, shift), ref, rtol=0, atol=1e-12)
+    assert np.allclose(O.affine_act(Y, scale, shift, relu=True), torch.relu(torch.from_numpy(ref)).numpy(),
+                       rtol=0, atol=1e-12)
+    s0, h0 = O.batchnorm_coefficients(Y, eps=eps)
+    Z = O.affine_act(Y, s0, h0)
+    assert np.allclose(Z.mean(axis=0), 0, atol=1e-12)
+    assert np.allclose(Z.var(axis=0), Y.var(axis=0) / (Y.var(axis=0) + eps), rtol=1e-12)
+    # identity when neither coefficient is given; ReLU splits x = relu(x) - relu(-x)
+    assert np.array_equal(O.affine_act(Y), Y)
+    assert np.allclose(O.affine_act(Y, relu=True) - O.affine_act(-Y, relu=True), Y, rtol=0, atol=0)
+    # a planted mistake: the unbiased variance (n - 1) misses torch's normalisation
+    bad = (Y - Y.mean(0)) / np.sqrt(Y.var(axis=0, ddof=1) + eps) * gamma + beta
+    assert not np.allclose(bad, ref, rtol=0, atol=1e-6)
