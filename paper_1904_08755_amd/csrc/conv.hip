@@ -370,15 +370,27 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
 // offsets' sizes (the centre offset of a submanifold map has one pair per
 // row, the others far fewer).
 __global__ void k_dw_items(const int64_t* seg, int K, int64_t ch, int64_t* ibase, int64_t* chunk) {
-    if (blockIdx.x != 0 || threadIdx.x != 0) return;
-    int64_t t = 0;
-    for (int k = 0; k < K; ++k) {
-        const int64_t n = seg[k + 1] - seg[k];
-        ibase[k] = t;
-        chunk[k] = ch;
-        t += n > 0 ? (n + ch - 1) / ch : 0;
+    // one wave: 64 offsets per round, their item counts scanned with shuffles
+    if (blockIdx.x != 0 || threadIdx.x >= 64) return;
+    const int lane = threadIdx.x;
+    int64_t carry = 0;
+    for (int k0 = 0; k0 < K; k0 += 64) {
+        const int k = k0 + lane;
+        const int64_t n = k < K ? seg[k + 1] - seg[k] : 0;
+        const int64_t c = n > 0 ? (n + ch - 1) / ch : 0;
+        int64_t inc = c;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int64_t u = __shfl_up(inc, d, 64);
+            if (lane >= d) inc += u;
+        }
+        if (k < K) {
+            ibase[k] = carry + inc - c;
+            chunk[k] = ch;
+        }
+        carry += __shfl(inc, 63, 64);
     }
-    ibase[K] = t;
+    if (lane == 0) ibase[K] = carry;
 }
 
 // Per-wave partial tiles are summed in wave order (deterministic), then stored.

@@ -75,14 +75,29 @@ __global__ void __launch_bounds__(kThreads) k_bbox(const int32_t* coords, int64_
     load_row(coords, 0, ncol, st, v0);   // n > 0 here
     bool out_of_range = false;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += stride) {
-        int64_t v[kMaxCols];
-        load_row(coords, r, ncol, st, v);
-        for (int c = 0; c < ncol; ++c) {
-            out_of_range |= v[c] < INT_MIN || v[c] > INT_MAX;   // strided value left int32
-            lo[c] = v[c] < lo[c] ? v[c] : lo[c];
-            hi[c] = v[c] > hi[c] ? v[c] : hi[c];
-            vary[c] |= (int)(v[c] ^ v0[c]);
+    // kBboxRows rows per thread and round, all loaded before any is used
+    constexpr int kBboxRows = 4;
+    for (int64_t r0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r0 < n; r0 += kBboxRows * stride) {
+        int32_t raw[kBboxRows][kMaxCols];
+#pragma unroll
+        for (int i = 0; i < kBboxRows; ++i) {
+            const int64_t r = r0 + i * stride;
+            const int64_t rr = r < n ? r : r0;   // a row past the end repeats the first one
+#pragma unroll
+            for (int c = 0; c < kMaxCols; ++c) raw[i][c] = c < ncol ? coords[rr * ncol + c] : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < kBboxRows; ++i) {
+#pragma unroll
+            for (int c = 0; c < kMaxCols; ++c) {
+                if (c >= ncol) break;
+                int64_t x = raw[i][c];
+                if (st.on && c > 0) x = floor_mul(x, st.s[c]);
+                out_of_range |= x < INT_MIN || x > INT_MAX;   // strided value left int32
+                lo[c] = x < lo[c] ? x : lo[c];
+                hi[c] = x > hi[c] ? x : hi[c];
+                vary[c] |= (int)(x ^ v0[c]);
+            }
         }
     }
     if (out_of_range) atomicOr(&h->status, ST_RANGE);

@@ -272,17 +272,21 @@ __global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, in
     const bool valid = j < n_out;
     const int64_t g = j >> 6;
     const unsigned long long below = lanemask_lt();
-    constexpr int B = 8;   // offsets whose table entries are loaded together
+    constexpr int B = 8;   // offsets whose table entries (and group starts) are loaded together
     for (int k0 = 0; k0 < K; k0 += B) {
         int32_t r[B];
+        int64_t gs[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) r[b] = valid && k0 + b < K ? nbr[(int64_t)(k0 + b) * n_out + j] : -1;
+        for (int b = 0; b < B; ++b) {
+            r[b] = valid && k0 + b < K ? nbr[(int64_t)(k0 + b) * n_out + j] : -1;
+            gs[b] = g < G && k0 + b < K ? gidx[(int64_t)(k0 + b) * G + g] : 0;
+        }
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const bool hit = r[b] >= 0;
             const unsigned long long m = __ballot(hit);
             if (hit) {
-                const int64_t pos = gidx[(int64_t)(k0 + b) * G + g] + __popcll(m & below);
+                const int64_t pos = gs[b] + __popcll(m & below);
                 if (pos < cap) {
                     in_idx[pos] = r[b];
                     out_idx[pos] = (int32_t)j;

@@ -46,8 +46,14 @@ static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 // ---------------------------------------------------------------------------
 // masks from the dense map
 // ---------------------------------------------------------------------------
+// (Also clears the sort's counters and first look-back entries, zero[0, nzero),
+// which the histogram kernel after it starts to fill.)
 __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int K,
-                                                             uint32_t* __restrict__ keys) {
+                                                             uint32_t* __restrict__ keys, uint32_t* __restrict__ zero,
+                                                             int64_t nzero) {
+    for (int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x; i < nzero;
+         i += (int64_t)gridDim.x * kPlanThreads)
+        zero[i] = 0;
     const int64_t j = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
     if (j >= n) return;
     uint32_t m = 0;
@@ -80,11 +86,6 @@ constexpr uint32_t kStIncl = 1u << 31;            // entry holds the inclusive p
 constexpr uint32_t kStCount = kStAgg - 1;
 constexpr int64_t kRsMaxKeys = kStCount;          // counts must fit below the flag bits
 constexpr int kSpinMax = 1 << 22;                 // bound on polls of one entry (never reached)
-
-__global__ void k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        p[i] = 0;
-}
 
 __global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restrict__ keys, int64_t n, int passes,
                                                          uint32_t* __restrict__ ghist) {
@@ -279,10 +280,20 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
     const int64_t row = valid ? perm[i] : 0;
     const int64_t base = ibase[b];
     uint32_t m = u;
-    for (int j = 0; m != 0; ++j) {
-        const int k = __ffs(m) - 1;
-        m &= m - 1;
-        items[(base + j) * 16 + r] = ((key >> k) & 1u) ? nbr[(int64_t)k * n + row] : -1;
+    // four of the block's offsets per round, their table entries loaded together
+    for (int j = 0; m != 0; j += 4) {
+        int kk[4];
+        int32_t v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            kk[t] = m ? __ffs(m) - 1 : -1;
+            m &= m - 1;
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = kk[t] >= 0 && ((key >> kk[t]) & 1u) ? nbr[(int64_t)kk[t] * n + row] : -1;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (kk[t] >= 0) items[(base + j + t) * 16 + r] = v[t];
     }
 }
 
@@ -320,10 +331,7 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
         return GSC_OK;
     }
     const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
-    const unsigned zblocks = (unsigned)((nzero + 255) / 256 < 1024 ? (nzero + 255) / 256 : 1024);
-    hipLaunchKernelGGL(k_zero_u32, dim3(zblocks), dim3(256), 0, s, ghist, nzero);
-    GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka);
+    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka, ghist, nzero);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
     GSC_LAUNCH_CHECK();
