@@ -163,6 +163,9 @@ def run_pool(args):
                         torch.empty((n, C), dtype=torch.int32, device="cuda"),
                         torch.empty((n,), dtype=torch.int32, device="cuda"))
     dX = torch.empty((n, C), dtype=torch.float32, device="cuda")
+    unpooled = gsc.Pooled(torch.empty((n, C), dtype=torch.float32, device="cuda"), None,
+                          torch.empty((n,), dtype=torch.int32, device="cuda"))
+    dXc = torch.empty((n, C), dtype=torch.float32, device="cuda")
 
     def one(mark):
         gsc.gsc_coords_build(coords, table, sync=False)
@@ -174,6 +177,11 @@ def run_pool(args):
         mark("fwd")
         g = gsc.gsc_sparse_pool_bwd(p.Y, tmap, args.pool, p, dX=dX)
         mark("bwd")
+        if args.unpool:   # back to the fine rows (the transposed pooling) and its gradient
+            u = gsc.gsc_sparse_pool_fwd(p.Y, tmap, args.pool, out=unpooled)
+            mark("unpool_fwd")
+            gsc.gsc_sparse_pool_bwd(u.Y, fmap, args.pool, u, dX=dXc[:p.Y.shape[0]])
+            mark("unpool_bwd")
         return fmap, p, g
 
     for _ in range(args.warmup):
@@ -194,12 +202,14 @@ def run_pool(args):
         evs.append(ev)
     torch.cuda.synchronize()
     sec = (time.perf_counter() - t0) / args.steps
-    ms = {k: [] for k in ("map", "fwd", "bwd")}
+    stages = ["map", "fwd", "bwd"] + (["unpool_fwd", "unpool_bwd"] if args.unpool else [])
+    ms = {k: [] for k in stages}
     for ev in evs:
         d = dict(ev)
-        ms["map"].append(d["start"].elapsed_time(d["map"]))
-        ms["fwd"].append(d["map"].elapsed_time(d["fwd"]))
-        ms["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
+        prev = "start"
+        for k in stages:
+            ms[k].append(d[prev].elapsed_time(d[k]))
+            prev = k
     ms = {k: float(np.mean(v)) for k, v in ms.items()}
     n_pairs, n_out = fmap.count(), fmap.n_out
     nbytes = pool_bytes(n_pairs, n_out, C, K, args.pool)
@@ -209,10 +219,11 @@ def run_pool(args):
             "bytes_per_launch": int(nbytes), "avg_launch_us": round(ms["fwd"] * 1e3, 2)}
     cpu = None if args.no_cpu_baseline else pool_cpu_baseline(args.pool)
     out = {
-        "metric": f"sparse {args.pool}-pool fwd+bwd voxels/s", "value": round(wl.n / sec, 1), "unit": "voxels/s",
+        "metric": f"sparse {args.pool}-pool fwd+bwd{' and unpool fwd+bwd' if args.unpool else ''} voxels/s", "value": round(wl.n / sec, 1), "unit": "voxels/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{wl.name}_{args.pool}pool2_s2", "voxels": wl.n, "pooled_rows": n_out,
+        "config": {"workload": f"{wl.name}_{args.pool}pool2_s2{'_unpool' if args.unpool else ''}", "voxels": wl.n,
+                   "pooled_rows": n_out,
                    "map_pairs": n_pairs, "channels": C, "parallelism": "single GPU"},
         "pool_fwd_bwd_voxels_per_s": round(wl.n / ((ms["fwd"] + ms["bwd"]) * 1e-3), 1),
         "stage_ms": {k: round(v, 4) for k, v in ms.items()},
@@ -294,6 +305,9 @@ def main():
     ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
     ap.add_argument("--pool", choices=["max", "avg", "sum"], default=None,
                     help="time pooling instead (Sec. 4.3, 4.4): the 2^3 stride-2 window over the scene of workload 1")
+    ap.add_argument("--unpool", action="store_true",
+                    help="with --pool avg|sum: also unpool (the transposed pooling, Sec. 4.4) back to the input rows, "
+                         "forward and backward")
     ap.add_argument("--quantize", action="store_true",
                     help="time sparse tensor quantization (Alg. 1) of the two indoor scenes' points at 2 cm instead")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -314,6 +328,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     gsc.lib()
+    if args.unpool and args.pool not in ("avg", "sum"):
+        print("--unpool needs --pool avg or --pool sum", file=sys.stderr)
+        sys.exit(2)
     if args.pool:
         return run_pool(args)
     if args.quantize:

@@ -23,7 +23,8 @@
  *                        features and the weights (chain rule of Eq. 3)
  *   gsc_sparse_pool_*    max / average / sum pooling over a kernel map and
  *   gsc_global_pool_*    global pooling, with their gradients (Sec. 4.3,
- *                        Alg. 3; Sec. 4.4, Alg. 4)
+ *                        Alg. 3; Sec. 4.4, Alg. 4); on the role-reversed
+ *                        map, the transposed pooling (unpooling)
  *
  * Conventions
  *   - A coordinate row is (b, x_1, ..., x_D) of int32, batch index first;
@@ -348,6 +349,11 @@ typedef enum { GSC_POOL_MAX = 0, GSC_POOL_AVG = 1, GSC_POOL_SUM = 2 } gsc_pool_m
  * arg (n_out x C int32; required for MAX, else nullable): the input row
  * attaining the maximum, the first in offset order on ties (-1: none).  cnt
  * (n_out int32, nullable): the number of inputs of each output (Alg. 4's N).
+ * Unpooling (the transposed pooling of Sec. 4.4) is this call in AVG or SUM
+ * mode on the role-reversed map (the map gsc_sparse_pool_bwd takes: coarse
+ * rows in, fine rows out): each fine row receives the mean or the sum of the
+ * coarse rows it is pooled into; its gradient is gsc_sparse_pool_bwd on the
+ * pooling's own map.
  * Asynchronous.  Errors: EINVAL, EHIP. */
 int gsc_sparse_pool_fwd(int32_t mode, const float* X, int64_t n_in, int32_t C,
                         const int32_t* nbr, int32_t K, int64_t n_out,

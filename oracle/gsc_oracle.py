@@ -382,6 +382,24 @@ def pool_backward(dY: np.ndarray, maps: List[Pairs], n_in: int, mode: str, arg: 
     return dX
 
 
+def unpool_forward(X: np.ndarray, maps: List[Pairs], n_fine: int, mode: str):
+    """Transposed pooling (unpooling, Sec. 4.4): Alg. 4 on the pooling map with
+    the roles of I and O reversed, so fine row i receives the sum (sum) or the
+    mean (avg) of the coarse rows it is pooled into.  ``maps`` is the pooling
+    map (fine inputs I, coarse outputs O); X holds the coarse features.
+    Returns (Y, arg, N) as pool_forward, N counting each fine row's coarse rows."""
+    assert mode in ("avg", "sum")
+    return pool_forward(X, transposed_map(maps), n_fine, mode)
+
+
+def unpool_backward(dY: np.ndarray, maps: List[Pairs], n_coarse: int, mode: str, N: np.ndarray):
+    """Gradient of unpool_forward with respect to the coarse features: coarse
+    row j receives dY[i] (sum) or dY[i] / N[i] (avg) of every fine row i
+    pooled into it."""
+    assert mode in ("avg", "sum")
+    return pool_backward(dY, transposed_map(maps), n_coarse, mode, None, N)
+
+
 def global_pool_forward(X: np.ndarray, batch: np.ndarray, n_batch: int, mode: str):
     """Global pooling (Sec. 4.4): the kernel map sends every input of batch
     index b to one output (the origin of b), then pool_forward; output b is the

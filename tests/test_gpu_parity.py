@@ -585,6 +585,28 @@ def test_pool_parity(mode, window, C):
     assert rel_err(to_np(dX), ref_dX) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("window", [2, 3])
+@pytest.mark.parametrize("mode", ["avg", "sum"])
+def test_unpool_parity(mode, window):
+    """Unpooling (Sec. 4.4, transposed pooling): gsc_sparse_pool_fwd on the
+    role-reversed map takes coarse features back to the fine rows, and
+    gsc_sparse_pool_bwd on the forward map gives its gradient."""
+    wl, coords, out, fmap, tmap, _, _, ref_maps = _pool_case(95 + window, 0.3, window, extra_outputs=5)
+    n_out = out.shape[0]
+    _say(f"[gpu] unpool {mode} window {window}: n_coarse={n_out} n_fine={wl.n}")
+    Xc, _ = WL.random_features(97, n_out, 32)
+    Gf, _ = WL.random_features(98, wl.n, 32)
+    u = gsc.gsc_sparse_pool_fwd(torch.from_numpy(Xc).to(DEV), tmap, mode)
+    dXc = gsc.gsc_sparse_pool_bwd(torch.from_numpy(Gf).to(DEV), fmap, mode, u)
+    torch.cuda.synchronize()
+    U, _, N = O.unpool_forward(Xc, ref_maps, wl.n, mode)
+    assert np.array_equal(to_np(u.cnt), N) and N.min() >= 1
+    assert rel_err(to_np(u.Y), U) <= TOL["f32"]
+    ref = O.unpool_backward(Gf, ref_maps, n_out, mode, N)
+    assert np.all(to_np(dXc)[-5:] == 0)                               # coarse rows no fine row reaches
+    assert rel_err(to_np(dXc), ref) <= TOL["f32"]
+
+
 @pytest.mark.parametrize("mode", ["max", "avg", "sum"])
 def test_global_pool_parity(mode):
     c = WL.random_coords(91, 3000, 3, -20, 21, batch=3)

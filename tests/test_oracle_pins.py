@@ -14,7 +14,9 @@ computed by means that share nothing with the oracle's own code.
 * pooling (Sec. 4.3, 4.4): torch max_pool3d over a -inf background and
   (sum, count) window sums by avg_pool3d for the size-2 partition and the
   overlapping size-3 window at stride 2, their autograd gradients, and
-  per-batch torch reductions for global pooling;
+  per-batch torch reductions for global pooling; unpooling as the transpose
+  of the dense sum pooling (its autograd gradient) and, for the partition,
+  the parent row's features;
 * quantization (Sec. 4.1, Alg. 1): a hand-written example (golden file) and
   np.unique over the floored rows;
 * batch normalisation and ReLU after a convolution (Sec. 4.5): torch's
@@ -541,6 +543,36 @@ def test_pool_vs_dense(K, mode):
     assert rel_err(dX, refdX) < 1e-12
     # every output of a strided pool has at least one input; the window sizes bound the count
     assert N.min() >= 1 and N.max() <= K ** 3
+
+
+@pytest.mark.parametrize("K", [2, 3])
+def test_unpool_vs_dense_transpose(K):
+    """Unpooling (Sec. 4.4, the transposed pooling) is the transpose of sum
+    pooling: the gradient of the dense torch pooling with respect to its input,
+    taken against the coarse features, gives the fine rows' sums, and against
+    ones their counts; avg divides the two.  For the {0,1}^3 partition every
+    fine row has exactly one coarse row, its floor(c / 2) * 2 parent, and takes
+    that row's features."""
+    c, X, out, maps, lo, shape = _pool_setup(75 + K, K)
+    Yc = np.asarray(WL.random_features(6, len(out), 4)[0], np.float64)
+    _, ref_sum = _dense_pool(c, X, out, lo, shape, K, "sum", grad=Yc)
+    _, ref_cnt = _dense_pool(c, X, out, lo, shape, K, "sum", grad=np.ones_like(Yc))
+    U, _, N = O.unpool_forward(Yc, maps, len(c), "sum")
+    assert rel_err(U, ref_sum) < 1e-12
+    assert np.array_equal(N, np.rint(ref_cnt[:, 0]).astype(np.int64)) and N.min() >= 1
+    A, _, _ = O.unpool_forward(Yc, maps, len(c), "avg")
+    assert rel_err(A, ref_sum / ref_cnt) < 1e-12
+    if K == 2:
+        parent = np.concatenate([c[:, :1], np.floor_divide(c[:, 1:], 2) * 2], axis=1)
+        row_of = {tuple(r): j for j, r in enumerate(out.tolist())}
+        idx = np.array([row_of[tuple(r)] for r in parent.tolist()])
+        assert np.array_equal(A, Yc[idx]) and np.array_equal(U, Yc[idx])
+    # its gradient is sum pooling of the fine gradient (avg: each fine row's share)
+    G = np.asarray(WL.random_features(7, len(c), 4)[0], np.float64)
+    for mode in ("sum", "avg"):
+        dYc = O.unpool_backward(G, maps, len(out), mode, N)
+        ref, _ = _dense_pool(c, G / (N[:, None] if mode == "avg" else 1.0), out, lo, shape, K, "sum")
+        assert rel_err(dYc, ref) < 1e-12
 
 
 def test_global_pool_vs_per_batch_reductions():
