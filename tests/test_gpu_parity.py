@@ -753,3 +753,19 @@ def test_conv_affine_no_input_rows():
                                         relu=True)
     torch.cuda.synchronize()
     assert np.array_equal(to_np(Y0), np.broadcast_to(np.maximum(shift, 0), (3, 32)))
+
+
+def test_block_engines_at_32_offsets():
+    """K = 32, the widest region a block plan takes (masks use all 32 bits;
+    the last offset is bit 31), on both engines, and K = 33, which the row
+    form takes."""
+    extra = np.array([[2, 0, 0], [-2, 0, 0], [0, 2, 0], [0, -2, 0], [0, 0, 2], [0, 0, -2]], np.int32)
+    offs32 = np.concatenate([regions.hypercube(3, 3), extra[:5]]).astype(np.int32)
+    offs33 = np.concatenate([regions.hypercube(3, 3), extra]).astype(np.int32)
+    coords = WL.random_coords(181, 3000, 3, -9, 9, batch=2)
+    assert gsc.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 32) and gsc.gsc_conv_block_engine(gsc.GSC_BF16, 64, 64, 32)
+    assert not gsc.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33)
+    _say("[gpu] block engines at K = 32 (fp32 32->32, bf16 64->64), row form at K = 33")
+    _plan_case(coords, 32, 32, offs32, 182)
+    _plan_case(coords, 64, 64, offs32, 183, dtype="bf16")
+    _conv_case(coords, 16, 16, offs33, 184)
