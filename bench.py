@@ -43,6 +43,37 @@ def fwd_bytes(n_pairs, n_out, ci, co, K, s):
     return n_pairs * (s * ci + 8) + n_out * s * co + K * ci * co * s
 
 
+def measured_peaks(torch):
+    """The box's own ceilings, for context beside the published ones: a device
+    to device copy of 1 GiB (read + write bytes per second) and a 8192^3 bf16
+    matrix product (hipBLASLt through torch), each the best of a few runs."""
+    src = torch.empty(2**28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    best_copy, best_mm = float("inf"), float("inf")
+    for _ in range(5):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.mm(a, b)
+        e2.record()
+        torch.cuda.synchronize()
+        best_copy = min(best_copy, e0.elapsed_time(e1))
+        best_mm = min(best_mm, e1.elapsed_time(e2))
+    del src, dst, a, b
+    return {"copy_GBs": round(2 * 2**30 / (best_copy * 1e-3) / 1e9, 1),
+            "bf16_gemm_TFLOPs": round(2 * 8192**3 / (best_mm * 1e-3) / 1e12, 1)}
+
+
+def stage_stats(samples):
+    """Median, 10th and 90th percentiles of per-step stage times (ms)."""
+    import numpy as np
+    return {q: {k: round(float(np.percentile(v, pct)), 4) for k, v in samples.items()}
+            for q, pct in (("median", 50), ("p10", 10), ("p90", 90))}
+
+
 def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool, epilogue: bool = False) -> str:
     """Name of the kernel gsc_sparse_conv_fwd launches for this layer (the
     library's dispatch: block engine on a plan, else the map's row form)."""
@@ -389,6 +420,7 @@ def main():
         stage["fwd"].append(d["plan"].elapsed_time(d["fwd"]))
         stage["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
     ms = {k: float(np.mean(v)) for k, v in stage.items()}
+    stats = stage_stats(stage)
 
     L0 = wl.layers[0]
     s = 2 if wl.dtype == "bf16" else 4
@@ -456,9 +488,16 @@ def main():
         "kernel_map_build_ms": round(ms["map"], 4),
         "block_plan_ms": round(ms["plan"], 4),
         "stage_ms": {k: round(v, 4) for k, v in ms.items()},
+        "stage_ms_median": stats["median"], "stage_ms_p10": stats["p10"], "stage_ms_p90": stats["p90"],
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if roof is not None and not args.copy_calibration:   # (a counter run's only copy is the calibration)
+        peaks = measured_peaks(torch)
+        ref = peaks["bf16_gemm_TFLOPs"] if roof["bound"] == "mfma" else peaks["copy_GBs"]
+        roof["measured_peak"] = ref
+        roof["frac_of_measured_peak"] = round(roof["achieved"] / ref, 4)
+        out["measured_peaks"] = peaks
     print(json.dumps(out), flush=True)
 
 
