@@ -769,3 +769,25 @@ def test_block_engines_at_32_offsets():
     _plan_case(coords, 32, 32, offs32, 182)
     _plan_case(coords, 64, 64, offs32, 183, dtype="bf16")
     _conv_case(coords, 16, 16, offs33, 184)
+
+
+def test_7d_space_time_chroma():
+    """7D coordinates (b, x, y, z, t, r, g, b) as the space-time-chroma
+    convolution of Sec. 6 uses them, with keys inside the 62-bit packing: the
+    7D cross (15 offsets) on the block engine and a trilateral region (the
+    spatial 3^3 cube plus the temporal and the three chroma crosses, 35
+    offsets) on the row form."""
+    coords = WL.random_coords(191, 4000, 7, -2, 2, batch=2)
+    cross = regions.hypercross(3, 7)
+    tri = {tuple(o) + (0,) * 4 for o in regions.hypercube(3, 3).tolist()}
+    for ax in range(3, 7):
+        for s in (-1, 1):
+            o = [0] * 7
+            o[ax] = s
+            tri.add(tuple(o))
+    tri = np.array(sorted(tri), np.int32)
+    assert len(cross) == 15 and len(tri) == 35 and regions.is_symmetric(tri)
+    _say("[gpu] 7D space-time-chroma: cross (15) on the block engine, trilateral (35) on the row form")
+    _plan_case(coords, 16, 32, cross, 192)
+    _conv_case(coords, 16, 16, cross, 193)
+    _conv_case(coords, 8, 16, tri, 194)
