@@ -151,7 +151,8 @@ class StepPlan:
     def run(self, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
         """Enqueue one pass.  ``mark(name)`` (optional) is called after each
         stage is enqueued: "map" (coordinates + kernel maps), "plan" (tile
-        plans), "fwd", "bwd"."""
+        plans), "fwd", "bwd"; a two-layer pass also marks "fwd0" after the
+        first layer's forward."""
         mark = mark or (lambda name: None)
         dw = self.dw
         if self.kinds == ["subm"]:
@@ -198,6 +199,7 @@ class StepPlan:
         self.plans = [m for m in (pkd, ptd) if m.plan is not None]
         mark("plan")
         Y1 = gsc.gsc_sparse_conv_fwd(dw.X, dw.Ws[0], pkd, Y=self.Y1[:n_out], stream=stream, ws=self.ws_fwd1)
+        mark("fwd0")   # the first layer's forward alone
         Y2 = gsc.gsc_sparse_conv_fwd(Y1, dw.Ws[1], ptd, Y=self.Y2, stream=stream, ws=self.ws_fwd2)
         mark("fwd")
         dY1, dW2 = gsc.gsc_sparse_conv_bwd(Y1, dw.Ws[1], dw.dY, ptd, pkd, None, dX=self.dY1[:n_out], dW=self.dW2,
