@@ -195,36 +195,60 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
 
 // strided: find-or-insert the strided key, keep the smallest input row that
 // produces it; remember the slot of every row.
+// Rows of one wave are consecutive, so rows with the same (strided) key are
+// often neighbouring lanes: only the first lane of each run of equal keys
+// inserts (its row is the run's smallest) and the others take its slot by a
+// shuffle, which spares the contended atomics on the shared slot.
 __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, int64_t n, StrideArg st,
                                                          TableHeader* h, Slot* slots, int64_t* slot_of) {
     const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
-    if (r >= n) return;
-    if (h->status & ST_RANGE) {
-        slot_of[r] = 0;
+    const bool valid = r < n;
+    if (h->status & ST_RANGE) {   // uniform
+        if (valid) slot_of[r] = 0;
         return;
     }
     const int ncol = h->ncol;
     const unsigned long long mask = (unsigned long long)h->capacity - 1;
-    int64_t v[kMaxCols];
-    load_row(coords, r, ncol, st, v);
-    unsigned long long key;
-    if (!pack_key(h, ncol, v, &key)) {
-        atomicOr(&h->status, ST_RANGE);
-        slot_of[r] = 0;
-        return;
-    }
-    unsigned long long s = home_slot(h, key, mask);
-    for (unsigned long long i = 0; i <= mask; ++i) {
-        unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
-        if (prev == kEmptyKey || prev == key) {
-            atomicMin(&slots[s].val, (int32_t)r);
-            slot_of[r] = (int64_t)s;
-            return;
+    unsigned long long key = 0;
+    bool ok = false;
+    if (valid) {
+        int64_t v[kMaxCols];
+        load_row(coords, r, ncol, st, v);
+        ok = pack_key(h, ncol, v, &key);
+        if (!ok) {
+            atomicOr(&h->status, ST_RANGE);
+            slot_of[r] = 0;
         }
-        s = (s + 1) & mask;
     }
-    atomicOr(&h->status, ST_FULL);
-    slot_of[r] = 0;
+    const int lane = __lane_id();
+    const unsigned long long pkey = __shfl_up(key, 1, 64);
+    const bool pok = __shfl_up((int)ok, 1, 64) != 0;
+    const bool follower = ok && lane > 0 && pok && pkey == key;
+    const unsigned long long leaders = __ballot(ok && !follower);
+    unsigned long long s = 0;
+    if (ok && !follower) {
+        s = home_slot(h, key, mask);
+        bool placed = false;
+        for (unsigned long long i = 0; i <= mask; ++i) {
+            const unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
+            if (prev == kEmptyKey || prev == key) {
+                atomicMin(&slots[s].val, (int32_t)r);
+                placed = true;
+                break;
+            }
+            s = (s + 1) & mask;
+        }
+        if (!placed) {
+            atomicOr(&h->status, ST_FULL);
+            s = 0;
+        }
+    }
+    // a follower's run starts at the highest leader lane at or below it
+    const unsigned long long upto = lane == 63 ? ~0ull : ((2ull << lane) - 1ull);
+    const unsigned long long lm = leaders & upto;
+    const int ld = lm ? 63 - __clzll(lm) : lane;
+    const unsigned long long ls = __shfl(s, ld, 64);
+    if (ok) slot_of[r] = (int64_t)(follower ? ls : s);
 }
 
 // mark representatives (slot holds this row) and count them per 64-row group
