@@ -18,7 +18,9 @@ Conventions (readings of the paper, listed with the others in the design notes):
 Parity status: every function is pinned by the CPU tests (brute-force maps,
 closed-form counts, dense-convolution special cases, adjoint identities, finite
 differences, dense max/average pooling and their gradients, per-batch
-reductions, a hand-written quantization example and np.unique, batch
+reductions, hand-written quantization examples (exact floors at voxel sizes
+that are not powers of two among them), np.unique and the floor's bracketing
+inequality in integer arithmetic, batch
 statistics after normalisation); the row order
 of ``output_coordinates`` is an implementation choice and is compared
 canonically, not pinned.
@@ -26,6 +28,8 @@ canonically, not pinned.
 from __future__ import annotations
 
 import itertools
+import math
+from fractions import Fraction
 from typing import Dict, List, Sequence, Tuple
 
 import numpy as np
@@ -277,10 +281,18 @@ def map_pair_count(maps: List[Pairs]) -> int:
 # --------------------------------------------------------------------------- #
 # Sparse tensor quantization (Sec. 4.1, Alg. 1)
 # --------------------------------------------------------------------------- #
+def floor_quotient(p, v) -> int:
+    """floor(p / v) for two stored float32 values, taken on the exact real
+    quotient (Sec. 4.1, Alg. 1 floors C_p / v_l with C_p real-valued).
+    ``Fraction(float(x))`` is the exact binary value of x, so no rounded
+    quotient decides on which side of a voxel boundary a point falls."""
+    return math.floor(Fraction(float(p)) / Fraction(float(v)))
+
+
 def quantize(points: np.ndarray, batch: np.ndarray, voxel, labels=None, ignore_label: int = -100):
-    """Alg. 1 in the paper's order.  C' = floor(C / v) per spatial axis, in
-    float32 (the precision the GPU path divides in, so both take the same
-    floor); the keys are the coordinate rows (batch index first); the pairs
+    """Alg. 1 in the paper's order.  C' = floor(C / v) per spatial axis, the
+    floor of the exact quotient of the stored float32 point and voxel size
+    (``floor_quotient``); the keys are the coordinate rows (batch index first); the pairs
     (i, l) are sorted by key, stably, so within a key the points keep their
     order; UniqueByKey keeps the first point of every run of equal (key,
     label); ReduceByKey merges the runs of one key with f, which turns any
@@ -291,7 +303,7 @@ def quantize(points: np.ndarray, batch: np.ndarray, voxel, labels=None, ignore_l
     P = np.asarray(points, dtype=np.float32)
     N, D = P.shape
     v = np.broadcast_to(np.asarray(voxel, dtype=np.float32), (D,))
-    Cq = np.floor(P / v[None, :]).astype(np.int64)                  # C'_p (float32 quotient, then floor)
+    Cq = [[floor_quotient(x, v[d]) for d, x in enumerate(row)] for row in P.tolist()]   # C'_p
     keys = [(int(b),) + tuple(int(x) for x in row) for b, row in zip(np.asarray(batch).tolist(), Cq)]
     lab = [0] * N if labels is None else [int(x) for x in np.asarray(labels).tolist()]
     order = sorted(range(N), key=lambda i: keys[i])                   # SortByKey (stable)

@@ -17,7 +17,9 @@ computed by means that share nothing with the oracle's own code.
   per-batch torch reductions for global pooling; unpooling as the transpose
   of the dense sum pooling (its autograd gradient) and, for the partition,
   the parent row's features;
-* quantization (Sec. 4.1, Alg. 1): a hand-written example (golden file) and
+* quantization (Sec. 4.1, Alg. 1): hand-written examples (golden files: a small
+  scene, and exact floors at voxels that are not powers of two), the floor's
+  bracketing inequality in integer arithmetic, and
   np.unique over the floored rows;
 * batch normalisation and ReLU after a convolution (Sec. 4.5): torch's
   batch_norm with batch statistics and the moments of the normalised columns.
@@ -669,6 +671,69 @@ def test_quantize_vs_numpy_unique():
     # voxels on either side of 0
     trunc = np.concatenate([b[:, None], np.trunc(P / np.float32(0.25)).astype(np.int64)], 1)
     assert len(np.unique(trunc, axis=0)) != len(u)
+
+
+def _exact_floor_lines():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "quantize_exact_floor.txt")):
+        f = line.split("#")[0].split()
+        if f:
+            rows.append((f[0], f[1], f[2], f[3], int(f[4]), None if f[5] == "same" else int(f[5])))
+    return rows
+
+
+def test_quantize_exact_floor_golden():
+    """Alg. 1's floor(C_p / v_l) at voxels that are not powers of two: the
+    floor of the exact quotient of the stored float32 values, worked out by
+    hand in the golden file (0.7 / 0.1 -> 6, although the float32 quotient
+    rounds to 7.0).  The file's exact decimal values are checked against the
+    float32 numbers, and the floors against a 80-digit decimal division."""
+    import decimal
+    ctx = decimal.Context(prec=80, rounding=decimal.ROUND_FLOOR)
+    rows = _exact_floor_lines()
+    assert len(rows) >= 10
+    for p, v, pe, ve, want, _ in rows:
+        pf, vf = np.float32(p), np.float32(v)
+        assert decimal.Decimal(float(pf)) == decimal.Decimal(pe) and decimal.Decimal(float(vf)) == decimal.Decimal(ve)
+        assert int(ctx.divide(decimal.Decimal(pe), decimal.Decimal(ve)).to_integral_value(decimal.ROUND_FLOOR)) == want
+        C, _, _, inv = O.quantize(np.array([[pf, pf]], np.float32), np.array([0]), (vf, vf))
+        assert C.tolist() == [[0, want, want]]
+        assert O.floor_quotient(pf, vf) == want
+
+
+def test_quantize_float32_quotient_is_a_planted_mistake():
+    """The reading that floors the quotient rounded to float32 puts 0.7 in
+    voxel 7 at v = 0.1 (and four more golden points one voxel off): the golden
+    pin tells the two readings apart."""
+    rows = _exact_floor_lines()
+    moved = [(p, v, want, f32) for p, v, _, _, want, f32 in rows if f32 is not None]
+    assert len(moved) >= 5
+    for p, v, want, f32 in moved:
+        rounded = int(np.floor(np.float32(p) / np.float32(v)))
+        assert rounded == f32 != want
+
+
+@pytest.mark.parametrize("voxel", [0.1, 0.05, 0.02, (0.03, 0.07, 0.11)])
+def test_quantize_floor_brackets_point(voxel):
+    """The voxel index n of every point satisfies n v <= p < (n + 1) v,
+    checked in integer arithmetic on the exact binary values of p and v (a
+    definition of the floor that does not divide), on points that crowd the
+    voxel boundaries: multiples of v rounded to float32, and their float32
+    neighbours."""
+    rng = np.random.default_rng(17)
+    v = np.broadcast_to(np.asarray(voxel, np.float32), (3,))
+    n = rng.integers(-400, 400, size=(700, 3))
+    P = (n * v.astype(np.float64)).astype(np.float32)
+    P[::3] = np.nextafter(P[::3], np.float32(-np.inf))
+    P[1::3] = np.nextafter(P[1::3], np.float32(np.inf))
+    C, _, _, inv = O.quantize(P, np.zeros(len(P), np.int64), voxel)
+    got = C[inv][:, 1:]
+    for i in range(len(P)):
+        for d in range(3):
+            pn, pd = float(P[i, d]).as_integer_ratio()
+            vn, vd = float(v[d]).as_integer_ratio()
+            k = int(got[i, d])
+            assert k * vn * pd <= pn * vd < (k + 1) * vn * pd
 
 
 # --------------------------------------------------------------------------- #
