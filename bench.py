@@ -1,18 +1,25 @@
 #!/usr/bin/env python3
 """Benchmark of the generalized-sparse-convolution hot path on one MI355X.
 
-One step = one pass of the whole hot path over the workload, inputs already
+One step = one pass of the whole hot path over a workload, inputs already
 resident in HBM: coordinate hash table, output coordinates (strided layers),
-kernel maps, convolution forward, input gradient and weight gradient.
+kernel maps, block plans, convolution forward, input gradient and weight
+gradient.
 
-    python bench.py [--steps K] [--warmup W] [--workload 1]
+    python bench.py [--steps K] [--warmup W]            # all five workloads
+    python bench.py --workload N [...]                  # one workload
 
-Prints one JSON line.  ``value`` is voxels (input rows) per second of whole
-steps; the conv-only rate, the effective GFLOP/s and the kernel-map build time
-are reported beside it.  ``roofline`` covers the dominant kernel (the
-forward gather-MFMA-scatter), timed with HIP events on the stream it runs on.
-``cpu_baseline`` times the CPU oracle (test infrastructure, never tuned) on
-the same workload on this host's cores.
+By default every workload (0..4) is timed in turn and the JSON line's headline
+(``value``, ``roofline``) is workload 4, the indoor scenes at 2 cm with 256
+channels in bfloat16, the largest of them by arithmetic; the others are
+reported under ``configs`` with their stage times, their forward+backward time
+against its roofline target and the roofline fraction of their forward
+kernel.  ``value`` is voxels (input rows) per second of whole steps; the
+conv-only rate, the effective GFLOP/s and the kernel-map build time are
+reported beside it.  ``roofline`` covers the dominant kernel (the forward
+gather-MFMA-scatter), timed with HIP events on the stream it runs on.
+``cpu_baseline`` times the CPU oracle (test infrastructure, never tuned) on a
+bounded sample of the headline workload, stage by stage, on this host's cores.
 """
 from __future__ import annotations
 
@@ -108,39 +115,92 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
-def cpu_baseline(wl, budget_s: float = 30.0):
-    """Time the CPU oracle on this host over one full pass of the workload."""
+def _blas_threads():
+    """Cores this process may run on and the BLAS thread pools numpy uses
+    (limited to those cores)."""
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threadpool_limits(cores)
+        blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()]
+    except Exception:
+        blas = []
+    threads = max([t for _, t in blas if t] or [1])
+    return cores, min(threads, cores), blas
+
+
+def _oracle_pass(O, coords, layers, D, X, dY):
+    """One pass of the oracle over a sparse tensor, stage by stage (seconds):
+    coordinate map, output coordinates (strided layers), kernel maps, forward,
+    backward (the same stages the GPU pass times)."""
+    import numpy as np
+    t = {}
+    t0 = time.perf_counter()
+    O.coordinate_map(coords)
+    t["coords"] = time.perf_counter() - t0
+    X = X.astype(np.float64)
+    dY = dY.astype(np.float64)
+    kinds = [L.kind for L in layers]
+    if kinds == ["subm"]:
+        L = layers[0]
+        t0 = time.perf_counter()
+        m = O.kernel_map(coords, coords, O.region(L.region, L.ksize, D))
+        t["map"] = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        O.conv_forward(X, L.W, m, len(coords))
+        t["fwd"] = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        O.conv_backward(X, L.W, dY, m)
+        t["bwd"] = time.perf_counter() - t0
+        return t
+    L0, L1 = layers
+    t0 = time.perf_counter()
+    out = O.output_coordinates(coords, L0.stride)
+    t["out_coords"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    kd = O.kernel_map(coords, out, O.region(L0.region, L0.ksize, D))
+    td = O.transposed_map(kd)
+    t["map"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    Y1 = O.conv_forward(X, L0.W, kd, len(out))
+    O.conv_forward(Y1, L1.W, td, len(coords))
+    t["fwd"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    dY1, _ = O.conv_backward(Y1, L1.W, dY, td)
+    O.conv_backward(X, L0.W, dY1, kd)
+    t["bwd"] = time.perf_counter() - t0
+    return t
+
+
+def cpu_baseline(wl, max_rows: int = 400000, reps: int = 1):
+    """Time the CPU oracle on this host: one pass over the first ``max_rows``
+    coordinate rows of the workload in (b, x, y, z[, t]) order (a slab of the
+    first scene, taken as a sparse tensor of its own), or over all of it when
+    it is smaller; the median of ``reps`` passes.  Per-stage milliseconds and
+    voxels per second of the whole pass."""
     import numpy as np
     import oracle.gsc_oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()]
-        threads = max([t for _, t in blas if t] or [1])
-    except Exception:
-        blas, threads = [], 1
-    kinds = [L.kind for L in wl.layers]
-    t0 = time.perf_counter()
-    X = wl.X.astype(np.float64)
-    dY = wl.dY.astype(np.float64)
-    if kinds == ["subm"]:
-        L = wl.layers[0]
-        m = O.kernel_map(wl.coords, wl.coords, O.region(L.region, L.ksize, wl.D))
-        O.conv_forward(X, L.W, m, wl.n)
-        O.conv_backward(X, L.W, dY, m)
+    cores, threads, blas = _blas_threads()
+    n = min(wl.n, max_rows)
+    order = np.lexsort(wl.coords.T[::-1])[:n]
+    order.sort()   # rows keep their relative order
+    coords = wl.coords[order]
+    X, dY = wl.X[order], wl.dY[order]
+    runs = [_oracle_pass(O, coords, wl.layers, wl.D, X, dY) for _ in range(reps)]
+    import statistics
+    stages = {k: statistics.median(r[k] for r in runs) for k in runs[0]}
+    total = statistics.median(sum(r.values()) for r in runs)
+    if n == wl.n:
+        sample = f"all {n} voxels of {wl.name}"
     else:
-        L0, L1 = wl.layers
-        out = O.output_coordinates(wl.coords, L0.stride)
-        kd = O.kernel_map(wl.coords, out, O.region(L0.region, L0.ksize, wl.D))
-        td = O.transposed_map(kd)
-        Y1 = O.conv_forward(X, L0.W, kd, len(out))
-        O.conv_forward(Y1, L1.W, td, wl.n)
-        dY1, _ = O.conv_backward(Y1, L1.W, dY, td)
-        O.conv_backward(X, L0.W, dY1, kd)
-    t = time.perf_counter() - t0
-    return {"value": wl.n / t, "unit": "voxels/s", "cores": threads, "kind": "oracle",
-            "sample": f"one full pass of {wl.name} ({wl.n} voxels): dict map (single-threaded Python) + "
-                      f"float64 numpy matmuls ({threads} BLAS threads); {t:.1f} s",
-            "seconds": t, "blas": blas}
+        sample = (f"the first {n} of the {wl.n} voxels of {wl.name} in (b, x, y, z) order (a slab of the first "
+                  f"scene, x <= {int(coords[:, 1].max())}), as a sparse tensor of its own")
+    return {"value": n / total, "unit": "voxels/s", "cores": threads, "kind": "oracle",
+            "sample": f"{sample}; {'median of ' + str(reps) + ' passes' if reps > 1 else 'one pass'}: "
+                      f"dict coordinate and kernel maps (single-threaded Python) + float64 numpy matmuls "
+                      f"({threads} BLAS threads on {cores} cores); {total:.1f} s",
+            "stage_ms": {k: round(v * 1e3, 1) for k, v in stages.items()},
+            "seconds": round(total, 3), "voxels": n, "affinity_cores": cores, "blas": blas}
 
 
 def pool_bytes(n_pairs, n_out, C, K, mode):
@@ -320,12 +380,161 @@ def run_quantize(args):
     print(json.dumps(out), flush=True)
 
 
+# forward+backward targets (microseconds) of the workloads: 50 % of the HBM
+# roofline for the fp32 layers (C <= 64), 40 % of the bf16 MFMA peak for the
+# 256-channel layer; workload 0 is bound by launch latency (no target)
+TARGET_US = {0: None, 1: 140.0, 2: 338.0, 3: 90.0, 4: 352.0}
+
+
+def conv_pass_bytes(pairs, layers, n_ins, n_outs, s):
+    """Gather-model bytes of forward + input gradient + weight gradient of
+    every layer: one gathered row and one index pair per kernel-map pair and
+    pass, every output row written once, the weights read once (dW written
+    once in fp32)."""
+    tot = 0.0
+    for m, L, n_in, n_out in zip(pairs, layers, n_ins, n_outs):
+        K = L.W.shape[0]
+        tot += fwd_bytes(m, n_out, L.c_in, L.c_out, K, s)
+        tot += m * (s * L.c_out + 8) + n_in * s * L.c_in + K * L.c_in * L.c_out * s
+        tot += m * (s * (L.c_in + L.c_out) + 8) + 4 * K * L.c_in * L.c_out
+    return tot
+
+
+def bench_conv(args, wid: int, region=None, affine: bool = False, no_plan: bool = False,
+               steps: int = None, warmup: int = None) -> dict:
+    """Time ``steps`` whole passes of workload ``wid`` (after ``warmup``
+    untimed ones) and return its results: per-step time, voxels/s, stage
+    times (mean, median, p10, p90) from HIP events on the stream, the
+    forward+backward time against its target, and the roofline of the
+    forward kernel of the first layer."""
+    import numpy as np
+    import torch
+
+    from paper_1904_08755_amd import gsc, pipeline
+    from paper_1904_08755_amd import workloads as WL
+
+    steps = args.steps if steps is None else steps
+    warmup = args.warmup if warmup is None else warmup
+    t = time.perf_counter()
+    wl = WL.make_workload(wid, region=region)
+    log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")
+    dw = pipeline.to_device(wl, "cuda")
+    epi = None
+    if affine:
+        rng = np.random.default_rng(np.random.SeedSequence(WL.ROOT_SEED, spawn_key=(wl.config_id, 9)))
+        co = wl.layers[0].c_out
+        epi = (torch.from_numpy(rng.uniform(0.5, 2.0, co).astype(np.float32)).cuda(),
+               torch.from_numpy(rng.uniform(-0.5, 0.5, co).astype(np.float32)).cuda())
+    torch.cuda.synchronize()
+
+    plan0 = pipeline.StepPlan(dw, use_plan=not no_plan, epilogue=epi)
+    for _ in range(warmup):
+        plan0.run()
+    gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
+    del plan0
+    torch.cuda.synchronize()
+    log(f"  warmup done ({warmup} steps)")
+
+    steps_events = []
+    plan = pipeline.StepPlan(dw, use_plan=not no_plan, epilogue=epi)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ev = []
+
+        def mark(name, ev=ev):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            ev.append((name, e))
+
+        mark("start")
+        last = plan.run(mark)
+        steps_events.append(ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sec = (t1 - t0) / steps
+    log(f"  timed {steps} steps: {sec * 1e3:.3f} ms/step")
+
+    stage = {"map": [], "plan": [], "fwd": [], "bwd": []}
+    for ev in steps_events:
+        d = dict(ev)
+        stage["map"].append(d["start"].elapsed_time(d["map"]))
+        stage["plan"].append(d["map"].elapsed_time(d["plan"]))
+        stage["fwd"].append(d["plan"].elapsed_time(d["fwd"]))
+        stage["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
+    ms = {k: float(np.mean(v)) for k, v in stage.items()}
+    stats = stage_stats(stage)
+
+    L0 = wl.layers[0]
+    s = 2 if wl.dtype == "bf16" else 4
+    pairs = [km.count() for km in last.kmaps]
+    n_outs = [km.n_out for km in last.kmaps]
+    n_ins = [wl.n] + n_outs[:-1]
+    flops = sum(6.0 * m * L.c_in * L.c_out for m, L in zip(pairs, wl.layers))
+    conv_s = (ms["fwd"] + ms["bwd"]) * 1e-3
+    fb_med_us = (stats["median"]["fwd"] + stats["median"]["bwd"]) * 1e3
+    km0 = last.kmaps[0]
+    # dominant kernel: the forward convolution of layer 0
+    planned = bool(plan.plans)
+    kernel = forward_kernel(gsc, wl.dtype, L0.c_in, L0.c_out, km0.K, planned, epilogue=epi is not None)
+    wname = wl.name.replace("_cube3", "")
+    traffic = measured_traffic(kernel, wname)
+    dom_bytes = fwd_bytes(pairs[0], n_outs[0], L0.c_in, L0.c_out, km0.K, s)
+    if len(wl.layers) == 1:
+        dom_ms = ms["fwd"]
+    else:   # the first layer's forward launch, timed on its own
+        dom_ms = float(np.mean([dict(ev)["plan"].elapsed_time(dict(ev)["fwd0"]) for ev in steps_events]))
+    pass_bytes = conv_pass_bytes(pairs, wl.layers, n_ins, n_outs, s)
+    roof = None
+    if dom_ms and wl.dtype == "bf16":
+        # wide bf16 layer: the per-offset contractions on the MFMA units
+        dom_flops = 2.0 * pairs[0] * L0.c_in * L0.c_out
+        ach = dom_flops / (dom_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                "kernel": kernel, "flops_per_launch": int(dom_flops),
+                "bytes_per_launch": int(dom_bytes), "avg_launch_us": round(dom_ms * 1e3, 2)}
+        fb = {"bound": "mfma", "unit": "TFLOP/s", "achieved": round(flops / conv_s / 1e12, 2),
+              "frac": round(flops / conv_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
+    elif dom_ms:
+        ach = dom_bytes / (dom_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": kernel, "bytes_per_launch": int(dom_bytes),
+                "avg_launch_us": round(dom_ms * 1e3, 2)}
+        fb = {"bound": "hbm", "unit": "GB/s", "achieved": round(pass_bytes / conv_s / 1e9, 1),
+              "frac": round(pass_bytes / conv_s / 1e9 / HBM_PEAK_GBS, 4)}
+    fb.update({"us": round(conv_s * 1e6, 2), "us_median": round(fb_med_us, 2),
+               "target_us": TARGET_US.get(wid) if region in (None, "hybrid") else None,
+               "flops": flops, "gather_model_bytes": int(pass_bytes)})
+    out = {
+        "workload": wl.name, "dtype": wl.dtype, "voxels": wl.n, "D": wl.D,
+        "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
+        "kernel_map_pairs": pairs, "block_plan": planned,
+        "ms_per_step": round(sec * 1e3, 4), "voxels_per_s": round(wl.n / sec, 1),
+        "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
+        "effective_gflops": round(flops / conv_s / 1e9, 1),
+        "kernel_map_build_ms": round(ms["map"], 4),
+        "block_plan_ms": round(ms["plan"], 4),
+        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
+        "stage_ms_median": stats["median"], "stage_ms_p10": stats["p10"], "stage_ms_p90": stats["p90"],
+        "fwd_bwd": fb,
+        "roofline": roof,
+        "_wl": wl,
+    }
+    if epi is not None:
+        out["epilogue"] = "batchnorm_affine+relu"
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=1, help="0..4 (default 1: indoor scene, batch 2, 32->32)")
+    ap.add_argument("--workload", type=int, default=None,
+                    help="0..4: time this workload only (default: all five, headline workload 4, the indoor "
+                         "scenes at 2 cm with 256 channels in bf16)")
     ap.add_argument("--region", choices=["hybrid", "cube", "spatial", "cross"], default=None,
                     help="region of workload 3 (3D video): hybrid (default, 29 offsets), cube (tesseract, 81), "
                          "spatial (3^3 at zero time offset, 27: each frame on its own), cross (9)")
@@ -351,11 +560,9 @@ def main():
               "(no collectives); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
-    from paper_1904_08755_amd import gsc, pipeline
-    from paper_1904_08755_amd import workloads as WL
+    from paper_1904_08755_amd import gsc
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     gsc.lib()
@@ -366,94 +573,25 @@ def main():
         return run_pool(args)
     if args.quantize:
         return run_quantize(args)
-    t = time.perf_counter()
     if args.region is not None and args.workload != 3:
         print("--region applies to workload 3 (the 3D video) only", file=sys.stderr)
         sys.exit(2)
-    wl = WL.make_workload(args.workload, region=args.region)
-    log(f"workload {wl.name}: n={wl.n} ({time.perf_counter() - t:.1f} s to generate)")
-    dw = pipeline.to_device(wl, "cuda")
-    epi = None
-    if args.affine:
-        if len(wl.layers) != 1:
-            print("--affine applies to the single-layer workloads (0, 1, 3, 4)", file=sys.stderr)
-            sys.exit(2)
-        rng = np.random.default_rng(np.random.SeedSequence(WL.ROOT_SEED, spawn_key=(wl.config_id, 9)))
-        co = wl.layers[0].c_out
-        epi = (torch.from_numpy(rng.uniform(0.5, 2.0, co).astype(np.float32)).cuda(),
-               torch.from_numpy(rng.uniform(-0.5, 0.5, co).astype(np.float32)).cuda())
-    torch.cuda.synchronize()
+    if args.affine and args.workload not in (0, 1, 3, 4):
+        print("--affine applies to one of the single-layer workloads (--workload 0, 1, 3 or 4)", file=sys.stderr)
+        sys.exit(2)
 
-    plan0 = pipeline.StepPlan(dw, use_plan=not args.no_plan, epilogue=epi)
-    for _ in range(args.warmup):
-        plan0.run()
-    gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
-    del plan0
-    torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps)")
-
-    steps_events = []
-    plan = pipeline.StepPlan(dw, use_plan=not args.no_plan, epilogue=epi)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        ev = []
-
-        def mark(name, ev=ev):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
-            ev.append((name, e))
-
-        mark("start")
-        last = plan.run(mark)
-        steps_events.append(ev)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    sec = (t1 - t0) / args.steps
-    log(f"timed {args.steps} steps: {sec * 1e3:.3f} ms/step")
-
-    stage = {"map": [], "plan": [], "fwd": [], "bwd": []}
-    for ev in steps_events:
-        d = dict(ev)
-        stage["map"].append(d["start"].elapsed_time(d["map"]))
-        stage["plan"].append(d["map"].elapsed_time(d["plan"]))
-        stage["fwd"].append(d["plan"].elapsed_time(d["fwd"]))
-        stage["bwd"].append(d["fwd"].elapsed_time(d["bwd"]))
-    ms = {k: float(np.mean(v)) for k, v in stage.items()}
-    stats = stage_stats(stage)
-
-    L0 = wl.layers[0]
-    s = 2 if wl.dtype == "bf16" else 4
-    pairs = [km.count() for km in last.kmaps]
-    flops = sum(6.0 * m * L.c_in * L.c_out for m, L in zip(pairs, wl.layers))
-    conv_s = (ms["fwd"] + ms["bwd"]) * 1e-3
-    km0 = last.kmaps[0]
-    n_out0 = km0.n_out
-    # dominant kernel: the forward convolution of layer 0
-    planned = bool(plan.plans)
-    kernel = forward_kernel(gsc, wl.dtype, L0.c_in, L0.c_out, km0.K, planned, epilogue=epi is not None)
-    wname = wl.name.replace("_cube3", "")
-    traffic = measured_traffic(kernel, wname)
-    dom_bytes = fwd_bytes(pairs[0], n_out0, L0.c_in, L0.c_out, km0.K, s)
-    if len(wl.layers) == 1:
-        dom_ms = ms["fwd"]
-    else:   # the first layer's forward launch, timed on its own
-        dom_ms = float(np.mean([dict(ev)["plan"].elapsed_time(dict(ev)["fwd0"]) for ev in steps_events]))
-    roof = None
-    if dom_ms and wl.dtype == "bf16":
-        # wide bf16 layer: the per-offset contractions on the MFMA units
-        dom_flops = 2.0 * pairs[0] * L0.c_in * L0.c_out
-        ach = dom_flops / (dom_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
-                "kernel": kernel, "flops_per_launch": int(dom_flops),
-                "bytes_per_launch": int(dom_bytes), "avg_launch_us": round(dom_ms * 1e3, 2)}
-    elif dom_ms:
-        ach = dom_bytes / (dom_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": kernel, "bytes_per_launch": int(dom_bytes),
-                "avg_launch_us": round(dom_ms * 1e3, 2)}
+    others = {}
+    if args.workload is None:   # every workload; the headline is workload 4
+        for wid in (0, 1, 2, 3):
+            r = bench_conv(args, wid, no_plan=args.no_plan)
+            r.pop("_wl")
+            others[r.pop("workload")] = r
+        head_id = 4
+    else:
+        head_id = args.workload
+    head = bench_conv(args, head_id, region=args.region, affine=args.affine, no_plan=args.no_plan)
+    wl = head.pop("_wl")
+    roof = head.pop("roofline")
 
     if args.copy_calibration:
         src = torch.empty(64 * 2**20, dtype=torch.float32, device="cuda")
@@ -468,33 +606,38 @@ def main():
         log("cpu baseline (oracle) ...")
         cpu = cpu_baseline(wl)
         log(f"cpu baseline: {cpu['seconds']:.1f} s")
+        if args.workload is None:   # the small workload 0 whole, median of 5
+            from paper_1904_08755_amd import workloads as WL
+            cpu["random64_c3to16_cube3"] = cpu_baseline(WL.make_workload(0), reps=5)
 
+    config = {"workload": head.pop("workload"), "voxels": head.pop("voxels"), "D": head.pop("D"),
+              "layers": head.pop("layers"), "kernel_map_pairs": head.pop("kernel_map_pairs"),
+              "block_plan": head.pop("block_plan"), "parallelism": "single GPU"}
+    if "epilogue" in head:
+        config["epilogue"] = head.pop("epilogue")
+    dtype = head.pop("dtype")
+    ms_step = head.pop("ms_per_step")
+    head.pop("voxels_per_s")
     out = {
         "metric": METRIC,
-        "value": round(wl.n / sec, 1),
+        "value": round(wl.n / (ms_step * 1e-3), 1),
         "unit": "voxels/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(sec * 1e3, 4),
+        "ms_per_step": ms_step,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": wl.dtype,
+        "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "voxels": wl.n, "D": wl.D,
-                   "layers": [f"{L.kind}:{L.region}{L.ksize}/s{L.stride}:{L.c_in}->{L.c_out}" for L in wl.layers],
-                   "kernel_map_pairs": pairs, "block_plan": bool(plan.plans), "parallelism": "single GPU",
-                   **({"epilogue": "batchnorm_affine+relu"} if epi is not None else {})},
-        "conv_fwd_bwd_voxels_per_s": round(wl.n / conv_s, 1),
-        "effective_gflops": round(flops / conv_s / 1e9, 1),
-        "kernel_map_build_ms": round(ms["map"], 4),
-        "block_plan_ms": round(ms["plan"], 4),
-        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
-        "stage_ms_median": stats["median"], "stage_ms_p10": stats["p10"], "stage_ms_p90": stats["p90"],
+        "config": config,
+        **head,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if others:
+        out["configs"] = others
     if roof is not None and not args.copy_calibration:   # (a counter run's only copy is the calibration)
         peaks = measured_peaks(torch)
         ref = peaks["bf16_gemm_TFLOPs"] if roof["bound"] == "mfma" else peaks["copy_GBs"]

@@ -135,8 +135,9 @@ size_t gsc_quantize_ws_bytes(int64_t n, int32_t D);
 
 /* Points (device, n x D float32) with batch indices (device, n int32, or NULL
  * for batch 0) become voxels: coordinate (b, floor(p_1 / v_1), ...,
- * floor(p_D / v_D)), the quotient being the correctly rounded float32
- * division; voxel (host, D positive floats).  One output row per distinct
+ * floor(p_D / v_D)), the floor of the exact quotient of the stored float32
+ * values (0.7f / 0.1f is voxel 6, although the quotient rounded to float32 is
+ * 7.0); voxel (host, D positive floats, taken as float32).  One output row per distinct
  * coordinate, written to out_coords (device, capacity n rows of 1 + D int32)
  * in the order of each voxel's first point; *n_out (host) receives their
  * number.  rep (device, capacity n int32): the first point of each voxel (the

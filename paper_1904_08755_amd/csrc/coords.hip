@@ -310,9 +310,16 @@ __global__ void __launch_bounds__(kThreads) k_quantize(const float* __restrict__
     qc[r * ncol] = batch ? batch[r] : 0;
     bool bad = false;
     for (int d = 0; d < D; ++d) {
-        const float q = floorf(points[r * D + d] / va.v[d]);
-        bad |= !(q >= -1073741824.f && q <= 1073741824.f);   // also NaN
-        qc[r * ncol + 1 + d] = bad ? 0 : (int32_t)q;
+        // floor of the exact quotient p / v of the stored float32 values.  The
+        // quotient rounded to double is at least floor(p / v) (every integer
+        // below 2^53 is a double) and at most floor(p / v) + 1; the fma
+        // residual p - f v is rounded once, so its sign is that of the exact
+        // residual, and a negative one means f overshoots by one.
+        const double p = (double)points[r * D + d], v = (double)va.v[d];
+        double f = floor(p / v);
+        if (fma(-f, v, p) < 0.0) f -= 1.0;
+        bad |= !(f >= -1073741824.0 && f <= 1073741824.0);   // also NaN
+        qc[r * ncol + 1 + d] = bad ? 0 : (int32_t)f;
     }
     if (bad) atomicOr(&h->status, ST_RANGE);
 }

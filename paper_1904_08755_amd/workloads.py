@@ -128,7 +128,14 @@ def sample_points(geom: SceneGeom, rng: np.random.Generator, n_points: int,
 
 
 def voxel_rows(p: np.ndarray, voxel: float, b: int, t: Optional[int] = None) -> np.ndarray:
-    v = np.floor(p / voxel).astype(np.int64)
+    """Voxel rows of points stored as float32, at a voxel size stored as
+    float32: floor of the exact quotient of those two values.  The quotient of
+    two float32 numbers rounded to float64 lies within 2^-53 of it relative,
+    while a quotient that is not an integer lies at least 2^-24 (relative to
+    the integer) from the next one, so for indices below 2^29 the float64
+    floor is the exact one."""
+    p32 = np.asarray(p, dtype=np.float32).astype(np.float64)
+    v = np.floor(p32 / float(np.float32(voxel))).astype(np.int64)
     cols = [np.full((len(v), 1), b, np.int64), v]
     if t is not None:
         cols.append(np.full((len(v), 1), t, np.int64))

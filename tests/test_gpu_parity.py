@@ -657,6 +657,44 @@ def test_quantize_golden_on_gpu():
     _quant_compare(np.array(pts, np.float32), np.array(b, np.int32), 0.5, np.array(L, np.int32))
 
 
+def test_quantize_exact_floor_on_gpu():
+    """Voxel indices at voxel sizes that are not powers of two: the floor of the
+    exact quotient (hand-worked golden file; 0.7 / 0.1 -> 6)."""
+    rows = []
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", "quantize_exact_floor.txt")):
+        f = line.split("#")[0].split()
+        if f:
+            rows.append((np.float32(f[0]), np.float32(f[1]), int(f[4])))
+    for v in sorted({r[1] for r in rows}):
+        sel = [(p, want) for p, vv, want in rows if vv == v]
+        P = np.array([[p, p] for p, _ in sel], np.float32)
+        q = gsc.gsc_quantize(_t(P, torch.float32), (float(v), float(v)), batch=_t(np.arange(len(sel), dtype=np.int32)))
+        torch.cuda.synchronize()
+        got = q.coords.cpu().numpy()[q.inverse.cpu().numpy()]
+        assert got[:, 1].tolist() == [w for _, w in sel] and got[:, 2].tolist() == [w for _, w in sel], v
+        _quant_compare(P, np.arange(len(sel), dtype=np.int32), (float(v), float(v)), None)
+
+
+def test_quantize_matches_workload_voxels():
+    """The GPU quantization of the indoor-scene workload's own points (two
+    scenes of 161,000 points at 2 cm) gives exactly the workload's voxel set:
+    the generator and the kernel floor the same exact quotient."""
+    pts, bs = [], []
+    n = WL.SCENE_POINTS_2CM
+    for bi in range(2):
+        geom = WL.draw_scene(WL.rng_for(1, WL.S_GEOM, bi))
+        p = WL.sample_points(geom, WL.rng_for(1, WL.S_GEOM, bi, 1), n)
+        pts.append(np.asarray(p, np.float32))
+        bs.append(np.full(len(p), bi, np.int32))
+    q = gsc.gsc_quantize(_t(np.concatenate(pts), torch.float32), 0.02, batch=_t(np.concatenate(bs)))
+    torch.cuda.synchronize()
+    got = q.coords.cpu().numpy()
+    ref = WL.make_workload(1).coords
+    _say(f"  scene points {2 * n} -> voxels {len(got)} (workload {len(ref)})")
+    assert len(got) == len(ref)
+    assert np.array_equal(np.unique(got, axis=0), ref)
+
+
 def test_quantize_random_and_scene():
     rng = np.random.default_rng(95)
     P = rng.uniform(-4, 4, size=(60000, 3)).astype(np.float32)
