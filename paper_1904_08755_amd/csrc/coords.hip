@@ -30,7 +30,7 @@ __device__ __forceinline__ void load_row(const int32_t* coords, int64_t r, int n
 }
 
 __global__ void __launch_bounds__(kThreads) k_table_init(TableHeader* h, Slot* slots, int64_t cap, int ncol,
-                                                         int64_t n, int32_t init_val, const int32_t* src) {
+                                                         int64_t n, int32_t init_val) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cap; i += stride) {
         Slot e;
@@ -54,7 +54,6 @@ __global__ void __launch_bounds__(kThreads) k_table_init(TableHeader* h, Slot* s
         }
         h->nblk = 0;
         for (int i = 0; i < 3; ++i) h->blk_shift[i] = 0;
-        h->src = src;
         for (int c = 0; c < kMaxCols; ++c) h->vary[c] = 0;
     }
 }
@@ -409,8 +408,7 @@ static int build_enqueue(const int32_t* coords, int64_t n, int32_t D, void* tabl
     const int64_t cap = table_capacity(n);
     TableHeader* h = reinterpret_cast<TableHeader*>(table);
     Slot* slots = table_slots(table);
-    hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol, n, -1,
-                       coords);
+    hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol, n, -1);
     GSC_LAUNCH_CHECK();
     StrideArg none{};
     if (n > 0) {
@@ -494,7 +492,7 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
     TableHeader* h = reinterpret_cast<TableHeader*>(out_table);
     Slot* slots = table_slots(out_table);
     hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol,
-                       (int64_t)0, (int32_t)INT_MAX, (const int32_t*)out_coords);
+                       (int64_t)0, (int32_t)INT_MAX);
     GSC_LAUNCH_CHECK();
     if (n_in == 0) {
         hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
@@ -576,7 +574,7 @@ int gsc_quantize(const float* points, const int32_t* batch, int64_t n, int32_t D
     TableHeader* h = reinterpret_cast<TableHeader*>(out_table);
     Slot* slots = table_slots(out_table);
     hipLaunchKernelGGL(k_table_init, dim3(grid_capped(cap)), dim3(kThreads), 0, s, h, slots, cap, ncol, (int64_t)0,
-                       (int32_t)INT_MAX, (const int32_t*)out_coords);
+                       (int32_t)INT_MAX);
     GSC_LAUNCH_CHECK();
     if (n == 0) {
         hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);

@@ -55,7 +55,6 @@ struct TableHeader {
     int32_t vary[kMaxCols];  // OR over rows of (row XOR first row): the bits that vary per column
     int32_t nblk;            // spatial columns whose lowest varying key bit selects the slot in a line
     int32_t blk_shift[3];    // that key bit, per blocked column
-    const int32_t* src;      // the coordinate array whose rows the table indexes (n rows)
 };
 static_assert(sizeof(TableHeader) <= kHeaderBytes, "header too large");
 

@@ -13,14 +13,19 @@
 // result does not depend on scheduling.
 //
 // A map of a coordinate set onto itself (the stride-1 layers of Sec. 3.1:
-// the output coordinates are the array the table was built from) over a
-// region closed under negation, listed so that o_{K-1-k} = -o_k with the
-// origin in the middle, is symmetric: (i, j) is a pair at offset k exactly
-// when (j, i) is one at offset K-1-k, and the middle offset pairs every row
-// with itself.  Such a map probes only the offsets before the middle: each
-// hit also writes its mirrored entry of the neighbour table (set to -1
-// beforehand), the middle offset is written directly, and a second pass
-// counts the mirrored offsets' pairs per group from the table.
+// the output coordinates are the rows the table was built from, in the same
+// order) over a region closed under negation, listed so that
+// o_{K-1-k} = -o_k with the origin in the middle, is symmetric: (i, j) is a
+// pair at offset k exactly when (j, i) is one at offset K-1-k, and the middle
+// offset pairs every row with itself.  Whenever the region is listed so and
+// the output has as many rows as the table, the count pass probes only the
+// offsets up to the middle one: each hit also writes its mirrored entry of
+// the neighbour table (set to -1 beforehand), and a second pass counts the
+// mirrored offsets' pairs per group from the table.  The middle offset
+// checks the premise: output row j must find table row j.  If one row does
+// not (other coordinates, another order, rows rewritten since the build),
+// the second pass probes the mirrored offsets itself instead, overwriting
+// their entries, so the result equals the full probe in every case.
 #include <climits>
 #include <vector>
 
@@ -89,9 +94,10 @@ struct KeyOps<unsigned long long> {
 template <typename KeyT, typename Offs>
 __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __restrict__ slots,
                                            const int32_t* __restrict__ out_coords, int64_t n_out, int ncol,
-                                           const Offs& offs, int K, int kprobe, bool self, int64_t G,
-                                           int32_t* __restrict__ cnt, int32_t* __restrict__ nbr, bool ok,
-                                           int64_t j) {
+                                           const Offs& offs, int K, int k_begin, int k_end, int mirror_end,
+                                           int mid, int64_t G, int32_t* __restrict__ cnt,
+                                           int32_t* __restrict__ nbr, bool ok, int64_t j,
+                                           int32_t* __restrict__ not_self) {
     const bool valid = ok && j < n_out;
     const int D = ncol - 1;
     const unsigned long long mask = ok ? (unsigned long long)h->capacity - 1 : 0;
@@ -125,16 +131,16 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
     in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    for (int k0 = 0; k0 < kprobe; k0 += kBatch) {
+    for (int k0 = k_begin; k0 < k_end; k0 += kBatch) {
         KeyT key[kBatch];
         unsigned long long pos[kBatch];
         bool pend[kBatch], hit[kBatch];
         int32_t row[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
-            const int k = min(k0 + b, kprobe - 1);
+            const int k = min(k0 + b, k_end - 1);
             const int32_t* o = offs.at((int64_t)k * D);
-            bool in = in_b && k0 + b < kprobe;
+            bool in = in_b && k0 + b < k_end;
             KeyT delta = 0;
 #pragma unroll
             for (int c = 1; c < kMaxCols; ++c) {
@@ -185,68 +191,88 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
 #pragma unroll
         for (int b = 0; b < kBatch; ++b) {
             const int k = k0 + b;
-            if (k < kprobe) {
+            if (k < k_end) {
                 const unsigned long long m = __ballot(hit[b]);
                 if (writer) cnt[(int64_t)k * G + g] = __popcll(m);
                 if (j < n_out) nbr[(int64_t)k * n_out + j] = hit[b] ? row[b] : -1;
                 // the mirrored pair (j, row) at offset K-1-k
-                if (self && hit[b] && row[b] >= 0 && row[b] < n_out) nbr[(int64_t)(K - 1 - k) * n_out + row[b]] = (int32_t)j;
+                if (k < mirror_end && hit[b] && row[b] >= 0 && row[b] < n_out)
+                    nbr[(int64_t)(K - 1 - k) * n_out + row[b]] = (int32_t)j;
+                // the middle offset of a self map pairs every row with itself
+                if (k == mid) {
+                    const unsigned long long bad = __ballot(j < n_out && !(hit[b] && row[b] == j));
+                    if (bad && __lane_id() == 0) atomicOr(not_self, 1);
+                }
             }
         }
     }
-    if (self) {   // the middle offset: every row with itself
-        const int c = kprobe;
-        const unsigned long long m = __ballot(j < n_out);
-        if (writer) cnt[(int64_t)c * G + g] = __popcll(m);
-        if (j < n_out) nbr[(int64_t)c * n_out + j] = (int32_t)j;
-    }
 }
 
-// Whether a map onto out_coords over a symmetric region (sym) is a map of the
-// table's own coordinate set onto itself.
-__device__ __forceinline__ bool self_map(const TableHeader* h, int ncol, const int32_t* out_coords, int64_t n_out,
-                                         int sym) {
-    return sym && header_ok(h, ncol) && h->src == out_coords && h->n == n_out;
+// Whether a map onto out_coords over a symmetric listing (sym) may be a map
+// of the table's coordinate set onto itself: the table is valid and has as
+// many rows as the output.  The count pass checks the rest (row j finds row j).
+__device__ __forceinline__ bool self_candidate(const TableHeader* h, int ncol, int64_t n_out, int sym) {
+    return sym && header_ok(h, ncol) && h->n == n_out;
 }
 
 template <typename Offs>
 __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* __restrict__ out_coords,
                                                          int64_t n_out, int ncol, Offs offs, int K, int sym, int64_t G,
                                                          int32_t* __restrict__ cnt, int32_t* __restrict__ nbr,
-                                                         int64_t* err) {
+                                                         int64_t* err, int32_t* not_self) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
     const Slot* __restrict__ slots = table_slots(table);
     const bool ok = header_ok(h, ncol);
     if (blockIdx.x == 0 && threadIdx.x == 0) *err = ok ? 0 : 1;
-    const bool self = self_map(h, ncol, out_coords, n_out, sym);
-    const int kprobe = self ? (K - 1) / 2 : K;
+    const bool self = self_candidate(h, ncol, n_out, sym);
+    const int k_end = self ? (K + 1) / 2 : K;        // up to and including the middle offset
+    const int mirror_end = self ? (K - 1) / 2 : 0;   // offsets whose hits are mirrored
+    const int mid = self ? (K - 1) / 2 : -1;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     if (h->total_bits <= 32)   // uniform: all lanes take the same path
-        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, kprobe, self, G, cnt, nbr, ok, j);
+        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok,
+                             j, not_self);
     else
-        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, kprobe, self, G, cnt, nbr, ok, j);
+        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt,
+                                       nbr, ok, j, not_self);
 }
 
-// Self map: the mirrored offsets' rows of the neighbour table start empty.
-__global__ void __launch_bounds__(kThreads) k_kmap_self_init(const void* table, const int32_t* out_coords,
-                                                             int64_t n_out, int ncol, int K, int sym,
-                                                             int32_t* __restrict__ nbr) {
+// Symmetric listing: clear the self-map check, and if the map may be a self
+// map, start the mirrored offsets' rows of the neighbour table empty.
+__global__ void __launch_bounds__(kThreads) k_kmap_self_init(const void* table, int64_t n_out, int ncol, int K,
+                                                             int sym, int32_t* __restrict__ nbr,
+                                                             int32_t* __restrict__ not_self) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    if (!self_map(h, ncol, out_coords, n_out, sym)) return;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *not_self = 0;
+    if (!self_candidate(h, ncol, n_out, sym)) return;
     const int64_t first = (int64_t)((K + 1) / 2) * n_out, n = (int64_t)(K / 2) * n_out;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         nbr[first + i] = -1;
 }
 
-// Self map: pair counts of the mirrored offsets per 64-row group, from the
-// neighbour table.
-__global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* table, const int32_t* out_coords,
-                                                                int64_t n_out, int ncol, int K, int sym, int64_t G,
-                                                                const int32_t* __restrict__ nbr,
-                                                                int32_t* __restrict__ cnt) {
+// Symmetric listing, second pass over the offsets after the middle one: for a
+// self map (the count pass found every row at its own index) their pair
+// counts per 64-row group come from the mirrored entries of the neighbour
+// table; otherwise every row probes them itself.
+template <typename Offs>
+__global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* table,
+                                                                const int32_t* __restrict__ out_coords, int64_t n_out,
+                                                                int ncol, Offs offs, int K, int sym, int64_t G,
+                                                                int32_t* __restrict__ nbr, int32_t* __restrict__ cnt,
+                                                                int32_t* not_self) {
     const TableHeader* h = reinterpret_cast<const TableHeader*>(table);
-    if (!self_map(h, ncol, out_coords, n_out, sym)) return;
+    if (!self_candidate(h, ncol, n_out, sym)) return;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+    if (*not_self) {
+        const Slot* __restrict__ slots = table_slots(table);
+        if (h->total_bits <= 32)
+            count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true,
+                                 j, not_self);
+        else
+            count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt,
+                                           nbr, true, j, not_self);
+        return;
+    }
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
     constexpr int B = 8;
@@ -303,21 +329,22 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
                         int sym, int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg,
                         int64_t* gidx, int64_t* n_pairs, int64_t* res, int32_t* cnt, int32_t* nbr, void* scan_ws,
                         hipStream_t s) {
+    int32_t* not_self = reinterpret_cast<int32_t*>(res + 2);
     const unsigned nblk = (unsigned)((n_out + kThreads - 1) / kThreads);
     if (nblk > 0) {
         if (sym && K > 1) {   // whether the map is a self map is read from the table on the device
             const int64_t n_init = (int64_t)(K / 2) * n_out;
             const int64_t gi = (n_init + kThreads - 1) / kThreads;
-            hipLaunchKernelGGL(k_kmap_self_init, dim3((unsigned)(gi < 4096 ? gi : 4096)), dim3(kThreads), 0, s, in_table, out_coords,
-                               n_out, ncol, K, sym, nbr);
+            hipLaunchKernelGGL(k_kmap_self_init, dim3((unsigned)(gi < 4096 ? (gi > 0 ? gi : 1) : 4096)), dim3(kThreads), 0,
+                               s, in_table, n_out, ncol, K, sym, nbr, not_self);
             GSC_LAUNCH_CHECK();
         }
         hipLaunchKernelGGL((k_kmap_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol,
-                           offs, K, sym, G, cnt, nbr, res + 1);
+                           offs, K, sym, G, cnt, nbr, res + 1, not_self);
         GSC_LAUNCH_CHECK();
         if (sym && K > 1) {
-            hipLaunchKernelGGL(k_kmap_mirror_count, dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out,
-                               ncol, K, sym, G, nbr, cnt);
+            hipLaunchKernelGGL((k_kmap_mirror_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords,
+                               n_out, ncol, offs, K, sym, G, nbr, cnt, not_self);
             GSC_LAUNCH_CHECK();
         }
     }
@@ -347,40 +374,20 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
     return GSC_OK;
 }
 
-}  // namespace gsc
-
-using namespace gsc;
-
-extern "C" {
-
-int64_t gsc_kmap_groups(int64_t n_out) { return n_out <= 0 ? 0 : (n_out + 63) / 64; }
-
-size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D) {
-    if (n_out < 0 || K < 1 || D < 1) return 0;
-    const int64_t G = gsc_kmap_groups(n_out);
-    size_t b = align256((size_t)K * D * sizeof(int32_t));      // offsets (scaled)
-    b += align256(2 * sizeof(int64_t));                         // total, error flag
-    b += align256((size_t)K * G * sizeof(int32_t));             // counts
-    b += align256((size_t)K * n_out * sizeof(int32_t));         // neighbour table
-    b += scan_ws_bytes(K * G);
-    return b + 256;
-}
-
-int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D, const int32_t* offsets,
-                   int32_t K, const int32_t* tensor_stride, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
-                   int64_t* seg, int64_t* gidx, int32_t* nbr_out, int64_t* n_pairs, void* ws, size_t ws_bytes,
-                   void* stream) {
-    clear_error();
+// Host-side checks and the offsets scaled by the tensor stride (by value in
+// `arg` when K * D <= kOffArgMax, always in `offs`); sym = the listing is
+// symmetric (K odd, o_{K-1-k} = -o_k, the origin in the middle).
+static int kmap_prepare(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D,
+                        const int32_t* offsets, int32_t K, const int32_t* tensor_stride, int32_t* in_idx,
+                        int32_t* out_idx, int64_t cap_pairs, int64_t* seg, int64_t* gidx, int64_t* n_pairs,
+                        OffsArg& arg, std::vector<int32_t>& offs, int& sym) {
     if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "kernel_map: D=%d outside [1,%d]", D, kMaxCols - 1);
     if (K < 1) return fail(GSC_EINVAL, "kernel_map: K=%d must be >= 1", K);
     if (n_out < 0 || n_out > INT32_MAX) return fail(GSC_EINVAL, "kernel_map: n_out=%lld invalid", (long long)n_out);
-    if (!in_table || !offsets || !seg || !gidx || !ws)
-        return fail(GSC_EINVAL, "kernel_map: null in_table/offsets/seg/gidx/ws");
+    if (!in_table || !offsets || !seg || !gidx) return fail(GSC_EINVAL, "kernel_map: null in_table/offsets/seg/gidx");
     if (n_out > 0 && !out_coords) return fail(GSC_EINVAL, "kernel_map: out_coords is null");
     if (cap_pairs < 0) return fail(GSC_EINVAL, "kernel_map: cap_pairs < 0");
     if (cap_pairs > 0 && (!in_idx || !out_idx)) return fail(GSC_EINVAL, "kernel_map: null in_idx/out_idx");
-    if (ws_bytes < gsc_kmap_ws_bytes(n_out, K, D))
-        return fail(GSC_ESHORT, "kernel_map: ws needs %zu bytes, got %zu", gsc_kmap_ws_bytes(n_out, K, D), ws_bytes);
     const bool by_value = (int64_t)K * D <= kOffArgMax;
     if (!n_pairs) {   // asynchronous mode
         if (cap_pairs < (int64_t)K * n_out)
@@ -389,10 +396,8 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
         if (!by_value)
             return fail(GSC_EINVAL, "kernel_map: asynchronous mode needs K*D <= %d (got %d)", kOffArgMax, K * D);
     }
-    OffsArg arg;
-    std::vector<int32_t> offs((size_t)K * D);
-    // symmetric listing: K odd, the middle offset the origin, o_{K-1-k} = -o_k
-    int sym = K % 2 == 1 ? 1 : 0;
+    offs.assign((size_t)K * D, 0);
+    sym = K % 2 == 1 ? 1 : 0;
     for (int k = 0; k < K && sym; ++k)
         for (int d = 0; d < D; ++d) {
             const int32_t a = offsets[(size_t)k * D + d], b = offsets[(size_t)(K - 1 - k) * D + d];
@@ -408,6 +413,43 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
             offs[(size_t)k * D + d] = (int32_t)v;
             if (by_value) arg.v[(size_t)k * D + d] = (int32_t)v;
         }
+    return GSC_OK;
+}
+
+}  // namespace gsc
+
+using namespace gsc;
+
+extern "C" {
+
+int64_t gsc_kmap_groups(int64_t n_out) { return n_out <= 0 ? 0 : (n_out + 63) / 64; }
+
+size_t gsc_kmap_ws_bytes(int64_t n_out, int32_t K, int32_t D) {
+    if (n_out < 0 || K < 1 || D < 1) return 0;
+    const int64_t G = gsc_kmap_groups(n_out);
+    size_t b = align256((size_t)K * D * sizeof(int32_t));      // offsets (scaled)
+    b += align256(3 * sizeof(int64_t));                         // total, error flag, self-map check
+    b += align256((size_t)K * G * sizeof(int32_t));             // counts
+    b += align256((size_t)K * n_out * sizeof(int32_t));         // neighbour table
+    b += scan_ws_bytes(K * G);
+    return b + 256;
+}
+
+int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D, const int32_t* offsets,
+                   int32_t K, const int32_t* tensor_stride, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
+                   int64_t* seg, int64_t* gidx, int32_t* nbr_out, int64_t* n_pairs, void* ws, size_t ws_bytes,
+                   void* stream) {
+    clear_error();
+    if (!ws) return fail(GSC_EINVAL, "kernel_map: null ws");
+    if (ws_bytes < gsc_kmap_ws_bytes(n_out, K, D))
+        return fail(GSC_ESHORT, "kernel_map: ws needs %zu bytes, got %zu", gsc_kmap_ws_bytes(n_out, K, D), ws_bytes);
+    OffsArg arg;
+    std::vector<int32_t> offs;
+    int sym = 0;
+    int rc = kmap_prepare(in_table, out_coords, n_out, D, offsets, K, tensor_stride, in_idx, out_idx, cap_pairs, seg,
+                          gidx, n_pairs, arg, offs, sym);
+    if (rc) return rc;
+    const bool by_value = (int64_t)K * D <= kOffArgMax;
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int ncol = D + 1;
@@ -415,8 +457,8 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     char* w = reinterpret_cast<char*>(ws);
     int32_t* d_offs = reinterpret_cast<int32_t*>(w);
     w += align256((size_t)K * D * sizeof(int32_t));
-    int64_t* res = reinterpret_cast<int64_t*>(w);   // res[0] = total, res[1] = header error
-    w += align256(2 * sizeof(int64_t));
+    int64_t* res = reinterpret_cast<int64_t*>(w);   // res[0] = total, res[1] = header error, res[2] = self check
+    w += align256(3 * sizeof(int64_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += align256((size_t)K * G * sizeof(int32_t));
     int32_t* nbr = nbr_out ? nbr_out : reinterpret_cast<int32_t*>(w);   // the caller's dense map, if asked for

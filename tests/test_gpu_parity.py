@@ -120,16 +120,12 @@ def _conv_case(coords, ci, co, offs, seed, dtype="f32", ts=1):
     return km
 
 
-def _map_arrays(km):
-    m = km.count()
-    return (to_np(km.in_idx[:m]), to_np(km.out_idx[:m]), to_np(km.seg), to_np(km.gidx), to_np(km.nbr))
-
-
 @pytest.mark.parametrize("case", ["cube3", "cube5", "cross3", "hybrid4d", "cube3_ts2", "sync_async"])
 def test_self_map_matches_copy(case):
-    """A map of the table's own coordinate array onto itself over a symmetric
-    region probes half the offsets and mirrors the rest; it must equal the map
-    onto a copy of the array (which probes every offset) bit for bit, and the
+    """A map of the table's own coordinate set onto itself over a symmetric
+    listing probes half the offsets and mirrors the rest; it must equal the
+    map over the same offsets listed in another (non-symmetric) order, which
+    probes every offset, bit for bit once the order is undone, and the
     oracle's map."""
     if case == "hybrid4d":
         wl = WL.make_workload(3, scale=0.3)
@@ -147,17 +143,60 @@ def test_self_map_matches_copy(case):
     table = gsc.gsc_coords_build(coords)
     self_map = gsc.gsc_kernel_map(table, coords, offs, tensor_stride=ts, dense=True,
                                   sync=case != "sync_async")
-    copy_map = gsc.gsc_kernel_map(table, coords.clone(), offs, tensor_stride=ts, dense=True)
+    rolled = np.roll(np.asarray(offs), 1, axis=0)                   # not a symmetric listing: full probe
+    full_map = gsc.gsc_kernel_map(table, coords, rolled, tensor_stride=ts, dense=True)
     torch.cuda.synchronize()
-    a, b = _map_arrays(self_map), _map_arrays(copy_map)
-    for x, y in zip(a, b):
-        assert np.array_equal(x, y)
+    K = len(offs)
+    a, b = gpu_pairs(self_map), gpu_pairs(full_map)
+    for k in range(K):
+        assert np.array_equal(a[k][0], b[(k + 1) % K][0]) and np.array_equal(a[k][1], b[(k + 1) % K][1])
+    n = wl.n
+    assert np.array_equal(to_np(self_map.nbr), np.roll(to_np(full_map.nbr).reshape(K, n), -1, axis=0))
     c_np = to_np(coords)
     ref = O.kernel_map(c_np, c_np, np.asarray(offs), ts or 1)
-    got = gpu_pairs(self_map)
-    for k in range(len(offs)):
-        assert np.array_equal(got[k][0], np.asarray(ref[k][0])) and np.array_equal(got[k][1], np.asarray(ref[k][1]))
-    _say(f"  {case}: K={len(offs)} pairs={self_map.count()}")
+    for k in range(K):
+        assert np.array_equal(a[k][0], np.asarray(ref[k][0])) and np.array_equal(a[k][1], np.asarray(ref[k][1]))
+    check_gidx(self_map)
+    _say(f"  {case}: K={K} pairs={self_map.count()}")
+
+
+@pytest.mark.parametrize("change", ["shift_in_place", "permuted_copy", "two_rows_swapped", "one_row_moved"])
+def test_self_map_premise_checked(change):
+    """Output coordinates that are not the table's rows in the table's order,
+    though as many: rows rewritten in place after the build (the same
+    pointer), the rows in another order, two rows swapped, one row moved to a
+    free coordinate.  The map must still be the full probe's, i.e. the
+    oracle's map from the coordinates the table was built from to the output
+    coordinates."""
+    wl = WL.make_workload(1, scale=0.15)
+    offs = regions.hypercube(3, 3)
+    coords = torch.from_numpy(wl.coords.copy()).to(DEV)
+    table = gsc.gsc_coords_build(coords)
+    base = wl.coords.copy()
+    if change == "shift_in_place":
+        coords[:, 1] += 1                                             # same array, new values
+    elif change == "permuted_copy":
+        perm = np.random.default_rng(5).permutation(wl.n)
+        coords = torch.from_numpy(base[perm]).to(DEV)
+    elif change == "two_rows_swapped":
+        c2 = base.copy()
+        c2[[10, 500]] = c2[[500, 10]]
+        coords.copy_(torch.from_numpy(c2))
+    else:
+        c2 = base.copy()
+        c2[77, 1:] = base[:, 1:].max(0) + 5                          # outside every neighbourhood
+        coords.copy_(torch.from_numpy(c2))
+    for sync in (True, False):
+        km = gsc.gsc_kernel_map(table, coords, offs, dense=True, sync=sync)
+        torch.cuda.synchronize()
+        ref = O.kernel_map(base, to_np(coords).astype(np.int64), offs)
+        maps_equal_exact(gpu_pairs(km), ref)
+        check_gidx(km)
+        nb = to_np(km.nbr).astype(np.int64)
+        for k, (ri, ro) in enumerate(ref):
+            row = np.full(wl.n, -1)
+            row[np.asarray(ro, np.int64)] = ri
+            assert np.array_equal(nb[k], row)
 
 
 def test_empty_input():
