@@ -201,6 +201,30 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
                    int64_t* seg, int64_t* gidx, int32_t* nbr, int64_t* n_pairs,
                    void* ws, size_t ws_bytes, void* stream);
 
+/* Allocation-free kernel map, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): gsc_kernel_map in its asynchronous mode (never synchronises;
+ * cap_pairs >= K * n_out, K * D <= 768; the total is left on the device in
+ * seg[K] = gidx[K*G]) with the dense form nbr (device, K * n_out int32)
+ * required, and no workspace argument: the per-(offset, group) counts, the
+ * scan partials and the status words live in a device array that the
+ * library holds, gsc_kernel_map_noalloc_bytes(n_out, K) of its 8 MiB (each
+ * GPU the library runs on holds its own copy until the process ends).  The
+ * call allocates and frees nothing; it needs every count and flag it reads to
+ * be written by itself first, so the array's contents from an earlier call do
+ * not matter.  All calls on one GPU share that GPU's array: calls that
+ * overlap on one GPU (on different streams, or from several threads) race and
+ * must be serialised by the caller.  The stream must belong to the current
+ * device.  Arguments and results otherwise as gsc_kernel_map.  Errors:
+ * EINVAL (as gsc_kernel_map, and a null nbr), ESHORT (cap_pairs below
+ * K * n_out), ERANGE (more scratch than the 8 MiB, e.g. n_out above about
+ * 4.9 M rows at K = 27: then call gsc_kernel_map with a workspace), EHIP. */
+size_t gsc_kernel_map_noalloc_bytes(int64_t n_out, int32_t K);
+int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D,
+                           const int32_t* offsets, int32_t K, const int32_t* tensor_stride,
+                           int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
+                           int64_t* seg, int64_t* gidx, int32_t* nbr, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Block plan of a kernel map (an ordering of the output rows for a4 - a6). */
 /* ------------------------------------------------------------------------ */

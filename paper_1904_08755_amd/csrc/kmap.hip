@@ -27,6 +27,7 @@
 // the second pass probes the mirrored offsets itself instead, overwriting
 // their entries, so the result equals the full probe in every case.
 #include <climits>
+#include <mutex>
 #include <vector>
 
 #include "gsc_internal.h"
@@ -416,6 +417,33 @@ static int kmap_prepare(const void* in_table, const int32_t* out_coords, int64_t
     return GSC_OK;
 }
 
+// Scratch of the allocation-free kernel map: a device array of fixed size in
+// the library's code object.  Each GPU holds its own copy at its own address,
+// taken once per device with hipGetSymbolAddress (the array's name is not a
+// device address in host code).  Calls on one GPU share it, so calls that
+// overlap on one GPU race.
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+static int noalloc_scratch(char** out) {
+    int dev = -1;
+    GSC_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(GSC_EINVAL, "kernel_map_noalloc: device %d unsupported", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        GSC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(GSC_EHIP, "kernel_map_noalloc: no address for the scratch array on device %d", dev);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = reinterpret_cast<char*>(g_scratch_ptr[dev]);
+    return GSC_OK;
+}
+
 }  // namespace gsc
 
 using namespace gsc;
@@ -471,6 +499,42 @@ int gsc_kernel_map(const void* in_table, const int32_t* out_coords, int64_t n_ou
     GSC_HIP(hipMemcpyAsync(d_offs, offs.data(), offs.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
     return kmap_enqueue(in_table, out_coords, n_out, ncol, OffsPtr{d_offs}, K, sym, G, in_idx, out_idx, cap_pairs,
                         seg, gidx, n_pairs, res, cnt, nbr, scan_ws, s);
+}
+
+size_t gsc_kernel_map_noalloc_bytes(int64_t n_out, int32_t K) {
+    if (n_out < 0 || K < 1) return 0;
+    const int64_t G = gsc_kmap_groups(n_out);
+    return align256(3 * sizeof(int64_t)) + align256((size_t)K * G * sizeof(int32_t)) + scan_ws_bytes(K * G);
+}
+
+int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int64_t n_out, int32_t D,
+                           const int32_t* offsets, int32_t K, const int32_t* tensor_stride, int32_t* in_idx,
+                           int32_t* out_idx, int64_t cap_pairs, int64_t* seg, int64_t* gidx, int32_t* nbr,
+                           void* stream) {
+    clear_error();
+    if (!nbr) return fail(GSC_EINVAL, "kernel_map_noalloc: the dense form nbr is required");
+    const size_t need = gsc_kernel_map_noalloc_bytes(n_out, K);
+    if (n_out >= 0 && K >= 1 && need > kNoAllocScratchBytes)
+        return fail(GSC_ERANGE, "kernel_map_noalloc: needs %zu bytes of scratch, the library holds %zu per GPU "
+                    "(n_out=%lld, K=%d); use gsc_kernel_map with a workspace", need, kNoAllocScratchBytes,
+                    (long long)n_out, K);
+    OffsArg arg;
+    std::vector<int32_t> offs;
+    int sym = 0;
+    int rc = kmap_prepare(in_table, out_coords, n_out, D, offsets, K, tensor_stride, in_idx, out_idx, cap_pairs, seg,
+                          gidx, nullptr, arg, offs, sym);
+    if (rc) return rc;
+    char* w = nullptr;
+    rc = noalloc_scratch(&w);
+    if (rc) return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int64_t G = gsc_kmap_groups(n_out);
+    int64_t* res = reinterpret_cast<int64_t*>(w);
+    w += align256(3 * sizeof(int64_t));
+    int32_t* cnt = reinterpret_cast<int32_t*>(w);
+    w += align256((size_t)K * G * sizeof(int32_t));
+    return kmap_enqueue(in_table, out_coords, n_out, D + 1, arg, K, sym, G, in_idx, out_idx, cap_pairs, seg, gidx,
+                        nullptr, res, cnt, nbr, w, s);
 }
 
 }  // extern "C"

@@ -54,6 +54,9 @@ _SIGS = {
     "gsc_kmap_ws_bytes": (_sz, [_i64, _i32, _i32]),
     "gsc_kernel_map": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp, _vp,
                                       _vp, _c_i64p, _vp, _sz, _vp]),
+    "gsc_kernel_map_noalloc_bytes": (_sz, [_i64, _i32]),
+    "gsc_kernel_map_noalloc": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp,
+                                              _vp, _vp, _vp]),
     "gsc_plan_blocks": (_i64, [_i64]),
     "gsc_conv_plan_ws_bytes": (_sz, [_i64, _i32]),
     "gsc_conv_plan": (ctypes.c_int, [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
@@ -263,6 +266,33 @@ def gsc_kernel_map(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, te
         m = n_pairs.value
         return KernelMap(bufs.in_idx[:m], bufs.out_idx[:m], bufs.seg, bufs.gidx, m, n_out, offs, m, nbr)
     return KernelMap(bufs.in_idx, bufs.out_idx, bufs.seg, bufs.gidx, None, n_out, offs, bufs.cap, nbr)
+
+
+def gsc_kernel_map_noalloc(in_table: torch.Tensor, out_coords: torch.Tensor, offsets, bufs: MapBuffers,
+                           tensor_stride=None, stream=None, host_offsets=None, host_ts=None) -> KernelMap:
+    """gsc_kernel_map in its asynchronous mode without a workspace: the
+    library's own per-GPU scratch array serves instead (for callers that
+    cannot allocate).  ``bufs`` must hold the dense form (MapBuffers(...,
+    dense=True)); its ``ws`` is not used."""
+    _need(in_table, torch.uint8, "in_table", 1)
+    _need(out_coords, torch.int32, "out_coords", 2)
+    offs = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    K, D = offs.shape
+    n_out = out_coords.shape[0]
+    if out_coords.shape[1] != D + 1:
+        raise ValueError("offsets must be K x D with D = out_coords columns - 1")
+    if bufs.nbr is None or bufs.nbr.numel() < K * n_out:
+        raise ValueError("gsc_kernel_map_noalloc needs MapBuffers(..., dense=True) for n_out rows")
+    if host_offsets is None:
+        host_offsets = _host_i32(offs)
+    if host_ts is None and tensor_stride is not None:
+        host_ts = _host_i32([tensor_stride] * D if np.isscalar(tensor_stride) else tensor_stride)
+    rc = lib().gsc_kernel_map_noalloc(_ptr(in_table), _ptr(out_coords), n_out, D, host_offsets, K, host_ts,
+                                      _ptr(bufs.in_idx), _ptr(bufs.out_idx), bufs.cap, _ptr(bufs.seg),
+                                      _ptr(bufs.gidx), _ptr(bufs.nbr), _stream(stream))
+    _check(rc)
+    return KernelMap(bufs.in_idx, bufs.out_idx, bufs.seg, bufs.gidx, None, n_out, offs, bufs.cap,
+                     bufs.nbr[: K * n_out].view(K, n_out))
 
 
 def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offsets, tensor_stride=None,
