@@ -87,7 +87,9 @@ def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool, epi
     dt = gsc.GSC_BF16 if dtype == "bf16" else gsc.GSC_F32
     ep = "true" if epilogue else "false"
     if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
-        if dtype == "bf16":   # 256 output columns run as two 128-column workgroups per tile
+        if dtype == "bf16":
+            if K <= 30:   # the tile engine (16 blocks by all output columns per workgroup)
+                return f"k_conv_tile_bf16<{ci}, {co}, gsc::WIdentity, {ep}>"
             return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity, {ep}>"
         return f"k_conv_blk_f32<{ci}, {co}, false, {ep}>"
     if dtype == "bf16":

@@ -272,9 +272,10 @@ int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32
 /* a4 / a5. Convolution forward (Alg. 2), transposed convolution.           */
 /* ------------------------------------------------------------------------ */
 /* Workspace bytes for gsc_sparse_conv_fwd (0 when none is needed).  The
- * bfloat16 engine for wide layers (c_in in {32, 64, 128, 256}, c_out in {64,
- * 128, 256}, K <= 64) keeps a transposed copy of W there:
- * K * c_in * c_out * 2 bytes. */
+ * bfloat16 engines for wide layers (c_in in {32, 64, 128, 256}, c_out in {64,
+ * 128, 256}, K <= 64) keep a transposed copy of W there (K * c_in * c_out * 2
+ * bytes, rounded up to 256) followed by 256 bytes for the counter with which
+ * the block engine hands out its tiles. */
 size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t K);
 
 /* Y = 0; for every offset k and pair p of it: Y[out_idx[p]] += X[in_idx[p]] W[k].
@@ -348,7 +349,9 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
  * gsc_conv_block_engine(dtype, c_out, c_in, K) is 1.
  * dX (nullable: skip) has X's dtype; dW (nullable: skip) is float32.  Both are
  * overwritten.  ws: gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K) bytes (only
- * needed when dW is computed).  The dW reduction order is fixed, so dW is
+ * needed when dW is computed; given in full, it also holds the counter with
+ * which the bfloat16 block engine of dX hands out its tiles, large ones
+ * first: without it dX takes longer).  The dW reduction order is fixed, so dW is
  * deterministic.  Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY,
                         int64_t n_in, int32_t c_in, int32_t c_out, int32_t K,

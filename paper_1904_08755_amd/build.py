@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgsc.so")
 SOURCES = ["common.hip", "coords.hip", "kmap.hip", "plan.hip", "conv.hip", "conv_bf16.hip", "conv_blk.hip",
-           "pool.hip"]
+           "conv_tile.hip", "pool.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

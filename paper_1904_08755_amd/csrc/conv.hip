@@ -736,9 +736,15 @@ static bool fwd_uses_bf16_engine(int32_t dtype, int32_t c_in, int32_t c_out, int
     return dtype == GSC_BF16 && conv_bf16_supported(c_in, c_out, K);
 }
 
+// Workspace of the forward pass: the bf16 engines' transposed weights, then
+// (tile engine) the tile counter.
+static size_t fwd_counter_offset(int32_t c_in, int32_t c_out, int32_t K) {
+    return (transpose_ws_bytes(K, c_in, c_out) + 255) & ~(size_t)255;
+}
+
 size_t gsc_conv_fwd_ws_bytes(int32_t dtype, int32_t c_in, int32_t c_out, int32_t K) {
     if (c_in < 1 || c_out < 1 || K < 1) return 0;
-    return fwd_uses_bf16_engine(dtype, c_in, c_out, K) ? transpose_ws_bytes(K, c_in, c_out) : 0;
+    return fwd_uses_bf16_engine(dtype, c_in, c_out, K) ? fwd_counter_offset(c_in, c_out, K) + 256 : 0;
 }
 
 // The plan (perm, bmask, ibase, items) is all given or all null (checked
@@ -786,6 +792,13 @@ static int conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, co
         if (dtype == GSC_BF16) {   // B_k = W[k]: the engine reads its columns, so the transposed copy
             rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
             if (rc) return rc;
+            if (n_in > 0 && tile_bf16_supported(c_in, c_out, K)) {
+                unsigned* counter = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
+                                                                fwd_counter_offset(c_in, c_out, K));
+                return conv_tile_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan,
+                                                 (n_out + kPlanBlockRows - 1) / kPlanBlockRows, n_out, Y, counter, s,
+                                                 ep);
+            }
             return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s, ep);
         }
         static const WSel kNoSel{};
@@ -839,10 +852,16 @@ int gsc_sparse_conv_fwd_affine(int32_t dtype, const void* X, int64_t n_in, int32
                     Y, n_out, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream));
 }
 
+// Workspace of the backward pass: the weight gradient's chunk tables and
+// partial sums, then the tile counter of the input gradient's tile engine.
+static size_t bwd_counter_offset(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K) {
+    const int64_t items = dw_items_bound(n_pairs, K, dw_chunk(c_in, c_out));
+    return 2 * al256((size_t)(K + 1) * sizeof(int64_t)) + al256((size_t)items * c_in * c_out * sizeof(float));
+}
+
 size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32_t K) {
     if (n_pairs < 0 || c_in < 1 || c_out < 1 || K < 1) return 0;
-    const int64_t items = dw_items_bound(n_pairs, K, dw_chunk(c_in, c_out));
-    return 2 * al256((size_t)(K + 1) * sizeof(int64_t)) + al256((size_t)items * c_in * c_out * sizeof(float)) + 256;
+    return bwd_counter_offset(n_pairs, c_in, c_out, K) + 256;
 }
 
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in, int32_t c_in,
@@ -877,7 +896,17 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         if (planned && gsc_conv_block_engine(dtype, c_out, c_in, K) && aligned16(dY) && aligned16(W) &&
             (dtype != GSC_BF16 || blk_bf16_fits(n_out, c_out))) {
             const BlockPlan plan{t_perm, t_bmask, t_ibase, t_items};
-            if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
+            if (dtype == GSC_BF16 && n_out > 0 && tile_bf16_supported(c_out, c_in, K)) {
+                // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout.  The tile
+                // counter sits after the weight gradient's part of ws, when ws is given in full.
+                unsigned* counter = nullptr;
+                if (ws && n_pairs >= 0 && ws_bytes >= gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K))
+                    counter = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
+                                                          bwd_counter_offset(n_pairs, c_in, c_out, K));
+                rc = conv_tile_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan,
+                                          (n_in + kPlanBlockRows - 1) / kPlanBlockRows, n_in, dX, counter, s,
+                                          Epilogue{});
+            } else if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
                 rc = conv_blk_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan, n_in, dX, s);
             else
                 rc = conv_blk_f32(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,

@@ -44,6 +44,18 @@ template <typename Sel>
 int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
                   const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s, const Epilogue& ep = Epilogue{});
 
+// The bf16 tile engine (conv_tile.hip): the same product as conv_blk_bf16
+// for ca, cb in {64, 128, 256}, K <= 30, a tile of 16 blocks by all cb
+// columns per workgroup, persistent workgroups.  nb = number of plan blocks;
+// counter (nullable): 4 bytes of device memory the call uses to hand out
+// tiles (large ones first; without it the tiles go out in a fixed order).
+// n_x * ca below 2^30.  Asynchronous.
+bool tile_bf16_supported(int ca, int cb, int K);
+template <typename Sel>
+int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
+                   const BlockPlan& plan, int64_t nb, int64_t n_y, void* Y, unsigned* counter, hipStream_t s,
+                   const Epilogue& ep);
+
 // Y (n x c, float32 or bf16 by dtype) = the epilogue applied in place (the
 // row-form paths, whose sums are complete only in Y).  Asynchronous.
 int affine_act(int dtype, void* Y, int64_t n, int c, const Epilogue& ep, hipStream_t s);

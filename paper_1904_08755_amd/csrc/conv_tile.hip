@@ -1,0 +1,522 @@
+// bf16 tile engine for wide layers: the sum of Eq. 3 over a block plan, a
+// tile of 16 blocks (256 output positions) by all output columns per
+// workgroup, v_mfma_f32_16x16x32_bf16 with fp32 sums, bf16 output (nearest
+// even).
+//
+// The tile is computed step by step; a step is one offset k of the union of
+// the tile's block masks and 32 channels of the reduction.  Per step the
+// workgroup copies into LDS, with buffer loads that write LDS directly:
+//   - the 16 input rows of every block having k (32 channels of each: one
+//     load instruction of 64 lanes x 16 bytes per block; a block without k,
+//     or a position without a pair, reads out of range and so gets zeros),
+//   - the 32 x C_out slice of the offset's weight matrix.
+// Steps go through a ring of four LDS stages.  During step s the copies of
+// step s + 4 are issued into the stage step s has just left, the MFMA
+// operands of step s + 1 are read from LDS into registers, and the products
+// of step s run on the operands read during step s - 1; the step ends once
+// the copies of step s + 2 are complete (three steps after they were
+// issued).  The steps of an offset are unrolled, and what they need of the
+// offset (its blocks, its weight matrix, its input rows) is worked out once
+// per offset: the scalar instructions of the bookkeeping share the SIMD's
+// issue slots with the MFMAs.  Eight waves (two per SIMD) share the tile: wave (r, c) keeps the
+// sums of blocks [16/WR r, 16/WR (r+1)) by 64 output columns c in registers
+// and, for each block having k, multiplies the block's 16 x 32 rows by the
+// 32 x 64 weights (four MFMAs per block).  Every output row's products are
+// added in increasing offset order, so the result does not depend on the
+// plan's row order and is bit-reproducible.  The sums are written once,
+// through LDS, as whole bf16 rows.
+//
+// The grid is persistent (one workgroup per CU) and takes tiles from the
+// last to the first through a counter in device memory: tiles later in the
+// plan hold rows with more neighbours (the plan sorts rows by neighbour
+// mask), so the large tiles go out first and the small ones fill the gaps.
+// Without a counter the workgroups take tiles nt-1-g, nt-1-g-G, ... .
+//
+// LDS layout of a stage: block b's rows at b * 1 KiB, row r's 64 bytes at
+// r * 64 with 16-byte chunk c at ((c ^ ((r >> 1) & 3)) * 16); output column
+// n's 32 weights at n * 64, chunk c at ((c ^ ((n >> 1) & 3)) * 16).  The XOR
+// keeps the eight 16-byte reads that the LDS serves together in distinct
+// banks.  (A load instruction writes 16 bytes per lane at lane * 16 of its
+// destination, so the swizzle is applied to the chunk each lane fetches.)
+// The tile's item table (16 row indices per block and offset) sits in
+// dynamic LDS, 1 KiB per offset of the region.
+#include <type_traits>
+
+#include "conv_blk.h"
+
+namespace gsc {
+
+typedef __bf16 tbf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int tu32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 tbf16x2 __attribute__((ext_vector_type(2)));
+typedef float tfloatx2 __attribute__((ext_vector_type(2)));
+
+constexpr int kTileBlocks = 16;                         // blocks (of 16 positions) per tile
+constexpr int kTilePos = kTileBlocks * kPlanBlockRows;  // 256 positions
+constexpr int kTileThreads = 512;                       // eight waves
+constexpr int kTileStageBytes = 16384;                  // rows of a stage; weights of a stage at most as much
+constexpr int kTileMaxK = 30;                           // item table in the LDS left by the stages
+constexpr int kTileBufFlags = 0x00020000;               // buffer descriptor word 3: 32-bit data format
+constexpr uint32_t kTileNone = 0x80000000u;             // an offset past any buffer the engine reads
+
+// s_waitcnt operand: vmcnt(n) and lgkmcnt(0), expcnt left free (gfx9 encoding)
+template <int N>
+struct VmLgkmWait {
+    static constexpr int value = (N & 15) | ((N >> 4) << 14) | (7 << 4);
+};
+
+template <int CA, int CB>
+struct TileCfg {
+    static constexpr int WC = CB / 64;               // column groups of 64
+    static constexpr int WR = 8 / WC;                // position groups
+    static constexpr int BPW = kTileBlocks / WR;     // blocks per wave
+    static constexpr int NJ = 4;                     // 16-column blocks per wave
+    static constexpr int H = CA / 32;                // steps per offset
+    static constexpr int BINS = CB / 16;             // weight load instructions per step (1 KiB each)
+    static constexpr int BL = BINS >= 8 ? BINS / 8 : 1;   // ... per wave (dummies where BINS < 8)
+    static constexpr int LOADS = 2 + BL;             // load instructions per wave and step
+    static_assert(CB == 64 || CB == 128 || CB == 256, "output width");
+    static_assert(CA == 64 || CA == 128 || CA == 256, "reduction width");
+};
+
+__device__ __forceinline__ uint32_t tile_pack_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(tfloatx2{lo, hi}, tbf16x2));
+}
+// value of lane l ^ 1 (DPP quad_perm 1, 0, 3, 2)
+__device__ __forceinline__ float tile_xor1(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false));
+}
+__device__ __forceinline__ void tile_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// What the steps of one offset need (see the kernel): the offset k (-1:
+// none), which of a wave's blocks have it (bk), the byte offset of its
+// weight matrix (wb) and the lane's row offsets in the two copied blocks.
+struct OffState {
+    int k;
+    uint32_t bk, wb;
+    uint32_t vr[2];
+};
+
+template <int CA, int CB, typename Sel, bool EP>
+__global__ void __launch_bounds__(kTileThreads, 1)
+k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __restrict__ Bt, int K, Sel sel,
+                 const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
+                 const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
+                 int64_t ntiles, unsigned* __restrict__ counter, Epilogue ep, uint16_t* __restrict__ Y) {
+    using C = TileCfg<CA, CB>;
+    // four stages, each array its own object so that the compiler can tell
+    // the copies into one stage from the reads of another
+    __shared__ __attribute__((aligned(1024))) uint8_t sa0[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sa1[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sa2[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sa3[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sb0[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sb1[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sb2[kTileStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t sb3[kTileStageBytes];
+    __shared__ int32_t perm_s[kTilePos];
+    __shared__ int64_t next_s;                                          // the next tile to take
+    __shared__ __attribute__((aligned(1024))) uint8_t sdummy[1024];   // destination of copies that carry nothing
+    extern __shared__ __attribute__((aligned(16))) int32_t idx_s[];    // the tile's items: 16 K x 16 ints
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int wr = wave / C::WC, wc = wave % C::WC;
+    const int sel_lane = lane < K ? sel(lane) : 0;
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)(n_x * CA * 2), kTileBufFlags);
+    const __amdgpu_buffer_rsrc_t wrs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Bt, (short)0, (int)((int64_t)K * CB * CA * 2), kTileBufFlags);
+
+    // load lanes: row (or column) l / 4 of the instruction's 16, data chunk
+    // (l % 4) ^ swizzle, stored at l * 16 of the destination
+    const int lrow = lane >> 2;
+    const uint32_t lchunk = 16u * (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));
+    // weight columns this wave copies: instructions wave * BL + i (16 columns each)
+    uint32_t bcol[C::BL];
+#pragma unroll
+    for (int i = 0; i < C::BL; ++i) {
+        const int ins = wave * C::BL + i;
+        bcol[i] = ins < C::BINS ? (uint32_t)((16 * ins + lrow) * CA * 2) + lchunk : kTileNone;
+    }
+    // fragment read offsets: lane (r16, q) reads row (or column) r16, chunk q
+    const int r16 = lane & 15, q = lane >> 4;
+    const int frag = r16 * 64 + ((q ^ ((r16 >> 1) & 3)) * 16);
+
+    auto stage_a = [&](auto P) -> uint8_t* {
+        constexpr int p = decltype(P)::value;
+        return p == 0 ? sa0 : (p == 1 ? sa1 : (p == 2 ? sa2 : sa3));
+    };
+    auto stage_b = [&](auto P) -> uint8_t* {
+        constexpr int p = decltype(P)::value;
+        return p == 0 ? sb0 : (p == 1 ? sb1 : (p == 2 ? sb2 : sb3));
+    };
+
+    // tile sequence: from the counter (taken one tile ahead), else static
+    auto take = [&](int64_t i) -> int64_t {
+        const int64_t t = counter ? (int64_t)atomicAdd(counter, 1u) : i;
+        return t < ntiles ? ntiles - 1 - t : -1;
+    };
+    auto uniform = [](int64_t v) {   // a value every lane holds, as a scalar
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+        return (int64_t)(((uint64_t)hi << 32) | lo);
+    };
+    if (tid == 0) next_s = take(blockIdx.x);
+    __syncthreads();
+    int64_t tile = uniform(next_s);
+    for (int64_t round = 1; tile >= 0; ++round) {
+        const int64_t b0 = tile * kTileBlocks;
+        const int nbt = (int)min((int64_t)kTileBlocks, nb - b0);
+
+        // the tile's blocks (wave-uniform)
+        uint32_t bm[kTileBlocks];
+        int32_t ibl[kTileBlocks];
+        const int64_t ib0 = ibase[b0];
+        uint32_t U = 0;
+#pragma unroll
+        for (int b = 0; b < kTileBlocks; ++b) {
+            bm[b] = b < nbt ? bmask[b0 + b] : 0u;
+            ibl[b] = b < nbt ? (int32_t)(ibase[b0 + b] - ib0) : 0;
+            U |= bm[b];
+        }
+        const int n_items = (int)(ibase[b0 + nbt] - ib0);
+        // the previous tile's last reads of the LDS (item table, output
+        // rows, output staging, next tile) are done before they are overwritten
+        tile_barrier();
+        if (tid == 0) next_s = take(blockIdx.x + round * (int64_t)gridDim.x);
+        {   // the tile's items (at most 16 K x 16 ints): 16-byte loads, all in flight before any store
+            constexpr int kPer = (kTileBlocks * kTileMaxK * 4 + kTileThreads - 1) / kTileThreads;
+            const tu32x4* src = reinterpret_cast<const tu32x4*>(items + ib0 * 16);
+            const int last = n_items * 4 - 1;
+            if (last >= 0) {
+                tu32x4 v[kPer];
+#pragma unroll
+                for (int u = 0; u < kPer; ++u) v[u] = src[min(tid + u * kTileThreads, last)];
+#pragma unroll
+                for (int u = 0; u < kPer; ++u) asm volatile("" : "+v"(v[u]));   // all loads issued before any store
+#pragma unroll
+                for (int u = 0; u < kPer; ++u)
+                    if (tid + u * kTileThreads <= last) reinterpret_cast<tu32x4*>(idx_s)[tid + u * kTileThreads] = v[u];
+            }
+        }
+        if (tid < kTilePos) {
+            const int64_t pos = b0 * kPlanBlockRows + tid;
+            perm_s[tid] = pos < n_y ? perm[pos] : -1;
+        }
+        __syncthreads();   // items and output rows staged
+
+        // the blocks whose rows this wave copies: wave and wave + 8
+        uint32_t bmw[2];
+        int32_t iblw[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            bmw[j] = 0u;
+            iblw[j] = 0;
+#pragma unroll
+            for (int b = 0; b < kTileBlocks; ++b)
+                if (b == wave + 8 * j) {
+                    bmw[j] = bm[b];
+                    iblw[j] = ibl[b];
+                }
+        }
+        // the blocks whose sums this wave keeps: BPW wr .. BPW wr + BPW - 1
+        uint32_t bmv[C::BPW];
+#pragma unroll
+        for (int b = 0; b < C::BPW; ++b) {
+            bmv[b] = 0u;
+#pragma unroll
+            for (int r = 0; r < C::WR; ++r)
+                if (r == wr) bmv[b] = bm[C::BPW * r + b];
+        }
+
+        // Per-offset state (wave-uniform except the row offsets): the
+        // offset k (-1: none), which of this wave's blocks have it (bk), the
+        // byte offset of its weight matrix (wb) and the two copied blocks'
+        // row offsets for this lane (vr, kTileNone where there is no row).
+        // The steps of an iteration (L = max(4, H) steps: one offset, or two
+        // when an offset takes two steps) use the states of the current
+        // iteration, their copies four steps ahead those of the next one.
+        constexpr int H = C::H;
+        constexpr int L = H > 4 ? H : 4;    // steps per iteration
+        constexpr int NO = L / H;           // offsets per iteration
+        uint32_t urem = U;                  // offsets not yet taken
+        auto take_offset = [&](OffState& d) {
+            d.k = urem ? __ffs(urem) - 1 : -1;
+            urem &= urem - 1u;
+            const int k = d.k >= 0 ? d.k : 0;
+            d.bk = 0u;
+#pragma unroll
+            for (int b = 0; b < C::BPW; ++b) d.bk |= ((bmv[b] >> k) & 1u) << b;
+            d.bk = d.k >= 0 ? d.bk : 0u;
+            d.wb = (uint32_t)__builtin_amdgcn_readlane(sel_lane, k) * (uint32_t)(CB * CA * 2);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const uint32_t m = bmw[j];
+                const bool has = d.k >= 0 && ((m >> k) & 1u);
+                const int il = has ? iblw[j] + __popc(m & ((1u << k) - 1u)) : 0;
+                const int32_t r = idx_s[il * 16 + lrow];
+                d.vr[j] = has && r >= 0 && r < n_x ? (uint32_t)r * (uint32_t)(CA * 2) + lchunk : kTileNone;
+            }
+        };
+        // copies of part h of offset state d into stage P (C::LOADS instructions per wave, always)
+        auto issue = [&](const OffState& d, int h, auto P) {
+            uint8_t* sa = stage_a(P);
+            uint8_t* sb = stage_b(P);
+            const bool valid = d.k >= 0;
+            const uint32_t wbase = d.wb + (uint32_t)(h * 64);
+#pragma unroll
+            for (int i = 0; i < C::BL; ++i) {
+                const int ins = wave * C::BL + i;
+                const uint32_t off = valid ? bcol[i] : kTileNone;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    wrs, (__attribute__((address_space(3))) void*)(ins < C::BINS ? sb + ins * 1024 : sdummy), 16, off,
+                    wbase, 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const uint32_t off = d.vr[j];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    xr, (__attribute__((address_space(3))) void*)(sa + (wave + 8 * j) * 1024), 16, off, h * 64, 0, 0);
+            }
+        };
+
+        floatx4 acc[C::BPW][C::NJ];
+#pragma unroll
+        for (int b = 0; b < C::BPW; ++b)
+#pragma unroll
+            for (int j = 0; j < C::NJ; ++j) acc[b][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+        if (U != 0u) {
+            OffState dc[NO], dn[NO];   // offsets of the current and the next iteration
+#pragma unroll
+            for (int o = 0; o < NO; ++o) take_offset(dc[o]);
+#pragma unroll
+            for (int o = 0; o < NO; ++o) take_offset(dn[o]);
+            // operands in registers: the weights of two steps (this one and
+            // the next), the rows of one block at a time (a block's rows of
+            // the next step are read once its products of this step are
+            // issued)
+            tu32x4 bfr[2][C::NJ], afr[C::BPW];
+            issue(dc[0], 0, std::integral_constant<int, 0>{});
+            issue(dc[1 / H], 1 % H, std::integral_constant<int, 1>{});
+            issue(dc[2 / H], 2 % H, std::integral_constant<int, 2>{});
+            issue(dc[3 / H], 3 % H, std::integral_constant<int, 3>{});
+            __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);   // steps 0 and 1 copied
+            tile_barrier();
+#pragma unroll
+            for (int j = 0; j < C::NJ; ++j)
+                bfr[0][j] = *reinterpret_cast<const tu32x4*>(sb0 + (64 * wc + 16 * j) * 64 + frag);
+#pragma unroll
+            for (int b = 0; b < C::BPW; ++b)
+                if ((dc[0].bk >> b) & 1u)
+                    afr[b] = *reinterpret_cast<const tu32x4*>(sa0 + (C::BPW * wr + b) * 1024 + frag);
+            // every wave has read stage 0 before step 0 copies into it
+            __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);
+            tile_barrier();
+            // step j of the iteration (static): stage j % 4; copies of the
+            // step four ahead into that stage; operands of step j + 1 from
+            // stage (j + 1) % 4; products of step j; then wait for the copies
+            // of step j + 2
+            auto step = [&](auto J) {
+                constexpr int j = decltype(J)::value;
+                constexpr int st = j % 4, stn = (j + 1) % 4;
+                constexpr bool ahead_here = j + 4 < L;               // the step four ahead is in this iteration
+                constexpr int ja = ahead_here ? j + 4 : j + 4 - L;
+                if constexpr (ahead_here)
+                    issue(dc[ja / H], ja % H, std::integral_constant<int, st>{});
+                else
+                    issue(dn[ja / H], ja % H, std::integral_constant<int, st>{});
+                const uint8_t* san = stage_a(std::integral_constant<int, stn>{});
+                const uint8_t* sbn = stage_b(std::integral_constant<int, stn>{});
+#pragma unroll
+                for (int c = 0; c < C::NJ; ++c)
+                    bfr[(j + 1) & 1][c] = *reinterpret_cast<const tu32x4*>(sbn + (64 * wc + 16 * c) * 64 + frag);
+                const uint32_t bk = dc[j / H].bk;
+                // the next step has this step's offset: one test per block
+                constexpr bool same = j + 1 < L && (j + 1) % H != 0;
+                const uint32_t bn = j + 1 < L ? dc[((j + 1) % L) / H].bk : dn[0].bk;
+#pragma unroll
+                for (int b = 0; b < C::BPW; ++b) {
+                    if (same) {
+                        if ((bk >> b) & 1u) {
+#pragma unroll
+                            for (int c = 0; c < C::NJ; ++c)
+                                acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    __builtin_bit_cast(tbf16x8, afr[b]), __builtin_bit_cast(tbf16x8, bfr[j & 1][c]),
+                                    acc[b][c], 0, 0, 0);
+                            afr[b] = *reinterpret_cast<const tu32x4*>(san + (C::BPW * wr + b) * 1024 + frag);
+                        }
+                    } else {
+                        if ((bk >> b) & 1u) {
+#pragma unroll
+                            for (int c = 0; c < C::NJ; ++c)
+                                acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    __builtin_bit_cast(tbf16x8, afr[b]), __builtin_bit_cast(tbf16x8, bfr[j & 1][c]),
+                                    acc[b][c], 0, 0, 0);
+                        }
+                        if ((bn >> b) & 1u)
+                            afr[b] = *reinterpret_cast<const tu32x4*>(san + (C::BPW * wr + b) * 1024 + frag);
+                    }
+                }
+                // the copies of two steps on are complete, this step's operand reads done
+                __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);
+                tile_barrier();
+            };
+            static_assert(L % 4 == 0, "iterations of whole stage rounds");
+            while (true) {
+                step(std::integral_constant<int, 0>{});
+                step(std::integral_constant<int, 1>{});
+                step(std::integral_constant<int, 2>{});
+                step(std::integral_constant<int, 3>{});
+                if constexpr (L == 8) {
+                    step(std::integral_constant<int, 4>{});
+                    step(std::integral_constant<int, 5>{});
+                    step(std::integral_constant<int, 6>{});
+                    step(std::integral_constant<int, 7>{});
+                }
+#pragma unroll
+                for (int o = 0; o < NO; ++o) dc[o] = dn[o];
+                if (dc[0].k < 0) break;
+#pragma unroll
+                for (int o = 0; o < NO; ++o) take_offset(dn[o]);
+            }
+            __builtin_amdgcn_s_waitcnt(VmLgkmWait<0>::value);   // the trailing (empty) copies
+            tile_barrier();
+        }
+
+        // Write the tile through LDS, 64 positions per pass (rows 0-31 in
+        // stage array sa0, 32-63 in sa1): the sums become bf16 pairs (lane
+        // (c, q) holds rows 4q .. 4q+3 of column c; after an exchange with
+        // lane c ^ 1 an even lane holds rows 4q, 4q+1 of columns c, c+1 and an
+        // odd one rows 4q+2, 4q+3 of columns c-1, c), then whole output rows
+        // go out 16 bytes per lane.
+        constexpr int RB = CB * 2;                        // bytes per output row
+        constexpr int LPR = RB / 16;                      // lanes per output row
+        constexpr int RPI = kTileThreads / LPR;           // rows per copy iteration
+        static_assert(32 * RB <= kTileStageBytes, "32 output rows fit a stage array");
+        const bool odd = r16 & 1;
+        float esc[C::NJ], esh[C::NJ];
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j) {
+            const int col = 64 * wc + 16 * j + r16;
+            esc[j] = EP && ep.scale ? ep.scale[col] : 1.f;
+            esh[j] = EP && ep.shift ? ep.shift[col] : 0.f;
+        }
+#pragma unroll
+        for (int pass = 0; pass < kTileBlocks / 4; ++pass) {
+            if (pass) tile_barrier();   // the previous pass has been copied out
+#pragma unroll
+            for (int b = 0; b < C::BPW; ++b) {
+                const int blk = C::BPW * wr + b;
+                if (blk / 4 != pass) continue;   // blocks 4 pass .. 4 pass + 3
+                uint8_t* outb = (blk & 2) ? sa1 : sa0;   // rows 32 .. 63 of the pass in sa1
+#pragma unroll
+                for (int j = 0; j < C::NJ; ++j) {
+                    floatx4 v = acc[b][j];
+                    if constexpr (EP) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) v[i] = epi_apply(v[i], esc[j], esh[j], ep.relu);
+                    }
+                    const float e0 = tile_xor1(odd ? v[0] : v[2]);
+                    const float e1 = tile_xor1(odd ? v[1] : v[3]);
+                    const uint32_t p0 = odd ? tile_pack_bf16(e0, v[2]) : tile_pack_bf16(v[0], e0);
+                    const uint32_t p1 = odd ? tile_pack_bf16(e1, v[3]) : tile_pack_bf16(v[1], e1);
+                    const int row = 16 * (blk & 1) + 4 * q + (odd ? 2 : 0);   // 0 .. 31 within the array
+                    const int cb = (64 * wc + 16 * j + (r16 & ~1)) * 2;      // byte of the column pair
+                    *reinterpret_cast<uint32_t*>(outb + row * RB + cb) = p0;
+                    *reinterpret_cast<uint32_t*>(outb + (row + 1) * RB + cb) = p1;
+                }
+            }
+            tile_barrier();   // the pass is staged
+#pragma unroll
+            for (int r0 = 0; r0 < 64; r0 += RPI) {
+                const int pos = r0 + tid / LPR;
+                if (pos < 64) {
+                    const int32_t row = perm_s[64 * pass + pos];
+                    if (row >= 0 && row < n_y) {
+                        const uint8_t* src = (pos & 32) ? sa1 : sa0;
+                        const tu32x4 val = *reinterpret_cast<const tu32x4*>(src + (pos & 31) * RB + (tid % LPR) * 16);
+                        *reinterpret_cast<tu32x4*>(Y + (int64_t)row * CB + (tid % LPR) * 8) = val;
+                    }
+                }
+            }
+        }
+        tile = uniform(next_s);   // written before the item staging's barrier
+    }
+}
+
+// The tile counter starts at zero (a kernel, not a memset, so that the call
+// can be captured in a graph).
+__global__ void k_tile_counter_zero(unsigned* counter) { *counter = 0u; }
+
+bool tile_bf16_supported(int ca, int cb, int K) {
+    return (ca == 64 || ca == 128 || ca == 256) && (cb == 64 || cb == 128 || cb == 256) && K >= 1 && K <= kTileMaxK;
+}
+
+static int tile_grid_cap() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
+template <int CA, int CB, typename Sel, bool EP>
+static int launch_tile_kernel(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
+                              const BlockPlan& p, int64_t nb, int64_t n_y, const Epilogue& ep, uint16_t* Y,
+                              unsigned* counter, hipStream_t s) {
+    const int64_t tiles = (nb + kTileBlocks - 1) / kTileBlocks;
+    if (tiles == 0) return GSC_OK;
+    const int64_t grid = tiles < tile_grid_cap() ? tiles : tile_grid_cap();
+    const size_t dyn = (size_t)kTileBlocks * K * 16 * sizeof(int32_t);
+    auto kern = k_conv_tile_bf16<CA, CB, Sel, EP>;
+    GSC_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)dyn));
+    if (counter) {
+        hipLaunchKernelGGL(k_tile_counter_zero, dim3(1), dim3(1), 0, s, counter);
+        GSC_LAUNCH_CHECK();
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kTileThreads), dyn, s, X, n_x, Bt, K, sel, p.perm, p.bmask,
+                       p.ibase, p.items, nb, n_y, tiles, counter, ep, Y);
+    GSC_LAUNCH_CHECK();
+    return GSC_OK;
+}
+
+template <typename Sel>
+int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
+                   const BlockPlan& plan, int64_t nb, int64_t n_y, void* Y, unsigned* counter, hipStream_t s,
+                   const Epilogue& ep) {
+    auto X16 = reinterpret_cast<const uint16_t*>(X);
+    auto B16 = reinterpret_cast<const uint16_t*>(Bt);
+    auto Y16 = reinterpret_cast<uint16_t*>(Y);
+    const bool epi = std::is_same<Sel, WIdentity>::value && ep.on();   // the epilogue is a forward-pass option
+#define GSC_TILE_CASE(A, B)                                                                                    \
+    if (ca == A && cb == B) {                                                                                  \
+        if (epi)                                                                                               \
+            return launch_tile_kernel<A, B, Sel, true>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter, s); \
+        return launch_tile_kernel<A, B, Sel, false>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter, s);  \
+    }
+    GSC_TILE_CASE(64, 64) GSC_TILE_CASE(64, 128) GSC_TILE_CASE(64, 256) GSC_TILE_CASE(128, 64)
+    GSC_TILE_CASE(128, 128) GSC_TILE_CASE(128, 256) GSC_TILE_CASE(256, 64) GSC_TILE_CASE(256, 128)
+    GSC_TILE_CASE(256, 256)
+#undef GSC_TILE_CASE
+    return fail(GSC_EINVAL, "conv: no bf16 tile engine for %dx%d", ca, cb);
+}
+
+template int conv_tile_bf16<WIdentity>(int, int, const void*, int64_t, const void*, const WIdentity&, int,
+                                       const BlockPlan&, int64_t, int64_t, void*, unsigned*, hipStream_t,
+                                       const Epilogue&);
+template int conv_tile_bf16<WSel>(int, int, const void*, int64_t, const void*, const WSel&, int, const BlockPlan&,
+                                  int64_t, int64_t, void*, unsigned*, hipStream_t, const Epilogue&);
+
+}  // namespace gsc

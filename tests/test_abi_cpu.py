@@ -132,7 +132,7 @@ def test_conv_validation(L):
     assert fwd(0, 4, 27, -1) == gsc.GSC_EINVAL
     # the bf16 engine for wide layers needs a workspace for the transposed weights
     need = L.gsc_conv_fwd_ws_bytes(gsc.GSC_BF16, 256, 256, 27)
-    assert need == 27 * 256 * 256 * 2
+    assert need == 27 * 256 * 256 * 2 + 256   # transposed weights, then the tile counter
     assert L.gsc_conv_fwd_ws_bytes(gsc.GSC_F32, 256, 256, 27) == 0
     assert fwd(gsc.GSC_BF16, 256, 27, co=256) == gsc.GSC_ESHORT
     assert fwd(gsc.GSC_BF16, 256, 27, co=256, ws=fake, wsb=need - 1) == gsc.GSC_ESHORT
