@@ -948,6 +948,11 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
             GSC_DW_CASE(16, 16) GSC_DW_CASE(16, 32) GSC_DW_CASE(16, 64) GSC_DW_CASE(32, 16) GSC_DW_CASE(32, 32)
             GSC_DW_CASE(32, 64) GSC_DW_CASE(64, 16) GSC_DW_CASE(64, 32) GSC_DW_CASE(64, 64)
 #undef GSC_DW_CASE
+        } else if (dtype == GSC_BF16 && dw_tile_bf16_supported(c_in, c_out) && blk_bf16_fits(n_in, c_in) &&
+                   blk_bf16_fits(n_out, c_out)) {
+            int rc = dw_tile_bf16(c_in, c_out, X, n_in, dY, n_out, in_idx, out_idx, seg, ibase, chunk, K, items, part,
+                                  s);
+            if (rc) return rc;
         } else if (dtype == GSC_BF16 && dw_bf16_supported(c_in, c_out)) {
             int rc = dw_bf16(c_in, c_out, X, n_in, dY, n_out, in_idx, out_idx, seg, ibase, chunk, K, items, part, s);
             if (rc) return rc;

@@ -56,6 +56,14 @@ int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, c
                    const BlockPlan& plan, int64_t nb, int64_t n_y, void* Y, unsigned* counter, hipStream_t s,
                    const Epilogue& ep);
 
+// Weight gradient of a wide bf16 layer (conv_tile.hip), ci, co in {128,
+// 256): the partial sum of each work item (dw_item) over its pairs, written
+// to part[item] (ci x co float32); grid = items.  Asynchronous.
+bool dw_tile_bf16_supported(int ci, int co);
+int dw_tile_bf16(int ci, int co, const void* X, int64_t n_in, const void* dY, int64_t n_out, const int32_t* in_idx,
+                 const int32_t* out_idx, const int64_t* seg, const int64_t* ibase, const int64_t* chunk, int K,
+                 int64_t items, float* part, hipStream_t s);
+
 // Y (n x c, float32 or bf16 by dtype) = the epilogue applied in place (the
 // row-form paths, whose sums are complete only in Y).  Asynchronous.
 int affine_act(int dtype, void* Y, int64_t n, int c, const Epilogue& ep, hipStream_t s);

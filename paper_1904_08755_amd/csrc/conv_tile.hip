@@ -455,6 +455,282 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
 // can be captured in a graph).
 __global__ void k_tile_counter_zero(unsigned* counter) { *counter = 0u; }
 
+// ---------------------------------------------------------------------------
+// Weight gradient for wide layers (the chain rule of Eq. 3): dW_k =
+// sum over the pairs p of offset k of X[I_p]^T dY[O_p].  A workgroup takes
+// one work item (a chunk of the pairs of one offset, see dw_item) and
+// computes the whole C_in x C_out product of its pairs, 32 pairs per step;
+// its partial sum goes to part[item], and k_dw_reduce adds an offset's
+// partials in item order (so dW is deterministic).
+//
+// The reduction runs over pairs, while an MFMA operand holds eight
+// consecutive reduction elements per lane: here eight pairs of one channel.
+// The rows are copied into LDS as they are (pair-major, by buffer loads that
+// write LDS directly, in a four-stage ring as in the tile engine), and the
+// operands are read with the LDS transpose read (ds_read_b64_tr_b16: within
+// each 16 lanes, lane i receives element i % 4 of the 8-byte chunks that
+// lanes i / 4, i / 4 + 4, i / 4 + 8, i / 4 + 12 address), two per operand.
+// A row of C channels is stored with its 32-byte chunks permuted by the
+// row's index modulo 4 (chunk c at (c ^ (p % 4)) * 32), so the four rows a
+// transpose read touches fall in distinct banks.  Eight waves: wave (r, c)
+// keeps rows [128 r, 128 r + 128) of dW by C_out / WC columns in registers.
+// ---------------------------------------------------------------------------
+typedef short ts16x4 __attribute__((ext_vector_type(4)));
+
+template <int CI, int CO>
+struct DwTileCfg {
+    static constexpr int WR = CI / 128;                 // dW row groups of 128
+    static constexpr int WC = 8 / WR;                   // column groups
+    static constexpr int NI = 8;                        // 16-row blocks per wave
+    static constexpr int NJ = CO / WC / 16;             // 16-column blocks per wave
+    static constexpr int XI = CI / 128;                 // X copy instructions per wave and step (1 KiB each)
+    static constexpr int YI = CO / 128;                 // dY copy instructions per wave and step
+    static constexpr int LOADS = XI + YI;
+    static constexpr int XB = 32 * CI * 2;              // bytes of a step's X rows
+    static constexpr int YB = 32 * CO * 2;
+    static_assert(CI == 128 || CI == 256, "dW rows");
+    static_assert(CO == 128 || CO == 256, "dW columns");
+    static_assert(NJ >= 1, "columns per wave");
+};
+
+template <int CI, int CO>
+__global__ void __launch_bounds__(kTileThreads, 1)
+k_dw_tile_bf16(const uint16_t* __restrict__ X, int64_t n_in, const uint16_t* __restrict__ dY, int64_t n_out,
+               const int32_t* __restrict__ in_idx, const int32_t* __restrict__ out_idx,
+               const int64_t* __restrict__ seg, const int64_t* __restrict__ ibase, const int64_t* __restrict__ chunk,
+               int K, float* __restrict__ part) {
+    using C = DwTileCfg<CI, CO>;
+    __shared__ __attribute__((aligned(1024))) uint8_t sx0[C::XB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sx1[C::XB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sx2[C::XB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sx3[C::XB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sy0[C::YB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sy1[C::YB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sy2[C::YB];
+    __shared__ __attribute__((aligned(1024))) uint8_t sy3[C::YB];
+
+    const int64_t item = blockIdx.x;
+    int k;
+    int64_t p_begin, p_end;
+    if (!dw_item(ibase, chunk, seg, K, item, &k, &p_begin, &p_end)) return;
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int wr = wave / C::WC, wc = wave % C::WC;
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)(n_in * CI * 2), kTileBufFlags);
+    const __amdgpu_buffer_rsrc_t yr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)dY, (short)0, (int)(n_out * CO * 2), kTileBufFlags);
+
+    // copy lanes: instruction j of this wave covers rows (pairs) of the
+    // step; lane l takes 16 bytes of its row, the data chunk that the
+    // permutation puts at position l of the instruction's 1 KiB
+    constexpr int XL = CI / 8, YL = CO / 8;            // lanes per row
+    auto lane_src = [&](int lanes_per_row, int row) -> uint32_t {
+        const int u16 = lane % lanes_per_row;          // 16-byte slot in the row
+        const int w = (u16 >> 1) ^ (row & 3);           // its 32-byte data chunk
+        return (uint32_t)(w * 32 + (u16 & 1) * 16);
+    };
+    // the step's 4 pairs of this wave: 4 wave .. 4 wave + 3 (X and dY alike)
+    auto sx = [&](auto P) -> uint8_t* {
+        constexpr int p = decltype(P)::value;
+        return p == 0 ? sx0 : (p == 1 ? sx1 : (p == 2 ? sx2 : sx3));
+    };
+    auto sy = [&](auto P) -> uint8_t* {
+        constexpr int p = decltype(P)::value;
+        return p == 0 ? sy0 : (p == 1 ? sy1 : (p == 2 ? sy2 : sy3));
+    };
+    // row indices of this wave's 4 pairs of the step at pair p0 (scalar
+    // loads, taken one step before the copies that use them)
+    struct PairRows {
+        int32_t gi[4], go[4];
+        bool ok[4];
+    };
+    auto load_rows = [&](int64_t p0, PairRows& pr) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t pp = p0 + 4 * wave + r;
+            const int64_t pc = pp < p_end ? pp : p_end - 1;
+            pr.gi[r] = __builtin_amdgcn_readfirstlane(in_idx[pc]);
+            pr.go[r] = __builtin_amdgcn_readfirstlane(out_idx[pc]);
+            pr.ok[r] = pp < p_end;
+        }
+    };
+    auto issue = [&](const PairRows& pr, auto P) {
+        uint8_t* dx = sx(P);
+        uint8_t* dy = sy(P);
+        int32_t gi[4], go[4];
+        bool ok[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            gi[r] = pr.gi[r];
+            go[r] = pr.go[r];
+            ok[r] = pr.ok[r] && gi[r] >= 0 && gi[r] < n_in && go[r] >= 0 && go[r] < n_out;
+        }
+#pragma unroll
+        for (int j = 0; j < C::XI; ++j) {
+            const int rl = j * (64 / XL) + lane / XL;   // pair of the wave (0..3)
+            const int row = 4 * wave + rl;               // row of the stage
+            int32_t g = gi[0];
+            bool v = ok[0];
+#pragma unroll
+            for (int r = 1; r < 4; ++r) {
+                g = rl == r ? gi[r] : g;
+                v = rl == r ? ok[r] : v;
+            }
+            const uint32_t off = v ? (uint32_t)g * (uint32_t)(CI * 2) + lane_src(XL, row) : kTileNone;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                xr, (__attribute__((address_space(3))) void*)(dx + (wave * C::XI + j) * 1024), 16, off, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < C::YI; ++j) {
+            const int rl = j * (64 / YL) + lane / YL;
+            const int row = 4 * wave + rl;
+            int32_t g = go[0];
+            bool v = ok[0];
+#pragma unroll
+            for (int r = 1; r < 4; ++r) {
+                g = rl == r ? go[r] : g;
+                v = rl == r ? ok[r] : v;
+            }
+            const uint32_t off = v ? (uint32_t)g * (uint32_t)(CO * 2) + lane_src(YL, row) : kTileNone;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                yr, (__attribute__((address_space(3))) void*)(dy + (wave * C::YI + j) * 1024), 16, off, 0, 0, 0);
+        }
+    };
+
+    // transpose reads: lane (i, q) addresses row 8 q + i / 4 (+ 4 for the
+    // second read), 8 bytes at channel base + 4 (i % 4)
+    const int i16 = lane & 15, q = lane >> 4;
+    const int trow = 8 * q + (i16 >> 2);
+    auto tr_addr = [&](int row_bytes, int c0) -> int {   // c0: first channel of the 16-channel block
+        return trow * row_bytes + (((c0 >> 4) ^ (trow & 3)) * 32) + 8 * (i16 & 3);
+    };
+    int xa[C::NI], yb[C::NJ];
+#pragma unroll
+    for (int a = 0; a < C::NI; ++a) xa[a] = tr_addr(CI * 2, 128 * wr + 16 * a);
+#pragma unroll
+    for (int b = 0; b < C::NJ; ++b) yb[b] = tr_addr(CO * 2, (CO / C::WC) * wc + 16 * b);
+    // A step's 24 transpose reads are one block of inline assembly that
+    // also waits for them: the builtin's memory operand does not tell the
+    // compiler which stage it reads, so it would wait for every copy in
+    // flight (into other stages too) before each read; and no instruction
+    // may touch a read's registers before the read has completed.  Block a
+    // + 4 of X sits 128 bytes after block a (its chunk index differs in bit
+    // 2 only, which the row permutation leaves alone); the second read of an
+    // operand is four rows (2 KiB) on.
+    auto frags = [&](const uint8_t* bx, const uint8_t* by, tbf16x8 (&av)[C::NI], tbf16x8 (&bv)[C::NJ]) {
+        static_assert(C::NI == 8 && C::NJ == 4 && CI == 256 && CO == 256, "the read block is written for 256 x 256");
+        const uint32_t x0 = (uint32_t)(uintptr_t)(bx + xa[0]), x1 = (uint32_t)(uintptr_t)(bx + xa[1]);
+        const uint32_t x2 = (uint32_t)(uintptr_t)(bx + xa[2]), x3 = (uint32_t)(uintptr_t)(bx + xa[3]);
+        const uint32_t y0 = (uint32_t)(uintptr_t)(by + yb[0]), y1 = (uint32_t)(uintptr_t)(by + yb[1]);
+        const uint32_t y2 = (uint32_t)(uintptr_t)(by + yb[2]), y3 = (uint32_t)(uintptr_t)(by + yb[3]);
+        ts16x4 r[24];
+        asm volatile(
+            "ds_read_b64_tr_b16 %0, %24\n ds_read_b64_tr_b16 %1, %24 offset:2048\n"
+            "ds_read_b64_tr_b16 %2, %25\n ds_read_b64_tr_b16 %3, %25 offset:2048\n"
+            "ds_read_b64_tr_b16 %4, %26\n ds_read_b64_tr_b16 %5, %26 offset:2048\n"
+            "ds_read_b64_tr_b16 %6, %27\n ds_read_b64_tr_b16 %7, %27 offset:2048\n"
+            "ds_read_b64_tr_b16 %8, %28\n ds_read_b64_tr_b16 %9, %28 offset:2048\n"
+            "ds_read_b64_tr_b16 %10, %29\n ds_read_b64_tr_b16 %11, %29 offset:2048\n"
+            "ds_read_b64_tr_b16 %12, %30\n ds_read_b64_tr_b16 %13, %30 offset:2048\n"
+            "ds_read_b64_tr_b16 %14, %31\n ds_read_b64_tr_b16 %15, %31 offset:2048\n"
+            "ds_read_b64_tr_b16 %16, %28 offset:128\n ds_read_b64_tr_b16 %17, %28 offset:2176\n"
+            "ds_read_b64_tr_b16 %18, %29 offset:128\n ds_read_b64_tr_b16 %19, %29 offset:2176\n"
+            "ds_read_b64_tr_b16 %20, %30 offset:128\n ds_read_b64_tr_b16 %21, %30 offset:2176\n"
+            "ds_read_b64_tr_b16 %22, %31 offset:128\n ds_read_b64_tr_b16 %23, %31 offset:2176\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+              "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]), "=&v"(r[13]),
+              "=&v"(r[14]), "=&v"(r[15]), "=&v"(r[16]), "=&v"(r[17]), "=&v"(r[18]), "=&v"(r[19]), "=&v"(r[20]),
+              "=&v"(r[21]), "=&v"(r[22]), "=&v"(r[23])
+            : "v"(y0), "v"(y1), "v"(y2), "v"(y3), "v"(x0), "v"(x1), "v"(x2), "v"(x3)
+            : "memory");
+        auto join = [](ts16x4 lo, ts16x4 hi) {
+            const ts16x4 v8[2] = {lo, hi};
+            return __builtin_bit_cast(tbf16x8, v8);
+        };
+#pragma unroll
+        for (int b = 0; b < 4; ++b) bv[b] = join(r[2 * b], r[2 * b + 1]);
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+            av[a] = join(r[8 + 2 * a], r[9 + 2 * a]);
+            av[a + 4] = join(r[16 + 2 * a], r[17 + 2 * a]);
+        }
+    };
+
+    floatx4 acc[C::NI][C::NJ];
+#pragma unroll
+    for (int a = 0; a < C::NI; ++a)
+#pragma unroll
+        for (int b = 0; b < C::NJ; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // step s reads stage s % 4; the copies of step s + 3 go into the stage
+    // that step s - 1 has read; a step ends once step s + 1 is copied
+    const int64_t steps = (p_end - p_begin + 31) / 32;
+    PairRows pr;
+    load_rows(p_begin, pr);
+    issue(pr, std::integral_constant<int, 0>{});
+    load_rows(p_begin + 32, pr);
+    issue(pr, std::integral_constant<int, 1>{});
+    load_rows(p_begin + 64, pr);
+    issue(pr, std::integral_constant<int, 2>{});
+    load_rows(p_begin + 96, pr);
+    __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);   // step 0 copied
+    tile_barrier();
+    auto step = [&](int64_t s, auto P) {
+        constexpr int p = decltype(P)::value;
+        issue(pr, std::integral_constant<int, (p + 3) % 4>{});   // the copies of step s + 3
+        load_rows(p_begin + 32 * (s + 4), pr);
+        const uint8_t* bx = sx(P);
+        const uint8_t* by = sy(P);
+        tbf16x8 bv[C::NJ], av[C::NI];
+        frags(bx, by, av, bv);
+        __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);   // step s + 1's copies done
+#pragma unroll
+        for (int a = 0; a < C::NI; ++a)
+#pragma unroll
+            for (int b = 0; b < C::NJ; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+        tile_barrier();
+    };
+    for (int64_t s = 0; s < steps; s += 4) {
+        step(s, std::integral_constant<int, 0>{});
+        if (s + 1 < steps) step(s + 1, std::integral_constant<int, 1>{});
+        if (s + 2 < steps) step(s + 2, std::integral_constant<int, 2>{});
+        if (s + 3 < steps) step(s + 3, std::integral_constant<int, 3>{});
+    }
+    __builtin_amdgcn_s_waitcnt(VmLgkmWait<0>::value);   // the trailing (empty) copies
+
+    // the item's partial sums: lane (c, q) holds rows 4q .. 4q+3 of column c
+    float* out = part + (item * CI + 128 * wr) * (int64_t)CO + (CO / C::WC) * wc;
+#pragma unroll
+    for (int a = 0; a < C::NI; ++a)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int b = 0; b < C::NJ; ++b) out[(int64_t)(16 * a + 4 * q + i) * CO + 16 * b + i16] = acc[a][b][i];
+}
+
+bool dw_tile_bf16_supported(int ci, int co) { return ci == 256 && co == 256; }
+
+int dw_tile_bf16(int ci, int co, const void* X, int64_t n_in, const void* dY, int64_t n_out, const int32_t* in_idx,
+                 const int32_t* out_idx, const int64_t* seg, const int64_t* ibase, const int64_t* chunk, int K,
+                 int64_t items, float* part, hipStream_t s) {
+    if (items <= 0) return GSC_OK;
+#define GSC_DWT_CASE(A, B)                                                                                    \
+    if (ci == A && co == B) {                                                                                 \
+        hipLaunchKernelGGL((k_dw_tile_bf16<A, B>), dim3((unsigned)items), dim3(kTileThreads), 0, s,            \
+                           reinterpret_cast<const uint16_t*>(X), n_in, reinterpret_cast<const uint16_t*>(dY), n_out, \
+                           in_idx, out_idx, seg, ibase, chunk, K, part);                                      \
+        GSC_LAUNCH_CHECK();                                                                                   \
+        return GSC_OK;                                                                                        \
+    }
+    GSC_DWT_CASE(256, 256)
+#undef GSC_DWT_CASE
+    return fail(GSC_EINVAL, "dw_tile_bf16: unsupported channels %d x %d", ci, co);
+}
+
 bool tile_bf16_supported(int ca, int cb, int K) {
     return (ca == 64 || ca == 128 || ca == 256) && (cb == 64 || cb == 128 || cb == 256) && K >= 1 && K <= kTileMaxK;
 }
