@@ -225,7 +225,9 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                     iblw[j] = ibl[b];
                 }
         }
-        // the blocks whose sums this wave keeps: BPW wr .. BPW wr + BPW - 1
+        // the blocks whose sums this wave keeps: wr, wr + WR, wr + 2 WR, ...
+        // (interleaved, so that the waves of a column range see blocks from
+        // all of the tile's mask classes and take similar numbers of products)
         uint32_t bmv[C::BPW];
 #pragma unroll
         for (int b = 0; b < C::BPW; ++b) {
@@ -241,7 +243,9 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
         // row offsets for this lane (vr, kTileNone where there is no row).
         // The steps of an iteration (L = max(4, H) steps: one offset, or two
         // when an offset takes two steps) use the states of the current
-        // iteration, their copies four steps ahead those of the next one.
+        // iteration, their copies four steps ahead those of the next one;
+        // the states of the iteration after that are taken during step 1,
+        // where their LDS reads hide behind the products.
         constexpr int H = C::H;
         constexpr int L = H > 4 ? H : 4;    // steps per iteration
         constexpr int NO = L / H;           // offsets per iteration
@@ -293,7 +297,7 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
             for (int j = 0; j < C::NJ; ++j) acc[b][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
         if (U != 0u) {
-            OffState dc[NO], dn[NO];   // offsets of the current and the next iteration
+            OffState dc[NO], dn[NO], dnn[NO];   // offsets of this iteration, the next and the one after
 #pragma unroll
             for (int o = 0; o < NO; ++o) take_offset(dc[o]);
 #pragma unroll
@@ -319,19 +323,18 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
             // every wave has read stage 0 before step 0 copies into it
             __builtin_amdgcn_s_waitcnt(VmLgkmWait<2 * C::LOADS>::value);
             tile_barrier();
-            // step j of the iteration (static): stage j % 4; copies of the
-            // step four ahead into that stage; operands of step j + 1 from
-            // stage (j + 1) % 4; products of step j; then wait for the copies
-            // of step j + 2
+            // step j of the iteration (static): stage j % 4; the products of
+            // step j on the operands read during the step before, and the
+            // operands of step j + 1 read from stage (j + 1) % 4; halfway
+            // through the products the copies of the step four ahead go into
+            // stage j % 4 (whose operands every wave read during the step
+            // before), and in step 1 the offsets of the iteration after next
+            // are taken; then wait for the copies of step j + 2
             auto step = [&](auto J) {
                 constexpr int j = decltype(J)::value;
                 constexpr int st = j % 4, stn = (j + 1) % 4;
                 constexpr bool ahead_here = j + 4 < L;               // the step four ahead is in this iteration
                 constexpr int ja = ahead_here ? j + 4 : j + 4 - L;
-                if constexpr (ahead_here)
-                    issue(dc[ja / H], ja % H, std::integral_constant<int, st>{});
-                else
-                    issue(dn[ja / H], ja % H, std::integral_constant<int, st>{});
                 const uint8_t* san = stage_a(std::integral_constant<int, stn>{});
                 const uint8_t* sbn = stage_b(std::integral_constant<int, stn>{});
 #pragma unroll
@@ -343,6 +346,16 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                 const uint32_t bn = j + 1 < L ? dc[((j + 1) % L) / H].bk : dn[0].bk;
 #pragma unroll
                 for (int b = 0; b < C::BPW; ++b) {
+                    if (b == C::BPW / 2) {
+                        if constexpr (ahead_here)
+                            issue(dc[ja / H], ja % H, std::integral_constant<int, st>{});
+                        else
+                            issue(dn[ja / H], ja % H, std::integral_constant<int, st>{});
+                        if constexpr (j == 1) {
+#pragma unroll
+                            for (int o = 0; o < NO; ++o) take_offset(dnn[o]);
+                        }
+                    }
                     if (same) {
                         if ((bk >> b) & 1u) {
 #pragma unroll
@@ -381,10 +394,11 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                     step(std::integral_constant<int, 7>{});
                 }
 #pragma unroll
-                for (int o = 0; o < NO; ++o) dc[o] = dn[o];
+                for (int o = 0; o < NO; ++o) {
+                    dc[o] = dn[o];
+                    dn[o] = dnn[o];
+                }
                 if (dc[0].k < 0) break;
-#pragma unroll
-                for (int o = 0; o < NO; ++o) take_offset(dn[o]);
             }
             __builtin_amdgcn_s_waitcnt(VmLgkmWait<0>::value);   // the trailing (empty) copies
             tile_barrier();

@@ -76,9 +76,9 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __re
 // takes tiles of kRsTile keys in ticket order (an atomic counter, so every
 // tile a block waits for is already running), publishes its tile's count of
 // each digit and looks back over the earlier tiles' published counts to find
-// how many keys with that digit precede the tile (decoupled look-back: a
-// tile's entry holds either its own count or, once known, its inclusive
-// prefix).  The keys are then placed stably: in rounds of kRsThreads keys in
+// how many keys with that digit precede the tile (the decoupled look-back
+// of Merrill and Garland's single-pass prefix scan: a tile's entry holds
+// either its own count or, once known, its inclusive prefix).  The keys are then placed stably: in rounds of kRsThreads keys in
 // index order, lanes with equal digits found with kRsBits ballots.
 constexpr int kRsMaxPasses = 4;                   // keys of up to 40 bits
 constexpr uint32_t kStAgg = 1u << 30;             // entry holds the tile's own count
