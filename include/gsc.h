@@ -340,8 +340,10 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
  * dX is computed on the dX map (t_in_idx, t_out_idx, t_seg, t_gidx, t_n_pairs):
  * the same pairs with roles reversed (t_in_idx = output rows, t_out_idx = input
  * rows, increasing within each segment, t_gidx its group index over n_in rows),
- * and t_wsel (host, K ints) names the offset whose weight segment s of the dX
- * map uses: dX[t_out_idx[p]] += dY[t_in_idx[p]] W[t_wsel[s]]^T.  For the
+ * and t_wsel (host, K ints, a permutation of 0..K-1: each segment of the dX
+ * map holds the pairs of one forward offset) names the offset whose weight
+ * segment s of the dX map uses: dX[t_out_idx[p]] += dY[t_in_idx[p]]
+ * W[t_wsel[s]]^T.  For the
  * role-reversed map from gsc_kernel_map t_wsel is the identity; for a stride-1
  * map whose offset set is symmetric the forward map itself serves, with
  * t_wsel[s] = the offset -o_s.  (t_perm, t_bmask, t_ibase, t_items) is the
@@ -352,7 +354,8 @@ size_t gsc_conv_bwd_ws_bytes(int64_t n_pairs, int32_t c_in, int32_t c_out, int32
  * needed when dW is computed; given in full, it also holds the counter with
  * which the bfloat16 block engine of dX hands out its tiles, large ones
  * first: without it dX takes longer).  The dW reduction order is fixed, so dW is
- * deterministic.  Asynchronous.  Errors: EINVAL, ESHORT (ws), EHIP. */
+ * deterministic.  Asynchronous.  Errors: EINVAL (also a t_wsel that is not a
+ * permutation), ESHORT (ws), EHIP. */
 int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void* dY,
                         int64_t n_in, int32_t c_in, int32_t c_out, int32_t K,
                         const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg, int64_t n_pairs,

@@ -16,6 +16,7 @@
 // the pair index as the reduction dimension) and stores it as a partial; a
 // second kernel adds the partials of each offset in a fixed order.
 #include <climits>
+#include <vector>
 
 #include "conv_common.h"
 #include "conv_bf16.h"
@@ -884,10 +885,14 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         if (n_in > 0 && (!t_gidx || !t_wsel)) return fail(GSC_EINVAL, "conv_bwd: null t_gidx/t_wsel");
         if (t_n_pairs > 0 && (!dY || !t_in_idx || !t_out_idx))
             return fail(GSC_EINVAL, "conv_bwd: null dY/t_in_idx/t_out_idx");
+        // the role-reversed map's offsets pair one to one with the forward map's
         WSel sel;
+        std::vector<uint8_t> seen((size_t)K, 0);
         for (int k = 0; k < K; ++k) {
             if (t_wsel[k] < 0 || t_wsel[k] >= K)
                 return fail(GSC_EINVAL, "conv_bwd: t_wsel[%d]=%d outside [0,%d)", k, t_wsel[k], K);
+            if (seen[t_wsel[k]]++)
+                return fail(GSC_EINVAL, "conv_bwd: t_wsel is not a permutation (%d appears twice)", t_wsel[k]);
             sel.w[k] = (int16_t)t_wsel[k];
         }
         bool planned = false;

@@ -140,6 +140,10 @@ def test_conv_validation(L):
     rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake,
                                10, sel, None, None, None, None, fake, None, 10, None, 0, None)
     assert rc == gsc.GSC_EINVAL and "t_wsel" in _err(L)
+    sel = (ctypes.c_int32 * 3)(2, 0, 2)   # in range, but offset 2's weights twice and offset 1's never
+    rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 3, fake, fake, fake, 10, fake, fake, fake, fake,
+                               10, sel, None, None, None, None, fake, None, 10, None, 0, None)
+    assert rc == gsc.GSC_EINVAL and "permutation" in _err(L)
     sel = (ctypes.c_int32 * 2)(0, 1)
     rc = L.gsc_sparse_conv_bwd(0, fake, fake, fake, 10, 4, 4, 2, fake, fake, fake, 10, fake, fake, fake, fake,
                                10, sel, None, None, None, None, None,
