@@ -250,9 +250,21 @@ int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int6
  *                     j-th set bit k of bmask[b] (increasing k); entry
  *                     items[16t + r] is the input row paired at offset k with
  *                     the output row at position 16b + r, or -1 if none.
- * cap_items must be >= K * nb (an upper bound of the item count).  ws:
- * gsc_conv_plan_ws_bytes(n_out, K) bytes.  Asynchronous, deterministic.
- * Errors: EINVAL (K > 32, null pointers), ESHORT (cap_items, ws), EHIP. */
+ * cap_items must be >= K * nb (an upper bound of the item count).
+ *
+ * A map with 32 < K <= 128 offsets (the 3^4 tesseract's 81, the 5^3 cube's
+ * 125) is planned in R = gsc_plan_ranges(K) = ceil(K / 32) ranges of
+ * consecutive offsets: range r holds offsets k0 = r*S .. min(K, k0 + S) - 1
+ * with S = ceil(K / R), and is the plan above of the map restricted to them
+ * (bit k - k0 of a mask for offset k), stored at perm + r*n_out,
+ * bmask + r*nb, ibase + r*(nb+1) (item numbers counted from the range's
+ * first item) and items + 16*k0*nb.  So perm, bmask and ibase hold R times
+ * the sizes above; cap_items is still >= K * nb.  The engines add the ranges'
+ * sums in range order.
+ *
+ * ws: gsc_conv_plan_ws_bytes(n_out, K) bytes.  Asynchronous, deterministic.
+ * Errors: EINVAL (K > 128, null pointers), ESHORT (cap_items, ws), EHIP. */
+int32_t gsc_plan_ranges(int32_t K);
 int64_t gsc_plan_blocks(int64_t n_out);
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K);
 int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K,
@@ -264,8 +276,10 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K,
  * (forward: c_red = c_in; input gradient: c_red = c_out of the layer and the
  * output is c_in wide), else 0; a plan passed for another shape is ignored
  * and the map's row form is used.  Present engines: float32 with c_red, c_out
- * in {16, 32, 64} and K * c_red * c_out * 4 <= 147456; bfloat16 (fp32 sums)
- * with c_red, c_out in {64, 128, 256}.  Both take K <= 32. */
+ * in {16, 32, 64} and S * c_red * c_out * 4 <= 147456, S = the offsets of a
+ * plan range (K itself for K <= 32, ceil(K / ceil(K / 32)) for K <= 128: the
+ * ranges run one after another, each adding its sums to the output rows);
+ * bfloat16 (fp32 sums) with c_red, c_out in {64, 128, 256} and K <= 32. */
 int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K);
 
 /* ------------------------------------------------------------------------ */

@@ -762,8 +762,31 @@ static int plan_args(const char* who, int64_t n, const int32_t* perm, const uint
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
+// The fp32 engine over a plan of one or more ranges of offsets (see
+// gsc_conv_plan): one launch per range, each adding its sums to the rows
+// written by the ranges before it; the epilogue goes with the last.
+static int blk_f32_ranges(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel,
+                          int K, const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep) {
+    const int R = plan_ranges(K), S = plan_range_size(K);
+    if (R == 1) return conv_blk_f32(ca, cb, X, n_x, W, wt, sel, K, plan, n_y, Y, s, ep);
+    const int64_t nb = gsc_plan_blocks(n_y);
+    for (int r = 0; r < R; ++r) {
+        const int k0 = r * S, kr = K - k0 < S ? K - k0 : S;
+        const BlockPlan pr{plan.perm + (int64_t)r * n_y, plan.bmask + (int64_t)r * nb,
+                           plan.ibase + (int64_t)r * (nb + 1), plan.items + (int64_t)k0 * nb * 16};
+        WSel sr{};
+        for (int k = 0; k < kr && wt; ++k) sr.w[k] = sel.w[k0 + k];
+        const float* Wr = wt ? W : W + (int64_t)k0 * ca * cb;   // forward: the range's own matrices
+        const int rc = conv_blk_f32(ca, cb, X, n_x, Wr, wt, sr, kr, pr, n_y, Y, s, r == R - 1 ? ep : Epilogue{},
+                                    r > 0);
+        if (rc) return rc;
+    }
+    return GSC_OK;
+}
+
 int32_t gsc_conv_block_engine(int32_t dtype, int32_t c_red, int32_t c_out, int32_t K) {
-    if (dtype == GSC_F32) return blk_f32_supported(c_red, c_out, K) ? 1 : 0;
+    if (dtype == GSC_F32)
+        return K >= 1 && K <= kPlanMaxKAll && blk_f32_supported(c_red, c_out, plan_range_size(K)) ? 1 : 0;
     if (dtype == GSC_BF16) return blk_bf16_supported(c_red, c_out, K) ? 1 : 0;
     return 0;
 }
@@ -803,8 +826,8 @@ static int conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, co
             return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s, ep);
         }
         static const WSel kNoSel{};
-        return conv_blk_f32(c_in, c_out, reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(W),
-                            false, kNoSel, K, plan, n_out, reinterpret_cast<float*>(Y), s, ep);
+        return blk_f32_ranges(c_in, c_out, reinterpret_cast<const float*>(X), n_in, reinterpret_cast<const float*>(W),
+                              false, kNoSel, K, plan, n_out, reinterpret_cast<float*>(Y), s, ep);
     }
     // row form: the sums are complete only once the call's kernels are done,
     // so the epilogue is a pass of its own over Y
@@ -914,9 +937,9 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
             } else if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
                 rc = conv_blk_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan, n_in, dX, s);
             else
-                rc = conv_blk_f32(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,
-                                  reinterpret_cast<const float*>(W), true, sel, K, plan, n_in,
-                                  reinterpret_cast<float*>(dX), s);
+                rc = blk_f32_ranges(c_out, c_in, reinterpret_cast<const float*>(dY), n_out,
+                                    reinterpret_cast<const float*>(W), true, sel, K, plan, n_in,
+                                    reinterpret_cast<float*>(dX), s, Epilogue{});
         }
         else if (dtype == GSC_F32)
             rc = launch_os<float, float, true>(dY, n_out, W, t_in_idx, t_out_idx, t_gidx, nullptr, K, c_out, c_in,

@@ -25,11 +25,12 @@ bool blk_f32_supported(int ca, int cb, int K);
 
 // Y (n_y x cb) = sum over the plan's items of X[item rows] * B_k with
 // B_k = W[k] (ca x cb) when !wt, or B_k = W[sel(k)]^T (W: K x cb x ca) when
-// wt.  Asynchronous.
-// A forward call (!wt) may carry an epilogue, applied to the sums before
-// they are stored.
+// wt; with accum, Y += that sum instead.  Asynchronous.
+// A forward call (!wt) may carry an epilogue, applied to the sums (with
+// accum: to Y plus the sums) before they are stored.
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
-                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep = Epilogue{});
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep = Epilogue{},
+                 bool accum = false);
 
 // bf16 engine for wide layers: reduction width ca and output width cb in
 // {64, 128, 256}, K <= 32.  Y (n_y x cb, bf16) = sum over the plan's items

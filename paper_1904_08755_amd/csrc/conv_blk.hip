@@ -76,7 +76,7 @@ __global__ void __launch_bounds__((BlkF32<CA, CB>::THREADS))
 k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, int K, WSel sel,
                const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
                const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
-               Epilogue ep, float* __restrict__ Y) {
+               Epilogue ep, int accum, float* __restrict__ Y) {
     using C = BlkF32<CA, CB>;
     __shared__ float wl[kBlkLdsBytes / 4];
     // Weights in fragment order: lane (c, q) of offset k needs, for MFMA step
@@ -243,10 +243,15 @@ k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict
                     const int32_t row = __shfl(pmr[p], 4 * q + i, 64);
                     const int64_t pos = (int64_t)mt[p].b * 16 + 4 * q + i;
                     if (pos < n_y && row >= 0 && row < n_y) {
+                        float* yr = Y + (int64_t)row * CB + r16;
+                        float prev[C::NNB];
 #pragma unroll
-                        for (int j = 0; j < C::NNB; ++j)
-                            Y[(int64_t)row * CB + 16 * j + r16] =
-                                EP ? epi_apply(acc[j][i], esc[j], esh[j], ep.relu) : acc[j][i];
+                        for (int j = 0; j < C::NNB; ++j) prev[j] = accum ? yr[16 * j] : 0.f;
+#pragma unroll
+                        for (int j = 0; j < C::NNB; ++j) {
+                            const float v = acc[j][i] + prev[j];
+                            yr[16 * j] = EP ? epi_apply(v, esc[j], esh[j], ep.relu) : v;
+                        }
                     }
                 }
 #pragma unroll
@@ -685,38 +690,40 @@ static int device_cus() {
 
 template <int CA, int CB, bool WT, bool EP>
 static void launch_blk_f32(const float* X, int64_t n_x, const float* W, const WSel& sel, int K, const BlockPlan& p,
-                           int64_t nb, int64_t n_y, const Epilogue& ep, float* Y, hipStream_t s) {
+                           int64_t nb, int64_t n_y, const Epilogue& ep, bool accum, float* Y, hipStream_t s) {
     using C = BlkF32<CA, CB>;
     int64_t grid = (nb + C::WAVES - 1) / C::WAVES;
     const int cus = device_cus();
     if (grid > cus) grid = cus;
     hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT, EP>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X, n_x, W, K,
-                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, Y);
+                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, accum ? 1 : 0, Y);
 }
 
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,
-                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep) {
+                 const BlockPlan& plan, int64_t n_y, float* Y, hipStream_t s, const Epilogue& ep, bool accum) {
     if (!blk_f32_supported(ca, cb, K)) return fail(GSC_EINVAL, "conv: no fp32 block engine for %dx%d, K=%d", ca, cb, K);
     if (ep.on() && wt) return fail(GSC_EINVAL, "conv: the epilogue applies to the forward pass only");
     const int64_t nb = (n_y + kPlanBlockRows - 1) / kPlanBlockRows;
     if (nb == 0) return GSC_OK;
     if (n_x == 0) {   // no input rows to read (the engine always issues its row loads)
         const int64_t n = n_y * cb;
-        hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256),
-                           0, s, Y, n);
-        GSC_LAUNCH_CHECK();
+        if (!accum) {
+            hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)),
+                               dim3(256), 0, s, Y, n);
+            GSC_LAUNCH_CHECK();
+        }
         return ep.on() ? affine_act(GSC_F32, Y, n_y, cb, ep, s) : GSC_OK;
     }
-#define GSC_BLK_CASE(A, B)                                                                  \
-    if (ca == A && cb == B) {                                                               \
-        if (wt)                                                                             \
-            launch_blk_f32<A, B, true, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);   \
-        else if (ep.on())                                                                   \
-            launch_blk_f32<A, B, false, true>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);   \
-        else                                                                                \
-            launch_blk_f32<A, B, false, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, Y, s);  \
-        GSC_LAUNCH_CHECK();                                                                 \
-        return GSC_OK;                                                                      \
+#define GSC_BLK_CASE(A, B)                                                                         \
+    if (ca == A && cb == B) {                                                                      \
+        if (wt)                                                                                    \
+            launch_blk_f32<A, B, true, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, accum, Y, s);  \
+        else if (ep.on())                                                                          \
+            launch_blk_f32<A, B, false, true>(X, n_x, W, sel, K, plan, nb, n_y, ep, accum, Y, s);  \
+        else                                                                                       \
+            launch_blk_f32<A, B, false, false>(X, n_x, W, sel, K, plan, nb, n_y, ep, accum, Y, s); \
+        GSC_LAUNCH_CHECK();                                                                        \
+        return GSC_OK;                                                                             \
     }
     GSC_BLK_CASE(16, 16) GSC_BLK_CASE(16, 32) GSC_BLK_CASE(16, 64) GSC_BLK_CASE(32, 16) GSC_BLK_CASE(32, 32)
     GSC_BLK_CASE(32, 64) GSC_BLK_CASE(64, 16) GSC_BLK_CASE(64, 32) GSC_BLK_CASE(64, 64)

@@ -220,8 +220,18 @@ size_t scan_ws_bytes(int64_t m);
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
                 hipStream_t s);
 
-// Largest offset count of a block plan (neighbour masks are 32-bit).
+// Largest offset count of one range of a block plan (neighbour masks are
+// 32-bit).  A map with more offsets is planned in ranges of consecutive
+// offsets (at most kPlanMaxRanges, of plan_range_size(K) offsets each but the
+// last), each range a plan of its own over the same rows.
 constexpr int kPlanMaxK = 32;
+constexpr int kPlanMaxRanges = 4;
+constexpr int kPlanMaxKAll = kPlanMaxK * kPlanMaxRanges;
+inline int plan_ranges(int K) { return (K + kPlanMaxK - 1) / kPlanMaxK; }
+inline int plan_range_size(int K) {
+    const int R = plan_ranges(K);
+    return (K + R - 1) / R;
+}
 
 // Rows of a block of the block plan (one MFMA row block).
 constexpr int kPlanBlockRows = 16;

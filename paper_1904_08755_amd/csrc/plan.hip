@@ -367,8 +367,10 @@ extern "C" {
 
 int64_t gsc_plan_blocks(int64_t n_out) { return n_out <= 0 ? 0 : (n_out + 15) / 16; }
 
+int32_t gsc_plan_ranges(int32_t K) { return K < 1 || K > kPlanMaxKAll ? 0 : plan_ranges(K); }
+
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
-    if (n_out < 0 || n_out > kRsMaxKeys || K < 1 || K > kPlanMaxK) return 0;
+    if (n_out < 0 || n_out > kRsMaxKeys || K < 1 || K > kPlanMaxKAll) return 0;
     const int64_t nb = (n_out + 15) / 16;
     const int64_t nrs = (n_out + kRsTile - 1) / kRsTile;
     size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
@@ -383,7 +385,7 @@ size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
 int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
                   int32_t* items, int64_t cap_items, void* ws, size_t ws_bytes, void* stream) {
     clear_error();
-    if (K < 1 || K > kPlanMaxK) return fail(GSC_EINVAL, "conv_plan: K=%d outside [1,%d]", K, kPlanMaxK);
+    if (K < 1 || K > kPlanMaxKAll) return fail(GSC_EINVAL, "conv_plan: K=%d outside [1,%d]", K, kPlanMaxKAll);
     if (n_out < 0 || n_out > kRsMaxKeys)
         return fail(GSC_EINVAL, "conv_plan: n_out=%lld outside [0, %lld]", (long long)n_out, (long long)kRsMaxKeys);
     if (!ibase || !ws) return fail(GSC_EINVAL, "conv_plan: null ibase/ws");
@@ -395,7 +397,18 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, u
                     (long long)need_items);
     const size_t need = gsc_conv_plan_ws_bytes(n_out, K);
     if (ws_bytes < need) return fail(GSC_ESHORT, "conv_plan: ws needs %zu bytes, got %zu", need, ws_bytes);
-    return plan_enqueue(nbr, n_out, K, perm, bmask, ibase, items, ws, reinterpret_cast<hipStream_t>(stream));
+    // one plan per range of offsets, one after another on the stream (they share ws)
+    const int R = plan_ranges(K), S = plan_range_size(K);
+    const int64_t nb = gsc_plan_blocks(n_out);
+    for (int r = 0; r < R; ++r) {
+        const int k0 = r * S, kr = K - k0 < S ? K - k0 : S;
+        const int rc = plan_enqueue(nbr ? nbr + (int64_t)k0 * n_out : nullptr, n_out, kr,
+                                    perm ? perm + (int64_t)r * n_out : nullptr, bmask ? bmask + (int64_t)r * nb : nullptr,
+                                    ibase + (int64_t)r * (nb + 1), items ? items + (int64_t)k0 * nb * 16 : nullptr, ws,
+                                    reinterpret_cast<hipStream_t>(stream));
+        if (rc) return rc;
+    }
+    return GSC_OK;
 }
 
 }  // extern "C"

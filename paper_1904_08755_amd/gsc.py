@@ -58,6 +58,7 @@ _SIGS = {
     "gsc_kernel_map_noalloc": (ctypes.c_int, [_vp, _vp, _i64, _i32, _c_i32p, _i32, _c_i32p, _vp, _vp, _i64, _vp,
                                               _vp, _vp, _vp]),
     "gsc_plan_blocks": (_i64, [_i64]),
+    "gsc_plan_ranges": (_i32, [_i32]),
     "gsc_conv_plan_ws_bytes": (_sz, [_i64, _i32]),
     "gsc_conv_plan": (ctypes.c_int, [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "gsc_conv_block_engine": (_i32, [_i32, _i32, _i32, _i32]),
@@ -306,9 +307,9 @@ def transposed_kernel_map(out_table: torch.Tensor, in_coords: torch.Tensor, offs
 @dataclasses.dataclass
 class BlockPlan:
     """Block plan of a kernel map (see gsc_conv_plan in include/gsc.h)."""
-    perm: torch.Tensor         # int32 [n_out]: output row at each position
-    bmask: torch.Tensor        # uint32 bits as int32 [nb]: union mask of each 16-position block
-    ibase: torch.Tensor        # int64 [nb + 1]: first item of each block
+    perm: torch.Tensor         # int32 [R * n_out]: output row at each position (R = offset ranges)
+    bmask: torch.Tensor        # uint32 bits as int32 [R * nb]: union mask of each 16-position block
+    ibase: torch.Tensor        # int64 [R * (nb + 1)]: first item of each block
     items: torch.Tensor        # int32 [cap_items, 16]: input rows of each item (-1: none)
 
     def ptrs(self):
@@ -323,15 +324,24 @@ def gsc_conv_block_engine(dtype: int, c_red: int, c_out: int, K: int) -> bool:
     return bool(lib().gsc_conv_block_engine(dtype, c_red, c_out, K))
 
 
+def gsc_plan_ranges(K: int) -> int:
+    return int(lib().gsc_plan_ranges(K))
+
+
 class PlanBuffers:
-    """Caller-owned buffers of one block plan (reusable across calls)."""
+    """Caller-owned buffers of one block plan (reusable across calls); a map
+    with more than 32 offsets has gsc_plan_ranges(K) plans, one per range of
+    offsets, stored one after another."""
 
     def __init__(self, n_out: int, K: int, device):
         nb = gsc_plan_blocks(n_out)
+        R = gsc_plan_ranges(K)
+        if R < 1:
+            raise ValueError(f"no block plan for K={K} offsets")
         self.cap_items = K * nb
-        self.perm = torch.empty(max(n_out, 1), dtype=torch.int32, device=device)
-        self.bmask = torch.empty(max(nb, 1), dtype=torch.int32, device=device)
-        self.ibase = torch.empty(nb + 1, dtype=torch.int64, device=device)
+        self.perm = torch.empty(max(R * n_out, 1), dtype=torch.int32, device=device)
+        self.bmask = torch.empty(max(R * nb, 1), dtype=torch.int32, device=device)
+        self.ibase = torch.empty(R * (nb + 1), dtype=torch.int64, device=device)
         self.items = torch.empty((max(self.cap_items, 1), 16), dtype=torch.int32, device=device)
         self.ws = _ws(lib().gsc_conv_plan_ws_bytes(n_out, K), device)
 
@@ -346,7 +356,7 @@ def gsc_conv_plan(kmap: KernelMap, bufs: Optional[PlanBuffers] = None, stream=No
         bufs = PlanBuffers(n_out, K, kmap.seg.device)
     _check(lib().gsc_conv_plan(_ptr(kmap.nbr), n_out, K, _ptr(bufs.perm), _ptr(bufs.bmask), _ptr(bufs.ibase),
                                _ptr(bufs.items), bufs.cap_items, _ptr(bufs.ws), bufs.ws.numel(), _stream(stream)))
-    plan = BlockPlan(bufs.perm[:n_out], bufs.bmask, bufs.ibase, bufs.items)
+    plan = BlockPlan(bufs.perm[: gsc_plan_ranges(K) * n_out], bufs.bmask, bufs.ibase, bufs.items)
     return dataclasses.replace(kmap, plan=plan)
 
 

@@ -305,6 +305,40 @@ def random_coords(seed: int, n: int, D: int, lo: int, hi: int, batch: int = 1) -
     return rows.astype(np.int32)
 
 
+def space_time_chroma_coords(seed: int, frames: int = 3, crops: int = 12, half: int = 16,
+                             second_colour: float = 0.3) -> np.ndarray:
+    """7D rows (b, x, y, z, t, r, g, b) at the extents the space-time-chroma
+    convolution of Sec. 6 meets: the 2 cm voxels of an indoor scene seen in
+    ``frames`` frames, and RGB colour channels of 0..255 each.
+
+    To keep the row count small while the coordinates still span the whole
+    scene, only the voxels within ``half`` voxels (per axis) of ``crops``
+    centres are kept: the six voxels with the smallest and largest x, y and z
+    (so the box is the full scene's) and random ones.  A voxel's colour is
+    constant over cells of 8 x 8 x 8 voxels (a hash of the cell), so spatial
+    and temporal neighbours often share it; a fraction ``second_colour`` of the
+    voxels also holds a second colour, one channel off by one, so neighbours
+    along the colour axes occur too."""
+    rows, _ = scene_coords(2000 + seed, 1, 1.0, 0.02, SCENE_POINTS_2CM, frames=frames)
+    rng = np.random.default_rng(np.random.SeedSequence(ROOT_SEED, spawn_key=(1003, seed)))
+    xyz = rows[:, 1:4].astype(np.int64)
+    centres = [int(xyz[:, a].argmin()) for a in range(3)] + [int(xyz[:, a].argmax()) for a in range(3)]
+    centres += rng.choice(len(rows), max(crops - 6, 0), replace=False).tolist()
+    keep = np.zeros(len(rows), bool)
+    for i in centres:
+        keep |= np.all(np.abs(xyz - xyz[i]) <= half, axis=1)
+    r4 = rows[keep].astype(np.int64)
+    cell = r4[:, 1:4] // 8
+    h = (cell[:, 0] * 73856093) ^ (cell[:, 1] * 19349663) ^ (cell[:, 2] * 83492791)
+    rgb = np.stack([(h >> s) & 255 for s in (0, 8, 16)], axis=1)
+    r7 = np.concatenate([r4, rgb], axis=1)
+    two = r7[rng.random(len(r7)) < second_colour].copy()
+    ch = 5 + rng.integers(0, 3, len(two))
+    at = np.arange(len(two))
+    two[at, ch] = np.clip(two[at, ch] + rng.choice([-1, 1], len(two)), 0, 255)
+    return unique_rows(np.concatenate([r7, two], axis=0).astype(np.int32))
+
+
 def random_features(seed: int, n: int, c: int, dtype: str = "f32"):
     rng = np.random.default_rng(np.random.SeedSequence(ROOT_SEED, spawn_key=(1001, seed)))
     return _as_dtype(rng.standard_normal((n, c)).astype(np.float32), dtype)

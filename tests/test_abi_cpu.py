@@ -154,12 +154,14 @@ def test_conv_validation(L):
 def test_plan_validation(L):
     fake = ctypes.c_void_p(0x1000)
     ws = L.gsc_conv_plan_ws_bytes(100, 27)
-    assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 33) == 0
+    assert ws > 0 and L.gsc_conv_plan_ws_bytes(100, 129) == 0 and L.gsc_conv_plan_ws_bytes(100, 81) > 0
+    # maps with more than 32 offsets: plans over ranges of consecutive offsets
+    assert [L.gsc_plan_ranges(K) for K in (1, 32, 33, 64, 81, 125, 128, 129, 0)] == [1, 1, 2, 2, 3, 4, 4, 0, 0]
     assert L.gsc_plan_blocks(0) == 0 and L.gsc_plan_blocks(16) == 1 and L.gsc_plan_blocks(17) == 2
     cap = 27 * 7
     plan = lambda K, wsb=ws, cap=cap, ib=fake: L.gsc_conv_plan(fake, 100, K, fake, fake, ib, fake, cap, fake, wsb,
                                                                None)
-    assert plan(33) == gsc.GSC_EINVAL and "K=33" in _err(L)
+    assert plan(129) == gsc.GSC_EINVAL and "K=129" in _err(L)
     assert plan(0) == gsc.GSC_EINVAL
     assert plan(27, wsb=ws - 1) == gsc.GSC_ESHORT
     assert plan(27, cap=cap - 1) == gsc.GSC_ESHORT and str(cap) in _err(L)
@@ -168,7 +170,11 @@ def test_plan_validation(L):
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 27) == 1
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 9) == 1
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 10) == 0
-    assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33) == 0
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33) == 1    # two ranges of 17 offsets
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 81) == 1    # three of 27
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 81) == 0    # 27 weight matrices of 16 KiB do not fit
+    assert L.gsc_conv_block_engine(gsc.GSC_F32, 16, 16, 129) == 0
+    assert L.gsc_conv_block_engine(gsc.GSC_BF16, 256, 256, 33) == 0
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 3, 16, 27) == 0
     assert L.gsc_conv_block_engine(gsc.GSC_BF16, 256, 256, 27) == 1
     assert L.gsc_conv_block_engine(gsc.GSC_BF16, 32, 32, 27) == 0

@@ -306,31 +306,47 @@ def test_bf16_wide_channel_engine(ci, co, region):
 def _check_plan(km):
     """The block plan of a map: rows stably sorted by neighbour mask, 16-row
     blocks with their union masks and item bases, and each item holding the
-    input rows of its block's positions at its offset (-1 where none)."""
+    input rows of its block's positions at its offset (-1 where none).  A map
+    with more than 32 offsets has one such plan per range of consecutive
+    offsets (ceil(K / 32) ranges of equal size but the last)."""
     pl = km.plan
     n, K = km.n_out, km.K
     nb = (n + 15) // 16
-    perm = pl.perm.cpu().numpy().astype(np.int64)
-    assert np.array_equal(np.sort(perm), np.arange(n))
     pairs = gpu_pairs(km)
-    mask = np.zeros(n, np.int64)
     nbr = np.full((max(n, 1), K), -1, np.int64)
     for k, (i, o) in enumerate(pairs):
-        mask[o] |= np.int64(1) << np.int64(k)
         nbr[o, k] = i
     assert np.array_equal(km.nbr.cpu().numpy().T.astype(np.int64), nbr[:n])   # the dense form lists the same pairs
+    R = -(-K // 32)
+    S = -(-K // R)
+    assert gsc.gsc_plan_ranges(K) == R
+    perm_all = pl.perm.cpu().numpy().astype(np.int64)
+    bm_all = pl.bmask.cpu().numpy().astype(np.int64) & 0xFFFFFFFF
+    ib_all = pl.ibase.cpu().numpy()
+    items_all = pl.items.cpu().numpy()
+    for r in range(R):
+        k0, k1 = r * S, min(K, r * S + S)
+        _check_plan_range(n, nbr[:, k0:k1], perm_all[r * n:(r + 1) * n], bm_all[r * nb:(r + 1) * nb],
+                          ib_all[r * (nb + 1):(r + 1) * (nb + 1)], items_all[k0 * nb:])
+
+
+def _check_plan_range(n, nbr, perm, bm, ib, items):
+    nb = (n + 15) // 16
+    K = nbr.shape[1]
+    assert np.array_equal(np.sort(perm), np.arange(n))
+    mask = np.zeros(max(n, 1), np.int64)
+    for k in range(K):
+        mask |= (nbr[:, k] >= 0).astype(np.int64) << np.int64(k)
     ms = mask[perm]
     assert np.all(ms[1:] >= ms[:-1])                                   # sorted by mask
     same = ms[1:] == ms[:-1]
     assert np.all(perm[1:][same] > perm[:-1][same])                    # stable: row order within a mask
-    bm = pl.bmask.cpu().numpy()[:nb].astype(np.int64) & 0xFFFFFFFF
     msp = np.zeros(nb * 16, np.int64)
     msp[:n] = ms
     assert np.array_equal(bm, np.bitwise_or.reduce(msp.reshape(nb, 16), axis=1) if nb else bm)
     cnt = np.array([bin(int(x)).count("1") for x in bm], np.int64)
-    ib = pl.ibase.cpu().numpy()[: nb + 1]
     assert ib[0] == 0 and np.array_equal(np.diff(ib), cnt)
-    items = pl.items.cpu().numpy()[: ib[-1]]
+    items = items[: ib[-1]]
     below = np.zeros(nb, np.int64)                                     # set bits of bmask below offset k
     pos = np.arange(nb)[:, None] * 16 + np.arange(16)[None, :]
     rows = perm[np.minimum(pos, max(n - 1, 0))] if n else pos
@@ -459,6 +475,27 @@ def test_4d_hybrid_and_tesseract():
     _conv_case(coords, 8, 8, regions.hybrid(3, 4), 77)
     _conv_case(coords, 8, 8, regions.hypercube(3, 4), 78)
     _conv_case(coords, 8, 8, regions.spatial(3, 4), 79)
+
+
+@pytest.mark.parametrize("region", ["tesseract", "cube5", "cube3+axes2"])
+def test_block_engine_offset_ranges(region):
+    """Maps with more than 32 offsets on the fp32 block engine (Sec. 5.1:
+    the 3^4 tesseract's 81 offsets, the 5^3 cube's 125, and 33 offsets): one plan per
+    range of consecutive offsets, the ranges' sums added in range order, in
+    the forward pass and the input gradient."""
+    if region == "tesseract":
+        coords, offs, ci, co = WL.random_coords(171, 3000, 4, -5, 5, batch=1), regions.hypercube(3, 4), 32, 32
+    elif region == "cube5":
+        coords, offs, ci, co = WL.random_coords(172, 2500, 3, -9, 9, batch=2), regions.hypercube(5, 3), 16, 32
+    else:
+        two = np.concatenate([2 * np.eye(3, dtype=np.int32), -2 * np.eye(3, dtype=np.int32)])
+        offs = np.concatenate([regions.hypercube(3, 3), two])   # the cube and six axis steps of 2: 33
+        coords, ci, co = WL.random_coords(173, 3000, 3, -10, 10, batch=2), 32, 16
+    K = len(offs)
+    assert K > 32 and gsc.gsc_plan_ranges(K) == -(-K // 32)
+    assert gsc.gsc_conv_block_engine(gsc.GSC_F32, ci, co, K) and gsc.gsc_conv_block_engine(gsc.GSC_F32, co, ci, K)
+    _say(f"[gpu] block engine over offset ranges: {region} K={K} {ci}->{co}")
+    _plan_case(coords, ci, co, offs, 174 + K)
 
 
 def test_dilated_kernel():
@@ -758,7 +795,7 @@ def test_quantize_random_and_scene():
 @pytest.mark.parametrize("dtype,ci,co,region,planned", [
     ("f32", 32, 32, "cube3", True), ("f32", 16, 64, "cube2", True), ("f32", 32, 32, "cube3", False),
     ("f32", 3, 16, "cube3", False), ("bf16", 256, 256, "cube3", True), ("bf16", 64, 128, "cube2", True),
-    ("bf16", 256, 256, "cube3", False), ("bf16", 48, 80, "cube3", False)])
+    ("bf16", 256, 256, "cube3", False), ("bf16", 48, 80, "cube3", False), ("f32", 16, 16, "cube5", True)])
 @pytest.mark.parametrize("mode", ["bn_relu", "scale_only", "shift_relu", "none"])
 def test_conv_affine_epilogue(dtype, ci, co, region, planned, mode):
     """gsc_sparse_conv_fwd_affine against the oracle's convolution followed by
@@ -833,38 +870,91 @@ def test_conv_affine_no_input_rows():
 
 
 def test_block_engines_at_32_offsets():
-    """K = 32, the widest region a block plan takes (masks use all 32 bits;
-    the last offset is bit 31), on both engines, and K = 33, which the row
-    form takes."""
+    """K = 32, the widest region one block plan takes (masks use all 32 bits;
+    the last offset is bit 31), on both engines, and K = 33, which the fp32
+    engine takes in two plan ranges and the bf16 path on the row form."""
     extra = np.array([[2, 0, 0], [-2, 0, 0], [0, 2, 0], [0, -2, 0], [0, 0, 2], [0, 0, -2]], np.int32)
     offs32 = np.concatenate([regions.hypercube(3, 3), extra[:5]]).astype(np.int32)
     offs33 = np.concatenate([regions.hypercube(3, 3), extra]).astype(np.int32)
     coords = WL.random_coords(181, 3000, 3, -9, 9, batch=2)
     assert gsc.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 32) and gsc.gsc_conv_block_engine(gsc.GSC_BF16, 64, 64, 32)
-    assert not gsc.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33)
-    _say("[gpu] block engines at K = 32 (fp32 32->32, bf16 64->64), row form at K = 33")
+    assert gsc.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 33) and gsc.gsc_plan_ranges(33) == 2
+    assert not gsc.gsc_conv_block_engine(gsc.GSC_BF16, 64, 64, 33)
+    _say("[gpu] block engines at K = 32 (fp32 32->32, bf16 64->64); K = 33 in two ranges and on the row form")
     _plan_case(coords, 32, 32, offs32, 182)
     _plan_case(coords, 64, 64, offs32, 183, dtype="bf16")
     _conv_case(coords, 16, 16, offs33, 184)
+    _conv_case(coords, 64, 64, offs33, 185, dtype="bf16")
 
 
-def test_7d_space_time_chroma():
-    """7D coordinates (b, x, y, z, t, r, g, b) as the space-time-chroma
-    convolution of Sec. 6 uses them, with keys inside the 62-bit packing: the
-    7D cross (15 offsets) on the block engine and a trilateral region (the
-    spatial 3^3 cube plus the temporal and the three chroma crosses, 35
-    offsets) on the row form."""
-    coords = WL.random_coords(191, 4000, 7, -2, 2, batch=2)
-    cross = regions.hypercross(3, 7)
+def _trilateral_7d():
+    """A trilateral region of the 7D space-time-chroma space (Sec. 6): the
+    spatial 3^3 cube plus the temporal and the three colour crosses (35)."""
     tri = {tuple(o) + (0,) * 4 for o in regions.hypercube(3, 3).tolist()}
     for ax in range(3, 7):
         for s in (-1, 1):
             o = [0] * 7
             o[ax] = s
             tri.add(tuple(o))
-    tri = np.array(sorted(tri), np.int32)
+    return np.array(sorted(tri), np.int32)
+
+
+def _key_bits(coords):
+    span = coords.astype(np.int64).max(0) - coords.astype(np.int64).min(0)
+    return sum(int(s).bit_length() for s in span)
+
+
+def test_7d_space_time_chroma():
+    """7D coordinates (b, x, y, z, t, r, g, b) as the space-time-chroma
+    convolution of Sec. 6 uses them, with keys inside the 62-bit packing: the
+    7D cross (15 offsets) and a trilateral region (35 offsets, two plan
+    ranges) on the block engine and on the row form."""
+    coords = WL.random_coords(191, 4000, 7, -2, 2, batch=2)
+    cross = regions.hypercross(3, 7)
+    tri = _trilateral_7d()
     assert len(cross) == 15 and len(tri) == 35 and regions.is_symmetric(tri)
-    _say("[gpu] 7D space-time-chroma: cross (15) on the block engine, trilateral (35) on the row form")
+    _say("[gpu] 7D space-time-chroma (small box): cross (15) and trilateral (35), block engine and row form")
     _plan_case(coords, 16, 32, cross, 192)
+    _plan_case(coords, 16, 16, tri, 195)
     _conv_case(coords, 16, 16, cross, 193)
     _conv_case(coords, 8, 16, tri, 194)
+
+
+def test_7d_space_time_chroma_real_extents():
+    """7D rows at a real scene's extents (Sec. 6): the 2 cm voxels of an
+    indoor scene over three frames with RGB channels of 0..255 (52 key bits),
+    through the 7D cross and the trilateral region on the block engine and
+    the row form."""
+    coords = WL.space_time_chroma_coords(1)
+    bits = _key_bits(coords)
+    span = coords.max(0) - coords.min(0)
+    assert bits >= 50 and np.all(span[5:] >= 250) and span[4] == 2 and np.all(span[1:4] >= 150)
+    cross, tri = regions.hypercross(3, 7), _trilateral_7d()
+    _say(f"[gpu] 7D space-time-chroma, real extents: {len(coords)} rows, {bits} key bits")
+    _plan_case(coords, 16, 32, cross, 196)
+    _plan_case(coords, 16, 16, tri, 197)
+    _conv_case(coords, 16, 16, cross, 198)
+    _conv_case(coords, 8, 16, tri, 199)
+
+
+def test_7d_key_width_limit():
+    """The packed key's limit on 7D rows: the space-time-chroma rows with
+    their spatial axes scaled until the box needs exactly 62 bits still map
+    exactly; one bit more is rejected with ERANGE (the table is not built)."""
+    base = WL.space_time_chroma_coords(1).astype(np.int64)
+    at = base.copy()
+    at[:, 1] *= 16
+    at[:, 2:4] *= 8
+    over = at.copy()
+    over[:, 3] *= 2
+    assert _key_bits(at) == 62 and _key_bits(over) == 63
+    _say(f"[gpu] 7D key width: {_key_bits(at)} bits maps, {_key_bits(over)} is rejected")
+    at = at.astype(np.int32)
+    c = _t(at)
+    table = gsc.gsc_coords_build(c)
+    offs = _trilateral_7d()
+    km = gsc.gsc_kernel_map(table, c, offs)
+    maps_equal_exact(gpu_pairs(km), O.kernel_map(at, at, offs))
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_coords_build(_t(over.astype(np.int32)))
+    assert e.value.code == gsc.GSC_ERANGE
