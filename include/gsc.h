@@ -62,7 +62,8 @@ typedef enum {
     GSC_ERANGE = -3,  /* coordinates span more than 62 bits of packed key          */
     GSC_EDUP = -4,    /* a coordinate row occurs twice                             */
     GSC_EFULL = -5,   /* hash table has no free slot                               */
-    GSC_EHIP = -6     /* a HIP runtime call failed                                 */
+    GSC_EHIP = -6,    /* a HIP runtime call failed                                 */
+    GSC_ETIMEOUT = -7 /* a bounded device-side wait gave up: the result is invalid */
 } gsc_status;
 
 typedef enum { GSC_F32 = 0, GSC_BF16 = 1 } gsc_dtype;
@@ -225,6 +226,31 @@ int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int6
                            int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs,
                            int64_t* seg, int64_t* gidx, int32_t* nbr, void* stream);
 
+/* The role-reversed map (Sec. 4.2: the transposed convolution's pairs are
+ * the forward ones with input and output exchanged) of a map, built from its
+ * pairs alone, without a coordinate table.  Input (device): in_idx, out_idx
+ * and seg[K + 1] of a map as gsc_kernel_map writes it (any region, stride or
+ * output set: an input row occurs at most once per offset), cap_pairs = the
+ * length of the pair arrays (>= seg[K]; only seg[K] pairs are read), n_rev =
+ * the number of the map's input rows (they become the output rows).  Output
+ * (device, caller-allocated): t_in_idx, t_out_idx (cap_pairs each) with
+ * t_in_idx = the former output row and t_out_idx = the former input row,
+ * grouped by offset in the same order and increasing in t_out_idx within an
+ * offset; t_seg[K + 1]; t_gidx[K * G + 1], G = gsc_kmap_groups(n_rev), as
+ * gsc_kernel_map's gidx over the n_rev rows; t_nbr[K * n_rev], the dense form
+ * (the input of gsc_conv_plan).  ws: gsc_kernel_map_transpose_ws_bytes(n_rev,
+ * K).  Segment k of the result holds the pairs of offset k, so a backward
+ * call on it takes the identity as t_wsel.  Asynchronous.  A pair whose
+ * input row lies outside [0, n_rev) is left out and flagged in ws:
+ * gsc_kernel_map_transpose_status(ws, stream) synchronises and returns EINVAL
+ * then, else GSC_OK.  Errors: EINVAL, ESHORT (ws), EHIP. */
+size_t gsc_kernel_map_transpose_ws_bytes(int64_t n_rev, int32_t K);
+int gsc_kernel_map_transpose(const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg, int32_t K,
+                             int64_t cap_pairs, int64_t n_rev, int32_t* t_in_idx, int32_t* t_out_idx,
+                             int64_t* t_seg, int64_t* t_gidx, int32_t* t_nbr, void* ws, size_t ws_bytes,
+                             void* stream);
+int gsc_kernel_map_transpose_status(const void* ws, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Block plan of a kernel map (an ordering of the output rows for a4 - a6). */
 /* ------------------------------------------------------------------------ */
@@ -263,13 +289,27 @@ int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int6
  * sums in range order.
  *
  * ws: gsc_conv_plan_ws_bytes(n_out, K) bytes.  Asynchronous, deterministic.
- * Errors: EINVAL (K > 128, null pointers), ESHORT (cap_items, ws), EHIP. */
+ * Errors: EINVAL (K > 128, null pointers), ESHORT (cap_items, ws), EHIP.
+ *
+ * The sort's passes find each tile's place by looking back at the counts
+ * earlier tiles publish, polling an entry not yet published a bounded number
+ * of times (far more than a running tile needs).  Should a pass give up, it
+ * finishes with a wrong prefix, sets a status word in ws and every later step
+ * of the call stays inside its arrays; gsc_conv_plan_status then returns
+ * ETIMEOUT, and the plan must be built again before it is used.
+ * (The environment variable GSC_PLAN_SPIN_LIMIT overrides the bound for
+ * tests; a negative value gives up at once.) */
 int32_t gsc_plan_ranges(int32_t K);
 int64_t gsc_plan_blocks(int64_t n_out);
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K);
 int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K,
                   int32_t* perm, uint32_t* bmask, int64_t* ibase, int32_t* items, int64_t cap_items,
                   void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronise `stream` and return the status of the last gsc_conv_plan call
+ * that used `ws` (with the same n_out and K): GSC_OK, or GSC_ETIMEOUT if one
+ * of its sort passes gave up (EINVAL, ESHORT for bad arguments, EHIP). */
+int gsc_conv_plan_status(const void* ws, size_t ws_bytes, int64_t n_out, int32_t K, void* stream);
 
 /* 1 if gsc_sparse_conv_fwd/bwd have a block engine for a convolution whose
  * gathered rows have c_red channels and whose output rows have c_out channels
@@ -378,6 +418,27 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                         const int32_t* t_perm, const uint32_t* t_bmask, const int64_t* t_ibase,
                         const int32_t* t_items,
                         void* dX, float* dW, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
+
+/* gsc_sparse_conv_bwd from the forward map alone (the form that needs no
+ * caller-built dX map): X (n_in x c_in) and dY (n_out x c_out) are the
+ * forward convolution's input and output gradient, W its K x c_in x c_out
+ * weights, and (in_idx, out_idx, seg) its map with cap_pairs = the pair
+ * arrays' length.  transpose = 0: the forward convolution ran the map as it
+ * is (in_idx: rows of X, out_idx: rows of Y); transpose != 0: it was the
+ * transposed convolution on that map (Sec. 4.2: out_idx rows of X, in_idx
+ * rows of Y).  The call builds the dX map (gsc_kernel_map_transpose) and,
+ * when a block engine applies, its plan (gsc_conv_plan) in ws, then computes
+ * dX (nullable) and dW (nullable, float32) as gsc_sparse_conv_bwd does.  ws:
+ * gsc_conv_bwd_fwdmap_ws_bytes(dtype, n_in, cap_pairs, c_in, c_out, K)
+ * bytes.  Asynchronous; slower than gsc_sparse_conv_bwd with a dX map and
+ * plan kept from the forward pass, which is what a training loop should use.
+ * Errors: EINVAL, ESHORT (ws), EHIP. */
+size_t gsc_conv_bwd_fwdmap_ws_bytes(int32_t dtype, int64_t n_in, int64_t cap_pairs, int32_t c_in, int32_t c_out,
+                                    int32_t K);
+int gsc_sparse_conv_bwd_fwdmap(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in,
+                               int32_t c_in, int32_t c_out, int32_t K, const int32_t* in_idx, const int32_t* out_idx,
+                               const int64_t* seg, int64_t cap_pairs, int32_t transpose, void* dX, float* dW,
+                               int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Pooling over a kernel map (Sec. 4.3 max pooling, Alg. 3; Sec. 4.4         */

@@ -1004,4 +1004,96 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
     return GSC_OK;
 }
 
+// Workspace of gsc_sparse_conv_bwd_fwdmap: the weight gradient's part (as
+// gsc_sparse_conv_bwd's, with its tile counter), the dX map (dense form,
+// pairs, segments, group index) and the transposition's scratch, then, when a
+// block engine takes the input gradient, the dX map's plan and its scratch.
+struct FwdmapWs {
+    size_t dw, dense, t_in, t_out, t_seg, t_gidx, tr, perm, bmask, ibase, items, plan, total;
+};
+
+static FwdmapWs fwdmap_layout(int32_t dtype, int64_t n_in, int64_t cap, int32_t c_in, int32_t c_out, int32_t K) {
+    FwdmapWs L{};
+    const int64_t G = gsc_kmap_groups(n_in);
+    size_t o = 0;
+    auto take = [&](size_t b) {
+        const size_t at = o;
+        o += al256(b);
+        return at;
+    };
+    L.dw = take(gsc_conv_bwd_ws_bytes(cap, c_in, c_out, K));
+    L.dense = take((size_t)K * n_in * sizeof(int32_t));
+    L.t_in = take((size_t)cap * sizeof(int32_t));
+    L.t_out = take((size_t)cap * sizeof(int32_t));
+    L.t_seg = take((size_t)(K + 1) * sizeof(int64_t));
+    L.t_gidx = take((size_t)(K * G + 1) * sizeof(int64_t));
+    L.tr = take(gsc_kernel_map_transpose_ws_bytes(n_in, K));
+    if (gsc_conv_block_engine(dtype, c_out, c_in, K)) {
+        const int64_t R = gsc_plan_ranges(K), nb = gsc_plan_blocks(n_in);
+        L.perm = take((size_t)R * n_in * sizeof(int32_t));
+        L.bmask = take((size_t)R * nb * sizeof(uint32_t));
+        L.ibase = take((size_t)R * (nb + 1) * sizeof(int64_t));
+        L.items = take((size_t)K * nb * 16 * sizeof(int32_t));
+        L.plan = take(gsc_conv_plan_ws_bytes(n_in, K));
+    } else {
+        L.perm = L.bmask = L.ibase = L.items = L.plan = SIZE_MAX;
+    }
+    L.total = o;
+    return L;
+}
+
+size_t gsc_conv_bwd_fwdmap_ws_bytes(int32_t dtype, int64_t n_in, int64_t cap_pairs, int32_t c_in, int32_t c_out,
+                                    int32_t K) {
+    if ((dtype != GSC_F32 && dtype != GSC_BF16) || n_in < 0 || cap_pairs < 0 || c_in < 1 || c_out < 1 || K < 1 ||
+        K > kMaxKConv)
+        return 0;
+    return fwdmap_layout(dtype, n_in, cap_pairs, c_in, c_out, K).total;
+}
+
+int gsc_sparse_conv_bwd_fwdmap(int32_t dtype, const void* X, const void* W, const void* dY, int64_t n_in,
+                               int32_t c_in, int32_t c_out, int32_t K, const int32_t* in_idx, const int32_t* out_idx,
+                               const int64_t* seg, int64_t cap_pairs, int32_t transpose, void* dX, float* dW,
+                               int64_t n_out, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (dtype != GSC_F32 && dtype != GSC_BF16) return fail(GSC_EINVAL, "conv_bwd_fwdmap: unknown dtype %d", dtype);
+    if (K < 1 || K > kMaxKConv) return fail(GSC_EINVAL, "conv_bwd_fwdmap: K=%d outside [1,%d]", K, kMaxKConv);
+    if (n_in < 0 || n_out < 0 || n_in > INT32_MAX || n_out > INT32_MAX || cap_pairs < 0 || c_in < 1 || c_out < 1)
+        return fail(GSC_EINVAL, "conv_bwd_fwdmap: bad sizes");
+    if (!seg || !ws) return fail(GSC_EINVAL, "conv_bwd_fwdmap: null seg/ws");
+    const size_t need = gsc_conv_bwd_fwdmap_ws_bytes(dtype, n_in, cap_pairs, c_in, c_out, K);
+    if (ws_bytes < need) return fail(GSC_ESHORT, "conv_bwd_fwdmap: ws needs %zu bytes, got %zu", need, ws_bytes);
+    // a: the pairs' rows of X, b: their rows of Y (the transposed convolution ran the map with roles exchanged)
+    const int32_t* a = transpose ? out_idx : in_idx;
+    const int32_t* b = transpose ? in_idx : out_idx;
+    const FwdmapWs L = fwdmap_layout(dtype, n_in, cap_pairs, c_in, c_out, K);
+    char* w = reinterpret_cast<char*>(ws);
+    int32_t* t_in = reinterpret_cast<int32_t*>(w + L.t_in);
+    int32_t* t_out = reinterpret_cast<int32_t*>(w + L.t_out);
+    int64_t* t_seg = reinterpret_cast<int64_t*>(w + L.t_seg);
+    int64_t* t_gidx = reinterpret_cast<int64_t*>(w + L.t_gidx);
+    int32_t* dense = reinterpret_cast<int32_t*>(w + L.dense);
+    const bool planned = L.plan != SIZE_MAX;
+    int32_t* perm = planned ? reinterpret_cast<int32_t*>(w + L.perm) : nullptr;
+    uint32_t* bmask = planned ? reinterpret_cast<uint32_t*>(w + L.bmask) : nullptr;
+    int64_t* ibase = planned ? reinterpret_cast<int64_t*>(w + L.ibase) : nullptr;
+    int32_t* items = planned ? reinterpret_cast<int32_t*>(w + L.items) : nullptr;
+    int rc;
+    if (dX) {
+        // the dX map: the same pairs listed by their row of X (and its plan)
+        rc = gsc_kernel_map_transpose(a, b, seg, K, cap_pairs, n_in, t_in, t_out, t_seg, t_gidx, dense, w + L.tr,
+                                      gsc_kernel_map_transpose_ws_bytes(n_in, K), stream);
+        if (rc) return rc;
+        if (planned) {
+            rc = gsc_conv_plan(dense, n_in, K, perm, bmask, ibase, items, (int64_t)K * gsc_plan_blocks(n_in),
+                               w + L.plan, gsc_conv_plan_ws_bytes(n_in, K), stream);
+            if (rc) return rc;
+        }
+    }
+    std::vector<int32_t> ident((size_t)K);
+    for (int k = 0; k < K; ++k) ident[k] = k;   // segment k of the dX map holds offset k's pairs
+    return gsc_sparse_conv_bwd(dtype, X, W, dY, n_in, c_in, c_out, K, a, b, seg, cap_pairs, t_in, t_out, t_seg,
+                               t_gidx, cap_pairs, ident.data(), perm, bmask, ibase, items, dX, dW, n_out, w + L.dw,
+                               gsc_conv_bwd_ws_bytes(cap_pairs, c_in, c_out, K), stream);
+}
+
 }  // extern "C"

@@ -26,6 +26,7 @@
 // not (other coordinates, another order, rows rewritten since the build),
 // the second pass probes the mirrored offsets itself instead, overwriting
 // their entries, so the result equals the full probe in every case.
+#include <algorithm>
 #include <climits>
 #include <mutex>
 #include <vector>
@@ -325,6 +326,53 @@ __global__ void __launch_bounds__(kThreads) k_kmap_fill(int64_t n_out, int K, in
 
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// ---------------------------------------------------------------------------
+// Role reversal of a map without the coordinate table (Sec. 4.2: the pairs of
+// the transposed convolution are those of the forward one with input and
+// output exchanged).  A map lists each input row at most once per offset (its
+// output coordinate is the input's minus the scaled offset), so the reversed
+// map's dense form is a scatter of the pairs; the count, scan and fill passes
+// of the kernel map then list the pairs by the former input row.
+// ---------------------------------------------------------------------------
+__global__ void k_fill_neg1(int32_t* __restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = -1;
+}
+
+// nbr[k * n_rev + in_idx[p]] = out_idx[p] for the pairs p < seg[K] (offset k
+// of pair p found by a search of seg); a row outside [0, n_rev) is skipped
+// (the caller's map is checked: err[0] is set).
+__global__ void __launch_bounds__(kThreads) k_map_scatter(const int32_t* __restrict__ in_idx,
+                                                          const int32_t* __restrict__ out_idx,
+                                                          const int64_t* __restrict__ seg, int K, int64_t cap,
+                                                          int64_t n_rev, int32_t* __restrict__ nbr,
+                                                          int32_t* __restrict__ err) {
+    const int64_t total = seg[K] < cap ? seg[K] : cap;
+    for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < total; p += (int64_t)gridDim.x * kThreads) {
+        int lo = 0, hi = K;   // the k with seg[k] <= p < seg[k + 1]
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (seg[mid] <= p) lo = mid;
+            else hi = mid;
+        }
+        const int32_t r = in_idx[p];
+        if (r >= 0 && r < n_rev) nbr[(int64_t)lo * n_rev + r] = out_idx[p];
+        else atomicOr(err, 1);
+    }
+}
+
+// cnt[k * G + g] = entries >= 0 of nbr[k * n][64 g .. 64 g + 63].
+__global__ void __launch_bounds__(kThreads) k_nbr_count(const int32_t* __restrict__ nbr, int64_t n, int K, int64_t G,
+                                                        int32_t* __restrict__ cnt) {
+    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t g = j >> 6;
+    const bool valid = j < n;
+    for (int k = 0; k < K; ++k) {
+        const unsigned long long m = __ballot(valid && nbr[(int64_t)k * n + j] >= 0);
+        if ((threadIdx.x & 63) == 0 && g < G) cnt[(int64_t)k * G + g] = (int32_t)__popcll(m);
+    }
+}
+
 template <typename Offs>
 static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t n_out, int ncol, Offs offs, int K,
                         int sym, int64_t G, int32_t* in_idx, int32_t* out_idx, int64_t cap_pairs, int64_t* seg,
@@ -535,6 +583,71 @@ int gsc_kernel_map_noalloc(const void* in_table, const int32_t* out_coords, int6
     w += align256((size_t)K * G * sizeof(int32_t));
     return kmap_enqueue(in_table, out_coords, n_out, D + 1, arg, K, sym, G, in_idx, out_idx, cap_pairs, seg, gidx,
                         nullptr, res, cnt, nbr, w, s);
+}
+
+size_t gsc_kernel_map_transpose_ws_bytes(int64_t n_rev, int32_t K) {
+    if (n_rev < 0 || K < 1) return 0;
+    const int64_t G = gsc_kmap_groups(n_rev);
+    return align256(sizeof(int64_t)) + align256((size_t)K * G * sizeof(int32_t)) + scan_ws_bytes(K * G) + 256;
+}
+
+int gsc_kernel_map_transpose(const int32_t* in_idx, const int32_t* out_idx, const int64_t* seg, int32_t K,
+                             int64_t cap_pairs, int64_t n_rev, int32_t* t_in_idx, int32_t* t_out_idx, int64_t* t_seg,
+                             int64_t* t_gidx, int32_t* t_nbr, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (K < 1 || cap_pairs < 0 || n_rev < 0 || n_rev > INT32_MAX)
+        return fail(GSC_EINVAL, "kernel_map_transpose: bad K=%d, cap_pairs=%lld or n_rev=%lld", K,
+                    (long long)cap_pairs, (long long)n_rev);
+    if (!seg || !t_seg || !t_gidx || !t_nbr || !ws)
+        return fail(GSC_EINVAL, "kernel_map_transpose: null seg/t_seg/t_gidx/t_nbr/ws");
+    if (cap_pairs > 0 && (!in_idx || !out_idx || !t_in_idx || !t_out_idx))
+        return fail(GSC_EINVAL, "kernel_map_transpose: null pair arrays");
+    const size_t need = gsc_kernel_map_transpose_ws_bytes(n_rev, K);
+    if (ws_bytes < need)
+        return fail(GSC_ESHORT, "kernel_map_transpose: ws needs %zu bytes, got %zu", need, ws_bytes);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int64_t G = gsc_kmap_groups(n_rev);
+    char* w = reinterpret_cast<char*>(ws);
+    int32_t* err = reinterpret_cast<int32_t*>(w);
+    w += align256(sizeof(int64_t));
+    int32_t* cnt = reinterpret_cast<int32_t*>(w);
+    w += align256((size_t)K * G * sizeof(int32_t));
+    const int64_t n_dense = (int64_t)K * n_rev;
+    hipLaunchKernelGGL(k_fill_neg1, dim3((unsigned)std::min<int64_t>((n_dense + kThreads - 1) / kThreads + 1, 4096)),
+                       dim3(kThreads), 0, s, t_nbr, n_dense);
+    GSC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_zero_i64, dim3(1), dim3(64), 0, s, reinterpret_cast<int64_t*>(err), (int64_t)1);
+    GSC_LAUNCH_CHECK();
+    if (cap_pairs > 0) {
+        hipLaunchKernelGGL(k_map_scatter, dim3((unsigned)std::min<int64_t>((cap_pairs + kThreads - 1) / kThreads, 8192)),
+                           dim3(kThreads), 0, s, in_idx, out_idx, seg, K, cap_pairs, n_rev, t_nbr, err);
+        GSC_LAUNCH_CHECK();
+    }
+    const unsigned nblk = (unsigned)((n_rev + kThreads - 1) / kThreads);
+    if (nblk > 0) {
+        hipLaunchKernelGGL(k_nbr_count, dim3(nblk), dim3(kThreads), 0, s, t_nbr, n_rev, K, G, cnt);
+        GSC_LAUNCH_CHECK();
+    }
+    int rc = scan_counts(cnt, K * G, t_gidx, nullptr, w, s);
+    if (rc) return rc;
+    rc = seg_from_gidx(t_gidx, K, G, t_seg, s);
+    if (rc) return rc;
+    if (nblk > 0 && cap_pairs > 0) {
+        hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, n_rev, K, G, t_nbr, t_gidx, t_in_idx,
+                           t_out_idx, cap_pairs);
+        GSC_LAUNCH_CHECK();
+    }
+    return GSC_OK;
+}
+
+int gsc_kernel_map_transpose_status(const void* ws, void* stream) {
+    clear_error();
+    if (!ws) return fail(GSC_EINVAL, "kernel_map_transpose_status: null ws");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int32_t e = 0;
+    GSC_HIP(hipMemcpyAsync(&e, ws, sizeof(e), hipMemcpyDeviceToHost, s));
+    GSC_HIP(hipStreamSynchronize(s));
+    return e ? fail(GSC_EINVAL, "kernel_map_transpose: a pair's input row lies outside [0, n_rev)") : GSC_OK;
 }
 
 }  // extern "C"

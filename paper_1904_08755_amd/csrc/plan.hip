@@ -29,6 +29,7 @@
 //           items.
 // Everything is deterministic and runs without a host round trip.
 #include <climits>
+#include <cstdlib>
 
 #include "gsc_internal.h"
 
@@ -50,7 +51,8 @@ static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 // which the histogram kernel after it starts to fill.)
 __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int K,
                                                              uint32_t* __restrict__ keys, uint32_t* __restrict__ zero,
-                                                             int64_t nzero) {
+                                                             int64_t nzero, uint32_t* __restrict__ lb_status) {
+    if (lb_status && blockIdx.x == 0 && threadIdx.x == 0) *lb_status = 0u;   // the plan call's first kernel
     for (int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x; i < nzero;
          i += (int64_t)gridDim.x * kPlanThreads)
         zero[i] = 0;
@@ -85,7 +87,7 @@ constexpr uint32_t kStAgg = 1u << 30;             // entry holds the tile's own 
 constexpr uint32_t kStIncl = 1u << 31;            // entry holds the inclusive prefix
 constexpr uint32_t kStCount = kStAgg - 1;
 constexpr int64_t kRsMaxKeys = kStCount;          // counts must fit below the flag bits
-constexpr int kSpinMax = 1 << 22;                 // bound on polls of one entry (never reached)
+constexpr int kSpinMax = 1 << 22;                 // bound on polls of one entry (not reached in practice)
 
 __global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restrict__ keys, int64_t n, int passes,
                                                          uint32_t* __restrict__ ghist) {
@@ -139,7 +141,8 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
                                                         uint32_t* __restrict__ status,
                                                         uint32_t* __restrict__ status_next,
                                                         uint32_t* __restrict__ ticket, uint32_t* __restrict__ kout,
-                                                        int32_t* __restrict__ vout) {
+                                                        int32_t* __restrict__ vout, int spin_max,
+                                                        uint32_t* __restrict__ lb_status) {
     constexpr int W = kRsThreads / 64;
     static_assert(kRsThreads == kRsBins, "one thread per digit in the look-back");
     __shared__ int64_t start[kRsBins];
@@ -187,11 +190,16 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
 #pragma unroll
                 for (int i = 0; i < LW; ++i) {
                     if (done) break;
-                    uint32_t x = v[i];
-                    for (int spin = 0; x == 0 && spin < kSpinMax; ++spin) {   // not published yet: it will be
+                    uint32_t x = spin_max < 0 ? 0u : v[i];   // spin_max < 0: give up at once (tests only)
+                    for (int spin = 0; x == 0 && spin < spin_max; ++spin) {   // not published yet: it will be
                         __builtin_amdgcn_s_sleep(1);
                         x = __hip_atomic_load(status + (j0 - i) * kRsBins + tid, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    if (x == 0) {   // gave up: the prefix is wrong, and the plan call's status says so
+                        __hip_atomic_fetch_or(lb_status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        done = true;
+                        break;
                     }
                     before += x & kStCount;
                     done = (x & kStIncl) != 0;
@@ -254,10 +262,14 @@ __device__ __forceinline__ uint32_t block_or16(uint32_t v) {
     return v;
 }
 
-__global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __restrict__ keys, int64_t n, int64_t nb,
-                                                            uint32_t* __restrict__ bmask, int32_t* __restrict__ cnt) {
+// (The sorted keys are masked to the K offsets and the rows clamped to
+// [0, n): after a look-back that gave up they need not be what the sort
+// meant, and the plan must still stay inside its arrays.)
+__global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __restrict__ keys, uint32_t kmask,
+                                                            int64_t n, int64_t nb, uint32_t* __restrict__ bmask,
+                                                            int32_t* __restrict__ cnt) {
     const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
-    const uint32_t u = block_or16(i < n ? keys[i] : 0u);
+    const uint32_t u = block_or16(i < n ? keys[i] & kmask : 0u);
     const int64_t b = i >> 4;
     if ((threadIdx.x & 15) == 0 && b < nb) {
         bmask[b] = u;
@@ -265,7 +277,7 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __re
     }
 }
 
-__global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __restrict__ keys,
+__global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __restrict__ keys, uint32_t kmask,
                                                            const int32_t* __restrict__ perm,
                                                            const int32_t* __restrict__ nbr,
                                                            const int64_t* __restrict__ ibase, int64_t n, int64_t nb,
@@ -274,10 +286,11 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
     const int64_t b = i >> 4;
     const int r = threadIdx.x & 15;
     const bool valid = i < n;
-    const uint32_t key = valid ? keys[i] : 0u;
+    const uint32_t key = valid ? keys[i] & kmask : 0u;
     const uint32_t u = block_or16(key);
     if (b >= nb) return;   // whole blocks of 16 lanes leave together
-    const int64_t row = valid ? perm[i] : 0;
+    const int32_t pr = valid ? perm[i] : 0;
+    const int64_t row = pr >= 0 && pr < n ? pr : 0;
     const int64_t base = ibase[b];
     uint32_t m = u;
     // four of the block's offsets per round, their table entries loaded together
@@ -297,8 +310,19 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
     }
 }
 
+// Sets ibase[0] = 0 and clears the look-back status (a plan over no rows).
+__global__ void k_plan_empty(int64_t* ibase, uint32_t* lb_status) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        ibase[0] = 0;
+        if (lb_status) *lb_status = 0u;
+    }
+}
+
+// lb_status: the plan call's look-back status word, cleared here when
+// clear_status (the call's first range) and set by a pass that gave up.
 static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
-                        int32_t* items, void* ws, hipStream_t s) {
+                        int32_t* items, void* ws, uint32_t* lb_status, bool clear_status, int spin_max,
+                        hipStream_t s) {
     const int64_t nb = (n + 15) / 16;
     const int64_t nrs = (n + kRsTile - 1) / kRsTile;
     const int passes = (K + kRsBits - 1) / kRsBits;
@@ -325,13 +349,16 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
     w += al256((size_t)nb * sizeof(int32_t));
     void* scan_ws = w;
 
+    uint32_t* lb_clear = clear_status ? lb_status : nullptr;
     if (n == 0) {
-        hipLaunchKernelGGL(k_zero_i64, dim3(1), dim3(256), 0, s, ibase, (int64_t)1);
+        hipLaunchKernelGGL(k_plan_empty, dim3(1), dim3(64), 0, s, ibase, lb_clear);
         GSC_LAUNCH_CHECK();
         return GSC_OK;
     }
+    const uint32_t kmask = K >= 32 ? ~0u : (1u << K) - 1u;
     const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
-    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka, ghist, nzero);
+    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka, ghist, nzero,
+                       lb_clear);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
     GSC_LAUNCH_CHECK();
@@ -345,18 +372,35 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
         uint32_t* st = (p & 1) ? st1 : st0;
         uint32_t* st_next = (p & 1) ? st0 : st1;
         hipLaunchKernelGGL(k_rs_pass, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n, p * kRsBits,
-                           gbase + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout);
+                           gbase + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout, spin_max, lb_status);
         GSC_LAUNCH_CHECK();
         kin = kout;
         vin = vout;
     }
-    hipLaunchKernelGGL(k_blk_count, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, n, nb, bmask, cnt);
+    hipLaunchKernelGGL(k_blk_count, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, kmask, n, nb, bmask, cnt);
     GSC_LAUNCH_CHECK();
     int rc = scan_counts(cnt, nb, ibase, nullptr, scan_ws, s);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, perm, nbr, ibase, n, nb, items);
+    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, kmask, perm, nbr, ibase, n, nb,
+                       items);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
+}
+
+// The look-back status word sits in the last 256 bytes of the plan's ws.
+static uint32_t* plan_status_word(void* ws, int64_t n_out, int K) {
+    return reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + gsc_conv_plan_ws_bytes(n_out, K) - 256);
+}
+
+// Polls of one look-back entry before a pass gives up: kSpinMax, or the value
+// of the environment variable GSC_PLAN_SPIN_LIMIT (a test hook: a negative
+// value gives up at the first poll, so the failure path can be exercised
+// while every kernel still ends normally).
+static int lookback_spin_limit() {
+    const char* e = getenv("GSC_PLAN_SPIN_LIMIT");
+    if (!e || !*e) return kSpinMax;
+    const long v = strtol(e, nullptr, 10);
+    return v < -1 ? -1 : (v > kSpinMax ? kSpinMax : (int)v);
 }
 
 }  // namespace gsc
@@ -400,14 +444,33 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, u
     // one plan per range of offsets, one after another on the stream (they share ws)
     const int R = plan_ranges(K), S = plan_range_size(K);
     const int64_t nb = gsc_plan_blocks(n_out);
+    uint32_t* lb_status = plan_status_word(ws, n_out, K);
+    const int spin_max = lookback_spin_limit();
     for (int r = 0; r < R; ++r) {
         const int k0 = r * S, kr = K - k0 < S ? K - k0 : S;
         const int rc = plan_enqueue(nbr ? nbr + (int64_t)k0 * n_out : nullptr, n_out, kr,
                                     perm ? perm + (int64_t)r * n_out : nullptr, bmask ? bmask + (int64_t)r * nb : nullptr,
                                     ibase + (int64_t)r * (nb + 1), items ? items + (int64_t)k0 * nb * 16 : nullptr, ws,
-                                    reinterpret_cast<hipStream_t>(stream));
+                                    lb_status, r == 0, spin_max, reinterpret_cast<hipStream_t>(stream));
         if (rc) return rc;
     }
+    return GSC_OK;
+}
+
+int gsc_conv_plan_status(const void* ws, size_t ws_bytes, int64_t n_out, int32_t K, void* stream) {
+    clear_error();
+    const size_t need = gsc_conv_plan_ws_bytes(n_out, K);
+    if (!ws || need == 0) return fail(GSC_EINVAL, "conv_plan_status: null ws or bad n_out/K");
+    if (ws_bytes < need) return fail(GSC_ESHORT, "conv_plan_status: ws needs %zu bytes, got %zu", need, ws_bytes);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    uint32_t word = 0;
+    if (hipMemcpyAsync(&word, plan_status_word(const_cast<void*>(ws), n_out, K), sizeof(word), hipMemcpyDeviceToHost,
+                       s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(GSC_EHIP, "conv_plan_status: %s", hipGetErrorString(hipGetLastError()));
+    if (word != 0)
+        return fail(GSC_ETIMEOUT, "conv_plan: a radix pass gave up waiting for an earlier tile's count; the plan "
+                                  "is not valid");
     return GSC_OK;
 }
 

@@ -19,12 +19,12 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgsc.so")
 
-GSC_OK, GSC_EINVAL, GSC_ESHORT, GSC_ERANGE, GSC_EDUP, GSC_EFULL, GSC_EHIP = 0, -1, -2, -3, -4, -5, -6
+GSC_OK, GSC_EINVAL, GSC_ESHORT, GSC_ERANGE, GSC_EDUP, GSC_EFULL, GSC_EHIP, GSC_ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
 GSC_F32, GSC_BF16 = 0, 1
 GROUP_ROWS = 64
 
 _STATUS = {GSC_EINVAL: "EINVAL", GSC_ESHORT: "ESHORT", GSC_ERANGE: "ERANGE", GSC_EDUP: "EDUP",
-           GSC_EFULL: "EFULL", GSC_EHIP: "EHIP"}
+           GSC_EFULL: "EFULL", GSC_EHIP: "EHIP", GSC_ETIMEOUT: "ETIMEOUT"}
 
 
 class GscError(RuntimeError):
@@ -59,6 +59,14 @@ _SIGS = {
                                               _vp, _vp, _vp]),
     "gsc_plan_blocks": (_i64, [_i64]),
     "gsc_plan_ranges": (_i32, [_i32]),
+    "gsc_kernel_map_transpose_ws_bytes": (_sz, [_i64, _i32]),
+    "gsc_kernel_map_transpose": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                                                _vp]),
+    "gsc_kernel_map_transpose_status": (ctypes.c_int, [_vp, _vp]),
+    "gsc_conv_bwd_fwdmap_ws_bytes": (_sz, [_i32, _i64, _i64, _i32, _i32, _i32]),
+    "gsc_sparse_conv_bwd_fwdmap": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp, _vp, _i64,
+                                                  _i32, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "gsc_conv_plan_status": (ctypes.c_int, [_vp, _sz, _i64, _i32, _vp]),
     "gsc_conv_plan_ws_bytes": (_sz, [_i64, _i32]),
     "gsc_conv_plan": (ctypes.c_int, [_vp, _i64, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "gsc_conv_block_engine": (_i32, [_i32, _i32, _i32, _i32]),
@@ -360,6 +368,36 @@ def gsc_conv_plan(kmap: KernelMap, bufs: Optional[PlanBuffers] = None, stream=No
     return dataclasses.replace(kmap, plan=plan)
 
 
+def gsc_conv_plan_status(kmap: KernelMap, bufs: PlanBuffers, stream=None) -> None:
+    """Synchronise and raise GscError (ETIMEOUT) if the plan built into
+    ``bufs`` for ``kmap`` came from a sort pass that gave up."""
+    _check(lib().gsc_conv_plan_status(_ptr(bufs.ws), bufs.ws.numel(), kmap.n_out, kmap.K, _stream(stream)))
+
+
+def gsc_kernel_map_transpose(kmap: KernelMap, n_rev: int, stream=None, check: bool = True) -> KernelMap:
+    """The role-reversed map of ``kmap`` (pairs listed by the former input
+    row, over ``n_rev`` rows) built from its pairs alone, with its dense form;
+    segment k holds offset k's pairs, so its t_wsel is the identity.  With
+    ``check`` the call synchronises and raises if a pair's input row lies
+    outside [0, n_rev)."""
+    K, dev = kmap.K, kmap.seg.device
+    cap = kmap.n_bound
+    G = gsc_kmap_groups(n_rev)
+    t_in = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    t_out = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    t_seg = torch.empty(K + 1, dtype=torch.int64, device=dev)
+    t_gidx = torch.empty(K * G + 1, dtype=torch.int64, device=dev)
+    t_nbr = torch.empty((K, max(n_rev, 1)), dtype=torch.int32, device=dev)
+    ws = _ws(lib().gsc_kernel_map_transpose_ws_bytes(n_rev, K), dev)
+    _check(lib().gsc_kernel_map_transpose(_ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg), K, cap, n_rev,
+                                          _ptr(t_in), _ptr(t_out), _ptr(t_seg), _ptr(t_gidx), _ptr(t_nbr), _ptr(ws),
+                                          ws.numel(), _stream(stream)))
+    if check:
+        _check(lib().gsc_kernel_map_transpose_status(_ptr(ws), _stream(stream)))
+    return KernelMap(t_in, t_out, t_seg, t_gidx, kmap.n_pairs, n_rev, -np.asarray(kmap.offsets), cap,
+                     nbr=t_nbr[:, :n_rev])
+
+
 def negation_permutation(offsets) -> np.ndarray:
     """s -> index of -o_s (for symmetric offset sets)."""
     offs = np.asarray(offsets)
@@ -472,6 +510,32 @@ def gsc_sparse_conv_bwd(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap
         _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
         _ptr(ws) if need_dw else None, ws.numel() if need_dw else 0, _stream(stream)))
     return (dX if need_dx else None), (dW if need_dw else None)
+
+
+def gsc_sparse_conv_bwd_fwdmap(X: torch.Tensor, W: torch.Tensor, dY: torch.Tensor, kmap: KernelMap,
+                               transpose: bool = False, need_dx: bool = True, need_dw: bool = True,
+                               ws: Optional[torch.Tensor] = None, stream=None):
+    """(dX or None, dW or None) from the forward map alone: the library builds
+    the dX map (and its plan) itself.  ``transpose``: the forward pass was the
+    transposed convolution on ``kmap`` (out_idx rows of X, in_idx rows of Y)."""
+    dt = _dt(X)
+    _need(X, X.dtype, "X", 2)
+    _need(W, X.dtype, "W", 3)
+    _need(dY, X.dtype, "dY", 2)
+    K, ci, co = W.shape
+    n_in, n_out = X.shape[0], dY.shape[0]
+    if X.shape[1] != ci or dY.shape[1] != co or kmap.K != K:
+        raise ValueError("shape mismatch")
+    dev = X.device
+    dX = torch.empty((n_in, ci), dtype=X.dtype, device=dev) if need_dx else None
+    dW = torch.empty((K, ci, co), dtype=torch.float32, device=dev) if need_dw else None
+    if ws is None:
+        ws = _ws(lib().gsc_conv_bwd_fwdmap_ws_bytes(dt, n_in, kmap.n_bound, ci, co, K), dev)
+    _check(lib().gsc_sparse_conv_bwd_fwdmap(
+        dt, _ptr(X), _ptr(W), _ptr(dY), n_in, ci, co, K, _ptr(kmap.in_idx), _ptr(kmap.out_idx), _ptr(kmap.seg),
+        kmap.n_bound, 1 if transpose else 0, _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
+        _ptr(ws), ws.numel(), _stream(stream)))
+    return dX, dW
 
 
 # --------------------------------------------------------------------------- #

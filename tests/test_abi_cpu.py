@@ -151,6 +151,26 @@ def test_conv_validation(L):
     assert rc == gsc.GSC_ESHORT
 
 
+def test_map_transpose_and_fwdmap_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    need = L.gsc_kernel_map_transpose_ws_bytes(100, 27)
+    assert need > 0 and L.gsc_kernel_map_transpose_ws_bytes(-1, 27) == 0
+    tr = lambda K=27, cap=50, n=100, ws=fake, wsb=need, seg=fake: L.gsc_kernel_map_transpose(
+        fake, fake, seg, K, cap, n, fake, fake, fake, fake, fake, ws, wsb, None)
+    assert tr(K=0) == gsc.GSC_EINVAL
+    assert tr(seg=None) == gsc.GSC_EINVAL
+    assert tr(ws=None) == gsc.GSC_EINVAL
+    assert tr(wsb=need - 1) == gsc.GSC_ESHORT
+    assert L.gsc_kernel_map_transpose_status(None, None) == gsc.GSC_EINVAL
+    wb = L.gsc_conv_bwd_fwdmap_ws_bytes(gsc.GSC_F32, 100, 500, 32, 32, 27)
+    assert wb > L.gsc_conv_bwd_ws_bytes(500, 32, 32, 27) and L.gsc_conv_bwd_fwdmap_ws_bytes(7, 100, 500, 32, 32, 27) == 0
+    bwd = lambda dt=0, K=27, wsb=wb: L.gsc_sparse_conv_bwd_fwdmap(
+        dt, fake, fake, fake, 100, 32, 32, K, fake, fake, fake, 500, 0, fake, None, 100, fake, wsb, None)
+    assert bwd(dt=7) == gsc.GSC_EINVAL
+    assert bwd(K=0) == gsc.GSC_EINVAL
+    assert bwd(wsb=wb - 1) == gsc.GSC_ESHORT
+
+
 def test_plan_validation(L):
     fake = ctypes.c_void_p(0x1000)
     ws = L.gsc_conv_plan_ws_bytes(100, 27)
@@ -166,6 +186,8 @@ def test_plan_validation(L):
     assert plan(27, wsb=ws - 1) == gsc.GSC_ESHORT
     assert plan(27, cap=cap - 1) == gsc.GSC_ESHORT and str(cap) in _err(L)
     assert plan(27, ib=None) == gsc.GSC_EINVAL
+    assert L.gsc_conv_plan_status(None, ws, 100, 27, None) == gsc.GSC_EINVAL
+    assert L.gsc_conv_plan_status(fake, ws - 1, 100, 27, None) == gsc.GSC_ESHORT
     # the block engines and the shapes they take
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 32, 32, 27) == 1
     assert L.gsc_conv_block_engine(gsc.GSC_F32, 64, 64, 9) == 1

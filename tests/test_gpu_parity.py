@@ -358,6 +358,28 @@ def _check_plan_range(n, nbr, perm, bm, ib, items):
         below += (bm >> k) & 1
 
 
+def test_plan_lookback_give_up_is_reported(monkeypatch):
+    """A sort pass whose look-back gives up (forced from the host: the
+    environment's spin limit makes every poll give up at once) finishes
+    normally and the plan call's status reports ETIMEOUT; with the normal
+    bound the same buffers give a valid plan and status OK."""
+    coords = WL.random_coords(175, 24000, 3, -25, 25, batch=2)   # about a dozen sort tiles
+    c = _t(coords)
+    offs = regions.hypercube(3, 3)
+    km = gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, offs, dense=True)
+    bufs = gsc.PlanBuffers(km.n_out, km.K, DEV)
+    _say(f"[gpu] look-back give-up forced on n={km.n_out}")
+    monkeypatch.setenv("GSC_PLAN_SPIN_LIMIT", "-1")
+    gsc.gsc_conv_plan(km, bufs)
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_conv_plan_status(km, bufs)
+    assert e.value.code == gsc.GSC_ETIMEOUT
+    monkeypatch.delenv("GSC_PLAN_SPIN_LIMIT")
+    pm = gsc.gsc_conv_plan(km, bufs)
+    gsc.gsc_conv_plan_status(km, bufs)
+    _check_plan(pm)
+
+
 @pytest.mark.parametrize("cid", [1, 2, 3])
 def test_conv_plan_block_engine(cid):
     # the block engines on the plan against the oracle, the row-form kernels
@@ -958,3 +980,83 @@ def test_7d_key_width_limit():
     with pytest.raises(gsc.GscError) as e:
         gsc.gsc_coords_build(_t(over.astype(np.int32)))
     assert e.value.code == gsc.GSC_ERANGE
+
+
+# --------------------------------------------------------------------------- #
+# the dX map from the pairs alone, and the backward from the forward map
+# --------------------------------------------------------------------------- #
+def _strided_case(seed):
+    """A stride-2 downsampling map (size-2 kernel): fine coordinates in, the
+    oracle's coarse coordinates out; returns the GPU map and the oracle's."""
+    fine = WL.random_coords(seed, 5000, 3, -16, 16, batch=2)
+    coarse = O.output_coordinates(fine, 2).astype(np.int32)
+    offs = regions.hypercube(2, 3)
+    km = gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(fine)), _t(coarse), offs)
+    return fine, coarse, km, O.kernel_map(fine, coarse, np.asarray(offs))
+
+
+@pytest.mark.parametrize("case", ["cube3", "asymmetric", "stride2"])
+def test_kernel_map_transpose_matches_table_query(case):
+    """The role-reversed map built from a map's pairs (Sec. 4.2) equals the one
+    the table query with negated offsets gives: pairs, segments, group index
+    and dense form, bit for bit."""
+    if case == "stride2":
+        fine, coarse, km, m = _strided_case(176)
+        n_rev = len(fine)
+        ref = gsc.transposed_kernel_map(gsc.gsc_coords_build(_t(coarse)), _t(fine), km.offsets, tensor_stride=1,
+                                        dense=True)
+    else:
+        coords = WL.random_coords(177, 4000, 3, -12, 12, batch=2)
+        c = _t(coords)
+        offs = regions.hypercube(3, 3) if case == "cube3" else np.array(
+            [[0, 0, 0], [1, 0, 0], [0, 2, 0], [1, 1, -1], [-2, 0, 1]], np.int32)
+        table = gsc.gsc_coords_build(c)
+        km = gsc.gsc_kernel_map(table, c, offs)
+        ref = gsc.transposed_kernel_map(table, c, offs, dense=True)
+        n_rev = len(coords)
+        m = O.kernel_map(coords, coords, np.asarray(offs))
+    _say(f"[gpu] map transpose {case}: {km.n_pairs} pairs")
+    tm = gsc.gsc_kernel_map_transpose(km, n_rev)
+    torch.cuda.synchronize()
+    maps_equal_exact(gpu_pairs(tm), O.transposed_map(m))
+    for (a, b), (x, y) in zip(gpu_pairs(tm), gpu_pairs(ref)):
+        assert np.array_equal(a, x) and np.array_equal(b, y)
+    assert torch.equal(tm.seg.cpu(), ref.seg.cpu())
+    assert torch.equal(tm.gidx.cpu(), ref.gidx.cpu())
+    assert torch.equal(tm.nbr.cpu(), ref.nbr.cpu())
+
+
+@pytest.mark.parametrize("dtype,ci,co,case,transpose", [
+    ("f32", 32, 32, "cube3", False), ("f32", 16, 8, "stride2", False), ("f32", 8, 16, "stride2", True),
+    ("bf16", 64, 64, "cube3", False), ("bf16", 48, 24, "stride2", True), ("f32", 3, 5, "cube3", False)])
+def test_conv_bwd_from_forward_map(dtype, ci, co, case, transpose):
+    """gsc_sparse_conv_bwd_fwdmap (the forward map plus a transpose flag; the
+    library builds the dX map and its plan) against the oracle's gradients of
+    the forward (transpose = 0) or the transposed convolution on the map."""
+    if case == "stride2":
+        fine, coarse, km, m = _strided_case(178)
+        n_fine, n_coarse = len(fine), len(coarse)
+    else:
+        coords = WL.random_coords(179, 3000, 3, -10, 10, batch=2)
+        c = _t(coords)
+        offs = regions.hypercube(3, 3)
+        km = gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, offs)
+        m = O.kernel_map(coords, coords, np.asarray(offs))
+        n_fine = n_coarse = len(coords)
+    maps_equal_exact(gpu_pairs(km), m)
+    n_x, n_y = (n_coarse, n_fine) if transpose else (n_fine, n_coarse)
+    maps = O.transposed_map(m) if transpose else m
+    X, Xb = WL.random_features(180, n_x, ci, dtype)
+    W, Wb = WL.random_weights(181, km.K, ci, co, dtype)
+    G, Gb = WL.random_features(182, n_y, co, dtype)
+    if dtype == "bf16":
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tX, tW, tG = dev(Xb), dev(Wb), dev(Gb)
+    else:
+        tX, tW, tG = _t(X, torch.float32), _t(W, torch.float32), _t(G, torch.float32)
+    _say(f"[gpu] bwd from the forward map: {dtype} {ci}->{co} {case} transpose={transpose}")
+    dX, dW = gsc.gsc_sparse_conv_bwd_fwdmap(tX, tW, tG, km, transpose=transpose)
+    torch.cuda.synchronize()
+    dXr, dWr = O.conv_backward(X, W, G, maps)
+    assert rel_err(to_np(dX), dXr) <= TOL[dtype]
+    assert rel_err(to_np(dW), dWr) <= TOL[dtype]
