@@ -381,6 +381,24 @@ int gsc_sparse_conv_fwd_affine(int32_t dtype, const void* X, int64_t n_in, int32
                                const int32_t* items, const float* scale, const float* shift, int32_t act,
                                void* Y, int64_t n_out, void* ws, size_t ws_bytes, void* stream);
 
+/* Backward of that epilogue (the chain rule of Y = act(S * scale + shift),
+ * per element): with dY the gradient of Y (n x c, the dtype of Y) and G =
+ * dY where the ReLU passed (Y > 0) or everywhere without it,
+ *   dZ = G * scale            (n x c, Y's dtype: the dY of gsc_sparse_conv_bwd),
+ *   dscale[c] = sum over rows of G * S,   dshift[c] = sum over rows of G
+ * (float32, each nullable), S recovered from Y as (Y - shift) / scale, so a
+ * channel with scale 0 gets a non-finite dscale (and a bf16 Y gives S to bf16
+ * precision).  For batch normalisation with its statistics held fixed:
+ * dgamma = (dscale - mean * dshift) / sqrt(var + eps), dbeta = dshift.
+ * Y, scale, shift, act as passed to gsc_sparse_conv_fwd_affine.  ws:
+ * gsc_affine_act_bwd_ws_bytes(n, c) bytes, needed only for the sums.  The
+ * sums are added in a fixed order (deterministic).  Asynchronous.  Errors:
+ * EINVAL, ESHORT (ws), EHIP. */
+size_t gsc_affine_act_bwd_ws_bytes(int64_t n, int32_t c);
+int gsc_affine_act_bwd(int32_t dtype, const void* Y, const void* dY, int64_t n, int32_t c, const float* scale,
+                       const float* shift, int32_t act, void* dZ, float* dscale, float* dshift, void* ws,
+                       size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* a6 / a7. Backward: dX and dW.                                             */
 /* ------------------------------------------------------------------------ */

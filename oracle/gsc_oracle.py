@@ -229,6 +229,21 @@ def affine_act(Y: np.ndarray, scale=None, shift=None, relu: bool = False) -> np.
     return np.maximum(Z, 0.0) if relu else Z
 
 
+def affine_act_backward(S: np.ndarray, dY: np.ndarray, scale=None, shift=None, relu: bool = False):
+    """Gradients of Y = affine_act(S, scale, shift, relu) (Sec. 4.5's
+    non-spatial functions, by the chain rule per element): with G = dY where
+    S * scale + shift > 0 (everywhere without the ReLU), returns dS = G * scale
+    and, per channel, dscale = sum over rows of G * S and dshift = sum of G."""
+    S = np.asarray(S, dtype=np.float64)
+    G = np.array(dY, dtype=np.float64)
+    C = S.shape[1]
+    sc = np.ones(C) if scale is None else np.asarray(scale, dtype=np.float64)
+    sh = np.zeros(C) if shift is None else np.asarray(shift, dtype=np.float64)
+    if relu:
+        G[S * sc[None, :] + sh[None, :] <= 0.0] = 0.0
+    return G * sc[None, :], (G * S).sum(axis=0), G.sum(axis=0)
+
+
 # --------------------------------------------------------------------------- #
 # Eq. 3 evaluated one output (or one input) row at a time, for sampled checks
 # at sizes where the full map is too slow in Python.

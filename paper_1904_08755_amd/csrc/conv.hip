@@ -727,6 +727,82 @@ int affine_act(int dtype, void* Y, int64_t n, int c, const Epilogue& ep, hipStre
     return GSC_OK;
 }
 
+// Backward of the epilogue y = act(z * scale + shift) (Sec. 4.5, the
+// non-spatial functions after a convolution; the chain rule per element):
+// g = dy where the ReLU passed (y > 0; everywhere without it), dz = g * scale,
+// and per channel dscale = sum over rows of g * z, dshift = sum of g, with z
+// recovered from y as (y - shift) / scale on the rows where g counts.  Rows
+// are split into kAbChunks chunks at most; a block sums its chunk per channel
+// (lane l of a channel takes rows l, l + L, ...; the L lanes are added in
+// lane order), the chunk sums go to part, and a second kernel adds them in
+// chunk order (so the sums are deterministic).
+constexpr int kAbThreads = 256;
+constexpr int64_t kAbChunks = 1024;
+
+static int64_t ab_chunks(int64_t n) {
+    const int64_t c = (n + 63) / 64;
+    return c < 1 ? 1 : (c > kAbChunks ? kAbChunks : c);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kAbThreads) k_affine_act_bwd(const T* __restrict__ y, const T* __restrict__ dy,
+                                                               int64_t n, int c, Epilogue ep, T* __restrict__ dz,
+                                                               float* __restrict__ part_s, float* __restrict__ part_t) {
+    __shared__ float ss[kAbThreads], st[kAbThreads];
+    const int64_t chunks = gridDim.x;
+    const int64_t r0 = n * blockIdx.x / chunks, r1 = n * (blockIdx.x + 1) / chunks;
+    const int L = c < kAbThreads ? kAbThreads / c : 1;   // lanes per channel
+    const int t = threadIdx.x;
+    for (int cb = 0; cb < c; cb += kAbThreads) {   // channels cb .. cb + (L > 1 ? c : 256) - 1
+        const int lane = t / (L > 1 ? c : kAbThreads);
+        const int ch = cb + t % (L > 1 ? c : kAbThreads);
+        float gs = 0.f, gt = 0.f;
+        if (lane < L && ch < c) {
+            const float sc = ep.scale ? ep.scale[ch] : 1.f;
+            const float sh = ep.shift ? ep.shift[ch] : 0.f;
+            for (int64_t r = r0 + lane; r < r1; r += L) {
+                const int64_t i = r * c + ch;
+                const float yv = to_f32(y[i]);
+                const float g = ep.relu && !(yv > 0.f) ? 0.f : to_f32(dy[i]);
+                store_out(&dz[i], g * sc);
+                if (part_s && g != 0.f) {
+                    gs += g * ((yv - sh) / sc);
+                    gt += g;
+                }
+            }
+        }
+        if (part_s) {
+            __syncthreads();   // the previous channel group's sums are read
+            ss[t] = gs;
+            st[t] = gt;
+            __syncthreads();
+            const int span = L > 1 ? c : kAbThreads;
+            if (t < span && cb + t < c) {
+                float a = 0.f, b = 0.f;
+                for (int l = 0; l < L; ++l) {
+                    a += ss[l * span + t];
+                    b += st[l * span + t];
+                }
+                part_s[(int64_t)blockIdx.x * c + cb + t] = a;
+                part_t[(int64_t)blockIdx.x * c + cb + t] = b;
+            }
+        }
+    }
+}
+
+__global__ void k_affine_act_bwd_sum(const float* __restrict__ part_s, const float* __restrict__ part_t,
+                                     int64_t chunks, int c, float* __restrict__ dscale, float* __restrict__ dshift) {
+    const int ch = blockIdx.x * blockDim.x + threadIdx.x;
+    if (ch >= c) return;
+    double a = 0.0, b = 0.0;
+    for (int64_t k = 0; k < chunks; ++k) {
+        a += part_s[k * c + ch];
+        b += part_t[k * c + ch];
+    }
+    if (dscale) dscale[ch] = (float)a;
+    if (dshift) dshift[ch] = (float)b;
+}
+
 }  // namespace gsc
 
 using namespace gsc;
@@ -1094,6 +1170,52 @@ int gsc_sparse_conv_bwd_fwdmap(int32_t dtype, const void* X, const void* W, cons
     return gsc_sparse_conv_bwd(dtype, X, W, dY, n_in, c_in, c_out, K, a, b, seg, cap_pairs, t_in, t_out, t_seg,
                                t_gidx, cap_pairs, ident.data(), perm, bmask, ibase, items, dX, dW, n_out, w + L.dw,
                                gsc_conv_bwd_ws_bytes(cap_pairs, c_in, c_out, K), stream);
+}
+
+size_t gsc_affine_act_bwd_ws_bytes(int64_t n, int32_t c) {
+    if (n < 0 || c < 1) return 0;
+    return 2 * al256((size_t)ab_chunks(n) * c * sizeof(float));
+}
+
+int gsc_affine_act_bwd(int32_t dtype, const void* Y, const void* dY, int64_t n, int32_t c, const float* scale,
+                       const float* shift, int32_t act, void* dZ, float* dscale, float* dshift, void* ws,
+                       size_t ws_bytes, void* stream) {
+    clear_error();
+    if (dtype != GSC_F32 && dtype != GSC_BF16) return fail(GSC_EINVAL, "affine_act_bwd: unknown dtype %d", dtype);
+    if (act != GSC_ACT_NONE && act != GSC_ACT_RELU) return fail(GSC_EINVAL, "affine_act_bwd: unknown act %d", act);
+    if (n < 0 || c < 1) return fail(GSC_EINVAL, "affine_act_bwd: bad sizes n=%lld c=%d", (long long)n, c);
+    if (n > 0 && (!Y || !dY || !dZ)) return fail(GSC_EINVAL, "affine_act_bwd: null Y/dY/dZ");
+    const bool sums = dscale || dshift;
+    if (sums) {
+        const size_t need = gsc_affine_act_bwd_ws_bytes(n, c);
+        if (!ws || ws_bytes < need)
+            return fail(GSC_ESHORT, "affine_act_bwd: ws needs %zu bytes, got %zu", need, ws ? ws_bytes : (size_t)0);
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    Epilogue ep;
+    ep.scale = scale;
+    ep.shift = shift;
+    ep.relu = act == GSC_ACT_RELU;
+    const int64_t chunks = ab_chunks(n);
+    float* part_s = sums ? reinterpret_cast<float*>(ws) : nullptr;
+    float* part_t = sums ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                                    al256((size_t)chunks * c * sizeof(float)))
+                         : nullptr;
+    if (dtype == GSC_BF16)
+        hipLaunchKernelGGL(k_affine_act_bwd<uint16_t>, dim3((unsigned)chunks), dim3(kAbThreads), 0, s,
+                           reinterpret_cast<const uint16_t*>(Y), reinterpret_cast<const uint16_t*>(dY), n, c, ep,
+                           reinterpret_cast<uint16_t*>(dZ), part_s, part_t);
+    else
+        hipLaunchKernelGGL(k_affine_act_bwd<float>, dim3((unsigned)chunks), dim3(kAbThreads), 0, s,
+                           reinterpret_cast<const float*>(Y), reinterpret_cast<const float*>(dY), n, c, ep,
+                           reinterpret_cast<float*>(dZ), part_s, part_t);
+    GSC_LAUNCH_CHECK();
+    if (sums) {
+        hipLaunchKernelGGL(k_affine_act_bwd_sum, dim3((unsigned)((c + 255) / 256)), dim3(256), 0, s, part_s, part_t,
+                           chunks, c, dscale, dshift);
+        GSC_LAUNCH_CHECK();
+    }
+    return GSC_OK;
 }
 
 }  // extern "C"

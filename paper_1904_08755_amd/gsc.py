@@ -59,6 +59,8 @@ _SIGS = {
                                               _vp, _vp, _vp]),
     "gsc_plan_blocks": (_i64, [_i64]),
     "gsc_plan_ranges": (_i32, [_i32]),
+    "gsc_affine_act_bwd_ws_bytes": (_sz, [_i64, _i32]),
+    "gsc_affine_act_bwd": (ctypes.c_int, [_i32, _vp, _vp, _i64, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gsc_kernel_map_transpose_ws_bytes": (_sz, [_i64, _i32]),
     "gsc_kernel_map_transpose": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
                                                 _vp]),
@@ -536,6 +538,30 @@ def gsc_sparse_conv_bwd_fwdmap(X: torch.Tensor, W: torch.Tensor, dY: torch.Tenso
         kmap.n_bound, 1 if transpose else 0, _ptr(dX) if need_dx else None, _ptr(dW) if need_dw else None, n_out,
         _ptr(ws), ws.numel(), _stream(stream)))
     return dX, dW
+
+
+def gsc_affine_act_bwd(Y: torch.Tensor, dY: torch.Tensor, scale: Optional[torch.Tensor] = None,
+                       shift: Optional[torch.Tensor] = None, relu: bool = False, need_sums: bool = True,
+                       stream=None):
+    """Backward of gsc_sparse_conv_fwd_affine's epilogue: (dZ, dscale, dshift),
+    dZ the gradient of the convolution's sums (Y's dtype), dscale and dshift
+    float32 per channel (None without ``need_sums``)."""
+    _need(Y, Y.dtype, "Y", 2)
+    _need(dY, Y.dtype, "dY", 2)
+    n, c = Y.shape
+    if dY.shape != Y.shape:
+        raise ValueError("dY must have Y's shape")
+    dev = Y.device
+    dZ = torch.empty_like(Y)
+    dsc = torch.empty(c, dtype=torch.float32, device=dev) if need_sums else None
+    dsh = torch.empty(c, dtype=torch.float32, device=dev) if need_sums else None
+    ws = _ws(lib().gsc_affine_act_bwd_ws_bytes(n, c), dev) if need_sums else None
+    _check(lib().gsc_affine_act_bwd(_dt(Y), _ptr(Y), _ptr(dY), n, c, None if scale is None else _ptr(scale),
+                                    None if shift is None else _ptr(shift), GSC_ACT_RELU if relu else GSC_ACT_NONE,
+                                    _ptr(dZ), None if dsc is None else _ptr(dsc), None if dsh is None else _ptr(dsh),
+                                    None if ws is None else _ptr(ws), 0 if ws is None else ws.numel(),
+                                    _stream(stream)))
+    return dZ, dsc, dsh
 
 
 # --------------------------------------------------------------------------- #

@@ -171,6 +171,18 @@ def test_map_transpose_and_fwdmap_validation(L):
     assert bwd(wsb=wb - 1) == gsc.GSC_ESHORT
 
 
+def test_affine_backward_validation(L):
+    fake = ctypes.c_void_p(0x1000)
+    need = L.gsc_affine_act_bwd_ws_bytes(1000, 32)
+    assert need > 0 and L.gsc_affine_act_bwd_ws_bytes(-1, 32) == 0
+    ab = lambda dt=0, act=1, ws=fake, wsb=need, dsc=fake: L.gsc_affine_act_bwd(
+        dt, fake, fake, 1000, 32, None, None, act, fake, dsc, None, ws, wsb, None)
+    assert ab(dt=7) == gsc.GSC_EINVAL
+    assert ab(act=5) == gsc.GSC_EINVAL
+    assert ab(wsb=need - 1) == gsc.GSC_ESHORT
+    assert ab(ws=None) == gsc.GSC_ESHORT
+
+
 def test_plan_validation(L):
     fake = ctypes.c_void_p(0x1000)
     ws = L.gsc_conv_plan_ws_bytes(100, 27)

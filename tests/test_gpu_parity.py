@@ -1060,3 +1060,61 @@ def test_conv_bwd_from_forward_map(dtype, ci, co, case, transpose):
     dXr, dWr = O.conv_backward(X, W, G, maps)
     assert rel_err(to_np(dX), dXr) <= TOL[dtype]
     assert rel_err(to_np(dW), dWr) <= TOL[dtype]
+
+
+# --------------------------------------------------------------------------- #
+# training through the fused epilogue (Sec. 4.5): its backward, then the conv's
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("dtype,ci,co,planned,relu", [
+    ("f32", 32, 32, True, True), ("f32", 16, 24, False, True), ("f32", 32, 32, True, False),
+    ("bf16", 256, 256, True, True), ("bf16", 64, 128, True, True), ("bf16", 48, 80, False, True)])
+def test_conv_bn_relu_backward(dtype, ci, co, planned, relu):
+    """conv -> batch normalisation -> ReLU in training: the fused forward,
+    gsc_affine_act_bwd (dZ, dscale, dshift), then gsc_sparse_conv_bwd on dZ,
+    against the oracle's chain rule.  The gradient is zero where the ReLU's
+    input lies within the kernels' rounding of 0 (float32 sums: 1e-3; a bf16
+    output, which the row form rounds before the affine map and again after
+    it: 0.1), so the oracle (float64) and the kernels need not take that
+    decision alike."""
+    coords = WL.random_coords(190 + ci + co, 2600, 3, -12, 12, batch=2)
+    offs = regions.hypercube(3, 3)
+    X, Xb = WL.random_features(191, len(coords), ci, dtype)
+    W, Wb = WL.random_weights(192, len(offs), ci, co, dtype)
+    m = O.kernel_map(coords, coords, np.asarray(offs))
+    S = O.conv_forward(X, W, m, len(coords))
+    rng = np.random.default_rng(193)
+    scale, shift = O.batchnorm_coefficients(S, rng.uniform(0.5, 2.0, co), rng.uniform(-0.5, 0.5, co))
+    scale, shift = scale.astype(np.float32), shift.astype(np.float32)
+    dY, dYb = WL.random_features(194, len(coords), co, dtype)
+    near = np.abs(S * scale.astype(np.float64) + shift.astype(np.float64)) < (1e-3 if dtype == "f32" else 0.1)
+    dY = np.where(near, 0.0, dY).astype(np.float32)
+    if dYb is not None:   # bf16 bits (f32 has none)
+        dYb = np.where(near, 0, dYb).astype(dYb.dtype)
+    if dtype == "bf16":
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to(DEV).view(torch.bfloat16)
+        tX, tW, tdY = dev(Xb), dev(Wb), dev(dYb)
+    else:
+        tX, tW, tdY = _t(X, torch.float32), _t(W, torch.float32), _t(dY, torch.float32)
+    c = _t(coords)
+    table = gsc.gsc_coords_build(c)
+    km = gsc.gsc_kernel_map(table, c, offs, dense=planned)
+    tm = gsc.transposed_kernel_map(table, c, offs, dense=planned)
+    if planned:
+        km, tm = gsc.gsc_conv_plan(km), gsc.gsc_conv_plan(tm)
+    _say(f"[gpu] conv-BN-ReLU backward {dtype} {ci}->{co} planned={planned} relu={relu}")
+    tsc, tsh = _t(scale, torch.float32), _t(shift, torch.float32)
+    Y = gsc.gsc_sparse_conv_fwd_affine(tX, tW, km, tsc, tsh, relu=relu)
+    dZ, dsc, dsh = gsc.gsc_affine_act_bwd(Y, tdY, tsc, tsh, relu=relu)
+    dX, dW = gsc.gsc_sparse_conv_bwd(tX, tW, dZ, km, tm, np.arange(len(offs)))
+    torch.cuda.synchronize()
+    dZr, dscr, dshr = O.affine_act_backward(S, dY, scale, shift, relu)
+    dXr, dWr = O.conv_backward(X, W, dZr, m)
+    tol = TOL[dtype]
+    assert rel_err(to_np(dZ), dZr) <= tol
+    assert rel_err(to_np(dsh), dshr) <= tol
+    assert rel_err(to_np(dsc), dscr) <= (tol if dtype == "f32" else 2 * tol)
+    assert rel_err(to_np(dX), dXr) <= tol
+    assert rel_err(to_np(dW), dWr) <= tol
+    # deterministic sums
+    _, dsc2, dsh2 = gsc.gsc_affine_act_bwd(Y, tdY, tsc, tsh, relu=relu)
+    assert torch.equal(dsc, dsc2) and torch.equal(dsh, dsh2)

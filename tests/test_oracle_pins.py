@@ -763,3 +763,36 @@ def test_batchnorm_relu_vs_torch():
     # a planted mistake: the unbiased variance (n - 1) misses torch's normalisation
     bad = (Y - Y.mean(0)) / np.sqrt(Y.var(axis=0, ddof=1) + eps) * gamma + beta
     assert not np.allclose(bad, ref, rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("relu", [True, False])
+def test_epilogue_backward_vs_torch_autograd(relu):
+    """The oracle's epilogue backward against torch autograd of batch_norm
+    with fixed statistics (eval mode, float64) and ReLU: dS is the input's
+    gradient, dshift the bias's, and the weight's follows as
+    (dscale - mean * dshift) / sqrt(var + eps)."""
+    rng = np.random.default_rng(12)
+    S = rng.standard_normal((400, 20)) * rng.uniform(0.5, 3.0, 20) + rng.uniform(-2, 2, 20)
+    dY = rng.standard_normal((400, 20))
+    gamma, beta, eps = rng.uniform(0.5, 2.0, 20), rng.uniform(-1, 1, 20), 1e-3
+    mean, var = rng.uniform(-1, 1, 20), rng.uniform(0.5, 4.0, 20)
+    tS = torch.from_numpy(S).requires_grad_()
+    tg = torch.from_numpy(gamma).requires_grad_()
+    tb = torch.from_numpy(beta).requires_grad_()
+    out = F.batch_norm(tS, torch.from_numpy(mean), torch.from_numpy(var), tg, tb, training=False, eps=eps)
+    if relu:
+        out = torch.relu(out)
+    out.backward(torch.from_numpy(dY))
+    sd = np.sqrt(var + eps)
+    scale, shift = gamma / sd, beta - mean * gamma / sd
+    dS, dscale, dshift = O.affine_act_backward(S, dY, scale, shift, relu)
+    assert np.allclose(dS, tS.grad.numpy(), rtol=1e-12, atol=1e-12)
+    assert np.allclose(dshift, tb.grad.numpy(), rtol=1e-12, atol=1e-10)
+    assert np.allclose((dscale - mean * dshift) / sd, tg.grad.numpy(), rtol=1e-10, atol=1e-10)
+    if relu:   # planted mistakes: the mask from S instead of the affine value, or no mask
+        bad = np.where(S > 0, dY, 0.0) * scale
+        assert not np.allclose(bad, tS.grad.numpy(), atol=1e-6)
+        assert not np.allclose(dY * scale, tS.grad.numpy(), atol=1e-6)
+    # no coefficients: the identity's gradient
+    dS0, dsc0, dsh0 = O.affine_act_backward(S, dY)
+    assert np.array_equal(dS0, dY) and np.allclose(dsh0, dY.sum(0)) and np.allclose(dsc0, (dY * S).sum(0))
