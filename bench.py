@@ -429,7 +429,10 @@ def bench_conv(args, wid: int, region=None, affine: bool = False, no_plan: bool 
                torch.from_numpy(rng.uniform(-0.5, 0.5, co).astype(np.float32)).cuda())
     torch.cuda.synchronize()
 
-    plan0 = pipeline.StepPlan(dw, use_plan=not no_plan, epilogue=epi)
+    # block plans or the row form: the faster of the two on this workload
+    use_plan = not no_plan and pipeline.choose_block_plans(dw, epi)
+    log(f"  block plans: {'yes' if use_plan else 'no'}" + ("" if no_plan else " (measured choice)"))
+    plan0 = pipeline.StepPlan(dw, use_plan=use_plan, epilogue=epi)
     for _ in range(warmup):
         plan0.run()
     gsc.gsc_table_status(plan0.table)   # the build of the warm-up passes succeeded
@@ -438,7 +441,7 @@ def bench_conv(args, wid: int, region=None, affine: bool = False, no_plan: bool 
     log(f"  warmup done ({warmup} steps)")
 
     steps_events = []
-    plan = pipeline.StepPlan(dw, use_plan=not no_plan, epilogue=epi)
+    plan = pipeline.StepPlan(dw, use_plan=use_plan, epilogue=epi)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):

@@ -71,12 +71,12 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-template <int CA, int CB, bool WT, bool EP>
+template <int CA, int CB, bool WT, bool EP, bool ACC>
 __global__ void __launch_bounds__((BlkF32<CA, CB>::THREADS))
 k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W, int K, WSel sel,
                const int32_t* __restrict__ perm, const uint32_t* __restrict__ bmask,
                const int64_t* __restrict__ ibase, const int32_t* __restrict__ items, int64_t nb, int64_t n_y,
-               Epilogue ep, int accum, float* __restrict__ Y) {
+               Epilogue ep, float* __restrict__ Y) {
     using C = BlkF32<CA, CB>;
     __shared__ float wl[kBlkLdsBytes / 4];
     // Weights in fragment order: lane (c, q) of offset k needs, for MFMA step
@@ -244,9 +244,9 @@ k_conv_blk_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict
                     const int64_t pos = (int64_t)mt[p].b * 16 + 4 * q + i;
                     if (pos < n_y && row >= 0 && row < n_y) {
                         float* yr = Y + (int64_t)row * CB + r16;
-                        float prev[C::NNB];
+                        float prev[C::NNB];   // the earlier offset ranges' sums (ACC)
 #pragma unroll
-                        for (int j = 0; j < C::NNB; ++j) prev[j] = accum ? yr[16 * j] : 0.f;
+                        for (int j = 0; j < C::NNB; ++j) prev[j] = ACC ? yr[16 * j] : 0.f;
 #pragma unroll
                         for (int j = 0; j < C::NNB; ++j) {
                             const float v = acc[j][i] + prev[j];
@@ -691,12 +691,17 @@ static int device_cus() {
 template <int CA, int CB, bool WT, bool EP>
 static void launch_blk_f32(const float* X, int64_t n_x, const float* W, const WSel& sel, int K, const BlockPlan& p,
                            int64_t nb, int64_t n_y, const Epilogue& ep, bool accum, float* Y, hipStream_t s) {
+    // (accum is a template argument: a run-time test would leave a wait for every load in flight at each store)
     using C = BlkF32<CA, CB>;
     int64_t grid = (nb + C::WAVES - 1) / C::WAVES;
     const int cus = device_cus();
     if (grid > cus) grid = cus;
-    hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT, EP>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X, n_x, W, K,
-                       sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, accum ? 1 : 0, Y);
+    if (accum)
+        hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT, EP, true>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X,
+                           n_x, W, K, sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, Y);
+    else
+        hipLaunchKernelGGL((k_conv_blk_f32<CA, CB, WT, EP, false>), dim3((unsigned)grid), dim3(C::THREADS), 0, s, X,
+                           n_x, W, K, sel, p.perm, p.bmask, p.ibase, p.items, nb, n_y, ep, Y);
 }
 
 int conv_blk_f32(int ca, int cb, const float* X, int64_t n_x, const float* W, bool wt, const WSel& sel, int K,

@@ -148,6 +148,10 @@ class StepPlan:
         else:
             raise ValueError(f"unsupported layer sequence {self.kinds}")
 
+    def planned(self) -> bool:
+        """Whether the passes build block plans (some block engine applies)."""
+        return bool(self.plan_maps if self.kinds == ["subm"] else (self.plan_kd or self.plan_td))
+
     def run(self, mark: Optional[Callable[[str], None]] = None, stream=None) -> StepResult:
         """Enqueue one pass.  ``mark(name)`` (optional) is called after each
         stage is enqueued: "map" (coordinates + kernel maps), "plan" (tile
@@ -208,6 +212,30 @@ class StepPlan:
                                           ws=self.ws_bwd1, stream=stream, host_wsel=self.host_ident)
         mark("bwd")
         return StepResult(out_coords, [kd, td], [Y1, Y2], dX, [dW1, dW2], [dY1])
+
+
+def choose_block_plans(dw: DeviceWorkload, epilogue=None, reps: int = 3, margin: float = 0.9) -> bool:
+    """Whether the passes over ``dw`` should build block plans: both ways are
+    run and timed on the device (``reps`` passes each after a warm-up pass),
+    and the row form is chosen only when its pass takes under ``margin`` times
+    the planned one (the block engines add in a fixed order, so they are
+    preferred when the two are close).  False without a block engine."""
+    sp = StepPlan(dw, True, epilogue)
+    if not sp.planned():
+        return False
+    times = {}
+    for mode, plan in ((True, sp), (False, StepPlan(dw, False, epilogue))):
+        plan.run()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            plan.run()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        times[mode] = sorted(ts)[len(ts) // 2]
+    return not times[False] < margin * times[True]
 
 
 def run_step(dw: DeviceWorkload, mark: Optional[Callable[[str], None]] = None, stream=None,

