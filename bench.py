@@ -91,7 +91,7 @@ def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool, epi
             if K <= 30:   # the tile engine (16 blocks by all output columns per workgroup)
                 return f"k_conv_tile_bf16<{ci}, {co}, gsc::WIdentity, {ep}>"
             return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity, {ep}>"
-        return f"k_conv_blk_f32<{ci}, {co}, false, {ep}>"
+        return f"k_conv_blk_f32<{ci}, {co}, false, {ep}, false>"
     if dtype == "bf16":
         if ci in (128, 256) and co in (128, 256):
             return f"k_conv_bf16_dma<{ci}, {co}, gsc::WIdentity>"
@@ -402,7 +402,7 @@ def conv_pass_bytes(pairs, layers, n_ins, n_outs, s):
     return tot
 
 
-def bench_conv(args, wid: int, region=None, affine: bool = False, no_plan: bool = False,
+def bench_conv(args, wid: int, region=None, affine: bool = False, plan_mode: str = "auto",
                steps: int = None, warmup: int = None) -> dict:
     """Time ``steps`` whole passes of workload ``wid`` (after ``warmup``
     untimed ones) and return its results: per-step time, voxels/s, stage
@@ -430,8 +430,8 @@ def bench_conv(args, wid: int, region=None, affine: bool = False, no_plan: bool 
     torch.cuda.synchronize()
 
     # block plans or the row form: the faster of the two on this workload
-    use_plan = not no_plan and pipeline.choose_block_plans(dw, epi)
-    log(f"  block plans: {'yes' if use_plan else 'no'}" + ("" if no_plan else " (measured choice)"))
+    use_plan = plan_mode == "yes" or (plan_mode == "auto" and pipeline.choose_block_plans(dw, epi))
+    log(f"  block plans: {'yes' if use_plan else 'no'}" + (" (measured choice)" if plan_mode == "auto" else ""))
     plan0 = pipeline.StepPlan(dw, use_plan=use_plan, epilogue=epi)
     for _ in range(warmup):
         plan0.run()
@@ -547,7 +547,10 @@ def main():
                     help="forward with batch normalisation (per-channel affine form) and ReLU fused into the "
                          "convolution's output write (Sec. 4.5); single-layer workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-plan", action="store_true", help="convolve on the kernel maps in row form (no block plan)")
+    ap.add_argument("--plan", choices=["auto", "yes", "no"], default="auto",
+                    help="block plans: the faster of plans and row form timed on the workload (auto), or always/never "
+                         "(a profiler's per-launch overhead can change what auto measures)")
+    ap.add_argument("--no-plan", action="store_true", help="the same as --plan no")
     ap.add_argument("--pool", choices=["max", "avg", "sum"], default=None,
                     help="time pooling instead (Sec. 4.3, 4.4): the 2^3 stride-2 window over the scene of workload 1")
     ap.add_argument("--unpool", action="store_true",
@@ -585,16 +588,17 @@ def main():
         print("--affine applies to one of the single-layer workloads (--workload 0, 1, 3 or 4)", file=sys.stderr)
         sys.exit(2)
 
+    plan_mode = "no" if args.no_plan else args.plan
     others = {}
     if args.workload is None:   # every workload; the headline is workload 4
         for wid in (0, 1, 2, 3):
-            r = bench_conv(args, wid, no_plan=args.no_plan)
+            r = bench_conv(args, wid, plan_mode=plan_mode)
             r.pop("_wl")
             others[r.pop("workload")] = r
         head_id = 4
     else:
         head_id = args.workload
-    head = bench_conv(args, head_id, region=args.region, affine=args.affine, no_plan=args.no_plan)
+    head = bench_conv(args, head_id, region=args.region, affine=args.affine, plan_mode=plan_mode)
     wl = head.pop("_wl")
     roof = head.pop("roofline")
 
