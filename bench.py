@@ -3,7 +3,8 @@
 
 One step = one pass of the whole hot path over a workload, inputs already
 resident in HBM: coordinate hash table, output coordinates (strided layers),
-kernel maps, block plans, convolution forward, input gradient and weight
+kernel maps, block plans (where they pay: a pass with and one without are
+timed first, ``--plan auto``), convolution forward, input gradient and weight
 gradient.
 
     python bench.py [--steps K] [--warmup W]            # all five workloads
