@@ -589,6 +589,36 @@ def test_stride_coords_floor_and_order():
     assert np.array_equal(gpu_pairs(km)[0][0], np.arange(len(got)))
 
 
+@pytest.mark.parametrize("lead", [0, 3, 61, 250])
+def test_stride_order_with_runs_across_lanes(lead):
+    """Strided output coordinates from rows whose equal strided keys come in
+    runs (the 8 fine voxels of each coarse cell consecutively, as sorted
+    scene rows give them), shifted by ``lead`` singleton rows so that runs
+    cross the 64-lane and 256-thread boundaries: the output keeps the order of
+    each key's first input row exactly, and every input row's stride-2 map
+    pair points at its own cell."""
+    rng = np.random.default_rng(186 + lead)
+    cells = np.unique(rng.integers(-20, 20, size=(700, 3)), axis=0) * 2   # coarse cells
+    rng.shuffle(cells)
+    fine = (cells[:, None, :] + regions.hypercube(2, 3)[None, :, :]).reshape(-1, 3)
+    singles = np.stack([np.full(lead, 101), np.arange(lead) * 2, np.zeros(lead)], axis=1) if lead else np.zeros((0, 3))
+    xyz = np.concatenate([singles, fine]).astype(np.int32)
+    coords = np.concatenate([np.zeros((len(xyz), 1), np.int32), xyz], axis=1)
+    out, out_table = gsc.gsc_coords_stride(_t(coords), 2)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    first = {}
+    for r, row in enumerate(coords.tolist()):
+        key = (row[0],) + tuple((v // 2) * 2 for v in row[1:])
+        first.setdefault(key, r)
+    order = sorted(first, key=first.get)
+    assert got.tolist() == [list(k) for k in order]
+    # every fine row pairs with the cell it lies in
+    km = gsc.gsc_kernel_map(gsc.gsc_coords_build(_t(coords)), out, regions.hypercube(2, 3))
+    ref = O.kernel_map(coords, got, O.hypercube(2, 3))
+    maps_equal_exact(gpu_pairs(km), ref)
+
+
 def test_stride_then_second_level():
     coords = WL.random_coords(82, 6000, 3, -17, 17, batch=2)
     c = _t(coords)
