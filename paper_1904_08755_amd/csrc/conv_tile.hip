@@ -23,8 +23,8 @@
 // and, for each block having k, multiplies the block's 16 x 32 rows by the
 // 32 x 64 weights (four MFMAs per block).  Every output row's products are
 // added in increasing offset order, so the result does not depend on the
-// plan's row order and is bit-reproducible.  The sums are written once,
-// through LDS, as whole bf16 rows.
+// plan's row order and is bit-reproducible.  The sums are written once, as
+// bf16, straight from the registers.
 //
 // The grid is persistent (one workgroup per CU) and takes tiles from the
 // last to the first through a counter in device memory: tiles later in the
@@ -187,7 +187,7 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
         }
         const int n_items = (int)(ibase[b0 + nbt] - ib0);
         // the previous tile's last reads of the LDS (item table, output
-        // rows, output staging, next tile) are done before they are overwritten
+        // rows, next tile) are done before they are overwritten
         tile_barrier();
         if (tid == 0) next_s = take(blockIdx.x + round * (int64_t)gridDim.x);
         {   // the tile's items (at most 16 K x 16 ints): 16-byte loads, all in flight before any store
@@ -225,9 +225,7 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                     iblw[j] = ibl[b];
                 }
         }
-        // the blocks whose sums this wave keeps: wr, wr + WR, wr + 2 WR, ...
-        // (interleaved, so that the waves of a column range see blocks from
-        // all of the tile's mask classes and take similar numbers of products)
+        // the blocks whose sums this wave keeps: BPW wr .. BPW wr + BPW - 1
         uint32_t bmv[C::BPW];
 #pragma unroll
         for (int b = 0; b < C::BPW; ++b) {
@@ -404,16 +402,12 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
             tile_barrier();
         }
 
-        // Write the tile through LDS, 64 positions per pass (rows 0-31 in
-        // stage array sa0, 32-63 in sa1): the sums become bf16 pairs (lane
-        // (c, q) holds rows 4q .. 4q+3 of column c; after an exchange with
-        // lane c ^ 1 an even lane holds rows 4q, 4q+1 of columns c, c+1 and an
-        // odd one rows 4q+2, 4q+3 of columns c-1, c), then whole output rows
-        // go out 16 bytes per lane.
-        constexpr int RB = CB * 2;                        // bytes per output row
-        constexpr int LPR = RB / 16;                      // lanes per output row
-        constexpr int RPI = kTileThreads / LPR;           // rows per copy iteration
-        static_assert(32 * RB <= kTileStageBytes, "32 output rows fit a stage array");
+        // Write the tile straight from registers: the sums become bf16 pairs
+        // (lane (c, q) holds rows 4q .. 4q+3 of column c; after an exchange
+        // with lane c ^ 1 an even lane holds rows 4q, 4q+1 of columns c, c+1
+        // and an odd one rows 4q+2, 4q+3 of columns c-1, c), one 4-byte store
+        // per lane, row and column block (measured as fast as staging whole
+        // rows through LDS, and it needs no barrier).
         const bool odd = r16 & 1;
         float esc[C::NJ], esh[C::NJ];
 #pragma unroll
@@ -423,42 +417,24 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
             esh[j] = EP && ep.shift ? ep.shift[col] : 0.f;
         }
 #pragma unroll
-        for (int pass = 0; pass < kTileBlocks / 4; ++pass) {
-            if (pass) tile_barrier();   // the previous pass has been copied out
+        for (int b = 0; b < C::BPW; ++b) {
+            const int blk = C::BPW * wr + b;
+            const int pos = 16 * blk + 4 * q + (odd ? 2 : 0);
+            const int32_t row0 = perm_s[pos], row1 = perm_s[pos + 1];
 #pragma unroll
-            for (int b = 0; b < C::BPW; ++b) {
-                const int blk = C::BPW * wr + b;
-                if (blk / 4 != pass) continue;   // blocks 4 pass .. 4 pass + 3
-                uint8_t* outb = (blk & 2) ? sa1 : sa0;   // rows 32 .. 63 of the pass in sa1
+            for (int j = 0; j < C::NJ; ++j) {
+                floatx4 v = acc[b][j];
+                if constexpr (EP) {
 #pragma unroll
-                for (int j = 0; j < C::NJ; ++j) {
-                    floatx4 v = acc[b][j];
-                    if constexpr (EP) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) v[i] = epi_apply(v[i], esc[j], esh[j], ep.relu);
-                    }
-                    const float e0 = tile_xor1(odd ? v[0] : v[2]);
-                    const float e1 = tile_xor1(odd ? v[1] : v[3]);
-                    const uint32_t p0 = odd ? tile_pack_bf16(e0, v[2]) : tile_pack_bf16(v[0], e0);
-                    const uint32_t p1 = odd ? tile_pack_bf16(e1, v[3]) : tile_pack_bf16(v[1], e1);
-                    const int row = 16 * (blk & 1) + 4 * q + (odd ? 2 : 0);   // 0 .. 31 within the array
-                    const int cb = (64 * wc + 16 * j + (r16 & ~1)) * 2;      // byte of the column pair
-                    *reinterpret_cast<uint32_t*>(outb + row * RB + cb) = p0;
-                    *reinterpret_cast<uint32_t*>(outb + (row + 1) * RB + cb) = p1;
+                    for (int i = 0; i < 4; ++i) v[i] = epi_apply(v[i], esc[j], esh[j], ep.relu);
                 }
-            }
-            tile_barrier();   // the pass is staged
-#pragma unroll
-            for (int r0 = 0; r0 < 64; r0 += RPI) {
-                const int pos = r0 + tid / LPR;
-                if (pos < 64) {
-                    const int32_t row = perm_s[64 * pass + pos];
-                    if (row >= 0 && row < n_y) {
-                        const uint8_t* src = (pos & 32) ? sa1 : sa0;
-                        const tu32x4 val = *reinterpret_cast<const tu32x4*>(src + (pos & 31) * RB + (tid % LPR) * 16);
-                        *reinterpret_cast<tu32x4*>(Y + (int64_t)row * CB + (tid % LPR) * 8) = val;
-                    }
-                }
+                const float e0 = tile_xor1(odd ? v[0] : v[2]);
+                const float e1 = tile_xor1(odd ? v[1] : v[3]);
+                const uint32_t p0 = odd ? tile_pack_bf16(e0, v[2]) : tile_pack_bf16(v[0], e0);
+                const uint32_t p1 = odd ? tile_pack_bf16(e1, v[3]) : tile_pack_bf16(v[1], e1);
+                const int col = 64 * wc + 16 * j + (r16 & ~1);
+                if (row0 >= 0 && row0 < n_y) *reinterpret_cast<uint32_t*>(Y + (int64_t)row0 * CB + col) = p0;
+                if (row1 >= 0 && row1 < n_y) *reinterpret_cast<uint32_t*>(Y + (int64_t)row1 * CB + col) = p1;
             }
         }
         tile = uniform(next_s);   // written before the item staging's barrier
