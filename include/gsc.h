@@ -261,15 +261,20 @@ int gsc_kernel_map_transpose_status(const void* ws, void* stream);
  * pair) and multiply them by the offset's weight matrix, keeping the block's
  * sums in registers; so a block costs one product per distinct offset of its
  * rows.  The plan orders the output rows by neighbour mask (bit k set when
- * the row has a pair at offset k), so rows with equal masks share blocks.
+ * the row has a pair at offset k), so rows with equal masks share blocks;
+ * the sort key puts the mask's popcount (capped) above the mask, so rows
+ * with fewer neighbours come first and runs of blocks share offsets too.
  *
  * Input: the dense form of a kernel map over n_out output rows with K <= 32
  * offsets, nbr[k * n_out + j] = input row paired with output row j at offset
  * k or -1 (as gsc_kernel_map writes it).  Output (device, caller-allocated),
  * with
  * nb = gsc_plan_blocks(n_out) = ceil(n_out / 16):
- *   perm[n_out]       perm[i] = the output row at position i (a stable sort
- *                     of the rows by mask);
+ *   perm[n_out]       perm[i] = the output row at position i: a stable sort
+ *                     of the rows by key = (min(popcount(mask), cap) << K)
+ *                     | mask, cap = 2^p - 1, p = min(10 ceil(K / 10) - K,
+ *                     32 - K, 6) (the bits the sort's last 10-bit digit
+ *                     leaves free; K = 27: counts capped at 7);
  *   bmask[nb]         bmask[b] = OR of the masks of positions 16b..16b+15;
  *   ibase[nb + 1]     exclusive scan of popcount(bmask); ibase[nb] = items;
  *   items[16 * cap_items]  item t = ibase[b] + j belongs to block b and the

@@ -157,58 +157,79 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
         return p == 0 ? sb0 : (p == 1 ? sb1 : (p == 2 ? sb2 : sb3));
     };
 
-    // tile sequence: from the counter (taken one tile ahead), else static
-    auto take = [&](int64_t i) -> int64_t {
-        const int64_t t = counter ? (int64_t)atomicAdd(counter, 1u) : i;
-        return t < ntiles ? ntiles - 1 - t : -1;
-    };
+    // tile sequence: from the counter (taken one tile ahead), else static;
+    // tile t of the sequence is plan tile ntiles - 1 - t
+    auto tile_of = [&](int64_t t) -> int64_t { return t < ntiles ? ntiles - 1 - t : -1; };
     auto uniform = [](int64_t v) {   // a value every lane holds, as a scalar
         const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
         const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
         return (int64_t)(((uint64_t)hi << 32) | lo);
     };
-    if (tid == 0) next_s = take(blockIdx.x);
+    if (tid == 0) next_s = tile_of(counter ? (int64_t)atomicAdd(counter, 1u) : (int64_t)blockIdx.x);
     __syncthreads();
     int64_t tile = uniform(next_s);
     for (int64_t round = 1; tile >= 0; ++round) {
         const int64_t b0 = tile * kTileBlocks;
         const int nbt = (int)min((int64_t)kTileBlocks, nb - b0);
 
-        // the tile's blocks (wave-uniform)
+        // The tile's blocks (wave-uniform): lane b < nbt loads bmask[b0 + b]
+        // and lane b <= nbt ibase[b0 + b] (one round trip for all of them),
+        // then each value is read out of its lane.
+        const uint32_t bm_l = lane < nbt ? bmask[b0 + lane] : 0u;
+        const int64_t ib_l = lane <= nbt ? ibase[b0 + lane] : 0;
+        const int64_t ib0 = uniform(ib_l);
+        const uint32_t ib0_lo = (uint32_t)ib0;
         uint32_t bm[kTileBlocks];
         int32_t ibl[kTileBlocks];
-        const int64_t ib0 = ibase[b0];
         uint32_t U = 0;
 #pragma unroll
         for (int b = 0; b < kTileBlocks; ++b) {
-            bm[b] = b < nbt ? bmask[b0 + b] : 0u;
-            ibl[b] = b < nbt ? (int32_t)(ibase[b0 + b] - ib0) : 0;
+            bm[b] = (uint32_t)__builtin_amdgcn_readlane((int)bm_l, b);   // 0 past the tile's blocks
+            ibl[b] = b < nbt ? (int32_t)((uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ib_l, b) - ib0_lo) : 0;
             U |= bm[b];
         }
-        const int n_items = (int)(ibase[b0 + nbt] - ib0);
+        // a tile holds at most 16 K items: the difference fits in 32 bits
+        const int n_items = (int)((uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ib_l, nbt) - ib0_lo);
         // the previous tile's last reads of the LDS (item table, output
         // rows, next tile) are done before they are overwritten
         tile_barrier();
-        if (tid == 0) next_s = take(blockIdx.x + round * (int64_t)gridDim.x);
-        {   // the tile's items (at most 16 K x 16 ints): 16-byte loads, all in flight before any store
+        // The next tile from the counter: the atomic is issued here and its
+        // result is first used after the loads below have returned, so the
+        // two round trips overlap.  (The address is laundered through an
+        // empty asm so that the compiler does not turn the single-lane atomic
+        // into a wave reduction that waits for the result on the spot.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Wsometimes-uninitialized"
+        unsigned t_raw;   // defined, and used, by thread 0 only (no merge with another value to copy it into)
+        if (tid == 0 && counter) {
+            __attribute__((address_space(1))) unsigned* c = (__attribute__((address_space(1))) unsigned*)counter;
+            asm volatile("" : "+v"(c));
+            t_raw = __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        {   // the tile's items (at most 16 K x 16 ints, 16-byte loads) and
+            // output rows: all loads in flight before any store
             constexpr int kPer = (kTileBlocks * kTileMaxK * 4 + kTileThreads - 1) / kTileThreads;
             const tu32x4* src = reinterpret_cast<const tu32x4*>(items + ib0 * 16);
             const int last = n_items * 4 - 1;
+            const int64_t pos = b0 * kPlanBlockRows + tid;
+            int32_t prow = tid < kTilePos && pos < n_y ? perm[pos] : -1;
+            tu32x4 v[kPer] = {};
             if (last >= 0) {
-                tu32x4 v[kPer];
 #pragma unroll
                 for (int u = 0; u < kPer; ++u) v[u] = src[min(tid + u * kTileThreads, last)];
+            }
 #pragma unroll
-                for (int u = 0; u < kPer; ++u) asm volatile("" : "+v"(v[u]));   // all loads issued before any store
+            for (int u = 0; u < kPer; ++u) asm volatile("" : "+v"(v[u]));
+            asm volatile("" : "+v"(prow));
+            if (last >= 0) {
 #pragma unroll
                 for (int u = 0; u < kPer; ++u)
                     if (tid + u * kTileThreads <= last) reinterpret_cast<tu32x4*>(idx_s)[tid + u * kTileThreads] = v[u];
             }
+            if (tid < kTilePos) perm_s[tid] = prow;
         }
-        if (tid < kTilePos) {
-            const int64_t pos = b0 * kPlanBlockRows + tid;
-            perm_s[tid] = pos < n_y ? perm[pos] : -1;
-        }
+        if (tid == 0) next_s = tile_of(counter ? (int64_t)t_raw : blockIdx.x + round * (int64_t)gridDim.x);
+#pragma clang diagnostic pop
         __syncthreads();   // items and output rows staged
 
         // the blocks whose rows this wave copies: wave and wave + 8
@@ -338,10 +359,13 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
 #pragma unroll
                 for (int c = 0; c < C::NJ; ++c)
                     bfr[(j + 1) & 1][c] = *reinterpret_cast<const tu32x4*>(sbn + (64 * wc + 16 * c) * 64 + frag);
-                const uint32_t bk = dc[j / H].bk;
+                // fresh scalar copies: one bit test and branch per block
+                uint32_t bk = dc[j / H].bk;
+                asm volatile("" : "+s"(bk));
                 // the next step has this step's offset: one test per block
                 constexpr bool same = j + 1 < L && (j + 1) % H != 0;
-                const uint32_t bn = j + 1 < L ? dc[((j + 1) % L) / H].bk : dn[0].bk;
+                uint32_t bn = j + 1 < L ? dc[((j + 1) % L) / H].bk : dn[0].bk;
+                asm volatile("" : "+s"(bn));
 #pragma unroll
                 for (int b = 0; b < C::BPW; ++b) {
                     if (b == C::BPW / 2) {

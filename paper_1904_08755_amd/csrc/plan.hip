@@ -9,7 +9,12 @@
 // offsets occur; the plan orders the output rows by neighbour mask (bit k set
 // when the row has a pair at offset k), so rows with the same neighbourhood
 // shape share blocks, and the blocks' offset sets shrink to about those of
-// single rows.
+// single rows.  The sort key puts the mask's popcount, capped to the bits
+// that the last 10-bit digit leaves free, above the mask: rows are grouped
+// by neighbour count first, so a run of blocks (the tile engine's tile of
+// 16) also has fewer distinct offsets, and the plan's positions come in
+// rough order of cost (which the tile engine uses to hand out its largest
+// tiles first).
 //
 // Output, for n_out rows, nb = ceil(n_out / 16) blocks:
 //   perm[i]      output row at position i (i < n_out);
@@ -22,12 +27,14 @@
 // Input: the map's dense form nbr[k][j] (input row or -1), which the kernel
 // map writes as it probes.  Steps:
 //   masks:  every row's mask from its column of nbr;
-//   sort:   stable LSD radix sort of (mask, row) by mask, 10-bit digits, one
-//           kernel per digit;
+//   sort:   stable LSD radix sort of (key, row) by key = (min(popcount of
+//           the mask, cap) << K) | mask, 10-bit digits, one kernel per digit
+//           (cap: plan_key_cap);
 //   count:  block unions and item counts; a scan gives ibase;
 //   fill:   one lane per position writes its entry of each of its block's
 //           items.
 // Everything is deterministic and runs without a host round trip.
+#include <algorithm>
 #include <climits>
 #include <cstdlib>
 
@@ -50,8 +57,9 @@ static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 // (Also clears the sort's counters and first look-back entries, zero[0, nzero),
 // which the histogram kernel after it starts to fill.)
 __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int K,
-                                                             uint32_t* __restrict__ keys, uint32_t* __restrict__ zero,
-                                                             int64_t nzero, uint32_t* __restrict__ lb_status) {
+                                                             uint32_t cap, uint32_t* __restrict__ keys,
+                                                             uint32_t* __restrict__ zero, int64_t nzero,
+                                                             uint32_t* __restrict__ lb_status) {
     if (lb_status && blockIdx.x == 0 && threadIdx.x == 0) *lb_status = 0u;   // the plan call's first kernel
     for (int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x; i < nzero;
          i += (int64_t)gridDim.x * kPlanThreads)
@@ -67,7 +75,8 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __re
 #pragma unroll
         for (int b = 0; b < B; ++b) m |= (uint32_t)(r[b] >= 0) << ((k0 + b) & 31);
     }
-    keys[j] = m;
+    const uint32_t c = min((uint32_t)__popc(m), cap);
+    keys[j] = cap ? m | (c << K) : m;   // cap > 0 only where K + its bits <= 32
 }
 
 // ---------------------------------------------------------------------------
@@ -318,6 +327,15 @@ __global__ void k_plan_empty(int64_t* ibase, uint32_t* lb_status) {
     }
 }
 
+// The popcount field of the sort key: as many bits as the last 10-bit digit
+// of the K-bit mask leaves free (at most 6, and within a 32-bit key); its
+// largest value, 0 when there is no room.  K = 27: 3 bits, counts capped at 7.
+static int plan_key_pbits(int K) {
+    const int spare = (K + kRsBits - 1) / kRsBits * kRsBits - K;
+    return std::min(std::min(spare, 32 - K), 6);
+}
+static uint32_t plan_key_cap(int K) { return (1u << plan_key_pbits(K)) - 1u; }
+
 // lb_status: the plan call's look-back status word, cleared here when
 // clear_status (the call's first range) and set by a pass that gave up.
 static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
@@ -325,7 +343,7 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
                         hipStream_t s) {
     const int64_t nb = (n + 15) / 16;
     const int64_t nrs = (n + kRsTile - 1) / kRsTile;
-    const int passes = (K + kRsBits - 1) / kRsBits;
+    const int passes = (K + plan_key_pbits(K) + kRsBits - 1) / kRsBits;   // as many as for the mask alone
     char* w = reinterpret_cast<char*>(ws);
     uint32_t* ka = reinterpret_cast<uint32_t*>(w);
     w += al256((size_t)n * sizeof(uint32_t));
@@ -357,8 +375,8 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
     }
     const uint32_t kmask = K >= 32 ? ~0u : (1u << K) - 1u;
     const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
-    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, ka, ghist, nzero,
-                       lb_clear);
+    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, plan_key_cap(K), ka,
+                       ghist, nzero, lb_clear);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
     GSC_LAUNCH_CHECK();

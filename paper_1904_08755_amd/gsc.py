@@ -357,7 +357,7 @@ class PlanBuffers:
 
 
 def gsc_conv_plan(kmap: KernelMap, bufs: Optional[PlanBuffers] = None, stream=None) -> KernelMap:
-    """The map with its block plan attached (rows ordered by neighbour mask,
+    """The map with its block plan attached (rows ordered by neighbour count and mask,
     16-row blocks, per-block items of 16 input rows)."""
     n_out, K = kmap.n_out, kmap.K
     if kmap.nbr is None:

@@ -12,7 +12,7 @@ to learn how many output coordinates it has.
 
 Block plans: with ``use_plan`` (the default) every map that a block engine
 can use (gsc_conv_block_engine) gets its block plan (gsc_conv_plan): output
-rows ordered by neighbour mask, 16-row blocks with their per-offset items.
+rows ordered by neighbour count and mask, 16-row blocks with their per-offset items.
 The forward and input-gradient passes then run on the plan; the weight
 gradients always use the maps in row form.
 

@@ -304,7 +304,8 @@ def test_bf16_wide_channel_engine(ci, co, region):
 
 
 def _check_plan(km):
-    """The block plan of a map: rows stably sorted by neighbour mask, 16-row
+    """The block plan of a map: rows stably sorted by neighbour count (capped
+    to the spare bits of the sort's last 10-bit digit), then mask, 16-row
     blocks with their union masks and item bases, and each item holding the
     input rows of its block's positions at its offset (-1 where none).  A map
     with more than 32 offsets has one such plan per range of consecutive
@@ -337,10 +338,14 @@ def _check_plan_range(n, nbr, perm, bm, ib, items):
     mask = np.zeros(max(n, 1), np.int64)
     for k in range(K):
         mask |= (nbr[:, k] >= 0).astype(np.int64) << np.int64(k)
+    pbits = min(-(-K // 10) * 10 - K, 32 - K, 6)                      # popcount field of the key
+    cnt_rows = np.array([bin(int(x)).count("1") for x in mask], np.int64)
+    key = (np.minimum(cnt_rows, (1 << pbits) - 1) << np.int64(K)) | mask
+    ks = key[perm]
+    assert np.all(ks[1:] >= ks[:-1])                                   # sorted by key
+    same = ks[1:] == ks[:-1]
+    assert np.all(perm[1:][same] > perm[:-1][same])                    # stable: row order within a key
     ms = mask[perm]
-    assert np.all(ms[1:] >= ms[:-1])                                   # sorted by mask
-    same = ms[1:] == ms[:-1]
-    assert np.all(perm[1:][same] > perm[:-1][same])                    # stable: row order within a mask
     msp = np.zeros(nb * 16, np.int64)
     msp[:n] = ms
     assert np.array_equal(bm, np.bitwise_or.reduce(msp.reshape(nb, 16), axis=1) if nb else bm)
