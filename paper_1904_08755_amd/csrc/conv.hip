@@ -370,10 +370,14 @@ k_conv_f32(const float* __restrict__ X, int64_t n_x, const float* __restrict__ W
 // ibase[K] = total.  Equal chunks keep the work items balanced whatever the
 // offsets' sizes (the centre offset of a submanifold map has one pair per
 // row, the others far fewer).
-__global__ void k_dw_items(const int64_t* seg, int K, int64_t ch, int64_t* ibase, int64_t* chunk) {
+// counter (nullable) is set to 0 on the way (the input gradient's tile
+// counter, when that pass runs after this kernel).
+__global__ void k_dw_items(const int64_t* seg, int K, int64_t ch, int64_t* ibase, int64_t* chunk,
+                           unsigned* counter) {
     // one wave: 64 offsets per round, their item counts scanned with shuffles
     if (blockIdx.x != 0 || threadIdx.x >= 64) return;
     const int lane = threadIdx.x;
+    if (counter && lane == 0) *counter = 0u;
     int64_t carry = 0;
     for (int k0 = 0; k0 < K; k0 += 64) {
         const int k = k0 + lane;
@@ -606,35 +610,40 @@ k_dw_f32(const float* __restrict__ X, int64_t n_in, const float* __restrict__ dY
     dw_store_partial<CI, CO>(sh, d, NA, NB, wave, q, r16, CI, CO, part + item * CI * (int64_t)CO, CO);
 }
 
-// dW[k] = sum of offset k's partials in a fixed order.  A block covers 64
-// elements of one offset; wave w adds partials w, w + 4, w + 8, ... with
-// eight loads in flight, and the four wave sums are combined in wave order.
+// dW[k] = sum of offset k's partials in a fixed order.  A block covers 64 V
+// elements of one offset (V = 4: a 16-byte load per lane, for wide layers
+// with ci * co a multiple of 4 and dW 16-byte aligned); wave w adds partials w, w + 4, w + 8,
+// ... with eight loads in flight, and the four wave sums are combined in wave
+// order.
+template <int V>
 __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict__ part, const int64_t* __restrict__ ibase,
                                                         int ci, int co, float* __restrict__ dW) {
-    __shared__ float sh[4][64];
+    typedef float vec __attribute__((ext_vector_type(V)));
+    __shared__ vec sh[4][64];
     const int k = blockIdx.y;
     const int64_t cc = (int64_t)ci * co;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t e = (int64_t)blockIdx.x * 64 + lane;
-    const int64_t i0 = ibase[k], i1 = ibase[k + 1];
+    const int64_t e = ((int64_t)blockIdx.x * 64 + lane) * V;
     const int64_t ee = e < cc ? e : 0;
-    float acc8[8];
+    const int64_t i0 = ibase[k], i1 = ibase[k + 1];
+    vec acc8[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc8[u] = 0.f;
+    for (int u = 0; u < 8; ++u) acc8[u] = vec(0.f);
     for (int64_t it = i0 + wave; it < i1; it += 32) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int64_t i = it + 4 * u;
-            const float v = part[(i < i1 ? i : i0) * cc + ee];
-            acc8[u] += i < i1 ? v : 0.f;
+            const vec v = *reinterpret_cast<const vec*>(part + (i < i1 ? i : i0) * cc + ee);
+            acc8[u] += i < i1 ? v : vec(0.f);   // a select, not a branch: all eight loads stay in flight
         }
     }
-    float v = 0.f;
+    vec v = vec(0.f);
 #pragma unroll
     for (int u = 0; u < 8; ++u) v += acc8[u];
     sh[wave][lane] = v;
     __syncthreads();
-    if (wave == 0 && e < cc) dW[(int64_t)k * cc + e] = ((sh[0][lane] + sh[1][lane]) + sh[2][lane]) + sh[3][lane];
+    if (wave == 0 && e < cc)
+        *reinterpret_cast<vec*>(dW + (int64_t)k * cc + e) = ((sh[0][lane] + sh[1][lane]) + sh[2][lane]) + sh[3][lane];
 }
 
 static int dw_tiles(int ci, int co) { return ((ci + kDwTile - 1) / kDwTile) * ((co + kDwTile - 1) / kDwTile); }
@@ -890,15 +899,15 @@ static int conv_fwd(int32_t dtype, const void* X, int64_t n_in, int32_t c_in, co
         if (n_in > 0 && !X) return fail(GSC_EINVAL, "conv_fwd: X is null");
         const BlockPlan plan{perm, bmask, ibase, items};
         if (dtype == GSC_BF16) {   // B_k = W[k]: the engine reads its columns, so the transposed copy
-            rc = transpose_w_bf16(W, K, c_in, c_out, ws, s);
+            const bool tile = n_in > 0 && tile_bf16_supported(c_in, c_out, K);
+            unsigned* counter = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
+                                                            fwd_counter_offset(c_in, c_out, K));
+            rc = transpose_w_bf16(W, K, c_in, c_out, ws, s, tile ? counter : nullptr);   // also zeroes the counter
             if (rc) return rc;
-            if (n_in > 0 && tile_bf16_supported(c_in, c_out, K)) {
-                unsigned* counter = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
-                                                                fwd_counter_offset(c_in, c_out, K));
+            if (tile)
                 return conv_tile_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan,
                                                  (n_out + kPlanBlockRows - 1) / kPlanBlockRows, n_out, Y, counter, s,
-                                                 ep);
-            }
+                                                 ep, /*counter_ready=*/true);
             return conv_blk_bf16<WIdentity>(c_in, c_out, X, n_in, ws, WIdentity{}, K, plan, n_out, Y, s, ep);
         }
         static const WSel kNoSel{};
@@ -979,6 +988,20 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
     if (K < 1 || K > kMaxKConv) return fail(GSC_EINVAL, "conv_bwd: K=%d outside [1,%d]", K, kMaxKConv);
     if (!W) return fail(GSC_EINVAL, "conv_bwd: W is null");
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (dW) {
+        if (n_pairs < 0) return fail(GSC_EINVAL, "conv_bwd: n_pairs < 0");
+        if (!seg || !ws) return fail(GSC_EINVAL, "conv_bwd: null seg/ws");
+        if (n_pairs > 0 && (!X || !dY || !in_idx || !out_idx)) return fail(GSC_EINVAL, "conv_bwd: null X/dY/idx");
+        const size_t need = gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K);
+        if (ws_bytes < need) return fail(GSC_ESHORT, "conv_bwd: ws needs %zu bytes, got %zu", need, ws_bytes);
+    }
+    // the weight gradient's work items (at the start of ws)
+    const int64_t dw_ch = dw_chunk(c_in, c_out);
+    int64_t* dw_ibase = ws ? reinterpret_cast<int64_t*>(ws) : nullptr;
+    int64_t* dw_chunks =
+        ws ? reinterpret_cast<int64_t*>(reinterpret_cast<char*>(ws) + al256((size_t)(K + 1) * sizeof(int64_t)))
+           : nullptr;
+    bool dw_items_done = false;
     if (dX) {
         if (t_n_pairs < 0) return fail(GSC_EINVAL, "conv_bwd: t_n_pairs < 0");
         if (n_in > 0 && (!t_gidx || !t_wsel)) return fail(GSC_EINVAL, "conv_bwd: null t_gidx/t_wsel");
@@ -1007,9 +1030,15 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
                 if (ws && n_pairs >= 0 && ws_bytes >= gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K))
                     counter = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
                                                           bwd_counter_offset(n_pairs, c_in, c_out, K));
+                if (counter && dW) {   // one small launch: the weight gradient's items and the tile counter
+                    hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, dw_ch, dw_ibase, dw_chunks,
+                                       counter);
+                    GSC_LAUNCH_CHECK();
+                    dw_items_done = true;
+                }
                 rc = conv_tile_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan,
                                           (n_in + kPlanBlockRows - 1) / kPlanBlockRows, n_in, dX, counter, s,
-                                          Epilogue{});
+                                          Epilogue{}, /*counter_ready=*/dw_items_done);
             } else if (dtype == GSC_BF16)   // B_k[ch][col] = W[sel(k)][col][ch]: W is already the engine's layout
                 rc = conv_blk_bf16<WSel>(c_out, c_in, dY, n_out, W, sel, K, plan, n_in, dX, s);
             else
@@ -1029,19 +1058,16 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         if (rc) return rc;
     }
     if (dW) {
-        if (n_pairs < 0) return fail(GSC_EINVAL, "conv_bwd: n_pairs < 0");
-        if (!seg || !ws) return fail(GSC_EINVAL, "conv_bwd: null seg/ws");
-        if (n_pairs > 0 && (!X || !dY || !in_idx || !out_idx)) return fail(GSC_EINVAL, "conv_bwd: null X/dY/idx");
-        const size_t need = gsc_conv_bwd_ws_bytes(n_pairs, c_in, c_out, K);
-        if (ws_bytes < need) return fail(GSC_ESHORT, "conv_bwd: ws needs %zu bytes, got %zu", need, ws_bytes);
-        const int64_t ch = dw_chunk(c_in, c_out);
+        const int64_t ch = dw_ch;
         const int64_t items = dw_items_bound(n_pairs, K, ch);
         char* w = reinterpret_cast<char*>(ws);
-        int64_t* ibase = reinterpret_cast<int64_t*>(w);
-        int64_t* chunk = reinterpret_cast<int64_t*>(w + al256((size_t)(K + 1) * sizeof(int64_t)));
+        int64_t* ibase = dw_ibase;
+        int64_t* chunk = dw_chunks;
         float* part = reinterpret_cast<float*>(w + 2 * al256((size_t)(K + 1) * sizeof(int64_t)));
-        hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, ch, ibase, chunk);
-        GSC_LAUNCH_CHECK();
+        if (!dw_items_done) {
+            hipLaunchKernelGGL(k_dw_items, dim3(1), dim3(64), 0, s, seg, K, ch, ibase, chunk, nullptr);
+            GSC_LAUNCH_CHECK();
+        }
         if (dtype == GSC_F32 && dw_f32_specialised(c_in, c_out)) {
             auto X32 = reinterpret_cast<const float*>(X);
             auto dY32 = reinterpret_cast<const float*>(dY);
@@ -1073,8 +1099,13 @@ int gsc_sparse_conv_bwd(int32_t dtype, const void* X, const void* W, const void*
         }
         GSC_LAUNCH_CHECK();
         const int64_t cc = (int64_t)c_in * c_out;
-        hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)((cc + 63) / 64), (unsigned)K), dim3(kThreads), 0, s, part,
-                           ibase, c_in, c_out, dW);
+        // 16-byte lanes where that still leaves thousands of blocks (wide layers)
+        if (cc % 4 == 0 && cc >= 16384 && reinterpret_cast<uintptr_t>(dW) % 16 == 0)
+            hipLaunchKernelGGL(k_dw_reduce<4>, dim3((unsigned)((cc + 255) / 256), (unsigned)K), dim3(kThreads), 0, s,
+                               part, ibase, c_in, c_out, dW);
+        else
+            hipLaunchKernelGGL(k_dw_reduce<1>, dim3((unsigned)((cc + 63) / 64), (unsigned)K), dim3(kThreads), 0, s,
+                               part, ibase, c_in, c_out, dW);
         GSC_LAUNCH_CHECK();
     }
     return GSC_OK;

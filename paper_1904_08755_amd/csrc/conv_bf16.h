@@ -18,9 +18,11 @@ template <typename Sel>
 int conv_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const int32_t* gat, const int32_t* sca,
               const int64_t* gidx, const int32_t* perm, int K, int64_t n_y, void* Y, Sel sel, hipStream_t s);
 
-// Bt[w][col][k] = W[w][k][col] for K matrices of rows x cols bf16.
+// Bt[w][col][k] = W[w][k][col] for K matrices of rows x cols bf16; sets
+// *zero_counter (nullable, device memory) to 0 on the way.
 size_t transpose_ws_bytes(int K, int rows, int cols);
-int transpose_w_bf16(const void* W, int K, int rows, int cols, void* Bt, hipStream_t s);
+int transpose_w_bf16(const void* W, int K, int rows, int cols, void* Bt, hipStream_t s,
+                     unsigned* zero_counter = nullptr);
 
 // Weight-gradient partials for bf16 with ci, co multiples of 128.
 bool dw_bf16_supported(int ci, int co);

@@ -53,15 +53,58 @@ struct BfShape {
     static_assert(CA % 32 == 0 && CB % 64 == 0 && NB >= 1, "unsupported shape");
 };
 
-// Bt[w][col][k] = W[w][k][col] for a K x rows x cols stack of bf16 matrices.
-__global__ void k_transpose_w(const uint16_t* __restrict__ W, int rows, int cols, int64_t total,
-                              uint16_t* __restrict__ Bt) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t rc = (int64_t)rows * cols;
-        const int64_t w = i / rc;
-        const int64_t e = i - w * rc;
-        const int64_t col = e / rows, k = e - col * rows;   // i walks Bt in order: coalesced writes
-        Bt[i] = W[w * rc + k * cols + col];
+// Bt[w][col][k] = W[w][k][col] for a K x rows x cols stack of bf16 matrices:
+// a workgroup moves one 64 x 64 tile of one matrix through LDS.  V16: rows
+// and cols multiples of 8 and both matrices 16-byte aligned, so the tile is
+// read and written 16 bytes (8 elements) per lane; otherwise one element per
+// lane.  The padded LDS rows keep the column reads on distinct banks.
+// counter (nullable) is set to 0 on the way: the tile engine launched after
+// it hands out its tiles with it.
+constexpr int kTrTile = 64;
+template <bool V16>
+__global__ void __launch_bounds__(256) k_transpose_w(const uint16_t* __restrict__ W, int rows, int cols,
+                                                     uint16_t* __restrict__ Bt, unsigned* __restrict__ counter) {
+    constexpr int P = V16 ? 8 : 2;   // row padding (elements)
+    __shared__ __attribute__((aligned(16))) uint16_t tile[kTrTile][kTrTile + P];
+    if (counter && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) *counter = 0u;
+    const int64_t w = blockIdx.z;
+    const int r0 = blockIdx.y * kTrTile, c0 = blockIdx.x * kTrTile;
+    const uint16_t* src = W + w * (int64_t)rows * cols;
+    uint16_t* dst = Bt + w * (int64_t)rows * cols;
+    if constexpr (V16) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {   // 512 chunks of 8 elements: row j / 8, columns 8 (j % 8) ..
+            const int j = threadIdx.x + 256 * i, r = j >> 3, c = (j & 7) * 8;
+            if (r0 + r < rows && c0 + c < cols)
+                *reinterpret_cast<u32x4*>(&tile[r][c]) =
+                    *reinterpret_cast<const u32x4*>(src + (int64_t)(r0 + r) * cols + c0 + c);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {   // output row (column of W) j / 8, elements 8 (j % 8) ..
+            const int j = threadIdx.x + 256 * i, c = j >> 3, r = (j & 7) * 8;
+            if (c0 + c < cols && r0 + r < rows) {
+                uint32_t u[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    u[e] = (uint32_t)tile[r + 2 * e][c] | ((uint32_t)tile[r + 2 * e + 1][c] << 16);
+                *reinterpret_cast<u32x4*>(dst + (int64_t)(c0 + c) * rows + r0 + r) = u32x4{u[0], u[1], u[2], u[3]};
+            }
+        }
+    } else {
+        const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+#pragma unroll
+        for (int i = 0; i < kTrTile / 4; ++i) {
+            const int r = q + 4 * i;
+            if (r0 + r < rows && c0 + lane < cols) tile[r][lane] = src[(int64_t)(r0 + r) * cols + c0 + lane];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kTrTile / 4; ++i) {
+            const int c = q + 4 * i;
+            if (c0 + c < cols && r0 + lane < rows) dst[(int64_t)(c0 + c) * rows + r0 + lane] = tile[lane][c];
+        }
     }
 }
 
@@ -770,12 +813,18 @@ bool conv_bf16_supported(int ca, int cb, int K) {
 
 size_t transpose_ws_bytes(int K, int rows, int cols) { return (size_t)K * rows * cols * sizeof(uint16_t); }
 
-int transpose_w_bf16(const void* W, int K, int rows, int cols, void* Bt, hipStream_t s) {
-    const int64_t total = (int64_t)K * rows * cols;
-    int64_t blocks = (total + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<const uint16_t*>(W),
-                       rows, cols, total, reinterpret_cast<uint16_t*>(Bt));
+int transpose_w_bf16(const void* W, int K, int rows, int cols, void* Bt, hipStream_t s, unsigned* zero_counter) {
+    if (K <= 0 || rows <= 0 || cols <= 0) return GSC_OK;
+    const dim3 grid((unsigned)((cols + kTrTile - 1) / kTrTile), (unsigned)((rows + kTrTile - 1) / kTrTile),
+                    (unsigned)K);
+    const bool v16 = rows % 8 == 0 && cols % 8 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(Bt) % 16 == 0;
+    if (v16)
+        hipLaunchKernelGGL(k_transpose_w<true>, grid, dim3(256), 0, s, reinterpret_cast<const uint16_t*>(W), rows,
+                           cols, reinterpret_cast<uint16_t*>(Bt), zero_counter);
+    else
+        hipLaunchKernelGGL(k_transpose_w<false>, grid, dim3(256), 0, s, reinterpret_cast<const uint16_t*>(W), rows,
+                           cols, reinterpret_cast<uint16_t*>(Bt), zero_counter);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }

@@ -49,13 +49,14 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
 // for ca, cb in {64, 128, 256}, K <= 30, a tile of 16 blocks by all cb
 // columns per workgroup, persistent workgroups.  nb = number of plan blocks;
 // counter (nullable): 4 bytes of device memory the call uses to hand out
-// tiles (large ones first; without it the tiles go out in a fixed order).
-// n_x * ca below 2^30.  Asynchronous.
+// tiles (large ones first; without it the tiles go out in a fixed order),
+// set to 0 by the call unless counter_ready (an earlier launch on the stream
+// did).  n_x * ca below 2^30.  Asynchronous.
 bool tile_bf16_supported(int ca, int cb, int K);
 template <typename Sel>
 int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
                    const BlockPlan& plan, int64_t nb, int64_t n_y, void* Y, unsigned* counter, hipStream_t s,
-                   const Epilogue& ep);
+                   const Epilogue& ep, bool counter_ready = false);
 
 // Weight gradient of a wide bf16 layer (conv_tile.hip), ci, co in {128,
 // 256): the partial sum of each work item (dw_item) over its pairs, written

@@ -764,7 +764,7 @@ static int tile_grid_cap() {
 template <int CA, int CB, typename Sel, bool EP>
 static int launch_tile_kernel(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
                               const BlockPlan& p, int64_t nb, int64_t n_y, const Epilogue& ep, uint16_t* Y,
-                              unsigned* counter, hipStream_t s) {
+                              unsigned* counter, bool counter_ready, hipStream_t s) {
     const int64_t tiles = (nb + kTileBlocks - 1) / kTileBlocks;
     if (tiles == 0) return GSC_OK;
     const int64_t grid = tiles < tile_grid_cap() ? tiles : tile_grid_cap();
@@ -772,7 +772,7 @@ static int launch_tile_kernel(const uint16_t* X, int64_t n_x, const uint16_t* Bt
     auto kern = k_conv_tile_bf16<CA, CB, Sel, EP>;
     GSC_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)dyn));
-    if (counter) {
+    if (counter && !counter_ready) {
         hipLaunchKernelGGL(k_tile_counter_zero, dim3(1), dim3(1), 0, s, counter);
         GSC_LAUNCH_CHECK();
     }
@@ -785,7 +785,7 @@ static int launch_tile_kernel(const uint16_t* X, int64_t n_x, const uint16_t* Bt
 template <typename Sel>
 int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, const Sel& sel, int K,
                    const BlockPlan& plan, int64_t nb, int64_t n_y, void* Y, unsigned* counter, hipStream_t s,
-                   const Epilogue& ep) {
+                   const Epilogue& ep, bool counter_ready) {
     auto X16 = reinterpret_cast<const uint16_t*>(X);
     auto B16 = reinterpret_cast<const uint16_t*>(Bt);
     auto Y16 = reinterpret_cast<uint16_t*>(Y);
@@ -793,8 +793,10 @@ int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, c
 #define GSC_TILE_CASE(A, B)                                                                                    \
     if (ca == A && cb == B) {                                                                                  \
         if (epi)                                                                                               \
-            return launch_tile_kernel<A, B, Sel, true>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter, s); \
-        return launch_tile_kernel<A, B, Sel, false>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter, s);  \
+            return launch_tile_kernel<A, B, Sel, true>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter,      \
+                                                       counter_ready, s);                                          \
+        return launch_tile_kernel<A, B, Sel, false>(X16, n_x, B16, K, sel, plan, nb, n_y, ep, Y16, counter,         \
+                                                    counter_ready, s);                                             \
     }
     GSC_TILE_CASE(64, 64) GSC_TILE_CASE(64, 128) GSC_TILE_CASE(64, 256) GSC_TILE_CASE(128, 64)
     GSC_TILE_CASE(128, 128) GSC_TILE_CASE(128, 256) GSC_TILE_CASE(256, 64) GSC_TILE_CASE(256, 128)
@@ -805,8 +807,8 @@ int conv_tile_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, c
 
 template int conv_tile_bf16<WIdentity>(int, int, const void*, int64_t, const void*, const WIdentity&, int,
                                        const BlockPlan&, int64_t, int64_t, void*, unsigned*, hipStream_t,
-                                       const Epilogue&);
+                                       const Epilogue&, bool);
 template int conv_tile_bf16<WSel>(int, int, const void*, int64_t, const void*, const WSel&, int, const BlockPlan&,
-                                  int64_t, int64_t, void*, unsigned*, hipStream_t, const Epilogue&);
+                                  int64_t, int64_t, void*, unsigned*, hipStream_t, const Epilogue&, bool);
 
 }  // namespace gsc
