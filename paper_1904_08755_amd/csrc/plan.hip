@@ -83,7 +83,8 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __re
 // stable LSD radix sort of (key, value) by key, one kernel per pass
 // ---------------------------------------------------------------------------
 // The digit counts of every pass over all keys come first (one histogram
-// kernel), so a pass knows where each digit's range starts.  A pass kernel
+// kernel); each tile of a pass scans its pass's counts to know where each
+// digit's range starts.  A pass kernel
 // takes tiles of kRsTile keys in ticket order (an atomic counter, so every
 // tile a block waits for is already running), publishes its tile's count of
 // each digit and looks back over the earlier tiles' published counts to find
@@ -122,31 +123,9 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restr
     }
 }
 
-// gbase[p][d] = number of keys whose pass-p digit is below d.
-__global__ void __launch_bounds__(kRsThreads) k_rs_gscan(const uint32_t* __restrict__ ghist, int passes,
-                                                         int64_t* __restrict__ gbase) {
-    __shared__ int64_t wsum[kRsThreads / 64];
-    const int d = threadIdx.x, w = d >> 6, l = d & 63;
-    for (int p = 0; p < passes; ++p) {
-        const int64_t v = ghist[p * kRsBins + d];
-        int64_t inc = v;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int64_t u = __shfl_up(inc, o, 64);
-            if (l >= o) inc += u;
-        }
-        if (l == 63) wsum[w] = inc;
-        __syncthreads();
-        int64_t before = 0;
-        for (int i = 0; i < w; ++i) before += wsum[i];
-        gbase[p * kRsBins + d] = before + inc - v;
-        __syncthreads();
-    }
-}
-
 __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restrict__ kin,
                                                         const int32_t* __restrict__ vin, int64_t n, int shift,
-                                                        const int64_t* __restrict__ gbase,
+                                                        const uint32_t* __restrict__ ghist,
                                                         uint32_t* __restrict__ status,
                                                         uint32_t* __restrict__ status_next,
                                                         uint32_t* __restrict__ ticket, uint32_t* __restrict__ kout,
@@ -158,11 +137,24 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
     __shared__ int32_t hist[kRsBins];
     __shared__ int32_t wcnt[W][kRsBins];
     __shared__ int64_t tile_sh;
-    const int tid = threadIdx.x, wave = tid >> 6;
+    __shared__ int64_t wsum[W];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     if (tid == 0) tile_sh = atomicAdd(ticket, 1u);
     hist[tid] = 0;
     for (int i = tid; i < W * kRsBins; i += kRsThreads) (&wcnt[0][0])[i] = 0;
+    // where digit tid's keys start in this pass's output (the keys of smaller
+    // digits): every tile scans the pass's digit counts itself
+    const int64_t dc = ghist[tid];
+    int64_t dinc = dc;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t u = __shfl_up(dinc, o, 64);
+        if (lane >= o) dinc += u;
+    }
+    if (lane == 63) wsum[wave] = dinc;
     __syncthreads();
+    int64_t dbase = dinc - dc;
+    for (int i = 0; i < wave; ++i) dbase += wsum[i];
     const int64_t t = tile_sh;
     const int64_t base = t * kRsTile;
     status_next[t * kRsBins + tid] = 0;   // the next pass's entry of this tile (that array is idle now)
@@ -216,7 +208,7 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
             }
             __hip_atomic_store(mine, kStIncl | (before + c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        start[tid] = gbase[tid] + before;
+        start[tid] = dbase + before;
     }
     const unsigned long long below = lanemask_lt();
 #pragma unroll
@@ -361,8 +353,6 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
     w += al256((size_t)nzero * sizeof(uint32_t));
     uint32_t* st1 = reinterpret_cast<uint32_t*>(w);
     w += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
-    int64_t* gbase = reinterpret_cast<int64_t*>(w);
-    w += al256((size_t)kRsMaxPasses * kRsBins * sizeof(int64_t));
     int32_t* cnt = reinterpret_cast<int32_t*>(w);
     w += al256((size_t)nb * sizeof(int32_t));
     void* scan_ws = w;
@@ -380,8 +370,6 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
     GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_rs_gscan, dim3(1), dim3(kRsThreads), 0, s, ghist, passes, gbase);
-    GSC_LAUNCH_CHECK();
     const uint32_t* kin = ka;
     const int32_t* vin = nullptr;
     for (int p = 0; p < passes; ++p) {
@@ -390,7 +378,7 @@ static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uin
         uint32_t* st = (p & 1) ? st1 : st0;
         uint32_t* st_next = (p & 1) ? st0 : st1;
         hipLaunchKernelGGL(k_rs_pass, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n, p * kRsBits,
-                           gbase + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout, spin_max, lb_status);
+                           ghist + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout, spin_max, lb_status);
         GSC_LAUNCH_CHECK();
         kin = kout;
         vin = vout;
@@ -438,7 +426,6 @@ size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
     size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
     b += al256((size_t)(kRsMaxPasses * kRsBins + kRsMaxPasses + nrs * kRsBins) * sizeof(uint32_t));
     b += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
-    b += al256((size_t)kRsMaxPasses * kRsBins * sizeof(int64_t));
     b += al256((size_t)nb * sizeof(int32_t));
     b += scan_ws_bytes(nb);
     return b + 256;
