@@ -292,6 +292,30 @@ def test_bf16_odd_channels():
     _conv_case(coords, 24, 40, regions.hypercube(3, 3), 76, dtype="bf16")
 
 
+def test_bf16_forward_misaligned_weights():
+    """Weights that start 2 bytes past a 16-byte boundary: the forward's
+    transposed copy of W takes the element-wise path (the 16-byte one needs
+    aligned matrices), and the result is still the oracle's."""
+    coords = WL.random_coords(97, 1500, 3, -10, 10, batch=2)
+    offs = regions.hypercube(3, 3)
+    ci, co = 32, 64
+    X, Xb = WL.random_features(98, len(coords), ci, "bf16")
+    W, Wb = WL.random_weights(99, len(offs), ci, co, "bf16")
+    dev = lambda b: torch.from_numpy(b.view(np.int16)).to(DEV).view(torch.bfloat16)
+    flat = torch.zeros(Wb.size + 8, dtype=torch.bfloat16, device=DEV)
+    base = (16 - flat.data_ptr() % 16) % 16 // 2 + 1      # one element past an aligned start
+    tW = flat[base:base + Wb.size].view(len(offs), ci, co)
+    tW.copy_(dev(Wb))
+    assert tW.data_ptr() % 16 == 2
+    table = gsc.gsc_coords_build(_t(coords))
+    km = gsc.gsc_kernel_map(table, _t(coords), offs)
+    _say("[gpu] bf16 forward, weights 2 bytes off alignment")
+    Y = gsc.gsc_sparse_conv_fwd(dev(Xb), tW, km)
+    torch.cuda.synchronize()
+    m = O.kernel_map(coords, coords, np.asarray(offs))
+    assert rel_err(to_np(Y), O.conv_forward(X, W, m, len(coords))) <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("ci,co,region", [(256, 256, "cube2"), (128, 256, "cube3"), (256, 128, "cube2"),
                                            (64, 128, "cube3"), (128, 64, "cube2"), (32, 256, "cube3")])
 def test_bf16_wide_channel_engine(ci, co, region):
