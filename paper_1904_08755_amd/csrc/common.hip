@@ -74,7 +74,8 @@ constexpr int64_t kScanSingleMax = (int64_t)kScanSingleThreads * kScanSingleE;
 
 __global__ void __launch_bounds__(kScanSingleThreads) k_scan_single(const int32_t* __restrict__ cnt, int64_t m,
                                                                     int64_t* __restrict__ out,
-                                                                    int64_t* __restrict__ total_out) {
+                                                                    int64_t* __restrict__ total_out,
+                                                                    int64_t* __restrict__ every_out, int64_t every) {
     __shared__ int64_t sh[kScanSingleThreads / 64];
     const int t = threadIdx.x, w = t >> 6, l = __lane_id();
     const int64_t b = (int64_t)t * kScanSingleE;
@@ -93,14 +94,22 @@ __global__ void __launch_bounds__(kScanSingleThreads) k_scan_single(const int32_
         all += sh[i];
     }
     int64_t run = base + inc - s;
+    int64_t nxt = every_out ? (b + every - 1) / every * every : -1;   // next index to copy to every_out
 #pragma unroll
     for (int i = 0; i < kScanSingleE; ++i) {
-        if (b + i < m) out[b + i] = run;
+        if (b + i < m) {
+            out[b + i] = run;
+            if (b + i == nxt) {
+                every_out[nxt / every] = run;
+                nxt += every;
+            }
+        }
         run += v[i];
     }
     if (t == 0) {
         out[m] = all;
         if (total_out) *total_out = all;
+        if (every_out) every_out[m / every] = all;
     }
 }
 
@@ -109,7 +118,8 @@ __global__ void __launch_bounds__(kScanSingleThreads) k_scan_single(const int32_
 // L2), then scans its own tile.  The last block also writes the total.
 __global__ void __launch_bounds__(kScanThreads) k_scan_down2(const int32_t* __restrict__ cnt, int64_t m,
                                                              const int64_t* __restrict__ part, int64_t nb,
-                                                             int64_t* __restrict__ out, int64_t* __restrict__ total_out) {
+                                                             int64_t* __restrict__ out, int64_t* __restrict__ total_out,
+                                                             int64_t* __restrict__ every_out, int64_t every) {
     __shared__ int64_t sh[kScanThreads / 64];
     __shared__ int64_t carry_sh;
     const int w = threadIdx.x >> 6, l = __lane_id();
@@ -136,14 +146,22 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_down2(const int32_t* __re
     }
     int64_t tot;
     int64_t run = carry + block_exclusive(s, sh, &tot);
+    int64_t nxt = every_out ? (base + every - 1) / every * every : -1;   // next index to copy to every_out
 #pragma unroll
     for (int i = 0; i < kScanPer; ++i) {
-        if (base + i < m) out[base + i] = run;
+        if (base + i < m) {
+            out[base + i] = run;
+            if (base + i == nxt) {
+                every_out[nxt / every] = run;
+                nxt += every;
+            }
+        }
         run += v[i];
     }
     if (blockIdx.x == nb - 1 && threadIdx.x == 0) {
         out[m] = carry + tot;
         if (total_out) *total_out = carry + tot;
+        if (every_out) every_out[m / every] = carry + tot;
     }
 }
 
@@ -167,9 +185,12 @@ size_t scan_ws_bytes(int64_t m) {
     return (size_t)((nb > 0 ? nb : 1) * sizeof(int64_t) + 256);
 }
 
-int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws, hipStream_t s) {
+int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws, hipStream_t s,
+                int64_t* every_out, int64_t every) {
+    if (every_out && (every <= 0 || m % every != 0)) return fail(GSC_EINVAL, "scan: bad every=%lld", (long long)every);
     if (m <= kScanSingleMax) {
-        hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(kScanSingleThreads), 0, s, cnt, m, out, total_out);
+        hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(kScanSingleThreads), 0, s, cnt, m, out, total_out, every_out,
+                           every);
         GSC_LAUNCH_CHECK();
         return GSC_OK;
     }
@@ -177,7 +198,8 @@ int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out,
     const int64_t nb = (m + kScanTile - 1) / kScanTile;
     hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part);
     GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_scan_down2, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part, nb, out, total_out);
+    hipLaunchKernelGGL(k_scan_down2, dim3((unsigned)nb), dim3(kScanThreads), 0, s, cnt, m, part, nb, out, total_out,
+                       every_out, every);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }

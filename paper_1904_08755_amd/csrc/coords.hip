@@ -130,43 +130,92 @@ __global__ void __launch_bounds__(kThreads) k_bbox(const int32_t* coords, int64_
     }
 }
 
-// one thread: bit widths and shifts of the packed key
-__global__ void k_plan(TableHeader* h) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    const int ncol = h->ncol;
+// The packed key's layout from the bounding box: bit widths and shifts per
+// column, and the blocked columns of the slot hash (see home_slot).
+struct KeyLayout {
+    int32_t shift[kMaxCols], bits[kMaxCols];
+    int32_t total_bits, nblk, blk_shift[3];
+};
+
+__device__ void key_layout(const TableHeader* h, int ncol, KeyLayout* kl) {
     int total = 0;
-    int bits[kMaxCols];
-    for (int c = 0; c < ncol; ++c) {
-        int64_t range = (int64_t)h->hi[c] - (int64_t)h->lo[c];
+    for (int c = 0; c < kMaxCols; ++c) {
         int b = 0;
-        if (range > 0) b = 64 - __clzll((unsigned long long)range);
-        if (h->lo[c] > h->hi[c]) b = 0;   // no rows
-        bits[c] = b;
+        if (c < ncol) {
+            const int64_t range = (int64_t)h->hi[c] - (int64_t)h->lo[c];
+            if (range > 0) b = 64 - __clzll((unsigned long long)range);
+            if (h->lo[c] > h->hi[c]) b = 0;   // no rows
+        }
+        kl->bits[c] = b;
         total += b;
     }
     int sh = 0;
-    for (int c = ncol - 1; c >= 0; --c) {
-        h->shift[c] = sh;
-        h->bits[c] = bits[c];
-        sh += bits[c];
+    for (int c = kMaxCols - 1; c >= 0; --c) {
+        kl->shift[c] = c < ncol ? sh : 0;
+        if (c < ncol) sh += kl->bits[c];
     }
-    h->total_bits = total;
-    if (total > kMaxKeyBits) h->status |= ST_RANGE;
+    kl->total_bits = total;
     int nb = 0;
+    for (int i = 0; i < 3; ++i) kl->blk_shift[i] = 0;
     for (int c = 1; c < ncol && nb < 3; ++c) {
         const int t = h->vary[c] ? __ffs(h->vary[c]) - 1 : -1;   // lowest varying bit
-        if (t >= 0 && t < bits[c]) h->blk_shift[nb++] = h->shift[c] + t;
+        if (t >= 0 && t < kl->bits[c]) kl->blk_shift[nb++] = kl->shift[c] + t;
     }
-    h->nblk = nb;
+    kl->nblk = nb;
+}
+
+// the layout into the header (ST_RANGE when the key needs more than kMaxKeyBits)
+__device__ void store_key_layout(TableHeader* h, int ncol, const KeyLayout& kl) {
+    for (int c = 0; c < ncol; ++c) {
+        h->shift[c] = kl.shift[c];
+        h->bits[c] = kl.bits[c];
+    }
+    h->total_bits = kl.total_bits;
+    if (kl.total_bits > kMaxKeyBits) atomicOr(&h->status, ST_RANGE);
+    for (int i = 0; i < 3; ++i) h->blk_shift[i] = kl.blk_shift[i];
+    h->nblk = kl.nblk;
+}
+
+// one thread: the key layout of a table with no rows to insert
+__global__ void k_plan(TableHeader* h) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    KeyLayout kl;
+    key_layout(h, h->ncol, &kl);
+    store_key_layout(h, h->ncol, kl);
+}
+
+// The insert kernels work the key layout out from the bounding box
+// themselves (thread 0 of every block, into LDS), so no launch of its own
+// sits between the box and the inserts; block 0 also stores it in the header
+// for the kernels after them.  Returns the view a query needs and whether
+// the key fits (all blocks compute the same).
+__device__ __forceinline__ bool block_key_view(TableHeader* h, int ncol, KeyLayout* kl_s, TableView* tv) {
+    if (threadIdx.x == 0) {
+        key_layout(h, ncol, kl_s);
+        if (blockIdx.x == 0) store_key_layout(h, ncol, *kl_s);
+    }
+    __syncthreads();
+    tv->sh.mask = (unsigned long long)h->capacity - 1;
+    tv->sh.nblk = kl_s->nblk;
+    for (int i = 0; i < 3; ++i) tv->sh.blk_shift[i] = kl_s->blk_shift[i];
+    tv->ncol = ncol;
+    for (int c = 0; c < kMaxCols; ++c) {
+        tv->lo[c] = c < ncol ? h->lo[c] : 0;
+        tv->hi[c] = c < ncol ? h->hi[c] : 0;
+        tv->shift[c] = kl_s->shift[c];
+    }
+    return kl_s->total_bits <= kMaxKeyBits;
 }
 
 __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int64_t n, TableHeader* h,
                                                      Slot* slots) {
-    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
-    if (r >= n) return;
-    if (h->status & ST_RANGE) return;
+    __shared__ KeyLayout kl_s;
     const int ncol = h->ncol;
-    const TableView tv = table_view(h, ncol);
+    TableView tv;
+    const bool fits = block_key_view(h, ncol, &kl_s, &tv);
+    const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    if (r >= n || !fits) return;
+    if (h->status & ST_RANGE) return;   // set by the box: a row outside int32
     const unsigned long long mask = tv.sh.mask;
     int64_t v[kMaxCols];
     StrideArg none{};
@@ -200,20 +249,23 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
 // shuffle, which spares the contended atomics on the shared slot.
 __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, int64_t n, StrideArg st,
                                                          TableHeader* h, Slot* slots, int64_t* slot_of) {
+    __shared__ KeyLayout kl_s;
+    const int ncol = h->ncol;
+    TableView tv;
+    const bool fits = block_key_view(h, ncol, &kl_s, &tv);
     const int64_t r = xcd_unit(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool valid = r < n;
-    if (h->status & ST_RANGE) {   // uniform
+    if (!fits || (h->status & ST_RANGE)) {   // uniform (the box's flag is set before this kernel)
         if (valid) slot_of[r] = 0;
         return;
     }
-    const int ncol = h->ncol;
-    const unsigned long long mask = (unsigned long long)h->capacity - 1;
+    const unsigned long long mask = tv.sh.mask;
     unsigned long long key = 0;
     bool ok = false;
     if (valid) {
         int64_t v[kMaxCols];
         load_row(coords, r, ncol, st, v);
-        ok = pack_key(h, ncol, v, &key);
+        ok = pack_key(tv, v, &key);
         if (!ok) {
             atomicOr(&h->status, ST_RANGE);
             slot_of[r] = 0;
@@ -226,7 +278,7 @@ __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, 
     const unsigned long long leaders = __ballot(ok && !follower);
     unsigned long long s = 0;
     if (ok && !follower) {
-        s = home_slot(h, key, mask);
+        s = home_slot(tv.sh, key);
         bool placed = false;
         for (unsigned long long i = 0; i <= mask; ++i) {
             const unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
@@ -415,12 +467,11 @@ static int build_enqueue(const int32_t* coords, int64_t n, int32_t D, void* tabl
         hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n, 256)), dim3(kThreads), 0, s, coords, n, ncol, none, h);
         GSC_LAUNCH_CHECK();
     }
-    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
-    GSC_LAUNCH_CHECK();
-    if (n > 0) {
+    if (n > 0)   // the inserts work out (and store) the key layout themselves
         hipLaunchKernelGGL(k_insert, dim3(grid_for(n)), dim3(kThreads), 0, s, coords, n, h, slots);
-        GSC_LAUNCH_CHECK();
-    }
+    else
+        hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
+    GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
 
@@ -513,8 +564,6 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
 
     hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n_in, 256)), dim3(kThreads), 0, s, in_coords, n_in, ncol, st, h);
     GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
-    GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_insert_min, dim3(grid_for(n_in)), dim3(kThreads), 0, s, in_coords, n_in, st, h, slots,
                        slot_of);
     GSC_LAUNCH_CHECK();
@@ -604,8 +653,6 @@ int gsc_quantize(const float* points, const int32_t* batch, int64_t n, int32_t D
     hipLaunchKernelGGL(k_quantize, dim3(grid_for(n)), dim3(kThreads), 0, s, points, batch, n, (int)D, va, qc, h);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_bbox, dim3(grid_capped(n, 256)), dim3(kThreads), 0, s, qc, n, ncol, none, h);
-    GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
     GSC_LAUNCH_CHECK();
     hipLaunchKernelGGL(k_insert_min, dim3(grid_for(n)), dim3(kThreads), 0, s, qc, n, none, h, slots, slot_of);
     GSC_LAUNCH_CHECK();

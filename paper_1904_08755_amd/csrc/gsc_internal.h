@@ -214,11 +214,13 @@ __device__ __forceinline__ int64_t floor_mul(int64_t a, int64_t s) {
 
 // ---------------------------------------------------------------------------
 // device-wide exclusive scan of int32 counts into int64 offsets:
-// out[i] = sum(cnt[0..i)), out[m] = total; optionally also *total_out.
+// out[i] = sum(cnt[0..i)), out[m] = total; optionally also *total_out, and
+// every_out[i / every] = out[i] for the multiples i of every (every > 0
+// dividing m: a kernel map's segment table seg[k] = gidx[k * G]).
 // ---------------------------------------------------------------------------
 size_t scan_ws_bytes(int64_t m);
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
-                hipStream_t s);
+                hipStream_t s, int64_t* every_out = nullptr, int64_t every = 0);
 
 // Largest offset count of one range of a block plan (neighbour masks are
 // 32-bit).  A map with more offsets is planned in ranges of consecutive

@@ -397,10 +397,14 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
             GSC_LAUNCH_CHECK();
         }
     }
-    int rc = scan_counts(cnt, K * G, gidx, res, scan_ws, s);
+    // the scan also writes seg[k] = gidx[k * G] (a launch of its own without groups)
+    int rc = G > 0 ? scan_counts(cnt, K * G, gidx, res, scan_ws, s, seg, G)
+                   : scan_counts(cnt, 0, gidx, res, scan_ws, s);
     if (rc) return rc;
-    rc = seg_from_gidx(gidx, K, G, seg, s);
-    if (rc) return rc;
+    if (G == 0) {
+        rc = seg_from_gidx(gidx, K, G, seg, s);
+        if (rc) return rc;
+    }
     int64_t bound = cap_pairs;
     if (n_pairs) {
         int64_t hres[2];
@@ -628,10 +632,13 @@ int gsc_kernel_map_transpose(const int32_t* in_idx, const int32_t* out_idx, cons
         hipLaunchKernelGGL(k_nbr_count, dim3(nblk), dim3(kThreads), 0, s, t_nbr, n_rev, K, G, cnt);
         GSC_LAUNCH_CHECK();
     }
-    int rc = scan_counts(cnt, K * G, t_gidx, nullptr, w, s);
+    int rc = G > 0 ? scan_counts(cnt, K * G, t_gidx, nullptr, w, s, t_seg, G)
+                   : scan_counts(cnt, 0, t_gidx, nullptr, w, s);
     if (rc) return rc;
-    rc = seg_from_gidx(t_gidx, K, G, t_seg, s);
-    if (rc) return rc;
+    if (G == 0) {
+        rc = seg_from_gidx(t_gidx, K, G, t_seg, s);
+        if (rc) return rc;
+    }
     if (nblk > 0 && cap_pairs > 0) {
         hipLaunchKernelGGL(k_kmap_fill, dim3(nblk), dim3(kThreads), 0, s, n_rev, K, G, t_nbr, t_gidx, t_in_idx,
                            t_out_idx, cap_pairs);
