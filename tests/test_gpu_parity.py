@@ -443,6 +443,18 @@ def test_conv_plan_structure_bf16_wide():
     _check_plan(gsc.gsc_conv_plan(km))
 
 
+def test_conv_plan_structure_full_size():
+    """The block plan of the full 2 cm scene pair (300,577 rows: 18,787
+    blocks, whose item counts take the two-kernel scan), entry by entry
+    against the map."""
+    wl = WL.make_workload(1)
+    dw = pipeline.to_device(wl, DEV)
+    table = gsc.gsc_coords_build(dw.coords)
+    km = gsc.gsc_kernel_map(table, dw.coords, dw.offsets[0], dense=True)
+    _say(f"[gpu] full-size plan n={wl.n}")
+    _check_plan(gsc.gsc_conv_plan(km))
+
+
 def _plan_case(coords, ci, co, offs, seed, ts=1, dtype="f32"):
     """_conv_case through the block engines: plans of the forward and the
     role-reversed map."""
