@@ -51,19 +51,41 @@ constexpr int kRsTile = kRsThreads * kRsPer;      // keys per block
 
 static size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// The popcount field of the sort key: as many bits as the last 10-bit digit
+// of the K-bit mask leaves free (at most 6, and within a 32-bit key); its
+// largest value, 0 when there is no room.  K = 27: 3 bits, counts capped at 7.
+__host__ __device__ inline int plan_key_pbits(int K) {
+    const int spare = (K + kRsBits - 1) / kRsBits * kRsBits - K;
+    const int a = spare < 32 - K ? spare : 32 - K;
+    return a < 6 ? a : 6;
+}
+__host__ __device__ inline uint32_t plan_key_cap(int K) { return (1u << plan_key_pbits(K)) - 1u; }
+
+// Offsets of plan range r of a K-offset map planned in ranges of S offsets
+// (the last one may be shorter), and their mask bits.
+__host__ __device__ inline int range_k0(int r, int S) { return r * S; }
+__host__ __device__ inline int range_len(int r, int S, int K) { return K - r * S < S ? K - r * S : S; }
+__host__ __device__ inline uint32_t range_kmask(int kr) { return kr >= 32 ? ~0u : (1u << kr) - 1u; }
+
 // ---------------------------------------------------------------------------
 // masks from the dense map
 // ---------------------------------------------------------------------------
-// (Also clears the sort's counters and first look-back entries, zero[0, nzero),
+// Range r = blockIdx.y of the plan: keys[r * n + j] for its offsets.  (Also
+// clears the sort's counters and first look-back entries, zero[0, nzero),
 // which the histogram kernel after it starts to fill.)
-__global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int K,
-                                                             uint32_t cap, uint32_t* __restrict__ keys,
+__global__ void __launch_bounds__(kPlanThreads) k_plan_masks(const int32_t* __restrict__ nbr, int64_t n, int Kall,
+                                                             int S, uint32_t* __restrict__ keys,
                                                              uint32_t* __restrict__ zero, int64_t nzero,
                                                              uint32_t* __restrict__ lb_status) {
-    if (lb_status && blockIdx.x == 0 && threadIdx.x == 0) *lb_status = 0u;   // the plan call's first kernel
-    for (int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x; i < nzero;
-         i += (int64_t)gridDim.x * kPlanThreads)
+    const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;   // block number over all ranges
+    if (lb_status && lin == 0 && threadIdx.x == 0) *lb_status = 0u;     // the plan call's first kernel
+    for (int64_t i = lin * kPlanThreads + threadIdx.x; i < nzero; i += (int64_t)gridDim.x * gridDim.y * kPlanThreads)
         zero[i] = 0;
+    const int rg = blockIdx.y;
+    const int K = range_len(rg, S, Kall);
+    const uint32_t cap = plan_key_cap(K);
+    nbr += (int64_t)range_k0(rg, S) * n;
+    keys += (int64_t)rg * n;
     const int64_t j = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
     if (j >= n) return;
     uint32_t m = 0;
@@ -99,9 +121,13 @@ constexpr uint32_t kStCount = kStAgg - 1;
 constexpr int64_t kRsMaxKeys = kStCount;          // counts must fit below the flag bits
 constexpr int kSpinMax = 1 << 22;                 // bound on polls of one entry (not reached in practice)
 
+// Range r = blockIdx.y: its keys at keys + r * n, its counts at
+// ghist + r * kRsMaxPasses * kRsBins.
 __global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restrict__ keys, int64_t n, int passes,
                                                          uint32_t* __restrict__ ghist) {
     __shared__ int32_t h[kRsMaxPasses][kRsBins];
+    keys += (int64_t)blockIdx.y * n;
+    ghist += (int64_t)blockIdx.y * kRsMaxPasses * kRsBins;
     for (int i = threadIdx.x; i < kRsMaxPasses * kRsBins; i += kRsThreads) (&h[0][0])[i] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kRsTile;
@@ -123,9 +149,14 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_ghist(const uint32_t* __restr
     }
 }
 
+// Tiles of all ranges share the ticket: ticket T is tile T % nrs of range
+// T / nrs, which looks back over its own range's tiles only (all of them
+// took smaller tickets).  Range r's keys and values are at r * n, its look-
+// back entries at r * nrs * kRsBins, its digit counts at r * kRsMaxPasses *
+// kRsBins (ghist points at the pass's row of range 0).
 __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restrict__ kin,
-                                                        const int32_t* __restrict__ vin, int64_t n, int shift,
-                                                        const uint32_t* __restrict__ ghist,
+                                                        const int32_t* __restrict__ vin, int64_t n, int64_t nrs,
+                                                        int R, int shift, const uint32_t* __restrict__ ghist,
                                                         uint32_t* __restrict__ status,
                                                         uint32_t* __restrict__ status_next,
                                                         uint32_t* __restrict__ ticket, uint32_t* __restrict__ kout,
@@ -142,9 +173,24 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
     if (tid == 0) tile_sh = atomicAdd(ticket, 1u);
     hist[tid] = 0;
     for (int i = tid; i < W * kRsBins; i += kRsThreads) (&wcnt[0][0])[i] = 0;
+    // the pass's digit counts: range 0's load while the ticket is out (a
+    // single-range plan waits for nothing more); a tile of another range
+    // loads its own once the ticket has told it its range
+    int64_t dc = ghist[tid];
+    int64_t rg = 0;   // the tile's range
+    if (R > 1) {      // uniform
+        __syncthreads();
+        rg = (int64_t)tile_sh / nrs;
+        if (rg != 0) dc = ghist[rg * kRsMaxPasses * kRsBins + tid];
+    }
+    kin += rg * n;
+    vout += rg * n;
+    kout += rg * n;
+    if (vin) vin += rg * n;
+    status += rg * nrs * kRsBins;
+    status_next += rg * nrs * kRsBins;
     // where digit tid's keys start in this pass's output (the keys of smaller
     // digits): every tile scans the pass's digit counts itself
-    const int64_t dc = ghist[tid];
     int64_t dinc = dc;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -155,7 +201,7 @@ __global__ void __launch_bounds__(kRsThreads) k_rs_pass(const uint32_t* __restri
     __syncthreads();
     int64_t dbase = dinc - dc;
     for (int i = 0; i < wave; ++i) dbase += wsum[i];
-    const int64_t t = tile_sh;
+    const int64_t t = tile_sh - rg * nrs;   // (visible: a barrier has passed since thread 0 set it)
     const int64_t base = t * kRsTile;
     status_next[t * kRsBins + tid] = 0;   // the next pass's entry of this tile (that array is idle now)
     uint32_t key[kRsPer];
@@ -263,12 +309,18 @@ __device__ __forceinline__ uint32_t block_or16(uint32_t v) {
     return v;
 }
 
-// (The sorted keys are masked to the K offsets and the rows clamped to
+// Range r = blockIdx.y (its keys at r * n, its blocks at r * nb).  (The
+// sorted keys are masked to the range's offsets and the rows clamped to
 // [0, n): after a look-back that gave up they need not be what the sort
 // meant, and the plan must still stay inside its arrays.)
-__global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __restrict__ keys, uint32_t kmask,
+__global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __restrict__ keys, int Kall, int S,
                                                             int64_t n, int64_t nb, uint32_t* __restrict__ bmask,
                                                             int32_t* __restrict__ cnt) {
+    const int rg = blockIdx.y;
+    const uint32_t kmask = range_kmask(range_len(rg, S, Kall));
+    keys += (int64_t)rg * n;
+    bmask += (int64_t)rg * nb;
+    cnt += (int64_t)rg * nb;
     const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
     const uint32_t u = block_or16(i < n ? keys[i] & kmask : 0u);
     const int64_t b = i >> 4;
@@ -278,11 +330,21 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_count(const uint32_t* __re
     }
 }
 
-__global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __restrict__ keys, uint32_t kmask,
+// Range r = blockIdx.y: keys and perm at r * n, the range's offsets' dense
+// rows from nbr + k0 * n, ibase at r * (nb + 1), items from items + 16 k0 nb.
+__global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __restrict__ keys, int Kall, int S,
                                                            const int32_t* __restrict__ perm,
                                                            const int32_t* __restrict__ nbr,
                                                            const int64_t* __restrict__ ibase, int64_t n, int64_t nb,
                                                            int32_t* __restrict__ items) {
+    const int rg = blockIdx.y;
+    const int k0 = range_k0(rg, S);
+    const uint32_t kmask = range_kmask(range_len(rg, S, Kall));
+    keys += (int64_t)rg * n;
+    perm += (int64_t)rg * n;
+    nbr += (int64_t)k0 * n;
+    ibase += (int64_t)rg * (nb + 1);
+    items += (int64_t)k0 * nb * 16;
     const int64_t i = (int64_t)blockIdx.x * kPlanThreads + threadIdx.x;
     const int64_t b = i >> 4;
     const int r = threadIdx.x & 15;
@@ -311,84 +373,103 @@ __global__ void __launch_bounds__(kPlanThreads) k_blk_fill(const uint32_t* __res
     }
 }
 
-// Sets ibase[0] = 0 and clears the look-back status (a plan over no rows).
-__global__ void k_plan_empty(int64_t* ibase, uint32_t* lb_status) {
-    if (threadIdx.x == 0 && blockIdx.x == 0) {
-        ibase[0] = 0;
-        if (lb_status) *lb_status = 0u;
+// Sets each range's ibase[0] = 0 (ibase[r]: nb = 0) and clears the
+// look-back status (a plan over no rows).
+__global__ void k_plan_empty(int64_t* ibase, int R, uint32_t* lb_status) {
+    if (blockIdx.x == 0 && (int)threadIdx.x < R) {
+        ibase[threadIdx.x] = 0;
+        if (lb_status && threadIdx.x == 0) *lb_status = 0u;
     }
 }
 
-// The popcount field of the sort key: as many bits as the last 10-bit digit
-// of the K-bit mask leaves free (at most 6, and within a 32-bit key); its
-// largest value, 0 when there is no room.  K = 27: 3 bits, counts capped at 7.
-static int plan_key_pbits(int K) {
-    const int spare = (K + kRsBits - 1) / kRsBits * kRsBits - K;
-    return std::min(std::min(spare, 32 - K), 6);
-}
-static uint32_t plan_key_cap(int K) { return (1u << plan_key_pbits(K)) - 1u; }
+// The workspace of a plan over n rows in R ranges: keys and values twice,
+// the zeroed counters (digit counts per range and pass, tickets, the first
+// pass's look-back entries), the second look-back array, block item counts,
+// the scan's scratch.
+struct PlanWs {
+    uint32_t *ka, *kb;
+    int32_t *va, *vb;
+    uint32_t *ghist, *ticket, *st0, *st1;
+    int64_t nzero;
+    int32_t* cnt;
+    void* scan_ws;
+    size_t bytes;   // up to here
+};
 
-// lb_status: the plan call's look-back status word, cleared here when
-// clear_status (the call's first range) and set by a pass that gave up.
-static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
-                        int32_t* items, void* ws, uint32_t* lb_status, bool clear_status, int spin_max,
-                        hipStream_t s) {
+static PlanWs plan_ws_layout(void* ws, int64_t n, int R) {
     const int64_t nb = (n + 15) / 16;
     const int64_t nrs = (n + kRsTile - 1) / kRsTile;
-    const int passes = (K + plan_key_pbits(K) + kRsBits - 1) / kRsBits;   // as many as for the mask alone
-    char* w = reinterpret_cast<char*>(ws);
-    uint32_t* ka = reinterpret_cast<uint32_t*>(w);
-    w += al256((size_t)n * sizeof(uint32_t));
-    uint32_t* kb = reinterpret_cast<uint32_t*>(w);
-    w += al256((size_t)n * sizeof(uint32_t));
-    int32_t* va = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)n * sizeof(int32_t));
-    int32_t* vb = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)n * sizeof(int32_t));
-    // zeroed together: digit counts, tickets, the first pass's look-back entries
-    uint32_t* ghist = reinterpret_cast<uint32_t*>(w);
-    uint32_t* ticket = ghist + kRsMaxPasses * kRsBins;
-    uint32_t* st0 = ticket + kRsMaxPasses;
-    const int64_t nzero = kRsMaxPasses * kRsBins + kRsMaxPasses + nrs * kRsBins;
-    w += al256((size_t)nzero * sizeof(uint32_t));
-    uint32_t* st1 = reinterpret_cast<uint32_t*>(w);
-    w += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
-    int32_t* cnt = reinterpret_cast<int32_t*>(w);
-    w += al256((size_t)nb * sizeof(int32_t));
-    void* scan_ws = w;
+    PlanWs L{};
+    char* base = reinterpret_cast<char*>(ws);
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        char* p = base ? base + o : nullptr;
+        o += al256(bytes);
+        return p;
+    };
+    L.ka = reinterpret_cast<uint32_t*>(take((size_t)R * n * sizeof(uint32_t)));
+    L.kb = reinterpret_cast<uint32_t*>(take((size_t)R * n * sizeof(uint32_t)));
+    L.va = reinterpret_cast<int32_t*>(take((size_t)R * n * sizeof(int32_t)));
+    L.vb = reinterpret_cast<int32_t*>(take((size_t)R * n * sizeof(int32_t)));
+    L.nzero = (int64_t)R * kRsMaxPasses * kRsBins + kRsMaxPasses + (int64_t)R * nrs * kRsBins;
+    L.ghist = reinterpret_cast<uint32_t*>(take((size_t)L.nzero * sizeof(uint32_t)));
+    L.ticket = L.ghist ? L.ghist + (int64_t)R * kRsMaxPasses * kRsBins : nullptr;
+    L.st0 = L.ticket ? L.ticket + kRsMaxPasses : nullptr;
+    L.st1 = reinterpret_cast<uint32_t*>(take((size_t)R * nrs * kRsBins * sizeof(uint32_t)));
+    L.cnt = reinterpret_cast<int32_t*>(take((size_t)R * nb * sizeof(int32_t)));
+    L.scan_ws = take(scan_ws_bytes(nb));
+    L.bytes = o;
+    return L;
+}
 
-    uint32_t* lb_clear = clear_status ? lb_status : nullptr;
+// All ranges of a plan (R ranges of S offsets, the last one K - (R-1) S)
+// go through one launch per step: the kernels take the range from the
+// grid's second dimension (the radix passes from the tile's ticket), so a
+// map with more than 32 offsets costs the launches of one plan.  The item
+// counts are scanned per range (ibase restarts at 0 in every range).
+// lb_status: the plan call's look-back status word, cleared by the first
+// kernel and set by a pass that gave up.
+static int plan_enqueue(const int32_t* nbr, int64_t n, int K, int R, int S, int32_t* perm, uint32_t* bmask,
+                        int64_t* ibase, int32_t* items, void* ws, uint32_t* lb_status, int spin_max, hipStream_t s) {
+    const int64_t nb = (n + 15) / 16;
+    const int64_t nrs = (n + kRsTile - 1) / kRsTile;
+    // as many passes as for the widest range's mask alone (the popcount field fills spare bits)
+    const int passes = (S + plan_key_pbits(S) + kRsBits - 1) / kRsBits;
+    const PlanWs L = plan_ws_layout(ws, n, R);
     if (n == 0) {
-        hipLaunchKernelGGL(k_plan_empty, dim3(1), dim3(64), 0, s, ibase, lb_clear);
+        hipLaunchKernelGGL(k_plan_empty, dim3(1), dim3(64), 0, s, ibase, R, lb_status);
         GSC_LAUNCH_CHECK();
         return GSC_OK;
     }
-    const uint32_t kmask = K >= 32 ? ~0u : (1u << K) - 1u;
     const unsigned pblocks = (unsigned)((n + kPlanThreads - 1) / kPlanThreads);
-    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks), dim3(kPlanThreads), 0, s, nbr, n, K, plan_key_cap(K), ka,
-                       ghist, nzero, lb_clear);
+    hipLaunchKernelGGL(k_plan_masks, dim3(pblocks, (unsigned)R), dim3(kPlanThreads), 0, s, nbr, n, K, S, L.ka, L.ghist,
+                       L.nzero, lb_status);
     GSC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, ka, n, passes, ghist);
+    hipLaunchKernelGGL(k_rs_ghist, dim3((unsigned)nrs, (unsigned)R), dim3(kRsThreads), 0, s, L.ka, n, passes, L.ghist);
     GSC_LAUNCH_CHECK();
-    const uint32_t* kin = ka;
+    const uint32_t* kin = L.ka;
     const int32_t* vin = nullptr;
     for (int p = 0; p < passes; ++p) {
-        uint32_t* kout = (p & 1) ? ka : kb;
-        int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? va : vb);
-        uint32_t* st = (p & 1) ? st1 : st0;
-        uint32_t* st_next = (p & 1) ? st0 : st1;
-        hipLaunchKernelGGL(k_rs_pass, dim3((unsigned)nrs), dim3(kRsThreads), 0, s, kin, vin, n, p * kRsBits,
-                           ghist + (int64_t)p * kRsBins, st, st_next, ticket + p, kout, vout, spin_max, lb_status);
+        uint32_t* kout = (p & 1) ? L.ka : L.kb;
+        int32_t* vout = (p == passes - 1) ? perm : ((p & 1) ? L.va : L.vb);
+        uint32_t* st = (p & 1) ? L.st1 : L.st0;
+        uint32_t* st_next = (p & 1) ? L.st0 : L.st1;
+        hipLaunchKernelGGL(k_rs_pass, dim3((unsigned)(nrs * R)), dim3(kRsThreads), 0, s, kin, vin, n, nrs, R,
+                           p * kRsBits, L.ghist + (int64_t)p * kRsBins, st, st_next, L.ticket + p, kout, vout,
+                           spin_max, lb_status);
         GSC_LAUNCH_CHECK();
         kin = kout;
         vin = vout;
     }
-    hipLaunchKernelGGL(k_blk_count, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, kmask, n, nb, bmask, cnt);
+    hipLaunchKernelGGL(k_blk_count, dim3(pblocks, (unsigned)R), dim3(kPlanThreads), 0, s, kin, K, S, n, nb, bmask,
+                       L.cnt);
     GSC_LAUNCH_CHECK();
-    int rc = scan_counts(cnt, nb, ibase, nullptr, scan_ws, s);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks), dim3(kPlanThreads), 0, s, kin, kmask, perm, nbr, ibase, n, nb,
-                       items);
+    for (int r = 0; r < R; ++r) {
+        const int rc = scan_counts(L.cnt + (int64_t)r * nb, nb, ibase + (int64_t)r * (nb + 1), nullptr, L.scan_ws, s);
+        if (rc) return rc;
+    }
+    hipLaunchKernelGGL(k_blk_fill, dim3(pblocks, (unsigned)R), dim3(kPlanThreads), 0, s, kin, K, S, perm, nbr, ibase,
+                       n, nb, items);
     GSC_LAUNCH_CHECK();
     return GSC_OK;
 }
@@ -421,14 +502,7 @@ int32_t gsc_plan_ranges(int32_t K) { return K < 1 || K > kPlanMaxKAll ? 0 : plan
 
 size_t gsc_conv_plan_ws_bytes(int64_t n_out, int32_t K) {
     if (n_out < 0 || n_out > kRsMaxKeys || K < 1 || K > kPlanMaxKAll) return 0;
-    const int64_t nb = (n_out + 15) / 16;
-    const int64_t nrs = (n_out + kRsTile - 1) / kRsTile;
-    size_t b = 4 * al256((size_t)n_out * sizeof(uint32_t));
-    b += al256((size_t)(kRsMaxPasses * kRsBins + kRsMaxPasses + nrs * kRsBins) * sizeof(uint32_t));
-    b += al256((size_t)nrs * kRsBins * sizeof(uint32_t));
-    b += al256((size_t)nb * sizeof(int32_t));
-    b += scan_ws_bytes(nb);
-    return b + 256;
+    return plan_ws_layout(nullptr, n_out, plan_ranges(K)).bytes + 256;
 }
 
 int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, uint32_t* bmask, int64_t* ibase,
@@ -446,20 +520,9 @@ int gsc_conv_plan(const int32_t* nbr, int64_t n_out, int32_t K, int32_t* perm, u
                     (long long)need_items);
     const size_t need = gsc_conv_plan_ws_bytes(n_out, K);
     if (ws_bytes < need) return fail(GSC_ESHORT, "conv_plan: ws needs %zu bytes, got %zu", need, ws_bytes);
-    // one plan per range of offsets, one after another on the stream (they share ws)
-    const int R = plan_ranges(K), S = plan_range_size(K);
-    const int64_t nb = gsc_plan_blocks(n_out);
-    uint32_t* lb_status = plan_status_word(ws, n_out, K);
-    const int spin_max = lookback_spin_limit();
-    for (int r = 0; r < R; ++r) {
-        const int k0 = r * S, kr = K - k0 < S ? K - k0 : S;
-        const int rc = plan_enqueue(nbr ? nbr + (int64_t)k0 * n_out : nullptr, n_out, kr,
-                                    perm ? perm + (int64_t)r * n_out : nullptr, bmask ? bmask + (int64_t)r * nb : nullptr,
-                                    ibase + (int64_t)r * (nb + 1), items ? items + (int64_t)k0 * nb * 16 : nullptr, ws,
-                                    lb_status, r == 0, spin_max, reinterpret_cast<hipStream_t>(stream));
-        if (rc) return rc;
-    }
-    return GSC_OK;
+    // every range of offsets in the same launches
+    return plan_enqueue(nbr, n_out, K, plan_ranges(K), plan_range_size(K), perm, bmask, ibase, items, ws,
+                        plan_status_word(ws, n_out, K), lookback_spin_limit(), reinterpret_cast<hipStream_t>(stream));
 }
 
 int gsc_conv_plan_status(const void* ws, size_t ws_bytes, int64_t n_out, int32_t K, void* stream) {
