@@ -612,9 +612,9 @@ k_dw_f32(const float* __restrict__ X, int64_t n_in, const float* __restrict__ dY
 
 // dW[k] = sum of offset k's partials in a fixed order.  A block covers 64 V
 // elements of one offset (V = 4: a 16-byte load per lane, for wide layers
-// with ci * co a multiple of 4 and dW 16-byte aligned); wave w adds partials w, w + 4, w + 8,
-// ... with eight loads in flight, and the four wave sums are combined in wave
-// order.
+// with ci * co a multiple of 4 and dW 16-byte aligned); wave w adds partials
+// w, w + 4, w + 8, ... with eight loads in flight, and the four wave sums are
+// combined in wave order.
 template <int V>
 __global__ void __launch_bounds__(kThreads) k_dw_reduce(const float* __restrict__ part, const int64_t* __restrict__ ibase,
                                                         int ci, int co, float* __restrict__ dW) {

@@ -29,8 +29,9 @@
 // The grid is persistent (one workgroup per CU) and takes tiles from the
 // last to the first through a counter in device memory: tiles later in the
 // plan hold rows with more neighbours (the plan sorts rows by neighbour
-// mask), so the large tiles go out first and the small ones fill the gaps.
-// Without a counter the workgroups take tiles nt-1-g, nt-1-g-G, ... .
+// count, then mask), so the large tiles go out first and the small ones fill
+// the gaps.  Without a counter the workgroups take tiles nt-1-g, nt-1-g-G,
+// ... .
 //
 // LDS layout of a stage: block b's rows at b * 1 KiB, row r's 64 bytes at
 // r * 64 with 16-byte chunk c at ((c ^ ((r >> 1) & 3)) * 16); output column
