@@ -387,14 +387,16 @@ def _check_plan_range(n, nbr, perm, bm, ib, items):
         below += (bm >> k) & 1
 
 
-def test_plan_lookback_give_up_is_reported(monkeypatch):
+@pytest.mark.parametrize("D", [3, 4])
+def test_plan_lookback_give_up_is_reported(monkeypatch, D):
     """A sort pass whose look-back gives up (forced from the host: the
     environment's spin limit makes every poll give up at once) finishes
     normally and the plan call's status reports ETIMEOUT; with the normal
-    bound the same buffers give a valid plan and status OK."""
-    coords = WL.random_coords(175, 24000, 3, -25, 25, batch=2)   # about a dozen sort tiles
+    bound the same buffers give a valid plan and status OK.  D = 4: the 81
+    offsets of the tesseract, three plan ranges sorted in the same launches."""
+    coords = WL.random_coords(175, 24000, D, -25 if D == 3 else -10, 25 if D == 3 else 10, batch=2)
     c = _t(coords)
-    offs = regions.hypercube(3, 3)
+    offs = regions.hypercube(3, D)
     km = gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, offs, dense=True)
     bufs = gsc.PlanBuffers(km.n_out, km.K, DEV)
     _say(f"[gpu] look-back give-up forced on n={km.n_out}")
