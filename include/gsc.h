@@ -91,8 +91,10 @@ size_t gsc_table_bytes(int64_t n);
  * table_bytes >= gsc_table_bytes(n)).  The table maps each row's coordinate to
  * its row index.  Synchronises `stream` once to read the device status.
  * Errors: EINVAL, ESHORT (table_bytes too small), ERANGE (bounding box needs
- * more than 62 key bits), EDUP (a repeated row), EFULL, EHIP.  n == 0 builds an
- * empty table. */
+ * more than 62 key bits), EDUP (a repeated row), EFULL (no free slot: not
+ * reached at the table's load factor of at most 1/4; the environment variable
+ * GSC_TABLE_CAP_LIMIT, a test hook read by gsc_table_bytes and the builds,
+ * caps the slot count to force it), EHIP.  n == 0 builds an empty table. */
 int gsc_coords_build(const int32_t* coords, int64_t n, int32_t D,
                      void* table, size_t table_bytes, void* stream);
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdlib>
 #include <cstddef>
 
 #include "../../include/gsc.h"
@@ -65,10 +66,18 @@ struct alignas(16) Slot {
 };
 static_assert(sizeof(Slot) == 16, "slot must be 16 bytes");
 
-// capacity: a power of two >= 4n (load factor <= 1/4) and >= 64
+// capacity: a power of two >= 4n (load factor <= 1/4) and >= 64.  The
+// environment variable GSC_TABLE_CAP_LIMIT (a test hook) caps it at the
+// largest power of two >= 64 not above its value, so that a table too small
+// for its rows, and the EFULL it reports, can be exercised; every insert and
+// query still stops after one pass over the slots.
 inline int64_t table_capacity(int64_t n) {
     int64_t cap = 64;
     while (cap < 4 * n) cap <<= 1;
+    if (const char* e = getenv("GSC_TABLE_CAP_LIMIT")) {
+        const long long lim = strtoll(e, nullptr, 10);
+        while (cap > 64 && cap > lim) cap >>= 1;
+    }
     return cap;
 }
 

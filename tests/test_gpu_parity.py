@@ -242,6 +242,28 @@ def test_duplicate_rejected():
     assert e.value.code == gsc.GSC_EDUP
 
 
+def test_table_full_reported(monkeypatch):
+    """A table too small for its rows (its capacity capped from the host
+    through the GSC_TABLE_CAP_LIMIT hook: 64 slots for 200 rows) reports
+    EFULL; every insert's probe ends after one pass over the slots, and a
+    kernel map queried from the failed table comes out empty (asynchronous)
+    or reports it (synchronous)."""
+    coords = _t(WL.random_coords(177, 200, 3, -20, 20, batch=1))
+    monkeypatch.setenv("GSC_TABLE_CAP_LIMIT", "64")
+    assert gsc.gsc_table_bytes(200) == gsc.gsc_table_bytes(1)   # 64 slots: the cap is in force
+    with pytest.raises(gsc.GscError) as e:
+        gsc.gsc_coords_build(coords)
+    assert e.value.code == gsc.GSC_EFULL
+    table = gsc.gsc_coords_build(coords, sync=False)
+    km = gsc.gsc_kernel_map(table, coords, regions.hypercube(3, 3), sync=False)
+    assert km.count() == 0
+    with pytest.raises(gsc.GscError) as e:   # the synchronous map reports the invalid table
+        gsc.gsc_kernel_map(table, coords, regions.hypercube(3, 3))
+    assert e.value.code == gsc.GSC_EINVAL
+    monkeypatch.delenv("GSC_TABLE_CAP_LIMIT")
+    gsc.gsc_table_status(gsc.gsc_coords_build(coords))   # the normal capacity holds them
+
+
 def test_key_range_rejected():
     # 8 columns each spanning 2^9 values need 72 key bits
     rows = np.zeros((2, 8), np.int32)
