@@ -288,26 +288,26 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                 d.vr[j] = has && r >= 0 && r < n_x ? (uint32_t)r * (uint32_t)(CA * 2) + lchunk : kTileNone;
             }
         };
-        // copies of part h of offset state d into stage P (C::LOADS instructions per wave, always)
+        // copies of part h of offset state d into stage P: C::LOADS
+        // instructions per wave, always; copy p < BL is weight instruction p,
+        // the others the rows of the two blocks this wave copies
+        auto issue_one = [&](const OffState& d, int h, auto P, int p) {
+            if (p < C::BL) {
+                const int ins = wave * C::BL + p;
+                const uint32_t off = d.k >= 0 ? bcol[p] : kTileNone;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    wrs, (__attribute__((address_space(3))) void*)(ins < C::BINS ? stage_b(P) + ins * 1024 : sdummy),
+                    16, off, d.wb + (uint32_t)(h * 64), 0, 0);
+            } else {
+                const int j = p - C::BL;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    xr, (__attribute__((address_space(3))) void*)(stage_a(P) + (wave + 8 * j) * 1024), 16, d.vr[j],
+                    h * 64, 0, 0);
+            }
+        };
         auto issue = [&](const OffState& d, int h, auto P) {
-            uint8_t* sa = stage_a(P);
-            uint8_t* sb = stage_b(P);
-            const bool valid = d.k >= 0;
-            const uint32_t wbase = d.wb + (uint32_t)(h * 64);
 #pragma unroll
-            for (int i = 0; i < C::BL; ++i) {
-                const int ins = wave * C::BL + i;
-                const uint32_t off = valid ? bcol[i] : kTileNone;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    wrs, (__attribute__((address_space(3))) void*)(ins < C::BINS ? sb + ins * 1024 : sdummy), 16, off,
-                    wbase, 0, 0);
-            }
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const uint32_t off = d.vr[j];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    xr, (__attribute__((address_space(3))) void*)(sa + (wave + 8 * j) * 1024), 16, off, h * 64, 0, 0);
-            }
+            for (int p = 0; p < C::LOADS; ++p) issue_one(d, h, P, p);
         };
 
         floatx4 acc[C::BPW][C::NJ];
@@ -369,12 +369,21 @@ k_conv_tile_bf16(const uint16_t* __restrict__ X, int64_t n_x, const uint16_t* __
                 asm volatile("" : "+s"(bn));
 #pragma unroll
                 for (int b = 0; b < C::BPW; ++b) {
-                    if (b == C::BPW / 2) {
-                        if constexpr (ahead_here)
-                            issue(dc[ja / H], ja % H, std::integral_constant<int, st>{});
-                        else
-                            issue(dn[ja / H], ja % H, std::integral_constant<int, st>{});
-                        if constexpr (j == 1) {
+                    // the copies go out spread over the products (copy p
+                    // before block p * BPW / LOADS: issued together they
+                    // queue at the vector memory unit and hold up every
+                    // wave's products at once)
+#pragma unroll
+                    for (int p = 0; p < C::LOADS; ++p) {
+                        if ((p * C::BPW) / C::LOADS == b) {
+                            if constexpr (ahead_here)
+                                issue_one(dc[ja / H], ja % H, std::integral_constant<int, st>{}, p);
+                            else
+                                issue_one(dn[ja / H], ja % H, std::integral_constant<int, st>{}, p);
+                        }
+                    }
+                    if constexpr (j == 1) {
+                        if (b == C::BPW / 2) {
 #pragma unroll
                             for (int o = 0; o < NO; ++o) take_offset(dnn[o]);
                         }
