@@ -46,7 +46,7 @@ int conv_blk_bf16(int ca, int cb, const void* X, int64_t n_x, const void* Bt, co
                   const BlockPlan& plan, int64_t n_y, void* Y, hipStream_t s, const Epilogue& ep = Epilogue{});
 
 // The bf16 tile engine (conv_tile.hip): the same product as conv_blk_bf16
-// for ca, cb in {64, 128, 256}, K <= 30, a tile of 16 blocks by all cb
+// for ca, cb in {64, 128, 256}, K <= 29, a tile of 16 blocks by all cb
 // columns per workgroup, persistent workgroups.  nb = number of plan blocks;
 // counter (nullable): 4 bytes of device memory the call uses to hand out
 // tiles (large ones first; without it the tiles go out in a fixed order),

@@ -56,7 +56,7 @@ constexpr int kTileBlocks = 16;                         // blocks (of 16 positio
 constexpr int kTilePos = kTileBlocks * kPlanBlockRows;  // 256 positions
 constexpr int kTileThreads = 512;                       // eight waves
 constexpr int kTileStageBytes = 16384;                  // rows of a stage; weights of a stage at most as much
-constexpr int kTileMaxK = 30;                           // item table in the LDS left by the stages
+constexpr int kTileMaxK = 29;                           // item table in the LDS left by the stages (29 KiB)
 constexpr int kTileBufFlags = 0x00020000;               // buffer descriptor word 3: 32-bit data format
 constexpr uint32_t kTileNone = 0x80000000u;             // an offset past any buffer the engine reads
 

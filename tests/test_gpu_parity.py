@@ -524,6 +524,19 @@ def test_block_engine_bf16(ci, co, region):
     _plan_case(coords, ci, co, regions.hypercube(int(region[-1]), 3), 141, dtype="bf16")
 
 
+@pytest.mark.parametrize("K", [29, 30, 32])
+def test_block_engine_bf16_offset_limit(K):
+    # the tile engine at its largest region (29 offsets: its item table fills
+    # the LDS left by the stages) and the regions past it (30 and 32 offsets,
+    # on the 16-block bf16 engine)
+    extra = np.array([[2, 0, 0], [-2, 0, 0], [0, 2, 0], [0, -2, 0], [0, 0, 2]], np.int32)
+    offs = np.concatenate([regions.hypercube(3, 3), extra[:K - 27]]).astype(np.int32)
+    assert len(offs) == K and gsc.gsc_conv_block_engine(gsc.GSC_BF16, 256, 256, K)
+    coords = WL.random_coords(150 + K, 1500, 3, -9, 9, batch=2)
+    _say(f"[gpu] bf16 block engines 256->256, {K} offsets")
+    _plan_case(coords, 256, 256, offs, 151, dtype="bf16")
+
+
 def test_block_engine_edges():
     # one voxel, a ragged last block, no input rows, 4D hybrid region
     _plan_case(np.array([[0, -7, 3, 11]], np.int32), 16, 32, regions.hypercube(3, 3), 131)
