@@ -59,7 +59,7 @@ typedef enum {
     GSC_OK = 0,
     GSC_EINVAL = -1,  /* invalid argument (null pointer, negative size, bad D, ...) */
     GSC_ESHORT = -2,  /* caller buffer too small; the required size is returned   */
-    GSC_ERANGE = -3,  /* coordinates span more than 62 bits of packed key          */
+    GSC_ERANGE = -3,  /* coordinates span more than 92 bits of packed key          */
     GSC_EDUP = -4,    /* a coordinate row occurs twice                             */
     GSC_EFULL = -5,   /* hash table has no free slot                               */
     GSC_EHIP = -6,    /* a HIP runtime call failed                                 */
@@ -80,9 +80,13 @@ int gsc_abi_version(void);
 /* ------------------------------------------------------------------------ */
 /* Bytes of a table for n coordinates: a 256-byte header (key packing,
  * bounding box, status) followed by a power-of-two number (>= 4n, >= 64) of
- * 16-byte slots {uint64 key, int32 row, int32 pad}.  Open addressing with
- * linear probing; the key is the row packed into <= 62 bits relative to the
- * bounding box of the coordinates (batch column most significant).  The home
+ * 16-byte slots {uint64 key, int32 row, int32 hi}.  Open addressing with
+ * linear probing; the key is the row packed into <= 92 bits relative to the
+ * bounding box of the coordinates (batch column most significant): up to 62
+ * bits in `key` alone, a wider key with its low 62 bits in `key` and the rest
+ * in `hi` (an insert claims a slot by an atomic compare-and-swap on `key`
+ * and then writes `hi`; an insert meeting the same low bits waits for that
+ * write, boundedly: past the bound the build reports EFULL).  The home
  * slot keeps each 2 x 2 x 2 block of neighbouring coordinates in one 128-byte
  * line of slots, so a neighbourhood query touches few lines. */
 size_t gsc_table_bytes(int64_t n);
@@ -91,7 +95,7 @@ size_t gsc_table_bytes(int64_t n);
  * table_bytes >= gsc_table_bytes(n)).  The table maps each row's coordinate to
  * its row index.  Synchronises `stream` once to read the device status.
  * Errors: EINVAL, ESHORT (table_bytes too small), ERANGE (bounding box needs
- * more than 62 key bits), EDUP (a repeated row), EFULL (no free slot: not
+ * more than 92 key bits), EDUP (a repeated row), EFULL (no free slot: not
  * reached at the table's load factor of at most 1/4; the environment variable
  * GSC_TABLE_CAP_LIMIT, a test hook read by gsc_table_bytes and the builds,
  * caps the slot count to force it), EHIP.  n == 0 builds an empty table. */
@@ -151,7 +155,7 @@ size_t gsc_quantize_ws_bytes(int64_t n, int32_t D);
  * (>= gsc_table_bytes(n) bytes) receives the hash table of the voxel
  * coordinates, usable by gsc_kernel_map.  Synchronises `stream` once.
  * Errors: EINVAL, ESHORT, ERANGE (a coordinate outside +-2^30, or a box needing
- * more than 62 key bits), EHIP. */
+ * more than 92 key bits), EHIP. */
 int gsc_quantize(const float* points, const int32_t* batch, int64_t n, int32_t D, const float* voxel,
                  const int32_t* labels, int32_t ignore_label, int32_t* out_coords, int64_t* n_out, int32_t* rep,
                  int32_t* out_labels, int32_t* inverse, void* out_table, size_t out_table_bytes,

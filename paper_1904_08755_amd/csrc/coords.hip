@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(kThreads) k_table_init(TableHeader* h, Slot* s
         Slot e;
         e.key = kEmptyKey;
         e.val = init_val;
-        e.pad = 0;
+        e.hi = kHiUnset;
         slots[i] = e;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -207,6 +207,61 @@ __device__ __forceinline__ bool block_key_view(TableHeader* h, int ncol, KeyLayo
     return kl_s->total_bits <= kMaxKeyBits;
 }
 
+// Wide keys: the CAS claims a slot by the key's low 62 bits and the claiming
+// thread then writes the high bits into Slot::hi.  A thread that meets the
+// same low bits reads Slot::hi, and while it is still unset it polls the same
+// slot again: the writer has claimed it and stores right after.  The claim's
+// store comes before any comparison in every round, so a writer in the same
+// wave has stored before its neighbours look.  Rounds end when the key is
+// placed, found (and_found: what to do then) or the table is walked through;
+// a slot whose high bits stay unset past kWidePolls polls ends with ST_FULL.
+constexpr int kWidePolls = 1 << 22;
+
+// One round of a wide find-or-insert at slot s: returns 1 placed (this thread
+// claimed the slot), 2 found (the slot holds the key), 3 retry the same slot,
+// 0 move on.
+__device__ __forceinline__ int wide_round(Slot* slots, unsigned long long s, unsigned long long lo, int32_t hi) {
+    const unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, lo);
+    const bool won = prev == kEmptyKey;
+    if (won) __hip_atomic_store(&slots[s].hi, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (won) return 1;
+    if (prev != lo) return 0;
+    const int32_t h2 = __hip_atomic_load(&slots[s].hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return h2 == kHiUnset ? 3 : (h2 == hi ? 2 : 0);
+}
+
+// a row of a table with wide keys (k_insert)
+__device__ void insert_wide(const TableView& tv, const int64_t* v, int64_t r, TableHeader* h, Slot* slots) {
+    u128 key;
+    if (!pack_key_wide(tv, v, &key)) {   // cannot happen: the box holds every row
+        atomicOr(&h->status, ST_RANGE);
+        return;
+    }
+    const unsigned long long lo = wide_lo(key), mask = tv.sh.mask;
+    const int32_t hi = wide_hi(key);
+    unsigned long long s = home_slot_wide(tv.sh, key);
+    int polls = 0;
+    for (unsigned long long i = 0; i <= mask;) {
+        const int res = wide_round(slots, s, lo, hi);
+        if (res == 1) {
+            slots[s].val = (int32_t)r;
+            return;
+        }
+        if (res == 2) {
+            atomicOr(&h->status, ST_DUP);
+            return;
+        }
+        if (res == 3) {
+            if (++polls > kWidePolls) break;
+            continue;
+        }
+        s = (s + 1) & mask;
+        ++i;
+    }
+    atomicOr(&h->status, ST_FULL);
+}
+
 __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int64_t n, TableHeader* h,
                                                      Slot* slots) {
     __shared__ KeyLayout kl_s;
@@ -220,6 +275,10 @@ __global__ void __launch_bounds__(kThreads) k_insert(const int32_t* coords, int6
     int64_t v[kMaxCols];
     StrideArg none{};
     load_row(coords, r, ncol, none, v);
+    if (kl_s.total_bits > kNarrowKeyBits) {   // uniform
+        insert_wide(tv, v, r, h, slots);
+        return;
+    }
     unsigned long long key;
     if (!pack_key(tv, v, &key)) {  // cannot happen: the box holds every row
         atomicOr(&h->status, ST_RANGE);
@@ -260,12 +319,21 @@ __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, 
         return;
     }
     const unsigned long long mask = tv.sh.mask;
-    unsigned long long key = 0;
+    const bool wide = kl_s.total_bits > kNarrowKeyBits;   // uniform
+    unsigned long long key = 0;   // a narrow key, or a wide key's low 62 bits
+    int32_t khi = 0;              // a wide key's high bits
+    u128 wkey = 0;
     bool ok = false;
     if (valid) {
         int64_t v[kMaxCols];
         load_row(coords, r, ncol, st, v);
-        ok = pack_key(tv, v, &key);
+        if (wide) {
+            ok = pack_key_wide(tv, v, &wkey);
+            key = wide_lo(wkey);
+            khi = wide_hi(wkey);
+        } else {
+            ok = pack_key(tv, v, &key);
+        }
         if (!ok) {
             atomicOr(&h->status, ST_RANGE);
             slot_of[r] = 0;
@@ -273,21 +341,41 @@ __global__ void __launch_bounds__(kThreads) k_insert_min(const int32_t* coords, 
     }
     const int lane = __lane_id();
     const unsigned long long pkey = __shfl_up(key, 1, 64);
+    const int32_t phi = __shfl_up(khi, 1, 64);
     const bool pok = __shfl_up((int)ok, 1, 64) != 0;
-    const bool follower = ok && lane > 0 && pok && pkey == key;
+    const bool follower = ok && lane > 0 && pok && pkey == key && phi == khi;
     const unsigned long long leaders = __ballot(ok && !follower);
     unsigned long long s = 0;
     if (ok && !follower) {
-        s = home_slot(tv.sh, key);
         bool placed = false;
-        for (unsigned long long i = 0; i <= mask; ++i) {
-            const unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
-            if (prev == kEmptyKey || prev == key) {
-                atomicMin(&slots[s].val, (int32_t)r);
-                placed = true;
-                break;
+        if (wide) {   // see insert_wide
+            s = home_slot_wide(tv.sh, wkey);
+            int polls = 0;
+            for (unsigned long long i = 0; i <= mask;) {
+                const int res = wide_round(slots, s, key, khi);
+                if (res == 1 || res == 2) {
+                    atomicMin(&slots[s].val, (int32_t)r);
+                    placed = true;
+                    break;
+                }
+                if (res == 3) {
+                    if (++polls > kWidePolls) break;
+                    continue;
+                }
+                s = (s + 1) & mask;
+                ++i;
             }
-            s = (s + 1) & mask;
+        } else {
+            s = home_slot(tv.sh, key);
+            for (unsigned long long i = 0; i <= mask; ++i) {
+                const unsigned long long prev = atomicCAS(&slots[s].key, kEmptyKey, key);
+                if (prev == kEmptyKey || prev == key) {
+                    atomicMin(&slots[s].val, (int32_t)r);
+                    placed = true;
+                    break;
+                }
+                s = (s + 1) & mask;
+            }
         }
         if (!placed) {
             atomicOr(&h->status, ST_FULL);

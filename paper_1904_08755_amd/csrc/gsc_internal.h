@@ -35,10 +35,17 @@ void clear_error();
 // coordinate hash table (lives in caller memory)
 // ---------------------------------------------------------------------------
 constexpr int kMaxCols = 8;                       // 1 batch column + up to 7 spatial
-constexpr unsigned long long kEmptyKey = ~0ull;    // packed keys use <= 62 bits
+constexpr unsigned long long kEmptyKey = ~0ull;    // Slot::key holds <= 62 key bits
 constexpr uint32_t kTableMagic = 0x54435347u;      // "GSCT"
 constexpr size_t kHeaderBytes = 256;
-constexpr int kMaxKeyBits = 62;
+// A packed key of up to kNarrowKeyBits bits lives in Slot::key alone; a wider
+// one (up to kMaxKeyBits) keeps its low 62 bits there and the rest in
+// Slot::hi, which the inserting thread writes right after claiming the slot
+// (kHiUnset until then).
+constexpr int kNarrowKeyBits = 62;
+constexpr int kMaxKeyBits = 92;
+constexpr int32_t kHiUnset = -1;
+typedef unsigned __int128 u128;
 
 enum : int { ST_DUP = 1, ST_FULL = 2, ST_RANGE = 4 };
 
@@ -62,7 +69,7 @@ static_assert(sizeof(TableHeader) <= kHeaderBytes, "header too large");
 struct alignas(16) Slot {
     unsigned long long key;
     int32_t val;
-    int32_t pad;
+    int32_t hi;   // key bits 62 and up of a wide key
 };
 static_assert(sizeof(Slot) == 16, "slot must be 16 bytes");
 
@@ -103,19 +110,14 @@ __device__ __forceinline__ uint32_t hash_key(unsigned long long k) {
     return fmix32((uint32_t)k ^ ((uint32_t)(k >> 32) * 0x9e3779b1u));
 }
 
-// Pack a coordinate (already offset, in 64-bit) into a key.  Returns false if
-// it lies outside the table's bounding box: such a coordinate cannot be in
-// the table, so a query for it is a miss (never an alias of another key).
-__device__ __forceinline__ bool pack_key(const TableHeader* h, int ncol, const int64_t* v,
-                                         unsigned long long* key) {
-    unsigned long long k = 0;
-    for (int c = 0; c < ncol; ++c) {
-        if (v[c] < h->lo[c] || v[c] > h->hi[c]) return false;
-        k |= (unsigned long long)(v[c] - h->lo[c]) << h->shift[c];
-    }
-    *key = k;
-    return true;
+// Hash of a wide key: its high word folded into the low one, then hash_key.
+__device__ __forceinline__ uint32_t hash_key_wide(u128 k) {
+    return hash_key((unsigned long long)k ^ ((unsigned long long)(k >> 64) * 0x9e3779b97f4a7c15ull));
 }
+__device__ __forceinline__ unsigned long long wide_lo(u128 k) {
+    return (unsigned long long)k & ((1ull << kNarrowKeyBits) - 1ull);
+}
+__device__ __forceinline__ int32_t wide_hi(u128 k) { return (int32_t)(uint32_t)(k >> kNarrowKeyBits); }
 
 // Home slot of a key.  The lowest varying bit of each of the first (up to)
 // three spatial columns (bit 0 for unit tensor stride, bit 1 for coordinates
@@ -149,11 +151,18 @@ __device__ __forceinline__ unsigned long long home_slot(const SlotHash& sh, unsi
     return (((unsigned long long)hash_key(bkey) << sh.nblk) | local) & sh.mask;
 }
 
-__device__ __forceinline__ unsigned long long home_slot(const TableHeader* h, unsigned long long key,
-                                                        unsigned long long mask) {
-    SlotHash sh = slot_hash(h);
-    sh.mask = mask;
-    return home_slot(sh, key);
+// the same for a wide key (blocked bits, then hash_key_wide of the rest)
+__device__ __forceinline__ unsigned long long home_slot_wide(const SlotHash& sh, u128 key) {
+    unsigned long long local = 0;
+    u128 bkey = key;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        if (i < sh.nblk) {
+            local |= (unsigned long long)((key >> sh.blk_shift[i]) & 1u) << i;
+            bkey &= ~((u128)1 << sh.blk_shift[i]);
+        }
+    }
+    return (((unsigned long long)hash_key_wide(bkey) << sh.nblk) | local) & sh.mask;
 }
 
 // Register copy of the fields a query needs: loaded once per thread, so that
@@ -177,7 +186,10 @@ __device__ __forceinline__ TableView table_view(const TableHeader* h, int ncol) 
     return t;
 }
 
-// (unrolled over kMaxCols with a guard, so the arrays stay in registers)
+// Pack a coordinate (already offset, in 64-bit) into a key; false if it lies
+// outside the table's bounding box (such a coordinate cannot be in the table,
+// so a query for it is a miss, never an alias of another key).  Unrolled
+// over kMaxCols with a guard, so the arrays stay in registers.
 __device__ __forceinline__ bool pack_key(const TableView& t, const int64_t* v, unsigned long long* key) {
     unsigned long long k = 0;
     bool in = true;
@@ -192,26 +204,19 @@ __device__ __forceinline__ bool pack_key(const TableView& t, const int64_t* v, u
     return in;
 }
 
-// Linear-probing lookup from slot s; at most `capacity` probes, so it ends
-// even on a table left full by a failed build.
-__device__ __forceinline__ int32_t table_find_from(const Slot* slots, unsigned long long mask,
-                                                   unsigned long long key, unsigned long long s) {
-    for (unsigned long long i = 0; i <= mask; ++i) {
-        const Slot e = slots[s];
-        if (e.key == key) return e.val;
-        if (e.key == kEmptyKey) return -1;
-        s = (s + 1) & mask;
+// the same for a wide key
+__device__ __forceinline__ bool pack_key_wide(const TableView& t, const int64_t* v, u128* key) {
+    u128 k = 0;
+    bool in = true;
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c) {
+        if (c < t.ncol) {
+            in = in && v[c] >= t.lo[c] && v[c] <= t.hi[c];
+            k |= (u128)(unsigned long long)(v[c] - t.lo[c]) << t.shift[c];
+        }
     }
-    return -1;
-}
-
-__device__ __forceinline__ int32_t table_find(const TableHeader* h, const Slot* slots, unsigned long long mask,
-                                              unsigned long long key) {
-    return table_find_from(slots, mask, key, home_slot(h, key, mask));
-}
-
-__device__ __forceinline__ int32_t table_find(const TableView& t, const Slot* slots, unsigned long long key) {
-    return table_find_from(slots, t.sh.mask, key, home_slot(t.sh, key));
+    *key = k;
+    return in;
 }
 
 // floor(a / s) * s for s > 0

@@ -54,41 +54,38 @@ __device__ __forceinline__ bool header_ok(const TableHeader* h, int ncol) {
     return h->magic == kTableMagic && h->ncol == ncol && h->status == 0;
 }
 
-// Key of u + off; false if it lies outside the table's bounding box (a miss).
-__device__ __forceinline__ bool query_key(const TableHeader* h, int ncol, const int64_t* u, const int32_t* off,
-                                          unsigned long long* key) {
-    int64_t q[kMaxCols];
-    q[0] = u[0];
-    for (int c = 1; c < ncol; ++c) q[c] = u[c] + off[c - 1];
-    return pack_key(h, ncol, q, key);
-}
-
 constexpr int kBatch = 4;   // probes issued together per lane in the count pass (4 measured faster than 8 or 16)
+// ... for wide keys: two, so that their path needs no more registers than the others
+template <typename KeyT>
+constexpr int batch_of() { return sizeof(KeyT) > 8 ? 1 : kBatch; }
 
 // Key arithmetic in KeyT (uint32_t when the table's keys fit in 32 bits, the
-// usual case, else uint64_t).  The packed key is linear in the coordinate:
-// key(u + o) = base(u) + delta(o), exact (mod 2^bits) whenever every column of
-// u + o lies in the table's box, so a probe is a range check per column and
-// one add.
+// usual case, uint64_t up to 62 bits, else the 128-bit wide key).  The packed
+// key is linear in the coordinate: key(u + o) = base(u) + delta(o), exact (mod
+// 2^bits) whenever every column of u + o lies in the table's box, so a probe
+// is a range check per column and one add.
 template <typename KeyT>
 struct KeyOps;
 
 template <>
 struct KeyOps<uint32_t> {
     static __device__ __forceinline__ uint32_t hash(uint32_t k) { return fmix32(k); }
-    static __device__ __forceinline__ bool eq(unsigned long long slot_key, uint32_t k) {
-        return slot_key == (unsigned long long)k;
-    }
+    static __device__ __forceinline__ bool eq(const Slot& e, uint32_t k) { return e.key == (unsigned long long)k; }
 };
 template <>
 struct KeyOps<unsigned long long> {
     static __device__ __forceinline__ uint32_t hash(unsigned long long k) { return hash_key(k); }
-    static __device__ __forceinline__ bool eq(unsigned long long slot_key, unsigned long long k) { return slot_key == k; }
+    static __device__ __forceinline__ bool eq(const Slot& e, unsigned long long k) { return e.key == k; }
+};
+template <>
+struct KeyOps<u128> {
+    static __device__ __forceinline__ uint32_t hash(u128 k) { return hash_key_wide(k); }
+    static __device__ __forceinline__ bool eq(const Slot& e, u128 k) { return e.key == wide_lo(k) && e.hi == wide_hi(k); }
 };
 
-// Count pass.  Each lane owns one output row.  Offsets are probed kBatch at a
+// Count pass.  Each lane owns one output row.  Offsets are probed NB at a
 // time; every load is issued unconditionally (a lane whose query is out of
-// the box reads slot 0 and ignores it) so the kBatch loads are in flight
+// the box reads slot 0 and ignores it) so the NB loads are in flight
 // together, and collision chains are followed in rounds.  A probe reads the
 // whole 16-byte slot, so a hit also yields the input row, which goes to
 // nbr[k * n_out + j] (-1 for a miss); hits are counted per 64-row group with
@@ -124,7 +121,7 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
             base += (KeyT)(uint32_t)rel[c] << shc[c];    // (KeyT)(int) sign-extends for 64-bit keys below
         }
     }
-    if (sizeof(KeyT) == 8) {   // redo with sign extension: rel may be negative when u is outside the box
+    if (sizeof(KeyT) >= 8) {   // redo with sign extension: rel may be negative when u is outside the box
         base = 0;
 #pragma unroll
         for (int c = 0; c < kMaxCols; ++c)
@@ -133,13 +130,14 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
     in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    for (int k0 = k_begin; k0 < k_end; k0 += kBatch) {
-        KeyT key[kBatch];
-        unsigned long long pos[kBatch];
-        bool pend[kBatch], hit[kBatch];
-        int32_t row[kBatch];
+    constexpr int NB = batch_of<KeyT>();
+    for (int k0 = k_begin; k0 < k_end; k0 += NB) {
+        KeyT key[NB];
+        unsigned long long pos[NB];
+        bool pend[NB], hit[NB];
+        int32_t row[NB];
 #pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
+        for (int b = 0; b < NB; ++b) {
             const int k = min(k0 + b, k_end - 1);
             const int32_t* o = offs.at((int64_t)k * D);
             bool in = in_b && k0 + b < k_end;
@@ -165,22 +163,23 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
             row[b] = -1;
         }
         for (unsigned long long round = 0; round <= mask; ++round) {
-            Slot e[kBatch];
+            Slot e[NB];
             if (round == 0) {
 #pragma unroll
-                for (int b = 0; b < kBatch; ++b) e[b] = slots[pos[b]];   // unconditional: all in flight
+                for (int b = 0; b < NB; ++b) e[b] = slots[pos[b]];   // unconditional: all in flight
             } else {   // collision chains: few probes still pending
 #pragma unroll
-                for (int b = 0; b < kBatch; ++b) {
+                for (int b = 0; b < NB; ++b) {
                     e[b].key = kEmptyKey;
                     e[b].val = -1;
+                    e[b].hi = kHiUnset;
                     if (pend[b]) e[b] = slots[pos[b]];
                 }
             }
             bool any = false;
 #pragma unroll
-            for (int b = 0; b < kBatch; ++b) {
-                const bool h1 = pend[b] && KeyOps<KeyT>::eq(e[b].key, key[b]);
+            for (int b = 0; b < NB; ++b) {
+                const bool h1 = pend[b] && KeyOps<KeyT>::eq(e[b], key[b]);
                 const bool stop = h1 || e[b].key == kEmptyKey;
                 hit[b] = hit[b] || h1;
                 row[b] = h1 ? e[b].val : row[b];
@@ -191,7 +190,7 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
             if (!__any(any)) break;
         }
 #pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
+        for (int b = 0; b < NB; ++b) {
             const int k = k0 + b;
             if (k < k_end) {
                 const unsigned long long m = __ballot(hit[b]);
@@ -234,9 +233,12 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
     if (h->total_bits <= 32)   // uniform: all lanes take the same path
         count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok,
                              j, not_self);
-    else
+    else if (h->total_bits <= kNarrowKeyBits)
         count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt,
                                        nbr, ok, j, not_self);
+    else
+        count_rows<u128>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok, j,
+                         not_self);
 }
 
 // Symmetric listing: clear the self-map check, and if the map may be a self
@@ -270,9 +272,12 @@ __global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* tabl
         if (h->total_bits <= 32)
             count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true,
                                  j, not_self);
-        else
+        else if (h->total_bits <= kNarrowKeyBits)
             count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt,
                                            nbr, true, j, not_self);
+        else
+            count_rows<u128>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true, j,
+                             not_self);
         return;
     }
     const int64_t g = j >> 6;

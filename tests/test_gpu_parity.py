@@ -265,13 +265,17 @@ def test_table_full_reported(monkeypatch):
 
 
 def test_key_range_rejected():
-    # 8 columns each spanning 2^9 values need 72 key bits
+    # 8 columns each spanning 2^12 values need 96 key bits, past the 92 the
+    # wide key holds; spanning 2^9 values (72 bits) they build
     rows = np.zeros((2, 8), np.int32)
-    rows[1, 1:] = 511
-    rows[1, 0] = 511
+    rows[1, :] = 4095
     with pytest.raises(gsc.GscError) as e:
         gsc.gsc_coords_build(_t(rows))
     assert e.value.code == gsc.GSC_ERANGE
+    rows[1, :] = 511
+    c = _t(rows)
+    km = gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, np.zeros((1, 7), np.int32))
+    assert np.array_equal(gpu_pairs(km)[0][0], np.arange(2))
 
 
 def test_kernel_map_short_then_retry():
@@ -1068,26 +1072,78 @@ def test_7d_space_time_chroma_real_extents():
 
 
 def test_7d_key_width_limit():
-    """The packed key's limit on 7D rows: the space-time-chroma rows with
-    their spatial axes scaled until the box needs exactly 62 bits still map
-    exactly; one bit more is rejected with ERANGE (the table is not built)."""
+    """The packed key's limits on 7D rows: the space-time-chroma rows with
+    their spatial axes scaled until the box needs exactly 62 bits (the widest
+    key held in one 64-bit word), 63 bits (the wide form: 62 bits in the
+    slot's key word, the rest in its second word) and 92 bits (the widest key)
+    still map exactly; one bit more is rejected with ERANGE (the table is not
+    built)."""
     base = WL.space_time_chroma_coords(1).astype(np.int64)
     at = base.copy()
     at[:, 1] *= 16
     at[:, 2:4] *= 8
     over = at.copy()
     over[:, 3] *= 2
-    assert _key_bits(at) == 62 and _key_bits(over) == 63
-    _say(f"[gpu] 7D key width: {_key_bits(at)} bits maps, {_key_bits(over)} is rejected")
-    at = at.astype(np.int32)
-    c = _t(at)
-    table = gsc.gsc_coords_build(c)
+    top = at.copy()
+    top[:, 1:4] *= 1024
+    past = top.copy()
+    past[:, 3] *= 2
+    assert [_key_bits(a) for a in (at, over, top, past)] == [62, 63, 92, 93]
+    _say("[gpu] 7D key width: 62, 63 and 92 bits map, 93 is rejected")
     offs = _trilateral_7d()
-    km = gsc.gsc_kernel_map(table, c, offs)
-    maps_equal_exact(gpu_pairs(km), O.kernel_map(at, at, offs))
+    for a in (at, over, top):
+        a = a.astype(np.int32)
+        c = _t(a)
+        km = gsc.gsc_kernel_map(gsc.gsc_coords_build(c), c, offs)
+        maps_equal_exact(gpu_pairs(km), O.kernel_map(a, a, offs))
     with pytest.raises(gsc.GscError) as e:
-        gsc.gsc_coords_build(_t(over.astype(np.int32)))
+        gsc.gsc_coords_build(_t(past.astype(np.int32)))
     assert e.value.code == gsc.GSC_ERANGE
+
+
+def _wide_7d_rows():
+    """The space-time-chroma rows of one building seen twice: the scene's
+    crops and the same crops 2^13 voxels (164 m) further along x, y and z, a
+    box of 68 key bits."""
+    base = WL.space_time_chroma_coords(1).astype(np.int64)
+    far = base.copy()
+    far[:, 1:4] += 1 << 13
+    rows = np.concatenate([base, far]).astype(np.int32)
+    assert 62 < _key_bits(rows) <= 92
+    return rows
+
+
+def test_7d_wide_keys():
+    """Rows whose box needs more than 62 key bits take the wide key form:
+    exact maps over the 7D cross and the trilateral region, and convolutions
+    on the block engine and the row form."""
+    coords = _wide_7d_rows()
+    cross, tri = regions.hypercross(3, 7), _trilateral_7d()
+    _say(f"[gpu] 7D wide keys: {len(coords)} rows, {_key_bits(coords)} key bits")
+    c = _t(coords)
+    table = gsc.gsc_coords_build(c)
+    for offs in (cross, tri):
+        maps_equal_exact(gpu_pairs(gsc.gsc_kernel_map(table, c, offs)), O.kernel_map(coords, coords, offs))
+    _plan_case(coords, 16, 32, cross, 203)
+    _conv_case(coords, 8, 16, tri, 204)
+
+
+def test_7d_wide_keys_strided():
+    """Strided output coordinates of wide-key rows: the oracle's set, in
+    first-input-row order, and an output table that answers for them."""
+    coords = _wide_7d_rows()
+    _say(f"[gpu] 7D wide keys, stride 2: {len(coords)} rows")
+    out, out_table = gsc.gsc_coords_stride(_t(coords), 2)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = O.output_coordinates(coords, 2)
+    assert len(got) == len(ref) and {tuple(r) for r in got.tolist()} == {tuple(r) for r in ref.tolist()}
+    first = {}
+    for r, row in enumerate(coords.tolist()):
+        first.setdefault((row[0],) + tuple((v // 2) * 2 for v in row[1:]), r)
+    assert [first[tuple(r)] for r in got.tolist()] == sorted(first.values())
+    km = gsc.gsc_kernel_map(out_table, out, np.zeros((1, 7), np.int32))
+    assert np.array_equal(gpu_pairs(km)[0][0], np.arange(len(got)))
 
 
 # --------------------------------------------------------------------------- #
