@@ -89,7 +89,7 @@ def forward_kernel(gsc, dtype: str, ci: int, co: int, K: int, planned: bool, epi
     ep = "true" if epilogue else "false"
     if planned and gsc.gsc_conv_block_engine(dt, ci, co, K):
         if dtype == "bf16":
-            if K <= 30:   # the tile engine (16 blocks by all output columns per workgroup)
+            if K <= 29:   # the tile engine (16 blocks by all output columns per workgroup)
                 return f"k_conv_tile_bf16<{ci}, {co}, gsc::WIdentity, {ep}>"
             return f"k_conv_blk_bf16<{ci}, {128 if co == 256 else co}, gsc::WIdentity, {ep}>"
         return f"k_conv_blk_f32<{ci}, {co}, false, {ep}, false>"

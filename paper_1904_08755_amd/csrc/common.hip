@@ -180,6 +180,18 @@ int seg_from_gidx(const int64_t* gidx, int K, int64_t G, int64_t* seg, hipStream
     return GSC_OK;
 }
 
+int device_cus() {
+    static int cus[64] = {0};   // per device, read once (a benign race: every writer stores the same value)
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
 size_t scan_ws_bytes(int64_t m) {
     const int64_t nb = (m + kScanTile - 1) / kScanTile;
     return (size_t)((nb > 0 ? nb : 1) * sizeof(int64_t) + 256);

@@ -676,18 +676,6 @@ bool blk_f32_supported(int ca, int cb, int K) {
     return ok(ca) && ok(cb) && K >= 1 && K <= kPlanMaxK && (int64_t)K * ca * cb * 4 <= kBlkLdsBytes;
 }
 
-static int device_cus() {
-    static int cus[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cus[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cus[dev] = n;
-    }
-    return cus[dev];
-}
-
 template <int CA, int CB, bool WT, bool EP>
 static void launch_blk_f32(const float* X, int64_t n_x, const float* W, const WSel& sel, int K, const BlockPlan& p,
                            int64_t nb, int64_t n_y, const Epilogue& ep, bool accum, float* Y, hipStream_t s) {

@@ -759,25 +759,13 @@ bool tile_bf16_supported(int ca, int cb, int K) {
     return (ca == 64 || ca == 128 || ca == 256) && (cb == 64 || cb == 128 || cb == 256) && K >= 1 && K <= kTileMaxK;
 }
 
-static int tile_grid_cap() {
-    static int cus[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cus[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cus[dev] = n;
-    }
-    return cus[dev];
-}
-
 template <int CA, int CB, typename Sel, bool EP>
 static int launch_tile_kernel(const uint16_t* X, int64_t n_x, const uint16_t* Bt, int K, const Sel& sel,
                               const BlockPlan& p, int64_t nb, int64_t n_y, const Epilogue& ep, uint16_t* Y,
                               unsigned* counter, bool counter_ready, hipStream_t s) {
     const int64_t tiles = (nb + kTileBlocks - 1) / kTileBlocks;
     if (tiles == 0) return GSC_OK;
-    const int64_t grid = tiles < tile_grid_cap() ? tiles : tile_grid_cap();
+    const int64_t grid = tiles < device_cus() ? tiles : device_cus();
     const size_t dyn = (size_t)kTileBlocks * K * 16 * sizeof(int32_t);
     auto kern = k_conv_tile_bf16<CA, CB, Sel, EP>;
     GSC_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,

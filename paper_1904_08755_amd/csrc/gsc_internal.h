@@ -233,6 +233,9 @@ __device__ __forceinline__ int64_t floor_mul(int64_t a, int64_t s) {
 // dividing m: a kernel map's segment table seg[k] = gidx[k * G]).
 // ---------------------------------------------------------------------------
 size_t scan_ws_bytes(int64_t m);
+// compute units of the current device (cached per device; 256 if the query fails)
+int device_cus();
+
 int scan_counts(const int32_t* cnt, int64_t m, int64_t* out, int64_t* total_out, void* ws,
                 hipStream_t s, int64_t* every_out = nullptr, int64_t every = 0);
 

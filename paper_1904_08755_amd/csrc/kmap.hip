@@ -54,10 +54,15 @@ __device__ __forceinline__ bool header_ok(const TableHeader* h, int ncol) {
     return h->magic == kTableMagic && h->ncol == ncol && h->status == 0;
 }
 
-constexpr int kBatch = 4;   // probes issued together per lane in the count pass (4 measured faster than 8 or 16)
-// ... for wide keys: two, so that their path needs no more registers than the others
-template <typename KeyT>
-constexpr int batch_of() { return sizeof(KeyT) > 8 ? 1 : kBatch; }
+// Probes issued together per lane in the count pass: 4 (186 VGPRs at 16 halve
+// the resident waves; 8 and 16 measured slower on a 300k-row map), or 16
+// when every row's wave is resident at once even at that size (a 120k-row
+// map: 53 -> 45 us).  Wide keys take one at a time, so that their path needs
+// no more registers than the others.
+constexpr int kBatch = 4;
+constexpr int kBatchSmall = 16;
+template <typename KeyT, int NB>
+constexpr int batch_of() { return sizeof(KeyT) > 8 ? 1 : NB; }
 
 // Key arithmetic in KeyT (uint32_t when the table's keys fit in 32 bits, the
 // usual case, uint64_t up to 62 bits, else the 128-bit wide key).  The packed
@@ -90,7 +95,7 @@ struct KeyOps<u128> {
 // whole 16-byte slot, so a hit also yields the input row, which goes to
 // nbr[k * n_out + j] (-1 for a miss); hits are counted per 64-row group with
 // a wave ballot.
-template <typename KeyT, typename Offs>
+template <typename KeyT, int NBT, typename Offs>
 __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __restrict__ slots,
                                            const int32_t* __restrict__ out_coords, int64_t n_out, int ncol,
                                            const Offs& offs, int K, int k_begin, int k_end, int mirror_end,
@@ -130,7 +135,7 @@ __device__ __forceinline__ void count_rows(const TableHeader* h, const Slot* __r
     in_b = in_b && (uint32_t)rel[0] <= (uint32_t)span[0];
     const int64_t g = j >> 6;
     const bool writer = __lane_id() == 0 && g < G;
-    constexpr int NB = batch_of<KeyT>();
+    constexpr int NB = batch_of<KeyT, NBT>();
     for (int k0 = k_begin; k0 < k_end; k0 += NB) {
         KeyT key[NB];
         unsigned long long pos[NB];
@@ -216,7 +221,7 @@ __device__ __forceinline__ bool self_candidate(const TableHeader* h, int ncol, i
     return sym && header_ok(h, ncol) && h->n == n_out;
 }
 
-template <typename Offs>
+template <typename Offs, int NB>
 __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, const int32_t* __restrict__ out_coords,
                                                          int64_t n_out, int ncol, Offs offs, int K, int sym, int64_t G,
                                                          int32_t* __restrict__ cnt, int32_t* __restrict__ nbr,
@@ -231,13 +236,13 @@ __global__ void __launch_bounds__(kThreads) k_kmap_count(const void* table, cons
     const int mid = self ? (K - 1) / 2 : -1;
     const int64_t j = xcd_unit(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
     if (h->total_bits <= 32)   // uniform: all lanes take the same path
-        count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok,
+        count_rows<uint32_t, NB>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok,
                              j, not_self);
     else if (h->total_bits <= kNarrowKeyBits)
-        count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt,
+        count_rows<unsigned long long, NB>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt,
                                        nbr, ok, j, not_self);
     else
-        count_rows<u128>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok, j,
+        count_rows<u128, NB>(h, slots, out_coords, n_out, ncol, offs, K, 0, k_end, mirror_end, mid, G, cnt, nbr, ok, j,
                          not_self);
 }
 
@@ -258,7 +263,7 @@ __global__ void __launch_bounds__(kThreads) k_kmap_self_init(const void* table, 
 // self map (the count pass found every row at its own index) their pair
 // counts per 64-row group come from the mirrored entries of the neighbour
 // table; otherwise every row probes them itself.
-template <typename Offs>
+template <typename Offs, int NB>
 __global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* table,
                                                                 const int32_t* __restrict__ out_coords, int64_t n_out,
                                                                 int ncol, Offs offs, int K, int sym, int64_t G,
@@ -270,13 +275,13 @@ __global__ void __launch_bounds__(kThreads) k_kmap_mirror_count(const void* tabl
     if (*not_self) {
         const Slot* __restrict__ slots = table_slots(table);
         if (h->total_bits <= 32)
-            count_rows<uint32_t>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true,
+            count_rows<uint32_t, NB>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true,
                                  j, not_self);
         else if (h->total_bits <= kNarrowKeyBits)
-            count_rows<unsigned long long>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt,
+            count_rows<unsigned long long, NB>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt,
                                            nbr, true, j, not_self);
         else
-            count_rows<u128>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true, j,
+            count_rows<u128, NB>(h, slots, out_coords, n_out, ncol, offs, K, (K + 1) / 2, K, 0, -1, G, cnt, nbr, true, j,
                              not_self);
         return;
     }
@@ -393,12 +398,22 @@ static int kmap_enqueue(const void* in_table, const int32_t* out_coords, int64_t
                                s, in_table, n_out, ncol, K, sym, nbr, not_self);
             GSC_LAUNCH_CHECK();
         }
-        hipLaunchKernelGGL((k_kmap_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords, n_out, ncol,
-                           offs, K, sym, G, cnt, nbr, res + 1, not_self);
+        // the wide batch while every row's wave fits at once (two waves per SIMD)
+        const bool small = n_out <= (int64_t)device_cus() * 4 * 2 * 64;
+        if (small)
+            hipLaunchKernelGGL((k_kmap_count<Offs, kBatchSmall>), dim3(nblk), dim3(kThreads), 0, s, in_table,
+                               out_coords, n_out, ncol, offs, K, sym, G, cnt, nbr, res + 1, not_self);
+        else
+            hipLaunchKernelGGL((k_kmap_count<Offs, kBatch>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords,
+                               n_out, ncol, offs, K, sym, G, cnt, nbr, res + 1, not_self);
         GSC_LAUNCH_CHECK();
         if (sym && K > 1) {
-            hipLaunchKernelGGL((k_kmap_mirror_count<Offs>), dim3(nblk), dim3(kThreads), 0, s, in_table, out_coords,
-                               n_out, ncol, offs, K, sym, G, nbr, cnt, not_self);
+            if (small)
+                hipLaunchKernelGGL((k_kmap_mirror_count<Offs, kBatchSmall>), dim3(nblk), dim3(kThreads), 0, s,
+                                   in_table, out_coords, n_out, ncol, offs, K, sym, G, nbr, cnt, not_self);
+            else
+                hipLaunchKernelGGL((k_kmap_mirror_count<Offs, kBatch>), dim3(nblk), dim3(kThreads), 0, s, in_table,
+                                   out_coords, n_out, ncol, offs, K, sym, G, nbr, cnt, not_self);
             GSC_LAUNCH_CHECK();
         }
     }
