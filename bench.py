@@ -25,6 +25,8 @@ bounded sample of the headline workload, stage by stage, on this host's cores.
 from __future__ import annotations
 
 import argparse
+import contextlib
+import gc
 import json
 import os
 import re
@@ -39,6 +41,19 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 MFMA_FP32_PEAK_TFLOPS = 157.3
 METRIC = "sparse-conv fwd+bwd voxels/s & effective GFLOP/s; kernel-map build ms"
+
+
+@contextlib.contextmanager
+def no_gc():
+    """No garbage-collection pass inside a timed region: one over the
+    process's objects stalls the host for tens of ms, and the GPU then idles
+    between the kernels it was to be given."""
+    gc.collect()
+    gc.disable()
+    try:
+        yield
+    finally:
+        gc.enable()
 
 
 def log(*a):
@@ -282,20 +297,21 @@ def run_pool(args):
         one(lambda name: None)
     torch.cuda.synchronize()
     evs = []
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        ev = []
+    with no_gc():
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            ev = []
 
-        def mark(name, ev=ev):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
-            ev.append((name, e))
+            def mark(name, ev=ev):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                ev.append((name, e))
 
-        mark("start")
-        fmap, p, dX = one(mark)
-        evs.append(ev)
-    torch.cuda.synchronize()
-    sec = (time.perf_counter() - t0) / args.steps
+            mark("start")
+            fmap, p, dX = one(mark)
+            evs.append(ev)
+        torch.cuda.synchronize()
+        sec = (time.perf_counter() - t0) / args.steps
     stages = ["map", "fwd", "bwd"] + (["unpool_fwd", "unpool_bwd"] if args.unpool else [])
     ms = {k: [] for k in stages}
     for ev in evs:
@@ -358,11 +374,12 @@ def run_quantize(args):
     for _ in range(args.warmup):
         q = gsc.gsc_quantize(tp, 0.02, batch=tb, labels=tl)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        q = gsc.gsc_quantize(tp, 0.02, batch=tb, labels=tl)
-    torch.cuda.synchronize()
-    sec = (time.perf_counter() - t0) / args.steps
+    with no_gc():
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            q = gsc.gsc_quantize(tp, 0.02, batch=tb, labels=tl)
+        torch.cuda.synchronize()
+        sec = (time.perf_counter() - t0) / args.steps
     n, n_out = len(P), int(q.coords.shape[0])
     cpu = None
     if not args.no_cpu_baseline:
@@ -444,20 +461,21 @@ def bench_conv(args, wid: int, region=None, affine: bool = False, plan_mode: str
     steps_events = []
     plan = pipeline.StepPlan(dw, use_plan=use_plan, epilogue=epi)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        ev = []
+    with no_gc():
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            ev = []
 
-        def mark(name, ev=ev):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
-            ev.append((name, e))
+            def mark(name, ev=ev):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                ev.append((name, e))
 
-        mark("start")
-        last = plan.run(mark)
-        steps_events.append(ev)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+            mark("start")
+            last = plan.run(mark)
+            steps_events.append(ev)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
     sec = (t1 - t0) / steps
     log(f"  timed {steps} steps: {sec * 1e3:.3f} ms/step")
 
