@@ -212,9 +212,9 @@ __device__ __forceinline__ bool block_key_view(TableHeader* h, int ncol, KeyLayo
 // same low bits reads Slot::hi, and while it is still unset it polls the same
 // slot again: the writer has claimed it and stores right after.  The claim's
 // store comes before any comparison in every round, so a writer in the same
-// wave has stored before its neighbours look.  Rounds end when the key is
-// placed, found (and_found: what to do then) or the table is walked through;
-// a slot whose high bits stay unset past kWidePolls polls ends with ST_FULL.
+// wave has stored before its neighbours look.  The probing ends when the key
+// is placed or found or the table has been walked through; a slot whose high
+// bits stay unset past kWidePolls polls ends it with ST_FULL.
 constexpr int kWidePolls = 1 << 22;
 
 // One round of a wide find-or-insert at slot s: returns 1 placed (this thread
