@@ -134,6 +134,25 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
                       int32_t* out_coords, int64_t* n_out, void* out_table, size_t out_table_bytes,
                       void* ws, size_t ws_bytes, void* stream);
 
+/* gsc_coords_stride without its host round trip (Sec. 4.2, as above): the
+ * kernels are enqueued on `stream`, followed by an asynchronous copy of 16
+ * bytes into `result` (host, 2 int64; pinned memory keeps the call from
+ * blocking, pageable memory makes the copy, and so the call, wait for the
+ * stream).  Once the stream has passed that copy (an event recorded after
+ * the call, or a synchronisation), gsc_coords_stride_result turns `result`
+ * into the output row count and the build's status.  Work that needs only
+ * `out_table` (a kernel map onto other coordinates) can be enqueued before
+ * that.  Errors (of this call): EINVAL, ESHORT, EHIP. */
+int gsc_coords_stride_async(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                            int32_t* out_coords, int64_t* result, void* out_table, size_t out_table_bytes,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* The outcome of a gsc_coords_stride_async call from its `result` (host):
+ * `*n_out` (host) receives the number of output rows.  Errors: EINVAL (null
+ * pointer), ERANGE (the strided box needs more key bits than a key holds),
+ * EFULL (no free slot). */
+int gsc_coords_stride_result(const int64_t* result, int64_t* n_out);
+
 /* ------------------------------------------------------------------------ */
 /* Sparse tensor quantization (Sec. 4.1, Alg. 1): the step before a1.       */
 /* ------------------------------------------------------------------------ */

@@ -8,6 +8,9 @@
 // numeric order of keys is the lexicographic order of rows.
 #include <climits>
 
+#include <cstddef>
+#include <cstring>
+
 #include "gsc_internal.h"
 
 namespace gsc {
@@ -604,28 +607,25 @@ size_t gsc_stride_ws_bytes(int64_t n_in) {
     return b + 256;
 }
 
-int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
-                      int32_t* out_coords, int64_t* n_out, void* out_table, size_t out_table_bytes, void* ws,
-                      size_t ws_bytes, void* stream) {
-    clear_error();
-    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "coords_stride: D=%d outside [1,%d]", D, kMaxCols - 1);
-    if (n_in < 0 || n_in > INT32_MAX) return fail(GSC_EINVAL, "coords_stride: n_in=%lld invalid", (long long)n_in);
-    if (!stride || !n_out || !out_table) return fail(GSC_EINVAL, "coords_stride: null stride/n_out/out_table");
-    if (n_in > 0 && (!in_coords || !out_coords || !ws))
-        return fail(GSC_EINVAL, "coords_stride: null in_coords/out_coords/ws");
+// The kernels of gsc_coords_stride; the output count ends in the header (n).
+static int stride_enqueue(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                          int32_t* out_coords, void* out_table, size_t out_table_bytes, void* ws, size_t ws_bytes,
+                          hipStream_t s, const char* what) {
+    if (D < 1 || D + 1 > kMaxCols) return fail(GSC_EINVAL, "%s: D=%d outside [1,%d]", what, D, kMaxCols - 1);
+    if (n_in < 0 || n_in > INT32_MAX) return fail(GSC_EINVAL, "%s: n_in=%lld invalid", what, (long long)n_in);
+    if (!stride || !out_table) return fail(GSC_EINVAL, "%s: null stride/out_table", what);
+    if (n_in > 0 && (!in_coords || !out_coords || !ws)) return fail(GSC_EINVAL, "%s: null in_coords/out_coords/ws", what);
     StrideArg st{};
     st.on = 1;
     st.s[0] = 1;
     for (int d = 0; d < D; ++d) {
-        if (stride[d] < 1) return fail(GSC_EINVAL, "coords_stride: stride[%d]=%d must be >= 1", d, stride[d]);
+        if (stride[d] < 1) return fail(GSC_EINVAL, "%s: stride[%d]=%d must be >= 1", what, d, stride[d]);
         st.s[d + 1] = stride[d];
     }
     if (out_table_bytes < gsc_table_bytes(n_in))
-        return fail(GSC_ESHORT, "coords_stride: out_table needs %zu bytes, got %zu", gsc_table_bytes(n_in),
-                    out_table_bytes);
+        return fail(GSC_ESHORT, "%s: out_table needs %zu bytes, got %zu", what, gsc_table_bytes(n_in), out_table_bytes);
     if (n_in > 0 && ws_bytes < gsc_stride_ws_bytes(n_in))
-        return fail(GSC_ESHORT, "coords_stride: ws needs %zu bytes, got %zu", gsc_stride_ws_bytes(n_in), ws_bytes);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        return fail(GSC_ESHORT, "%s: ws needs %zu bytes, got %zu", what, gsc_stride_ws_bytes(n_in), ws_bytes);
     const int ncol = D + 1;
     const int64_t cap = table_capacity(n_in);
     TableHeader* h = reinterpret_cast<TableHeader*>(out_table);
@@ -636,8 +636,6 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
     if (n_in == 0) {
         hipLaunchKernelGGL(k_plan, dim3(1), dim3(64), 0, s, h);
         GSC_LAUNCH_CHECK();
-        GSC_HIP(hipStreamSynchronize(s));
-        *n_out = 0;
         return GSC_OK;
     }
     const int64_t groups = (n_in + 63) / 64;
@@ -662,10 +660,54 @@ int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const i
     hipLaunchKernelGGL(k_rep_write, dim3(grid_for(n_in)), dim3(kThreads), 0, s, in_coords, n_in, st, h, slots,
                        slot_of, off, out_coords, (int32_t*)nullptr);
     GSC_LAUNCH_CHECK();
+    return GSC_OK;
+}
+
+int gsc_coords_stride(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                      int32_t* out_coords, int64_t* n_out, void* out_table, size_t out_table_bytes, void* ws,
+                      size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!n_out) return fail(GSC_EINVAL, "coords_stride: null n_out");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int rc = stride_enqueue(in_coords, n_in, D, stride, out_coords, out_table, out_table_bytes, ws, ws_bytes, s,
+                            "coords_stride");
+    if (rc) return rc;
     TableHeader hh;
     rc = read_status(out_table, s, &hh);
     if (rc) return rc;
     rc = status_to_code(hh, "coords_stride");
+    if (rc) return rc;
+    *n_out = hh.n;
+    return GSC_OK;
+}
+
+// The header's n, status and total_bits, contiguous: what the asynchronous
+// form copies to the host.
+static_assert(offsetof(TableHeader, status) == offsetof(TableHeader, n) + 8 &&
+                  offsetof(TableHeader, total_bits) == offsetof(TableHeader, n) + 12,
+              "header layout of the stride result");
+
+int gsc_coords_stride_async(const int32_t* in_coords, int64_t n_in, int32_t D, const int32_t* stride,
+                            int32_t* out_coords, int64_t* result, void* out_table, size_t out_table_bytes, void* ws,
+                            size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!result) return fail(GSC_EINVAL, "coords_stride_async: null result");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int rc = stride_enqueue(in_coords, n_in, D, stride, out_coords, out_table, out_table_bytes, ws, ws_bytes, s,
+                            "coords_stride_async");
+    if (rc) return rc;
+    GSC_HIP(hipMemcpyAsync(result, &reinterpret_cast<TableHeader*>(out_table)->n, 16, hipMemcpyDeviceToHost, s));
+    return GSC_OK;
+}
+
+int gsc_coords_stride_result(const int64_t* result, int64_t* n_out) {
+    clear_error();
+    if (!result || !n_out) return fail(GSC_EINVAL, "coords_stride_result: null result/n_out");
+    TableHeader hh{};
+    hh.n = result[0];
+    std::memcpy(&hh.status, reinterpret_cast<const char*>(result) + 8, 4);
+    std::memcpy(&hh.total_bits, reinterpret_cast<const char*>(result) + 12, 4);
+    const int rc = status_to_code(hh, "coords_stride");
     if (rc) return rc;
     *n_out = hh.n;
     return GSC_OK;

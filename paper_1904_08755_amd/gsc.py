@@ -47,6 +47,8 @@ _SIGS = {
     "gsc_table_status": (ctypes.c_int, [_vp, _vp]),
     "gsc_stride_ws_bytes": (_sz, [_i64]),
     "gsc_coords_stride": (ctypes.c_int, [_vp, _i64, _i32, _c_i32p, _vp, _c_i64p, _vp, _sz, _vp, _sz, _vp]),
+    "gsc_coords_stride_async": (ctypes.c_int, [_vp, _i64, _i32, _c_i32p, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
+    "gsc_coords_stride_result": (ctypes.c_int, [_vp, _c_i64p]),
     "gsc_quantize_ws_bytes": (_sz, [_i64, _i32]),
     "gsc_quantize": (ctypes.c_int, [_vp, _vp, _i64, _i32, ctypes.POINTER(ctypes.c_float), _vp, _i32, _vp, _c_i64p,
                                     _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
@@ -178,8 +180,12 @@ def gsc_table_status(table: torch.Tensor, stream=None) -> None:
 # a2: output coordinates of a strided convolution
 # --------------------------------------------------------------------------- #
 def gsc_coords_stride(coords: torch.Tensor, stride: Sequence[int], out_table: Optional[torch.Tensor] = None,
-                      stream=None):
-    """Returns (out_coords [n_out, 1+D] int32, out_table)."""
+                      stream=None, defer: bool = False, result: Optional[torch.Tensor] = None):
+    """Returns (out_coords [n_out, 1+D] int32, out_table).  With ``defer``
+    the call returns a StridePending at once (gsc_coords_stride_async): work
+    that needs only ``out_table`` can be enqueued before its ``finish()``
+    reads the row count.  ``result`` (2 int64 in pinned host memory) may be
+    given to reuse it across calls."""
     _need(coords, torch.int32, "coords", 2)
     n, ncol = coords.shape
     D = ncol - 1
@@ -191,10 +197,36 @@ def gsc_coords_stride(coords: torch.Tensor, stride: Sequence[int], out_table: Op
     if out_table is None:
         out_table = torch.empty(gsc_table_bytes(n), dtype=torch.uint8, device=dev)
     ws = _ws(lib().gsc_stride_ws_bytes(n), dev)
+    if defer:
+        if result is None:
+            result = torch.empty(2, dtype=torch.int64, pin_memory=True)
+        _check(lib().gsc_coords_stride_async(_ptr(coords), n, D, _host_i32(st), _ptr(out), result.data_ptr(),
+                                             _ptr(out_table), out_table.numel(), _ptr(ws), ws.numel(),
+                                             _stream(stream)))
+        ev = torch.cuda.Event()
+        ev.record(torch.cuda.current_stream(dev) if stream is None else stream)
+        return StridePending(out, out_table, result, ev, ws)
     n_out = ctypes.c_int64(0)
     _check(lib().gsc_coords_stride(_ptr(coords), n, D, _host_i32(st), _ptr(out), ctypes.byref(n_out),
                                    _ptr(out_table), out_table.numel(), _ptr(ws), ws.numel(), _stream(stream)))
     return out[: n_out.value], out_table
+
+
+@dataclasses.dataclass
+class StridePending:
+    """An enqueued gsc_coords_stride_async: finish() waits for its result copy
+    (not for work enqueued after it) and returns (out_coords, out_table)."""
+    out: torch.Tensor
+    out_table: torch.Tensor
+    result: torch.Tensor
+    done: "torch.cuda.Event"
+    ws: torch.Tensor   # kept alive until the kernels that use it have run
+
+    def finish(self):
+        self.done.synchronize()
+        n_out = ctypes.c_int64(0)
+        _check(lib().gsc_coords_stride_result(self.result.data_ptr(), ctypes.byref(n_out)))
+        return self.out[: n_out.value], self.out_table
 
 
 # --------------------------------------------------------------------------- #

@@ -120,6 +120,7 @@ class StepPlan:
             offs = dw.offsets[0]
             K = len(offs)
             self.out_table = torch.empty(gsc.gsc_table_bytes(n), dtype=torch.uint8, device=dev)
+            self.stride_result = torch.empty(2, dtype=torch.int64, pin_memory=True)
             dt = gsc._dt(dw.X)
             eng = lambda a, b: gsc.gsc_conv_block_engine(dt, a, b, K)
             # kd feeds layer 0's forward and layer 1's dX; td layer 1's forward and layer 0's dX
@@ -191,12 +192,16 @@ class StepPlan:
         L0 = dw.wl.layers[0]
         offs = dw.offsets[0]
         gsc.gsc_coords_build(dw.coords, self.table, stream=stream, sync=False)
-        out_coords, _ = gsc.gsc_coords_stride(dw.coords, L0.stride, out_table=self.out_table, stream=stream)
+        # the output rows' count comes back while the transposed map (which
+        # needs only their table) is already enqueued behind them
+        pending = gsc.gsc_coords_stride(dw.coords, L0.stride, out_table=self.out_table, stream=stream, defer=True,
+                                        result=self.stride_result)
+        td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
+                                host_offsets=self.host_offs_neg, dense=self.plan_td)
+        out_coords, _ = pending.finish()
         n_out = out_coords.shape[0]
         kd = gsc.gsc_kernel_map(self.table, out_coords, offs, stream=stream, sync=False, bufs=self.kd,
                                 host_offsets=self.host_offs, dense=self.plan_kd)
-        td = gsc.gsc_kernel_map(self.out_table, dw.coords, -offs, stream=stream, sync=False, bufs=self.td,
-                                host_offsets=self.host_offs_neg, dense=self.plan_td)
         mark("map")
         pkd = gsc.gsc_conv_plan(kd, self.pkd, stream=stream) if self.plan_kd else kd
         ptd = gsc.gsc_conv_plan(td, self.ptd, stream=stream) if self.plan_td else td

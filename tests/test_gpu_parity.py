@@ -701,6 +701,29 @@ def test_stride_order_with_runs_across_lanes(lead):
     maps_equal_exact(gpu_pairs(km), ref)
 
 
+def test_stride_deferred_matches_sync(monkeypatch):
+    """The deferred strided output coordinates (gsc_coords_stride_async, its
+    count read after a map over its table was enqueued) equal the
+    synchronous call's rows and table; a failed deferred build reports EFULL
+    from its result."""
+    coords = WL.random_coords(84, 5000, 3, -16, 16, batch=2)
+    c = _t(coords)
+    offs = -regions.hypercube(2, 3)
+    ref_out, ref_table = gsc.gsc_coords_stride(c, 2)
+    ref_pairs = gpu_pairs(gsc.gsc_kernel_map(ref_table, c, offs))
+    pending = gsc.gsc_coords_stride(c, 2, defer=True)
+    km = gsc.gsc_kernel_map(pending.out_table, c, offs, sync=False)   # needs only the output table
+    out, table = pending.finish()
+    assert torch.equal(out, ref_out)
+    for (i1, o1), (i2, o2) in zip(gpu_pairs(km), ref_pairs):
+        assert np.array_equal(i1, i2) and np.array_equal(o1, o2)
+    monkeypatch.setenv("GSC_TABLE_CAP_LIMIT", "64")   # 64 slots for the ~2,500 output rows
+    pending = gsc.gsc_coords_stride(c, 2, defer=True)
+    with pytest.raises(gsc.GscError) as e:
+        pending.finish()
+    assert e.value.code == gsc.GSC_EFULL
+
+
 def test_stride_then_second_level():
     coords = WL.random_coords(82, 6000, 3, -17, 17, batch=2)
     c = _t(coords)
