@@ -275,12 +275,16 @@ def run_pool(args):
     unpooled = gsc.Pooled(torch.empty((n, C), dtype=torch.float32, device="cuda"), None,
                           torch.empty((n,), dtype=torch.int32, device="cuda"))
     dXc = torch.empty((n, C), dtype=torch.float32, device="cuda")
+    stride_result = torch.empty(2, dtype=torch.int64, pin_memory=True)
 
     def one(mark):
         gsc.gsc_coords_build(coords, table, sync=False)
-        out, _ = gsc.gsc_coords_stride(coords, 2, out_table=out_table)
-        fmap = gsc.gsc_kernel_map(table, out, offs, sync=False, bufs=fb, host_offsets=host_offs, dense=True)
+        # the count of the output rows is read once the map onto the input
+        # rows (which needs only the output table) is enqueued behind them
+        pending = gsc.gsc_coords_stride(coords, 2, out_table=out_table, defer=True, result=stride_result)
         tmap = gsc.gsc_kernel_map(out_table, coords, -offs, sync=False, bufs=tb, host_offsets=host_neg, dense=True)
+        out, _ = pending.finish()
+        fmap = gsc.gsc_kernel_map(table, out, offs, sync=False, bufs=fb, host_offsets=host_offs, dense=True)
         mark("map")
         p = gsc.gsc_sparse_pool_fwd(X, fmap, args.pool, out=pooled)
         mark("fwd")
