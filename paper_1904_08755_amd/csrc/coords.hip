@@ -440,9 +440,9 @@ struct VoxelArg {
     float v[kMaxCols - 1];   // voxel size per spatial axis
 };
 
-// qc[r] = (batch[r] or 0, floor(p_d / v_d)); the quotient is the correctly
-// rounded float32 division, then floor.  A coordinate outside +-2^30 sets the
-// range status.
+// qc[r] = (batch[r] or 0, floor(p_d / v_d)), the floor of the exact quotient
+// of the stored float32 values.  A coordinate outside +-2^30 sets the range
+// status.
 __global__ void __launch_bounds__(kThreads) k_quantize(const float* __restrict__ points,
                                                        const int32_t* __restrict__ batch, int64_t n, int D, VoxelArg va,
                                                        int32_t* __restrict__ qc, TableHeader* h) {

@@ -946,6 +946,23 @@ def test_quantize_random_and_scene():
     _say(f"  scene points {sum(len(p) for p in pts)} -> voxels {q.coords.shape[0]}")
 
 
+def test_quantize_wide_keys():
+    """Quantization of points whose voxel box needs more than 62 key bits
+    (clusters of points spread over +-2e5 m at 1 mm voxels: 29 bits per axis)
+    goes through the wide key form and still matches the oracle."""
+    rng = np.random.default_rng(97)
+    centres = rng.uniform(-2e5, 2e5, size=(1500, 3))
+    P = (np.repeat(centres, 4, axis=0) + rng.uniform(-2e-3, 2e-3, size=(6000, 3))).astype(np.float32)
+    b = rng.integers(0, 3, size=6000).astype(np.int32)
+    L = rng.integers(0, 3, size=6000).astype(np.int32)
+    v = np.floor(P.astype(np.float64) / np.float64(np.float32(1e-3)))
+    bits = sum(int(s).bit_length() for s in (v.max(0) - v.min(0)).astype(np.int64)) + int(b.max()).bit_length()
+    assert 62 < bits <= 92
+    _say(f"[gpu] quantize with wide keys: {bits} key bits")
+    q = _quant_compare(P, b, 1e-3, L)
+    assert q.coords.shape[0] < len(P)   # clustered points share voxels
+
+
 # --------------------------------------------------------------------------- #
 # forward with the per-channel affine map and ReLU fused (Sec. 4.5)
 # --------------------------------------------------------------------------- #
