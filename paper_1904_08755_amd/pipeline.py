@@ -8,7 +8,9 @@ host orchestration only: every stage is one call of libgsc.so.
 pass only enqueues library calls.  The table build and the kernel maps run in
 their asynchronous modes (the pair count stays on the device), so a pass of a
 submanifold layer has no host round trip at all; a strided layer needs one,
-to learn how many output coordinates it has.
+to learn how many output coordinates it has, and takes it from the deferred
+stride call once the transposed map (which needs only the output table) is
+enqueued, so the GPU does not idle while the host waits.
 
 Block plans: with ``use_plan`` (the default) every map that a block engine
 can use (gsc_conv_block_engine) gets its block plan (gsc_conv_plan): output
